@@ -1,0 +1,157 @@
+"""Fastmax fp64 CPU oracle -- test infrastructure only.
+
+A plain, slow, obviously-correct float64 implementation of Fastmax attention
+(arXiv 2402.07901, Sec. 2.2 definition, Sec. 2.4 factorisation, Sec. 2.3 score
+derivative), written in C (``fastmax_ref.c``) and wrapped here with ctypes.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline
+leg may import this package.  The HIP library never calls it, and the two
+share no code.  Inputs are float64 numpy arrays in [B, H, N, D] layout.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "fastmax_ref.c")
+_LIB = os.path.join(_HERE, "libfastmax_oracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP). Returns the library path."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+               "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _bind(path):
+    """Load a compiled oracle library and declare its signatures."""
+    lib = ctypes.CDLL(path)
+    dp = ctypes.POINTER(ctypes.c_double)
+    L = ctypes.c_long
+    I = ctypes.c_int
+    lib.fmo_num_threads.restype = I
+    lib.fmo_standardize.argtypes = [dp, L, L, dp, dp, dp]
+    lib.fmo_attention_matrix.argtypes = [dp, dp, L, L, I, I, dp]
+    lib.fmo_fwd_brute.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp]
+    lib.fmo_fwd_fact.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp]
+    lib.fmo_fwd_rows.argtypes = [dp, dp, dp, L, L, L, L, I, I, L,
+                                 ctypes.POINTER(ctypes.c_int64), dp, dp]
+    lib.fmo_bwd_brute.argtypes = [dp, dp, dp, dp, L, L, L, L, I, I,
+                                  dp, dp, dp]
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = _bind(_LIB)
+    return _lib
+
+
+def _f64(x):
+    return np.ascontiguousarray(x, dtype=np.float64)
+
+
+def _ptr(a):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _shape4(q):
+    if q.ndim != 4:
+        raise ValueError("expected [B, H, N, D]")
+    return q.shape
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle uses."""
+    return int(_load().fmo_num_threads())
+
+
+def standardize(x):
+    """Eqs. (6)-(7): per-row (q - mean) / population std over the last axis.
+
+    Returns (xhat, mean, std) with mean/std shaped like x without its last axis.
+    """
+    x = _f64(x)
+    D = x.shape[-1]
+    rows = x.size // D
+    xh = np.empty_like(x)
+    mu = np.empty(x.shape[:-1])
+    sg = np.empty(x.shape[:-1])
+    _load().fmo_standardize(_ptr(x), rows, D, _ptr(xh), _ptr(mu), _ptr(sg))
+    return xh, mu, sg
+
+
+def attention_matrix(q, k, p, causal):
+    """Explicit N x N Fastmax attention matrix of ONE head, q/k shaped [N, D]."""
+    q, k = _f64(q), _f64(k)
+    N, D = q.shape
+    A = np.empty((N, N))
+    _load().fmo_attention_matrix(_ptr(q), _ptr(k), N, D, int(p), int(causal),
+                                 _ptr(A))
+    return A
+
+
+def fwd_brute(q, k, v, p, causal):
+    """Brute force O(N^2 D) forward; returns (O, G)."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, D = _shape4(q)
+    out = np.empty_like(q)
+    g = np.empty((B, H, N))
+    _load().fmo_fwd_brute(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
+                          int(causal), _ptr(out), _ptr(g))
+    return out, g
+
+
+def fwd_fact(q, k, v, p, causal):
+    """Factorised moment forward (Sec. 2.4); returns (O, G)."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, D = _shape4(q)
+    out = np.empty_like(q)
+    g = np.empty((B, H, N))
+    _load().fmo_fwd_fact(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
+                         int(causal), _ptr(out), _ptr(g))
+    return out, g
+
+
+def fwd_rows(q, k, v, p, causal, rows):
+    """Brute force for selected rows (flat index b*H*N + h*N + i).
+
+    Returns (O_rows [n, D], G_rows [n]).
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, D = _shape4(q)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.empty((rows.size, D))
+    g = np.empty(rows.size)
+    _load().fmo_fwd_rows(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
+                         int(causal), rows.size,
+                         rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                         _ptr(out), _ptr(g))
+    return out, g
+
+
+def bwd_brute(q, k, v, dout, p, causal):
+    """Brute force O(N^2 D) backward; returns (dq, dk, dv)."""
+    q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
+    B, H, N, D = _shape4(q)
+    dq = np.empty_like(q)
+    dk = np.empty_like(q)
+    dv = np.empty_like(q)
+    _load().fmo_bwd_brute(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), B, H, N, D,
+                          int(p), int(causal), _ptr(dq), _ptr(dk), _ptr(dv))
+    return dq, dk, dv
