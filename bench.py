@@ -1,0 +1,204 @@
+#!/usr/bin/env python3
+"""Fastmax forward throughput on one MI355X (tokens*heads/s) with its
+roofline fraction and the fp64 CPU oracle timed beside it.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step = one full forward (standardisation, moments, query contraction,
+divide) over the whole workload, inputs already resident in HBM.  Prints ONE
+JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "Fastmax fwd tokens·heads/s on 1 GPU (D=64,p=2,causal); % MFMA peak"
+PEAK = {  # MI355X published dense peaks
+    ("mfma", "bf16"): 2500.0,   # TFLOP/s
+    ("mfma", "f16"): 2500.0,
+    ("mfma", "f32"): 157.3,
+    ("alu", "f32"): 157.3,
+    ("hbm", None): 8000.0,      # GB/s
+}
+
+
+def n_features(D, p):
+    return 1 + D + (D * (D + 1) // 2 if p == 2 else 0)
+
+
+def fwd_flops(B, H, N, D, p):
+    """Algorithmic forward flops: moment build + query contraction, each
+    2*P*(D+1) per token per head (symmetric packing of the quadratic term)."""
+    return 4.0 * n_features(D, p) * (D + 1) * B * H * N
+
+
+def source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2402_07901_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """Measured HBM bytes per launch from profiles/traffic.json, if it was
+    taken on the current kernel sources; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = data.get(f"{kernel}@{workload}")
+    if not ent or ent.get("source_hash") != source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(w, inp_bits):
+    """The fp64 oracle (factorised form) on a bounded sample of the workload."""
+    import numpy as np
+
+    import oracle
+    from paper_2402_07901_amd.inputs import bf16_bits_to_f64, make_inputs
+    threads = oracle.num_threads()
+    heads = max(1, min(w.B * w.H, threads))
+    if w.N <= 8192 and inp_bits is not None:
+        N = w.N
+        sel = [(i // w.H, i % w.H) for i in range(heads)]
+
+        def cut(x):
+            a = np.stack([x[b, h] for b, h in sel])[None]
+            return bf16_bits_to_f64(a) if w.dtype == "bf16" else a.astype(np.float64)
+        q, k, v = (cut(inp_bits[n]) for n in ("q", "k", "v"))
+        sample = f"first {heads} heads of the workload at full N={N}"
+    else:
+        N = 8192
+        inp = make_inputs(1, heads, N, w.D, w.key, w.dtype, w.mask_frac, w.mask_scale)
+        q, k, v = inp["q64"], inp["k64"], inp["v64"]
+        sample = f"{heads} heads at N={N} drawn with the workload's recipe"
+    t0 = time.perf_counter()
+    oracle.fwd_fact(q, k, v, w.p, w.causal)
+    dt = time.perf_counter() - t0
+    return {"value": heads * N / dt, "unit": "tokens*heads/s", "cores": threads,
+            "kind": "oracle", "sample": sample + f" (fwd_fact, {dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gpt_causal_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the Fastmax kernels here run on a single "
+              "MI355X and no multi-GPU path is built (heads would shard with no "
+              "communication). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2402_07901_amd import fastmax as fm
+    from paper_2402_07901_amd.inputs import WORKLOADS, workload_inputs
+
+    w = WORKLOADS[args.workload]
+    fm.lib()
+    dev = torch.device("cuda:0")
+    inp = workload_inputs(w, want64=False)
+
+    def to_dev(x):
+        if w.dtype == "bf16":
+            return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(x).to(dev)
+
+    q, k, v = (to_dev(inp[n]) for n in ("q", "k", "v"))
+    out = torch.empty_like(q)
+    g = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+    dt = fm.BF16 if w.dtype == "bf16" else fm.F32
+    need = fm.workspace_bytes(w.B, w.H, w.N, w.D, w.p, w.causal, dt, False)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
+                                need, stream)
+        if rc != fm.OK:
+            raise fm.FastmaxError(rc, "fastmax_fwd")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        stops[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_ms = [s.elapsed_time(e) for s, e in zip(starts, stops)]
+    avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    ms_per_step = wall / args.steps * 1e3
+
+    tokens_heads = w.B * w.H * w.N
+    value = tokens_heads / (ms_per_step / 1e3)
+    flops = fwd_flops(w.B, w.H, w.N, w.D, w.p)
+    kernel = "fastmax_fwd"
+    if w.p == 2 and w.dtype == "bf16":
+        bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "bf16")]
+        achieved = flops / avg_launch_s / 1e12
+    elif w.p == 2:
+        bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "f32")]
+        achieved = flops / avg_launch_s / 1e12
+    else:
+        bound, unit, peak = "hbm", "GB/s", PEAK[("hbm", None)]
+        elt = 2 if w.dtype == "bf16" else 4
+        achieved = tokens_heads * (4 * w.D * elt + 4) / avg_launch_s / 1e9
+
+    rec = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens*heads/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "D": w.D, "p": w.p,
+                   "causal": w.causal, "io_dtype": w.dtype, "global_batch": w.B,
+                   "seq_len": w.N, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": load_traffic(kernel, w.name),
+                     "kernel": kernel, "avg_launch_ms": avg_launch_s * 1e3,
+                     "algorithmic_flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,116 @@
+/*
+ * fastmax.h -- C ABI of the MI355X (gfx950) Fastmax attention library.
+ *
+ * Fastmax (Gerami, Hoover, Dulepet, Duraiswami, "FAST: Factorizable Attention
+ * for Speeding up Transformers", arXiv 2402.07901) computes, per head,
+ *
+ *     q^_i = (q_i - mean q_i) / std(q_i - mean q_i)       (Sec. 2.2, Eqs. 6-7)
+ *     k^_n likewise
+ *     s_in = q^_i . k^_n,   w_in = f_p(s_in) = sum_{l<=p} s_in^l / l!
+ *                                                    (Sec. 2.2, Eq. "taylor")
+ *     G_i  = sum_n w_in,    F_i = sum_n w_in v_n,    O_i = F_i / G_i
+ *                                     (Sec. 2.2 a_ij, Eq. "tobeexpanded";
+ *                                      Sec. 2.4 Eq. "bigo")
+ *
+ * with n running over all N tokens, or over n <= i when causal (Sec. 2.1
+ * tril mask; Sec. 2.4 causal F and G).  The library evaluates it exactly
+ * through the factorisation of Sec. 2.4 (moments of k^ and v contracted
+ * against powers of q^), never forming the N x N matrix.
+ *
+ * Conventions shared by every entry point
+ *  - Layout: q, k, v, out, dout, dq, dk, dv are [B, H, N, D] contiguous
+ *    (D fastest) in the I/O dtype `dt`; g is [B, H, N] float32.
+ *    Statistics and accumulation are float32 whatever `dt` is.
+ *  - Pointers are device pointers (HBM) and must be 16-byte aligned.
+ *  - Ownership: the caller owns every buffer, including `workspace`.  The
+ *    library keeps no pointer after return, allocates no device memory,
+ *    creates no stream and holds no global mutable state (thread-safe).
+ *  - Asynchrony: work is enqueued on `stream` (0 = the null stream);
+ *    FASTMAX_OK means "enqueued".  Outputs are valid once the stream reaches
+ *    that point.  Inputs must stay valid until then.
+ *  - Validation happens on the host before the first HIP call: on any error
+ *    nothing is enqueued and nothing is written.
+ *  - Supported: D in {16, 32, 64}; p in {1, 2}; causal in {0, 1};
+ *    dt in {FASTMAX_F32, FASTMAX_BF16}; B, H, N >= 1 and B*H*N*D < 2^62.
+ *  - A token whose q or k row is constant has std 0; its standardised row is
+ *    undefined (as in the paper) and its outputs are not finite.
+ *  - Errors are reported only through the return code (nothing printed).
+ */
+#ifndef FASTMAX_H
+#define FASTMAX_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FASTMAX_F32 = 0,  /* float32 I/O  */
+    FASTMAX_BF16 = 1  /* bfloat16 I/O (round-to-nearest-even on output) */
+} fastmax_dtype_t;
+
+enum {
+    FASTMAX_OK = 0,
+    FASTMAX_EINVAL = -1,       /* p, causal or dt out of range; B, H or N < 1 */
+    FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64}        */
+    FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
+    FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */
+    FASTMAX_EWORKSPACE = -5,   /* workspace NULL or smaller than required     */
+    FASTMAX_EHIP = -6          /* the HIP runtime rejected a launch           */
+};
+
+/*
+ * Bytes of device workspace fastmax_fwd (backward = 0) or fastmax_bwd
+ * (backward = 1) needs for this problem.  0 means no workspace is needed
+ * (NULL may then be passed).  Returns 0 as well for arguments the entry
+ * point would reject.  The workspace need not be zeroed.
+ */
+size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
+                               fastmax_dtype_t dt, int backward);
+
+/*
+ * Forward pass (Sec. 2.2 definition; evaluated by the Sec. 2.4 factorisation,
+ * with the causal moments carried across chunks of tokens).
+ *   q, k, v : inputs  [B, H, N, D] in dt
+ *   out     : output  [B, H, N, D] in dt, O = F / G
+ *   g       : optional output [B, H, N] float32, G_i = sum_n f_p(s_in)
+ *             (the row sums the backward needs, Sec. 2.5); NULL to skip.
+ * Returns FASTMAX_OK or a negative FASTMAX_E* code.
+ */
+int fastmax_fwd(const void *q, const void *k, const void *v, void *out,
+                float *g, int B, int H, int N, int D, int p, int causal,
+                fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                hipStream_t stream);
+
+/*
+ * Backward pass: gradients of sum(dout * O) with respect to q, k and v,
+ * following the score derivative of Sec. 2.3 (Eq. "bound", read with
+ * a_in / a_il) and the custom-gradient idea of Sec. 2.5: only O and G are
+ * saved from the forward; q^, k^ are recomputed and every N x N quantity is
+ * replaced by moment contractions.
+ *   q, k, v : forward inputs            [B, H, N, D] in dt
+ *   out     : forward output O          [B, H, N, D] in dt
+ *   dout    : upstream gradient dL/dO   [B, H, N, D] in dt
+ *   g       : forward row sums G        [B, H, N] float32 (from fastmax_fwd)
+ *   dq, dk, dv : outputs                [B, H, N, D] in dt
+ * The same (p, causal) as the forward must be passed.
+ */
+int fastmax_bwd(const void *q, const void *k, const void *v, const void *out,
+                const void *dout, const float *g, void *dq, void *dk, void *dv,
+                int B, int H, int N, int D, int p, int causal,
+                fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                hipStream_t stream);
+
+/* Static description of a return code (never NULL). */
+const char *fastmax_strerror(int code);
+
+/* Library version as "major.minor.patch". */
+const char *fastmax_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASTMAX_H */

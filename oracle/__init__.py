@@ -42,11 +42,11 @@ def _bind(path):
     lib.fmo_num_threads.restype = I
     lib.fmo_standardize.argtypes = [dp, L, L, dp, dp, dp]
     lib.fmo_attention_matrix.argtypes = [dp, dp, L, L, I, I, dp]
-    lib.fmo_fwd_brute.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp]
+    lib.fmo_fwd_brute.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp, dp]
     lib.fmo_fwd_fact.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp]
     lib.fmo_fwd_rows.argtypes = [dp, dp, dp, L, L, L, L, I, I, L,
-                                 ctypes.POINTER(ctypes.c_int64), dp, dp]
-    lib.fmo_bwd_brute.argtypes = [dp, dp, dp, dp, L, L, L, L, I, I,
+                                 ctypes.POINTER(ctypes.c_int64), dp, dp, dp]
+    lib.fmo_bwd_brute.argtypes = [dp, dp, dp, dp, dp, L, L, L, L, I, I,
                                   dp, dp, dp]
     return lib
 
@@ -106,15 +106,17 @@ def attention_matrix(q, k, p, causal):
     return A
 
 
-def fwd_brute(q, k, v, p, causal):
-    """Brute force O(N^2 D) forward; returns (O, G)."""
+def fwd_brute(q, k, v, p, causal, with_abs=False):
+    """Brute force O(N^2 D) forward; returns (O, G) or, with ``with_abs``,
+    (O, G, sum_n |w_in|)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, N, D = _shape4(q)
     out = np.empty_like(q)
     g = np.empty((B, H, N))
+    gabs = np.empty((B, H, N)) if with_abs else None
     _load().fmo_fwd_brute(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
-                          int(causal), _ptr(out), _ptr(g))
-    return out, g
+                          int(causal), _ptr(out), _ptr(g), _ptr(gabs))
+    return (out, g, gabs) if with_abs else (out, g)
 
 
 def fwd_fact(q, k, v, p, causal):
@@ -128,30 +130,40 @@ def fwd_fact(q, k, v, p, causal):
     return out, g
 
 
-def fwd_rows(q, k, v, p, causal, rows):
+def fwd_rows(q, k, v, p, causal, rows, with_abs=False):
     """Brute force for selected rows (flat index b*H*N + h*N + i).
 
-    Returns (O_rows [n, D], G_rows [n]).
+    Returns (O_rows [n, D], G_rows [n]) and, with ``with_abs``, also
+    sum_n |w_in| per row.
     """
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, N, D = _shape4(q)
     rows = np.ascontiguousarray(rows, dtype=np.int64)
     out = np.empty((rows.size, D))
     g = np.empty(rows.size)
+    gabs = np.empty(rows.size) if with_abs else None
     _load().fmo_fwd_rows(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
                          int(causal), rows.size,
                          rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
-                         _ptr(out), _ptr(g))
-    return out, g
+                         _ptr(out), _ptr(g), _ptr(gabs))
+    return (out, g, gabs) if with_abs else (out, g)
 
 
-def bwd_brute(q, k, v, dout, p, causal):
-    """Brute force O(N^2 D) backward; returns (dq, dk, dv)."""
+def bwd_brute(q, k, v, dout, p, causal, o_used=None):
+    """Brute force O(N^2 D) backward; returns (dq, dk, dv).
+
+    ``o_used``: the forward output the gradient is taken at (default: the
+    exact O).  Tests pass the oracle's own O rounded to the I/O dtype to model
+    a backward that consumes the stored output."""
     q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
     B, H, N, D = _shape4(q)
+    if o_used is not None:
+        o_used = _f64(o_used)
+        assert o_used.shape == q.shape
     dq = np.empty_like(q)
     dk = np.empty_like(q)
     dv = np.empty_like(q)
-    _load().fmo_bwd_brute(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), B, H, N, D,
-                          int(p), int(causal), _ptr(dq), _ptr(dk), _ptr(dv))
+    _load().fmo_bwd_brute(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(o_used),
+                          B, H, N, D, int(p), int(causal), _ptr(dq), _ptr(dk),
+                          _ptr(dv))
     return dq, dk, dv

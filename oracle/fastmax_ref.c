@@ -128,26 +128,29 @@ void fmo_attention_matrix(const double *q, const double *k, long N, long D,
 /* ------------------------------------------------------------------------ */
 static void brute_row(const double *qh_i, const double *kh, const double *v,
                       long i, long N, long D, int p, int causal, double *o,
-                      double *g_out)
+                      double *g_out, double *gabs_out)
 {
     long nend = causal ? i + 1 : N;
-    double g = 0.0;
+    double g = 0.0, gabs = 0.0;
     for (long d = 0; d < D; ++d) o[d] = 0.0;
     for (long n = 0; n < nend; ++n) {
         double s = 0.0;
         for (long d = 0; d < D; ++d) s += qh_i[d] * kh[n * D + d];
         double w = f_taylor(s, p);
         g += w;
+        gabs += fabs(w);
         for (long d = 0; d < D; ++d) o[d] += w * v[n * D + d];
     }
     for (long d = 0; d < D; ++d) o[d] /= g;
     if (g_out) *g_out = g;
+    if (gabs_out) *gabs_out = gabs;
 }
 
-/* Full brute-force forward, O(N^2 D) per head. g may be NULL. */
+/* Full brute-force forward, O(N^2 D) per head.  g (row sums G_i) and gabs
+ * (sum_n |w_in|, the scale of the cancellation in G for p = 1) may be NULL. */
 void fmo_fwd_brute(const double *q, const double *k, const double *v, long B,
                    long H, long N, long D, int p, int causal, double *out,
-                   double *g)
+                   double *g, double *gabs)
 {
     long rows = B * H * N;
     double *qh = malloc(sizeof(double) * rows * D);
@@ -158,17 +161,18 @@ void fmo_fwd_brute(const double *q, const double *k, const double *v, long B,
     for (long r = 0; r < rows; ++r) {
         long head = r / N, i = r % N;
         brute_row(qh + r * D, kh + head * N * D, v + head * N * D, i, N, D, p,
-                  causal, out + r * D, g ? g + r : NULL);
+                  causal, out + r * D, g ? g + r : NULL, gabs ? gabs + r : NULL);
     }
     free(qh);
     free(kh);
 }
 
 /* Brute force on a sample of rows.  rows[] holds flat indices b*H*N + h*N + i;
- * out_rows is [nrows, D], g_rows is [nrows] (may be NULL). */
+ * out_rows is [nrows, D]; g_rows and gabs_rows are [nrows] (may be NULL). */
 void fmo_fwd_rows(const double *q, const double *k, const double *v, long B,
                   long H, long N, long D, int p, int causal, long nrows,
-                  const int64_t *rows, double *out_rows, double *g_rows)
+                  const int64_t *rows, double *out_rows, double *g_rows,
+                  double *gabs_rows)
 {
     (void)B;
     (void)H;
@@ -183,7 +187,8 @@ void fmo_fwd_rows(const double *q, const double *k, const double *v, long B,
         for (long n = 0; n < nend; ++n)
             standardize_row(k + (head * N + n) * D, D, kh + n * D, NULL, NULL);
         brute_row(qh, kh, v + head * N * D, i, N, D, p, causal,
-                  out_rows + t * D, g_rows ? g_rows + t : NULL);
+                  out_rows + t * D, g_rows ? g_rows + t : NULL,
+                  gabs_rows ? gabs_rows + t : NULL);
         free(qh);
         free(kh);
     }
@@ -346,9 +351,13 @@ static void std_backward_row(const double *xh, const double *dxh, double sig,
     for (long d = 0; d < D; ++d) dx[d] = (dxh[d] - m1 - xh[d] * m2) / sig;
 }
 
+/* o_used (nullable, [B,H,N,D]) is the forward output the gradient is taken
+ * at: NULL means the exact O computed here; a caller may pass that O rounded
+ * to its storage precision (the stored output a bf16 backward consumes). */
 void fmo_bwd_brute(const double *q, const double *k, const double *v,
-                   const double *dout, long B, long H, long N, long D, int p,
-                   int causal, double *dq, double *dk, double *dv)
+                   const double *dout, const double *o_used, long B, long H,
+                   long N, long D, int p, int causal, double *dq, double *dk,
+                   double *dv)
 {
     long heads = B * H;
     for (long hd = 0; hd < heads; ++hd) {
@@ -366,7 +375,10 @@ void fmo_bwd_brute(const double *q, const double *k, const double *v,
         /* forward, per row */
 #pragma omp parallel for schedule(dynamic, 8)
         for (long i = 0; i < N; ++i)
-            brute_row(qh + i * D, kh, vb, i, N, D, p, causal, o + i * D, G + i);
+            brute_row(qh + i * D, kh, vb, i, N, D, p, causal, o + i * D, G + i,
+                      NULL);
+        if (o_used)
+            memcpy(o, o_used + hd * N * D, sizeof(double) * N * D);
         /* dq^_i: row i, sums over its allowed columns l */
 #pragma omp parallel for schedule(dynamic, 8)
         for (long i = 0; i < N; ++i) {

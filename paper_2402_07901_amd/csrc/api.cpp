@@ -1,0 +1,99 @@
+// C ABI of the Fastmax library: host-side validation, workspace sizing and
+// dispatch to the HIP kernels.  Every check runs before the first HIP call.
+#include <stdint.h>
+
+#include "../../include/fastmax.h"
+#include "fm_internal.h"
+
+namespace {
+
+bool supported_d(int D) { return D == 16 || D == 32 || D == 64; }
+
+int check_common(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+{
+    if (B < 1 || H < 1 || N < 1) return FASTMAX_EINVAL;
+    if (p != 1 && p != 2) return FASTMAX_EINVAL;
+    if (causal != 0 && causal != 1) return FASTMAX_EINVAL;
+    if (dt != FASTMAX_F32 && dt != FASTMAX_BF16) return FASTMAX_EINVAL;
+    if (!supported_d(D)) return FASTMAX_EUNSUPPORTED;
+    // B*H*N*D < 2^62 and B*H fits a grid dimension
+    unsigned __int128 tot = (unsigned __int128)B * H * N * D;
+    if (tot >= ((unsigned __int128)1 << 62)) return FASTMAX_EINVAL;
+    if ((long long)B * H > 0x7fffffffLL) return FASTMAX_EINVAL;
+    return FASTMAX_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t fwd_ws(int, int, int, int, int, int, fastmax_dtype_t) { return 0; }
+
+size_t bwd_ws(int B, int H, int N, int D, int, int, fastmax_dtype_t)
+{
+    return fm::generic_bwd_workspace(B, H, N, D);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
+                               fastmax_dtype_t dt, int backward)
+{
+    if (check_common(B, H, N, D, p, causal, dt) != FASTMAX_OK) return 0;
+    return backward ? bwd_ws(B, H, N, D, p, causal, dt) : fwd_ws(B, H, N, D, p, causal, dt);
+}
+
+int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,
+                int N, int D, int p, int causal, fastmax_dtype_t dt, void *workspace,
+                size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_common(B, H, N, D, p, causal, dt);
+    if (rc != FASTMAX_OK) return rc;
+    if (!q || !k || !v || !out) return FASTMAX_ENULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+        (g && !aligned16(g)))
+        return FASTMAX_EALIGN;
+    size_t need = fwd_ws(B, H, N, D, p, causal, dt);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
+    if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
+    hipError_t e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal,
+                                   dt == FASTMAX_BF16, stream);
+    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
+int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, const void *dout,
+                const float *g, void *dq, void *dk, void *dv, int B, int H, int N, int D, int p,
+                int causal, fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                hipStream_t stream)
+{
+    int rc = check_common(B, H, N, D, p, causal, dt);
+    if (rc != FASTMAX_OK) return rc;
+    if (!q || !k || !v || !out || !dout || !g || !dq || !dk || !dv) return FASTMAX_ENULL;
+    const void *ptrs[] = {q, k, v, out, dout, g, dq, dk, dv};
+    for (const void *ptr : ptrs)
+        if (!aligned16(ptr)) return FASTMAX_EALIGN;
+    size_t need = bwd_ws(B, H, N, D, p, causal, dt);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
+    if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
+    hipError_t e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
+                                   dt == FASTMAX_BF16, workspace, stream);
+    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
+const char *fastmax_strerror(int code)
+{
+    switch (code) {
+    case FASTMAX_OK: return "success";
+    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, or B/H/N < 1)";
+    case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32 or 64)";
+    case FASTMAX_ENULL: return "required pointer is NULL";
+    case FASTMAX_EALIGN: return "pointer not 16-byte aligned";
+    case FASTMAX_EWORKSPACE: return "workspace missing or too small";
+    case FASTMAX_EHIP: return "HIP runtime error while enqueuing";
+    default: return "unknown error code";
+    }
+}
+
+const char *fastmax_version(void) { return "0.1.0"; }
+
+}  // extern "C"

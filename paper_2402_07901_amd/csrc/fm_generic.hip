@@ -1,0 +1,686 @@
+// Generic Fastmax kernels: float32 VALU arithmetic, the moment state of one
+// column slice held in LDS, tokens processed in chunks of CH.  They serve
+// every supported (D, p, causal, dtype) and are the reference GPU path the
+// MFMA kernels are checked against; the MFMA kernels take over where they
+// apply.
+//
+// Notation (Sec. 2.4): phi(k) = [1, k, (k_m k_l)_{m<=l}] are the key-side
+// features, psi(q) = [1, q, (c_ml q_m q_l)_{m<=l}] with c_mm = 1/2 and
+// c_ml = 1 (m < l) the query-side ones, so psi(q).phi(k) = f_p(q.k).  The
+// moment state of a slice of value columns J is S[f][j] = sum_n phi_f(k^_n)
+// v'_nj, v' = [v | 1] (the ones column yields G).  Causal rows use the
+// chunk-exclusive prefix of S plus the in-chunk tril block.
+#include <hip/hip_runtime.h>
+
+#include "fm_common.h"
+#include "fm_internal.h"
+
+namespace fm {
+namespace generic {
+
+constexpr int CH = 16;    // tokens per chunk
+constexpr int NT = 256;   // threads per workgroup
+
+template <int D, bool P2> struct feat {
+    static constexpr int P = n_features(D, P2 ? 2 : 1);
+    static constexpr int NPAIR = P2 ? D * (D + 1) / 2 : 0;
+};
+
+// Builds the (m, l) table of the quadratic features in LDS.
+template <int D, bool P2>
+__device__ void build_pairs(uint8_t *pm, uint8_t *pl)
+{
+    constexpr int NPAIR = feat<D, P2>::NPAIR;
+    for (int t = threadIdx.x; t < NPAIR; t += NT) {
+        int m = 0, r = t;
+        while (r >= D - m) { r -= D - m; ++m; }
+        pm[t] = (uint8_t)m;
+        pl[t] = (uint8_t)(m + r);
+    }
+}
+
+// Key-side feature phi_f of a standardised row x (LDS).
+template <int D>
+__device__ __forceinline__ float phi(int f, const float *x, const uint8_t *pm, const uint8_t *pl)
+{
+    if (f == 0) return 1.0f;
+    if (f <= D) return x[f - 1];
+    int t = f - 1 - D;
+    return x[pm[t]] * x[pl[t]];
+}
+
+// Query-side feature psi_f (carries the 1/2 of the diagonal pairs).
+template <int D>
+__device__ __forceinline__ float psi(int f, const float *x, const uint8_t *pm, const uint8_t *pl)
+{
+    if (f == 0) return 1.0f;
+    if (f <= D) return x[f - 1];
+    int t = f - 1 - D;
+    int m = pm[t], l = pl[t];
+    float v = x[m] * x[l];
+    return m == l ? 0.5f * v : v;
+}
+
+// Loads `rows` token rows starting at token n0 of a head and standardises
+// them (Sec. 2.2, Eqs. 6-7: population std, no epsilon) into dst (stride
+// D + 1, float32).  Rows past N are zero.  Optionally writes 1/std.
+template <int D, typename T>
+__device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_out)
+{
+    constexpr int DP = D + 1;
+    for (int e = threadIdx.x; e < CH * D; e += NT) {
+        int r = e / D, d = e % D;
+        int n = n0 + r;
+        dst[r * DP + d] = n < N ? io<T>::ld(src, (size_t)n * D + d) : 0.0f;
+    }
+    __syncthreads();
+    if (threadIdx.x < CH) {
+        int r = threadIdx.x;
+        float *x = dst + r * DP;
+        if (n0 + r < N) {
+            float mu = 0.0f;
+            for (int d = 0; d < D; ++d) mu += x[d];
+            mu *= 1.0f / D;
+            float var = 0.0f;
+            for (int d = 0; d < D; ++d) {
+                float c = x[d] - mu;
+                var = fmaf(c, c, var);
+            }
+            float rs = rsqrtf(var * (1.0f / D));
+            for (int d = 0; d < D; ++d) x[d] = (x[d] - mu) * rs;
+            if (rstd_out) rstd_out[r] = rs;
+        } else if (rstd_out) {
+            rstd_out[r] = 0.0f;
+        }
+    }
+    __syncthreads();
+}
+
+// S[f][j] += sum_{r < CH} phi_f(x_r) val[r][j], j < WS.
+template <int D, bool P2, int WS>
+__device__ void state_update(float *S, const float *x, const float *val, const uint8_t *pm,
+                             const uint8_t *pl)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int DP = D + 1;
+    for (int f = threadIdx.x; f < P; f += NT) {
+        float acc[WS];
+#pragma unroll
+        for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
+        for (int r = 0; r < CH; ++r) {
+            float ph = phi<D>(f, x + r * DP, pm, pl);
+#pragma unroll
+            for (int j = 0; j < WS; ++j) acc[j] = fmaf(ph, val[r * WS + j], acc[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < WS; ++j) S[f * WS + j] += acc[j];
+    }
+}
+
+// out[r][j] += sum_f psi_f(x_r) S[f][j]   (LDS atomics; out is CH x WS).
+template <int D, bool P2, int WS>
+__device__ void contract_psi(const float *S, const float *x, float *out, const uint8_t *pm,
+                             const uint8_t *pl)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int DP = D + 1;
+    constexpr int NG = NT / CH;
+    const int r = threadIdx.x % CH, fg = threadIdx.x / CH;
+    float acc[WS];
+#pragma unroll
+    for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
+    for (int f = fg; f < P; f += NG) {
+        float ps = psi<D>(f, x + r * DP, pm, pl);
+#pragma unroll
+        for (int j = 0; j < WS; ++j) acc[j] = fmaf(ps, S[f * WS + j], acc[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < WS; ++j) atomicAdd(&out[r * WS + j], acc[j]);
+}
+
+// Gradient-side contraction (backward):
+//   out[r][a] = sum_{j<WS} coef[r][j] (S[1+a][j] + [p=2] sum_m x_rm S[(a,m)][j])
+// which is the moment form of sum_n f'(s_rn) (coef_r . val_n) y_n[a] when S
+// holds the moments of (y, val).
+template <int D, bool P2, int WS>
+__device__ void contract_grad(const float *S, const float *x, const float *coef, float *out)
+{
+    constexpr int DP = D + 1;
+    constexpr int AG = NT / CH;          // a-groups
+    const int r = threadIdx.x % CH, ag = threadIdx.x / CH;
+    const float *xr = x + r * DP;
+    for (int a = ag; a < D; a += AG) {
+        float acc = 0.0f;
+        for (int j = 0; j < WS; ++j) {
+            float inner = S[(1 + a) * WS + j];
+            if (P2) {
+                for (int m = 0; m < D; ++m) {
+                    int lo = m < a ? m : a, hi = m < a ? a : m;
+                    inner = fmaf(xr[m], S[pair_feature(D, lo, hi) * WS + j], inner);
+                }
+            }
+            acc = fmaf(coef[r * WS + j], inner, acc);
+        }
+        out[r * D + a] = acc;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Forward.  grid = (B*H, slices); slice s owns value columns [s*W, s*W+W)
+// plus the ones column (local index W), so every slice has G for its divide.
+// ---------------------------------------------------------------------------
+template <int D, bool P2, int WS, bool CAUSAL, typename T>
+__global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const T *__restrict__ k,
+                                                 const T *__restrict__ v, T *__restrict__ out,
+                                                 float *__restrict__ g, int N)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int NPAIR = feat<D, P2>::NPAIR;
+    constexpr int W = WS - 1;
+    constexpr int DP = D + 1;
+    constexpr int POW = P2 ? 2 : 1;
+
+    __shared__ float S[P * WS];
+    __shared__ float xq[CH * DP];
+    __shared__ float xk[CH * DP];
+    __shared__ float vv[CH * WS];
+    __shared__ float wblk[CH * CH];
+    __shared__ float F[CH * WS];
+    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+
+    const int head = blockIdx.x;
+    const int c0 = blockIdx.y * W;
+    const size_t hb = (size_t)head * N * D;
+    q += hb;
+    k += hb;
+    v += hb;
+    out += hb;
+    if (g) g += (size_t)head * N;
+
+    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    build_pairs<D, P2>(pm, pl);
+    __syncthreads();
+
+    auto load_vals = [&](int n0) {
+        for (int e = threadIdx.x; e < CH * WS; e += NT) {
+            int r = e / WS, j = e % WS, n = n0 + r;
+            float x = 0.0f;
+            if (n < N) {
+                if (j == W) x = 1.0f;
+                else if (c0 + j < D) x = io<T>::ld(v, (size_t)n * D + c0 + j);
+            }
+            vv[e] = x;
+        }
+    };
+    auto write_out = [&](int n0) {
+        for (int e = threadIdx.x; e < CH * W; e += NT) {
+            int r = e / W, j = e % W, n = n0 + r;
+            if (n < N && c0 + j < D)
+                io<T>::st(out, (size_t)n * D + c0 + j, F[r * WS + j] / F[r * WS + W]);
+        }
+        if (g && blockIdx.y == 0)
+            for (int r = threadIdx.x; r < CH; r += NT)
+                if (n0 + r < N) g[n0 + r] = F[r * WS + W];
+    };
+
+    const int nch = (N + CH - 1) / CH;
+    if (!CAUSAL) {
+        for (int c = 0; c < nch; ++c) {
+            load_std<D>(k, c * CH, N, xk, nullptr);
+            load_vals(c * CH);
+            __syncthreads();
+            state_update<D, P2, WS>(S, xk, vv, pm, pl);
+            __syncthreads();
+        }
+        for (int c = 0; c < nch; ++c) {
+            load_std<D>(q, c * CH, N, xq, nullptr);
+            for (int e = threadIdx.x; e < CH * WS; e += NT) F[e] = 0.0f;
+            __syncthreads();
+            contract_psi<D, P2, WS>(S, xq, F, pm, pl);
+            __syncthreads();
+            write_out(c * CH);
+            __syncthreads();
+        }
+    } else {
+        for (int c = 0; c < nch; ++c) {
+            const int n0 = c * CH;
+            load_std<D>(q, n0, N, xq, nullptr);
+            load_std<D>(k, n0, N, xk, nullptr);
+            load_vals(n0);
+            // in-chunk tril block of weights
+            {
+                int i = threadIdx.x / CH, t = threadIdx.x % CH;
+                float w = 0.0f;
+                if (t <= i) {
+                    float s = 0.0f;
+                    for (int d = 0; d < D; ++d) s = fmaf(xq[i * DP + d], xk[t * DP + d], s);
+                    w = taylor<POW>(s);
+                }
+                wblk[i * CH + t] = w;
+            }
+            __syncthreads();
+            for (int e = threadIdx.x; e < CH * WS; e += NT) {
+                int i = e / WS, j = e % WS;
+                float acc = 0.0f;
+                for (int t = 0; t <= i; ++t) acc = fmaf(wblk[i * CH + t], vv[t * WS + j], acc);
+                F[e] = acc;
+            }
+            __syncthreads();
+            contract_psi<D, P2, WS>(S, xq, F, pm, pl);   // exclusive prefix S_<c
+            __syncthreads();
+            write_out(n0);
+            state_update<D, P2, WS>(S, xk, vv, pm, pl);
+            __syncthreads();
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Backward.
+//   u_i = dO_i / G_i,  c_i = (dO_i . O_i) / G_i,  u~_i = [u_i, -c_i]
+//   dw_in = u~_i . v'_n,  ds_in = f'(s_in) dw_in       (Sec. 2.3, Eq. bound)
+//   dq^_i = sum_n ds_in k^_n,  dk^_n = sum_i ds_in q^_i,  dv_n = sum_i w_in u_i
+// Columns j run over the D+1 columns of v' / u~; slices split them.
+// ---------------------------------------------------------------------------
+
+// c_i = (dO_i . O_i) / G_i, one row per thread.
+template <int D, typename T>
+__global__ __launch_bounds__(NT) void bwd_rowdot_kernel(const T *__restrict__ o,
+                                                        const T *__restrict__ dout,
+                                                        const float *__restrict__ g,
+                                                        float *__restrict__ cvec, size_t rows)
+{
+    size_t r = (size_t)blockIdx.x * NT + threadIdx.x;
+    if (r >= rows) return;
+    float acc = 0.0f;
+    for (int d = 0; d < D; ++d)
+        acc = fmaf(io<T>::ld(dout, r * D + d), io<T>::ld(o, r * D + d), acc);
+    cvec[r] = acc / g[r];
+}
+
+// Loads CH rows of u~ restricted to global columns [gc0, gc0 + WS).
+template <int D, int WS, typename T>
+__device__ void load_utilde(const T *dout, const float *g, const float *cvec, int n0, int N,
+                            int gc0, float *dst)
+{
+    for (int e = threadIdx.x; e < CH * WS; e += NT) {
+        int r = e / WS, j = e % WS, n = n0 + r, gc = gc0 + j;
+        float x = 0.0f;
+        if (n < N) {
+            if (gc < D) x = io<T>::ld(dout, (size_t)n * D + gc) / g[n];
+            else if (gc == D) x = -cvec[n];
+        }
+        dst[e] = x;
+    }
+}
+
+template <int D, int WS, typename T>
+__device__ void load_vprime(const T *v, int n0, int N, int gc0, float *dst)
+{
+    for (int e = threadIdx.x; e < CH * WS; e += NT) {
+        int r = e / WS, j = e % WS, n = n0 + r, gc = gc0 + j;
+        float x = 0.0f;
+        if (n < N) {
+            if (gc < D) x = io<T>::ld(v, (size_t)n * D + gc);
+            else if (gc == D) x = 1.0f;
+        }
+        dst[e] = x;
+    }
+}
+
+// In-chunk (tril) part of all three gradients; plain stores initialise the
+// float32 accumulators (zeros for the non-causal problem, whose every pair is
+// handled by the moment kernels).
+template <int D, bool P2, bool CAUSAL, typename T>
+__global__ __launch_bounds__(NT) void bwd_intra_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+    const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
+    float *__restrict__ dqh, float *__restrict__ dkh, float *__restrict__ dva, int N)
+{
+    constexpr int DP = D + 1;
+    constexpr int D1 = D + 1;
+    constexpr int POW = P2 ? 2 : 1;
+    __shared__ float xq[CH * DP];
+    __shared__ float xk[CH * DP];
+    __shared__ float vp[CH * D1];
+    __shared__ float ut[CH * D1];
+    __shared__ float E[CH * CH];   // f'(s) dw
+    __shared__ float Wm[CH * CH];  // f(s)
+
+    const int head = blockIdx.x, n0 = blockIdx.y * CH;
+    const size_t hb = (size_t)head * N * D;
+    q += hb; k += hb; v += hb; dout += hb;
+    g += (size_t)head * N;
+    cvec += (size_t)head * N;
+    dqh += hb; dkh += hb; dva += hb;
+
+    if (!CAUSAL) {
+        for (int e = threadIdx.x; e < CH * D; e += NT) {
+            int r = e / D, n = n0 + r;
+            if (n < N) {
+                size_t o = (size_t)n * D + e % D;
+                dqh[o] = 0.0f; dkh[o] = 0.0f; dva[o] = 0.0f;
+            }
+        }
+        return;
+    }
+    load_std<D>(q, n0, N, xq, nullptr);
+    load_std<D>(k, n0, N, xk, nullptr);
+    load_vprime<D, D1>(v, n0, N, 0, vp);
+    load_utilde<D, D1>(dout, g, cvec, n0, N, 0, ut);
+    __syncthreads();
+    {
+        int i = threadIdx.x / CH, t = threadIdx.x % CH;
+        float e = 0.0f, w = 0.0f;
+        if (t <= i && n0 + i < N) {
+            float s = 0.0f;
+            for (int d = 0; d < D; ++d) s = fmaf(xq[i * DP + d], xk[t * DP + d], s);
+            float dw = 0.0f;
+            for (int j = 0; j < D1; ++j) dw = fmaf(ut[i * D1 + j], vp[t * D1 + j], dw);
+            e = dtaylor<POW>(s) * dw;
+            w = taylor<POW>(s);
+        }
+        E[i * CH + t] = e;
+        Wm[i * CH + t] = w;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < CH * D; e += NT) {
+        int r = e / D, a = e % D, n = n0 + r;
+        if (n >= N) continue;
+        float aq = 0.0f, ak = 0.0f, av = 0.0f;
+        for (int t = 0; t < CH; ++t) {
+            aq = fmaf(E[r * CH + t], xk[t * DP + a], aq);   // row r as query
+            ak = fmaf(E[t * CH + r], xq[t * DP + a], ak);   // row r as key
+            av = fmaf(Wm[t * CH + r], ut[t * D1 + a], av);
+        }
+        size_t o = (size_t)n * D + a;
+        dqh[o] = aq;
+        dkh[o] = ak;
+        dva[o] = av;
+    }
+}
+
+// dq^ from the forward-direction moments of (k^, v'): grid = (B*H, slices over
+// the D+1 columns of v').  Causal rows see the chunk-exclusive prefix.
+template <int D, bool P2, int WS, bool CAUSAL, typename T>
+__global__ __launch_bounds__(NT) void bwd_qscan_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+    const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
+    float *__restrict__ dqh, int N)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int NPAIR = feat<D, P2>::NPAIR;
+    constexpr int DP = D + 1;
+    __shared__ float S[P * WS];
+    __shared__ float xq[CH * DP];
+    __shared__ float xk[CH * DP];
+    __shared__ float vp[CH * WS];
+    __shared__ float ut[CH * WS];
+    __shared__ float part[CH * D];
+    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+
+    const int head = blockIdx.x, gc0 = blockIdx.y * WS;
+    const size_t hb = (size_t)head * N * D;
+    q += hb; k += hb; v += hb; dout += hb; dqh += hb;
+    g += (size_t)head * N;
+    cvec += (size_t)head * N;
+
+    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    build_pairs<D, P2>(pm, pl);
+    __syncthreads();
+    const int nch = (N + CH - 1) / CH;
+
+    auto contract_and_add = [&](int n0) {
+        load_std<D>(q, n0, N, xq, nullptr);
+        load_utilde<D, WS>(dout, g, cvec, n0, N, gc0, ut);
+        __syncthreads();
+        contract_grad<D, P2, WS>(S, xq, ut, part);
+        __syncthreads();
+        for (int e = threadIdx.x; e < CH * D; e += NT) {
+            int n = n0 + e / D;
+            if (n < N) atomicAdd(&dqh[(size_t)n * D + e % D], part[e]);
+        }
+        __syncthreads();
+    };
+    auto update = [&](int n0) {
+        load_std<D>(k, n0, N, xk, nullptr);
+        load_vprime<D, WS>(v, n0, N, gc0, vp);
+        __syncthreads();
+        state_update<D, P2, WS>(S, xk, vp, pm, pl);
+        __syncthreads();
+    };
+    if (!CAUSAL) {
+        for (int c = 0; c < nch; ++c) update(c * CH);
+        for (int c = 0; c < nch; ++c) contract_and_add(c * CH);
+    } else {
+        for (int c = 0; c < nch; ++c) {
+            contract_and_add(c * CH);
+            update(c * CH);
+        }
+    }
+}
+
+// dk^ and dv from the reverse-direction moments of (q^, u~):
+//   T[f][j] = sum_i phi_f(q^_i) u~_ij over rows i after the chunk (causal) or
+//   all rows; dk^_n[a] += sum_j v'_nj (T[1+a][j] + sum_m k^_nm T[(a,m)][j]),
+//   dv_n[j] += sum_f psi_f(k^_n) T[f][j].
+template <int D, bool P2, int WS, bool CAUSAL, typename T>
+__global__ __launch_bounds__(NT) void bwd_kscan_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+    const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
+    float *__restrict__ dkh, float *__restrict__ dva, int N)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int NPAIR = feat<D, P2>::NPAIR;
+    constexpr int DP = D + 1;
+    __shared__ float S[P * WS];
+    __shared__ float xq[CH * DP];
+    __shared__ float xk[CH * DP];
+    __shared__ float vp[CH * WS];
+    __shared__ float ut[CH * WS];
+    __shared__ float part[CH * D];
+    __shared__ float pv[CH * WS];
+    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+
+    const int head = blockIdx.x, gc0 = blockIdx.y * WS;
+    const size_t hb = (size_t)head * N * D;
+    q += hb; k += hb; v += hb; dout += hb; dkh += hb; dva += hb;
+    g += (size_t)head * N;
+    cvec += (size_t)head * N;
+
+    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    build_pairs<D, P2>(pm, pl);
+    __syncthreads();
+    const int nch = (N + CH - 1) / CH;
+
+    auto contract_and_add = [&](int n0) {
+        load_std<D>(k, n0, N, xk, nullptr);
+        load_vprime<D, WS>(v, n0, N, gc0, vp);
+        for (int e = threadIdx.x; e < CH * WS; e += NT) pv[e] = 0.0f;
+        __syncthreads();
+        contract_grad<D, P2, WS>(S, xk, vp, part);
+        contract_psi<D, P2, WS>(S, xk, pv, pm, pl);
+        __syncthreads();
+        for (int e = threadIdx.x; e < CH * D; e += NT) {
+            int n = n0 + e / D;
+            if (n < N) atomicAdd(&dkh[(size_t)n * D + e % D], part[e]);
+        }
+        for (int e = threadIdx.x; e < CH * WS; e += NT) {
+            int n = n0 + e / WS, gc = gc0 + e % WS;
+            if (n < N && gc < D) atomicAdd(&dva[(size_t)n * D + gc], pv[e]);
+        }
+        __syncthreads();
+    };
+    auto update = [&](int n0) {
+        load_std<D>(q, n0, N, xq, nullptr);
+        load_utilde<D, WS>(dout, g, cvec, n0, N, gc0, ut);
+        __syncthreads();
+        state_update<D, P2, WS>(S, xq, ut, pm, pl);
+        __syncthreads();
+    };
+    if (!CAUSAL) {
+        for (int c = 0; c < nch; ++c) update(c * CH);
+        for (int c = 0; c < nch; ++c) contract_and_add(c * CH);
+    } else {
+        for (int c = nch - 1; c >= 0; --c) {
+            contract_and_add(c * CH);
+            update(c * CH);
+        }
+    }
+}
+
+// Back through Eqs. (6)-(7) and cast: dx = (dx^ - mean dx^ - x^ mean(dx^ x^)) / std.
+template <int D, typename T>
+__global__ __launch_bounds__(NT) void bwd_finish_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const float *__restrict__ dqh,
+    const float *__restrict__ dkh, const float *__restrict__ dva, T *__restrict__ dq,
+    T *__restrict__ dk, T *__restrict__ dv, size_t rows)
+{
+    size_t r = (size_t)blockIdx.x * NT + threadIdx.x;
+    if (r >= rows) return;
+    const size_t b = r * D;
+    for (int which = 0; which < 2; ++which) {
+        const T *x = which ? k : q;
+        const float *dxh = which ? dkh : dqh;
+        T *dx = which ? dk : dq;
+        float mu = 0.0f;
+        for (int d = 0; d < D; ++d) mu += io<T>::ld(x, b + d);
+        mu *= 1.0f / D;
+        float var = 0.0f;
+        for (int d = 0; d < D; ++d) {
+            float c = io<T>::ld(x, b + d) - mu;
+            var = fmaf(c, c, var);
+        }
+        float rs = rsqrtf(var * (1.0f / D));
+        float m1 = 0.0f, m2 = 0.0f;
+        for (int d = 0; d < D; ++d) {
+            float xh = (io<T>::ld(x, b + d) - mu) * rs;
+            m1 += dxh[b + d];
+            m2 = fmaf(dxh[b + d], xh, m2);
+        }
+        m1 *= 1.0f / D;
+        m2 *= 1.0f / D;
+        for (int d = 0; d < D; ++d) {
+            float xh = (io<T>::ld(x, b + d) - mu) * rs;
+            io<T>::st(dx, b + d, (dxh[b + d] - m1 - xh * m2) * rs);
+        }
+    }
+    for (int d = 0; d < D; ++d) io<T>::st(dv, b + d, dva[b + d]);
+}
+
+// Column-slice width (including the ones column) that keeps the LDS state
+// of a workgroup under 64 KiB.
+template <int D, bool P2> struct slice_width;
+template <> struct slice_width<16, true> { static constexpr int v = 17; };
+template <> struct slice_width<32, true> { static constexpr int v = 17; };
+template <> struct slice_width<64, true> { static constexpr int v = 5; };
+template <> struct slice_width<16, false> { static constexpr int v = 17; };
+template <> struct slice_width<32, false> { static constexpr int v = 33; };
+template <> struct slice_width<64, false> { static constexpr int v = 65; };
+
+template <int D, bool P2, typename T>
+static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void *out, float *g,
+                               int BH, int N, int causal, hipStream_t st)
+{
+    constexpr int WS = slice_width<D, P2>::v;
+    constexpr int W = WS - 1;
+    dim3 grid(BH, (D + W - 1) / W);
+    if (causal)
+        hipLaunchKernelGGL((fwd_kernel<D, P2, WS, true, T>), grid, dim3(NT), 0, st,
+                           (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N);
+    else
+        hipLaunchKernelGGL((fwd_kernel<D, P2, WS, false, T>), grid, dim3(NT), 0, st,
+                           (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N);
+    return hipGetLastError();
+}
+
+template <int D, bool P2, bool CAUSAL, typename T>
+static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, const void *o,
+                                const void *dout, const float *g, void *dq, void *dk, void *dv,
+                                int BH, int N, float *ws, hipStream_t st)
+{
+    constexpr int WS = slice_width<D, P2>::v;
+    const size_t rows = (size_t)BH * N;
+    float *cvec = ws;
+    float *dqh = cvec + rows;
+    float *dkh = dqh + rows * D;
+    float *dva = dkh + rows * D;
+    const int rb = (int)((rows + NT - 1) / NT);
+    hipLaunchKernelGGL((bwd_rowdot_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)o,
+                       (const T *)dout, g, cvec, rows);
+    hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T>), dim3(BH, (N + CH - 1) / CH),
+                       dim3(NT), 0, st, (const T *)q, (const T *)k, (const T *)v,
+                       (const T *)dout, g, cvec, dqh, dkh, dva, N);
+    dim3 grid(BH, (D + 1 + WS - 1) / WS);
+    hipLaunchKernelGGL((bwd_qscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
+                       (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dqh,
+                       N);
+    hipLaunchKernelGGL((bwd_kscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
+                       (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dkh,
+                       dva, N);
+    hipLaunchKernelGGL((bwd_finish_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)q,
+                       (const T *)k, dqh, dkh, dva, (T *)dq, (T *)dk, (T *)dv, rows);
+    return hipGetLastError();
+}
+
+template <int D, bool P2, typename T>
+static hipError_t bwd_dispatch(const void *q, const void *k, const void *v, const void *o,
+                               const void *dout, const float *g, void *dq, void *dk, void *dv,
+                               int BH, int N, int causal, float *ws, hipStream_t st)
+{
+    if (causal)
+        return bwd_dispatch2<D, P2, true, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, ws, st);
+    return bwd_dispatch2<D, P2, false, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, ws, st);
+}
+
+}  // namespace generic
+
+size_t generic_bwd_workspace(int B, int H, int N, int D)
+{
+    size_t rows = (size_t)B * H * N;
+    return sizeof(float) * (rows + 3 * rows * (size_t)D);
+}
+
+#define FM_DISPATCH_D_P(FN, D, p, ...)                                   \
+    ((D) == 16 ? ((p) == 2 ? FN<16, true, T>(__VA_ARGS__) : FN<16, false, T>(__VA_ARGS__)) : \
+     (D) == 32 ? ((p) == 2 ? FN<32, true, T>(__VA_ARGS__) : FN<32, false, T>(__VA_ARGS__)) : \
+                 ((p) == 2 ? FN<64, true, T>(__VA_ARGS__) : FN<64, false, T>(__VA_ARGS__)))
+
+template <typename T>
+static hipError_t gen_fwd_t(const void *q, const void *k, const void *v, void *out, float *g,
+                            int BH, int N, int D, int p, int causal, hipStream_t st)
+{
+    return FM_DISPATCH_D_P(generic::fwd_dispatch, D, p, q, k, v, out, g, BH, N, causal, st);
+}
+
+template <typename T>
+static hipError_t gen_bwd_t(const void *q, const void *k, const void *v, const void *o,
+                            const void *dout, const float *g, void *dq, void *dk, void *dv,
+                            int BH, int N, int D, int p, int causal, float *ws, hipStream_t st)
+{
+    return FM_DISPATCH_D_P(generic::bwd_dispatch, D, p, q, k, v, o, dout, g, dq, dk, dv, BH, N,
+                           causal, ws, st);
+}
+
+hipError_t generic_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
+                       int N, int D, int p, int causal, int is_bf16, hipStream_t st)
+{
+    if (is_bf16) return gen_fwd_t<bf16_t>(q, k, v, out, g, BH, N, D, p, causal, st);
+    return gen_fwd_t<float>(q, k, v, out, g, BH, N, D, p, causal, st);
+}
+
+hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st)
+{
+    if (is_bf16)
+        return gen_bwd_t<bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, p, causal,
+                                 (float *)ws, st);
+    return gen_bwd_t<float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, p, causal, (float *)ws,
+                            st);
+}
+
+}  // namespace fm

@@ -1,0 +1,17 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace fm {
+
+// Generic float32-VALU path: every (D, p, causal, dtype).
+hipError_t generic_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
+                       int N, int D, int p, int causal, int is_bf16, hipStream_t st);
+hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st);
+size_t generic_bwd_workspace(int B, int H, int N, int D);
+
+}  // namespace fm

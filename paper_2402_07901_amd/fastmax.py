@@ -1,0 +1,150 @@
+"""ctypes binding of the Fastmax C ABI (include/fastmax.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+library.  Tensors are PyTorch device tensors (they supply memory and the
+stream); the library must be built (``python -m paper_2402_07901_amd.build``)
+and fails loudly when it is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfastmax.so")
+
+F32 = 0
+BF16 = 1
+
+OK = 0
+EINVAL = -1
+EUNSUPPORTED = -2
+ENULL = -3
+EALIGN = -4
+EWORKSPACE = -5
+EHIP = -6
+
+_lib = None
+
+
+class FastmaxError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {strerror(code)} (code {code})")
+        self.code = code
+
+
+def lib():
+    """The loaded libfastmax.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} not found: build it with `python -m paper_2402_07901_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        L.fastmax_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
+        L.fastmax_workspace_bytes.restype = sz
+        L.fastmax_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp, sz, vp]
+        L.fastmax_fwd.restype = i
+        L.fastmax_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i,
+                                  vp, sz, vp]
+        L.fastmax_bwd.restype = i
+        L.fastmax_strerror.argtypes = [i]
+        L.fastmax_strerror.restype = ctypes.c_char_p
+        L.fastmax_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return lib().fastmax_strerror(int(code)).decode()
+
+
+def version() -> str:
+    return lib().fastmax_version().decode()
+
+
+def workspace_bytes(B, H, N, D, p, causal, dt, backward=False) -> int:
+    return int(lib().fastmax_workspace_bytes(B, H, N, D, p, int(causal), dt, int(backward)))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr()) if hasattr(t, "data_ptr") else ctypes.c_void_p(t)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else stream)
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_bytes, stream):
+    """Direct call of fastmax_fwd with raw pointers/ints; returns the code."""
+    return lib().fastmax_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(g), B, H, N, D, p,
+                             int(causal), dt, _ptr(workspace), ws_bytes, _stream(stream))
+
+
+def fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt, workspace,
+                    ws_bytes, stream):
+    return lib().fastmax_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(g), _ptr(dq),
+                             _ptr(dk), _ptr(dv), B, H, N, D, p, int(causal), dt, _ptr(workspace),
+                             ws_bytes, _stream(stream))
+
+
+def _alloc_ws(nbytes, device):
+    import torch
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def fastmax_fwd(q, k, v, p=2, causal=False, out=None, g=None, want_g=True, workspace=None,
+                stream=None):
+    """O = Fastmax(q, k, v) for [B, H, N, D] device tensors; returns (O, G)."""
+    import torch
+    B, H, N, D = q.shape
+    dt = _dtype_code(q)
+    if out is None:
+        out = torch.empty_like(q)
+    if g is None and want_g:
+        g = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    need = workspace_bytes(B, H, N, D, p, causal, dt, False)
+    if workspace is None:
+        workspace = _alloc_ws(need, q.device)
+    ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_n, stream)
+    if rc != OK:
+        raise FastmaxError(rc, "fastmax_fwd")
+    return out, g
+
+
+def fastmax_bwd(q, k, v, out, dout, g, p=2, causal=False, dq=None, dk=None, dv=None,
+                workspace=None, stream=None):
+    """Gradients (dq, dk, dv) of sum(dout * O)."""
+    import torch
+    B, H, N, D = q.shape
+    dt = _dtype_code(q)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    need = workspace_bytes(B, H, N, D, p, causal, dt, True)
+    if workspace is None:
+        workspace = _alloc_ws(need, q.device)
+    ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt, workspace,
+                         ws_n, stream)
+    if rc != OK:
+        raise FastmaxError(rc, "fastmax_bwd")
+    return dq, dk, dv

@@ -1,0 +1,128 @@
+"""Host-only tests of the C ABI (no GPU needed).
+
+Every call here carries at least one invalid argument, so the library must
+reject it during host validation, before any HIP call; the fake device
+pointers are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2402_07901_amd import fastmax as fm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fastmax.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(fm.LIB_PATH),
+                                reason="libfastmax.so not built")
+
+A = 0x100000  # 16-byte aligned fake pointer (never dereferenced)
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fastmax_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert {"fastmax_fwd", "fastmax_bwd", "fastmax_workspace_bytes",
+            "fastmax_strerror", "fastmax_version"} <= set(names)
+    L = ctypes.CDLL(fm.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_strerror_and_version():
+    for code in (fm.OK, fm.EINVAL, fm.EUNSUPPORTED, fm.ENULL, fm.EALIGN, fm.EWORKSPACE,
+                 fm.EHIP, 12345):
+        s = fm.strerror(code)
+        assert isinstance(s, str) and s
+    assert re.match(r"^\d+\.\d+\.\d+$", fm.version())
+
+
+def fwd(q=A, k=A, v=A, out=A, g=None, B=1, H=1, N=8, D=64, p=2, causal=1, dt=fm.BF16,
+        ws=None, wsb=0):
+    return fm.lib().fastmax_fwd(ctypes.c_void_p(q), ctypes.c_void_p(k), ctypes.c_void_p(v),
+                                ctypes.c_void_p(out), ctypes.c_void_p(g) if g else None, B, H,
+                                N, D, p, causal, dt, ctypes.c_void_p(ws) if ws else None, wsb,
+                                None)
+
+
+def bwd(ptrs=None, B=1, H=1, N=8, D=64, p=2, causal=1, dt=fm.BF16, ws=None, wsb=0):
+    ptrs = ptrs or [A] * 9
+    cp = [ctypes.c_void_p(x) if x else None for x in ptrs]
+    return fm.lib().fastmax_bwd(*cp, B, H, N, D, p, causal, dt,
+                                ctypes.c_void_p(ws) if ws else None, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), fm.EINVAL), (dict(H=0), fm.EINVAL), (dict(N=0), fm.EINVAL),
+    (dict(N=-5), fm.EINVAL), (dict(p=0), fm.EINVAL), (dict(p=3), fm.EINVAL),
+    (dict(causal=2), fm.EINVAL), (dict(dt=7), fm.EINVAL),
+    (dict(D=48), fm.EUNSUPPORTED), (dict(D=128), fm.EUNSUPPORTED), (dict(D=8), fm.EUNSUPPORTED),
+    (dict(B=1 << 20, H=1 << 20, N=1 << 20), fm.EINVAL),
+])
+def test_fwd_rejects_bad_shape_args(kw, code):
+    # also give a NULL q so that nothing could ever launch
+    assert fwd(q=0, **kw) in (code, fm.ENULL)
+    assert fwd(q=0, **kw) == code
+
+
+@pytest.mark.parametrize("which", ["q", "k", "v", "out"])
+def test_fwd_null(which):
+    assert fwd(**{which: 0}) == fm.ENULL
+
+
+@pytest.mark.parametrize("which", ["q", "k", "v", "out", "g"])
+def test_fwd_misaligned(which):
+    kw = {which: A + 4}
+    kw.setdefault("q", A)
+    assert fwd(**kw) == fm.EALIGN
+
+
+def test_bwd_null_and_align():
+    for i in range(9):
+        ptrs = [A] * 9
+        ptrs[i] = 0
+        assert bwd(ptrs) == fm.ENULL
+        ptrs = [A] * 9
+        ptrs[i] = A + 8
+        assert bwd(ptrs) == fm.EALIGN
+
+
+def test_bwd_workspace_checks():
+    need = fm.workspace_bytes(1, 1, 8, 64, 2, True, fm.BF16, True)
+    assert need > 0
+    assert bwd(ws=None, wsb=0) == fm.EWORKSPACE
+    assert bwd(ws=A, wsb=need - 1) == fm.EWORKSPACE
+    ptrs = [A] * 9
+    assert bwd(ptrs, ws=A + 4, wsb=need, p=5) == fm.EINVAL
+
+
+def test_bwd_rejects_bad_args():
+    assert bwd(B=0) == fm.EINVAL
+    assert bwd(D=100) == fm.EUNSUPPORTED
+    assert bwd(p=3) == fm.EINVAL
+
+
+def test_workspace_bytes():
+    for D in (16, 32, 64):
+        for p in (1, 2):
+            for causal in (0, 1):
+                for dt in (fm.F32, fm.BF16):
+                    nf = fm.workspace_bytes(2, 3, 100, D, p, causal, dt, False)
+                    nb = fm.workspace_bytes(2, 3, 100, D, p, causal, dt, True)
+                    assert nf >= 0 and nb >= 4 * 2 * 3 * 100 * (3 * D + 1)
+    assert fm.workspace_bytes(0, 1, 1, 64, 2, 1, fm.BF16, True) == 0
+    assert fm.workspace_bytes(1, 1, 1, 65, 2, 1, fm.BF16, True) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(fm, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(fm, "_lib", None)
+    with pytest.raises(RuntimeError, match="not found"):
+        fm.lib()

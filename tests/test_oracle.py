@@ -327,8 +327,8 @@ MUTATIONS = {
     "drop_factorial": ("term *= s / (double)l;", "term *= s;"),
     "sample_std": ("var /= (double)D;                 /* population variance */",
                    "var /= (double)(D - 1);"),
-    "exclusive_causal": ("long nend = causal ? i + 1 : N;\n    double g = 0.0;",
-                         "long nend = causal ? i : N;\n    double g = 0.0;"),
+    "exclusive_causal": ("long nend = causal ? i + 1 : N;\n    double g = 0.0, gabs",
+                         "long nend = causal ? i : N;\n    double g = 0.0, gabs"),
     "fact_drop_half_g": ("g += 0.5 * quad;", "g += quad;"),
     "fact_transposed_x2": ("M->x2[j * D + m] += k[m] * vj;", "M->x2[m * D + j] += k[m] * vj;"),
     "fact_wrong_query_index": ("for (long l = 0; l < D; ++l) inner += q[l] * x3jm[l];",
@@ -368,3 +368,18 @@ def test_planted_mistake_is_caught(mutation, tmp_path):
     finally:
         oracle._lib = saved
     assert caught, f"planted mistake {mutation} went unnoticed"
+
+
+def test_bwd_o_used_matches_exact_when_given_exact():
+    q, k, v = _rand(1, 2, 20, 8, 22)
+    do = np.random.default_rng(8).standard_normal(q.shape)
+    for p in (1, 2):
+        o, _ = oracle.fwd_brute(q, k, v, p, True)
+        a = oracle.bwd_brute(q, k, v, do, p, True)
+        b = oracle.bwd_brute(q, k, v, do, p, True, o_used=o)
+        for x, y in zip(a, b):
+            np.testing.assert_allclose(x, y, rtol=1e-12, atol=1e-12)
+        # perturbing O moves only the c_i = dO.O/G terms: dv is unchanged
+        c = oracle.bwd_brute(q, k, v, do, p, True, o_used=o * (1 + 1e-3))
+        np.testing.assert_array_equal(c[2], a[2])
+        assert np.abs(c[0] - a[0]).max() > 0
