@@ -56,8 +56,11 @@ int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g
     size_t need = fwd_ws(B, H, N, D, p, causal, dt);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
-    hipError_t e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal,
-                                   dt == FASTMAX_BF16, stream);
+    hipError_t e;
+    if (D == 64 && p == 2 && causal && dt == FASTMAX_BF16)
+        e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, stream);
+    else
+        e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 

@@ -14,4 +14,9 @@ hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *
                        int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st);
 size_t generic_bwd_workspace(int B, int H, int N, int D);
 
+// MFMA causal scan: D = 64, p = 2, bf16 I/O.
+hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
+                           int BH, int N, hipStream_t st);
+size_t mfma_causal_smem_bytes();
+
 }  // namespace fm
