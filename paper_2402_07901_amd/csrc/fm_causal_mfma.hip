@@ -1,8 +1,8 @@
 // Causal Fastmax forward on CDNA4 MFMA, head dimension 64, p = 2, bf16 I/O.
 //
 // Chunked causal scan (Sec. 2.4, causal moments "xcausal"/"ycausal" carried
-// across chunks of C tokens instead of per row).  One workgroup owns one
-// (batch, head, slice of 16 value columns); its four waves hold the moment
+// across chunks of 128 tokens instead of per row).  One workgroup owns one
+// (batch, head, slice of 16 value columns); its eight waves hold the moment
 // state S[f][j] = sum_n phi_f(k^_n) v_nj of the slice as fp32 MFMA
 // accumulators for the whole sequence, so the state never touches HBM.
 //
@@ -10,10 +10,11 @@
 // (m, u): rows l = 16u..16u+15 for one m, with u >= m/16 (symmetric tiles:
 // 160 of them) plus 4 linear tiles (k_l) -- 2624 feature rows instead of the
 // 4160 of the full square, 2080 + 65 being the minimum.  A "diagonal" tile
-// (u == m/16) carries both (m,l) and (l,m) and is accumulated with weight 1/2;
-// the others with weight 1, so psi(q).phi(k) = 1 + s + s^2/2 exactly
-// (constant term separate).  Wave w owns the tiles of m = w (mod 4) and the
-// linear tile u = w: 41 tiles, 164 accumulator registers.
+// (u == m/16) carries both (m,l) and (l,m) and enters the query contraction
+// with weight 1/2 (applied when the state is converted to fp16), the others
+// with weight 1, so psi(q).phi(k) = 1 + s + s^2/2 exactly (constant term
+// separate).  Wave w owns the tiles of m = w (mod 8) and, for w < 4, the
+// linear tile u = w: 21 tiles, 84 accumulator registers.
 //
 // Per chunk:
 //  (i)  query contraction F^T += S^T Psi(Q)^T.  The accumulator layout of a
@@ -21,13 +22,13 @@
 //       the A operand of the next MFMA by pairing two tiles per 32-wide K
 //       step (K index 8h+r <-> tile a row 4h+r, 8h+4+r <-> tile b row 4h+r);
 //       the Psi operand is generated in registers with packed fp16 multiplies
-//       in the same K order.  Each wave contracts its own tiles for all 64
+//       in the same K order.  Each wave contracts its own tiles for all 128
 //       tokens; partial F^T go through LDS.
 //  (ii) in-chunk block tril(f(Q K^T)) V on MFMA, and the denominator
 //       G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sums, with Y3 = sum k k^T
 //       kept as 10 symmetric fp32 accumulator tiles.
-//  (iii) state update S += Phi(K)^T V per m: A = K^T tiles (1/2 K^T for the
-//       diagonal tile), B = diag(k_m) V generated with packed multiplies.
+//  (iii) state update S += Phi(K)^T V per m: A = K^T tiles, B = diag(k_m) V
+//       generated with packed multiplies.
 //
 // Operands are fp16 (q^, k^ are standardised so |x| <= 8).  v is scaled by a
 // power of two 2^-e chosen per workgroup from max|v| so that every state
@@ -49,14 +50,13 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int D = 64;
-constexpr int C = 64;         // tokens per chunk
-constexpr int NW = 4;         // waves per workgroup
+constexpr int C = 128;        // tokens per chunk
+constexpr int NRT = C / 16;   // 16-token row tiles per chunk
+constexpr int NKS2 = C / 32;  // 32-token K steps of the state update
+constexpr int NW = 8;         // waves per workgroup (2 per SIMD)
 constexpr int NTH = NW * 64;
 constexpr int SL = 16;        // value columns per workgroup
 constexpr int NSL = D / SL;
-constexpr int NT = 41;        // state tiles per wave
-constexpr int NKS = (NT + 1) / 2;  // K steps of the query contraction
-constexpr int RS = D + 8;     // padded LDS row stride (halves)
 
 template <int I, int N, typename F>
 __device__ __forceinline__ void static_for(F &&f)
@@ -67,57 +67,63 @@ __device__ __forceinline__ void static_for(F &&f)
     }
 }
 
-struct Tile {
-    int kind;  // 0 linear, 1 quadratic, -1 padding
-    int m;     // channel m (quadratic) or -1
-    int idx;   // position of m in the wave's m list
-    int u;     // l tile
-};
-
-// t-th tile of wave W: t = 0 is the linear tile u = W; then for the wave's
-// channels m = W, W+4, ..., W+60 the tiles u = m/16 .. 3.
-__host__ __device__ constexpr Tile tile_of(int W, int t)
-{
-    if (t == 0) return Tile{0, -1, -1, W};
-    int r = t - 1;
-    for (int idx = 0; idx < 16; ++idx) {
-        int m = W + 4 * idx;
-        int n = 4 - m / 16;
-        if (r < n) return Tile{1, m, idx, m / 16 + r};
-        r -= n;
-    }
-    return Tile{-1, -1, -1, -1};
-}
-
-// first tile index of channel list position idx for wave W
-__host__ __device__ constexpr int first_tile(int W, int idx)
+// Tiles of a wave w: tile 0 is the linear tile u = w (waves 0..3 only; it
+// stays zero in waves 4..7), then for the wave's channels m = w + 8*idx
+// (idx = 0..7) the tiles u = idx/2 .. 3 (m/16 == idx/2 for every w < 8), so
+// all waves share one tile pattern: 1 + 4+4+3+3+2+2+1+1 = 21 tiles.
+constexpr int NT = 21;
+constexpr int NKS = (NT + 1) / 2;   // K steps of the query contraction
+__host__ __device__ constexpr int u0_of(int idx) { return idx / 2; }
+__host__ __device__ constexpr int first_tile(int idx)
 {
     int t = 1;
-    for (int i = 0; i < idx; ++i) t += 4 - (W + 4 * i) / 16;
+    for (int i = 0; i < idx; ++i) t += 4 - u0_of(i);
     return t;
 }
+struct Tile {
+    int kind;  // 0 linear, 1 quadratic, -1 padding
+    int idx;   // channel m = w + 8*idx
+    int u;     // l tile
+};
+__host__ __device__ constexpr Tile tile_of(int t)
+{
+    if (t == 0) return Tile{0, -1, -1};
+    for (int idx = 0; idx < 8; ++idx)
+        if (t < first_tile(idx) + 4 - u0_of(idx)) return Tile{1, idx, u0_of(idx) + t - first_tile(idx)};
+    return Tile{-1, -1, -1};
+}
+__host__ __device__ constexpr bool is_diag(int t)
+{
+    return t < NT && tile_of(t).kind == 1 && tile_of(t).u == u0_of(tile_of(t).idx);
+}
 
-// Y3 tiles (u <= u2) owned by wave W
-__host__ __device__ constexpr int y3_count(int W) { return W < 2 ? 3 : 2; }
-__host__ __device__ constexpr int y3_u(int W, int k)
+// Y3 tiles (u <= u2), 10 of them: waves 0 and 1 own two, the others one.
+__device__ __forceinline__ int y3_count(int w) { return w < 2 ? 2 : 1; }
+__device__ __forceinline__ void y3_tile(int w, int k, int &u, int &u2)
 {
-    constexpr int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
-    return us[(W < 2 ? 3 * W : 6 + 2 * (W - 2)) + k];
+    const int i = w < 2 ? 2 * w + k : 2 + w;
+    const int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
+    const int vs[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
+    u = us[i];
+    u2 = vs[i];
 }
-__host__ __device__ constexpr int y3_u2(int W, int k)
-{
-    constexpr int us[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
-    return us[(W < 2 ? 3 * W : 6 + 2 * (W - 2)) + k];
-}
+
+// LDS rows are padded by 16 bytes: 16 lanes reading the same column of 16
+// consecutive rows then fall on 16 distinct 4-bank groups, and offsets stay
+// affine so constant parts fold into the instructions.  Offsets in halves.
+constexpr int RS64 = 64 + 8;     // rows of 64 halves
+constexpr int RS128 = 128 + 8;   // rows of 128 halves
+__device__ __forceinline__ int sw64(int row, int col) { return row * RS64 + col; }
+__device__ __forceinline__ int sw128(int row, int col) { return row * RS128 + col; }
 
 struct Smem {
-    _Float16 qrow[C * RS];    // q^ row-major
-    _Float16 qperm[C * RS];   // q^ with channel m at (m % 4) * 16 + m / 4
-    _Float16 krow[C * RS];    // k^ row-major
-    _Float16 kT[D * RS];      // k^ transposed [m][token]
-    _Float16 vT[SL * RS];     // scaled v transposed [j][token]
-    _Float16 y3h[D * RS];     // scaled Y3 (prefix before the chunk)
-    float fpart[NW * C * SL]; // partial F^T per wave: [wave][token][j]
+    _Float16 qrow[C * RS64];    // q^ [token][m]
+    _Float16 qperm[C * RS64];   // q^ [token][(m % 8) * 8 + m / 8]
+    _Float16 krow[C * RS64];    // k^ [token][m]
+    _Float16 kT[D * RS128];     // k^ [m][token]
+    _Float16 vT[SL * RS128];    // scaled v [j][token]
+    _Float16 y3h[D * RS64];     // scaled Y3 (prefix before the chunk)
+    float fpart[NW * C * SL];   // partial F^T: [wave][column quad][token][4]
     float y2[D];              // sum k^ before the chunk
     float y2c[D];             // this chunk's sum k^
     float x1[SL];             // sum of scaled v before the chunk
@@ -173,56 +179,118 @@ __device__ __forceinline__ int pow2_exponent(float bound)
     return e < -100 ? -100 : (e > 100 ? 100 : e);
 }
 
-template <int W>
-__device__ __forceinline__ void run_wave(Smem &sm, const bf16_t *__restrict__ q,
+// Sum over an aligned octet of lanes with DPP: swap neighbours, swap pairs,
+// then mirror the two quads of each half row.
+__device__ __forceinline__ float octet_sum(float x)
+{
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, true));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, true));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, true));
+    return x;
+}
+
+// Standardises the 8 channels this lane holds of one token (the token's 64
+// channels are spread over the 8 lanes of an aligned octet) and returns them
+// as fp16.  Population variance, no epsilon; invalid rows become zero.
+__device__ __forceinline__ h8 standardise8(const float *xin, bool valid)
+{
+    float x[8];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += xin[i];
+    const float mu = octet_sum(s) * (1.0f / D);
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        x[i] = xin[i] - mu;
+        v = fmaf(x[i], x[i], v);
+    }
+    const float r = valid ? __builtin_amdgcn_rsqf(octet_sum(v) * (1.0f / D)) : 0.0f;
+    h8 o;
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+        const h2 pr = {(_Float16)(x[i] * r), (_Float16)(x[i + 1] * r)};
+        o[i] = pr[0];
+        o[i + 1] = pr[1];
+    }
+    return o;
+}
+
+// sum of 8 halves in fp32 (dot products with ones)
+__device__ __forceinline__ float hsum8(h8 a)
+{
+    const h2 one = {(_Float16)1.0f, (_Float16)1.0f};
+    float s = 0.f;
+    s = __builtin_amdgcn_fdot2(h2{a[0], a[1]}, one, s, false);
+    s = __builtin_amdgcn_fdot2(h2{a[2], a[3]}, one, s, false);
+    s = __builtin_amdgcn_fdot2(h2{a[4], a[5]}, one, s, false);
+    s = __builtin_amdgcn_fdot2(h2{a[6], a[7]}, one, s, false);
+    return s;
+}
+
+__device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                                          const bf16_t *__restrict__ k,
                                          const bf16_t *__restrict__ v, bf16_t *__restrict__ out,
                                          float *__restrict__ g, int N, int sl, int vexp)
 {
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int r16 = lane & 15;
-    const int h = lane >> 4;
+    const int w = threadIdx.x >> 6;    // wave
+    const bool has_lin = w < 4;
 
     f4 acc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-    constexpr int NY = y3_count(W);
-    f4 y3acc[NY];
-#pragma unroll
-    for (int t = 0; t < NY; ++t) y3acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+    f4 y3acc[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
+    int y3u[2], y3u2[2];
+    y3_tile(w, 0, y3u[0], y3u2[0]);
+    y3_tile(w, w < 2 ? 1 : 0, y3u[1], y3u2[1]);
+    const int ny3 = y3_count(w);
 
     const float vscale = ldexpf(1.0f, -vexp);   // v -> v * 2^-e
     const float oscale = ldexpf(1.0f, vexp);
     int gexp = 0;                                // Y3 in LDS is Y3 * 2^-gexp
     const int nch = (N + C - 1) / C;
 
-    // loader roles: row r, quarter qq (16 channels) of q and k
-    const int lr = tid >> 2, lq = tid & 3;
-    const int vr = tid >> 1, vh = tid & 1;       // v loader (tid < 128)
+    // Lane-derived LDS offsets are recomputed in every chunk from an opaque
+    // copy of the thread id: hoisted out of the loop they would stay live for
+    // the whole scan and spill.
+    int tid = threadIdx.x;
+    int lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    // loader roles: tokens 2*tg, 2*tg+1, channels 8*cg .. 8*cg+7
+    int tg = tid >> 3, cg = tid & 7;
+    int vt = tid >> 1, vh = tid & 1;             // v (tid < 256): token vt, columns 8*vh..
+    auto refresh_ids = [&]() {
+        asm volatile("" : "+v"(tid));
+        lane = tid & 63;
+        r16 = lane & 15;
+        h = lane >> 4;
+        tg = tid >> 3;
+        cg = tid & 7;
+        vt = tid >> 1;
+        vh = tid & 1;
+    };
 
-    uint4 pq0, pq1, pk0, pk1, pv;
+    uint4 pq[2], pk[2], pv;
     auto prefetch = [&](int c) {
-        const int n = c * C + lr;
         const uint4 z = {0u, 0u, 0u, 0u};
-        pq0 = pq1 = pk0 = pk1 = pv = z;
-        if (n < N) {
-            const uint4 *qp = (const uint4 *)(q + (size_t)n * D + 16 * lq);
-            const uint4 *kp = (const uint4 *)(k + (size_t)n * D + 16 * lq);
-            pq0 = qp[0];
-            pq1 = qp[1];
-            pk0 = kp[0];
-            pk1 = kp[1];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = c * C + 2 * tg + j;
+            pq[j] = pk[j] = z;
+            if (n < N) {
+                pq[j] = *(const uint4 *)(q + (size_t)n * D + 8 * cg);
+                pk[j] = *(const uint4 *)(k + (size_t)n * D + 8 * cg);
+            }
         }
-        const int nv = c * C + vr;
-        if (tid < 128 && nv < N)
-            pv = *(const uint4 *)(v + (size_t)nv * D + SL * sl + 8 * vh);
+        const int nv = c * C + vt;
+        pv = z;
+        if (tid < 2 * C && nv < N) pv = *(const uint4 *)(v + (size_t)nv * D + SL * sl + 8 * vh);
     };
     prefetch(0);
 
     for (int c = 0; c < nch; ++c) {
         const int n0 = c * C;
         const int nvalid = min(C, N - n0);
+        refresh_ids();
         // ---- fold the previous chunk's sums into the prefixes ----------------
         if (c > 0) {
             if (tid < D) sm.y2[tid] += sm.y2c[tid];
@@ -230,97 +298,75 @@ __device__ __forceinline__ void run_wave(Smem &sm, const bf16_t *__restrict__ q,
         }
         // ---- (L) standardise q, k (Sec. 2.2, Eqs. 6-7) and stage the chunk ----
         {
-            const bool valid = (n0 + lr) < N;
-            float xq[16], xk[16];
-            bf16x8_to_f32(pq0, xq);
-            bf16x8_to_f32(pq1, xq + 8);
-            bf16x8_to_f32(pk0, xk);
-            bf16x8_to_f32(pk1, xk + 8);
-            float sq = 0.f, sk = 0.f;
+            _Float16 kh[2][8];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { sq += xq[i]; sk += xk[i]; }
-            sq += __shfl_xor(sq, 1);
-            sq += __shfl_xor(sq, 2);
-            sk += __shfl_xor(sk, 1);
-            sk += __shfl_xor(sk, 2);
-            const float mq = sq * (1.0f / D), mk = sk * (1.0f / D);
-            float vq = 0.f, vk = 0.f;
+            for (int j = 0; j < 2; ++j) {
+                const int row = 2 * tg + j;
+                const bool valid = (n0 + row) < N;
+                float xq[8], xk[8];
+                bf16x8_to_f32(pq[j], xq);
+                bf16x8_to_f32(pk[j], xk);
+                const h8 hq = standardise8(xq, valid);
+                const h8 hk = standardise8(xk, valid);
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                xq[i] -= mq;
-                xk[i] -= mk;
-                vq = fmaf(xq[i], xq[i], vq);
-                vk = fmaf(xk[i], xk[i], vk);
+                for (int i = 0; i < 8; ++i) kh[j][i] = hk[i];
+                *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
+                *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk;
+                // channel m = 8*cg + i sits at (m % 8) * 8 + m / 8 = 8*i + cg
+#pragma unroll
+                for (int i = 0; i < 8; ++i) sm.qperm[sw64(row, 8 * i + cg)] = hq[i];
             }
-            vq += __shfl_xor(vq, 1);
-            vq += __shfl_xor(vq, 2);
-            vk += __shfl_xor(vk, 1);
-            vk += __shfl_xor(vk, 2);
-            const float rq = valid ? rsqrtf(vq * (1.0f / D)) : 0.0f;
-            const float rk = valid ? rsqrtf(vk * (1.0f / D)) : 0.0f;
-            _Float16 hq[16], hk[16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                hq[i] = (_Float16)(xq[i] * rq);
-                hk[i] = (_Float16)(xk[i] * rk);
-            }
-            _Float16 *qr = sm.qrow + lr * RS + 16 * lq;
-            _Float16 *kr = sm.krow + lr * RS + 16 * lq;
-            *(h8 *)qr = h8{hq[0], hq[1], hq[2], hq[3], hq[4], hq[5], hq[6], hq[7]};
-            *(h8 *)(qr + 8) = h8{hq[8], hq[9], hq[10], hq[11], hq[12], hq[13], hq[14], hq[15]};
-            *(h8 *)kr = h8{hk[0], hk[1], hk[2], hk[3], hk[4], hk[5], hk[6], hk[7]};
-            *(h8 *)(kr + 8) = h8{hk[8], hk[9], hk[10], hk[11], hk[12], hk[13], hk[14], hk[15]};
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-                *(h4 *)(sm.qperm + lr * RS + a * 16 + 4 * lq) =
-                    h4{hq[a], hq[a + 4], hq[a + 8], hq[a + 12]};
-#pragma unroll
-            for (int i = 0; i < 16; ++i) sm.kT[(16 * lq + i) * RS + lr] = hk[i];
-            if (tid < 128) {
+            for (int i = 0; i < 8; ++i)
+                *(h2 *)(sm.kT + sw128(8 * cg + i, 2 * tg)) = h2{kh[0][i], kh[1][i]};
+            if (tid < 2 * C) {
                 float xv[8];
                 bf16x8_to_f32(pv, xv);
 #pragma unroll
                 for (int i = 0; i < 8; ++i)
-                    sm.vT[(8 * vh + i) * RS + vr] = (_Float16)(xv[i] * vscale);
+                    sm.vT[sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vscale);
             }
         }
         __syncthreads();
-        if (c + 1 < nch) prefetch(c + 1);
 
         // ---- (I) query contraction, in-chunk block and denominators ---------
+        __builtin_amdgcn_sched_barrier(0);
+        refresh_ids();
         {
-            // state -> fp16 A operands, two tiles per K step
+            // state -> fp16 A operands, two tiles per K step; diagonal tiles
+            // carry the 1/2 of f_2's quadratic term
             h8 Ast[NKS];
             static_for<0, NKS>([&](auto pi) {
                 constexpr int p = decltype(pi)::value;
-                const h4 a = cvt4(acc[2 * p]);
-                const h4 b = (2 * p + 1 < NT) ? cvt4(acc[(2 * p + 1) < NT ? 2 * p + 1 : 0])
-                                              : h4{0, 0, 0, 0};
+                constexpr int ta = 2 * p, tb = 2 * p + 1;
+                h4 a = cvt4(acc[ta]);
+                if constexpr (is_diag(ta)) a = scale4(a, (_Float16)0.5f);
+                h4 b = h4{0, 0, 0, 0};
+                if constexpr (tb < NT) {
+                    b = cvt4(acc[tb < NT ? tb : 0]);
+                    if constexpr (is_diag(tb)) b = scale4(b, (_Float16)0.5f);
+                }
                 Ast[p] = cat(a, b);
             });
-            // Q^T fragments of this wave's row tile (for the in-chunk block and G)
-            const int tokW = 16 * W + r16;
-            const h8 QB0 = ld8(sm.qrow + tokW * RS + 8 * h);
-            const h8 QB1 = ld8(sm.qrow + tokW * RS + 32 + 8 * h);
 
-#pragma unroll
-            for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll 1
+            for (int rt = 0; rt < NRT; ++rt) {
                 const int tok = 16 * rt + r16;
                 h4 myl[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) myl[u] = ld4(sm.qrow + tok * RS + 16 * u + 4 * h);
-                const h8 qa = ld8(sm.qperm + tok * RS + 16 * W);
-                const h8 qb = ld8(sm.qperm + tok * RS + 16 * W + 8);
-                const _Float16 qm[16] = {qa[0], qa[1], qa[2], qa[3], qa[4], qa[5], qa[6], qa[7],
-                                         qb[0], qb[1], qb[2], qb[3], qb[4], qb[5], qb[6], qb[7]};
+                for (int u = 0; u < 4; ++u) myl[u] = ld4(sm.qrow + sw64(tok, 16 * u + 4 * h));
+                // linear features l = 16w + 4h + r (zero state in waves 4..7)
+                const h4 mylin = ld4(sm.qrow + sw64(tok, 16 * (w & 3) + 4 * h));
+                // the wave's channels m = w + 8*idx sit at qperm[8w + idx]
+                const h8 qm = ld8(sm.qperm + sw64(tok, 8 * w));
                 f4 F0 = {0.f, 0.f, 0.f, 0.f}, F1 = {0.f, 0.f, 0.f, 0.f};
                 auto gen = [&](auto ti) -> h4 {
                     constexpr int t = decltype(ti)::value;
-                    constexpr Tile T = tile_of(W, t < NT ? t : 0);
+                    constexpr Tile T = tile_of(t < NT ? t : 0);
                     if constexpr (t >= NT) {
                         return h4{0, 0, 0, 0};
                     } else if constexpr (T.kind == 0) {
-                        return myl[T.u];
+                        return mylin;
                     } else {
                         return scale4(myl[T.u], qm[T.idx]);
                     }
@@ -332,163 +378,154 @@ __device__ __forceinline__ void run_wave(Smem &sm, const bf16_t *__restrict__ q,
                     if constexpr (p & 1) F1 = mfma(Ast[p], B, F1);
                     else F0 = mfma(Ast[p], B, F0);
                 });
-                if (rt == W) {
-                    // in-chunk tril block: S^T tiles (rows t, cols i), i in this row tile
+                if (rt == w) {
+                    const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
+                    const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
+                    // in-chunk tril block, two S^T tiles (rows t, cols i = tok) at a
+                    // time, each pair feeding one MFMA of F^T += V^T W^T
                     float gi = 0.f;
-                    h4 wh[4];
-#pragma unroll
-                    for (int tt = 0; tt <= W; ++tt) {
+                    auto wtile = [&](int tt) -> h4 {
                         f4 S = {0.f, 0.f, 0.f, 0.f};
-                        S = mfma(ld8(sm.krow + (16 * tt + r16) * RS + 8 * h), QB0, S);
-                        S = mfma(ld8(sm.krow + (16 * tt + r16) * RS + 32 + 8 * h), QB1, S);
-                        f4 w;
+                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 8 * h)), QB0, S);
+                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 32 + 8 * h)), QB1, S);
+                        f4 wv;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            const float s = S[i];
-                            float x = fmaf(0.5f * s, s, 1.0f + s);
-                            if (tt == W && (4 * h + i) > r16) x = 0.0f;
-                            w[i] = x;
-                            gi += x;
+                            const float x = S[i];
+                            float y = fmaf(0.5f * x, x, 1.0f + x);
+                            if (tt == rt && (4 * h + i) > r16) y = 0.0f;
+                            wv[i] = y;
+                            gi += y;
                         }
-                        wh[tt] = cvt4(w);
-                    }
-#pragma unroll
-                    for (int pa = 0; pa <= W / 2; ++pa) {
-                        const int a = 2 * pa, b = 2 * pa + 1;
-                        const h4 va = ld4(sm.vT + r16 * RS + 16 * a + 4 * h);
-                        const h4 vb = (b <= W) ? ld4(sm.vT + r16 * RS + 16 * b + 4 * h)
-                                               : h4{0, 0, 0, 0};
-                        const h4 wb = (b <= W) ? wh[b < 4 ? b : 0] : h4{0, 0, 0, 0};
-                        F0 = mfma(cat(va, vb), cat(wh[a], wb), F0);
+                        return cvt4(wv);
+                    };
+                    for (int a = 0; a <= rt; a += 2) {
+                        const int b = a + 1;
+                        const h4 wa = wtile(a);
+                        const h4 va = ld4(sm.vT + sw128(r16, 16 * a + 4 * h));
+                        h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
+                        if (b <= rt) {
+                            wb = wtile(b);
+                            vb = ld4(sm.vT + sw128(r16, 16 * b + 4 * h));
+                        }
+                        F0 = mfma(cat(va, vb), cat(wa, wb), F0);
                     }
                     // G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sum
                     float gq = 0.f;
+                    const float ys = ldexpf(2.0f, -gexp);
 #pragma unroll
                     for (int cc = 0; cc < 4; ++cc) {
-                        const float ys = ldexpf(2.0f, -gexp);
                         f4 T;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[16 * cc + 4 * h + i];
-                        T = mfma(ld8(sm.y3h + (16 * cc + r16) * RS + 8 * h), QB0, T);
-                        T = mfma(ld8(sm.y3h + (16 * cc + r16) * RS + 32 + 8 * h), QB1, T);
+                        T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
+                        T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) gq = fmaf((float)myl[cc][i], T[i], gq);
                     }
                     float part = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gi);
                     part += __shfl_xor(part, 16);
                     part += __shfl_xor(part, 32);
-                    if (h == 0) sm.g[16 * W + r16] = (float)n0 + part;
+                    if (h == 0) sm.g[tok] = (float)n0 + part;
                 }
-                const f4 Fs = F0 + F1;
-                *(f4 *)(sm.fpart + (W * C + tok) * SL + 4 * h) = Fs;
+                *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
             }
-            // this chunk's sums of k^ (for y2) and of scaled v (for x1)
-            {
-                const int m = 16 * W + r16;
-                const h8 a = ld8(sm.kT + m * RS + 16 * h);
-                const h8 b = ld8(sm.kT + m * RS + 16 * h + 8);
+            // this chunk's sums of k^ (for y2, waves 0-3) and of scaled v (x1, wave 4)
+            if (w < 4) {
+                const int m = 16 * w + r16;
                 float s = 0.f;
 #pragma unroll
-                for (int i = 0; i < 8; ++i) s += (float)a[i] + (float)b[i];
+                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(sm.kT + sw128(m, 32 * h + 8 * cc)));
                 s += __shfl_xor(s, 16);
                 s += __shfl_xor(s, 32);
                 if (h == 0) sm.y2c[m] = s;
-                if (W == 0) {
-                    const h8 va = ld8(sm.vT + r16 * RS + 16 * h);
-                    const h8 vb = ld8(sm.vT + r16 * RS + 16 * h + 8);
-                    float sv = 0.f;
+            } else if (w == 4) {
+                float sv = 0.f;
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) sv += (float)va[i] + (float)vb[i];
-                    sv += __shfl_xor(sv, 16);
-                    sv += __shfl_xor(sv, 32);
-                    if (h == 0) sm.x1c[r16] = sv;
-                }
+                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(sm.vT + sw128(r16, 32 * h + 8 * cc)));
+                sv += __shfl_xor(sv, 16);
+                sv += __shfl_xor(sv, 32);
+                if (h == 0) sm.x1c[r16] = sv;
             }
         }
         __syncthreads();
 
         // ---- (R) combine partials, divide, store ------------------------------
         {
-            const int tok = tid >> 2, cq = tid & 3;
+            const int tok = tid & (C - 1), cq = tid >> 7;
             f4 F = *(const f4 *)(sm.x1 + 4 * cq);
 #pragma unroll
-            for (int w = 0; w < NW; ++w) F += *(const f4 *)(sm.fpart + (w * C + tok) * SL + 4 * cq);
+            for (int ww = 0; ww < NW; ++ww) F += *(const f4 *)(sm.fpart + ((ww * 4 + cq) * C + tok) * 4);
             const float Gi = sm.g[tok];
             if (n0 + tok < N) {
                 const float sc = oscale / Gi;
-                uint32_t lo = (uint32_t)f32_to_bf16(F[0] * sc) |
-                              ((uint32_t)f32_to_bf16(F[1] * sc) << 16);
-                uint32_t hi = (uint32_t)f32_to_bf16(F[2] * sc) |
-                              ((uint32_t)f32_to_bf16(F[3] * sc) << 16);
-                *(uint2 *)(out + (size_t)(n0 + tok) * D + SL * sl + 4 * cq) = uint2{lo, hi};
+                uint2 o;
+                o.x = (uint32_t)f32_to_bf16(F[0] * sc) | ((uint32_t)f32_to_bf16(F[1] * sc) << 16);
+                o.y = (uint32_t)f32_to_bf16(F[2] * sc) | ((uint32_t)f32_to_bf16(F[3] * sc) << 16);
+                *(uint2 *)(out + (size_t)(n0 + tok) * D + SL * sl + 4 * cq) = o;
                 if (g && sl == 0 && cq == 0) g[n0 + tok] = Gi;
             }
         }
 
         // ---- (U) state update S += Phi(K)^T V, Y3 += K^T K ---------------------
+        // (the next chunk's loads are issued here, after the fp16 state copy of
+        // phase I is dead, and complete behind the update's MFMAs)
+        __builtin_amdgcn_sched_barrier(0);
+        refresh_ids();
+        if (c + 1 < nch) prefetch(c + 1);
         {
-            h8 Ak[4][2], Akh[4][2];
+#pragma unroll 1
+            for (int s = 0; s < NKS2; ++s) {
+                h8 Ak[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int s = 0; s < 2; ++s) {
-                    Ak[u][s] = ld8(sm.kT + (16 * u + r16) * RS + 32 * s + 8 * h);
-                    Akh[u][s] = cat(scale4(h4{Ak[u][s][0], Ak[u][s][1], Ak[u][s][2], Ak[u][s][3]},
-                                           (_Float16)0.5f),
-                                    scale4(h4{Ak[u][s][4], Ak[u][s][5], Ak[u][s][6], Ak[u][s][7]},
-                                           (_Float16)0.5f));
-                }
-            h8 Vf[2];
-#pragma unroll
-            for (int s = 0; s < 2; ++s) Vf[s] = ld8(sm.vT + r16 * RS + 32 * s + 8 * h);
-            // linear tile
-#pragma unroll
-            for (int s = 0; s < 2; ++s) acc[0] = mfma(Ak[W][s], Vf[s], acc[0]);
-            // quadratic tiles
-            static_for<0, 16>([&](auto ii) {
-                constexpr int idx = decltype(ii)::value;
-                constexpr int m = W + 4 * idx;
-                constexpr int u0 = m / 16;
-                constexpr int t0 = first_tile(W, idx);
-#pragma unroll
-                for (int s = 0; s < 2; ++s) {
-                    const h8 km = ld8(sm.kT + m * RS + 32 * s + 8 * h);
-                    const h8 Wm = km * Vf[s];
+                for (int u = 0; u < 4; ++u) Ak[u] = ld8(sm.kT + sw128(16 * u + r16, 32 * s + 8 * h));
+                const h8 Vf = ld8(sm.vT + sw128(r16, 32 * s + 8 * h));
+                if (has_lin)   // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
+                    acc[0] = mfma(ld8(sm.kT + sw128(16 * w + r16, 32 * s + 8 * h)), Vf, acc[0]);
+                static_for<0, 8>([&](auto ii) {
+                    constexpr int idx = decltype(ii)::value;
+                    constexpr int u0 = u0_of(idx);
+                    constexpr int t0 = first_tile(idx);
+                    const int m = w + 8 * idx;
+                    const h8 km = ld8(sm.kT + sw128(m, 32 * s + 8 * h));
+                    const h8 Wm = km * Vf;
                     static_for<u0, 4>([&](auto ui) {
                         constexpr int u = decltype(ui)::value;
-                        constexpr int t = t0 + (u - u0);
-                        if constexpr (u == u0) acc[t] = mfma(Akh[u][s], Wm, acc[t]);
-                        else acc[t] = mfma(Ak[u][s], Wm, acc[t]);
+                        acc[t0 + (u - u0)] = mfma(Ak[u], Wm, acc[t0 + (u - u0)]);
                     });
-                }
-            });
-            // Y3 tiles
-            const int ntok = n0 + nvalid;
-            const int gnext = max(0, pow2_exponent(64.0f * (float)ntok));
-            const float gs = ldexpf(1.0f, -gnext);
-            static_for<0, NY>([&](auto ki) {
-                constexpr int kk = decltype(ki)::value;
-                constexpr int u = y3_u(W, kk), u2 = y3_u2(W, kk);
+                });
 #pragma unroll
-                for (int s = 0; s < 2; ++s) y3acc[kk] = mfma(Ak[u][s], Ak[u2][s], y3acc[kk]);
+                for (int kk = 0; kk < 2; ++kk)
+                    if (kk < ny3)
+                        y3acc[kk] = mfma(ld8(sm.kT + sw128(16 * y3u[kk] + r16, 32 * s + 8 * h)),
+                                         ld8(sm.kT + sw128(16 * y3u2[kk] + r16, 32 * s + 8 * h)),
+                                         y3acc[kk]);
+            }
+            // scaled fp16 copy of Y3 for the next chunk's denominators
+            const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
+            const float gs = ldexpf(1.0f, -gnext);
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                if (kk >= ny3) break;
+                const int u = y3u[kk], u2 = y3u2[kk];
                 // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
                 const int mcol = 16 * u2 + r16;
                 h4 hv;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) hv[i] = (_Float16)(y3acc[kk][i] * gs);
-                *(h4 *)(sm.y3h + mcol * RS + 16 * u + 4 * h) = hv;       // Y3[m][l]
+                *(h4 *)(sm.y3h + sw64(mcol, 16 * u + 4 * h)) = hv;       // Y3[m][l]
                 if (u != u2) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) sm.y3h[(16 * u + 4 * h + i) * RS + mcol] = hv[i];
+                    for (int i = 0; i < 4; ++i) sm.y3h[sw64(16 * u + 4 * h + i, mcol)] = hv[i];
                 }
-            });
+            }
             gexp = gnext;
         }
         __syncthreads();
     }
 }
 
-__global__ __launch_bounds__(NTH, 1) void fwd_causal_kernel(const bf16_t *__restrict__ q,
+__global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__restrict__ q,
                                                             const bf16_t *__restrict__ k,
                                                             const bf16_t *__restrict__ v,
                                                             bf16_t *__restrict__ out,
@@ -534,17 +571,14 @@ __global__ __launch_bounds__(NTH, 1) void fwd_causal_kernel(const bf16_t *__rest
     if ((tid & 63) == 0) sm.red[tid >> 6] = vmax;
     if (tid < D) { sm.y2[tid] = 0.f; sm.y2c[tid] = 0.f; }
     if (tid < SL) { sm.x1[tid] = 0.f; sm.x1c[tid] = 0.f; }
-    for (int e = tid; e < D * RS; e += NTH) sm.y3h[e] = (_Float16)0.0f;
+    for (int e = tid; e < D * RS64; e += NTH) sm.y3h[e] = (_Float16)0.0f;
     __syncthreads();
-    vmax = fmaxf(fmaxf(sm.red[0], sm.red[1]), fmaxf(sm.red[2], sm.red[3]));
+    vmax = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) vmax = fmaxf(vmax, sm.red[w]);
     const int vexp = pow2_exponent(vmax * 63.0f * (float)N);
 
-    switch (tid >> 6) {
-    case 0: run_wave<0>(sm, q, k, v, out, g, N, sl, vexp); break;
-    case 1: run_wave<1>(sm, q, k, v, out, g, N, sl, vexp); break;
-    case 2: run_wave<2>(sm, q, k, v, out, g, N, sl, vexp); break;
-    default: run_wave<3>(sm, q, k, v, out, g, N, sl, vexp); break;
-    }
+    run_scan(sm, q, k, v, out, g, N, sl, vexp);
 }
 
 }  // namespace mfma_causal
