@@ -124,11 +124,11 @@ struct Smem {
     _Float16 vT[SL * RS128];    // scaled v [j][token]
     _Float16 y3h[D * RS64];     // scaled Y3 (prefix before the chunk)
     float fpart[NW * C * SL];   // partial F^T: [wave][column quad][token][4]
+    float gpart[NW * C];        // partial denominators: [wave][token]
     float y2[D];              // sum k^ before the chunk
     float y2c[D];             // this chunk's sum k^
     float x1[SL];             // sum of scaled v before the chunk
     float x1c[SL];
-    float g[C];
     float red[NW];
 };
 
@@ -378,12 +378,16 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                     if constexpr (p & 1) F1 = mfma(Ast[p], B, F1);
                     else F0 = mfma(Ast[p], B, F0);
                 });
-                if (rt == w) {
+                // In-chunk tril block.  Row tile rt has rt/2 + 1 items (pairs of
+                // 16-token key tiles); the chunk's 20 items are dealt round-robin
+                // to the 8 waves.  Each item: two S^T tiles (rows t, cols i = tok),
+                // their weights f(s) and one MFMA F^T += V^T W^T.
+                const int ibase = (rt / 2) * (rt / 2 + 1) + ((rt & 1) ? rt / 2 + 1 : 0);
+                const int first = (w - ibase % NW + NW) % NW;   // first item j of this wave
+                float gpart = 0.f;
+                if (first <= rt / 2 || rt == w) {
                     const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
                     const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
-                    // in-chunk tril block, two S^T tiles (rows t, cols i = tok) at a
-                    // time, each pair feeding one MFMA of F^T += V^T W^T
-                    float gi = 0.f;
                     auto wtile = [&](int tt) -> h4 {
                         f4 S = {0.f, 0.f, 0.f, 0.f};
                         S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 8 * h)), QB0, S);
@@ -395,12 +399,12 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                             float y = fmaf(0.5f * x, x, 1.0f + x);
                             if (tt == rt && (4 * h + i) > r16) y = 0.0f;
                             wv[i] = y;
-                            gi += y;
+                            gpart += y;
                         }
                         return cvt4(wv);
                     };
-                    for (int a = 0; a <= rt; a += 2) {
-                        const int b = a + 1;
+                    for (int j = first; j <= rt / 2; j += NW) {
+                        const int a = 2 * j, b = a + 1;
                         const h4 wa = wtile(a);
                         const h4 va = ld4(sm.vT + sw128(r16, 16 * a + 4 * h));
                         h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
@@ -410,24 +414,27 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                         }
                         F0 = mfma(cat(va, vb), cat(wa, wb), F0);
                     }
-                    // G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sum
-                    float gq = 0.f;
-                    const float ys = ldexpf(2.0f, -gexp);
+                    if (rt == w) {
+                        // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
+                        float gq = 0.f;
+                        const float ys = ldexpf(2.0f, -gexp);
 #pragma unroll
-                    for (int cc = 0; cc < 4; ++cc) {
-                        f4 T;
+                        for (int cc = 0; cc < 4; ++cc) {
+                            f4 T;
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[16 * cc + 4 * h + i];
-                        T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
-                        T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
+                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[16 * cc + 4 * h + i];
+                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
+                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) gq = fmaf((float)myl[cc][i], T[i], gq);
+                            for (int i = 0; i < 4; ++i) gq = fmaf((float)myl[cc][i], T[i], gq);
+                        }
+                        gpart = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gpart);
+                        if (h == 0) gpart += (float)n0;
                     }
-                    float part = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gi);
-                    part += __shfl_xor(part, 16);
-                    part += __shfl_xor(part, 32);
-                    if (h == 0) sm.g[tok] = (float)n0 + part;
+                    gpart += __shfl_xor(gpart, 16);
+                    gpart += __shfl_xor(gpart, 32);
                 }
+                if (h == 0) sm.gpart[w * C + tok] = gpart;
                 *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
             }
             // this chunk's sums of k^ (for y2, waves 0-3) and of scaled v (x1, wave 4)
@@ -454,9 +461,12 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
         {
             const int tok = tid & (C - 1), cq = tid >> 7;
             f4 F = *(const f4 *)(sm.x1 + 4 * cq);
+            float Gi = 0.f;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) F += *(const f4 *)(sm.fpart + ((ww * 4 + cq) * C + tok) * 4);
-            const float Gi = sm.g[tok];
+            for (int ww = 0; ww < NW; ++ww) {
+                F += *(const f4 *)(sm.fpart + ((ww * 4 + cq) * C + tok) * 4);
+                Gi += sm.gpart[ww * C + tok];
+            }
             if (n0 + tok < N) {
                 const float sc = oscale / Gi;
                 uint2 o;
