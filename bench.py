@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt_causal_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
+                    help="only run a plain device-to-device copy of this many MiB "
+                         "(for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE) and exit")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -117,9 +120,19 @@ def main():
     from paper_2402_07901_amd import fastmax as fm
     from paper_2402_07901_amd.inputs import WORKLOADS, workload_inputs
 
+    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(max(1, args.steps)):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "steps": max(1, args.steps)}))
+        return
+
     w = WORKLOADS[args.workload]
     fm.lib()
-    dev = torch.device("cuda:0")
     inp = workload_inputs(w, want64=False)
 
     def to_dev(x):
