@@ -26,7 +26,7 @@ PEAK = {  # MI355X published dense peaks
     ("mfma", "bf16"): 2500.0,   # TFLOP/s
     ("mfma", "f16"): 2500.0,
     ("mfma", "f32"): 157.3,
-    ("alu", "f32"): 157.3,
+    ("alu", "f32"): 78.6,       # fp32 FMA without packed math: 256 CU x 4 SIMD x 16 lanes x 2 x 2.4 GHz
     ("hbm", None): 8000.0,      # GB/s
 }
 
@@ -101,6 +101,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt_causal_bf16")
+    ap.add_argument("--mode", choices=["fwd", "fwdbwd"], default="fwd",
+                    help="fwd: one forward per step (the headline); fwdbwd: forward + "
+                         "backward per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
                     help="only run a plain device-to-device copy of this many MiB "
@@ -141,6 +144,9 @@ def main():
         return torch.from_numpy(x).to(dev)
 
     q, k, v = (to_dev(inp[n]) for n in ("q", "k", "v"))
+    dout = to_dev(inp["dout"]) if (args.mode == "fwdbwd" and "dout" in inp) else None
+    if args.mode == "fwdbwd" and dout is None:
+        dout = torch.randn_like(q)
     out = torch.empty_like(q)
     g = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
     dt = fm.BF16 if w.dtype == "bf16" else fm.F32
@@ -148,11 +154,24 @@ def main():
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step():
+    if args.mode == "fwdbwd":
+        need_b = fm.workspace_bytes(w.B, w.H, w.N, w.D, w.p, w.causal, dt, True)
+        ws_b = torch.empty(max(need_b, 1), dtype=torch.uint8, device=dev)
+        dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    bwd_start = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+
+    def step(i=None):
         rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
                                 need, stream)
         if rc != fm.OK:
             raise fm.FastmaxError(rc, "fastmax_fwd")
+        if args.mode == "fwdbwd":
+            if i is not None:
+                bwd_start[i].record(stream)
+            rc = fm.fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, w.B, w.H, w.N, w.D, w.p,
+                                    w.causal, dt, ws_b, need_b, stream)
+            if rc != fm.OK:
+                raise fm.FastmaxError(rc, "fastmax_bwd")
 
     for _ in range(args.warmup):
         step()
@@ -164,11 +183,16 @@ def main():
     t0 = time.perf_counter()
     for i in range(args.steps):
         starts[i].record(stream)
-        step()
+        step(i)
         stops[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    launch_ms = [s.elapsed_time(e) for s, e in zip(starts, stops)]
+    if args.mode == "fwdbwd":
+        fwd_ms = [s.elapsed_time(e) for s, e in zip(starts, bwd_start)]
+        bwd_ms = [s.elapsed_time(e) for s, e in zip(bwd_start, stops)]
+        launch_ms = fwd_ms
+    else:
+        launch_ms = [s.elapsed_time(e) for s, e in zip(starts, stops)]
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
     ms_per_step = wall / args.steps * 1e3
 
@@ -180,7 +204,8 @@ def main():
         bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "bf16")]
         achieved = flops / avg_launch_s / 1e12
     elif w.p == 2:
-        bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "f32")]
+        # the float32 path computes on the vector ALU in fp32
+        bound, unit, peak = "alu", "TFLOP/s", PEAK[("alu", "f32")]
         achieved = flops / avg_launch_s / 1e12
     else:
         bound, unit, peak = "hbm", "GB/s", PEAK[("hbm", None)]
@@ -188,7 +213,8 @@ def main():
         achieved = tokens_heads * (4 * w.D * elt + 4) / avg_launch_s / 1e9
 
     rec = {
-        "metric": METRIC,
+        "metric": METRIC if (w.name == "gpt_causal_bf16" and args.mode == "fwd") else
+                  f"Fastmax {args.mode} tokens·heads/s on 1 GPU ({w.name})",
         "value": value,
         "unit": "tokens*heads/s",
         "n_gpus": 1,
@@ -200,14 +226,17 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "D": w.D, "p": w.p,
-                   "causal": w.causal, "io_dtype": w.dtype, "global_batch": w.B,
-                   "seq_len": w.N, "parallelism": "none (1 GPU)"},
+        "config": {"workload": w.name, "mode": args.mode, "B": w.B, "H": w.H, "N": w.N,
+                   "D": w.D, "p": w.p, "causal": w.causal, "io_dtype": w.dtype,
+                   "global_batch": w.B, "seq_len": w.N, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": load_traffic(kernel, w.name),
                      "kernel": kernel, "avg_launch_ms": avg_launch_s * 1e3,
                      "algorithmic_flops_per_launch": flops},
     }
+    if args.mode == "fwdbwd":
+        rec["backward"] = {"avg_ms": sum(bwd_ms) / len(bwd_ms),
+                           "note": "fastmax_bwd call (all its kernels), HIP events on the stream"}
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(rec), flush=True)
