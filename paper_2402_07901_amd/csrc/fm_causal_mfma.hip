@@ -117,17 +117,16 @@ __device__ __forceinline__ int sw64(int row, int col) { return row * RS64 + col;
 __device__ __forceinline__ int sw128(int row, int col) { return row * RS128 + col; }
 
 struct Smem {
-    _Float16 qrow[C * RS64];    // q^ [token][m]
-    _Float16 qperm[C * RS64];   // q^ [token][(m % 8) * 8 + m / 8]
-    _Float16 krow[C * RS64];    // k^ [token][m]
-    _Float16 kT[D * RS128];     // k^ [m][token]
-    _Float16 vT[SL * RS128];    // scaled v [j][token]
-    _Float16 y3h[D * RS64];     // scaled Y3 (prefix before the chunk)
-    float fpart[NW * C * SL];   // partial F^T: [wave][column quad][token][4]
-    float gpart[NW * C];        // partial denominators: [wave][token]
-    float y2[D];              // sum k^ before the chunk
-    float y2c[D];             // this chunk's sum k^
-    float x1[SL];             // sum of scaled v before the chunk
+    _Float16 qrow[C * RS64];        // q^ [token][m]
+    _Float16 krow[C * RS64];        // k^ [token][m]
+    _Float16 kT[2][D * RS128];      // k^ [m][token], double-buffered by chunk parity
+    _Float16 vT[2][SL * RS128];     // scaled v [j][token], double-buffered
+    _Float16 y3h[D * RS64];         // scaled Y3 (prefix before the chunk)
+    float fpart[NW * C * SL];       // partial F^T: [wave][column quad][token][4]
+    float gpart[NW * C];            // partial denominators: [wave][token]
+    float y2[2][D];                 // sum k^ before the chunk (by chunk parity)
+    float y2c[D];                   // this chunk's sum k^
+    float x1[2][SL];                // sum of scaled v before the chunk
     float x1c[SL];
     float red[NW];
 };
@@ -250,7 +249,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
     int gexp = 0;                                // Y3 in LDS is Y3 * 2^-gexp
     const int nch = (N + C - 1) / C;
 
-    // Lane-derived LDS offsets are recomputed in every chunk from an opaque
+    // Lane-derived LDS offsets are recomputed in every phase from an opaque
     // copy of the thread id: hoisted out of the loop they would stay live for
     // the whole scan and spill.
     int tid = threadIdx.x;
@@ -285,49 +284,50 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
         pv = z;
         if (tid < 2 * C && nv < N) pv = *(const uint4 *)(v + (size_t)nv * D + SL * sl + 8 * vh);
     };
+    // Staging of chunk c (Sec. 2.2, Eqs. 6-7): standardise q and k rows, store
+    // q^, k^ (row-major), k^ transposed and the scaled v transposed.
+    auto stage_q = [&](int c) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int row = 2 * tg + j;
+            float x[8];
+            bf16x8_to_f32(pq[j], x);
+            *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = standardise8(x, c * C + row < N);
+        }
+    };
+    auto stage_kv = [&](int c) {
+        const int buf = c & 1;
+        h8 hk[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int row = 2 * tg + j;
+            float x[8];
+            bf16x8_to_f32(pk[j], x);
+            hk[j] = standardise8(x, c * C + row < N);
+            *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            *(h2 *)(sm.kT[buf] + sw128(8 * cg + i, 2 * tg)) = h2{hk[0][i], hk[1][i]};
+        if (tid < 2 * C) {
+            float xv[8];
+            bf16x8_to_f32(pv, xv);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vscale);
+        }
+    };
+
+    // prologue: stage chunk 0
     prefetch(0);
+    stage_q(0);
+    stage_kv(0);
+    __syncthreads();
 
     for (int c = 0; c < nch; ++c) {
         const int n0 = c * C;
         const int nvalid = min(C, N - n0);
-        refresh_ids();
-        // ---- fold the previous chunk's sums into the prefixes ----------------
-        if (c > 0) {
-            if (tid < D) sm.y2[tid] += sm.y2c[tid];
-            else if (tid < D + SL) sm.x1[tid - D] += sm.x1c[tid - D];
-        }
-        // ---- (L) standardise q, k (Sec. 2.2, Eqs. 6-7) and stage the chunk ----
-        {
-            _Float16 kh[2][8];
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int row = 2 * tg + j;
-                const bool valid = (n0 + row) < N;
-                float xq[8], xk[8];
-                bf16x8_to_f32(pq[j], xq);
-                bf16x8_to_f32(pk[j], xk);
-                const h8 hq = standardise8(xq, valid);
-                const h8 hk = standardise8(xk, valid);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) kh[j][i] = hk[i];
-                *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
-                *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk;
-                // channel m = 8*cg + i sits at (m % 8) * 8 + m / 8 = 8*i + cg
-#pragma unroll
-                for (int i = 0; i < 8; ++i) sm.qperm[sw64(row, 8 * i + cg)] = hq[i];
-            }
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                *(h2 *)(sm.kT + sw128(8 * cg + i, 2 * tg)) = h2{kh[0][i], kh[1][i]};
-            if (tid < 2 * C) {
-                float xv[8];
-                bf16x8_to_f32(pv, xv);
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    sm.vT[sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vscale);
-            }
-        }
-        __syncthreads();
+        const int cur = c & 1, nxt = cur ^ 1;
 
         // ---- (I) query contraction, in-chunk block and denominators ---------
         __builtin_amdgcn_sched_barrier(0);
@@ -349,6 +349,8 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 Ast[p] = cat(a, b);
             });
 
+            const _Float16 *kTc = sm.kT[cur];
+            const _Float16 *vTc = sm.vT[cur];
 #pragma unroll 1
             for (int rt = 0; rt < NRT; ++rt) {
                 const int tok = 16 * rt + r16;
@@ -357,8 +359,10 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 for (int u = 0; u < 4; ++u) myl[u] = ld4(sm.qrow + sw64(tok, 16 * u + 4 * h));
                 // linear features l = 16w + 4h + r (zero state in waves 4..7)
                 const h4 mylin = ld4(sm.qrow + sw64(tok, 16 * (w & 3) + 4 * h));
-                // the wave's channels m = w + 8*idx sit at qperm[8w + idx]
-                const h8 qm = ld8(sm.qperm + sw64(tok, 8 * w));
+                // the wave's channels m = w + 8*idx
+                _Float16 qm[8];
+#pragma unroll
+                for (int idx = 0; idx < 8; ++idx) qm[idx] = sm.qrow[sw64(tok, w + 8 * idx)];
                 f4 F0 = {0.f, 0.f, 0.f, 0.f}, F1 = {0.f, 0.f, 0.f, 0.f};
                 auto gen = [&](auto ti) -> h4 {
                     constexpr int t = decltype(ti)::value;
@@ -406,11 +410,11 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                     for (int j = first; j <= rt / 2; j += NW) {
                         const int a = 2 * j, b = a + 1;
                         const h4 wa = wtile(a);
-                        const h4 va = ld4(sm.vT + sw128(r16, 16 * a + 4 * h));
+                        const h4 va = ld4(vTc + sw128(r16, 16 * a + 4 * h));
                         h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
                         if (b <= rt) {
                             wb = wtile(b);
-                            vb = ld4(sm.vT + sw128(r16, 16 * b + 4 * h));
+                            vb = ld4(vTc + sw128(r16, 16 * b + 4 * h));
                         }
                         F0 = mfma(cat(va, vb), cat(wa, wb), F0);
                     }
@@ -422,7 +426,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                         for (int cc = 0; cc < 4; ++cc) {
                             f4 T;
 #pragma unroll
-                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[16 * cc + 4 * h + i];
+                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[cur][16 * cc + 4 * h + i];
                             T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
                             T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
 #pragma unroll
@@ -442,14 +446,14 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 const int m = 16 * w + r16;
                 float s = 0.f;
 #pragma unroll
-                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(sm.kT + sw128(m, 32 * h + 8 * cc)));
+                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(kTc + sw128(m, 32 * h + 8 * cc)));
                 s += __shfl_xor(s, 16);
                 s += __shfl_xor(s, 32);
                 if (h == 0) sm.y2c[m] = s;
             } else if (w == 4) {
                 float sv = 0.f;
 #pragma unroll
-                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(sm.vT + sw128(r16, 32 * h + 8 * cc)));
+                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(vTc + sw128(r16, 32 * h + 8 * cc)));
                 sv += __shfl_xor(sv, 16);
                 sv += __shfl_xor(sv, 32);
                 if (h == 0) sm.x1c[r16] = sv;
@@ -457,10 +461,13 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
         }
         __syncthreads();
 
-        // ---- (R) combine partials, divide, store ------------------------------
+        // ---- (M) output of chunk c, state update with chunk c, staging of c+1 --
+        __builtin_amdgcn_sched_barrier(0);
+        refresh_ids();
         {
+            // combine partials, divide, store
             const int tok = tid & (C - 1), cq = tid >> 7;
-            f4 F = *(const f4 *)(sm.x1 + 4 * cq);
+            f4 F = *(const f4 *)(sm.x1[cur] + 4 * cq);
             float Gi = 0.f;
 #pragma unroll
             for (int ww = 0; ww < NW; ++ww) {
@@ -475,29 +482,30 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 *(uint2 *)(out + (size_t)(n0 + tok) * D + SL * sl + 4 * cq) = o;
                 if (g && sl == 0 && cq == 0) g[n0 + tok] = Gi;
             }
+            // prefixes for the next chunk
+            if (tid < D) sm.y2[nxt][tid] = sm.y2[cur][tid] + sm.y2c[tid];
+            else if (tid < D + SL) sm.x1[nxt][tid - D] = sm.x1[cur][tid - D] + sm.x1c[tid - D];
         }
-
-        // ---- (U) state update S += Phi(K)^T V, Y3 += K^T K ---------------------
-        // (the next chunk's loads are issued here, after the fp16 state copy of
-        // phase I is dead, and complete behind the update's MFMAs)
-        __builtin_amdgcn_sched_barrier(0);
-        refresh_ids();
-        if (c + 1 < nch) prefetch(c + 1);
+        const bool more = c + 1 < nch;
+        if (more) prefetch(c + 1);
         {
-#pragma unroll 1
-            for (int s = 0; s < NKS2; ++s) {
+            // state update S += Phi(K)^T V, Y3 += K^T K, interleaved with the
+            // staging of the next chunk (its loads land behind the first steps)
+            const _Float16 *kTc = sm.kT[cur];
+            const _Float16 *vTc = sm.vT[cur];
+            auto ustep = [&](int s) {
                 h8 Ak[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) Ak[u] = ld8(sm.kT + sw128(16 * u + r16, 32 * s + 8 * h));
-                const h8 Vf = ld8(sm.vT + sw128(r16, 32 * s + 8 * h));
+                for (int u = 0; u < 4; ++u) Ak[u] = ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h));
+                const h8 Vf = ld8(vTc + sw128(r16, 32 * s + 8 * h));
                 if (has_lin)   // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
-                    acc[0] = mfma(ld8(sm.kT + sw128(16 * w + r16, 32 * s + 8 * h)), Vf, acc[0]);
+                    acc[0] = mfma(ld8(kTc + sw128(16 * w + r16, 32 * s + 8 * h)), Vf, acc[0]);
                 static_for<0, 8>([&](auto ii) {
                     constexpr int idx = decltype(ii)::value;
                     constexpr int u0 = u0_of(idx);
                     constexpr int t0 = first_tile(idx);
                     const int m = w + 8 * idx;
-                    const h8 km = ld8(sm.kT + sw128(m, 32 * s + 8 * h));
+                    const h8 km = ld8(kTc + sw128(m, 32 * s + 8 * h));
                     const h8 Wm = km * Vf;
                     static_for<u0, 4>([&](auto ui) {
                         constexpr int u = decltype(ui)::value;
@@ -507,10 +515,16 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk)
                     if (kk < ny3)
-                        y3acc[kk] = mfma(ld8(sm.kT + sw128(16 * y3u[kk] + r16, 32 * s + 8 * h)),
-                                         ld8(sm.kT + sw128(16 * y3u2[kk] + r16, 32 * s + 8 * h)),
+                        y3acc[kk] = mfma(ld8(kTc + sw128(16 * y3u[kk] + r16, 32 * s + 8 * h)),
+                                         ld8(kTc + sw128(16 * y3u2[kk] + r16, 32 * s + 8 * h)),
                                          y3acc[kk]);
-            }
+            };
+            ustep(0);
+            ustep(1);
+            ustep(2);
+            if (more) stage_q(c + 1);
+            ustep(3);
+            if (more) stage_kv(c + 1);
             // scaled fp16 copy of Y3 for the next chunk's denominators
             const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
             const float gs = ldexpf(1.0f, -gnext);
@@ -579,8 +593,8 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
     if ((tid & 63) == 0) sm.red[tid >> 6] = vmax;
-    if (tid < D) { sm.y2[tid] = 0.f; sm.y2c[tid] = 0.f; }
-    if (tid < SL) { sm.x1[tid] = 0.f; sm.x1c[tid] = 0.f; }
+    if (tid < D) { sm.y2[0][tid] = 0.f; sm.y2c[tid] = 0.f; }
+    if (tid < SL) { sm.x1[0][tid] = 0.f; sm.x1c[tid] = 0.f; }
     for (int e = tid; e < D * RS64; e += NTH) sm.y3h[e] = (_Float16)0.0f;
     __syncthreads();
     vmax = 0.f;
