@@ -25,7 +25,20 @@ int check_common(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t 
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
-size_t fwd_ws(int, int, int, int, int, int, fastmax_dtype_t) { return 0; }
+// The segmented MFMA path rounds the moments to fp16; with very few keys G
+// can be far smaller than the moment terms it is summed from (G = f_2(s) >= 1/2
+// for one key against terms of size ~|q^||k^|^2/2), which amplifies that
+// rounding past the bf16 tolerance.  Below one 128-token chunk of keys the
+// fp32 generic kernel is exact to fp32 and costs next to nothing.
+bool mfma_noncausal(int N, int D, int p, int causal, fastmax_dtype_t dt)
+{
+    return D == 64 && p == 2 && !causal && dt == FASTMAX_BF16 && N >= 128;
+}
+
+size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+{
+    return mfma_noncausal(N, D, p, causal, dt) ? fm::mfma_nc_workspace(B * H, N) : 0;
+}
 
 size_t bwd_ws(int B, int H, int N, int D, int, int, fastmax_dtype_t)
 {
@@ -59,6 +72,8 @@ int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g
     hipError_t e;
     if (D == 64 && p == 2 && causal && dt == FASTMAX_BF16)
         e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, stream);
+    else if (mfma_noncausal(N, D, p, causal, dt))
+        e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, workspace, stream);
     else
         e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;

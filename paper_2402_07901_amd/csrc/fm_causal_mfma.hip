@@ -6,15 +6,8 @@
 // state S[f][j] = sum_n phi_f(k^_n) v_nj of the slice as fp32 MFMA
 // accumulators for the whole sequence, so the state never touches HBM.
 //
-// Features.  The quadratic features k_m k_l are grouped in 16x16 tiles
-// (m, u): rows l = 16u..16u+15 for one m, with u >= m/16 (symmetric tiles:
-// 160 of them) plus 4 linear tiles (k_l) -- 2624 feature rows instead of the
-// 4160 of the full square, 2080 + 65 being the minimum.  A "diagonal" tile
-// (u == m/16) carries both (m,l) and (l,m) and enters the query contraction
-// with weight 1/2 (applied when the state is converted to fp16), the others
-// with weight 1, so psi(q).phi(k) = 1 + s + s^2/2 exactly (constant term
-// separate).  Wave w owns the tiles of m = w (mod 8) and, for w < 4, the
-// linear tile u = w: 21 tiles, 84 accumulator registers.
+// Features: the 21-tile-per-wave pattern of fm_mfma.h (symmetric 16x16
+// tiles of k_m k_l plus the linear tiles); 84 accumulator registers per lane.
 //
 // Per chunk:
 //  (i)  query contraction F^T += S^T Psi(Q)^T.  The accumulator layout of a
@@ -40,16 +33,13 @@
 
 #include "fm_common.h"
 #include "fm_internal.h"
+#include "fm_mfma.h"
 
 namespace fm {
 namespace mfma_causal {
 
-typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef float f4 __attribute__((ext_vector_type(4)));
+using namespace mx;
 
-constexpr int D = 64;
 constexpr int C = 128;        // tokens per chunk
 constexpr int NRT = C / 16;   // 16-token row tiles per chunk
 constexpr int NKS2 = C / 32;  // 32-token K steps of the state update
@@ -57,64 +47,6 @@ constexpr int NW = 8;         // waves per workgroup (2 per SIMD)
 constexpr int NTH = NW * 64;
 constexpr int SL = 16;        // value columns per workgroup
 constexpr int NSL = D / SL;
-
-template <int I, int N, typename F>
-__device__ __forceinline__ void static_for(F &&f)
-{
-    if constexpr (I < N) {
-        f(std::integral_constant<int, I>{});
-        static_for<I + 1, N>(f);
-    }
-}
-
-// Tiles of a wave w: tile 0 is the linear tile u = w (waves 0..3 only; it
-// stays zero in waves 4..7), then for the wave's channels m = w + 8*idx
-// (idx = 0..7) the tiles u = idx/2 .. 3 (m/16 == idx/2 for every w < 8), so
-// all waves share one tile pattern: 1 + 4+4+3+3+2+2+1+1 = 21 tiles.
-constexpr int NT = 21;
-constexpr int NKS = (NT + 1) / 2;   // K steps of the query contraction
-__host__ __device__ constexpr int u0_of(int idx) { return idx / 2; }
-__host__ __device__ constexpr int first_tile(int idx)
-{
-    int t = 1;
-    for (int i = 0; i < idx; ++i) t += 4 - u0_of(i);
-    return t;
-}
-struct Tile {
-    int kind;  // 0 linear, 1 quadratic, -1 padding
-    int idx;   // channel m = w + 8*idx
-    int u;     // l tile
-};
-__host__ __device__ constexpr Tile tile_of(int t)
-{
-    if (t == 0) return Tile{0, -1, -1};
-    for (int idx = 0; idx < 8; ++idx)
-        if (t < first_tile(idx) + 4 - u0_of(idx)) return Tile{1, idx, u0_of(idx) + t - first_tile(idx)};
-    return Tile{-1, -1, -1};
-}
-__host__ __device__ constexpr bool is_diag(int t)
-{
-    return t < NT && tile_of(t).kind == 1 && tile_of(t).u == u0_of(tile_of(t).idx);
-}
-
-// Y3 tiles (u <= u2), 10 of them: waves 0 and 1 own two, the others one.
-__device__ __forceinline__ int y3_count(int w) { return w < 2 ? 2 : 1; }
-__device__ __forceinline__ void y3_tile(int w, int k, int &u, int &u2)
-{
-    const int i = w < 2 ? 2 * w + k : 2 + w;
-    const int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
-    const int vs[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
-    u = us[i];
-    u2 = vs[i];
-}
-
-// LDS rows are padded by 16 bytes: 16 lanes reading the same column of 16
-// consecutive rows then fall on 16 distinct 4-bank groups, and offsets stay
-// affine so constant parts fold into the instructions.  Offsets in halves.
-constexpr int RS64 = 64 + 8;     // rows of 64 halves
-constexpr int RS128 = 128 + 8;   // rows of 128 halves
-__device__ __forceinline__ int sw64(int row, int col) { return row * RS64 + col; }
-__device__ __forceinline__ int sw128(int row, int col) { return row * RS128 + col; }
 
 struct Smem {
     _Float16 qrow[C * RS64];        // q^ [token][m]
@@ -130,102 +62,6 @@ struct Smem {
     float x1c[SL];
     float red[NW];
 };
-
-__device__ __forceinline__ f4 mfma(h8 a, h8 b, f4 c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ h4 cvt4(f4 x)
-{
-    h2 lo = {(_Float16)x[0], (_Float16)x[1]};
-    h2 hi = {(_Float16)x[2], (_Float16)x[3]};
-    return h4{lo[0], lo[1], hi[0], hi[1]};
-}
-
-__device__ __forceinline__ h8 cat(h4 a, h4 b)
-{
-    return h8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-}
-
-__device__ __forceinline__ h4 scale4(h4 x, _Float16 s)
-{
-    h2 ss = {s, s};
-    h2 lo = h2{x[0], x[1]} * ss;
-    h2 hi = h2{x[2], x[3]} * ss;
-    return h4{lo[0], lo[1], hi[0], hi[1]};
-}
-
-__device__ __forceinline__ h8 ld8(const _Float16 *p) { return *(const h8 *)p; }
-__device__ __forceinline__ h4 ld4(const _Float16 *p) { return *(const h4 *)p; }
-
-// 8 bf16 (one 16-byte load) -> 8 floats
-__device__ __forceinline__ void bf16x8_to_f32(uint4 u, float *x)
-{
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        x[2 * i] = __uint_as_float(w[i] << 16);
-        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    }
-}
-
-// Smallest e with bound * 2^-e <= 2^15 (e may be negative), clamped.
-__device__ __forceinline__ int pow2_exponent(float bound)
-{
-    if (!(bound > 0.0f)) return 0;
-    int e = (int)ceilf(log2f(bound)) - 15;
-    return e < -100 ? -100 : (e > 100 ? 100 : e);
-}
-
-// Sum over an aligned octet of lanes with DPP: swap neighbours, swap pairs,
-// then mirror the two quads of each half row.
-__device__ __forceinline__ float octet_sum(float x)
-{
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, true));
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, true));
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, true));
-    return x;
-}
-
-// Standardises the 8 channels this lane holds of one token (the token's 64
-// channels are spread over the 8 lanes of an aligned octet) and returns them
-// as fp16.  Population variance, no epsilon; invalid rows become zero.
-__device__ __forceinline__ h8 standardise8(const float *xin, bool valid)
-{
-    float x[8];
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) s += xin[i];
-    const float mu = octet_sum(s) * (1.0f / D);
-    float v = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        x[i] = xin[i] - mu;
-        v = fmaf(x[i], x[i], v);
-    }
-    const float r = valid ? __builtin_amdgcn_rsqf(octet_sum(v) * (1.0f / D)) : 0.0f;
-    h8 o;
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-        const h2 pr = {(_Float16)(x[i] * r), (_Float16)(x[i + 1] * r)};
-        o[i] = pr[0];
-        o[i + 1] = pr[1];
-    }
-    return o;
-}
-
-// sum of 8 halves in fp32 (dot products with ones)
-__device__ __forceinline__ float hsum8(h8 a)
-{
-    const h2 one = {(_Float16)1.0f, (_Float16)1.0f};
-    float s = 0.f;
-    s = __builtin_amdgcn_fdot2(h2{a[0], a[1]}, one, s, false);
-    s = __builtin_amdgcn_fdot2(h2{a[2], a[3]}, one, s, false);
-    s = __builtin_amdgcn_fdot2(h2{a[4], a[5]}, one, s, false);
-    s = __builtin_amdgcn_fdot2(h2{a[6], a[7]}, one, s, false);
-    return s;
-}
 
 __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                                          const bf16_t *__restrict__ k,

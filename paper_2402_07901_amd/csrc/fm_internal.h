@@ -19,4 +19,10 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
                            int BH, int N, hipStream_t st);
 size_t mfma_causal_smem_bytes();
 
+// MFMA non-causal path: D = 64, p = 2, bf16 I/O (moment build, segment
+// reduction, query contraction).  ws holds mfma_nc_workspace(BH, N) bytes.
+hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
+                       int N, void *ws, hipStream_t st);
+size_t mfma_nc_workspace(int BH, int N);
+
 }  // namespace fm

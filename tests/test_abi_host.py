@@ -103,6 +103,24 @@ def test_bwd_workspace_checks():
     assert bwd(ptrs, ws=A + 4, wsb=need, p=5) == fm.EINVAL
 
 
+def test_fwd_workspace_checks():
+    # the segmented non-causal path (bf16, D = 64, p = 2) needs a workspace
+    need = fm.workspace_bytes(1, 2, 1000, 64, 2, False, fm.BF16, False)
+    assert need > 0
+    assert fwd(causal=0, N=1000, H=2, ws=None, wsb=0) == fm.EWORKSPACE
+    assert fwd(causal=0, N=1000, H=2, ws=A, wsb=need - 1) == fm.EWORKSPACE
+    assert fwd(causal=0, N=1000, H=2, ws=A + 4, wsb=need) == fm.EALIGN
+    # sized for the whole problem: grows with the number of heads and tokens
+    assert fm.workspace_bytes(1, 8, 131072, 64, 2, False, fm.BF16, False) > need
+    # the causal scan and the float32 / other-D paths need none
+    assert fm.workspace_bytes(1, 2, 1000, 64, 2, True, fm.BF16, False) == 0
+    assert fm.workspace_bytes(1, 2, 1000, 64, 2, False, fm.F32, False) == 0
+    assert fm.workspace_bytes(1, 2, 1000, 32, 2, False, fm.BF16, False) == 0
+    # fewer keys than one 128-token chunk: the fp32 kernel, no workspace
+    assert fm.workspace_bytes(1, 2, 127, 64, 2, False, fm.BF16, False) == 0
+    assert fm.workspace_bytes(1, 2, 128, 64, 2, False, fm.BF16, False) > 0
+
+
 def test_bwd_rejects_bad_args():
     assert bwd(B=0) == fm.EINVAL
     assert bwd(D=100) == fm.EUNSUPPORTED
