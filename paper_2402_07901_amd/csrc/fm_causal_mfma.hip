@@ -311,10 +311,10 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 Gi += sm.gpart[ww * C + tok];
             }
             if (n0 + tok < N) {
-                const float sc = oscale / Gi;
+                const float sc = oscale * __builtin_amdgcn_rcpf(Gi);
                 uint2 o;
-                o.x = (uint32_t)f32_to_bf16(F[0] * sc) | ((uint32_t)f32_to_bf16(F[1] * sc) << 16);
-                o.y = (uint32_t)f32_to_bf16(F[2] * sc) | ((uint32_t)f32_to_bf16(F[3] * sc) << 16);
+                o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
+                o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
                 *(uint2 *)(out + (size_t)(n0 + tok) * D + SL * sl + 4 * cq) = o;
                 if (g && sl == 0 && cq == 0) g[n0 + tok] = Gi;
             }

@@ -183,6 +183,15 @@ __device__ __forceinline__ h8 standardise8(const float *xin, bool valid)
     return o;
 }
 
+// Two floats -> two bf16 (round to nearest even, v_cvt_pk_bf16_f32) packed
+// low-first into one word.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
+{
+    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+    typedef float fl2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(fl2{a, b}, bf2));
+}
+
 // sum of 8 halves in fp32 (dot products with ones)
 __device__ __forceinline__ float hsum8(h8 a)
 {

@@ -352,6 +352,7 @@ __global__ __launch_bounds__(512) void nc_reduce(const float *__restrict__ part,
         const int p = rest % NKS, w = rest / NKS;
         const int ta = 2 * p, tb = 2 * p + 1;
         f4 a = {0.f, 0.f, 0.f, 0.f}, bb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
         for (int s = 0; s < nseg; ++s) {
             const float *src = part + ((((size_t)head * NCT + ct) * nseg + s) * NW + w) * WAVE_STATE_F +
                                4 * lane;
@@ -475,10 +476,10 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
         for (int cc = 0; cc < 4; ++cc) gq += sm.gpart[buf][cc * QS + tk];
         const float G = fmaf(sm.hdr[2 * D + NCT], gq, Nf);
         if (n < tok1) {
-            const float sc = sm.hdr[2 * D + ct] / G;
+            const float sc = sm.hdr[2 * D + ct] * __builtin_amdgcn_rcpf(G);
             uint2 o;
-            o.x = (uint32_t)f32_to_bf16(F[0] * sc) | ((uint32_t)f32_to_bf16(F[1] * sc) << 16);
-            o.y = (uint32_t)f32_to_bf16(F[2] * sc) | ((uint32_t)f32_to_bf16(F[3] * sc) << 16);
+            o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
+            o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
             *(uint2 *)(out + (size_t)n * D + 4 * cq) = o;
             if (g && cq == 0) g[n] = G;
         }
@@ -497,7 +498,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
         refresh_ids();
         if (more && tid < 256) prefetch(s + 1);
         const _Float16 *qr = sm.qrow[buf];
-#pragma unroll 1
+#pragma unroll
         for (int rt = 0; rt < QS / 16; ++rt) {
             const int tk = 16 * rt + r16;
             h4 myl[4];
