@@ -35,9 +35,17 @@ def sources():
     return out
 
 
+# Per-source extra flags.  The backward moment scan keeps a 256-register fp32
+# state per lane; with MFMA results selected into VGPRs (AGPRs then serve as
+# overflow) it allocates without spilling.
+EXTRA = {
+    "fm_bwd_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *COMMON, "-c", src, "-o", obj]
+    cmd = [HIPCC, *COMMON, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -40,8 +40,14 @@ size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
     return mfma_noncausal(N, D, p, causal, dt) ? fm::mfma_nc_workspace(B * H, N) : 0;
 }
 
-size_t bwd_ws(int B, int H, int N, int D, int, int, fastmax_dtype_t)
+bool mfma_causal(int D, int p, int causal, fastmax_dtype_t dt)
 {
+    return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
+}
+
+size_t bwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+{
+    if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_bwd_workspace(B * H, N);
     return fm::generic_bwd_workspace(B, H, N, D);
 }
 
@@ -70,7 +76,7 @@ int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
     hipError_t e;
-    if (D == 64 && p == 2 && causal && dt == FASTMAX_BF16)
+    if (mfma_causal(D, p, causal, dt))
         e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, stream);
     else if (mfma_noncausal(N, D, p, causal, dt))
         e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, workspace, stream);
@@ -93,8 +99,12 @@ int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, co
     size_t need = bwd_ws(B, H, N, D, p, causal, dt);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
-    hipError_t e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
-                                   dt == FASTMAX_BF16, workspace, stream);
+    hipError_t e;
+    if (mfma_causal(D, p, causal, dt))
+        e = fm::mfma_causal_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, workspace, stream);
+    else
+        e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
+                            dt == FASTMAX_BF16, workspace, stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 

@@ -1,0 +1,708 @@
+// Causal Fastmax backward on CDNA4 MFMA, head dimension 64, p = 2, bf16 I/O.
+//
+// The custom gradient of Sec. 2.5: only G is kept from the forward, q^ and
+// k^ are recomputed, and every N x N quantity is replaced by moments.  With
+// u_i = dO_i / G_i, c_i = (dO_i . O_i) / G_i, u~_i = [u_i, -c_i], v'_n = [v_n, 1]
+// and the score derivative of Sec. 2.3 (Eq. "bound": d a_in / d s_il =
+// f'(s_il) / G_i (delta_nl - a_in), f_2' = 1 + s):
+//
+//   dq^_i = sum_{n<=i} (1 + s_in)(u~_i . v'_n) k^_n
+//   dk^_n = sum_{i>=n} (1 + s_in)(u~_i . v'_n) q^_i
+//   dv_n  = sum_{i>=n} f(s_in) u_i
+//
+// Kernels:
+//  bwd_prep     1/G, c per token; per head max|u|, max|v|, max|c| (fp16 scales).
+//  (dv)         the causal scan kernel run in reverse with values u (no divide).
+//  bwd_intra    in-chunk pairs (both n <= i inside a 128-token chunk) of dq^ and
+//               dk^ on MFMA; initialises the fp32 accumulators dq^, dk^.
+//  bwd_mg_scan  the inter-chunk part, one kernel for both gradients:
+//                 out_t[l] = sum_s (1 + x^_t . y^_s)(z_t . w_s) y^_s[l]
+//               over the summed tokens s of earlier chunks in scan order,
+//               factorised (p = 1 in the weights, times a rank-(D+1) term):
+//                 out_t[l] = sum_{m,j} x^_tm z_tj X3[m][l][j] + sum_j z_tj M1[j][l]
+//               with X3[m][l][j] = sum_s y^_sm y^_sl w_sj and M1 = sum_s w_sj y^_sl
+//               (j over the D+1 columns).  dq^: x = q, y = k, z = u~, w = v',
+//               chunks in order.  dk^: x = k, y = q, z = v', w = u~, chunks in
+//               reverse order (X3 is then the T3 moment, M1 the T2 moment).
+//  bwd_finish   back through the standardisation (Eqs. 6-7).
+#include <hip/hip_runtime.h>
+
+#include <limits.h>
+
+#include "fm_common.h"
+#include "fm_internal.h"
+#include "fm_mfma.h"
+
+namespace fm {
+namespace mfma_bwd {
+
+using namespace mx;
+
+constexpr int C = 128;   // tokens per chunk
+
+// ---------------------------------------------------------------------------
+// bwd_prep: one workgroup per head, octets of lanes per token.
+
+__global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ o,
+                                                const bf16_t *__restrict__ dout,
+                                                const bf16_t *__restrict__ v,
+                                                const float *__restrict__ g,
+                                                float *__restrict__ rg, float *__restrict__ cc,
+                                                float *__restrict__ hmax, int N)
+{
+    __shared__ float red[3][4];
+    const int head = blockIdx.x, tid = threadIdx.x;
+    const size_t hb = (size_t)head * N;
+    o += hb * D;
+    dout += hb * D;
+    v += hb * D;
+    g += hb;
+    rg += hb;
+    cc += hb;
+    const int oc = tid >> 3, cg = tid & 7;
+    float umax = 0.f, vmax = 0.f, cmax = 0.f;
+    for (int n0 = 0; n0 < N; n0 += 32) {
+        const int n = n0 + oc;
+        const bool valid = n < N;
+        float xo[8] = {}, xd[8] = {}, xv[8] = {};
+        float r = 0.f;
+        if (valid) {
+            bf16x8_to_f32(*(const uint4 *)(o + (size_t)n * D + 8 * cg), xo);
+            bf16x8_to_f32(*(const uint4 *)(dout + (size_t)n * D + 8 * cg), xd);
+            bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + 8 * cg), xv);
+            r = 1.0f / g[n];
+        }
+        float dot = 0.f, am = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            dot = fmaf(xd[i], xo[i], dot);
+            am = fmaxf(am, fabsf(xd[i]));
+            vmax = fmaxf(vmax, fabsf(xv[i]));
+        }
+        dot = octet_sum(dot);
+        const float c = dot * r;
+        umax = fmaxf(umax, am * fabsf(r));
+        cmax = fmaxf(cmax, fabsf(c));
+        if (valid && cg == 0) {
+            rg[n] = r;
+            cc[n] = c;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        umax = fmaxf(umax, __shfl_xor(umax, off));
+        vmax = fmaxf(vmax, __shfl_xor(vmax, off));
+        cmax = fmaxf(cmax, __shfl_xor(cmax, off));
+    }
+    if ((tid & 63) == 0) {
+        red[0][tid >> 6] = umax;
+        red[1][tid >> 6] = vmax;
+        red[2][tid >> 6] = cmax;
+    }
+    __syncthreads();
+    if (tid < 3) {
+        float m = 0.f;
+        for (int w = 0; w < 4; ++w) m = fmaxf(m, red[tid][w]);
+        hmax[(size_t)head * 4 + tid] = m;
+    }
+}
+
+// per-head maxima: [0] max|u|, [1] max|v|, [2] max|c|
+struct HeadMax {
+    float u, v, c;
+};
+__device__ __forceinline__ HeadMax head_max(const float *hmax, int head)
+{
+    return HeadMax{hmax[(size_t)head * 4], hmax[(size_t)head * 4 + 1], hmax[(size_t)head * 4 + 2]};
+}
+
+// ---------------------------------------------------------------------------
+// bwd_intra: (head, chunk); four waves.
+
+struct ISmem {
+    _Float16 qrow[C * RS64];   // q^ [t][m]
+    _Float16 krow[C * RS64];   // k^ [s][m]
+    _Float16 vrow[C * RS64];   // v * 2^-ev [s][j]
+    _Float16 urow[C * RS64];   // u * 2^-eu [t][j]
+    _Float16 qT[D * RS128];    // q^ [m][t]
+    _Float16 kT[D * RS128];    // k^ [m][s]
+    float cc[C];
+};
+
+__global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
+                                                 const bf16_t *__restrict__ k,
+                                                 const bf16_t *__restrict__ v,
+                                                 const bf16_t *__restrict__ dout,
+                                                 const float *__restrict__ rg,
+                                                 const float *__restrict__ cc,
+                                                 const float *__restrict__ hmax,
+                                                 float *__restrict__ dqh, float *__restrict__ dkh,
+                                                 int N, int nch)
+{
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    ISmem &sm = *reinterpret_cast<ISmem *>(smem_raw);
+    const int head = blockIdx.x / nch, c = blockIdx.x % nch;
+    const int n0 = c * C;
+    const size_t hb = (size_t)head * N;
+    q += hb * D;
+    k += hb * D;
+    v += hb * D;
+    dout += hb * D;
+    rg += hb;
+    cc += hb;
+    dqh += hb * D;
+    dkh += hb * D;
+
+    const HeadMax hm = head_max(hmax, head);
+    const int ev = pow2_exponent(hm.v), eu = pow2_exponent(hm.u);
+    // |P| <= 65 (64 max|v| max|u| + max|c|)
+    const int ep = pow2_exponent(65.0f * fmaf(64.0f * hm.v, hm.u, hm.c));
+    const float sv = ldexpf(1.0f, -ev), su = ldexpf(1.0f, -eu);
+    const float sa = ldexpf(1.0f, ev + eu), sp = ldexpf(1.0f, -ep), so = ldexpf(1.0f, ep);
+
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    // staging: four passes of 32 tokens, an octet of lanes per token
+    {
+        const int oc = tid >> 3, cg = tid & 7;
+        for (int pass = 0; pass < 4; ++pass) {
+            const int t = 32 * pass + oc, n = n0 + t;
+            const bool valid = n < N;
+            float xq[8] = {}, xk[8] = {}, xv[8] = {}, xu[8] = {};
+            float r = 0.f;
+            if (valid) {
+                bf16x8_to_f32(*(const uint4 *)(q + (size_t)n * D + 8 * cg), xq);
+                bf16x8_to_f32(*(const uint4 *)(k + (size_t)n * D + 8 * cg), xk);
+                bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + 8 * cg), xv);
+                bf16x8_to_f32(*(const uint4 *)(dout + (size_t)n * D + 8 * cg), xu);
+                r = rg[n];
+            }
+            const h8 hq = standardise8(xq, valid), hk = standardise8(xk, valid);
+            h8 hv, hu;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                hv[i] = (_Float16)(xv[i] * sv);
+                hu[i] = (_Float16)(xu[i] * (r * su));
+            }
+            *(h8 *)(sm.qrow + sw64(t, 8 * cg)) = hq;
+            *(h8 *)(sm.krow + sw64(t, 8 * cg)) = hk;
+            *(h8 *)(sm.vrow + sw64(t, 8 * cg)) = hv;
+            *(h8 *)(sm.urow + sw64(t, 8 * cg)) = hu;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                sm.qT[sw128(8 * cg + i, t)] = hq[i];
+                sm.kT[sw128(8 * cg + i, t)] = hk[i];
+            }
+            if (cg == 0) sm.cc[t] = valid ? cc[n] : 0.f;
+        }
+    }
+    __syncthreads();
+
+    const h4 z4 = {0, 0, 0, 0};
+    // dq^: query tiles rt in {w, 7-w}; lane column t = 16 rt + r16
+    for (int pick = 0; pick < 2; ++pick) {
+        const int rt = pick ? 7 - w : w;
+        const int t = 16 * rt + r16;
+        const float ct = sm.cc[t];
+        const h8 QB0 = ld8(sm.qrow + sw64(t, 8 * h)), QB1 = ld8(sm.qrow + sw64(t, 32 + 8 * h));
+        const h8 UB0 = ld8(sm.urow + sw64(t, 8 * h)), UB1 = ld8(sm.urow + sw64(t, 32 + 8 * h));
+        // P[s][t] of key tile st: lane (column t, rows s = 16 st + 4h + i)
+        auto ptile = [&](int st) -> h4 {
+            f4 S = {0.f, 0.f, 0.f, 0.f}, A = {0.f, 0.f, 0.f, 0.f};
+            S = mfma(ld8(sm.krow + sw64(16 * st + r16, 8 * h)), QB0, S);
+            S = mfma(ld8(sm.krow + sw64(16 * st + r16, 32 + 8 * h)), QB1, S);
+            A = mfma(ld8(sm.vrow + sw64(16 * st + r16, 8 * h)), UB0, A);
+            A = mfma(ld8(sm.vrow + sw64(16 * st + r16, 32 + 8 * h)), UB1, A);
+            f4 P;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float pv = (1.0f + S[i]) * fmaf(A[i], sa, -ct) * sp;
+                if (st == rt && 4 * h + i > r16) pv = 0.f;
+                P[i] = pv;
+            }
+            return cvt4(P);
+        };
+        f4 acc[4];
+#pragma unroll
+        for (int lt = 0; lt < 4; ++lt) acc[lt] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int a = 0; a <= rt; a += 2) {
+            const int b = a + 1;
+            const h4 pa = ptile(a);
+            const h4 pb = b <= rt ? ptile(b) : z4;
+            const h8 B = cat(pa, pb);
+#pragma unroll
+            for (int lt = 0; lt < 4; ++lt) {
+                const h4 ka = ld4(sm.kT + sw128(16 * lt + r16, 16 * a + 4 * h));
+                const h4 kb = b <= rt ? ld4(sm.kT + sw128(16 * lt + r16, 16 * b + 4 * h)) : z4;
+                acc[lt] = mfma(cat(ka, kb), B, acc[lt]);
+            }
+        }
+        if (n0 + t < N) {
+#pragma unroll
+            for (int lt = 0; lt < 4; ++lt)
+                *(f4 *)(dqh + (size_t)(n0 + t) * D + 16 * lt + 4 * h) = acc[lt] * so;
+        }
+    }
+    // dk^: key tiles rs in {w, 7-w}; lane column s = 16 rs + r16
+    for (int pick = 0; pick < 2; ++pick) {
+        const int rs = pick ? 7 - w : w;
+        const int s = 16 * rs + r16;
+        const h8 KB0 = ld8(sm.krow + sw64(s, 8 * h)), KB1 = ld8(sm.krow + sw64(s, 32 + 8 * h));
+        const h8 VB0 = ld8(sm.vrow + sw64(s, 8 * h)), VB1 = ld8(sm.vrow + sw64(s, 32 + 8 * h));
+        // P^T[t][s] of query tile tt: lane (column s, rows t = 16 tt + 4h + i)
+        auto pttile = [&](int tt) -> h4 {
+            f4 S = {0.f, 0.f, 0.f, 0.f}, A = {0.f, 0.f, 0.f, 0.f};
+            S = mfma(ld8(sm.qrow + sw64(16 * tt + r16, 8 * h)), KB0, S);
+            S = mfma(ld8(sm.qrow + sw64(16 * tt + r16, 32 + 8 * h)), KB1, S);
+            A = mfma(ld8(sm.urow + sw64(16 * tt + r16, 8 * h)), VB0, A);
+            A = mfma(ld8(sm.urow + sw64(16 * tt + r16, 32 + 8 * h)), VB1, A);
+            f4 P;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float ct = sm.cc[16 * tt + 4 * h + i];
+                float pv = (1.0f + S[i]) * fmaf(A[i], sa, -ct) * sp;
+                if (tt == rs && 4 * h + i < r16) pv = 0.f;
+                P[i] = pv;
+            }
+            return cvt4(P);
+        };
+        f4 acc[4];
+#pragma unroll
+        for (int lt = 0; lt < 4; ++lt) acc[lt] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int a = rs; a < 8; a += 2) {
+            const int b = a + 1;
+            const h4 pa = pttile(a);
+            const h4 pb = b < 8 ? pttile(b) : z4;
+            const h8 B = cat(pa, pb);
+#pragma unroll
+            for (int lt = 0; lt < 4; ++lt) {
+                const h4 qa = ld4(sm.qT + sw128(16 * lt + r16, 16 * a + 4 * h));
+                const h4 qb = b < 8 ? ld4(sm.qT + sw128(16 * lt + r16, 16 * b + 4 * h)) : z4;
+                acc[lt] = mfma(cat(qa, qb), B, acc[lt]);
+            }
+        }
+        if (n0 + s < N) {
+#pragma unroll
+            for (int lt = 0; lt < 4; ++lt)
+                *(f4 *)(dkh + (size_t)(n0 + s) * D + 16 * lt + 4 * h) = acc[lt] * so;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// bwd_mg_scan: (head, 16-column output tile L); four waves, one per SIMD, each
+// holding X3[m][l in L][j] for its 16 channels m = 16w.. as 64 accumulator
+// tiles (rows j, columns l) in registers.
+
+constexpr int MG_NW = 4;
+constexpr int MG_NTH = MG_NW * 64;
+
+struct GSmem {
+    _Float16 xrow[C * RS64];      // x^ [t][m] of the chunk being contracted
+    _Float16 zrow[C * RS64];      // z * 2^-ez [t][j]
+    _Float16 yT[2][D * RS128];    // y^ [m][s], by parity of the processing step
+    _Float16 wT[2][D * RS128];    // w * 2^-ew [j][s]
+    _Float16 wDh[2][C];           // w_D * 2^-eD [s]
+    float zD[C];                  // z_D * 2^(eD - ew - ez) [t]
+    float fpart[MG_NW * 4 * C * 4];   // [wave][row quad][t][4]
+    float m1g[16];                // sum_s w_D y^_sl (units 2^-eD), l in L
+    f4 ex[MG_NW][3][64];          // the extra accumulator tiles, between uses
+};
+
+template <int DIR>
+__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scan(const bf16_t *__restrict__ x,
+                                                         const bf16_t *__restrict__ y,
+                                                         const bf16_t *__restrict__ z,
+                                                         const bf16_t *__restrict__ wv,
+                                                         const float *__restrict__ rg,
+                                                         const float *__restrict__ cc,
+                                                         const float *__restrict__ hmax,
+                                                         float *__restrict__ dxh, int N, int BH)
+{
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    GSmem &sm = *reinterpret_cast<GSmem *>(smem_raw);
+
+    // the four output tiles of a head on one XCD (shared x, y, z, w rows in L2)
+    const int nblk = gridDim.x, b = blockIdx.x;
+    int head, L;
+    if ((nblk & 31) == 0) {
+        const int xcd = b & 7, idx = b >> 3;
+        L = idx & 3;
+        head = (idx >> 2) * 8 + xcd;
+    } else {
+        head = b >> 2;
+        L = b & 3;
+    }
+    if (head >= BH) return;
+    const size_t hb = (size_t)head * N;
+    x += hb * D;
+    y += hb * D;
+    z += hb * D;
+    wv += hb * D;
+    rg += hb;
+    cc += hb;
+    dxh += hb * D;
+
+    // roles: DIR 0 (dq^): z = u (row scale 1/G), z_D = -c, w = v, w_D = 1;
+    //        DIR 1 (dk^): z = v, z_D = 1, w = u, w_D = -c.
+    const HeadMax hm = head_max(hmax, head);
+    const float zmax = DIR ? hm.v : hm.u, wmax = DIR ? hm.u : hm.v;
+    const float wdmax = DIR ? hm.c : 1.0f;
+    const int ew = pow2_exponent(64.0f * (float)N * wmax);
+    const int ez = pow2_exponent(zmax);
+    const int ed = pow2_exponent(64.0f * (float)N * wdmax);
+    const float sw = ldexpf(1.0f, -ew), sz = ldexpf(1.0f, -ez), sd = ldexpf(1.0f, -ed);
+    const float szd = ldexpf(1.0f, ed - ew - ez), sout = ldexpf(1.0f, ew + ez);
+
+    int tid = threadIdx.x;
+    const int w = tid >> 6;
+    int lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    auto refresh_ids = [&]() {
+        asm volatile("" : "+v"(tid));
+        lane = tid & 63;
+        r16 = lane & 15;
+        h = lane >> 4;
+    };
+
+    f4 acc[16][4];
+#pragma unroll
+    for (int m = 0; m < 16; ++m)
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) acc[m][jt] = f4{0.f, 0.f, 0.f, 0.f};
+    // extra tiles: wave 0 M1 (j tiles 0,1) and M1G; wave 1 M1 (j tiles 2,3);
+    // waves 2,3 X3G = sum_s w_D y^_sm y^_sl for m tiles 2(w-2), 2(w-2)+1
+    // (kept in LDS between uses so that the 64 main tiles fill the AGPRs)
+#pragma unroll
+    for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = f4{0.f, 0.f, 0.f, 0.f};
+
+    const int nch = (N + C - 1) / C;
+    auto chunk_of = [&](int kk) { return DIR ? nch - 1 - kk : kk; };
+
+    // staging of chunk c in two halves pr: lanes of an octet share a token;
+    // a thread takes tokens 64pr + 2tg, +1 (tg = tid/8), channels 8(tid%8)..
+    uint4 px[2], py[2], pz[2], pw[2];
+    float prg[2], pcc[2];
+    auto prefetch = [&](int c, int pr) {
+        const uint4 zero = {0u, 0u, 0u, 0u};
+        const int tg = tid >> 3, cg = tid & 7;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int t = 64 * pr + 2 * tg + e;
+            const int n = c * C + t;
+            px[e] = py[e] = pz[e] = pw[e] = zero;
+            prg[e] = pcc[e] = 0.f;
+            if (n < N) {
+                px[e] = *(const uint4 *)(x + (size_t)n * D + 8 * cg);
+                py[e] = *(const uint4 *)(y + (size_t)n * D + 8 * cg);
+                pz[e] = *(const uint4 *)(z + (size_t)n * D + 8 * cg);
+                pw[e] = *(const uint4 *)(wv + (size_t)n * D + 8 * cg);
+                prg[e] = rg[n];
+                pcc[e] = cc[n];
+            }
+        }
+    };
+    auto stage = [&](int c, int buf, int pr) {
+        const int tg = tid >> 3, cg = tid & 7;
+        {
+            h8 hy[2], hw[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int e = j;
+                const int t = 64 * pr + 2 * tg + j;
+                const bool valid = c * C + t < N;
+                float f[8];
+                bf16x8_to_f32(px[e], f);
+                *(h8 *)(sm.xrow + sw64(t, 8 * cg)) = standardise8(f, valid);
+                bf16x8_to_f32(py[e], f);
+                hy[j] = standardise8(f, valid);
+                const float zs = (DIR ? 1.0f : prg[e]) * sz;
+                const float ws = (DIR ? prg[e] : 1.0f) * sw;
+                bf16x8_to_f32(pz[e], f);
+                h8 hz;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) hz[i] = (_Float16)(f[i] * zs);
+                *(h8 *)(sm.zrow + sw64(t, 8 * cg)) = hz;
+                bf16x8_to_f32(pw[e], f);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) hw[j][i] = (_Float16)(f[i] * ws);
+                if (cg == 0) {
+                    const float zd = DIR ? 1.0f : -pcc[e];
+                    const float wd = DIR ? -pcc[e] : 1.0f;
+                    sm.zD[t] = valid ? zd * szd : 0.f;
+                    sm.wDh[buf][t] = (_Float16)(valid ? wd * sd : 0.f);
+                }
+            }
+            const int t0 = 64 * pr + 2 * tg;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                *(h2 *)(sm.yT[buf] + sw128(8 * cg + i, t0)) = h2{hy[0][i], hy[1][i]};
+                *(h2 *)(sm.wT[buf] + sw128(8 * cg + i, t0)) = h2{hw[0][i], hw[1][i]};
+            }
+        }
+    };
+
+    for (int pr = 0; pr < 2; ++pr) {
+        prefetch(chunk_of(0), pr);
+        stage(chunk_of(0), 0, pr);
+    }
+    __syncthreads();
+
+    for (int kk = 0; kk < nch; ++kk) {
+        const int c = chunk_of(kk);
+        const int cur = kk & 1;
+        const bool more = kk + 1 < nch;
+        __builtin_amdgcn_sched_barrier(0);
+        refresh_ids();
+        // ---- (A) contraction of chunk c with the moments of earlier chunks --
+        if (kk > 0) {
+            if (w == 0 && h == 0) sm.m1g[r16] = sm.ex[0][2][lane][0];
+            // two passes over the wave's channels m = 16w + 8mh .. +7; the
+            // partial sums of the first pass wait in this wave's LDS slot
+#pragma unroll
+            for (int mh = 0; mh < 2; ++mh) {
+                h8 Ast[8][2];
+#pragma unroll
+                for (int mm = 0; mm < 8; ++mm)
+#pragma unroll
+                    for (int p = 0; p < 2; ++p)
+                        Ast[mm][p] = cat(cvt4(acc[8 * mh + mm][2 * p]), cvt4(acc[8 * mh + mm][2 * p + 1]));
+                h8 Aex = {0, 0, 0, 0, 0, 0, 0, 0};
+                if (mh == 1) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
+#pragma unroll 1
+                for (int rt = 0; rt < C / 16; ++rt) {
+                    const int t = 16 * rt + r16;
+                    const h8 xv = ld8(sm.xrow + sw64(t, 16 * w + 8 * mh));
+                    h8 Zb[2];
+#pragma unroll
+                    for (int p = 0; p < 2; ++p)
+                        Zb[p] = cat(ld4(sm.zrow + sw64(t, 32 * p + 4 * h)),
+                                    ld4(sm.zrow + sw64(t, 32 * p + 16 + 4 * h)));
+                    f4 *slot = (f4 *)(sm.fpart + ((w * 4 + h) * C + t) * 4);
+                    f4 Dout = {0.f, 0.f, 0.f, 0.f};
+                    if (mh == 1) Dout = *slot;
+#pragma unroll
+                    for (int mm = 0; mm < 8; ++mm) {
+                        f4 E = {0.f, 0.f, 0.f, 0.f};
+                        E = mfma(Ast[mm][0], Zb[0], E);
+                        E = mfma(Ast[mm][1], Zb[1], E);
+                        const float xm = (float)xv[mm];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) Dout[i] = fmaf(xm, E[i], Dout[i]);
+                    }
+                    if (mh == 1) {
+                        const float zd = sm.zD[t];
+                        if (w < 2) {
+                            Dout = mfma(Aex, Zb[w], Dout);
+                            if (w == 0) {
+#pragma unroll
+                                for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, sm.m1g[4 * h + i], Dout[i]);
+                            }
+                        } else {
+                            const h8 Xb = cat(ld4(sm.xrow + sw64(t, 32 * (w - 2) + 4 * h)),
+                                              ld4(sm.xrow + sw64(t, 32 * (w - 2) + 16 + 4 * h)));
+                            f4 Eg = {0.f, 0.f, 0.f, 0.f};
+                            Eg = mfma(Aex, Xb, Eg);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, Eg[i], Dout[i]);
+                        }
+                    }
+                    *slot = Dout;
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- (B) add chunk c's contribution, update the moments with chunk c,
+        //          stage the next chunk ----------------------------------------
+        __builtin_amdgcn_sched_barrier(0);
+        refresh_ids();
+        if (kk > 0) {
+            const int t = tid & (C - 1), half = tid >> 7;
+            const int n = c * C + t;
+            if (n < N) {
+#pragma unroll
+                for (int qq = 0; qq < 2; ++qq) {
+                    const int qd = 2 * half + qq;
+                    f4 F = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int ww = 0; ww < MG_NW; ++ww)
+                        F += *(const f4 *)(sm.fpart + ((ww * 4 + qd) * C + t) * 4);
+                    f4 *dst = (f4 *)(dxh + (size_t)n * D + 16 * L + 4 * qd);
+                    *dst = *dst + F * sout;
+                }
+            }
+        }
+        {
+            const _Float16 *yTc = sm.yT[cur];
+            const _Float16 *wTc = sm.wT[cur];
+            // moments += chunk c, 32 tokens per K step; the next chunk is
+            // staged in two halves behind K steps 0-1 and 2-3
+#pragma unroll 1
+            for (int ks = 0; ks < C / 32; ++ks) {
+                if ((ks & 1) == 0 && more) prefetch(chunk_of(kk + 1), ks >> 1);
+                const int col = 32 * ks + 8 * h;
+                h8 Aw[4];
+#pragma unroll
+                for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(wTc + sw128(16 * jt + r16, col));
+                const h8 Yl = ld8(yTc + sw128(16 * L + r16, col));
+#pragma unroll
+                for (int m = 0; m < 16; ++m) {
+                    const h8 Ym = ld8(yTc + sw128(16 * w + m, col));
+                    const h8 Bm = Ym * Yl;
+#pragma unroll
+                    for (int jt = 0; jt < 4; ++jt) acc[m][jt] = mfma(Aw[jt], Bm, acc[m][jt]);
+                }
+                const h8 WD = ld8(sm.wDh[cur] + col);
+                f4 ex[3];
+#pragma unroll
+                for (int e = 0; e < 3; ++e) ex[e] = sm.ex[w][e][lane];
+                if (w == 0) {
+                    ex[0] = mfma(Aw[0], Yl, ex[0]);
+                    ex[1] = mfma(Aw[1], Yl, ex[1]);
+                    const h8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+                    ex[2] = mfma(r16 == 0 ? WD : zero8, Yl, ex[2]);
+                } else if (w == 1) {
+                    ex[0] = mfma(Aw[2], Yl, ex[0]);
+                    ex[1] = mfma(Aw[3], Yl, ex[1]);
+                } else {
+                    const h8 YW = Yl * WD;
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int mt = 2 * (w - 2) + e;
+                        ex[e] = mfma(ld8(yTc + sw128(16 * mt + r16, col)), YW, ex[e]);
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = ex[e];
+                if ((ks & 1) == 1 && more) stage(chunk_of(kk + 1), cur ^ 1, ks >> 1);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// bwd_finish: dx = (dx^ - mean dx^ - x^ mean(dx^ x^)) / std, an octet per row.
+
+__global__ __launch_bounds__(256) void bwd_finish(const bf16_t *__restrict__ q,
+                                                  const bf16_t *__restrict__ k,
+                                                  const float *__restrict__ dqh,
+                                                  const float *__restrict__ dkh,
+                                                  bf16_t *__restrict__ dq, bf16_t *__restrict__ dk,
+                                                  size_t rows)
+{
+    const size_t r = (size_t)blockIdx.x * 32 + (threadIdx.x >> 3);
+    const int cg = threadIdx.x & 7;
+    const bool valid = r < rows;
+    for (int which = 0; which < 2; ++which) {
+        const bf16_t *xs = which ? k : q;
+        const float *dh = which ? dkh : dqh;
+        bf16_t *dx = which ? dk : dq;
+        float xv[8] = {}, d[8] = {};
+        if (valid) {
+            bf16x8_to_f32(*(const uint4 *)(xs + r * D + 8 * cg), xv);
+            const f4 a = *(const f4 *)(dh + r * D + 8 * cg);
+            const f4 bq = *(const f4 *)(dh + r * D + 8 * cg + 4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                d[i] = a[i];
+                d[4 + i] = bq[i];
+            }
+        }
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += xv[i];
+        const float mu = octet_sum(s) * (1.0f / D);
+        float var = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            xv[i] -= mu;
+            var = fmaf(xv[i], xv[i], var);
+        }
+        const float rs = valid ? __builtin_amdgcn_rsqf(octet_sum(var) * (1.0f / D)) : 0.f;
+        float m1 = 0.f, m2 = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            xv[i] *= rs;
+            m1 += d[i];
+            m2 = fmaf(d[i], xv[i], m2);
+        }
+        m1 = octet_sum(m1) * (1.0f / D);
+        m2 = octet_sum(m2) * (1.0f / D);
+        if (valid) {
+            uint4 o;
+            uint32_t *ow = (uint32_t *)&o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                ow[i] = pack_bf16x2((d[2 * i] - m1 - xv[2 * i] * m2) * rs,
+                                    (d[2 * i + 1] - m1 - xv[2 * i + 1] * m2) * rs);
+            *(uint4 *)(dx + r * D + 8 * cg) = o;
+        }
+    }
+}
+
+}  // namespace mfma_bwd
+
+size_t mfma_causal_bwd_workspace(int BH, int N)
+{
+    const size_t rows = (size_t)BH * N;
+    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    return a256(rows * 4) * 2 + a256((size_t)BH * 16) + 2 * a256(rows * mx::D * 4);
+}
+
+hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
+                           const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                           int N, void *ws, hipStream_t st)
+{
+    using namespace mfma_bwd;
+    static_assert(sizeof(ISmem) <= 160 * 1024 && sizeof(GSmem) <= 160 * 1024, "LDS budget");
+    const size_t rows = (size_t)BH * N;
+    const int nch = (N + C - 1) / C;
+    if ((long long)BH * nch > INT_MAX || (long long)BH * 4 > INT_MAX ||
+        (rows + 31) / 32 > (size_t)INT_MAX)
+        return hipErrorInvalidConfiguration;
+    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    unsigned char *p = (unsigned char *)ws;
+    float *rg = (float *)p;
+    p += a256(rows * 4);
+    float *cc = (float *)p;
+    p += a256(rows * 4);
+    float *hmax = (float *)p;
+    p += a256((size_t)BH * 16);
+    float *dqh = (float *)p;
+    p += a256(rows * D * 4);
+    float *dkh = (float *)p;
+
+    const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
+    const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
+    hipLaunchKernelGGL(bwd_prep, dim3(BH), dim3(256), 0, st, O, DO, V, g, rg, cc, hmax, N);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = mfma_causal_dv(q, k, dout, rg, dv, BH, N, st);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute((const void *)bwd_intra, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)sizeof(ISmem));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(256), sizeof(ISmem), st, Q, K, V, DO, rg,
+                       cc, hmax, dqh, dkh, N, nch);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    for (int dir = 0; dir < 2; ++dir) {
+        const void *fn = dir ? (const void *)bwd_mg_scan<1> : (const void *)bwd_mg_scan<0>;
+        e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)sizeof(GSmem));
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(bwd_mg_scan<0>, dim3(BH * 4), dim3(MG_NTH), sizeof(GSmem), st, Q, K, DO,
+                       V, rg, cc, hmax, dqh, N, BH);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_mg_scan<1>, dim3(BH * 4), dim3(MG_NTH), sizeof(GSmem), st, K, Q, V,
+                       DO, rg, cc, hmax, dkh, N, BH);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q, K,
+                       dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows);
+    return hipGetLastError();
+}
+
+}  // namespace fm

@@ -63,10 +63,18 @@ struct Smem {
     float red[NW];
 };
 
+// DV = false: the forward O = F / G.  DV = true: the reverse-causal
+// numerator of the backward, dv_n = sum_{i >= n} f(k^_n . q^_i) u_i with
+// u_i = dO_i / G_i (Sec. 2.5): the scan runs over the tokens in reverse order
+// (logical token n is row N-1-n), q and k trade roles (the caller passes k as
+// q and q as k), v is dO scaled per row by rg = 1/G, and F is stored without
+// the divide; the denominator terms are skipped.
+template <bool DV>
 __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                                          const bf16_t *__restrict__ k,
                                          const bf16_t *__restrict__ v, bf16_t *__restrict__ out,
-                                         float *__restrict__ g, int N, int sl, int vexp)
+                                         float *__restrict__ g, const float *__restrict__ rg,
+                                         int N, int sl, int vexp)
 {
     const int w = threadIdx.x >> 6;    // wave
     const bool has_lin = w < 4;
@@ -105,6 +113,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
     };
 
     uint4 pq[2], pk[2], pv;
+    float prg = 1.0f;   // DV: 1/G of the v row
     auto prefetch = [&](int c) {
         const uint4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -112,13 +121,18 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
             const int n = c * C + 2 * tg + j;
             pq[j] = pk[j] = z;
             if (n < N) {
-                pq[j] = *(const uint4 *)(q + (size_t)n * D + 8 * cg);
-                pk[j] = *(const uint4 *)(k + (size_t)n * D + 8 * cg);
+                const size_t pn = DV ? (size_t)(N - 1 - n) : (size_t)n;
+                pq[j] = *(const uint4 *)(q + pn * D + 8 * cg);
+                pk[j] = *(const uint4 *)(k + pn * D + 8 * cg);
             }
         }
         const int nv = c * C + vt;
         pv = z;
-        if (tid < 2 * C && nv < N) pv = *(const uint4 *)(v + (size_t)nv * D + SL * sl + 8 * vh);
+        if (tid < 2 * C && nv < N) {
+            const size_t pn = DV ? (size_t)(N - 1 - nv) : (size_t)nv;
+            pv = *(const uint4 *)(v + pn * D + SL * sl + 8 * vh);
+            if constexpr (DV) prg = rg[pn];
+        }
     };
     // Staging of chunk c (Sec. 2.2, Eqs. 6-7): standardise q and k rows, store
     // q^, k^ (row-major), k^ transposed and the scaled v transposed.
@@ -148,9 +162,10 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
         if (tid < 2 * C) {
             float xv[8];
             bf16x8_to_f32(pv, xv);
+            const float vs = DV ? vscale * prg : vscale;
 #pragma unroll
             for (int i = 0; i < 8; ++i)
-                sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vscale);
+                sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vs);
         }
     };
 
@@ -225,7 +240,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 const int ibase = (rt / 2) * (rt / 2 + 1) + ((rt & 1) ? rt / 2 + 1 : 0);
                 const int first = (w - ibase % NW + NW) % NW;   // first item j of this wave
                 float gpart = 0.f;
-                if (first <= rt / 2 || rt == w) {
+                if (first <= rt / 2 || (!DV && rt == w)) {
                     const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
                     const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
                     auto wtile = [&](int tt) -> h4 {
@@ -254,7 +269,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                         }
                         F0 = mfma(cat(va, vb), cat(wa, wb), F0);
                     }
-                    if (rt == w) {
+                    if (!DV && rt == w) {
                         // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
                         float gq = 0.f;
                         const float ys = ldexpf(2.0f, -gexp);
@@ -278,7 +293,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
             }
             // this chunk's sums of k^ (for y2, waves 0-3) and of scaled v (x1, wave 4)
-            if (w < 4) {
+            if (!DV && w < 4) {
                 const int m = 16 * w + r16;
                 float s = 0.f;
 #pragma unroll
@@ -311,12 +326,13 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 Gi += sm.gpart[ww * C + tok];
             }
             if (n0 + tok < N) {
-                const float sc = oscale * __builtin_amdgcn_rcpf(Gi);
+                const float sc = DV ? oscale : oscale * __builtin_amdgcn_rcpf(Gi);
                 uint2 o;
                 o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
                 o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
-                *(uint2 *)(out + (size_t)(n0 + tok) * D + SL * sl + 4 * cq) = o;
-                if (g && sl == 0 && cq == 0) g[n0 + tok] = Gi;
+                const size_t pn = DV ? (size_t)(N - 1 - (n0 + tok)) : (size_t)(n0 + tok);
+                *(uint2 *)(out + pn * D + SL * sl + 4 * cq) = o;
+                if (!DV && g && sl == 0 && cq == 0) g[n0 + tok] = Gi;
             }
             // prefixes for the next chunk
             if (tid < D) sm.y2[nxt][tid] = sm.y2[cur][tid] + sm.y2c[tid];
@@ -350,7 +366,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
                 });
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk)
-                    if (kk < ny3)
+                    if (!DV && kk < ny3)
                         y3acc[kk] = mfma(ld8(kTc + sw128(16 * y3u[kk] + r16, 32 * s + 8 * h)),
                                          ld8(kTc + sw128(16 * y3u2[kk] + r16, 32 * s + 8 * h)),
                                          y3acc[kk]);
@@ -366,7 +382,7 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
             const float gs = ldexpf(1.0f, -gnext);
 #pragma unroll
             for (int kk = 0; kk < 2; ++kk) {
-                if (kk >= ny3) break;
+                if (DV || kk >= ny3) break;
                 const int u = y3u[kk], u2 = y3u2[kk];
                 // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
                 const int mcol = 16 * u2 + r16;
@@ -385,11 +401,14 @@ __device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
     }
 }
 
+template <bool DV>
 __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__restrict__ q,
                                                             const bf16_t *__restrict__ k,
                                                             const bf16_t *__restrict__ v,
                                                             bf16_t *__restrict__ out,
-                                                            float *__restrict__ g, int N, int BH)
+                                                            float *__restrict__ g,
+                                                            const float *__restrict__ rg, int N,
+                                                            int BH)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
@@ -415,6 +434,7 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
     v += hb;
     out += hb;
     if (g) g += (size_t)head * N;
+    if (rg) rg += (size_t)head * N;
 
     // max |v| over this slice -> power-of-two scale
     const int tid = threadIdx.x;
@@ -423,8 +443,9 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
         const int n = p >> 1, hh = p & 1;
         float x[8];
         bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh), x);
+        const float r = DV ? fabsf(rg[n]) : 1.0f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]));
+        for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * r);
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
@@ -438,7 +459,7 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
     for (int w = 0; w < NW; ++w) vmax = fmaxf(vmax, sm.red[w]);
     const int vexp = pow2_exponent(vmax * 63.0f * (float)N);
 
-    run_scan(sm, q, k, v, out, g, N, sl, vexp);
+    run_scan<DV>(sm, q, k, v, out, g, rg, N, sl, vexp);
 }
 
 }  // namespace mfma_causal
@@ -451,11 +472,27 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
     using namespace mfma_causal;
     static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
     const size_t smem = sizeof(Smem);
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel<false>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fwd_causal_kernel, dim3(BH * NSL), dim3(NTH), smem, st, (const bf16_t *)q,
-                       (const bf16_t *)k, (const bf16_t *)v, (bf16_t *)out, g, N, BH);
+    hipLaunchKernelGGL(fwd_causal_kernel<false>, dim3(BH * NSL), dim3(NTH), smem, st,
+                       (const bf16_t *)q, (const bf16_t *)k, (const bf16_t *)v, (bf16_t *)out, g,
+                       (const float *)nullptr, N, BH);
+    return hipGetLastError();
+}
+
+hipError_t mfma_causal_dv(const void *q, const void *k, const void *dout, const float *rg,
+                          void *dv, int BH, int N, hipStream_t st)
+{
+    using namespace mfma_causal;
+    const size_t smem = sizeof(Smem);
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel<true>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    // queries of this scan are the keys k (and vice versa), values dO / G
+    hipLaunchKernelGGL(fwd_causal_kernel<true>, dim3(BH * NSL), dim3(NTH), smem, st,
+                       (const bf16_t *)k, (const bf16_t *)q, (const bf16_t *)dout, (bf16_t *)dv,
+                       (float *)nullptr, rg, N, BH);
     return hipGetLastError();
 }
 

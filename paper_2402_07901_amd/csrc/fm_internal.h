@@ -18,6 +18,16 @@ size_t generic_bwd_workspace(int B, int H, int N, int D);
 hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
                            int BH, int N, hipStream_t st);
 size_t mfma_causal_smem_bytes();
+// The causal scan run in reverse on (k, q, dO / G) without the divide: dv.
+hipError_t mfma_causal_dv(const void *q, const void *k, const void *dout, const float *rg,
+                          void *dv, int BH, int N, hipStream_t st);
+
+// MFMA causal backward: D = 64, p = 2, bf16 I/O.  ws holds
+// mfma_causal_bwd_workspace(BH, N) bytes.
+hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
+                           const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                           int N, void *ws, hipStream_t st);
+size_t mfma_causal_bwd_workspace(int BH, int N);
 
 // MFMA non-causal path: D = 64, p = 2, bf16 I/O (moment build, segment
 // reduction, query contraction).  ws holds mfma_nc_workspace(BH, N) bytes.

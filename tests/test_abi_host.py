@@ -134,7 +134,8 @@ def test_workspace_bytes():
                 for dt in (fm.F32, fm.BF16):
                     nf = fm.workspace_bytes(2, 3, 100, D, p, causal, dt, False)
                     nb = fm.workspace_bytes(2, 3, 100, D, p, causal, dt, True)
-                    assert nf >= 0 and nb >= 4 * 2 * 3 * 100 * (3 * D + 1)
+                    # fp32 dq^ and dk^ plus two floats per row, on every path
+                    assert nf >= 0 and nb >= 4 * 2 * 3 * 100 * (2 * D + 2)
     assert fm.workspace_bytes(0, 1, 1, 64, 2, 1, fm.BF16, True) == 0
     assert fm.workspace_bytes(1, 1, 1, 65, 2, 1, fm.BF16, True) == 0
 

@@ -138,3 +138,59 @@ def test_constant_v_full_size(name):
     nk = (torch.arange(1, w.N + 1, device="cuda", dtype=torch.float32) if w.causal
           else torch.full((w.N,), float(w.N), device="cuda"))
     assert bool((g >= nk / 2 * (1 - 1e-5)).all())
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 129), (1, 2, 300), (2, 1, 777)])
+def test_bwd_multi_chunk_vs_brute(shape):
+    """Causal backward across several 128-token chunks (the moment scans in
+    both directions) with ragged tails, against the fp64 explicit backward."""
+    from test_parity_gpu import bwd_case
+    B, H, N = shape
+    label = f"mfma bwd B={B} H={H} N={N}"
+    say(label)
+    inp = make_inputs(B, H, N, 64, 700 + N, "bf16", with_dout=True)
+    bwd_case(inp, 2, True, "bf16", label=label)
+
+
+@pytest.mark.parametrize("ev,ed", [(-40, 0), (40, 0), (0, -40), (0, 40)])
+def test_bwd_value_scale_extremes(ev, ed):
+    """v and dO scaled by powers of two (exact in bf16): the gradients scale
+    accordingly and the per-head fp16 scales must follow."""
+    from test_parity_gpu import bwd_case
+    label = f"mfma bwd v*2^{ev} dO*2^{ed}"
+    say(label)
+    inp = make_inputs(1, 1, 400, 64, 800, "bf16", with_dout=True)
+    inp = with_v_scaled(inp, ev)
+    d32 = (inp["dout64"] * 2.0 ** ed).astype(np.float32)
+    inp["dout"] = f32_to_bf16_bits(d32)
+    inp["dout64"] = bf16_bits_to_f64(inp["dout"])
+    bwd_case(inp, 2, True, "bf16", label=label)
+
+
+def test_bwd_single_token():
+    """N = 1: O_1 = v_1 whatever q and k are, so dq = dk = 0 exactly and
+    dv = dO.  The computed dq, dk are pure rounding of u~ . v' = u.v - c
+    (exactly 0); they are bounded by the size of the terms that cancel,
+    eps (1 + |s|) sum_j |u_j v_j| max|k^| / std(q) with eps = 2e-2."""
+    import torch
+    inp = make_inputs(1, 3, 1, 64, 901, "bf16", with_dout=True)
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "dout"))
+    o, g = fm.fastmax_fwd(q, k, v, p=2, causal=True)
+    dq, dk, dv = fm.fastmax_bwd(q, k, v, o, do, g, p=2, causal=True)
+    torch.cuda.synchronize()
+    e = max_rel(to_f64(dv), inp["dout64"])
+    say(f"N=1: E(dv vs dO)={e:.3e}")
+    assert e <= TOL["bf16"]
+    for hh in range(3):
+        qq, kk_, vv, dd = (inp[n][0, hh, 0] for n in ("q64", "k64", "v64", "dout64"))
+        qh = (qq - qq.mean()) / qq.std()
+        kh = (kk_ - kk_.mean()) / kk_.std()
+        s = float(qh @ kh)
+        G = 1.0 + s + s * s / 2.0
+        mag = (1.0 + abs(s)) * float(np.abs(dd / G * vv).sum())
+        bq = 2e-2 * mag * np.abs(kh).max() / qq.std()
+        bk = 2e-2 * mag * np.abs(qh).max() / kk_.std()
+        aq = float(np.abs(to_f64(dq)[0, hh, 0]).max())
+        ak = float(np.abs(to_f64(dk)[0, hh, 0]).max())
+        say(f"N=1 head {hh}: |dq|={aq:.3e} (bound {bq:.3e}) |dk|={ak:.3e} (bound {bk:.3e})")
+        assert aq <= bq and ak <= bk
