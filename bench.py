@@ -41,6 +41,18 @@ def fwd_flops(B, H, N, D, p):
     return 4.0 * n_features(D, p) * (D + 1) * B * H * N
 
 
+def bwd_flops(B, H, N, D, p):
+    """Algorithmic backward flops (moment form of the custom gradient), per
+    token per head 2 x [P(D+1) forward state + D^2(D+1) dq contraction
+    + P(D+1) reverse state (symmetric in q (x) q) + D^2(D+1) dk contraction
+    + P D reverse dv state + P D dv contraction]; p = 2 only."""
+    if p != 2:
+        return None
+    P = n_features(D, p)
+    per = 2 * (2 * P * (D + 1) + 2 * D * D * (D + 1) + 2 * P * D)
+    return float(per) * B * H * N
+
+
 def source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2402_07901_amd", "csrc")
@@ -235,8 +247,16 @@ def main():
                      "algorithmic_flops_per_launch": flops},
     }
     if args.mode == "fwdbwd":
-        rec["backward"] = {"avg_ms": sum(bwd_ms) / len(bwd_ms),
+        bms = sum(bwd_ms) / len(bwd_ms)
+        bf = bwd_flops(w.B, w.H, w.N, w.D, w.p)
+        rec["backward"] = {"avg_ms": bms,
                            "note": "fastmax_bwd call (all its kernels), HIP events on the stream"}
+        if bf is not None and w.dtype == "bf16":
+            ach = bf / (bms / 1e3) / 1e12
+            rec["backward"].update({"algorithmic_flops_per_call": bf, "achieved": ach,
+                                    "unit": "TFLOP/s", "bound": "mfma",
+                                    "peak": PEAK[("mfma", "bf16")],
+                                    "frac": ach / PEAK[("mfma", "bf16")]})
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(rec), flush=True)

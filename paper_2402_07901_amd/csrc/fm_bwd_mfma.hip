@@ -41,17 +41,18 @@ using namespace mx;
 constexpr int C = 128;   // tokens per chunk
 
 // ---------------------------------------------------------------------------
-// bwd_prep: one workgroup per head, octets of lanes per token.
+// bwd_prep: one workgroup per (head, 128-token chunk), an octet of lanes per
+// token; per-chunk maxima go to pmax[head][chunk][4].
 
 __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ o,
                                                 const bf16_t *__restrict__ dout,
                                                 const bf16_t *__restrict__ v,
                                                 const float *__restrict__ g,
                                                 float *__restrict__ rg, float *__restrict__ cc,
-                                                float *__restrict__ hmax, int N)
+                                                float *__restrict__ pmax, int N, int nch)
 {
     __shared__ float red[3][4];
-    const int head = blockIdx.x, tid = threadIdx.x;
+    const int head = blockIdx.x / nch, c = blockIdx.x % nch, tid = threadIdx.x;
     const size_t hb = (size_t)head * N;
     o += hb * D;
     dout += hb * D;
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ o,
     cc += hb;
     const int oc = tid >> 3, cg = tid & 7;
     float umax = 0.f, vmax = 0.f, cmax = 0.f;
-    for (int n0 = 0; n0 < N; n0 += 32) {
+    for (int n0 = c * C; n0 < min(N, (c + 1) * C); n0 += 32) {
         const int n = n0 + oc;
         const bool valid = n < N;
         float xo[8] = {}, xd[8] = {}, xv[8] = {};
@@ -103,17 +104,24 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ o,
     if (tid < 3) {
         float m = 0.f;
         for (int w = 0; w < 4; ++w) m = fmaxf(m, red[tid][w]);
-        hmax[(size_t)head * 4 + tid] = m;
+        pmax[((size_t)head * nch + c) * 4 + tid] = m;
     }
 }
 
-// per-head maxima: [0] max|u|, [1] max|v|, [2] max|c|
+// per-head maxima over the chunks: [0] max|u|, [1] max|v|, [2] max|c|
 struct HeadMax {
     float u, v, c;
 };
-__device__ __forceinline__ HeadMax head_max(const float *hmax, int head)
+__device__ __forceinline__ HeadMax head_max(const float *pmax, int head, int nch)
 {
-    return HeadMax{hmax[(size_t)head * 4], hmax[(size_t)head * 4 + 1], hmax[(size_t)head * 4 + 2]};
+    HeadMax r{0.f, 0.f, 0.f};
+    const float *p = pmax + (size_t)head * nch * 4;
+    for (int c = 0; c < nch; ++c) {
+        r.u = fmaxf(r.u, p[4 * c]);
+        r.v = fmaxf(r.v, p[4 * c + 1]);
+        r.c = fmaxf(r.c, p[4 * c + 2]);
+    }
+    return r;
 }
 
 // ---------------------------------------------------------------------------
@@ -153,7 +161,7 @@ __global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
     dqh += hb * D;
     dkh += hb * D;
 
-    const HeadMax hm = head_max(hmax, head);
+    const HeadMax hm = head_max(hmax, head, nch);
     const int ev = pow2_exponent(hm.v), eu = pow2_exponent(hm.u);
     // |P| <= 65 (64 max|v| max|u| + max|c|)
     const int ep = pow2_exponent(65.0f * fmaf(64.0f * hm.v, hm.u, hm.c));
@@ -309,20 +317,18 @@ struct GSmem {
 };
 
 template <int DIR>
-__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scan(const bf16_t *__restrict__ x,
-                                                         const bf16_t *__restrict__ y,
-                                                         const bf16_t *__restrict__ z,
-                                                         const bf16_t *__restrict__ wv,
-                                                         const float *__restrict__ rg,
-                                                         const float *__restrict__ cc,
-                                                         const float *__restrict__ hmax,
-                                                         float *__restrict__ dxh, int N, int BH)
+__device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
+                                        const bf16_t *__restrict__ x,
+                                        const bf16_t *__restrict__ y,
+                                        const bf16_t *__restrict__ z,
+                                        const bf16_t *__restrict__ wv,
+                                        const float *__restrict__ rg,
+                                        const float *__restrict__ cc,
+                                        const float *__restrict__ hmax, float *__restrict__ dxh,
+                                        int N, int BH)
 {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    GSmem &sm = *reinterpret_cast<GSmem *>(smem_raw);
-
-    // the four output tiles of a head on one XCD (shared x, y, z, w rows in L2)
-    const int nblk = gridDim.x, b = blockIdx.x;
+    // the four output tiles of a head on one XCD (shared x, y, z, w rows in L2);
+    // b counts from the first block of this scan, whose id is a multiple of 8
     int head, L;
     if ((nblk & 31) == 0) {
         const int xcd = b & 7, idx = b >> 3;
@@ -344,7 +350,7 @@ __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scan(const bf16_t *__restric
 
     // roles: DIR 0 (dq^): z = u (row scale 1/G), z_D = -c, w = v, w_D = 1;
     //        DIR 1 (dk^): z = v, z_D = 1, w = u, w_D = -c.
-    const HeadMax hm = head_max(hmax, head);
+    const HeadMax hm = head_max(hmax, head, (N + C - 1) / C);
     const float zmax = DIR ? hm.v : hm.u, wmax = DIR ? hm.u : hm.v;
     const float wdmax = DIR ? hm.c : 1.0f;
     const int ew = pow2_exponent(64.0f * (float)N * wmax);
@@ -491,7 +497,11 @@ __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scan(const bf16_t *__restric
                     if (mh == 1) {
                         const float zd = sm.zD[t];
                         if (w < 2) {
-                            Dout = mfma(Aex, Zb[w], Dout);
+                            // z at this wave's M1 column pair (loaded: a runtime
+                            // index into Zb would become a chain of selects)
+                            const h8 Zw = cat(ld4(sm.zrow + sw64(t, 32 * w + 4 * h)),
+                                              ld4(sm.zrow + sw64(t, 32 * w + 16 + 4 * h)));
+                            Dout = mfma(Aex, Zw, Dout);
                             if (w == 0) {
 #pragma unroll
                                 for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, sm.m1g[4 * h + i], Dout[i]);
@@ -580,6 +590,28 @@ __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scan(const bf16_t *__restric
     }
 }
 
+// Both scans in one launch: blocks [0, 4BH) build dq^ (chunks in order),
+// blocks [4BH, 8BH) build dk^ (chunks in reverse order).
+__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const bf16_t *__restrict__ q,
+                                                          const bf16_t *__restrict__ k,
+                                                          const bf16_t *__restrict__ v,
+                                                          const bf16_t *__restrict__ dout,
+                                                          const float *__restrict__ rg,
+                                                          const float *__restrict__ cc,
+                                                          const float *__restrict__ hmax,
+                                                          float *__restrict__ dqh,
+                                                          float *__restrict__ dkh, int N, int BH)
+{
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    GSmem &sm = *reinterpret_cast<GSmem *>(smem_raw);
+    const int half = 4 * BH;
+    const int b = blockIdx.x;
+    if (b < half)
+        mg_scan<0>(sm, b, half, q, k, dout, v, rg, cc, hmax, dqh, N, BH);
+    else
+        mg_scan<1>(sm, b - half, half, k, q, v, dout, rg, cc, hmax, dkh, N, BH);
+}
+
 // ---------------------------------------------------------------------------
 // bwd_finish: dx = (dx^ - mean dx^ - x^ mean(dx^ x^)) / std, an octet per row.
 
@@ -646,7 +678,8 @@ size_t mfma_causal_bwd_workspace(int BH, int N)
 {
     const size_t rows = (size_t)BH * N;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return a256(rows * 4) * 2 + a256((size_t)BH * 16) + 2 * a256(rows * mx::D * 4);
+    const size_t nch = ((size_t)N + mfma_bwd::C - 1) / mfma_bwd::C;
+    return a256(rows * 4) * 2 + a256((size_t)BH * nch * 16) + 2 * a256(rows * mx::D * 4);
 }
 
 hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
@@ -657,7 +690,7 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     static_assert(sizeof(ISmem) <= 160 * 1024 && sizeof(GSmem) <= 160 * 1024, "LDS budget");
     const size_t rows = (size_t)BH * N;
     const int nch = (N + C - 1) / C;
-    if ((long long)BH * nch > INT_MAX || (long long)BH * 4 > INT_MAX ||
+    if ((long long)BH * nch > INT_MAX || (long long)BH * 8 > INT_MAX ||
         (rows + 31) / 32 > (size_t)INT_MAX)
         return hipErrorInvalidConfiguration;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -667,14 +700,15 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     float *cc = (float *)p;
     p += a256(rows * 4);
     float *hmax = (float *)p;
-    p += a256((size_t)BH * 16);
+    p += a256((size_t)BH * nch * 16);
     float *dqh = (float *)p;
     p += a256(rows * D * 4);
     float *dkh = (float *)p;
 
     const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
     const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
-    hipLaunchKernelGGL(bwd_prep, dim3(BH), dim3(256), 0, st, O, DO, V, g, rg, cc, hmax, N);
+    hipLaunchKernelGGL(bwd_prep, dim3(BH * nch), dim3(256), 0, st, O, DO, V, g, rg, cc, hmax, N,
+                       nch);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = mfma_causal_dv(q, k, dout, rg, dv, BH, N, st);
@@ -686,18 +720,11 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                        cc, hmax, dqh, dkh, N, nch);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    for (int dir = 0; dir < 2; ++dir) {
-        const void *fn = dir ? (const void *)bwd_mg_scan<1> : (const void *)bwd_mg_scan<0>;
-        e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)sizeof(GSmem));
-        if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(bwd_mg_scan<0>, dim3(BH * 4), dim3(MG_NTH), sizeof(GSmem), st, Q, K, DO,
-                       V, rg, cc, hmax, dqh, N, BH);
-    e = hipGetLastError();
+    e = hipFuncSetAttribute((const void *)bwd_mg_scans,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_mg_scan<1>, dim3(BH * 4), dim3(MG_NTH), sizeof(GSmem), st, K, Q, V,
-                       DO, rg, cc, hmax, dkh, N, BH);
+    hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, Q, K, V, DO,
+                       rg, cc, hmax, dqh, dkh, N, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q, K,
