@@ -256,7 +256,8 @@ def main():
             rec["backward"].update({"algorithmic_flops_per_call": bf, "achieved": ach,
                                     "unit": "TFLOP/s", "bound": "mfma",
                                     "peak": PEAK[("mfma", "bf16")],
-                                    "frac": ach / PEAK[("mfma", "bf16")]})
+                                    "frac": ach / PEAK[("mfma", "bf16")],
+                                    "traffic": load_traffic("fastmax_bwd", w.name)})
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(rec), flush=True)
