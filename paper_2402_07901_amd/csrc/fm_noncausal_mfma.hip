@@ -394,8 +394,10 @@ __global__ __launch_bounds__(512) void nc_reduce(const float *__restrict__ part,
 
 struct QSmem {
     float fpart[2][NW * NCT * 4 * QS * 4];   // [buf][wave][tile][row quad][token][4]
-    float gpart[2][4 * QS];                  // [buf][channel tile][token]
+    float gpart[2][16 * QS];                 // [buf][channel tile][row quad][token]
     _Float16 qrow[2][QS * RS64];             // q^ [token][m], double-buffered by step parity
+    _Float16 qperm[2][QS * RS64];            // q^ [token][8 (m % 8) + m / 8]: a wave's channels
+                                             // m = w + 8 idx are one 16-byte load
     _Float16 y3h[D * RS64];                  // scaled Y3
     float hdr[HDR];
 };
@@ -458,8 +460,11 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
     auto stage = [&](int s, int buf) {
         float x[8];
         bf16x8_to_f32(pq, x);
-        const int row = tid >> 3;
-        *(h8 *)(sm.qrow[buf] + sw64(row, 8 * (tid & 7))) = standardise8(x, tok0 + s * QS + row < tok1);
+        const int row = tid >> 3, cg = tid & 7;
+        const h8 hq = standardise8(x, tok0 + s * QS + row < tok1);
+        *(h8 *)(sm.qrow[buf] + sw64(row, 8 * cg)) = hq;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sm.qperm[buf][sw64(row, 8 * i + cg)] = hq[i];
     };
     const float Nf = (float)N;
     auto combine = [&](int s) {
@@ -473,7 +478,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
             F += *(const f4 *)(sm.fpart[buf] + (((ww * NCT + ct) * 4 + hq) * QS + tk) * 4);
         float gq = 0.f;
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc) gq += sm.gpart[buf][cc * QS + tk];
+        for (int k = 0; k < 16; ++k) gq += sm.gpart[buf][k * QS + tk];
         const float G = fmaf(sm.hdr[2 * D + NCT], gq, Nf);
         if (n < tok1) {
             const float sc = sm.hdr[2 * D + ct] * __builtin_amdgcn_rcpf(G);
@@ -505,9 +510,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
 #pragma unroll
             for (int u = 0; u < 4; ++u) myl[u] = ld4(qr + sw64(tk, 16 * u + 4 * h));
             const h4 mylin = ld4(qr + sw64(tk, 16 * (w & 3) + 4 * h));
-            _Float16 qm[8];
-#pragma unroll
-            for (int idx = 0; idx < 8; ++idx) qm[idx] = qr[sw64(tk, w + 8 * idx)];
+            const h8 qm = ld8(sm.qperm[buf] + sw64(tk, 8 * w));
             f4 F[NCT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) F[ct] = f4{0.f, 0.f, 0.f, 0.f};
@@ -544,9 +547,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
                 float gq = 0.f;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) gq = fmaf((float)ql[i], T[i], gq);
-                gq += __shfl_xor(gq, 16);
-                gq += __shfl_xor(gq, 32);
-                if (h == 0) sm.gpart[buf][cc * QS + tk] = gq;
+                sm.gpart[buf][(4 * cc + h) * QS + tk] = gq;
             }
         }
         if (s > 0) combine(s - 1);
