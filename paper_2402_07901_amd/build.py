@@ -35,12 +35,8 @@ def sources():
     return out
 
 
-# Per-source extra flags.  The backward moment scan keeps a 256-register fp32
-# state per lane; with MFMA results selected into VGPRs (AGPRs then serve as
-# overflow) it allocates without spilling.
-EXTRA = {
-    "fm_bwd_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-}
+# Per-source extra compiler flags (none needed at present).
+EXTRA = {}
 
 
 def _compile(src: str) -> str:

@@ -297,23 +297,24 @@ __global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
 }
 
 // ---------------------------------------------------------------------------
-// bwd_mg_scan: (head, 16-column output tile L); four waves, one per SIMD, each
-// holding X3[m][l in L][j] for its 16 channels m = 16w.. as 64 accumulator
-// tiles (rows j, columns l) in registers.
+// bwd_mg_scan: (head, 16-column output tile L); eight waves, two per SIMD,
+// each holding X3[m][l in L][j] for its 8 channels m = 8w.. as 32
+// accumulator tiles (rows j, columns l) in registers.
 
-constexpr int MG_NW = 4;
+constexpr int MG_NW = 8;
 constexpr int MG_NTH = MG_NW * 64;
+constexpr int MG_MPW = D / MG_NW;   // channels per wave
 
 struct GSmem {
     _Float16 xrow[C * RS64];      // x^ [t][m] of the chunk being contracted
     _Float16 zrow[C * RS64];      // z * 2^-ez [t][j]
-    _Float16 yT[2][D * RS128];    // y^ [m][s], by parity of the processing step
-    _Float16 wT[2][D * RS128];    // w * 2^-ew [j][s]
-    _Float16 wDh[2][C];           // w_D * 2^-eD [s]
+    _Float16 yT[D * RS128];       // y^ [m][s] of the chunk added to the moments
+    _Float16 wT[D * RS128];       // w * 2^-ew [j][s]
+    _Float16 wDh[C];              // w_D * 2^-eD [s]
     float zD[C];                  // z_D * 2^(eD - ew - ez) [t]
     float fpart[MG_NW * 4 * C * 4];   // [wave][row quad][t][4]
     float m1g[16];                // sum_s w_D y^_sl (units 2^-eD), l in L
-    f4 ex[MG_NW][3][64];          // the extra accumulator tiles, between uses
+    f4 ex[4][3][64];              // the extra accumulator tiles of waves 0-3, between uses
 };
 
 template <int DIR>
@@ -369,31 +370,32 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         h = lane >> 4;
     };
 
-    f4 acc[16][4];
+    f4 acc[MG_MPW][4];
 #pragma unroll
-    for (int m = 0; m < 16; ++m)
+    for (int m = 0; m < MG_MPW; ++m)
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) acc[m][jt] = f4{0.f, 0.f, 0.f, 0.f};
-    // extra tiles: wave 0 M1 (j tiles 0,1) and M1G; wave 1 M1 (j tiles 2,3);
-    // waves 2,3 X3G = sum_s w_D y^_sm y^_sl for m tiles 2(w-2), 2(w-2)+1
-    // (kept in LDS between uses so that the 64 main tiles fill the AGPRs)
+    // extra tiles (waves 0-3): wave 0 M1 (j tiles 0,1) and M1G; wave 1 M1 (j
+    // tiles 2,3); waves 2,3 X3G = sum_s w_D y^_sm y^_sl for m tiles 2(w-2),
+    // 2(w-2)+1; kept in LDS between uses
+    if (w < 4) {
 #pragma unroll
-    for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = f4{0.f, 0.f, 0.f, 0.f};
+    }
 
     const int nch = (N + C - 1) / C;
     auto chunk_of = [&](int kk) { return DIR ? nch - 1 - kk : kk; };
 
-    // staging of chunk c in two halves pr: lanes of an octet share a token;
-    // a thread takes tokens 64pr + 2tg, +1 (tg = tid/8), channels 8(tid%8)..
+    // staging of chunk c: lanes of an octet share a token; a thread takes
+    // tokens 2tg, 2tg+1 (tg = tid/8), channels 8(tid%8)..
     uint4 px[2], py[2], pz[2], pw[2];
     float prg[2], pcc[2];
-    auto prefetch = [&](int c, int pr) {
+    auto prefetch = [&](int c) {
         const uint4 zero = {0u, 0u, 0u, 0u};
         const int tg = tid >> 3, cg = tid & 7;
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-            const int t = 64 * pr + 2 * tg + e;
-            const int n = c * C + t;
+            const int n = c * C + 2 * tg + e;
             px[e] = py[e] = pz[e] = pw[e] = zero;
             prg[e] = pcc[e] = 0.f;
             if (n < N) {
@@ -406,77 +408,78 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
             }
         }
     };
-    auto stage = [&](int c, int buf, int pr) {
+    // the output side (x^ rows, scaled z rows, z_D)
+    auto stage_xz = [&](int c) {
         const int tg = tid >> 3, cg = tid & 7;
-        {
-            h8 hy[2], hw[2];
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int e = j;
-                const int t = 64 * pr + 2 * tg + j;
-                const bool valid = c * C + t < N;
-                float f[8];
-                bf16x8_to_f32(px[e], f);
-                *(h8 *)(sm.xrow + sw64(t, 8 * cg)) = standardise8(f, valid);
-                bf16x8_to_f32(py[e], f);
-                hy[j] = standardise8(f, valid);
-                const float zs = (DIR ? 1.0f : prg[e]) * sz;
-                const float ws = (DIR ? prg[e] : 1.0f) * sw;
-                bf16x8_to_f32(pz[e], f);
-                h8 hz;
+        for (int e = 0; e < 2; ++e) {
+            const int t = 2 * tg + e;
+            const bool valid = c * C + t < N;
+            float f[8];
+            bf16x8_to_f32(px[e], f);
+            *(h8 *)(sm.xrow + sw64(t, 8 * cg)) = standardise8(f, valid);
+            const float zs = (DIR ? 1.0f : prg[e]) * sz;
+            bf16x8_to_f32(pz[e], f);
+            h8 hz;
 #pragma unroll
-                for (int i = 0; i < 8; ++i) hz[i] = (_Float16)(f[i] * zs);
-                *(h8 *)(sm.zrow + sw64(t, 8 * cg)) = hz;
-                bf16x8_to_f32(pw[e], f);
+            for (int i = 0; i < 8; ++i) hz[i] = (_Float16)(f[i] * zs);
+            *(h8 *)(sm.zrow + sw64(t, 8 * cg)) = hz;
+            if (cg == 0) sm.zD[t] = valid ? (DIR ? 1.0f : -pcc[e]) * szd : 0.f;
+        }
+    };
+    // the summed side (y^ and scaled w transposed, w_D)
+    auto stage_yw = [&](int c) {
+        const int tg = tid >> 3, cg = tid & 7;
+        h8 hy[2], hw[2];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) hw[j][i] = (_Float16)(f[i] * ws);
-                if (cg == 0) {
-                    const float zd = DIR ? 1.0f : -pcc[e];
-                    const float wd = DIR ? -pcc[e] : 1.0f;
-                    sm.zD[t] = valid ? zd * szd : 0.f;
-                    sm.wDh[buf][t] = (_Float16)(valid ? wd * sd : 0.f);
-                }
-            }
-            const int t0 = 64 * pr + 2 * tg;
+        for (int e = 0; e < 2; ++e) {
+            const int t = 2 * tg + e;
+            const bool valid = c * C + t < N;
+            float f[8];
+            bf16x8_to_f32(py[e], f);
+            hy[e] = standardise8(f, valid);
+            const float ws = (DIR ? prg[e] : 1.0f) * sw;
+            bf16x8_to_f32(pw[e], f);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                *(h2 *)(sm.yT[buf] + sw128(8 * cg + i, t0)) = h2{hy[0][i], hy[1][i]};
-                *(h2 *)(sm.wT[buf] + sw128(8 * cg + i, t0)) = h2{hw[0][i], hw[1][i]};
-            }
+            for (int i = 0; i < 8; ++i) hw[e][i] = (_Float16)(f[i] * ws);
+            if (cg == 0) sm.wDh[t] = (_Float16)(valid ? (DIR ? -pcc[e] : 1.0f) * sd : 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            *(h2 *)(sm.yT + sw128(8 * cg + i, 2 * tg)) = h2{hy[0][i], hy[1][i]};
+            *(h2 *)(sm.wT + sw128(8 * cg + i, 2 * tg)) = h2{hw[0][i], hw[1][i]};
         }
     };
 
-    for (int pr = 0; pr < 2; ++pr) {
-        prefetch(chunk_of(0), pr);
-        stage(chunk_of(0), 0, pr);
-    }
+    prefetch(chunk_of(0));
+    stage_xz(chunk_of(0));
+    stage_yw(chunk_of(0));
     __syncthreads();
 
     for (int kk = 0; kk < nch; ++kk) {
         const int c = chunk_of(kk);
-        const int cur = kk & 1;
         const bool more = kk + 1 < nch;
         __builtin_amdgcn_sched_barrier(0);
         refresh_ids();
         // ---- (A) contraction of chunk c with the moments of earlier chunks --
         if (kk > 0) {
             if (w == 0 && h == 0) sm.m1g[r16] = sm.ex[0][2][lane][0];
-            // two passes over the wave's channels m = 16w + 8mh .. +7; the
+            // two passes over the wave's channels m = 8w + 4mh .. +3; the
             // partial sums of the first pass wait in this wave's LDS slot
 #pragma unroll
             for (int mh = 0; mh < 2; ++mh) {
-                h8 Ast[8][2];
+                h8 Ast[4][2];
 #pragma unroll
-                for (int mm = 0; mm < 8; ++mm)
+                for (int mm = 0; mm < 4; ++mm)
 #pragma unroll
                     for (int p = 0; p < 2; ++p)
-                        Ast[mm][p] = cat(cvt4(acc[8 * mh + mm][2 * p]), cvt4(acc[8 * mh + mm][2 * p + 1]));
+                        Ast[mm][p] = cat(cvt4(acc[4 * mh + mm][2 * p]), cvt4(acc[4 * mh + mm][2 * p + 1]));
                 h8 Aex = {0, 0, 0, 0, 0, 0, 0, 0};
-                if (mh == 1) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
+                if (mh == 1 && w < 4) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
 #pragma unroll 1
                 for (int rt = 0; rt < C / 16; ++rt) {
                     const int t = 16 * rt + r16;
-                    const h8 xv = ld8(sm.xrow + sw64(t, 16 * w + 8 * mh));
+                    const h4 xv = ld4(sm.xrow + sw64(t, MG_MPW * w + 4 * mh));
                     h8 Zb[2];
 #pragma unroll
                     for (int p = 0; p < 2; ++p)
@@ -486,7 +489,7 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
                     f4 Dout = {0.f, 0.f, 0.f, 0.f};
                     if (mh == 1) Dout = *slot;
 #pragma unroll
-                    for (int mm = 0; mm < 8; ++mm) {
+                    for (int mm = 0; mm < 4; ++mm) {
                         f4 E = {0.f, 0.f, 0.f, 0.f};
                         E = mfma(Ast[mm][0], Zb[0], E);
                         E = mfma(Ast[mm][1], Zb[1], E);
@@ -494,11 +497,10 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
 #pragma unroll
                         for (int i = 0; i < 4; ++i) Dout[i] = fmaf(xm, E[i], Dout[i]);
                     }
-                    if (mh == 1) {
+                    if (mh == 1 && w < 4) {
                         const float zd = sm.zD[t];
                         if (w < 2) {
-                            // z at this wave's M1 column pair (loaded: a runtime
-                            // index into Zb would become a chain of selects)
+                            // z at this wave's M1 column pair
                             const h8 Zw = cat(ld4(sm.zrow + sw64(t, 32 * w + 4 * h)),
                                               ld4(sm.zrow + sw64(t, 32 * w + 16 + 4 * h)));
                             Dout = mfma(Aex, Zw, Dout);
@@ -522,71 +524,71 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         __syncthreads();
 
         // ---- (B) add chunk c's contribution, update the moments with chunk c,
-        //          stage the next chunk ----------------------------------------
+        //          stage the output side of the next chunk ----------------------
         __builtin_amdgcn_sched_barrier(0);
         refresh_ids();
         if (kk > 0) {
-            const int t = tid & (C - 1), half = tid >> 7;
+            const int t = tid & (C - 1), qd = tid >> 7;
             const int n = c * C + t;
             if (n < N) {
+                f4 F = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int qq = 0; qq < 2; ++qq) {
-                    const int qd = 2 * half + qq;
-                    f4 F = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int ww = 0; ww < MG_NW; ++ww)
-                        F += *(const f4 *)(sm.fpart + ((ww * 4 + qd) * C + t) * 4);
-                    f4 *dst = (f4 *)(dxh + (size_t)n * D + 16 * L + 4 * qd);
-                    *dst = *dst + F * sout;
-                }
+                for (int ww = 0; ww < MG_NW; ++ww)
+                    F += *(const f4 *)(sm.fpart + ((ww * 4 + qd) * C + t) * 4);
+                f4 *dst = (f4 *)(dxh + (size_t)n * D + 16 * L + 4 * qd);
+                *dst = *dst + F * sout;
             }
         }
+        if (more) prefetch(chunk_of(kk + 1));
         {
-            const _Float16 *yTc = sm.yT[cur];
-            const _Float16 *wTc = sm.wT[cur];
-            // moments += chunk c, 32 tokens per K step; the next chunk is
-            // staged in two halves behind K steps 0-1 and 2-3
+            // moments += chunk c, 32 tokens per K step
 #pragma unroll 1
             for (int ks = 0; ks < C / 32; ++ks) {
-                if ((ks & 1) == 0 && more) prefetch(chunk_of(kk + 1), ks >> 1);
                 const int col = 32 * ks + 8 * h;
                 h8 Aw[4];
 #pragma unroll
-                for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(wTc + sw128(16 * jt + r16, col));
-                const h8 Yl = ld8(yTc + sw128(16 * L + r16, col));
+                for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(sm.wT + sw128(16 * jt + r16, col));
+                const h8 Yl = ld8(sm.yT + sw128(16 * L + r16, col));
 #pragma unroll
-                for (int m = 0; m < 16; ++m) {
-                    const h8 Ym = ld8(yTc + sw128(16 * w + m, col));
+                for (int m = 0; m < MG_MPW; ++m) {
+                    const h8 Ym = ld8(sm.yT + sw128(MG_MPW * w + m, col));
                     const h8 Bm = Ym * Yl;
 #pragma unroll
                     for (int jt = 0; jt < 4; ++jt) acc[m][jt] = mfma(Aw[jt], Bm, acc[m][jt]);
                 }
-                const h8 WD = ld8(sm.wDh[cur] + col);
-                f4 ex[3];
+                if (w < 4) {
+                    const h8 WD = ld8(sm.wDh + col);
+                    f4 ex[3];
 #pragma unroll
-                for (int e = 0; e < 3; ++e) ex[e] = sm.ex[w][e][lane];
-                if (w == 0) {
-                    ex[0] = mfma(Aw[0], Yl, ex[0]);
-                    ex[1] = mfma(Aw[1], Yl, ex[1]);
-                    const h8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
-                    ex[2] = mfma(r16 == 0 ? WD : zero8, Yl, ex[2]);
-                } else if (w == 1) {
-                    ex[0] = mfma(Aw[2], Yl, ex[0]);
-                    ex[1] = mfma(Aw[3], Yl, ex[1]);
-                } else {
-                    const h8 YW = Yl * WD;
+                    for (int e = 0; e < 3; ++e) ex[e] = sm.ex[w][e][lane];
+                    if (w == 0) {
+                        ex[0] = mfma(Aw[0], Yl, ex[0]);
+                        ex[1] = mfma(Aw[1], Yl, ex[1]);
+                        const h8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+                        ex[2] = mfma(r16 == 0 ? WD : zero8, Yl, ex[2]);
+                    } else if (w == 1) {
+                        ex[0] = mfma(Aw[2], Yl, ex[0]);
+                        ex[1] = mfma(Aw[3], Yl, ex[1]);
+                    } else {
+                        const h8 YW = Yl * WD;
 #pragma unroll
-                    for (int e = 0; e < 2; ++e) {
-                        const int mt = 2 * (w - 2) + e;
-                        ex[e] = mfma(ld8(yTc + sw128(16 * mt + r16, col)), YW, ex[e]);
+                        for (int e = 0; e < 2; ++e) {
+                            const int mt = 2 * (w - 2) + e;
+                            ex[e] = mfma(ld8(sm.yT + sw128(16 * mt + r16, col)), YW, ex[e]);
+                        }
                     }
-                }
 #pragma unroll
-                for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = ex[e];
-                if ((ks & 1) == 1 && more) stage(chunk_of(kk + 1), cur ^ 1, ks >> 1);
+                    for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = ex[e];
+                }
             }
         }
+        if (more) stage_xz(chunk_of(kk + 1));
         __syncthreads();
+        // ---- (C) stage the summed side of the next chunk (after the update) ---
+        if (more) {
+            stage_yw(chunk_of(kk + 1));
+            __syncthreads();
+        }
     }
 }
 
