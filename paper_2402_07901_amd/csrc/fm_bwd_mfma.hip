@@ -125,7 +125,8 @@ __device__ __forceinline__ HeadMax head_max(const float *pmax, int head, int nch
 }
 
 // ---------------------------------------------------------------------------
-// bwd_intra: (head, chunk); four waves.
+// bwd_intra: (head, chunk); eight waves: 0-3 the dq^ row tiles, 4-7 the dk^
+// key tiles, two each ({v, 7-v}: 9 of the chunk's 36 tile pairs per wave).
 
 struct ISmem {
     _Float16 qrow[C * RS64];   // q^ [t][m]
@@ -137,7 +138,7 @@ struct ISmem {
     float cc[C];
 };
 
-__global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
+__global__ __launch_bounds__(512) void bwd_intra(const bf16_t *__restrict__ q,
                                                  const bf16_t *__restrict__ k,
                                                  const bf16_t *__restrict__ v,
                                                  const bf16_t *__restrict__ dout,
@@ -172,8 +173,8 @@ __global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
     // staging: four passes of 32 tokens, an octet of lanes per token
     {
         const int oc = tid >> 3, cg = tid & 7;
-        for (int pass = 0; pass < 4; ++pass) {
-            const int t = 32 * pass + oc, n = n0 + t;
+        for (int pass = 0; pass < 2; ++pass) {
+            const int t = 64 * pass + oc, n = n0 + t;
             const bool valid = n < N;
             float xq[8] = {}, xk[8] = {}, xv[8] = {}, xu[8] = {};
             float r = 0.f;
@@ -206,9 +207,11 @@ __global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
     __syncthreads();
 
     const h4 z4 = {0, 0, 0, 0};
-    // dq^: query tiles rt in {w, 7-w}; lane column t = 16 rt + r16
+    const int v4 = w & 3;
+    // dq^ (waves 0-3): query tiles rt in {v4, 7-v4}; lane column t = 16 rt + r16
+    if (w < 4)
     for (int pick = 0; pick < 2; ++pick) {
-        const int rt = pick ? 7 - w : w;
+        const int rt = pick ? 7 - v4 : v4;
         const int t = 16 * rt + r16;
         const float ct = sm.cc[t];
         const h8 QB0 = ld8(sm.qrow + sw64(t, 8 * h)), QB1 = ld8(sm.qrow + sw64(t, 32 + 8 * h));
@@ -250,9 +253,10 @@ __global__ __launch_bounds__(256) void bwd_intra(const bf16_t *__restrict__ q,
                 *(f4 *)(dqh + (size_t)(n0 + t) * D + 16 * lt + 4 * h) = acc[lt] * so;
         }
     }
-    // dk^: key tiles rs in {w, 7-w}; lane column s = 16 rs + r16
+    // dk^ (waves 4-7): key tiles rs in {v4, 7-v4}; lane column s = 16 rs + r16
+    if (w >= 4)
     for (int pick = 0; pick < 2; ++pick) {
-        const int rs = pick ? 7 - w : w;
+        const int rs = pick ? 7 - v4 : v4;
         const int s = 16 * rs + r16;
         const h8 KB0 = ld8(sm.krow + sw64(s, 8 * h)), KB1 = ld8(sm.krow + sw64(s, 32 + 8 * h));
         const h8 VB0 = ld8(sm.vrow + sw64(s, 8 * h)), VB1 = ld8(sm.vrow + sw64(s, 32 + 8 * h));
@@ -718,7 +722,7 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     e = hipFuncSetAttribute((const void *)bwd_intra, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)sizeof(ISmem));
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(256), sizeof(ISmem), st, Q, K, V, DO, rg,
+    hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(512), sizeof(ISmem), st, Q, K, V, DO, rg,
                        cc, hmax, dqh, dkh, N, nch);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
