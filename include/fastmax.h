@@ -66,10 +66,13 @@ enum {
  * (backward = 1) needs for this problem.  0 means no workspace is needed
  * (NULL may then be passed).  Returns 0 as well for arguments the entry
  * point would reject.  The workspace need not be zeroed.  The forward needs
- * one when it splits the sequence into segments (non-causal, bf16, D = 64,
- * p = 2, N >= 128): per-segment partial moments, their fp16 sum and the per-head
- * denominator terms live there, about 0.7 MB per (head, segment) with at
- * most ceil(N / 128) segments and about 256 / (2 B H) of them per head.
+ * one when it splits each head's sequence into segments whose moment states
+ * are built in parallel: the non-causal bf16, D = 64, p = 2 path with
+ * N >= 128 (per-segment partial moments, their fp16 sum and the per-head
+ * denominator terms, about 0.7 MB per (head, segment)), and every other
+ * non-MFMA forward when B*H is small (fp32 segment states, enough segments
+ * for about 256 workgroups).  The causal bf16, D = 64, p = 2 forward needs
+ * none.
  */
 size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
                                fastmax_dtype_t dt, int backward);

@@ -35,14 +35,16 @@ bool mfma_noncausal(int N, int D, int p, int causal, fastmax_dtype_t dt)
     return D == 64 && p == 2 && !causal && dt == FASTMAX_BF16 && N >= 128;
 }
 
-size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
-{
-    return mfma_noncausal(N, D, p, causal, dt) ? fm::mfma_nc_workspace(B * H, N) : 0;
-}
-
 bool mfma_causal(int D, int p, int causal, fastmax_dtype_t dt)
 {
     return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
+}
+
+size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+{
+    if (mfma_causal(D, p, causal, dt)) return 0;
+    if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_workspace(B * H, N);
+    return fm::generic_fwd_workspace(B * H, N, D, p);
 }
 
 size_t bwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
@@ -81,7 +83,8 @@ int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g
     else if (mfma_noncausal(N, D, p, causal, dt))
         e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, workspace, stream);
     else
-        e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, stream);
+        e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, workspace,
+                            stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 

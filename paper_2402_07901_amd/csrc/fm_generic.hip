@@ -166,13 +166,63 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
 }
 
 // ---------------------------------------------------------------------------
-// Forward.  grid = (B*H, slices); slice s owns value columns [s*W, s*W+W)
-// plus the ones column (local index W), so every slice has G for its divide.
+// Forward.  grid = (B*H, slices, segments); slice s owns value columns
+// [s*W, s*W+W) plus the ones column (local index W), so every slice has G for
+// its divide.  With several segments (few heads), seg_state_kernel first
+// writes each segment's moment contribution to sseg; a causal segment starts
+// its scan from the sum of the earlier segments (the exclusive prefix of
+// Sec. 2.4's causal moments at the segment start), a non-causal one contracts
+// its queries against the sum of all segments.
 // ---------------------------------------------------------------------------
+template <int D, bool P2, int WS, typename T>
+__global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
+                                                       const T *__restrict__ v,
+                                                       float *__restrict__ sseg, int N, int cps)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int NPAIR = feat<D, P2>::NPAIR;
+    constexpr int W = WS - 1;
+    constexpr int DP = D + 1;
+
+    __shared__ float S[P * WS];
+    __shared__ float xk[CH * DP];
+    __shared__ float vv[CH * WS];
+    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+
+    const int head = blockIdx.x, c0 = blockIdx.y * W, seg = blockIdx.z;
+    const size_t hb = (size_t)head * N * D;
+    k += hb;
+    v += hb;
+    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    build_pairs<D, P2>(pm, pl);
+    __syncthreads();
+    const int nch = (N + CH - 1) / CH;
+    const int cb = seg * cps, ce = min(nch, cb + cps);
+    for (int c = cb; c < ce; ++c) {
+        load_std<D>(k, c * CH, N, xk, nullptr);
+        for (int e = threadIdx.x; e < CH * WS; e += NT) {
+            int r = e / WS, j = e % WS, n = c * CH + r;
+            float x = 0.0f;
+            if (n < N) {
+                if (j == W) x = 1.0f;
+                else if (c0 + j < D) x = io<T>::ld(v, (size_t)n * D + c0 + j);
+            }
+            vv[e] = x;
+        }
+        __syncthreads();
+        state_update<D, P2, WS>(S, xk, vv, pm, pl);
+        __syncthreads();
+    }
+    float *dst = sseg + (((size_t)head * gridDim.y + blockIdx.y) * gridDim.z + seg) * P * WS;
+    for (int e = threadIdx.x; e < P * WS; e += NT) dst[e] = S[e];
+}
+
 template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                  const T *__restrict__ v, T *__restrict__ out,
-                                                 float *__restrict__ g, int N)
+                                                 float *__restrict__ g, int N, int cps,
+                                                 const float *__restrict__ sseg)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -198,7 +248,18 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
     out += hb;
     if (g) g += (size_t)head * N;
 
-    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    const int nseg = gridDim.z, seg = blockIdx.z;
+    {
+        // initial state: the earlier segments (causal) or all of them
+        const float *src = sseg ? sseg + ((size_t)head * gridDim.y + blockIdx.y) * nseg * P * WS
+                                : nullptr;
+        const int upto = sseg ? (CAUSAL ? seg : nseg) : 0;
+        for (int e = threadIdx.x; e < P * WS; e += NT) {
+            float a = 0.0f;
+            for (int s2 = 0; s2 < upto; ++s2) a += src[(size_t)s2 * P * WS + e];
+            S[e] = a;
+        }
+    }
     build_pairs<D, P2>(pm, pl);
     __syncthreads();
 
@@ -225,15 +286,18 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
     };
 
     const int nch = (N + CH - 1) / CH;
+    const int cb = seg * cps, ce = min(nch, cb + cps);
     if (!CAUSAL) {
-        for (int c = 0; c < nch; ++c) {
-            load_std<D>(k, c * CH, N, xk, nullptr);
-            load_vals(c * CH);
-            __syncthreads();
-            state_update<D, P2, WS>(S, xk, vv, pm, pl);
-            __syncthreads();
+        if (!sseg) {
+            for (int c = 0; c < nch; ++c) {
+                load_std<D>(k, c * CH, N, xk, nullptr);
+                load_vals(c * CH);
+                __syncthreads();
+                state_update<D, P2, WS>(S, xk, vv, pm, pl);
+                __syncthreads();
+            }
         }
-        for (int c = 0; c < nch; ++c) {
+        for (int c = cb; c < ce; ++c) {
             load_std<D>(q, c * CH, N, xq, nullptr);
             for (int e = threadIdx.x; e < CH * WS; e += NT) F[e] = 0.0f;
             __syncthreads();
@@ -243,7 +307,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             __syncthreads();
         }
     } else {
-        for (int c = 0; c < nch; ++c) {
+        for (int c = cb; c < ce; ++c) {
             const int n0 = c * CH;
             load_std<D>(q, n0, N, xq, nullptr);
             load_std<D>(k, n0, N, xk, nullptr);
@@ -581,19 +645,52 @@ template <> struct slice_width<16, false> { static constexpr int v = 17; };
 template <> struct slice_width<32, false> { static constexpr int v = 33; };
 template <> struct slice_width<64, false> { static constexpr int v = 65; };
 
-template <int D, bool P2, typename T>
-static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void *out, float *g,
-                               int BH, int N, int causal, hipStream_t st)
+// Segments per head: enough workgroups for ~256 CUs, at most one per chunk.
+struct SegPlan {
+    int slices, nseg, cps;
+    size_t bytes;   // workspace for the segment states (0 with one segment)
+};
+template <int D, bool P2>
+SegPlan seg_plan(int BH, int N)
 {
     constexpr int WS = slice_width<D, P2>::v;
     constexpr int W = WS - 1;
-    dim3 grid(BH, (D + W - 1) / W);
+    SegPlan sp;
+    sp.slices = (D + W - 1) / W;
+    const int nch = (N + CH - 1) / CH;
+    long long want = 256 / ((long long)BH * sp.slices);
+    if (want < 1) want = 1;
+    if (want > nch) want = nch;
+    if (want > 65535) want = 65535;
+    sp.cps = (int)((nch + want - 1) / want);
+    sp.nseg = (nch + sp.cps - 1) / sp.cps;
+    sp.bytes = sp.nseg > 1 ? (size_t)BH * sp.slices * sp.nseg * feat<D, P2>::P * WS * sizeof(float)
+                           : 0;
+    return sp;
+}
+
+template <int D, bool P2, typename T>
+static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void *out, float *g,
+                               int BH, int N, int causal, void *ws, hipStream_t st)
+{
+    constexpr int WS = slice_width<D, P2>::v;
+    const SegPlan sp = seg_plan<D, P2>(BH, N);
+    dim3 grid(BH, sp.slices, sp.nseg);
+    float *sseg = sp.nseg > 1 ? (float *)ws : nullptr;
+    if (sseg) {
+        hipLaunchKernelGGL((seg_state_kernel<D, P2, WS, T>), grid, dim3(NT), 0, st, (const T *)k,
+                           (const T *)v, sseg, N, sp.cps);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (causal)
         hipLaunchKernelGGL((fwd_kernel<D, P2, WS, true, T>), grid, dim3(NT), 0, st,
-                           (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N);
+                           (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N, sp.cps,
+                           (const float *)sseg);
     else
         hipLaunchKernelGGL((fwd_kernel<D, P2, WS, false, T>), grid, dim3(NT), 0, st,
-                           (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N);
+                           (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N, sp.cps,
+                           (const float *)sseg);
     return hipGetLastError();
 }
 
@@ -651,9 +748,17 @@ size_t generic_bwd_workspace(int B, int H, int N, int D)
 
 template <typename T>
 static hipError_t gen_fwd_t(const void *q, const void *k, const void *v, void *out, float *g,
-                            int BH, int N, int D, int p, int causal, hipStream_t st)
+                            int BH, int N, int D, int p, int causal, void *ws, hipStream_t st)
 {
-    return FM_DISPATCH_D_P(generic::fwd_dispatch, D, p, q, k, v, out, g, BH, N, causal, st);
+    return FM_DISPATCH_D_P(generic::fwd_dispatch, D, p, q, k, v, out, g, BH, N, causal, ws, st);
+}
+
+size_t generic_fwd_workspace(int BH, int N, int D, int p)
+{
+    using namespace generic;
+    if (D == 16) return p == 2 ? seg_plan<16, true>(BH, N).bytes : seg_plan<16, false>(BH, N).bytes;
+    if (D == 32) return p == 2 ? seg_plan<32, true>(BH, N).bytes : seg_plan<32, false>(BH, N).bytes;
+    return p == 2 ? seg_plan<64, true>(BH, N).bytes : seg_plan<64, false>(BH, N).bytes;
 }
 
 template <typename T>
@@ -666,10 +771,10 @@ static hipError_t gen_bwd_t(const void *q, const void *k, const void *v, const v
 }
 
 hipError_t generic_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, int D, int p, int causal, int is_bf16, hipStream_t st)
+                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st)
 {
-    if (is_bf16) return gen_fwd_t<bf16_t>(q, k, v, out, g, BH, N, D, p, causal, st);
-    return gen_fwd_t<float>(q, k, v, out, g, BH, N, D, p, causal, st);
+    if (is_bf16) return gen_fwd_t<bf16_t>(q, k, v, out, g, BH, N, D, p, causal, ws, st);
+    return gen_fwd_t<float>(q, k, v, out, g, BH, N, D, p, causal, ws, st);
 }
 
 hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *o,

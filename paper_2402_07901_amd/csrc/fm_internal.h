@@ -8,7 +8,10 @@ namespace fm {
 
 // Generic float32-VALU path: every (D, p, causal, dtype).
 hipError_t generic_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, int D, int p, int causal, int is_bf16, hipStream_t st);
+                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st);
+// Forward workspace of the generic path: per-segment moment states when a
+// head's sequence is split into segments (few heads), else 0.
+size_t generic_fwd_workspace(int BH, int N, int D, int p);
 hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *o,
                        const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
                        int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st);

@@ -112,13 +112,19 @@ def test_fwd_workspace_checks():
     assert fwd(causal=0, N=1000, H=2, ws=A + 4, wsb=need) == fm.EALIGN
     # sized for the whole problem: grows with the number of heads and tokens
     assert fm.workspace_bytes(1, 8, 131072, 64, 2, False, fm.BF16, False) > need
-    # the causal scan and the float32 / other-D paths need none
+    # the causal MFMA scan needs none
     assert fm.workspace_bytes(1, 2, 1000, 64, 2, True, fm.BF16, False) == 0
-    assert fm.workspace_bytes(1, 2, 1000, 64, 2, False, fm.F32, False) == 0
-    assert fm.workspace_bytes(1, 2, 1000, 32, 2, False, fm.BF16, False) == 0
-    # fewer keys than one 128-token chunk: the fp32 kernel, no workspace
-    assert fm.workspace_bytes(1, 2, 127, 64, 2, False, fm.BF16, False) == 0
+    # the generic kernels need segment states only when few heads must be
+    # spread over the CUs; with many heads (>= 256 workgroups) none
+    for D, p, causal, dt in ((64, 2, False, fm.F32), (32, 2, False, fm.BF16),
+                             (32, 1, True, fm.F32), (16, 2, True, fm.F32)):
+        assert fm.workspace_bytes(1, 2, 1000, D, p, causal, dt, False) > 0
+        assert fm.workspace_bytes(64, 8, 1000, D, p, causal, dt, False) == 0
+    # fewer keys than one 128-token chunk: the generic kernel (segment states)
+    assert fm.workspace_bytes(1, 2, 127, 64, 2, False, fm.BF16, False) > 0
     assert fm.workspace_bytes(1, 2, 128, 64, 2, False, fm.BF16, False) > 0
+    # a single 16-token chunk cannot be split
+    assert fm.workspace_bytes(1, 1, 16, 32, 2, True, fm.F32, False) == 0
 
 
 def test_bwd_rejects_bad_args():
