@@ -2,31 +2,31 @@
 //
 // Chunked causal scan (Sec. 2.4, causal moments "xcausal"/"ycausal" carried
 // across chunks of 128 tokens instead of per row).  One workgroup owns one
-// (batch, head, slice of 16 value columns); its eight waves hold the moment
-// state S[f][j] = sum_n phi_f(k^_n) v_nj of the slice as fp32 MFMA
-// accumulators for the whole sequence, so the state never touches HBM.
+// (batch, head, slice of 16 value columns) and keeps the moment state
+// S[f][j] = sum_n phi_f(k^_n) v_nj of the slice on chip for the whole
+// sequence; the state never touches HBM.
 //
-// Features: the 21-tile-per-wave pattern of fm_mfma.h (symmetric 16x16
-// tiles of k_m k_l plus the linear tiles); 84 accumulator registers per lane.
+// Two kinds of waves share each SIMD:
+//  * state waves 0..3 hold the state as fp16 MFMA operands (41 feature tiles
+//    of 16 rows each, 84 registers per lane) and do the two contractions
+//    against it: the query contraction F^T += S^T Psi(Q)^T (Psi generated in
+//    registers with packed fp16 multiplies) and the state update
+//    S += Phi(K)^T V;
+//  * helper waves 4..7 stage the next chunk (standardisation, Eqs. 6-7;
+//    transposes), compute the in-chunk block tril(f(Q K^T)) V on MFMA and
+//    the denominators G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sums,
+//    and combine the partial numerators into O = F / G.
+// Per chunk there are two phases separated by barriers: (1) query
+// contraction | in-chunk block and denominators; (2) state update | output,
+// prefix sums, Y3 update and staging of the next chunk.  The two kinds of
+// work overlap on each SIMD instead of running in lockstep.
 //
-// Per chunk:
-//  (i)  query contraction F^T += S^T Psi(Q)^T.  The accumulator layout of a
-//       16x16 MFMA tile (lane: column j, rows 4h..4h+3) is used directly as
-//       the A operand of the next MFMA by pairing two tiles per 32-wide K
-//       step (K index 8h+r <-> tile a row 4h+r, 8h+4+r <-> tile b row 4h+r);
-//       the Psi operand is generated in registers with packed fp16 multiplies
-//       in the same K order.  Each wave contracts its own tiles for all 128
-//       tokens; partial F^T go through LDS.
-//  (ii) in-chunk block tril(f(Q K^T)) V on MFMA, and the denominator
-//       G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sums, with Y3 = sum k k^T
-//       kept as 10 symmetric fp32 accumulator tiles.
-//  (iii) state update S += Phi(K)^T V per m: A = K^T tiles, B = diag(k_m) V
-//       generated with packed multiplies.
-//
-// Operands are fp16 (q^, k^ are standardised so |x| <= 8).  v is scaled by a
-// power of two 2^-e chosen per workgroup from max|v| so that every state
-// entry (bounded by N * 63 * max|v|) stays below 2^15; the output is scaled
-// back.  Y3 is converted with its own power of two per chunk.
+// State numerics.  The state lives in fp16 (v is pre-scaled by a power of two
+// 2^-e per workgroup so that no entry, bounded by N * 63 * max|v|, can exceed
+// 2^15).  Each update rebuilds a tile's fp32 accumulator exactly with one MFMA
+// against a 0/1 permutation matrix, adds the chunk's contribution in fp32 and
+// rounds back to fp16 once per chunk.  Diagonal tiles are stored halved (the
+// 1/2 of f_2), and rebuilt with a 0/2 matrix.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -43,364 +43,93 @@ using namespace mx;
 constexpr int C = 128;        // tokens per chunk
 constexpr int NRT = C / 16;   // 16-token row tiles per chunk
 constexpr int NKS2 = C / 32;  // 32-token K steps of the state update
-constexpr int NW = 8;         // waves per workgroup (2 per SIMD)
+constexpr int NSW = 4;        // state waves (one per SIMD)
+constexpr int NW = 8;         // waves per workgroup
 constexpr int NTH = NW * 64;
+constexpr int NHT = NTH - NSW * 64;  // helper threads
 constexpr int SL = 16;        // value columns per workgroup
 constexpr int NSL = D / SL;
 
+// Feature tiles of state wave w: tile 0 is the linear tile u = w (features
+// k_l, l = 16w..16w+15); then for the wave's channels m = w + 4i (i = 0..15)
+// the quadratic tiles (m, u) for u = i/4 .. 3 (m/16 == i/4 for every w < 4):
+// 1 + 4*(4+3+2+1) = 41 tiles; 164 over the four waves.
+constexpr int NQ = 16;
+__host__ __device__ constexpr int u0_of(int i) { return i / 4; }
+__host__ __device__ constexpr int first_tile(int i)
+{
+    int t = 1;
+    for (int j = 0; j < i; ++j) t += 4 - u0_of(j);
+    return t;
+}
+constexpr int NT = first_tile(NQ);    // 41
+constexpr int NKS = (NT + 1) / 2;     // 21 K steps of the query contraction
+struct Tile {
+    int kind;  // 0 linear, 1 quadratic, -1 padding
+    int i;     // channel m = w + 4i
+    int u;     // l tile
+};
+__host__ __device__ constexpr Tile tile_of(int t)
+{
+    if (t == 0) return Tile{0, -1, -1};
+    for (int i = 0; i < NQ; ++i)
+        if (t < first_tile(i) + 4 - u0_of(i)) return Tile{1, i, u0_of(i) + t - first_tile(i)};
+    return Tile{-1, -1, -1};
+}
+__host__ __device__ constexpr bool is_diag(int t)
+{
+    return t < NT && tile_of(t).kind == 1 && tile_of(t).u == u0_of(tile_of(t).i);
+}
+static_assert(NT == 41 && tile_of(40).kind == 1 && tile_of(41).kind == -1, "tile pattern");
+
+// Y3 tiles (u <= u2), 10 of them: helpers 0 and 1 own three, 2 and 3 two.
+__device__ __forceinline__ int y3_count(int hw) { return hw < 2 ? 3 : 2; }
+__device__ __forceinline__ void y3_tile(int hw, int kk, int &u, int &u2)
+{
+    const int i = hw < 2 ? 3 * hw + kk : 6 + 2 * (hw - 2) + kk;
+    const int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
+    const int vs[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
+    u = us[i];
+    u2 = vs[i];
+}
+
 struct Smem {
     _Float16 qrow[C * RS64];        // q^ [token][m]
+    _Float16 qperm[C * RS64];       // q^ [token][16 (m % 4) + m / 4]: a state wave's channels
     _Float16 krow[C * RS64];        // k^ [token][m]
     _Float16 kT[2][D * RS128];      // k^ [m][token], double-buffered by chunk parity
     _Float16 vT[2][SL * RS128];     // scaled v [j][token], double-buffered
     _Float16 y3h[D * RS64];         // scaled Y3 (prefix before the chunk)
-    float fpart[NW * C * SL];       // partial F^T: [wave][column quad][token][4]
-    float gpart[NW * C];            // partial denominators: [wave][token]
+    float fpart[NSW * C * SL];      // partial F^T of the state waves: [wave][column quad][token][4]
     float y2[2][D];                 // sum k^ before the chunk (by chunk parity)
-    float y2c[D];                   // this chunk's sum k^
     float x1[2][SL];                // sum of scaled v before the chunk
-    float x1c[SL];
     float red[NW];
 };
 
+// rows a (slots 0..3) or b (slots 4..7) of a paired fp16 operand -> the
+// accumulator layout of that tile, times `one` (exact)
+__device__ __forceinline__ h8 perm_operand(int r16, int h, bool hi, _Float16 one)
+{
+    h8 p = {0, 0, 0, 0, 0, 0, 0, 0};
+    const bool on = h == (r16 >> 2);
+    const int slot = (r16 & 3) + (hi ? 4 : 0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) p[j] = (on && slot == j) ? one : (_Float16)0.0f;
+    return p;
+}
+
+template <int HALF>
+__device__ __forceinline__ h8 set_half(h8 x, h4 r)
+{
+    if constexpr (HALF == 0) return h8{r[0], r[1], r[2], r[3], x[4], x[5], x[6], x[7]};
+    else return h8{x[0], x[1], x[2], x[3], r[0], r[1], r[2], r[3]};
+}
 // DV = false: the forward O = F / G.  DV = true: the reverse-causal
 // numerator of the backward, dv_n = sum_{i >= n} f(k^_n . q^_i) u_i with
 // u_i = dO_i / G_i (Sec. 2.5): the scan runs over the tokens in reverse order
 // (logical token n is row N-1-n), q and k trade roles (the caller passes k as
 // q and q as k), v is dO scaled per row by rg = 1/G, and F is stored without
 // the divide; the denominator terms are skipped.
-template <bool DV>
-__device__ __forceinline__ void run_scan(Smem &sm, const bf16_t *__restrict__ q,
-                                         const bf16_t *__restrict__ k,
-                                         const bf16_t *__restrict__ v, bf16_t *__restrict__ out,
-                                         float *__restrict__ g, const float *__restrict__ rg,
-                                         int N, int sl, int vexp)
-{
-    const int w = threadIdx.x >> 6;    // wave
-    const bool has_lin = w < 4;
-
-    f4 acc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-    f4 y3acc[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
-    int y3u[2], y3u2[2];
-    y3_tile(w, 0, y3u[0], y3u2[0]);
-    y3_tile(w, w < 2 ? 1 : 0, y3u[1], y3u2[1]);
-    const int ny3 = y3_count(w);
-
-    const float vscale = ldexpf(1.0f, -vexp);   // v -> v * 2^-e
-    const float oscale = ldexpf(1.0f, vexp);
-    int gexp = 0;                                // Y3 in LDS is Y3 * 2^-gexp
-    const int nch = (N + C - 1) / C;
-
-    // Lane-derived LDS offsets are recomputed in every phase from an opaque
-    // copy of the thread id: hoisted out of the loop they would stay live for
-    // the whole scan and spill.
-    int tid = threadIdx.x;
-    int lane = tid & 63, r16 = lane & 15, h = lane >> 4;
-    // loader roles: tokens 2*tg, 2*tg+1, channels 8*cg .. 8*cg+7
-    int tg = tid >> 3, cg = tid & 7;
-    int vt = tid >> 1, vh = tid & 1;             // v (tid < 256): token vt, columns 8*vh..
-    auto refresh_ids = [&]() {
-        asm volatile("" : "+v"(tid));
-        lane = tid & 63;
-        r16 = lane & 15;
-        h = lane >> 4;
-        tg = tid >> 3;
-        cg = tid & 7;
-        vt = tid >> 1;
-        vh = tid & 1;
-    };
-
-    uint4 pq[2], pk[2], pv;
-    float prg = 1.0f;   // DV: 1/G of the v row
-    auto prefetch = [&](int c) {
-        const uint4 z = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int n = c * C + 2 * tg + j;
-            pq[j] = pk[j] = z;
-            if (n < N) {
-                const size_t pn = DV ? (size_t)(N - 1 - n) : (size_t)n;
-                pq[j] = *(const uint4 *)(q + pn * D + 8 * cg);
-                pk[j] = *(const uint4 *)(k + pn * D + 8 * cg);
-            }
-        }
-        const int nv = c * C + vt;
-        pv = z;
-        if (tid < 2 * C && nv < N) {
-            const size_t pn = DV ? (size_t)(N - 1 - nv) : (size_t)nv;
-            pv = *(const uint4 *)(v + pn * D + SL * sl + 8 * vh);
-            if constexpr (DV) prg = rg[pn];
-        }
-    };
-    // Staging of chunk c (Sec. 2.2, Eqs. 6-7): standardise q and k rows, store
-    // q^, k^ (row-major), k^ transposed and the scaled v transposed.
-    auto stage_q = [&](int c) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int row = 2 * tg + j;
-            float x[8];
-            bf16x8_to_f32(pq[j], x);
-            *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = standardise8(x, c * C + row < N);
-        }
-    };
-    auto stage_kv = [&](int c) {
-        const int buf = c & 1;
-        h8 hk[2];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int row = 2 * tg + j;
-            float x[8];
-            bf16x8_to_f32(pk[j], x);
-            hk[j] = standardise8(x, c * C + row < N);
-            *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            *(h2 *)(sm.kT[buf] + sw128(8 * cg + i, 2 * tg)) = h2{hk[0][i], hk[1][i]};
-        if (tid < 2 * C) {
-            float xv[8];
-            bf16x8_to_f32(pv, xv);
-            const float vs = DV ? vscale * prg : vscale;
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vs);
-        }
-    };
-
-    // prologue: stage chunk 0
-    prefetch(0);
-    stage_q(0);
-    stage_kv(0);
-    __syncthreads();
-
-    for (int c = 0; c < nch; ++c) {
-        const int n0 = c * C;
-        const int nvalid = min(C, N - n0);
-        const int cur = c & 1, nxt = cur ^ 1;
-
-        // ---- (I) query contraction, in-chunk block and denominators ---------
-        __builtin_amdgcn_sched_barrier(0);
-        refresh_ids();
-        {
-            // state -> fp16 A operands, two tiles per K step; diagonal tiles
-            // carry the 1/2 of f_2's quadratic term
-            h8 Ast[NKS];
-            static_for<0, NKS>([&](auto pi) {
-                constexpr int p = decltype(pi)::value;
-                constexpr int ta = 2 * p, tb = 2 * p + 1;
-                h4 a = cvt4(acc[ta]);
-                if constexpr (is_diag(ta)) a = scale4(a, (_Float16)0.5f);
-                h4 b = h4{0, 0, 0, 0};
-                if constexpr (tb < NT) {
-                    b = cvt4(acc[tb < NT ? tb : 0]);
-                    if constexpr (is_diag(tb)) b = scale4(b, (_Float16)0.5f);
-                }
-                Ast[p] = cat(a, b);
-            });
-
-            const _Float16 *kTc = sm.kT[cur];
-            const _Float16 *vTc = sm.vT[cur];
-#pragma unroll 1
-            for (int rt = 0; rt < NRT; ++rt) {
-                const int tok = 16 * rt + r16;
-                h4 myl[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) myl[u] = ld4(sm.qrow + sw64(tok, 16 * u + 4 * h));
-                // linear features l = 16w + 4h + r (zero state in waves 4..7)
-                const h4 mylin = ld4(sm.qrow + sw64(tok, 16 * (w & 3) + 4 * h));
-                // the wave's channels m = w + 8*idx
-                _Float16 qm[8];
-#pragma unroll
-                for (int idx = 0; idx < 8; ++idx) qm[idx] = sm.qrow[sw64(tok, w + 8 * idx)];
-                f4 F0 = {0.f, 0.f, 0.f, 0.f}, F1 = {0.f, 0.f, 0.f, 0.f};
-                auto gen = [&](auto ti) -> h4 {
-                    constexpr int t = decltype(ti)::value;
-                    constexpr Tile T = tile_of(t < NT ? t : 0);
-                    if constexpr (t >= NT) {
-                        return h4{0, 0, 0, 0};
-                    } else if constexpr (T.kind == 0) {
-                        return mylin;
-                    } else {
-                        return scale4(myl[T.u], qm[T.idx]);
-                    }
-                };
-                static_for<0, NKS>([&](auto pi) {
-                    constexpr int p = decltype(pi)::value;
-                    const h8 B = cat(gen(std::integral_constant<int, 2 * p>{}),
-                                     gen(std::integral_constant<int, 2 * p + 1>{}));
-                    if constexpr (p & 1) F1 = mfma(Ast[p], B, F1);
-                    else F0 = mfma(Ast[p], B, F0);
-                });
-                // In-chunk tril block.  Row tile rt has rt/2 + 1 items (pairs of
-                // 16-token key tiles); the chunk's 20 items are dealt round-robin
-                // to the 8 waves.  Each item: two S^T tiles (rows t, cols i = tok),
-                // their weights f(s) and one MFMA F^T += V^T W^T.
-                const int ibase = (rt / 2) * (rt / 2 + 1) + ((rt & 1) ? rt / 2 + 1 : 0);
-                const int first = (w - ibase % NW + NW) % NW;   // first item j of this wave
-                float gpart = 0.f;
-                if (first <= rt / 2 || (!DV && rt == w)) {
-                    const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
-                    const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
-                    auto wtile = [&](int tt) -> h4 {
-                        f4 S = {0.f, 0.f, 0.f, 0.f};
-                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 8 * h)), QB0, S);
-                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 32 + 8 * h)), QB1, S);
-                        f4 wv;
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float x = S[i];
-                            float y = fmaf(0.5f * x, x, 1.0f + x);
-                            if (tt == rt && (4 * h + i) > r16) y = 0.0f;
-                            wv[i] = y;
-                            gpart += y;
-                        }
-                        return cvt4(wv);
-                    };
-                    for (int j = first; j <= rt / 2; j += NW) {
-                        const int a = 2 * j, b = a + 1;
-                        const h4 wa = wtile(a);
-                        const h4 va = ld4(vTc + sw128(r16, 16 * a + 4 * h));
-                        h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
-                        if (b <= rt) {
-                            wb = wtile(b);
-                            vb = ld4(vTc + sw128(r16, 16 * b + 4 * h));
-                        }
-                        F0 = mfma(cat(va, vb), cat(wa, wb), F0);
-                    }
-                    if (!DV && rt == w) {
-                        // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
-                        float gq = 0.f;
-                        const float ys = ldexpf(2.0f, -gexp);
-#pragma unroll
-                        for (int cc = 0; cc < 4; ++cc) {
-                            f4 T;
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[cur][16 * cc + 4 * h + i];
-                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
-                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) gq = fmaf((float)myl[cc][i], T[i], gq);
-                        }
-                        gpart = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gpart);
-                        if (h == 0) gpart += (float)n0;
-                    }
-                    gpart += __shfl_xor(gpart, 16);
-                    gpart += __shfl_xor(gpart, 32);
-                }
-                if (h == 0) sm.gpart[w * C + tok] = gpart;
-                *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
-            }
-            // this chunk's sums of k^ (for y2, waves 0-3) and of scaled v (x1, wave 4)
-            if (!DV && w < 4) {
-                const int m = 16 * w + r16;
-                float s = 0.f;
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(kTc + sw128(m, 32 * h + 8 * cc)));
-                s += __shfl_xor(s, 16);
-                s += __shfl_xor(s, 32);
-                if (h == 0) sm.y2c[m] = s;
-            } else if (w == 4) {
-                float sv = 0.f;
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(vTc + sw128(r16, 32 * h + 8 * cc)));
-                sv += __shfl_xor(sv, 16);
-                sv += __shfl_xor(sv, 32);
-                if (h == 0) sm.x1c[r16] = sv;
-            }
-        }
-        __syncthreads();
-
-        // ---- (M) output of chunk c, state update with chunk c, staging of c+1 --
-        __builtin_amdgcn_sched_barrier(0);
-        refresh_ids();
-        {
-            // combine partials, divide, store
-            const int tok = tid & (C - 1), cq = tid >> 7;
-            f4 F = *(const f4 *)(sm.x1[cur] + 4 * cq);
-            float Gi = 0.f;
-#pragma unroll
-            for (int ww = 0; ww < NW; ++ww) {
-                F += *(const f4 *)(sm.fpart + ((ww * 4 + cq) * C + tok) * 4);
-                Gi += sm.gpart[ww * C + tok];
-            }
-            if (n0 + tok < N) {
-                const float sc = DV ? oscale : oscale * __builtin_amdgcn_rcpf(Gi);
-                uint2 o;
-                o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
-                o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
-                const size_t pn = DV ? (size_t)(N - 1 - (n0 + tok)) : (size_t)(n0 + tok);
-                *(uint2 *)(out + pn * D + SL * sl + 4 * cq) = o;
-                if (!DV && g && sl == 0 && cq == 0) g[n0 + tok] = Gi;
-            }
-            // prefixes for the next chunk
-            if (tid < D) sm.y2[nxt][tid] = sm.y2[cur][tid] + sm.y2c[tid];
-            else if (tid < D + SL) sm.x1[nxt][tid - D] = sm.x1[cur][tid - D] + sm.x1c[tid - D];
-        }
-        const bool more = c + 1 < nch;
-        if (more) prefetch(c + 1);
-        {
-            // state update S += Phi(K)^T V, Y3 += K^T K, interleaved with the
-            // staging of the next chunk (its loads land behind the first steps)
-            const _Float16 *kTc = sm.kT[cur];
-            const _Float16 *vTc = sm.vT[cur];
-            auto ustep = [&](int s) {
-                h8 Ak[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) Ak[u] = ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h));
-                const h8 Vf = ld8(vTc + sw128(r16, 32 * s + 8 * h));
-                if (has_lin)   // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
-                    acc[0] = mfma(ld8(kTc + sw128(16 * w + r16, 32 * s + 8 * h)), Vf, acc[0]);
-                static_for<0, 8>([&](auto ii) {
-                    constexpr int idx = decltype(ii)::value;
-                    constexpr int u0 = u0_of(idx);
-                    constexpr int t0 = first_tile(idx);
-                    const int m = w + 8 * idx;
-                    const h8 km = ld8(kTc + sw128(m, 32 * s + 8 * h));
-                    const h8 Wm = km * Vf;
-                    static_for<u0, 4>([&](auto ui) {
-                        constexpr int u = decltype(ui)::value;
-                        acc[t0 + (u - u0)] = mfma(Ak[u], Wm, acc[t0 + (u - u0)]);
-                    });
-                });
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk)
-                    if (!DV && kk < ny3)
-                        y3acc[kk] = mfma(ld8(kTc + sw128(16 * y3u[kk] + r16, 32 * s + 8 * h)),
-                                         ld8(kTc + sw128(16 * y3u2[kk] + r16, 32 * s + 8 * h)),
-                                         y3acc[kk]);
-            };
-            ustep(0);
-            ustep(1);
-            ustep(2);
-            if (more) stage_q(c + 1);
-            ustep(3);
-            if (more) stage_kv(c + 1);
-            // scaled fp16 copy of Y3 for the next chunk's denominators
-            const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
-            const float gs = ldexpf(1.0f, -gnext);
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                if (DV || kk >= ny3) break;
-                const int u = y3u[kk], u2 = y3u2[kk];
-                // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
-                const int mcol = 16 * u2 + r16;
-                h4 hv;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) hv[i] = (_Float16)(y3acc[kk][i] * gs);
-                *(h4 *)(sm.y3h + sw64(mcol, 16 * u + 4 * h)) = hv;       // Y3[m][l]
-                if (u != u2) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) sm.y3h[sw64(16 * u + 4 * h + i, mcol)] = hv[i];
-                }
-            }
-            gexp = gnext;
-        }
-        __syncthreads();
-    }
-}
-
 template <bool DV>
 __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__restrict__ q,
                                                             const bf16_t *__restrict__ k,
@@ -437,29 +166,387 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
     if (rg) rg += (size_t)head * N;
 
     // max |v| over this slice -> power-of-two scale
-    const int tid = threadIdx.x;
-    float vmax = 0.f;
-    for (int p = tid; p < 2 * N; p += NTH) {
-        const int n = p >> 1, hh = p & 1;
-        float x[8];
-        bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh), x);
-        const float r = DV ? fabsf(rg[n]) : 1.0f;
+    {
+        const int tid = threadIdx.x;
+        float vmax = 0.f;
+        for (int p = tid; p < 2 * N; p += NTH) {
+            const int n = p >> 1, hh = p & 1;
+            float x[8];
+            bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh), x);
+            const float r = DV ? fabsf(rg[n]) : 1.0f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * r);
+            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * r);
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
+        if ((tid & 63) == 0) sm.red[tid >> 6] = vmax;
+        if (tid < D) sm.y2[0][tid] = 0.f;
+        if (tid < SL) sm.x1[0][tid] = 0.f;
+        for (int e = tid; e < D * RS64; e += NTH) sm.y3h[e] = (_Float16)0.0f;
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
-    if ((tid & 63) == 0) sm.red[tid >> 6] = vmax;
-    if (tid < D) { sm.y2[0][tid] = 0.f; sm.y2c[tid] = 0.f; }
-    if (tid < SL) { sm.x1[0][tid] = 0.f; sm.x1c[tid] = 0.f; }
-    for (int e = tid; e < D * RS64; e += NTH) sm.y3h[e] = (_Float16)0.0f;
     __syncthreads();
-    vmax = 0.f;
+    float vmax = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) vmax = fmaxf(vmax, sm.red[w]);
     const int vexp = pow2_exponent(vmax * 63.0f * (float)N);
+    const float vscale = ldexpf(1.0f, -vexp);   // v -> v * 2^-e
+    const float oscale = ldexpf(1.0f, vexp);
+    const int nch = (N + C - 1) / C;
 
-    run_scan<DV>(sm, q, k, v, out, g, rg, N, sl, vexp);
+    const int w = threadIdx.x >> 6;
+    const bool is_state = w < NSW;
+    const int hw = w - NSW;   // helper index
+
+    // Lane-derived LDS offsets are recomputed in every phase from an opaque
+    // copy of the thread id: hoisted out of the loop they would stay live for
+    // the whole scan.
+    int tid = threadIdx.x;
+    int lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    auto refresh_ids = [&]() {
+        asm volatile("" : "+v"(tid));
+        lane = tid & 63;
+        r16 = lane & 15;
+        h = lane >> 4;
+    };
+
+    // The two roles run separate loops with the same barrier sequence (one
+    // after staging chunk 0, two per chunk); the role is uniform per wave.
+    if (is_state) {
+        // fp16 state, paired per query K step
+        h8 Ast[NKS];
+#pragma unroll
+        for (int p = 0; p < NKS; ++p) Ast[p] = h8{0, 0, 0, 0, 0, 0, 0, 0};
+        __syncthreads();
+        for (int c = 0; c < nch; ++c) {
+            // ---- (1) query contraction over the wave's tiles, 128 tokens ----
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            // the q^ values of a row tile: l blocks, the linear tile and the
+            // wave's channels; loaded one row tile ahead of their use
+            struct QRow {
+                h4 myl[4], mylin;
+                h8 qa, qb;
+            };
+            auto loadq = [&](int rt, QRow &r) {
+                const int tok = 16 * rt + r16;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) r.myl[u] = ld4(sm.qrow + sw64(tok, 16 * u + 4 * h));
+                r.mylin = ld4(sm.qrow + sw64(tok, 16 * w + 4 * h));
+                r.qa = ld8(sm.qperm + sw64(tok, 16 * w));
+                r.qb = ld8(sm.qperm + sw64(tok, 16 * w + 8));
+            };
+            auto contract = [&](int rt, const QRow &r) {
+                const int tok = 16 * rt + r16;
+                f4 F0 = {0.f, 0.f, 0.f, 0.f}, F1 = {0.f, 0.f, 0.f, 0.f};
+                auto gen = [&](auto ti) -> h4 {
+                    constexpr int t = decltype(ti)::value;
+                    constexpr Tile T = tile_of(t < NT ? t : 0);
+                    if constexpr (t >= NT) {
+                        return h4{0, 0, 0, 0};
+                    } else if constexpr (T.kind == 0) {
+                        return r.mylin;
+                    } else {
+                        const _Float16 qm = T.i < 8 ? r.qa[T.i & 7] : r.qb[T.i & 7];
+                        return scale4(r.myl[T.u], qm);
+                    }
+                };
+                static_for<0, NKS>([&](auto pi) {
+                    constexpr int p = decltype(pi)::value;
+                    const h8 B = cat(gen(std::integral_constant<int, 2 * p>{}),
+                                     gen(std::integral_constant<int, 2 * p + 1>{}));
+                    if constexpr (p & 1) F1 = mfma(Ast[p], B, F1);
+                    else F0 = mfma(Ast[p], B, F0);
+                });
+                *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
+            };
+            QRow ra, rb;
+            loadq(0, ra);
+#pragma unroll 1
+            for (int rt = 0; rt < NRT; rt += 2) {
+                loadq(rt + 1, rb);
+                contract(rt, ra);
+                if (rt + 2 < NRT) loadq(rt + 2, ra);
+                contract(rt + 1, rb);
+            }
+            __syncthreads();
+
+            // ---- (2) state update S += Phi(K)^T V (Sec. 2.4) ----------------
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            const _Float16 *kTc = sm.kT[c & 1];
+            const _Float16 *vTc = sm.vT[c & 1];
+            h8 Ak[4][NKS2];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s) Ak[u][s] = ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h));
+            h8 Vf[NKS2];
+#pragma unroll
+            for (int s = 0; s < NKS2; ++s) Vf[s] = ld8(vTc + sw128(r16, 32 * s + 8 * h));
+            const h8 pa = perm_operand(r16, h, false, (_Float16)1.0f);
+            const h8 pb = perm_operand(r16, h, true, (_Float16)1.0f);
+            const h8 pa2 = perm_operand(r16, h, false, (_Float16)2.0f);
+            const h8 pb2 = perm_operand(r16, h, true, (_Float16)2.0f);
+            {
+                // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
+                f4 acc = mfma(pa, Ast[0], f4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s)
+                    acc = mfma(ld8(kTc + sw128(16 * w + r16, 32 * s + 8 * h)), Vf[s], acc);
+                Ast[0] = set_half<0>(Ast[0], cvt4(acc));
+            }
+            static_for<0, NQ>([&](auto ii) {
+                constexpr int i = decltype(ii)::value;
+                constexpr int u0 = u0_of(i);
+                constexpr int t0 = first_tile(i);
+                constexpr int nu = 4 - u0;
+                const int m = w + 4 * i;
+                h8 Wm[NKS2];
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s) Wm[s] = ld8(kTc + sw128(m, 32 * s + 8 * h)) * Vf[s];
+                // rebuild the fp32 tiles (diagonal tile: stored halved, 0/2 matrix)
+                f4 acc[nu];
+                static_for<0, nu>([&](auto ui) {
+                    constexpr int uu = decltype(ui)::value;
+                    constexpr int t = t0 + uu;
+                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
+                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
+                });
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s)
+                    static_for<0, nu>([&](auto ui) {
+                        constexpr int uu = decltype(ui)::value;
+                        acc[uu] = mfma(Ak[u0 + uu][s], Wm[s], acc[uu]);
+                    });
+                static_for<0, nu>([&](auto ui) {
+                    constexpr int uu = decltype(ui)::value;
+                    constexpr int t = t0 + uu;
+                    h4 r = cvt4(acc[uu]);
+                    if constexpr (uu == 0) r = scale4(r, (_Float16)0.5f);
+                    Ast[t / 2] = set_half<t & 1>(Ast[t / 2], r);
+                });
+            });
+            __syncthreads();
+        }
+    } else {
+        // loader roles: tokens 4*tg .. 4*tg+3, channels 8*cg .. 8*cg+7; v:
+        // token vt, columns 8*vh .. 8*vh+7
+        uint4 pq[4], pk[4], pv;
+        float prg = 1.0f;
+        f4 y3acc[3] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
+        int gexp = 0;   // Y3 in LDS is Y3 * 2^-gexp
+
+        auto prefetch = [&](int c) {
+            const int ht = tid - NSW * 64;
+            const int tg = ht >> 3, cg = ht & 7;
+            const uint4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = c * C + 4 * tg + j;
+                pq[j] = pk[j] = z;
+                if (n < N) {
+                    const size_t pn = DV ? (size_t)(N - 1 - n) : (size_t)n;
+                    pq[j] = *(const uint4 *)(q + pn * D + 8 * cg);
+                    pk[j] = *(const uint4 *)(k + pn * D + 8 * cg);
+                }
+            }
+            const int vt = ht >> 1, vh = ht & 1;
+            const int nv = c * C + vt;
+            pv = z;
+            if (nv < N) {
+                const size_t pn = DV ? (size_t)(N - 1 - nv) : (size_t)nv;
+                pv = *(const uint4 *)(v + pn * D + SL * sl + 8 * vh);
+                if constexpr (DV) prg = rg[pn];
+            }
+        };
+        // Staging of chunk c (Sec. 2.2, Eqs. 6-7): standardise q and k rows,
+        // store q^ (row-major and channel-permuted), k^ (row-major and
+        // transposed) and the scaled v transposed.
+        auto stage = [&](int c) {
+            const int ht = tid - NSW * 64;
+            const int tg = ht >> 3, cg = ht & 7;
+            const int buf = c & 1;
+            h8 hk[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = 4 * tg + j;
+                const bool valid = c * C + row < N;
+                float x[8];
+                bf16x8_to_f32(pq[j], x);
+                const h8 hq = standardise8(x, valid);
+                *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
+                // channel 8cg + ww -> state wave ww, index 2cg; 8cg + 4 + ww -> 2cg + 1
+#pragma unroll
+                for (int ww = 0; ww < 4; ++ww)
+                    *(h2 *)(sm.qperm + sw64(row, 16 * ww + 2 * cg)) = h2{hq[ww], hq[4 + ww]};
+                bf16x8_to_f32(pk[j], x);
+                hk[j] = standardise8(x, valid);
+                *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                *(h4 *)(sm.kT[buf] + sw128(8 * cg + i, 4 * tg)) =
+                    h4{hk[0][i], hk[1][i], hk[2][i], hk[3][i]};
+            const int vt = ht >> 1, vh = ht & 1;
+            float xv[8];
+            bf16x8_to_f32(pv, xv);
+            const float vs = DV ? vscale * prg : vscale;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vs);
+        };
+
+        prefetch(0);
+        stage(0);
+        __syncthreads();
+        for (int c = 0; c < nch; ++c) {
+            const int n0 = c * C;
+            const int nvalid = min(C, N - n0);
+            const int cur = c & 1, nxt = cur ^ 1;
+            const bool more = c + 1 < nch;
+
+            // ---- (1) in-chunk block and denominators, row tiles hw, 7 - hw
+            //      (1 + 4, 1 + 4, 2 + 3, 2 + 3 tile-pair items) ---------------
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            if (more) prefetch(c + 1);
+            f4 Fin[2];
+            float Gs[2];
+            {
+                const _Float16 *vTc = sm.vT[cur];
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int rt = r ? NRT - 1 - hw : hw;
+                    const int tok = 16 * rt + r16;
+                    const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
+                    const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
+                    f4 F = {0.f, 0.f, 0.f, 0.f};
+                    float gpart = 0.f;
+                    // S^T tile (rows: keys 16tt.., columns: queries) -> f(s)
+                    auto wtile = [&](int tt) -> h4 {
+                        f4 S = {0.f, 0.f, 0.f, 0.f};
+                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 8 * h)), QB0, S);
+                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 32 + 8 * h)), QB1, S);
+                        f4 wv;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float x = S[i];
+                            float y = fmaf(0.5f * x, x, 1.0f + x);
+                            if (tt == rt && (4 * h + i) > r16) y = 0.0f;
+                            wv[i] = y;
+                            gpart += y;
+                        }
+                        return cvt4(wv);
+                    };
+#pragma unroll 1
+                    for (int j = 0; j <= rt / 2; ++j) {
+                        const int a = 2 * j, bb = a + 1;
+                        const h4 wa = wtile(a);
+                        const h4 va = ld4(vTc + sw128(r16, 16 * a + 4 * h));
+                        h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
+                        if (bb <= rt) {
+                            wb = wtile(bb);
+                            vb = ld4(vTc + sw128(r16, 16 * bb + 4 * h));
+                        }
+                        F = mfma(cat(va, vb), cat(wa, wb), F);
+                    }
+                    if (!DV) {
+                        // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
+                        float gq = 0.f;
+                        const float ys = ldexpf(2.0f, -gexp);
+#pragma unroll
+                        for (int cc = 0; cc < 4; ++cc) {
+                            const h4 ql = ld4(sm.qrow + sw64(tok, 16 * cc + 4 * h));
+                            f4 T;
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[cur][16 * cc + 4 * h + i];
+                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
+                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) gq = fmaf((float)ql[i], T[i], gq);
+                        }
+                        gpart = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gpart);
+                        if (h == 0) gpart += (float)n0;
+                    }
+                    gpart += __shfl_xor(gpart, 16);
+                    gpart += __shfl_xor(gpart, 32);
+                    Fin[r] = F;
+                    Gs[r] = gpart;
+                }
+            }
+            __syncthreads();
+
+            // ---- (2) output, prefix sums, Y3, staging of the next chunk ------
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            const _Float16 *kTc = sm.kT[cur];
+            const _Float16 *vTc = sm.vT[cur];
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int rt = r ? NRT - 1 - hw : hw;
+                const int tok = 16 * rt + r16;
+                f4 F = Fin[r] + *(const f4 *)(sm.x1[cur] + 4 * h);
+#pragma unroll
+                for (int ww = 0; ww < NSW; ++ww)
+                    F += *(const f4 *)(sm.fpart + ((ww * 4 + h) * C + tok) * 4);
+                if (n0 + tok < N) {
+                    const float sc = DV ? oscale : oscale * __builtin_amdgcn_rcpf(Gs[r]);
+                    uint2 o;
+                    o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
+                    o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
+                    const size_t pn = DV ? (size_t)(N - 1 - (n0 + tok)) : (size_t)(n0 + tok);
+                    *(uint2 *)(out + pn * D + SL * sl + 4 * h) = o;
+                    if (!DV && g && sl == 0 && h == 0) g[n0 + tok] = Gs[r];
+                }
+            }
+            // prefix sums: y2 (channels 16hw..16hw+15), x1 (helper 0)
+            if (!DV) {
+                const int m = 16 * hw + r16;
+                float s = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(kTc + sw128(m, 32 * h + 8 * cc)));
+                s += __shfl_xor(s, 16);
+                s += __shfl_xor(s, 32);
+                if (h == 0) sm.y2[nxt][m] = sm.y2[cur][m] + s;
+            }
+            if (hw == 0) {
+                float sv = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(vTc + sw128(r16, 32 * h + 8 * cc)));
+                sv += __shfl_xor(sv, 16);
+                sv += __shfl_xor(sv, 32);
+                if (h == 0) sm.x1[nxt][r16] = sm.x1[cur][r16] + sv;
+            }
+            if (!DV) {
+                // Y3 += K^T K and its scaled fp16 copy for the next chunk
+                const int ny3 = y3_count(hw);
+                const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
+                const float gs = ldexpf(1.0f, -gnext);
+#pragma unroll
+                for (int kk = 0; kk < 3; ++kk) {
+                    if (kk >= ny3) break;
+                    int u, u2;
+                    y3_tile(hw, kk, u, u2);
+#pragma unroll
+                    for (int s = 0; s < NKS2; ++s)
+                        y3acc[kk] = mfma(ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h)),
+                                         ld8(kTc + sw128(16 * u2 + r16, 32 * s + 8 * h)), y3acc[kk]);
+                    // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
+                    const int mcol = 16 * u2 + r16;
+                    h4 hv;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) hv[i] = (_Float16)(y3acc[kk][i] * gs);
+                    *(h4 *)(sm.y3h + sw64(mcol, 16 * u + 4 * h)) = hv;   // Y3[m][l]
+                    if (u != u2) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) sm.y3h[sw64(16 * u + 4 * h + i, mcol)] = hv[i];
+                    }
+                }
+                gexp = gnext;
+            }
+            if (more) stage(c + 1);
+            __syncthreads();
+        }
+    }
 }
 
 }  // namespace mfma_causal
@@ -471,6 +558,7 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
 {
     using namespace mfma_causal;
     static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
+    static_assert(NHT == 2 * C, "one helper thread per (token pair, v half)");
     const size_t smem = sizeof(Smem);
     hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel<false>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);

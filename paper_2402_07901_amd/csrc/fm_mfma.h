@@ -1,5 +1,5 @@
 // Device helpers shared by the D = 64, p = 2 MFMA kernels (causal scan,
-// non-causal moment build and query contraction): fp16 operand packing for
+// non-causal moment build and query contraction, backward): fp16 operand packing for
 // v_mfma_f32_16x16x32_f16, the per-wave feature-tile pattern of the moment
 // state, LDS row padding and per-token standardisation (Sec. 2.2, Eqs. 6-7).
 //
@@ -13,8 +13,10 @@
 // 4160 of the full square, 2080 + 65 being the minimum.  A "diagonal" tile
 // (u == m/16) carries both (m,l) and (l,m) and enters the query contraction
 // with weight 1/2, the others with weight 1, so psi(q).phi(k) = 1 + s + s^2/2
-// exactly (constant term separate).  With eight waves, wave w owns the tiles
-// of m = w (mod 8) and, for w < 4, the linear tile u = w: 21 tiles.
+// exactly (constant term separate).  The eight-wave pattern below (wave w
+// owns the tiles of m = w (mod 8) and, for w < 4, the linear tile u = w: 21
+// tiles) serves the non-causal moment build; the causal scan defines its own
+// four-wave pattern of 41 tiles.
 //
 // Pairing for the query contraction: K step p combines tiles 2p and 2p+1;
 // K index 8h+r <-> tile 2p row 4h+r, 8h+4+r <-> tile 2p+1 row 4h+r, which is
