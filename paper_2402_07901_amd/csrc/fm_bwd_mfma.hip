@@ -29,6 +29,8 @@
 
 #include <limits.h>
 
+#include <mutex>
+
 #include "fm_common.h"
 #include "fm_internal.h"
 #include "fm_mfma.h"
@@ -680,6 +682,40 @@ __global__ __launch_bounds__(256) void bwd_finish(const bf16_t *__restrict__ q,
 
 }  // namespace mfma_bwd
 
+namespace {
+
+// One side stream (default priority, non-blocking) and a fork/join event pair
+// per device, created on first use and kept for the life of the process.
+struct SideStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    std::mutex mu;
+};
+constexpr int MAX_DEVICES = 64;
+SideStream g_side[MAX_DEVICES];
+std::once_flag g_side_once[MAX_DEVICES];
+hipError_t g_side_err[MAX_DEVICES];
+
+hipError_t side_stream(SideStream **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::call_once(g_side_once[dev], [dev]() {
+        SideStream &s = g_side[dev];
+        hipError_t r = hipStreamCreateWithFlags(&s.stream, hipStreamNonBlocking);
+        if (r == hipSuccess) r = hipEventCreateWithFlags(&s.fork, hipEventDisableTiming);
+        if (r == hipSuccess) r = hipEventCreateWithFlags(&s.join, hipEventDisableTiming);
+        g_side_err[dev] = r;
+    });
+    if (g_side_err[dev] != hipSuccess) return g_side_err[dev];
+    *out = &g_side[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
 size_t mfma_causal_bwd_workspace(int BH, int N)
 {
     const size_t rows = (size_t)BH * N;
@@ -717,25 +753,50 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                        nch);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = mfma_causal_dv(q, k, dout, rg, dv, BH, N, st);
+    // dv (reverse-causal scan, needs only rg) runs on a side stream next to
+    // the in-chunk and moment-gradient kernels: its last, partly filled round
+    // of workgroups overlaps their work.  Fork and join through events; the
+    // enqueue sequence is serialised so that concurrent callers cannot
+    // interleave records and waits of the shared events.
+    SideStream *ss = nullptr;
+    e = side_stream(&ss);
     if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void *)bwd_intra, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)sizeof(ISmem));
+    std::lock_guard<std::mutex> lock(ss->mu);
+    e = hipEventRecord(ss->fork, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(512), sizeof(ISmem), st, Q, K, V, DO, rg,
-                       cc, hmax, dqh, dkh, N, nch);
-    e = hipGetLastError();
+    e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
     if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void *)bwd_mg_scans,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
+    const hipError_t edv = mfma_causal_dv(q, k, dout, rg, dv, BH, N, ss->stream);
+    e = hipEventRecord(ss->join, ss->stream);
+    if (e == hipSuccess && edv != hipSuccess) {
+        hipStreamWaitEvent(st, ss->join, 0);
+        return edv;
+    }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, Q, K, V, DO,
-                       rg, cc, hmax, dqh, dkh, N, BH);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q, K,
-                       dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows);
-    return hipGetLastError();
+    // from here on every path joins the side stream before returning
+    auto rest = [&]() -> hipError_t {
+        hipError_t r = hipFuncSetAttribute((const void *)bwd_intra,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)sizeof(ISmem));
+        if (r != hipSuccess) return r;
+        hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(512), sizeof(ISmem), st, Q, K, V, DO,
+                           rg, cc, hmax, dqh, dkh, N, nch);
+        r = hipGetLastError();
+        if (r != hipSuccess) return r;
+        r = hipFuncSetAttribute((const void *)bwd_mg_scans,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
+        if (r != hipSuccess) return r;
+        hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, Q, K, V,
+                           DO, rg, cc, hmax, dqh, dkh, N, BH);
+        r = hipGetLastError();
+        if (r != hipSuccess) return r;
+        hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q,
+                           K, dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows);
+        return hipGetLastError();
+    };
+    const hipError_t er = rest();
+    const hipError_t ej = hipStreamWaitEvent(st, ss->join, 0);
+    return er != hipSuccess ? er : ej;
 }
 
 }  // namespace fm
