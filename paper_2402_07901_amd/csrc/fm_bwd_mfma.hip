@@ -200,8 +200,8 @@ __global__ __launch_bounds__(512) void bwd_intra(const bf16_t *__restrict__ q,
             *(h8 *)(sm.urow + sw64(t, 8 * cg)) = hu;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                sm.qT[sw128(8 * cg + i, t)] = hq[i];
-                sm.kT[sw128(8 * cg + i, t)] = hk[i];
+                sm.qT[swx(8 * cg + i, t)] = hq[i];
+                sm.kT[swx(8 * cg + i, t)] = hk[i];
             }
             if (cg == 0) sm.cc[t] = valid ? cc[n] : 0.f;
         }
@@ -244,8 +244,8 @@ __global__ __launch_bounds__(512) void bwd_intra(const bf16_t *__restrict__ q,
             const h8 B = cat(pa, pb);
 #pragma unroll
             for (int lt = 0; lt < 4; ++lt) {
-                const h4 ka = ld4(sm.kT + sw128(16 * lt + r16, 16 * a + 4 * h));
-                const h4 kb = b <= rt ? ld4(sm.kT + sw128(16 * lt + r16, 16 * b + 4 * h)) : z4;
+                const h4 ka = ld4(sm.kT + swx(16 * lt + r16, 16 * a + 4 * h));
+                const h4 kb = b <= rt ? ld4(sm.kT + swx(16 * lt + r16, 16 * b + 4 * h)) : z4;
                 acc[lt] = mfma(cat(ka, kb), B, acc[lt]);
             }
         }
@@ -289,8 +289,8 @@ __global__ __launch_bounds__(512) void bwd_intra(const bf16_t *__restrict__ q,
             const h8 B = cat(pa, pb);
 #pragma unroll
             for (int lt = 0; lt < 4; ++lt) {
-                const h4 qa = ld4(sm.qT + sw128(16 * lt + r16, 16 * a + 4 * h));
-                const h4 qb = b < 8 ? ld4(sm.qT + sw128(16 * lt + r16, 16 * b + 4 * h)) : z4;
+                const h4 qa = ld4(sm.qT + swx(16 * lt + r16, 16 * a + 4 * h));
+                const h4 qb = b < 8 ? ld4(sm.qT + swx(16 * lt + r16, 16 * b + 4 * h)) : z4;
                 acc[lt] = mfma(cat(qa, qb), B, acc[lt]);
             }
         }
@@ -452,8 +452,8 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            *(h2 *)(sm.yT + sw128(8 * cg + i, 2 * tg)) = h2{hy[0][i], hy[1][i]};
-            *(h2 *)(sm.wT + sw128(8 * cg + i, 2 * tg)) = h2{hw[0][i], hw[1][i]};
+            *(h2 *)(sm.yT + swx(8 * cg + i, 2 * tg)) = h2{hy[0][i], hy[1][i]};
+            *(h2 *)(sm.wT + swx(8 * cg + i, 2 * tg)) = h2{hw[0][i], hw[1][i]};
         }
     };
 
@@ -553,11 +553,11 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
                 const int col = 32 * ks + 8 * h;
                 h8 Aw[4];
 #pragma unroll
-                for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(sm.wT + sw128(16 * jt + r16, col));
-                const h8 Yl = ld8(sm.yT + sw128(16 * L + r16, col));
+                for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(sm.wT + swx(16 * jt + r16, col));
+                const h8 Yl = ld8(sm.yT + swx(16 * L + r16, col));
 #pragma unroll
                 for (int m = 0; m < MG_MPW; ++m) {
-                    const h8 Ym = ld8(sm.yT + sw128(MG_MPW * w + m, col));
+                    const h8 Ym = ld8(sm.yT + swx(MG_MPW * w + m, col));
                     const h8 Bm = Ym * Yl;
 #pragma unroll
                     for (int jt = 0; jt < 4; ++jt) acc[m][jt] = mfma(Aw[jt], Bm, acc[m][jt]);
@@ -580,7 +580,7 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
 #pragma unroll
                         for (int e = 0; e < 2; ++e) {
                             const int mt = 2 * (w - 2) + e;
-                            ex[e] = mfma(ld8(sm.yT + sw128(16 * mt + r16, col)), YW, ex[e]);
+                            ex[e] = mfma(ld8(sm.yT + swx(16 * mt + r16, col)), YW, ex[e]);
                         }
                     }
 #pragma unroll

@@ -99,6 +99,14 @@ constexpr int RS64 = 64 + 8;     // rows of 64 halves
 constexpr int RS128 = 128 + 8;   // rows of 128 halves
 __device__ __forceinline__ int sw64(int row, int col) { return row * RS64 + col; }
 __device__ __forceinline__ int sw128(int row, int col) { return row * RS128 + col; }
+// Transposed operands ([channel][token]) staged by lanes that each hold 8
+// channels of a few tokens write rows 8 apart in one store instruction, which
+// the padding maps to the same banks.  XOR-ing the column (in 16-byte units)
+// with the row's group of 8 spreads those stores over all banks and keeps
+// every aligned 8- or 16-byte read contiguous.  Used where the staging
+// stores dominate (the backward's scans); the forward kernels keep plain
+// padding, whose reads need no per-lane address work.
+__device__ __forceinline__ int swx(int row, int col) { return row * RS128 + (col ^ (((row >> 3) & 7) << 3)); }
 
 
 __device__ __forceinline__ f4 mfma(h8 a, h8 b, f4 c)
