@@ -42,20 +42,58 @@ using namespace mx;
 
 constexpr int C = 128;   // tokens per chunk
 
+// standardise8 that also returns the reciprocal standard deviation
+__device__ __forceinline__ h8 standardise8_rs(const float *xin, float &rs)
+{
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += xin[i];
+    const float mu = octet_sum(s) * (1.0f / D);
+    float x[8], var = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        x[i] = xin[i] - mu;
+        var = fmaf(x[i], x[i], var);
+    }
+    rs = __builtin_amdgcn_rsqf(octet_sum(var) * (1.0f / D));
+    h8 o;
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+        const h2 pr = {(_Float16)(x[i] * rs), (_Float16)(x[i + 1] * rs)};
+        o[i] = pr[0];
+        o[i + 1] = pr[1];
+    }
+    return o;
+}
+
 // ---------------------------------------------------------------------------
 // bwd_prep: one workgroup per (head, 128-token chunk), an octet of lanes per
-// token; per-chunk maxima go to pmax[head][chunk][4].
+// token; per-chunk maxima go to pmax[head][chunk][4].  Also standardises q and
+// k once for the whole backward (Sec. 2.2, Eqs. 6-7): q^, k^ in fp16 and the
+// reciprocal standard deviations, which the later kernels read instead of
+// recomputing them.
 
-__global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ o,
+__global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
+                                                const bf16_t *__restrict__ k,
+                                                const bf16_t *__restrict__ o,
                                                 const bf16_t *__restrict__ dout,
                                                 const bf16_t *__restrict__ v,
                                                 const float *__restrict__ g,
                                                 float *__restrict__ rg, float *__restrict__ cc,
-                                                float *__restrict__ pmax, int N, int nch)
+                                                float *__restrict__ pmax, _Float16 *__restrict__ qh,
+                                                _Float16 *__restrict__ kh,
+                                                float *__restrict__ rsq, float *__restrict__ rsk,
+                                                int N, int nch)
 {
     __shared__ float red[3][4];
     const int head = blockIdx.x / nch, c = blockIdx.x % nch, tid = threadIdx.x;
     const size_t hb = (size_t)head * N;
+    q += hb * D;
+    k += hb * D;
+    qh += hb * D;
+    kh += hb * D;
+    rsq += hb;
+    rsk += hb;
     o += hb * D;
     dout += hb * D;
     v += hb * D;
@@ -89,6 +127,16 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ o,
         if (valid && cg == 0) {
             rg[n] = r;
             cc[n] = c;
+        }
+        if (valid) {
+            float x[8];
+            float rs;
+            bf16x8_to_f32(*(const uint4 *)(q + (size_t)n * D + 8 * cg), x);
+            *(h8 *)(qh + (size_t)n * D + 8 * cg) = standardise8_rs(x, rs);
+            if (cg == 0) rsq[n] = rs;
+            bf16x8_to_f32(*(const uint4 *)(k + (size_t)n * D + 8 * cg), x);
+            *(h8 *)(kh + (size_t)n * D + 8 * cg) = standardise8_rs(x, rs);
+            if (cg == 0) rsk[n] = rs;
         }
     }
 #pragma unroll
@@ -140,8 +188,8 @@ struct ISmem {
     float cc[C];
 };
 
-__global__ __launch_bounds__(512) void bwd_intra(const bf16_t *__restrict__ q,
-                                                 const bf16_t *__restrict__ k,
+__global__ __launch_bounds__(512) void bwd_intra(const _Float16 *__restrict__ q,
+                                                 const _Float16 *__restrict__ k,
                                                  const bf16_t *__restrict__ v,
                                                  const bf16_t *__restrict__ dout,
                                                  const float *__restrict__ rg,
@@ -178,16 +226,16 @@ __global__ __launch_bounds__(512) void bwd_intra(const bf16_t *__restrict__ q,
         for (int pass = 0; pass < 2; ++pass) {
             const int t = 64 * pass + oc, n = n0 + t;
             const bool valid = n < N;
-            float xq[8] = {}, xk[8] = {}, xv[8] = {}, xu[8] = {};
+            float xv[8] = {}, xu[8] = {};
+            h8 hq = {0, 0, 0, 0, 0, 0, 0, 0}, hk = hq;
             float r = 0.f;
             if (valid) {
-                bf16x8_to_f32(*(const uint4 *)(q + (size_t)n * D + 8 * cg), xq);
-                bf16x8_to_f32(*(const uint4 *)(k + (size_t)n * D + 8 * cg), xk);
+                hq = *(const h8 *)(q + (size_t)n * D + 8 * cg);
+                hk = *(const h8 *)(k + (size_t)n * D + 8 * cg);
                 bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + 8 * cg), xv);
                 bf16x8_to_f32(*(const uint4 *)(dout + (size_t)n * D + 8 * cg), xu);
                 r = rg[n];
             }
-            const h8 hq = standardise8(xq, valid), hk = standardise8(xk, valid);
             h8 hv, hu;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -325,8 +373,8 @@ struct GSmem {
 
 template <int DIR>
 __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
-                                        const bf16_t *__restrict__ x,
-                                        const bf16_t *__restrict__ y,
+                                        const _Float16 *__restrict__ x,
+                                        const _Float16 *__restrict__ y,
                                         const bf16_t *__restrict__ z,
                                         const bf16_t *__restrict__ wv,
                                         const float *__restrict__ rg,
@@ -376,11 +424,12 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         h = lane >> 4;
     };
 
-    f4 acc[MG_MPW][4];
+    // X3 of the wave's channels in fp16, paired per contraction K step (j
+    // tiles 2p, 2p+1); rebuilt in fp32 for each update (one MFMA per tile
+    // against a 0/1 permutation matrix) and rounded back once per chunk
+    h8 Ast[MG_MPW][2];
 #pragma unroll
-    for (int m = 0; m < MG_MPW; ++m)
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt) acc[m][jt] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int m = 0; m < MG_MPW; ++m) Ast[m][0] = Ast[m][1] = h8{0, 0, 0, 0, 0, 0, 0, 0};
     // extra tiles (waves 0-3): wave 0 M1 (j tiles 0,1) and M1G; wave 1 M1 (j
     // tiles 2,3); waves 2,3 X3G = sum_s w_D y^_sm y^_sl for m tiles 2(w-2),
     // 2(w-2)+1; kept in LDS between uses
@@ -422,8 +471,7 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
             const int t = 2 * tg + e;
             const bool valid = c * C + t < N;
             float f[8];
-            bf16x8_to_f32(px[e], f);
-            *(h8 *)(sm.xrow + sw64(t, 8 * cg)) = standardise8(f, valid);
+            *(h8 *)(sm.xrow + sw64(t, 8 * cg)) = __builtin_bit_cast(h8, px[e]);
             const float zs = (DIR ? 1.0f : prg[e]) * sz;
             bf16x8_to_f32(pz[e], f);
             h8 hz;
@@ -442,8 +490,7 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
             const int t = 2 * tg + e;
             const bool valid = c * C + t < N;
             float f[8];
-            bf16x8_to_f32(py[e], f);
-            hy[e] = standardise8(f, valid);
+            hy[e] = __builtin_bit_cast(h8, py[e]);
             const float ws = (DIR ? prg[e] : 1.0f) * sw;
             bf16x8_to_f32(pw[e], f);
 #pragma unroll
@@ -470,61 +517,48 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         // ---- (A) contraction of chunk c with the moments of earlier chunks --
         if (kk > 0) {
             if (w == 0 && h == 0) sm.m1g[r16] = sm.ex[0][2][lane][0];
-            // two passes over the wave's channels m = 8w + 4mh .. +3; the
-            // partial sums of the first pass wait in this wave's LDS slot
-#pragma unroll
-            for (int mh = 0; mh < 2; ++mh) {
-                h8 Ast[4][2];
-#pragma unroll
-                for (int mm = 0; mm < 4; ++mm)
-#pragma unroll
-                    for (int p = 0; p < 2; ++p)
-                        Ast[mm][p] = cat(cvt4(acc[4 * mh + mm][2 * p]), cvt4(acc[4 * mh + mm][2 * p + 1]));
-                h8 Aex = {0, 0, 0, 0, 0, 0, 0, 0};
-                if (mh == 1 && w < 4) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
+            h8 Aex = {0, 0, 0, 0, 0, 0, 0, 0};
+            if (w < 4) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
 #pragma unroll 1
-                for (int rt = 0; rt < C / 16; ++rt) {
-                    const int t = 16 * rt + r16;
-                    const h4 xv = ld4(sm.xrow + sw64(t, MG_MPW * w + 4 * mh));
-                    h8 Zb[2];
+            for (int rt = 0; rt < C / 16; ++rt) {
+                const int t = 16 * rt + r16;
+                const h8 xv = ld8(sm.xrow + sw64(t, MG_MPW * w));
+                h8 Zb[2];
 #pragma unroll
-                    for (int p = 0; p < 2; ++p)
-                        Zb[p] = cat(ld4(sm.zrow + sw64(t, 32 * p + 4 * h)),
-                                    ld4(sm.zrow + sw64(t, 32 * p + 16 + 4 * h)));
-                    f4 *slot = (f4 *)(sm.fpart + ((w * 4 + h) * C + t) * 4);
-                    f4 Dout = {0.f, 0.f, 0.f, 0.f};
-                    if (mh == 1) Dout = *slot;
+                for (int p = 0; p < 2; ++p)
+                    Zb[p] = cat(ld4(sm.zrow + sw64(t, 32 * p + 4 * h)),
+                                ld4(sm.zrow + sw64(t, 32 * p + 16 + 4 * h)));
+                f4 Dout = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int mm = 0; mm < 4; ++mm) {
-                        f4 E = {0.f, 0.f, 0.f, 0.f};
-                        E = mfma(Ast[mm][0], Zb[0], E);
-                        E = mfma(Ast[mm][1], Zb[1], E);
-                        const float xm = (float)xv[mm];
+                for (int mm = 0; mm < MG_MPW; ++mm) {
+                    f4 E = {0.f, 0.f, 0.f, 0.f};
+                    E = mfma(Ast[mm][0], Zb[0], E);
+                    E = mfma(Ast[mm][1], Zb[1], E);
+                    const float xm = (float)xv[mm];
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) Dout[i] = fmaf(xm, E[i], Dout[i]);
-                    }
-                    if (mh == 1 && w < 4) {
-                        const float zd = sm.zD[t];
-                        if (w < 2) {
-                            // z at this wave's M1 column pair
-                            const h8 Zw = cat(ld4(sm.zrow + sw64(t, 32 * w + 4 * h)),
-                                              ld4(sm.zrow + sw64(t, 32 * w + 16 + 4 * h)));
-                            Dout = mfma(Aex, Zw, Dout);
-                            if (w == 0) {
-#pragma unroll
-                                for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, sm.m1g[4 * h + i], Dout[i]);
-                            }
-                        } else {
-                            const h8 Xb = cat(ld4(sm.xrow + sw64(t, 32 * (w - 2) + 4 * h)),
-                                              ld4(sm.xrow + sw64(t, 32 * (w - 2) + 16 + 4 * h)));
-                            f4 Eg = {0.f, 0.f, 0.f, 0.f};
-                            Eg = mfma(Aex, Xb, Eg);
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, Eg[i], Dout[i]);
-                        }
-                    }
-                    *slot = Dout;
+                    for (int i = 0; i < 4; ++i) Dout[i] = fmaf(xm, E[i], Dout[i]);
                 }
+                if (w < 4) {
+                    const float zd = sm.zD[t];
+                    if (w < 2) {
+                        // z at this wave's M1 column pair
+                        const h8 Zw = cat(ld4(sm.zrow + sw64(t, 32 * w + 4 * h)),
+                                          ld4(sm.zrow + sw64(t, 32 * w + 16 + 4 * h)));
+                        Dout = mfma(Aex, Zw, Dout);
+                        if (w == 0) {
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, sm.m1g[4 * h + i], Dout[i]);
+                        }
+                    } else {
+                        const h8 Xb = cat(ld4(sm.xrow + sw64(t, 32 * (w - 2) + 4 * h)),
+                                          ld4(sm.xrow + sw64(t, 32 * (w - 2) + 16 + 4 * h)));
+                        f4 Eg = {0.f, 0.f, 0.f, 0.f};
+                        Eg = mfma(Aex, Xb, Eg);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, Eg[i], Dout[i]);
+                    }
+                }
+                *(f4 *)(sm.fpart + ((w * 4 + h) * C + t) * 4) = Dout;
             }
         }
         __syncthreads();
@@ -547,7 +581,21 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         }
         if (more) prefetch(chunk_of(kk + 1));
         {
-            // moments += chunk c, 32 tokens per K step
+            // moments += chunk c, 32 tokens per K step, on fp32 tiles rebuilt
+            // from the fp16 pairs
+            h8 pa = {0, 0, 0, 0, 0, 0, 0, 0}, pb = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const bool on = h == (r16 >> 2) && jj == (r16 & 3);
+                pa[jj] = on ? (_Float16)1.0f : (_Float16)0.0f;
+                pb[4 + jj] = on ? (_Float16)1.0f : (_Float16)0.0f;
+            }
+            f4 acc[MG_MPW][4];
+#pragma unroll
+            for (int m = 0; m < MG_MPW; ++m)
+#pragma unroll
+                for (int jt = 0; jt < 4; ++jt)
+                    acc[m][jt] = mfma((jt & 1) ? pb : pa, Ast[m][jt >> 1], f4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll 1
             for (int ks = 0; ks < C / 32; ++ks) {
                 const int col = 32 * ks + 8 * h;
@@ -587,6 +635,10 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
                     for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = ex[e];
                 }
             }
+#pragma unroll
+            for (int m = 0; m < MG_MPW; ++m)
+#pragma unroll
+                for (int p = 0; p < 2; ++p) Ast[m][p] = cat(cvt4(acc[m][2 * p]), cvt4(acc[m][2 * p + 1]));
         }
         if (more) stage_xz(chunk_of(kk + 1));
         __syncthreads();
@@ -600,8 +652,8 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
 
 // Both scans in one launch: blocks [0, 4BH) build dq^ (chunks in order),
 // blocks [4BH, 8BH) build dk^ (chunks in reverse order).
-__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const bf16_t *__restrict__ q,
-                                                          const bf16_t *__restrict__ k,
+__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__restrict__ q,
+                                                          const _Float16 *__restrict__ k,
                                                           const bf16_t *__restrict__ v,
                                                           const bf16_t *__restrict__ dout,
                                                           const float *__restrict__ rg,
@@ -721,7 +773,8 @@ size_t mfma_causal_bwd_workspace(int BH, int N)
     const size_t rows = (size_t)BH * N;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t nch = ((size_t)N + mfma_bwd::C - 1) / mfma_bwd::C;
-    return a256(rows * 4) * 2 + a256((size_t)BH * nch * 16) + 2 * a256(rows * mx::D * 4);
+    return a256(rows * 4) * 2 + a256((size_t)BH * nch * 16) + 2 * a256(rows * mx::D * 4) +
+           2 * a256(rows * mx::D * 2) + 2 * a256(rows * 4);
 }
 
 hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
@@ -746,11 +799,19 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     float *dqh = (float *)p;
     p += a256(rows * D * 4);
     float *dkh = (float *)p;
+    p += a256(rows * D * 4);
+    _Float16 *qh = (_Float16 *)p;
+    p += a256(rows * D * 2);
+    _Float16 *kh = (_Float16 *)p;
+    p += a256(rows * D * 2);
+    float *rsq = (float *)p;
+    p += a256(rows * 4);
+    float *rsk = (float *)p;
 
     const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
     const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
-    hipLaunchKernelGGL(bwd_prep, dim3(BH * nch), dim3(256), 0, st, O, DO, V, g, rg, cc, hmax, N,
-                       nch);
+    hipLaunchKernelGGL(bwd_prep, dim3(BH * nch), dim3(256), 0, st, Q, K, O, DO, V, g, rg, cc, hmax,
+                       qh, kh, rsq, rsk, N, nch);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // dv (reverse-causal scan, needs only rg) runs on a side stream next to
@@ -766,7 +827,7 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     if (e != hipSuccess) return e;
     e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
     if (e != hipSuccess) return e;
-    const hipError_t edv = mfma_causal_dv(q, k, dout, rg, dv, BH, N, ss->stream);
+    const hipError_t edv = mfma_causal_dv(qh, kh, dout, rg, dv, BH, N, ss->stream);
     e = hipEventRecord(ss->join, ss->stream);
     if (e == hipSuccess && edv != hipSuccess) {
         hipStreamWaitEvent(st, ss->join, 0);
@@ -779,15 +840,15 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)sizeof(ISmem));
         if (r != hipSuccess) return r;
-        hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(512), sizeof(ISmem), st, Q, K, V, DO,
-                           rg, cc, hmax, dqh, dkh, N, nch);
+        hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(512), sizeof(ISmem), st, qh, kh, V,
+                           DO, rg, cc, hmax, dqh, dkh, N, nch);
         r = hipGetLastError();
         if (r != hipSuccess) return r;
         r = hipFuncSetAttribute((const void *)bwd_mg_scans,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
         if (r != hipSuccess) return r;
-        hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, Q, K, V,
-                           DO, rg, cc, hmax, dqh, dkh, N, BH);
+        hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, qh, kh,
+                           V, DO, rg, cc, hmax, dqh, dkh, N, BH);
         r = hipGetLastError();
         if (r != hipSuccess) return r;
         hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q,

@@ -127,9 +127,10 @@ __device__ __forceinline__ h8 set_half(h8 x, h4 r)
 // DV = false: the forward O = F / G.  DV = true: the reverse-causal
 // numerator of the backward, dv_n = sum_{i >= n} f(k^_n . q^_i) u_i with
 // u_i = dO_i / G_i (Sec. 2.5): the scan runs over the tokens in reverse order
-// (logical token n is row N-1-n), q and k trade roles (the caller passes k as
-// q and q as k), v is dO scaled per row by rg = 1/G, and F is stored without
-// the divide; the denominator terms are skipped.
+// (logical token n is row N-1-n), q and k trade roles (the caller passes k^ as
+// q and q^ as k, both already standardised, in fp16), v is dO scaled per row
+// by rg = 1/G, and F is stored without the divide; the denominator terms are
+// skipped.
 template <bool DV>
 __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__restrict__ q,
                                                             const bf16_t *__restrict__ k,
@@ -372,15 +373,24 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
                 const int row = 4 * tg + j;
                 const bool valid = c * C + row < N;
                 float x[8];
-                bf16x8_to_f32(pq[j], x);
-                const h8 hq = standardise8(x, valid);
+                h8 hq;
+                if constexpr (DV) {
+                    hq = __builtin_bit_cast(h8, pq[j]);   // already standardised
+                } else {
+                    bf16x8_to_f32(pq[j], x);
+                    hq = standardise8(x, valid);
+                }
                 *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
                 // channel 8cg + ww -> state wave ww, index 2cg; 8cg + 4 + ww -> 2cg + 1
 #pragma unroll
                 for (int ww = 0; ww < 4; ++ww)
                     *(h2 *)(sm.qperm + sw64(row, 16 * ww + 2 * cg)) = h2{hq[ww], hq[4 + ww]};
-                bf16x8_to_f32(pk[j], x);
-                hk[j] = standardise8(x, valid);
+                if constexpr (DV) {
+                    hk[j] = __builtin_bit_cast(h8, pk[j]);
+                } else {
+                    bf16x8_to_f32(pk[j], x);
+                    hk[j] = standardise8(x, valid);
+                }
                 *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
             }
 #pragma unroll
@@ -569,7 +579,7 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
     return hipGetLastError();
 }
 
-hipError_t mfma_causal_dv(const void *q, const void *k, const void *dout, const float *rg,
+hipError_t mfma_causal_dv(const void *qh, const void *kh, const void *dout, const float *rg,
                           void *dv, int BH, int N, hipStream_t st)
 {
     using namespace mfma_causal;
@@ -577,9 +587,10 @@ hipError_t mfma_causal_dv(const void *q, const void *k, const void *dout, const 
     hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel<true>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    // queries of this scan are the keys k (and vice versa), values dO / G
+    // queries of this scan are the keys k^ (and vice versa), values dO / G;
+    // the 16-bit rows are passed through as raw bits
     hipLaunchKernelGGL(fwd_causal_kernel<true>, dim3(BH * NSL), dim3(NTH), smem, st,
-                       (const bf16_t *)k, (const bf16_t *)q, (const bf16_t *)dout, (bf16_t *)dv,
+                       (const bf16_t *)kh, (const bf16_t *)qh, (const bf16_t *)dout, (bf16_t *)dv,
                        (float *)nullptr, rg, N, BH);
     return hipGetLastError();
 }
