@@ -72,7 +72,9 @@ enum {
  * denominator terms, about 0.7 MB per (head, segment)), and every other
  * non-MFMA forward when B*H is small (fp32 segment states, enough segments
  * for about 256 workgroups).  The causal bf16, D = 64, p = 2 forward needs
- * none.
+ * none.  The backward always needs one: per token 1/G, c = dO.O/G, the fp32
+ * gradient accumulators of q^ and k^ and (causal bf16, D = 64, p = 2) the
+ * standardised q^, k^ in fp16, plus per-chunk maxima.
  */
 size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
                                fastmax_dtype_t dt, int backward);

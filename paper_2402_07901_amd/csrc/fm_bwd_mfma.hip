@@ -42,36 +42,12 @@ using namespace mx;
 
 constexpr int C = 128;   // tokens per chunk
 
-// standardise8 that also returns the reciprocal standard deviation
-__device__ __forceinline__ h8 standardise8_rs(const float *xin, float &rs)
-{
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) s += xin[i];
-    const float mu = octet_sum(s) * (1.0f / D);
-    float x[8], var = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        x[i] = xin[i] - mu;
-        var = fmaf(x[i], x[i], var);
-    }
-    rs = __builtin_amdgcn_rsqf(octet_sum(var) * (1.0f / D));
-    h8 o;
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-        const h2 pr = {(_Float16)(x[i] * rs), (_Float16)(x[i + 1] * rs)};
-        o[i] = pr[0];
-        o[i + 1] = pr[1];
-    }
-    return o;
-}
-
 // ---------------------------------------------------------------------------
 // bwd_prep: one workgroup per (head, 128-token chunk), an octet of lanes per
 // token; per-chunk maxima go to pmax[head][chunk][4].  Also standardises q and
-// k once for the whole backward (Sec. 2.2, Eqs. 6-7): q^, k^ in fp16 and the
-// reciprocal standard deviations, which the later kernels read instead of
-// recomputing them.
+// k once for the whole backward (Sec. 2.2, Eqs. 6-7): q^, k^ in fp16, which
+// the scans read instead of recomputing them (bwd_finish, which needs them in
+// fp32 for the cancellation-prone standardisation backward, recomputes them).
 
 __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
                                                 const bf16_t *__restrict__ k,
@@ -81,9 +57,7 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
                                                 const float *__restrict__ g,
                                                 float *__restrict__ rg, float *__restrict__ cc,
                                                 float *__restrict__ pmax, _Float16 *__restrict__ qh,
-                                                _Float16 *__restrict__ kh,
-                                                float *__restrict__ rsq, float *__restrict__ rsk,
-                                                int N, int nch)
+                                                _Float16 *__restrict__ kh, int N, int nch)
 {
     __shared__ float red[3][4];
     const int head = blockIdx.x / nch, c = blockIdx.x % nch, tid = threadIdx.x;
@@ -92,8 +66,6 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
     k += hb * D;
     qh += hb * D;
     kh += hb * D;
-    rsq += hb;
-    rsk += hb;
     o += hb * D;
     dout += hb * D;
     v += hb * D;
@@ -130,13 +102,10 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
         }
         if (valid) {
             float x[8];
-            float rs;
             bf16x8_to_f32(*(const uint4 *)(q + (size_t)n * D + 8 * cg), x);
-            *(h8 *)(qh + (size_t)n * D + 8 * cg) = standardise8_rs(x, rs);
-            if (cg == 0) rsq[n] = rs;
+            *(h8 *)(qh + (size_t)n * D + 8 * cg) = standardise8(x, true);
             bf16x8_to_f32(*(const uint4 *)(k + (size_t)n * D + 8 * cg), x);
-            *(h8 *)(kh + (size_t)n * D + 8 * cg) = standardise8_rs(x, rs);
-            if (cg == 0) rsk[n] = rs;
+            *(h8 *)(kh + (size_t)n * D + 8 * cg) = standardise8(x, true);
         }
     }
 #pragma unroll
@@ -774,7 +743,7 @@ size_t mfma_causal_bwd_workspace(int BH, int N)
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t nch = ((size_t)N + mfma_bwd::C - 1) / mfma_bwd::C;
     return a256(rows * 4) * 2 + a256((size_t)BH * nch * 16) + 2 * a256(rows * mx::D * 4) +
-           2 * a256(rows * mx::D * 2) + 2 * a256(rows * 4);
+           2 * a256(rows * mx::D * 2);
 }
 
 hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
@@ -803,15 +772,11 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     _Float16 *qh = (_Float16 *)p;
     p += a256(rows * D * 2);
     _Float16 *kh = (_Float16 *)p;
-    p += a256(rows * D * 2);
-    float *rsq = (float *)p;
-    p += a256(rows * 4);
-    float *rsk = (float *)p;
 
     const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
     const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
     hipLaunchKernelGGL(bwd_prep, dim3(BH * nch), dim3(256), 0, st, Q, K, O, DO, V, g, rg, cc, hmax,
-                       qh, kh, rsq, rsk, N, nch);
+                       qh, kh, N, nch);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // dv (reverse-causal scan, needs only rg) runs on a side stream next to
