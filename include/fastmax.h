@@ -71,8 +71,9 @@ enum {
  * N >= 128 (per-segment partial moments, their fp16 sum and the per-head
  * denominator terms, about 0.7 MB per (head, segment)), and every other
  * non-MFMA forward when B*H is small (fp32 segment states, enough segments
- * for about 256 workgroups).  The causal bf16, D = 64, p = 2 forward needs
- * none.  The backward always needs one: per token 1/G, c = dO.O/G, the fp32
+ * for about 256 workgroups).  The causal bf16, D = 64, p = 2 forward keeps
+ * the standardised q and k in fp16 (256 bytes per row).  The backward always
+ * needs one: per token 1/G, c = dO.O/G, the fp32
  * gradient accumulators of q^ and k^ and (causal bf16, D = 64, p = 2) the
  * standardised q^, k^ in fp16, plus per-chunk maxima.
  */

@@ -42,7 +42,7 @@ bool mfma_causal(int D, int p, int causal, fastmax_dtype_t dt)
 
 size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
 {
-    if (mfma_causal(D, p, causal, dt)) return 0;
+    if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_fwd_workspace(B * H, N);
     if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_workspace(B * H, N);
     return fm::generic_fwd_workspace(B * H, N, D, p);
 }
@@ -79,7 +79,7 @@ int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
     hipError_t e;
     if (mfma_causal(D, p, causal, dt))
-        e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, stream);
+        e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, workspace, stream);
     else if (mfma_noncausal(N, D, p, causal, dt))
         e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, workspace, stream);
     else

@@ -12,8 +12,9 @@
 //    against it: the query contraction F^T += S^T Psi(Q)^T (Psi generated in
 //    registers with packed fp16 multiplies) and the state update
 //    S += Phi(K)^T V;
-//  * helper waves 4..7 stage the next chunk (standardisation, Eqs. 6-7;
-//    transposes), compute the in-chunk block tril(f(Q K^T)) V on MFMA and
+//  * helper waves 4..7 stage the next chunk (q^ and k^, standardised once per
+//    call by standardise_qk (Sec. 2.2, Eqs. 6-7) and read in fp16; transposes;
+//    scaled v), compute the in-chunk block tril(f(Q K^T)) V on MFMA and
 //    the denominators G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sums,
 //    and combine the partial numerators into O = F / G.
 // Per chunk there are two phases separated by barriers: (1) query
@@ -28,6 +29,8 @@
 // rounds back to fp16 once per chunk.  Diagonal tiles are stored halved (the
 // 1/2 of f_2), and rebuilt with a 0/2 matrix.
 #include <hip/hip_runtime.h>
+
+#include <limits.h>
 
 #include <type_traits>
 
@@ -132,8 +135,8 @@ __device__ __forceinline__ h8 set_half(h8 x, h4 r)
 // by rg = 1/G, and F is stored without the divide; the denominator terms are
 // skipped.
 template <bool DV>
-__global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__restrict__ q,
-                                                            const bf16_t *__restrict__ k,
+__global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const _Float16 *__restrict__ q,
+                                                            const _Float16 *__restrict__ k,
                                                             const bf16_t *__restrict__ v,
                                                             bf16_t *__restrict__ out,
                                                             float *__restrict__ g,
@@ -360,9 +363,10 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
                 if constexpr (DV) prg = rg[pn];
             }
         };
-        // Staging of chunk c (Sec. 2.2, Eqs. 6-7): standardise q and k rows,
-        // store q^ (row-major and channel-permuted), k^ (row-major and
-        // transposed) and the scaled v transposed.
+        // Staging of chunk c: store q^ (row-major and channel-permuted), k^
+        // (row-major and transposed) and the scaled v transposed.  q^, k^
+        // arrive standardised (Sec. 2.2, Eqs. 6-7) in fp16; rows past N are
+        // zero.
         auto stage = [&](int c) {
             const int ht = tid - NSW * 64;
             const int tg = ht >> 3, cg = ht & 7;
@@ -371,26 +375,13 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int row = 4 * tg + j;
-                const bool valid = c * C + row < N;
-                float x[8];
-                h8 hq;
-                if constexpr (DV) {
-                    hq = __builtin_bit_cast(h8, pq[j]);   // already standardised
-                } else {
-                    bf16x8_to_f32(pq[j], x);
-                    hq = standardise8(x, valid);
-                }
+                const h8 hq = __builtin_bit_cast(h8, pq[j]);
                 *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
                 // channel 8cg + ww -> state wave ww, index 2cg; 8cg + 4 + ww -> 2cg + 1
 #pragma unroll
                 for (int ww = 0; ww < 4; ++ww)
                     *(h2 *)(sm.qperm + sw64(row, 16 * ww + 2 * cg)) = h2{hq[ww], hq[4 + ww]};
-                if constexpr (DV) {
-                    hk[j] = __builtin_bit_cast(h8, pk[j]);
-                } else {
-                    bf16x8_to_f32(pk[j], x);
-                    hk[j] = standardise8(x, valid);
-                }
+                hk[j] = __builtin_bit_cast(h8, pk[j]);
                 *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
             }
 #pragma unroll
@@ -559,23 +550,59 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const bf16_t *__rest
     }
 }
 
+// q^, k^ (Sec. 2.2, Eqs. 6-7) in fp16 for the scan: an octet of lanes per row,
+// 32 rows per workgroup.
+__global__ __launch_bounds__(256) void standardise_qk(const bf16_t *__restrict__ q,
+                                                      const bf16_t *__restrict__ k,
+                                                      _Float16 *__restrict__ qh,
+                                                      _Float16 *__restrict__ kh, size_t rows)
+{
+    const size_t r = (size_t)blockIdx.x * 32 + (threadIdx.x >> 3);
+    const int cg = threadIdx.x & 7;
+    const bool valid = r < rows;
+    float xq[8] = {}, xk[8] = {};
+    if (valid) {
+        bf16x8_to_f32(*(const uint4 *)(q + r * D + 8 * cg), xq);
+        bf16x8_to_f32(*(const uint4 *)(k + r * D + 8 * cg), xk);
+    }
+    const h8 hq = standardise8(xq, valid), hk = standardise8(xk, valid);
+    if (valid) {
+        *(h8 *)(qh + r * D + 8 * cg) = hq;
+        *(h8 *)(kh + r * D + 8 * cg) = hk;
+    }
+}
+
 }  // namespace mfma_causal
+
+size_t mfma_causal_fwd_workspace(int BH, int N)
+{
+    const size_t rows = (size_t)BH * N;
+    return 2 * (((rows * mx::D * 2) + 255) & ~(size_t)255);
+}
 
 size_t mfma_causal_smem_bytes() { return sizeof(mfma_causal::Smem); }
 
 hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
-                           int BH, int N, hipStream_t st)
+                           int BH, int N, void *ws, hipStream_t st)
 {
     using namespace mfma_causal;
     static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
     static_assert(NHT == 2 * C, "one helper thread per (token pair, v half)");
+    const size_t rows = (size_t)BH * N;
+    if ((rows + 31) / 32 > (size_t)INT_MAX) return hipErrorInvalidConfiguration;
+    _Float16 *qh = (_Float16 *)ws;
+    _Float16 *kh = (_Float16 *)((unsigned char *)ws + mfma_causal_fwd_workspace(BH, N) / 2);
+    hipLaunchKernelGGL(standardise_qk, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st,
+                       (const bf16_t *)q, (const bf16_t *)k, qh, kh, rows);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     const size_t smem = sizeof(Smem);
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel<false>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    e = hipFuncSetAttribute((const void *)fwd_causal_kernel<false>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fwd_causal_kernel<false>, dim3(BH * NSL), dim3(NTH), smem, st,
-                       (const bf16_t *)q, (const bf16_t *)k, (const bf16_t *)v, (bf16_t *)out, g,
-                       (const float *)nullptr, N, BH);
+                       (const _Float16 *)qh, (const _Float16 *)kh, (const bf16_t *)v,
+                       (bf16_t *)out, g, (const float *)nullptr, N, BH);
     return hipGetLastError();
 }
 
@@ -587,11 +614,10 @@ hipError_t mfma_causal_dv(const void *qh, const void *kh, const void *dout, cons
     hipError_t e = hipFuncSetAttribute((const void *)fwd_causal_kernel<true>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    // queries of this scan are the keys k^ (and vice versa), values dO / G;
-    // the 16-bit rows are passed through as raw bits
+    // queries of this scan are the keys k^ (and vice versa), values dO / G
     hipLaunchKernelGGL(fwd_causal_kernel<true>, dim3(BH * NSL), dim3(NTH), smem, st,
-                       (const bf16_t *)kh, (const bf16_t *)qh, (const bf16_t *)dout, (bf16_t *)dv,
-                       (float *)nullptr, rg, N, BH);
+                       (const _Float16 *)kh, (const _Float16 *)qh, (const bf16_t *)dout,
+                       (bf16_t *)dv, (float *)nullptr, rg, N, BH);
     return hipGetLastError();
 }
 

@@ -18,8 +18,10 @@ hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *
 size_t generic_bwd_workspace(int B, int H, int N, int D);
 
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
+// ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16.
 hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
-                           int BH, int N, hipStream_t st);
+                           int BH, int N, void *ws, hipStream_t st);
+size_t mfma_causal_fwd_workspace(int BH, int N);
 size_t mfma_causal_smem_bytes();
 // The causal scan run in reverse on (k^, q^, dO / G) without the divide: dv.
 // qh, kh: the standardised q and k in fp16 (as bwd_prep writes them).

@@ -112,8 +112,11 @@ def test_fwd_workspace_checks():
     assert fwd(causal=0, N=1000, H=2, ws=A + 4, wsb=need) == fm.EALIGN
     # sized for the whole problem: grows with the number of heads and tokens
     assert fm.workspace_bytes(1, 8, 131072, 64, 2, False, fm.BF16, False) > need
-    # the causal MFMA scan needs none
-    assert fm.workspace_bytes(1, 2, 1000, 64, 2, True, fm.BF16, False) == 0
+    # the causal MFMA scan keeps q^ and k^ in fp16: 256 bytes per row
+    need_c = fm.workspace_bytes(1, 2, 1000, 64, 2, True, fm.BF16, False)
+    assert need_c >= 2 * 1000 * 256
+    assert fwd(causal=1, N=1000, H=2, ws=None, wsb=0) == fm.EWORKSPACE
+    assert fwd(causal=1, N=1000, H=2, ws=A, wsb=need_c - 1) == fm.EWORKSPACE
     # the generic kernels need segment states only when few heads must be
     # spread over the CUs; with many heads (>= 256 workgroups) none
     for D, p, causal, dt in ((64, 2, False, fm.F32), (32, 2, False, fm.BF16),
