@@ -194,3 +194,51 @@ def test_bwd_single_token():
         ak = float(np.abs(to_f64(dk)[0, hh, 0]).max())
         say(f"N=1 head {hh}: |dq|={aq:.3e} (bound {bq:.3e}) |dk|={ak:.3e} (bound {bk:.3e})")
         assert aq <= bq and ak <= bk
+
+
+def test_bwd_long_ragged_vs_brute():
+    """Backward over 33 chunks with a ragged tail (N = 4173): every chunk of
+    the forward and reverse moment scans, against the fp64 explicit backward."""
+    from test_parity_gpu import bwd_case
+    label = "mfma bwd B=1 H=1 N=4173"
+    say(label)
+    inp = make_inputs(1, 1, 4173, 64, 4173, "bf16", with_dout=True)
+    bwd_case(inp, 2, True, "bf16", label=label)
+
+
+def test_bwd_deterministic():
+    """The backward has one writer per output element (no atomics): two calls
+    give bit-identical gradients."""
+    import torch
+    inp = make_inputs(2, 3, 1500, 64, 31, "bf16", with_dout=True)
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "dout"))
+    o, g = fm.fastmax_fwd(q, k, v, p=2, causal=True)
+    r1 = fm.fastmax_bwd(q, k, v, o, do, g, p=2, causal=True)
+    r2 = fm.fastmax_bwd(q, k, v, o, do, g, p=2, causal=True)
+    torch.cuda.synchronize()
+    for a, b in zip(r1, r2):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_user_stream_ordering():
+    """Forward and backward enqueued on a caller's non-default stream (the
+    backward forks part of its work onto the library's side stream and joins
+    it back): results equal the default-stream ones, and work the caller
+    enqueues after the call on its stream sees the finished outputs."""
+    import torch
+    inp = make_inputs(1, 4, 2000, 64, 47, "bf16", with_dout=True)
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "dout"))
+    o0, g0 = fm.fastmax_fwd(q, k, v, p=2, causal=True)
+    ref = fm.fastmax_bwd(q, k, v, o0, do, g0, p=2, causal=True)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        o1, g1 = fm.fastmax_fwd(q, k, v, p=2, causal=True, stream=s)
+        got = fm.fastmax_bwd(q, k, v, o1, do, g1, p=2, causal=True, stream=s)
+        # consumers on the same stream, before any host synchronisation
+        sums = [x.float().sum() for x in got]
+    s.synchronize()
+    assert torch.equal(o0.view(torch.int16), o1.view(torch.int16))
+    for a, b, sm in zip(ref, got, sums):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        assert float(sm) == float(b.float().sum())
