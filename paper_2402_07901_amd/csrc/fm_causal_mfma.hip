@@ -79,11 +79,9 @@ __host__ __device__ constexpr Tile tile_of(int t)
         if (t < first_tile(i) + 4 - u0_of(i)) return Tile{1, i, u0_of(i) + t - first_tile(i)};
     return Tile{-1, -1, -1};
 }
-__host__ __device__ constexpr bool is_diag(int t)
-{
-    return t < NT && tile_of(t).kind == 1 && tile_of(t).u == u0_of(tile_of(t).i);
-}
 static_assert(NT == 41 && tile_of(40).kind == 1 && tile_of(41).kind == -1, "tile pattern");
+// The first tile of each channel (u = i/4) is its diagonal tile.
+static_assert(tile_of(first_tile(5)).u == u0_of(5) && tile_of(first_tile(5)).i == 5, "tile pattern");
 
 // Y3 tiles (u <= u2), 10 of them: helpers 0 and 1 own three, 2 and 3 two.
 __device__ __forceinline__ int y3_count(int hw) { return hw < 2 ? 3 : 2; }
