@@ -12,7 +12,8 @@
 //
 // Kernels:
 //  bwd_prep     1/G, c per token; per head max|u|, max|v|, max|c| (fp16 scales).
-//  (dv)         the causal scan kernel run in reverse with values u (no divide).
+//  (dv)         the causal scan run in reverse with values u (no divide),
+//               launched together with bwd_intra.
 //  bwd_intra    in-chunk pairs (both n <= i inside a 128-token chunk) of dq^ and
 //               dk^ on MFMA; initialises the fp32 accumulators dq^, dk^.
 //  bwd_mg_scan  the inter-chunk part, one kernel for both gradients:
@@ -29,8 +30,7 @@
 
 #include <limits.h>
 
-#include <mutex>
-
+#include "fm_causal_scan.h"
 #include "fm_common.h"
 #include "fm_internal.h"
 #include "fm_mfma.h"
@@ -157,19 +157,17 @@ struct ISmem {
     float cc[C];
 };
 
-__global__ __launch_bounds__(512) void bwd_intra(const _Float16 *__restrict__ q,
-                                                 const _Float16 *__restrict__ k,
-                                                 const bf16_t *__restrict__ v,
-                                                 const bf16_t *__restrict__ dout,
-                                                 const float *__restrict__ rg,
-                                                 const float *__restrict__ cc,
-                                                 const float *__restrict__ hmax,
-                                                 float *__restrict__ dqh, float *__restrict__ dkh,
-                                                 int N, int nch)
+__device__ __forceinline__ void intra_block(ISmem &sm, const _Float16 *__restrict__ q,
+                                            const _Float16 *__restrict__ k,
+                                            const bf16_t *__restrict__ v,
+                                            const bf16_t *__restrict__ dout,
+                                            const float *__restrict__ rg,
+                                            const float *__restrict__ cc,
+                                            const float *__restrict__ hmax,
+                                            float *__restrict__ dqh, float *__restrict__ dkh, int N,
+                                            int nch, int blk)
 {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    ISmem &sm = *reinterpret_cast<ISmem *>(smem_raw);
-    const int head = blockIdx.x / nch, c = blockIdx.x % nch;
+    const int head = blk / nch, c = blk % nch;
     const int n0 = c * C;
     const size_t hb = (size_t)head * N;
     q += hb * D;
@@ -619,10 +617,10 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
     }
 }
 
-// Both scans in one launch: blocks [0, 4BH) build dq^ (chunks in order),
-// blocks [4BH, 8BH) build dk^ (chunks in reverse order).
-__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__restrict__ q,
-                                                          const _Float16 *__restrict__ k,
+// Both moment-gradient scans in one launch: blocks [0, 4BH) build dq^ (chunks
+// in order), blocks [4BH, 8BH) build dk^ (chunks in reverse order).
+__global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__restrict__ qh,
+                                                          const _Float16 *__restrict__ kh,
                                                           const bf16_t *__restrict__ v,
                                                           const bf16_t *__restrict__ dout,
                                                           const float *__restrict__ rg,
@@ -636,9 +634,39 @@ __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__rest
     const int half = 4 * BH;
     const int b = blockIdx.x;
     if (b < half)
-        mg_scan<0>(sm, b, half, q, k, dout, v, rg, cc, hmax, dqh, N, BH);
+        mg_scan<0>(sm, b, half, qh, kh, dout, v, rg, cc, hmax, dqh, N, BH);
     else
-        mg_scan<1>(sm, b - half, half, k, q, v, dout, rg, cc, hmax, dkh, N, BH);
+        mg_scan<1>(sm, b - half, half, kh, qh, v, dout, rg, cc, hmax, dkh, N, BH);
+}
+
+// dv and the in-chunk pairs in one launch: blocks [0, 4BH) run the causal scan
+// in reverse for dv (fm_causal_scan.h), the rest are the in-chunk blocks
+// (head, chunk).  The short in-chunk blocks come last and fill the CUs the
+// dv blocks leave idle in their last, partly filled round.
+__global__ __launch_bounds__(512, 2) void bwd_dv_intra(const _Float16 *__restrict__ qh,
+                                                       const _Float16 *__restrict__ kh,
+                                                       const bf16_t *__restrict__ v,
+                                                       const bf16_t *__restrict__ dout,
+                                                       const float *__restrict__ rg,
+                                                       const float *__restrict__ cc,
+                                                       const float *__restrict__ hmax,
+                                                       float *__restrict__ dqh,
+                                                       float *__restrict__ dkh,
+                                                       bf16_t *__restrict__ dv, int N, int nch,
+                                                       int BH)
+{
+    static_assert(mfma_causal::NTH == 512, "one block size for both");
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int ndv = 4 * BH;
+    const int b = blockIdx.x;
+    if (b < ndv) {
+        // queries of the dv scan are the keys k^ (and vice versa), values dO / G
+        mfma_causal::Smem &sm = *reinterpret_cast<mfma_causal::Smem *>(smem_raw);
+        mfma_causal::scan_block<true>(sm, kh, qh, dout, dv, nullptr, rg, N, BH, b, ndv);
+    } else {
+        ISmem &sm = *reinterpret_cast<ISmem *>(smem_raw);
+        intra_block(sm, qh, kh, v, dout, rg, cc, hmax, dqh, dkh, N, nch, b - ndv);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -703,40 +731,6 @@ __global__ __launch_bounds__(256) void bwd_finish(const bf16_t *__restrict__ q,
 
 }  // namespace mfma_bwd
 
-namespace {
-
-// One side stream (default priority, non-blocking) and a fork/join event pair
-// per device, created on first use and kept for the life of the process.
-struct SideStream {
-    hipStream_t stream = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
-    std::mutex mu;
-};
-constexpr int MAX_DEVICES = 64;
-SideStream g_side[MAX_DEVICES];
-std::once_flag g_side_once[MAX_DEVICES];
-hipError_t g_side_err[MAX_DEVICES];
-
-hipError_t side_stream(SideStream **out)
-{
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
-    std::call_once(g_side_once[dev], [dev]() {
-        SideStream &s = g_side[dev];
-        hipError_t r = hipStreamCreateWithFlags(&s.stream, hipStreamNonBlocking);
-        if (r == hipSuccess) r = hipEventCreateWithFlags(&s.fork, hipEventDisableTiming);
-        if (r == hipSuccess) r = hipEventCreateWithFlags(&s.join, hipEventDisableTiming);
-        g_side_err[dev] = r;
-    });
-    if (g_side_err[dev] != hipSuccess) return g_side_err[dev];
-    *out = &g_side[dev];
-    return hipSuccess;
-}
-
-}  // namespace
-
 size_t mfma_causal_bwd_workspace(int BH, int N)
 {
     const size_t rows = (size_t)BH * N;
@@ -751,10 +745,12 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                            int N, void *ws, hipStream_t st)
 {
     using namespace mfma_bwd;
-    static_assert(sizeof(ISmem) <= 160 * 1024 && sizeof(GSmem) <= 160 * 1024, "LDS budget");
+    static_assert(sizeof(ISmem) <= 160 * 1024 && sizeof(GSmem) <= 160 * 1024 &&
+                      sizeof(mfma_causal::Smem) <= 160 * 1024,
+                  "LDS budget");
     const size_t rows = (size_t)BH * N;
     const int nch = (N + C - 1) / C;
-    if ((long long)BH * nch > INT_MAX || (long long)BH * 8 > INT_MAX ||
+    if ((long long)BH * (nch + 4) > INT_MAX || (long long)BH * 8 > INT_MAX ||
         (rows + 31) / 32 > (size_t)INT_MAX)
         return hipErrorInvalidConfiguration;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -779,50 +775,25 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                        qh, kh, N, nch);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // dv (reverse-causal scan, needs only rg) runs on a side stream next to
-    // the in-chunk and moment-gradient kernels: its last, partly filled round
-    // of workgroups overlaps their work.  Fork and join through events; the
-    // enqueue sequence is serialised so that concurrent callers cannot
-    // interleave records and waits of the shared events.
-    SideStream *ss = nullptr;
-    e = side_stream(&ss);
+    const size_t smem1 = sizeof(ISmem) > sizeof(mfma_causal::Smem) ? sizeof(ISmem)
+                                                                    : sizeof(mfma_causal::Smem);
+    e = hipFuncSetAttribute((const void *)bwd_dv_intra,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem1);
     if (e != hipSuccess) return e;
-    std::lock_guard<std::mutex> lock(ss->mu);
-    e = hipEventRecord(ss->fork, st);
+    hipLaunchKernelGGL(bwd_dv_intra, dim3(BH * 4 + BH * nch), dim3(512), smem1, st, qh, kh, V, DO,
+                       rg, cc, hmax, dqh, dkh, (bf16_t *)dv, N, nch, BH);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
+    e = hipFuncSetAttribute((const void *)bwd_mg_scans,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
     if (e != hipSuccess) return e;
-    const hipError_t edv = mfma_causal_dv(qh, kh, dout, rg, dv, BH, N, ss->stream);
-    e = hipEventRecord(ss->join, ss->stream);
-    if (e == hipSuccess && edv != hipSuccess) {
-        hipStreamWaitEvent(st, ss->join, 0);
-        return edv;
-    }
+    hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, qh, kh, V,
+                       DO, rg, cc, hmax, dqh, dkh, N, BH);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // from here on every path joins the side stream before returning
-    auto rest = [&]() -> hipError_t {
-        hipError_t r = hipFuncSetAttribute((const void *)bwd_intra,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)sizeof(ISmem));
-        if (r != hipSuccess) return r;
-        hipLaunchKernelGGL(bwd_intra, dim3(BH * nch), dim3(512), sizeof(ISmem), st, qh, kh, V,
-                           DO, rg, cc, hmax, dqh, dkh, N, nch);
-        r = hipGetLastError();
-        if (r != hipSuccess) return r;
-        r = hipFuncSetAttribute((const void *)bwd_mg_scans,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
-        if (r != hipSuccess) return r;
-        hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, qh, kh,
-                           V, DO, rg, cc, hmax, dqh, dkh, N, BH);
-        r = hipGetLastError();
-        if (r != hipSuccess) return r;
-        hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q,
-                           K, dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows);
-        return hipGetLastError();
-    };
-    const hipError_t er = rest();
-    const hipError_t ej = hipStreamWaitEvent(st, ss->join, 0);
-    return er != hipSuccess ? er : ej;
+    hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q, K,
+                       dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows);
+    return hipGetLastError();
 }
 
 }  // namespace fm

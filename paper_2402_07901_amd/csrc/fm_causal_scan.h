@@ -1,0 +1,549 @@
+// The causal MFMA scan (D = 64, p = 2) as a device function, shared by the
+// forward launch (csrc/fm_causal_mfma.hip) and the backward's combined
+// dv / moment-gradient launch (csrc/fm_bwd_mfma.hip).
+//
+// Chunked causal scan (Sec. 2.4, causal moments "xcausal"/"ycausal" carried
+// across chunks of 128 tokens instead of per row).  One workgroup owns one
+// (batch, head, slice of 16 value columns) and keeps the moment state
+// S[f][j] = sum_n phi_f(k^_n) v_nj of the slice on chip for the whole
+// sequence; the state never touches HBM.
+//
+// Two kinds of waves share each SIMD:
+//  * state waves 0..3 hold the state as fp16 MFMA operands (41 feature tiles
+//    of 16 rows each, 84 registers per lane) and do the two contractions
+//    against it: the query contraction F^T += S^T Psi(Q)^T (Psi generated in
+//    registers with packed fp16 multiplies) and the state update
+//    S += Phi(K)^T V;
+//  * helper waves 4..7 stage the next chunk (q^ and k^, standardised once per
+//    call by standardise_qk (Sec. 2.2, Eqs. 6-7) and read in fp16; transposes;
+//    scaled v), compute the in-chunk block tril(f(Q K^T)) V on MFMA and
+//    the denominators G_i = n0 + q.y2 + 1/2 q^T Y3 q + in-chunk row sums,
+//    and combine the partial numerators into O = F / G.
+// Per chunk there are two phases separated by barriers: (1) query
+// contraction | in-chunk block and denominators; (2) state update | output,
+// prefix sums, Y3 update and staging of the next chunk.  The two kinds of
+// work overlap on each SIMD instead of running in lockstep.
+//
+// State numerics.  The state lives in fp16 (v is pre-scaled by a power of two
+// 2^-e per workgroup so that no entry, bounded by N * 63 * max|v|, can exceed
+// 2^15).  Each update rebuilds a tile's fp32 accumulator exactly with one MFMA
+// against a 0/1 permutation matrix, adds the chunk's contribution in fp32 and
+// rounds back to fp16 once per chunk.  Diagonal tiles are stored halved (the
+// 1/2 of f_2), and rebuilt with a 0/2 matrix.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "fm_common.h"
+#include "fm_mfma.h"
+
+namespace fm {
+namespace mfma_causal {
+
+using namespace mx;
+
+constexpr int C = 128;        // tokens per chunk
+constexpr int NRT = C / 16;   // 16-token row tiles per chunk
+constexpr int NKS2 = C / 32;  // 32-token K steps of the state update
+constexpr int NSW = 4;        // state waves (one per SIMD)
+constexpr int NW = 8;         // waves per workgroup
+constexpr int NTH = NW * 64;
+constexpr int NHT = NTH - NSW * 64;  // helper threads
+constexpr int SL = 16;        // value columns per workgroup
+constexpr int NSL = D / SL;
+
+// Feature tiles of state wave w: tile 0 is the linear tile u = w (features
+// k_l, l = 16w..16w+15); then for the wave's channels m = w + 4i (i = 0..15)
+// the quadratic tiles (m, u) for u = i/4 .. 3 (m/16 == i/4 for every w < 4):
+// 1 + 4*(4+3+2+1) = 41 tiles; 164 over the four waves.
+constexpr int NQ = 16;
+__host__ __device__ constexpr int u0_of(int i) { return i / 4; }
+__host__ __device__ constexpr int first_tile(int i)
+{
+    int t = 1;
+    for (int j = 0; j < i; ++j) t += 4 - u0_of(j);
+    return t;
+}
+constexpr int NT = first_tile(NQ);    // 41
+constexpr int NKS = (NT + 1) / 2;     // 21 K steps of the query contraction
+struct Tile {
+    int kind;  // 0 linear, 1 quadratic, -1 padding
+    int i;     // channel m = w + 4i
+    int u;     // l tile
+};
+__host__ __device__ constexpr Tile tile_of(int t)
+{
+    if (t == 0) return Tile{0, -1, -1};
+    for (int i = 0; i < NQ; ++i)
+        if (t < first_tile(i) + 4 - u0_of(i)) return Tile{1, i, u0_of(i) + t - first_tile(i)};
+    return Tile{-1, -1, -1};
+}
+static_assert(NT == 41 && tile_of(40).kind == 1 && tile_of(41).kind == -1, "tile pattern");
+// The first tile of each channel (u = i/4) is its diagonal tile.
+static_assert(tile_of(first_tile(5)).u == u0_of(5) && tile_of(first_tile(5)).i == 5, "tile pattern");
+
+// Y3 tiles (u <= u2), 10 of them: helpers 0 and 1 own three, 2 and 3 two.
+__device__ __forceinline__ int y3_count(int hw) { return hw < 2 ? 3 : 2; }
+__device__ __forceinline__ void y3_tile(int hw, int kk, int &u, int &u2)
+{
+    const int i = hw < 2 ? 3 * hw + kk : 6 + 2 * (hw - 2) + kk;
+    const int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
+    const int vs[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
+    u = us[i];
+    u2 = vs[i];
+}
+
+struct Smem {
+    _Float16 qrow[C * RS64];        // q^ [token][m]
+    _Float16 qperm[C * RS64];       // q^ [token][16 (m % 4) + m / 4]: a state wave's channels
+    _Float16 krow[C * RS64];        // k^ [token][m]
+    _Float16 kT[2][D * RS128];      // k^ [m][token], double-buffered by chunk parity
+    _Float16 vT[2][SL * RS128];     // scaled v [j][token], double-buffered
+    _Float16 y3h[D * RS64];         // scaled Y3 (prefix before the chunk)
+    float fpart[NSW * C * SL];      // partial F^T of the state waves: [wave][column quad][token][4]
+    float y2[2][D];                 // sum k^ before the chunk (by chunk parity)
+    float x1[2][SL];                // sum of scaled v before the chunk
+    float red[NW];
+};
+
+// rows a (slots 0..3) or b (slots 4..7) of a paired fp16 operand -> the
+// accumulator layout of that tile, times `one` (exact)
+__device__ __forceinline__ h8 perm_operand(int r16, int h, bool hi, _Float16 one)
+{
+    h8 p = {0, 0, 0, 0, 0, 0, 0, 0};
+    const bool on = h == (r16 >> 2);
+    const int slot = (r16 & 3) + (hi ? 4 : 0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) p[j] = (on && slot == j) ? one : (_Float16)0.0f;
+    return p;
+}
+
+template <int HALF>
+__device__ __forceinline__ h8 set_half(h8 x, h4 r)
+{
+    if constexpr (HALF == 0) return h8{r[0], r[1], r[2], r[3], x[4], x[5], x[6], x[7]};
+    else return h8{x[0], x[1], x[2], x[3], r[0], r[1], r[2], r[3]};
+}
+// DV = false: the forward O = F / G.  DV = true: the reverse-causal
+// numerator of the backward, dv_n = sum_{i >= n} f(k^_n . q^_i) u_i with
+// u_i = dO_i / G_i (Sec. 2.5): the scan runs over the tokens in reverse order
+// (logical token n is row N-1-n), q and k trade roles (the caller passes k^ as
+// q and q^ as k, both already standardised, in fp16), v is dO scaled per row
+// by rg = 1/G, and F is stored without the divide; the denominator terms are
+// skipped.
+// One workgroup of the scan: block b of nblk (the scan's own numbering; when
+// the scan shares a launch with other work, b counts from its first block,
+// whose id must be a multiple of 8 for the XCD mapping below).
+template <bool DV>
+__device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict__ q,
+                                           const _Float16 *__restrict__ k,
+                                           const bf16_t *__restrict__ v, bf16_t *__restrict__ out,
+                                           float *__restrict__ g, const float *__restrict__ rg,
+                                           int N, int BH, int b, int nblk)
+{
+    // XCD-aware mapping: consecutive block ids land on different XCDs
+    // (round-robin over 8); keep the 4 slices of a head on one XCD so that
+    // its q and k rows are shared through that XCD's L2.
+    int head, sl;
+    if ((nblk & 31) == 0) {
+        const int xcd = b & 7, idx = b >> 3;
+        sl = idx & 3;
+        head = (idx >> 2) * 8 + xcd;
+    } else {
+        head = b / NSL;
+        sl = b % NSL;
+    }
+    if (head >= BH) return;
+    const size_t hb = (size_t)head * N * D;
+    q += hb;
+    k += hb;
+    v += hb;
+    out += hb;
+    if (g) g += (size_t)head * N;
+    if (rg) rg += (size_t)head * N;
+
+    // max |v| over this slice -> power-of-two scale
+    {
+        const int tid = threadIdx.x;
+        float vmax = 0.f;
+        for (int p = tid; p < 2 * N; p += NTH) {
+            const int n = p >> 1, hh = p & 1;
+            float x[8];
+            bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh), x);
+            const float r = DV ? fabsf(rg[n]) : 1.0f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * r);
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
+        if ((tid & 63) == 0) sm.red[tid >> 6] = vmax;
+        if (tid < D) sm.y2[0][tid] = 0.f;
+        if (tid < SL) sm.x1[0][tid] = 0.f;
+        for (int e = tid; e < D * RS64; e += NTH) sm.y3h[e] = (_Float16)0.0f;
+    }
+    __syncthreads();
+    float vmax = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) vmax = fmaxf(vmax, sm.red[w]);
+    const int vexp = pow2_exponent(vmax * 63.0f * (float)N);
+    const float vscale = ldexpf(1.0f, -vexp);   // v -> v * 2^-e
+    const float oscale = ldexpf(1.0f, vexp);
+    const int nch = (N + C - 1) / C;
+
+    const int w = threadIdx.x >> 6;
+    const bool is_state = w < NSW;
+    const int hw = w - NSW;   // helper index
+
+    // Lane-derived LDS offsets are recomputed in every phase from an opaque
+    // copy of the thread id: hoisted out of the loop they would stay live for
+    // the whole scan.
+    int tid = threadIdx.x;
+    int lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    auto refresh_ids = [&]() {
+        asm volatile("" : "+v"(tid));
+        lane = tid & 63;
+        r16 = lane & 15;
+        h = lane >> 4;
+    };
+
+    // The two roles run separate loops with the same barrier sequence (one
+    // after staging chunk 0, two per chunk); the role is uniform per wave.
+    if (is_state) {
+        // fp16 state, paired per query K step
+        h8 Ast[NKS];
+#pragma unroll
+        for (int p = 0; p < NKS; ++p) Ast[p] = h8{0, 0, 0, 0, 0, 0, 0, 0};
+        __syncthreads();
+        for (int c = 0; c < nch; ++c) {
+            // ---- (1) query contraction over the wave's tiles, 128 tokens ----
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            // the q^ values of a row tile: l blocks, the linear tile and the
+            // wave's channels; loaded one row tile ahead of their use
+            struct QRow {
+                h4 myl[4], mylin;
+                h8 qa, qb;
+            };
+            auto loadq = [&](int rt, QRow &r) {
+                const int tok = 16 * rt + r16;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) r.myl[u] = ld4(sm.qrow + sw64(tok, 16 * u + 4 * h));
+                r.mylin = ld4(sm.qrow + sw64(tok, 16 * w + 4 * h));
+                r.qa = ld8(sm.qperm + sw64(tok, 16 * w));
+                r.qb = ld8(sm.qperm + sw64(tok, 16 * w + 8));
+            };
+            auto contract = [&](int rt, const QRow &r) {
+                const int tok = 16 * rt + r16;
+                f4 F0 = {0.f, 0.f, 0.f, 0.f}, F1 = {0.f, 0.f, 0.f, 0.f};
+                auto gen = [&](auto ti) -> h4 {
+                    constexpr int t = decltype(ti)::value;
+                    constexpr Tile T = tile_of(t < NT ? t : 0);
+                    if constexpr (t >= NT) {
+                        return h4{0, 0, 0, 0};
+                    } else if constexpr (T.kind == 0) {
+                        return r.mylin;
+                    } else {
+                        const _Float16 qm = T.i < 8 ? r.qa[T.i & 7] : r.qb[T.i & 7];
+                        return scale4(r.myl[T.u], qm);
+                    }
+                };
+                static_for<0, NKS>([&](auto pi) {
+                    constexpr int p = decltype(pi)::value;
+                    const h8 B = cat(gen(std::integral_constant<int, 2 * p>{}),
+                                     gen(std::integral_constant<int, 2 * p + 1>{}));
+                    if constexpr (p & 1) F1 = mfma(Ast[p], B, F1);
+                    else F0 = mfma(Ast[p], B, F0);
+                });
+                *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
+            };
+            QRow ra, rb;
+            loadq(0, ra);
+#pragma unroll 1
+            for (int rt = 0; rt < NRT; rt += 2) {
+                loadq(rt + 1, rb);
+                contract(rt, ra);
+                if (rt + 2 < NRT) loadq(rt + 2, ra);
+                contract(rt + 1, rb);
+            }
+            __syncthreads();
+
+            // ---- (2) state update S += Phi(K)^T V (Sec. 2.4) ----------------
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            const _Float16 *kTc = sm.kT[c & 1];
+            const _Float16 *vTc = sm.vT[c & 1];
+            h8 Ak[4][NKS2];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s) Ak[u][s] = ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h));
+            h8 Vf[NKS2];
+#pragma unroll
+            for (int s = 0; s < NKS2; ++s) Vf[s] = ld8(vTc + sw128(r16, 32 * s + 8 * h));
+            const h8 pa = perm_operand(r16, h, false, (_Float16)1.0f);
+            const h8 pb = perm_operand(r16, h, true, (_Float16)1.0f);
+            const h8 pa2 = perm_operand(r16, h, false, (_Float16)2.0f);
+            const h8 pb2 = perm_operand(r16, h, true, (_Float16)2.0f);
+            {
+                // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
+                f4 acc = mfma(pa, Ast[0], f4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s)
+                    acc = mfma(ld8(kTc + sw128(16 * w + r16, 32 * s + 8 * h)), Vf[s], acc);
+                Ast[0] = set_half<0>(Ast[0], cvt4(acc));
+            }
+            static_for<0, NQ>([&](auto ii) {
+                constexpr int i = decltype(ii)::value;
+                constexpr int u0 = u0_of(i);
+                constexpr int t0 = first_tile(i);
+                constexpr int nu = 4 - u0;
+                const int m = w + 4 * i;
+                h8 Wm[NKS2];
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s) Wm[s] = ld8(kTc + sw128(m, 32 * s + 8 * h)) * Vf[s];
+                // rebuild the fp32 tiles (diagonal tile: stored halved, 0/2 matrix)
+                f4 acc[nu];
+                static_for<0, nu>([&](auto ui) {
+                    constexpr int uu = decltype(ui)::value;
+                    constexpr int t = t0 + uu;
+                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
+                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
+                });
+#pragma unroll
+                for (int s = 0; s < NKS2; ++s)
+                    static_for<0, nu>([&](auto ui) {
+                        constexpr int uu = decltype(ui)::value;
+                        acc[uu] = mfma(Ak[u0 + uu][s], Wm[s], acc[uu]);
+                    });
+                static_for<0, nu>([&](auto ui) {
+                    constexpr int uu = decltype(ui)::value;
+                    constexpr int t = t0 + uu;
+                    h4 r = cvt4(acc[uu]);
+                    if constexpr (uu == 0) r = scale4(r, (_Float16)0.5f);
+                    Ast[t / 2] = set_half<t & 1>(Ast[t / 2], r);
+                });
+            });
+            __syncthreads();
+        }
+    } else {
+        // loader roles: tokens 4*tg .. 4*tg+3, channels 8*cg .. 8*cg+7; v:
+        // token vt, columns 8*vh .. 8*vh+7
+        uint4 pq[4], pk[4], pv;
+        float prg = 1.0f;
+        f4 y3acc[3] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
+        int gexp = 0;   // Y3 in LDS is Y3 * 2^-gexp
+
+        auto prefetch = [&](int c) {
+            const int ht = tid - NSW * 64;
+            const int tg = ht >> 3, cg = ht & 7;
+            const uint4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = c * C + 4 * tg + j;
+                pq[j] = pk[j] = z;
+                if (n < N) {
+                    const size_t pn = DV ? (size_t)(N - 1 - n) : (size_t)n;
+                    pq[j] = *(const uint4 *)(q + pn * D + 8 * cg);
+                    pk[j] = *(const uint4 *)(k + pn * D + 8 * cg);
+                }
+            }
+            const int vt = ht >> 1, vh = ht & 1;
+            const int nv = c * C + vt;
+            pv = z;
+            if (nv < N) {
+                const size_t pn = DV ? (size_t)(N - 1 - nv) : (size_t)nv;
+                pv = *(const uint4 *)(v + pn * D + SL * sl + 8 * vh);
+                if constexpr (DV) prg = rg[pn];
+            }
+        };
+        // Staging of chunk c: store q^ (row-major and channel-permuted), k^
+        // (row-major and transposed) and the scaled v transposed.  q^, k^
+        // arrive standardised (Sec. 2.2, Eqs. 6-7) in fp16; rows past N are
+        // zero.
+        auto stage = [&](int c) {
+            const int ht = tid - NSW * 64;
+            const int tg = ht >> 3, cg = ht & 7;
+            const int buf = c & 1;
+            h8 hk[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = 4 * tg + j;
+                const h8 hq = __builtin_bit_cast(h8, pq[j]);
+                *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
+                // channel 8cg + ww -> state wave ww, index 2cg; 8cg + 4 + ww -> 2cg + 1
+#pragma unroll
+                for (int ww = 0; ww < 4; ++ww)
+                    *(h2 *)(sm.qperm + sw64(row, 16 * ww + 2 * cg)) = h2{hq[ww], hq[4 + ww]};
+                hk[j] = __builtin_bit_cast(h8, pk[j]);
+                *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                *(h4 *)(sm.kT[buf] + sw128(8 * cg + i, 4 * tg)) =
+                    h4{hk[0][i], hk[1][i], hk[2][i], hk[3][i]};
+            const int vt = ht >> 1, vh = ht & 1;
+            float xv[8];
+            bf16x8_to_f32(pv, xv);
+            const float vs = DV ? vscale * prg : vscale;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vs);
+        };
+
+        prefetch(0);
+        stage(0);
+        __syncthreads();
+        for (int c = 0; c < nch; ++c) {
+            const int n0 = c * C;
+            const int nvalid = min(C, N - n0);
+            const int cur = c & 1, nxt = cur ^ 1;
+            const bool more = c + 1 < nch;
+
+            // ---- (1) in-chunk block and denominators, row tiles hw, 7 - hw
+            //      (1 + 4, 1 + 4, 2 + 3, 2 + 3 tile-pair items) ---------------
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            if (more) prefetch(c + 1);
+            f4 Fin[2];
+            float Gs[2];
+            {
+                const _Float16 *vTc = sm.vT[cur];
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int rt = r ? NRT - 1 - hw : hw;
+                    const int tok = 16 * rt + r16;
+                    const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
+                    const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
+                    f4 F = {0.f, 0.f, 0.f, 0.f};
+                    float gpart = 0.f;
+                    // S^T tile (rows: keys 16tt.., columns: queries) -> f(s)
+                    auto wtile = [&](int tt) -> h4 {
+                        f4 S = {0.f, 0.f, 0.f, 0.f};
+                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 8 * h)), QB0, S);
+                        S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 32 + 8 * h)), QB1, S);
+                        f4 wv;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float x = S[i];
+                            float y = fmaf(0.5f * x, x, 1.0f + x);
+                            if (tt == rt && (4 * h + i) > r16) y = 0.0f;
+                            wv[i] = y;
+                            gpart += y;
+                        }
+                        return cvt4(wv);
+                    };
+#pragma unroll 1
+                    for (int j = 0; j <= rt / 2; ++j) {
+                        const int a = 2 * j, bb = a + 1;
+                        const h4 wa = wtile(a);
+                        const h4 va = ld4(vTc + sw128(r16, 16 * a + 4 * h));
+                        h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
+                        if (bb <= rt) {
+                            wb = wtile(bb);
+                            vb = ld4(vTc + sw128(r16, 16 * bb + 4 * h));
+                        }
+                        F = mfma(cat(va, vb), cat(wa, wb), F);
+                    }
+                    if (!DV) {
+                        // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
+                        float gq = 0.f;
+                        const float ys = ldexpf(2.0f, -gexp);
+#pragma unroll
+                        for (int cc = 0; cc < 4; ++cc) {
+                            const h4 ql = ld4(sm.qrow + sw64(tok, 16 * cc + 4 * h));
+                            f4 T;
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[cur][16 * cc + 4 * h + i];
+                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
+                            T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) gq = fmaf((float)ql[i], T[i], gq);
+                        }
+                        gpart = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gpart);
+                        if (h == 0) gpart += (float)n0;
+                    }
+                    gpart += __shfl_xor(gpart, 16);
+                    gpart += __shfl_xor(gpart, 32);
+                    Fin[r] = F;
+                    Gs[r] = gpart;
+                }
+            }
+            __syncthreads();
+
+            // ---- (2) output, prefix sums, Y3, staging of the next chunk ------
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            const _Float16 *kTc = sm.kT[cur];
+            const _Float16 *vTc = sm.vT[cur];
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int rt = r ? NRT - 1 - hw : hw;
+                const int tok = 16 * rt + r16;
+                f4 F = Fin[r] + *(const f4 *)(sm.x1[cur] + 4 * h);
+#pragma unroll
+                for (int ww = 0; ww < NSW; ++ww)
+                    F += *(const f4 *)(sm.fpart + ((ww * 4 + h) * C + tok) * 4);
+                if (n0 + tok < N) {
+                    const float sc = DV ? oscale : oscale * __builtin_amdgcn_rcpf(Gs[r]);
+                    uint2 o;
+                    o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
+                    o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
+                    const size_t pn = DV ? (size_t)(N - 1 - (n0 + tok)) : (size_t)(n0 + tok);
+                    *(uint2 *)(out + pn * D + SL * sl + 4 * h) = o;
+                    if (!DV && g && sl == 0 && h == 0) g[n0 + tok] = Gs[r];
+                }
+            }
+            // prefix sums: y2 (channels 16hw..16hw+15), x1 (helper 0)
+            if (!DV) {
+                const int m = 16 * hw + r16;
+                float s = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(kTc + sw128(m, 32 * h + 8 * cc)));
+                s += __shfl_xor(s, 16);
+                s += __shfl_xor(s, 32);
+                if (h == 0) sm.y2[nxt][m] = sm.y2[cur][m] + s;
+            }
+            if (hw == 0) {
+                float sv = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(vTc + sw128(r16, 32 * h + 8 * cc)));
+                sv += __shfl_xor(sv, 16);
+                sv += __shfl_xor(sv, 32);
+                if (h == 0) sm.x1[nxt][r16] = sm.x1[cur][r16] + sv;
+            }
+            if (!DV) {
+                // Y3 += K^T K and its scaled fp16 copy for the next chunk
+                const int ny3 = y3_count(hw);
+                const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
+                const float gs = ldexpf(1.0f, -gnext);
+#pragma unroll
+                for (int kk = 0; kk < 3; ++kk) {
+                    if (kk >= ny3) break;
+                    int u, u2;
+                    y3_tile(hw, kk, u, u2);
+#pragma unroll
+                    for (int s = 0; s < NKS2; ++s)
+                        y3acc[kk] = mfma(ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h)),
+                                         ld8(kTc + sw128(16 * u2 + r16, 32 * s + 8 * h)), y3acc[kk]);
+                    // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
+                    const int mcol = 16 * u2 + r16;
+                    h4 hv;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) hv[i] = (_Float16)(y3acc[kk][i] * gs);
+                    *(h4 *)(sm.y3h + sw64(mcol, 16 * u + 4 * h)) = hv;   // Y3[m][l]
+                    if (u != u2) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) sm.y3h[sw64(16 * u + 4 * h + i, mcol)] = hv[i];
+                    }
+                }
+                gexp = gnext;
+            }
+            if (more) stage(c + 1);
+            __syncthreads();
+        }
+    }
+}
+
+}  // namespace mfma_causal
+}  // namespace fm

@@ -23,10 +23,6 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
                            int BH, int N, void *ws, hipStream_t st);
 size_t mfma_causal_fwd_workspace(int BH, int N);
 size_t mfma_causal_smem_bytes();
-// The causal scan run in reverse on (k^, q^, dO / G) without the divide: dv.
-// qh, kh: the standardised q and k in fp16 (as bwd_prep writes them).
-hipError_t mfma_causal_dv(const void *qh, const void *kh, const void *dout, const float *rg,
-                          void *dv, int BH, int N, hipStream_t st);
 
 // MFMA causal backward: D = 64, p = 2, bf16 I/O.  ws holds
 // mfma_causal_bwd_workspace(BH, N) bytes.
