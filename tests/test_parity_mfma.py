@@ -221,10 +221,9 @@ def test_bwd_deterministic():
 
 
 def test_user_stream_ordering():
-    """Forward and backward enqueued on a caller's non-default stream (the
-    backward forks part of its work onto the library's side stream and joins
-    it back): results equal the default-stream ones, and work the caller
-    enqueues after the call on its stream sees the finished outputs."""
+    """Forward and backward enqueued on a caller's non-default stream: results
+    equal the default-stream ones, and work the caller enqueues after the call
+    on its stream sees the finished outputs."""
     import torch
     inp = make_inputs(1, 4, 2000, 64, 47, "bf16", with_dout=True)
     q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "dout"))
