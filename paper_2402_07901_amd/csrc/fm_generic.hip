@@ -74,22 +74,37 @@ __device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_ou
         dst[r * DP + d] = n < N ? io<T>::ld(src, (size_t)n * D + d) : 0.0f;
     }
     __syncthreads();
-    if (threadIdx.x < CH) {
-        int r = threadIdx.x;
+    {
+        // 16 lanes per row (NT = 16 * CH): each holds D / 16 channels; sums
+        // over the row by butterfly shuffles within the 16 lanes
+        static_assert(NT == 16 * CH && D % 16 == 0, "16 lanes per row");
+        constexpr int E = D / 16;
+        const int r = threadIdx.x >> 4, l = threadIdx.x & 15;
         float *x = dst + r * DP;
+        float xv[E];
+        float s = 0.0f;
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            xv[i] = x[l + 16 * i];
+            s += xv[i];
+        }
+#pragma unroll
+        for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o, 16);
+        const float mu = s * (1.0f / D);
+        float var = 0.0f;
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            xv[i] -= mu;
+            var = fmaf(xv[i], xv[i], var);
+        }
+#pragma unroll
+        for (int o = 8; o >= 1; o >>= 1) var += __shfl_xor(var, o, 16);
         if (n0 + r < N) {
-            float mu = 0.0f;
-            for (int d = 0; d < D; ++d) mu += x[d];
-            mu *= 1.0f / D;
-            float var = 0.0f;
-            for (int d = 0; d < D; ++d) {
-                float c = x[d] - mu;
-                var = fmaf(c, c, var);
-            }
-            float rs = rsqrtf(var * (1.0f / D));
-            for (int d = 0; d < D; ++d) x[d] = (x[d] - mu) * rs;
-            if (rstd_out) rstd_out[r] = rs;
-        } else if (rstd_out) {
+            const float rs = rsqrtf(var * (1.0f / D));
+#pragma unroll
+            for (int i = 0; i < E; ++i) x[l + 16 * i] = xv[i] * rs;
+            if (rstd_out && l == 0) rstd_out[r] = rs;
+        } else if (rstd_out && l == 0) {
             rstd_out[r] = 0.0f;
         }
     }
@@ -218,6 +233,24 @@ __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
     for (int e = threadIdx.x; e < P * WS; e += NT) dst[e] = S[e];
 }
 
+// In place over the segments of each (head, slice): causal -> the exclusive
+// prefix sum (segment s gets the sum of segments < s), non-causal -> the total
+// in segment 0.  One thread per state element.
+template <int PWS, bool CAUSAL>
+__global__ __launch_bounds__(NT) void seg_prefix_kernel(float *__restrict__ sseg, int nseg)
+{
+    const int e = blockIdx.x * NT + threadIdx.x;
+    if (e >= PWS) return;
+    float *base = sseg + (size_t)blockIdx.y * nseg * PWS + e;
+    float run = 0.0f;
+    for (int s2 = 0; s2 < nseg; ++s2) {
+        const float x = base[(size_t)s2 * PWS];
+        if (CAUSAL) base[(size_t)s2 * PWS] = run;
+        run += x;
+    }
+    if (!CAUSAL) base[0] = run;
+}
+
 template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                  const T *__restrict__ v, T *__restrict__ out,
@@ -250,15 +283,13 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
 
     const int nseg = gridDim.z, seg = blockIdx.z;
     {
-        // initial state: the earlier segments (causal) or all of them
-        const float *src = sseg ? sseg + ((size_t)head * gridDim.y + blockIdx.y) * nseg * P * WS
+        // initial state: the sum of the earlier segments (causal) or of all
+        // of them, as seg_prefix_kernel left it in this segment's slot (in
+        // segment 0's for non-causal)
+        const float *src = sseg ? sseg + (((size_t)head * gridDim.y + blockIdx.y) * nseg +
+                                          (CAUSAL ? seg : 0)) * P * WS
                                 : nullptr;
-        const int upto = sseg ? (CAUSAL ? seg : nseg) : 0;
-        for (int e = threadIdx.x; e < P * WS; e += NT) {
-            float a = 0.0f;
-            for (int s2 = 0; s2 < upto; ++s2) a += src[(size_t)s2 * P * WS + e];
-            S[e] = a;
-        }
+        for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = src ? src[e] : 0.0f;
     }
     build_pairs<D, P2>(pm, pl);
     __syncthreads();
@@ -681,6 +712,16 @@ static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void
         hipLaunchKernelGGL((seg_state_kernel<D, P2, WS, T>), grid, dim3(NT), 0, st, (const T *)k,
                            (const T *)v, sseg, N, sp.cps);
         hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        constexpr int PWS = feat<D, P2>::P * WS;
+        const dim3 pgrid((PWS + NT - 1) / NT, BH * sp.slices);
+        if (causal)
+            hipLaunchKernelGGL((seg_prefix_kernel<PWS, true>), pgrid, dim3(NT), 0, st, sseg,
+                               sp.nseg);
+        else
+            hipLaunchKernelGGL((seg_prefix_kernel<PWS, false>), pgrid, dim3(NT), 0, st, sseg,
+                               sp.nseg);
+        e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     if (causal)
