@@ -55,8 +55,10 @@ constexpr int SL = 16;        // value columns per workgroup
 constexpr int NSL = D / SL;
 
 // Feature tiles of state wave w: tile 0 is the linear tile u = w (features
-// k_l, l = 16w..16w+15); then for the wave's channels m = w + 4i (i = 0..15)
-// the quadratic tiles (m, u) for u = i/4 .. 3 (m/16 == i/4 for every w < 4):
+// k_l, l = 16w..16w+15); then for the wave's channels
+// m = 16 (i/4) + 4w + i%4 (i = 0..15: channels 4w..4w+3 of each 16-channel
+// block, so a lane reads them as four 4-channel groups of a row-major q^ row)
+// the quadratic tiles (m, u) for u = i/4 .. 3 (m/16 == i/4):
 // 1 + 4*(4+3+2+1) = 41 tiles; 164 over the four waves.
 constexpr int NQ = 16;
 __host__ __device__ constexpr int u0_of(int i) { return i / 4; }
@@ -70,7 +72,7 @@ constexpr int NT = first_tile(NQ);    // 41
 constexpr int NKS = (NT + 1) / 2;     // 21 K steps of the query contraction
 struct Tile {
     int kind;  // 0 linear, 1 quadratic, -1 padding
-    int i;     // channel m = w + 4i
+    int i;     // channel m = 16 (i/4) + 4w + i%4
     int u;     // l tile
 };
 __host__ __device__ constexpr Tile tile_of(int t)
@@ -86,18 +88,18 @@ static_assert(tile_of(first_tile(5)).u == u0_of(5) && tile_of(first_tile(5)).i =
 
 // Y3 tiles (u <= u2), 10 of them: helpers 0 and 1 own three, 2 and 3 two.
 __device__ __forceinline__ int y3_count(int hw) { return hw < 2 ? 3 : 2; }
+// Tile i of the upper triangle in row order: (0,0) (0,1) (0,2) (0,3) (1,1)
+// ... (3,3); computed, not looked up (a table would be placed in memory and
+// each lookup would wait on a global load).
 __device__ __forceinline__ void y3_tile(int hw, int kk, int &u, int &u2)
 {
     const int i = hw < 2 ? 3 * hw + kk : 6 + 2 * (hw - 2) + kk;
-    const int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
-    const int vs[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
-    u = us[i];
-    u2 = vs[i];
+    u = (i >= 4) + (i >= 7) + (i >= 9);
+    u2 = i - (4 * u - (u * (u - 1)) / 2) + u;
 }
 
 struct Smem {
     _Float16 qrow[C * RS64];        // q^ [token][m]
-    _Float16 qperm[C * RS64];       // q^ [token][16 (m % 4) + m / 4]: a state wave's channels
     _Float16 krow[C * RS64];        // k^ [token][m]
     _Float16 kT[2][D * RS128];      // k^ [m][token], double-buffered by chunk parity
     _Float16 vT[2][SL * RS128];     // scaled v [j][token], double-buffered
@@ -224,15 +226,15 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             // wave's channels; loaded one row tile ahead of their use
             struct QRow {
                 h4 myl[4], mylin;
-                h8 qa, qb;
+                h4 qc[4];
             };
             auto loadq = [&](int rt, QRow &r) {
                 const int tok = 16 * rt + r16;
 #pragma unroll
                 for (int u = 0; u < 4; ++u) r.myl[u] = ld4(sm.qrow + sw64(tok, 16 * u + 4 * h));
                 r.mylin = ld4(sm.qrow + sw64(tok, 16 * w + 4 * h));
-                r.qa = ld8(sm.qperm + sw64(tok, 16 * w));
-                r.qb = ld8(sm.qperm + sw64(tok, 16 * w + 8));
+#pragma unroll
+                for (int a = 0; a < 4; ++a) r.qc[a] = ld4(sm.qrow + sw64(tok, 16 * a + 4 * w));
             };
             auto contract = [&](int rt, const QRow &r) {
                 const int tok = 16 * rt + r16;
@@ -245,7 +247,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                     } else if constexpr (T.kind == 0) {
                         return r.mylin;
                     } else {
-                        const _Float16 qm = T.i < 8 ? r.qa[T.i & 7] : r.qb[T.i & 7];
+                        const _Float16 qm = r.qc[T.i / 4][T.i % 4];
                         return scale4(r.myl[T.u], qm);
                     }
                 };
@@ -286,6 +288,23 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             const h8 pb = perm_operand(r16, h, true, (_Float16)1.0f);
             const h8 pa2 = perm_operand(r16, h, false, (_Float16)2.0f);
             const h8 pb2 = perm_operand(r16, h, true, (_Float16)2.0f);
+            // rebuild the fp32 tiles of channel i (diagonal tile: stored halved,
+            // 0/2 matrix).  Channel i+1 is rebuilt before channel i is rounded
+            // back: the pair it shares with channel i is then read before that
+            // write (its other half is multiplied by zero), so the channels do
+            // not form one dependency chain.
+            auto rebuild = [&](auto ii, f4(&acc)[4]) {
+                constexpr int i = decltype(ii)::value;
+                constexpr int t0 = first_tile(i);
+                static_for<0, 4 - u0_of(i)>([&](auto ui) {
+                    constexpr int uu = decltype(ui)::value;
+                    constexpr int t = t0 + uu;
+                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
+                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
+                });
+            };
+            f4 accA[4], accB[4];
+            rebuild(std::integral_constant<int, 0>{}, accA);
             {
                 // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
                 f4 acc = mfma(pa, Ast[0], f4{0.f, 0.f, 0.f, 0.f});
@@ -299,18 +318,13 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 constexpr int u0 = u0_of(i);
                 constexpr int t0 = first_tile(i);
                 constexpr int nu = 4 - u0;
-                const int m = w + 4 * i;
+                f4(&acc)[4] = (i & 1) ? accB : accA;
+                const int m = 16 * u0 + 4 * w + (i & 3);
                 h8 Wm[NKS2];
 #pragma unroll
                 for (int s = 0; s < NKS2; ++s) Wm[s] = ld8(kTc + sw128(m, 32 * s + 8 * h)) * Vf[s];
-                // rebuild the fp32 tiles (diagonal tile: stored halved, 0/2 matrix)
-                f4 acc[nu];
-                static_for<0, nu>([&](auto ui) {
-                    constexpr int uu = decltype(ui)::value;
-                    constexpr int t = t0 + uu;
-                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
-                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
-                });
+                if constexpr (i + 1 < NQ)
+                    rebuild(std::integral_constant<int, i + 1>{}, (i & 1) ? accA : accB);
 #pragma unroll
                 for (int s = 0; s < NKS2; ++s)
                     static_for<0, nu>([&](auto ui) {
@@ -358,7 +372,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 if constexpr (DV) prg = rg[pn];
             }
         };
-        // Staging of chunk c: store q^ (row-major and channel-permuted), k^
+        // Staging of chunk c: store q^ (row-major), k^
         // (row-major and transposed) and the scaled v transposed.  q^, k^
         // arrive standardised (Sec. 2.2, Eqs. 6-7) in fp16; rows past N are
         // zero.
@@ -372,10 +386,6 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 const int row = 4 * tg + j;
                 const h8 hq = __builtin_bit_cast(h8, pq[j]);
                 *(h8 *)(sm.qrow + sw64(row, 8 * cg)) = hq;
-                // channel 8cg + ww -> state wave ww, index 2cg; 8cg + 4 + ww -> 2cg + 1
-#pragma unroll
-                for (int ww = 0; ww < 4; ++ww)
-                    *(h2 *)(sm.qperm + sw64(row, 16 * ww + 2 * cg)) = h2{hq[ww], hq[4 + ww]};
                 hk[j] = __builtin_bit_cast(h8, pk[j]);
                 *(h8 *)(sm.krow + sw64(row, 8 * cg)) = hk[j];
             }
@@ -417,34 +427,47 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                     const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
                     f4 F = {0.f, 0.f, 0.f, 0.f};
                     float gpart = 0.f;
-                    // S^T tile (rows: keys 16tt.., columns: queries) -> f(s)
-                    auto wtile = [&](int tt) -> h4 {
-                        f4 S = {0.f, 0.f, 0.f, 0.f};
+                    // S^T tile (rows: keys 16tt.., columns: queries) -> 2 f(s):
+                    // the accumulator starts at 1, so t = s + 1 and
+                    // 2 f_2(s) = t^2 + 1 is one FMA; the factor 2 is removed
+                    // where F and G are combined
+                    auto wtile = [&](int tt, bool diag) -> h4 {
+                        f4 S = {1.f, 1.f, 1.f, 1.f};
                         S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 8 * h)), QB0, S);
                         S = mfma(ld8(sm.krow + sw64(16 * tt + r16, 32 + 8 * h)), QB1, S);
                         f4 wv;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            const float x = S[i];
-                            float y = fmaf(0.5f * x, x, 1.0f + x);
-                            if (tt == rt && (4 * h + i) > r16) y = 0.0f;
+                            float y = fmaf(S[i], S[i], 1.0f);
+                            if (diag && (4 * h + i) > r16) y = 0.0f;
                             wv[i] = y;
                             gpart += y;
                         }
                         return cvt4(wv);
                     };
+                    // whole tile pairs below the diagonal tile
 #pragma unroll 1
-                    for (int j = 0; j <= rt / 2; ++j) {
-                        const int a = 2 * j, bb = a + 1;
-                        const h4 wa = wtile(a);
+                    for (int j = 0; j < rt / 2; ++j) {
+                        const int a = 2 * j;
+                        const h4 wa = wtile(a, false), wb = wtile(a + 1, false);
+                        F = mfma(cat(ld4(vTc + sw128(r16, 16 * a + 4 * h)),
+                                     ld4(vTc + sw128(r16, 16 * a + 16 + 4 * h))),
+                                 cat(wa, wb), F);
+                    }
+                    {
+                        // the last pair holds the diagonal tile rt (masked to
+                        // keys <= query), alone when rt is even
+                        const int a = rt & ~1;
+                        const h4 wa = wtile(a, a == rt);
                         const h4 va = ld4(vTc + sw128(r16, 16 * a + 4 * h));
                         h4 wb = h4{0, 0, 0, 0}, vb = h4{0, 0, 0, 0};
-                        if (bb <= rt) {
-                            wb = wtile(bb);
-                            vb = ld4(vTc + sw128(r16, 16 * bb + 4 * h));
+                        if (a != rt) {
+                            wb = wtile(rt, true);
+                            vb = ld4(vTc + sw128(r16, 16 * rt + 4 * h));
                         }
                         F = mfma(cat(va, vb), cat(wa, wb), F);
                     }
+                    gpart *= 0.5f;
                     if (!DV) {
                         // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
                         float gq = 0.f;
@@ -480,7 +503,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             for (int r = 0; r < 2; ++r) {
                 const int rt = r ? NRT - 1 - hw : hw;
                 const int tok = 16 * rt + r16;
-                f4 F = Fin[r] + *(const f4 *)(sm.x1[cur] + 4 * h);
+                f4 F = 0.5f * Fin[r] + *(const f4 *)(sm.x1[cur] + 4 * h);
 #pragma unroll
                 for (int ww = 0; ww < NSW; ++ww)
                     F += *(const f4 *)(sm.fpart + ((ww * 4 + h) * C + tok) * 4);

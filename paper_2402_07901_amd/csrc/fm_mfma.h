@@ -85,11 +85,11 @@ __host__ __device__ constexpr bool is_diag(int t)
 __device__ __forceinline__ int y3_count(int w) { return w < 2 ? 2 : 1; }
 __device__ __forceinline__ void y3_tile(int w, int k, int &u, int &u2)
 {
+    // tile i of the upper triangle in row order (0,0) (0,1) .. (3,3), computed
+    // rather than looked up in a table (which would live in global memory)
     const int i = w < 2 ? 2 * w + k : 2 + w;
-    const int us[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
-    const int vs[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
-    u = us[i];
-    u2 = vs[i];
+    u = (i >= 4) + (i >= 7) + (i >= 9);
+    u2 = i - (4 * u - (u * (u - 1)) / 2) + u;
 }
 
 // LDS rows are padded by 16 bytes: 16 lanes reading the same column of 16
