@@ -105,8 +105,9 @@ struct Smem {
     _Float16 vT[2][SL * RS128];     // scaled v [j][token], double-buffered
     _Float16 y3h[D * RS64];         // scaled Y3 (prefix before the chunk)
     float fpart[NSW * C * SL];      // partial F^T of the state waves: [wave][column quad][token][4]
-    float y2[2][D];                 // sum k^ before the chunk (by chunk parity)
-    float x1[2][SL];                // sum of scaled v before the chunk
+    alignas(16) float y2[2][D];     // sum k^ before the chunk (by chunk parity)
+    alignas(16) float y2s[2][D];    // the same times 2^(1-gexp), gexp the Y3 scale
+    alignas(16) float x1[2][SL];    // sum of scaled v before the chunk
     float red[NW];
 };
 
@@ -181,7 +182,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
         if ((tid & 63) == 0) sm.red[tid >> 6] = vmax;
-        if (tid < D) sm.y2[0][tid] = 0.f;
+        if (tid < D) sm.y2[0][tid] = sm.y2s[0][tid] = 0.f;
         if (tid < SL) sm.x1[0][tid] = 0.f;
         for (int e = tid; e < D * RS64; e += NTH) sm.y3h[e] = (_Float16)0.0f;
     }
@@ -288,23 +289,6 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             const h8 pb = perm_operand(r16, h, true, (_Float16)1.0f);
             const h8 pa2 = perm_operand(r16, h, false, (_Float16)2.0f);
             const h8 pb2 = perm_operand(r16, h, true, (_Float16)2.0f);
-            // rebuild the fp32 tiles of channel i (diagonal tile: stored halved,
-            // 0/2 matrix).  Channel i+1 is rebuilt before channel i is rounded
-            // back: the pair it shares with channel i is then read before that
-            // write (its other half is multiplied by zero), so the channels do
-            // not form one dependency chain.
-            auto rebuild = [&](auto ii, f4(&acc)[4]) {
-                constexpr int i = decltype(ii)::value;
-                constexpr int t0 = first_tile(i);
-                static_for<0, 4 - u0_of(i)>([&](auto ui) {
-                    constexpr int uu = decltype(ui)::value;
-                    constexpr int t = t0 + uu;
-                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
-                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
-                });
-            };
-            f4 accA[4], accB[4];
-            rebuild(std::integral_constant<int, 0>{}, accA);
             {
                 // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
                 f4 acc = mfma(pa, Ast[0], f4{0.f, 0.f, 0.f, 0.f});
@@ -318,13 +302,18 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 constexpr int u0 = u0_of(i);
                 constexpr int t0 = first_tile(i);
                 constexpr int nu = 4 - u0;
-                f4(&acc)[4] = (i & 1) ? accB : accA;
                 const int m = 16 * u0 + 4 * w + (i & 3);
                 h8 Wm[NKS2];
 #pragma unroll
                 for (int s = 0; s < NKS2; ++s) Wm[s] = ld8(kTc + sw128(m, 32 * s + 8 * h)) * Vf[s];
-                if constexpr (i + 1 < NQ)
-                    rebuild(std::integral_constant<int, i + 1>{}, (i & 1) ? accA : accB);
+                // rebuild the fp32 tiles (diagonal tile: stored halved, 0/2 matrix)
+                f4 acc[nu];
+                static_for<0, nu>([&](auto ui) {
+                    constexpr int uu = decltype(ui)::value;
+                    constexpr int t = t0 + uu;
+                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
+                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
+                });
 #pragma unroll
                 for (int s = 0; s < NKS2; ++s)
                     static_for<0, nu>([&](auto ui) {
@@ -348,6 +337,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
         float prg = 1.0f;
         f4 y3acc[3] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
         int gexp = 0;   // Y3 in LDS is Y3 * 2^-gexp
+        const h8 ones8 = {1, 1, 1, 1, 1, 1, 1, 1};
 
         auto prefetch = [&](int c) {
             const int ht = tid - NSW * 64;
@@ -426,7 +416,10 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                     const h8 QB0 = ld8(sm.qrow + sw64(tok, 8 * h));
                     const h8 QB1 = ld8(sm.qrow + sw64(tok, 32 + 8 * h));
                     f4 F = {0.f, 0.f, 0.f, 0.f};
-                    float gpart = 0.f;
+                    // in-chunk row sums of the weights: every row of
+                    // ones x W is the column sum, so each lane holds the full
+                    // sum for its query
+                    f4 Gin = {0.f, 0.f, 0.f, 0.f};
                     // S^T tile (rows: keys 16tt.., columns: queries) -> 2 f(s):
                     // the accumulator starts at 1, so t = s + 1 and
                     // 2 f_2(s) = t^2 + 1 is one FMA; the factor 2 is removed
@@ -441,7 +434,6 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                             float y = fmaf(S[i], S[i], 1.0f);
                             if (diag && (4 * h + i) > r16) y = 0.0f;
                             wv[i] = y;
-                            gpart += y;
                         }
                         return cvt4(wv);
                     };
@@ -453,6 +445,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                         F = mfma(cat(ld4(vTc + sw128(r16, 16 * a + 4 * h)),
                                      ld4(vTc + sw128(r16, 16 * a + 16 + 4 * h))),
                                  cat(wa, wb), F);
+                        if constexpr (!DV) Gin = mfma(ones8, cat(wa, wb), Gin);
                     }
                     {
                         // the last pair holds the diagonal tile rt (masked to
@@ -466,18 +459,16 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                             vb = ld4(vTc + sw128(r16, 16 * rt + 4 * h));
                         }
                         F = mfma(cat(va, vb), cat(wa, wb), F);
+                        if constexpr (!DV) Gin = mfma(ones8, cat(wa, wb), Gin);
                     }
-                    gpart *= 0.5f;
+                    float gpart = 0.f;
                     if (!DV) {
                         // inter-chunk denominator q.y2 + 1/2 q^T Y3 q (+ n0)
                         float gq = 0.f;
-                        const float ys = ldexpf(2.0f, -gexp);
 #pragma unroll
                         for (int cc = 0; cc < 4; ++cc) {
                             const h4 ql = ld4(sm.qrow + sw64(tok, 16 * cc + 4 * h));
-                            f4 T;
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) T[i] = ys * sm.y2[cur][16 * cc + 4 * h + i];
+                            f4 T = *(const f4 *)(sm.y2s[cur] + 16 * cc + 4 * h);
                             T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 8 * h)), QB0, T);
                             T = mfma(ld8(sm.y3h + sw64(16 * cc + r16, 32 + 8 * h)), QB1, T);
 #pragma unroll
@@ -488,6 +479,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                     }
                     gpart += __shfl_xor(gpart, 16);
                     gpart += __shfl_xor(gpart, 32);
+                    gpart = fmaf(0.5f, Gin[0], gpart);
                     Fin[r] = F;
                     Gs[r] = gpart;
                 }
@@ -517,28 +509,31 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                     if (!DV && g && sl == 0 && h == 0) g[n0 + tok] = Gs[r];
                 }
             }
-            // prefix sums: y2 (channels 16hw..16hw+15), x1 (helper 0)
+            // prefix sums y2 (channels 16hw..16hw+15) and x1 (helper 0) as
+            // row sums (k^T or v^T) x ones: lane (r16, h) holds the sums of
+            // rows 4h..4h+3
+            const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
             if (!DV) {
-                const int m = 16 * hw + r16;
-                float s = 0.f;
+                f4 s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int cc = 0; cc < 4; ++cc) s += hsum8(ld8(kTc + sw128(m, 32 * h + 8 * cc)));
-                s += __shfl_xor(s, 16);
-                s += __shfl_xor(s, 32);
-                if (h == 0) sm.y2[nxt][m] = sm.y2[cur][m] + s;
+                for (int st = 0; st < NKS2; ++st)
+                    s4 = mfma(ld8(kTc + sw128(16 * hw + r16, 32 * st + 8 * h)), ones8, s4);
+                if (r16 == 0) {
+                    const f4 y = *(const f4 *)(sm.y2[cur] + 16 * hw + 4 * h) + s4;
+                    *(f4 *)(sm.y2[nxt] + 16 * hw + 4 * h) = y;
+                    *(f4 *)(sm.y2s[nxt] + 16 * hw + 4 * h) = ldexpf(2.0f, -gnext) * y;
+                }
             }
             if (hw == 0) {
-                float sv = 0.f;
+                f4 s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int cc = 0; cc < 4; ++cc) sv += hsum8(ld8(vTc + sw128(r16, 32 * h + 8 * cc)));
-                sv += __shfl_xor(sv, 16);
-                sv += __shfl_xor(sv, 32);
-                if (h == 0) sm.x1[nxt][r16] = sm.x1[cur][r16] + sv;
+                for (int st = 0; st < NKS2; ++st)
+                    s4 = mfma(ld8(vTc + sw128(r16, 32 * st + 8 * h)), ones8, s4);
+                if (r16 == 0) *(f4 *)(sm.x1[nxt] + 4 * h) = *(const f4 *)(sm.x1[cur] + 4 * h) + s4;
             }
             if (!DV) {
                 // Y3 += K^T K and its scaled fp16 copy for the next chunk
                 const int ny3 = y3_count(hw);
-                const int gnext = max(0, pow2_exponent(64.0f * (float)(n0 + nvalid)));
                 const float gs = ldexpf(1.0f, -gnext);
 #pragma unroll
                 for (int kk = 0; kk < 3; ++kk) {
