@@ -343,14 +343,28 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             const int ht = tid - NSW * 64;
             const int tg = ht >> 3, cg = ht & 7;
             const uint4 z = {0u, 0u, 0u, 0u};
+            const int nb = c * C + 4 * tg;
+            if (nb + 3 < N) {
+                // all four rows in range (every chunk but the last): one base
+                // address, the rows at fixed offsets from it
+                constexpr int step = DV ? -D : D;
+                const size_t p0 = DV ? (size_t)(N - 1 - nb) : (size_t)nb;
+                const _Float16 *qp = q + p0 * D + 8 * cg, *kp = k + p0 * D + 8 * cg;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int n = c * C + 4 * tg + j;
-                pq[j] = pk[j] = z;
-                if (n < N) {
-                    const size_t pn = DV ? (size_t)(N - 1 - n) : (size_t)n;
-                    pq[j] = *(const uint4 *)(q + pn * D + 8 * cg);
-                    pk[j] = *(const uint4 *)(k + pn * D + 8 * cg);
+                for (int j = 0; j < 4; ++j) {
+                    pq[j] = *(const uint4 *)(qp + j * step);
+                    pk[j] = *(const uint4 *)(kp + j * step);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int n = nb + j;
+                    pq[j] = pk[j] = z;
+                    if (n < N) {
+                        const size_t pn = DV ? (size_t)(N - 1 - n) : (size_t)n;
+                        pq[j] = *(const uint4 *)(q + pn * D + 8 * cg);
+                        pk[j] = *(const uint4 *)(k + pn * D + 8 * cg);
+                    }
                 }
             }
             const int vt = ht >> 1, vh = ht & 1;
