@@ -117,6 +117,10 @@ def main():
                     help="fwd: one forward per step (the headline); fwdbwd: forward + "
                          "backward per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold", type=int, default=None, metavar="ITERS",
+                    help="after the timed region, time ITERS calls each preceded by a "
+                         "512 MiB write that flushes the caches (default 10 for the bf16 "
+                         "MFMA workloads, 0 otherwise)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
                     help="only run a plain device-to-device copy of this many MiB "
                          "(for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE) and exit")
@@ -258,6 +262,69 @@ def main():
                                     "peak": PEAK[("mfma", "bf16")],
                                     "frac": ach / PEAK[("mfma", "bf16")],
                                     "traffic": load_traffic("fastmax_bwd", w.name)})
+    rec["roofline"]["median_launch_ms"] = float(np.median(launch_ms))
+    if args.mode == "fwdbwd":
+        rec["backward"]["median_ms"] = float(np.median(bwd_ms))
+
+    # cold calls: caches flushed by a 512 MiB write before each one
+    cold = args.cold if args.cold is not None else (10 if w.dtype == "bf16" and w.p == 2 else 0)
+    if cold > 0:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * cold)]
+
+        def cold_median(call):
+            for i in range(cold):
+                flush.fill_(i & 255)
+                ev[2 * i].record(stream)
+                call()
+                ev[2 * i + 1].record(stream)
+            torch.cuda.synchronize()
+            return float(np.median([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(cold)]))
+
+        def fwd_call():
+            rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
+                                    need, stream)
+            if rc != fm.OK:
+                raise fm.FastmaxError(rc, "fastmax_fwd")
+
+        def bwd_call():
+            rc = fm.fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, w.B, w.H, w.N, w.D, w.p,
+                                    w.causal, dt, ws_b, need_b, stream)
+            if rc != fm.OK:
+                raise fm.FastmaxError(rc, "fastmax_bwd")
+
+        rec["cold"] = {"iters": cold, "flush_bytes": 512 << 20,
+                       "fwd_median_ms": cold_median(fwd_call)}
+        if args.mode == "fwdbwd":
+            rec["cold"]["bwd_median_ms"] = cold_median(bwd_call)
+        del flush
+
+    # linear in N (long non-causal workload): the same recipe at N = 8192
+    if not w.causal and w.N > 8192 and w.dtype == "bf16" and w.p == 2 and args.mode == "fwd":
+        n_s = 8192
+        inp_s = workload_inputs(w, want64=False, N=n_s)
+        qs, ks, vs = (to_dev(inp_s[n]) for n in ("q", "k", "v"))
+        outs = torch.empty_like(qs)
+        need_s = fm.workspace_bytes(w.B, w.H, n_s, w.D, w.p, w.causal, dt, False)
+        ws_s = torch.empty(max(need_s, 1), dtype=torch.uint8, device=dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * max(args.steps, 1))]
+        for i in range(args.warmup + max(args.steps, 1)):
+            j = i - args.warmup
+            if j >= 0:
+                ev[2 * j].record(stream)
+            rc = fm.fastmax_fwd_raw(qs, ks, vs, outs, None, w.B, w.H, n_s, w.D, w.p, w.causal,
+                                    dt, ws_s, need_s, stream)
+            if rc != fm.OK:
+                raise fm.FastmaxError(rc, "fastmax_fwd")
+            if j >= 0:
+                ev[2 * j + 1].record(stream)
+        torch.cuda.synchronize()
+        t_s = float(np.median([ev[2 * j].elapsed_time(ev[2 * j + 1])
+                               for j in range(max(args.steps, 1))]))
+        t_f = rec["roofline"]["median_launch_ms"]
+        rec["linear_in_n"] = {"n_small": n_s, "n_full": w.N, "small_median_ms": t_s,
+                              "full_median_ms": t_f, "ratio": t_f / t_s,
+                              "ideal": w.N / n_s}
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(rec), flush=True)
