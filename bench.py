@@ -103,8 +103,26 @@ def cpu_baseline(w, inp_bits):
     t0 = time.perf_counter()
     oracle.fwd_fact(q, k, v, w.p, w.causal)
     dt = time.perf_counter() - t0
-    return {"value": heads * N / dt, "unit": "tokens*heads/s", "cores": threads,
-            "kind": "oracle", "sample": sample + f" (fwd_fact, {dt:.1f} s)"}
+    rec = {"value": heads * N / dt, "unit": "tokens*heads/s", "cores": threads,
+           "kind": "oracle", "sample": sample + f" (fwd_fact, {dt:.1f} s)",
+           "cpu_model": cpu_model()}
+    if N <= 4096:
+        # the explicit N x N definition as well, on the same sample
+        t0 = time.perf_counter()
+        oracle.fwd_brute(q, k, v, w.p, w.causal)
+        rec["brute_force_value"] = heads * N / (time.perf_counter() - t0)
+    return rec
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
