@@ -41,12 +41,13 @@ def _bind(path):
     I = ctypes.c_int
     lib.fmo_num_threads.restype = I
     lib.fmo_standardize.argtypes = [dp, L, L, dp, dp, dp]
-    lib.fmo_attention_matrix.argtypes = [dp, dp, L, L, I, I, dp]
-    lib.fmo_fwd_brute.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp, dp]
-    lib.fmo_fwd_fact.argtypes = [dp, dp, dp, L, L, L, L, I, I, dp, dp]
-    lib.fmo_fwd_rows.argtypes = [dp, dp, dp, L, L, L, L, I, I, L,
+    F = ctypes.c_double
+    lib.fmo_attention_matrix.argtypes = [dp, dp, L, L, I, I, F, dp]
+    lib.fmo_fwd_brute.argtypes = [dp, dp, dp, L, L, L, L, I, I, F, dp, dp, dp]
+    lib.fmo_fwd_fact.argtypes = [dp, dp, dp, L, L, L, L, I, I, F, dp, dp]
+    lib.fmo_fwd_rows.argtypes = [dp, dp, dp, L, L, L, L, I, I, F, L,
                                  ctypes.POINTER(ctypes.c_int64), dp, dp, dp]
-    lib.fmo_bwd_brute.argtypes = [dp, dp, dp, dp, dp, L, L, L, L, I, I,
+    lib.fmo_bwd_brute.argtypes = [dp, dp, dp, dp, dp, L, L, L, L, I, I, F,
                                   dp, dp, dp]
     return lib
 
@@ -96,41 +97,43 @@ def standardize(x):
     return xh, mu, sg
 
 
-def attention_matrix(q, k, p, causal):
-    """Explicit N x N Fastmax attention matrix of ONE head, q/k shaped [N, D]."""
+def attention_matrix(q, k, p, causal, scale=1.0):
+    """Explicit N x N Fastmax attention matrix of ONE head, q/k shaped [N, D];
+    weights f_p(scale * q^.k^)."""
     q, k = _f64(q), _f64(k)
     N, D = q.shape
     A = np.empty((N, N))
     _load().fmo_attention_matrix(_ptr(q), _ptr(k), N, D, int(p), int(causal),
-                                 _ptr(A))
+                                 float(scale), _ptr(A))
     return A
 
 
-def fwd_brute(q, k, v, p, causal, with_abs=False):
-    """Brute force O(N^2 D) forward; returns (O, G) or, with ``with_abs``,
-    (O, G, sum_n |w_in|)."""
+def fwd_brute(q, k, v, p, causal, with_abs=False, scale=1.0):
+    """Brute force O(N^2 D) forward with weights f_p(scale * s); returns
+    (O, G) or, with ``with_abs``, (O, G, sum_n |w_in|)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, N, D = _shape4(q)
     out = np.empty_like(q)
     g = np.empty((B, H, N))
     gabs = np.empty((B, H, N)) if with_abs else None
     _load().fmo_fwd_brute(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
-                          int(causal), _ptr(out), _ptr(g), _ptr(gabs))
+                          int(causal), float(scale), _ptr(out), _ptr(g), _ptr(gabs))
     return (out, g, gabs) if with_abs else (out, g)
 
 
-def fwd_fact(q, k, v, p, causal):
-    """Factorised moment forward (Sec. 2.4); returns (O, G)."""
+def fwd_fact(q, k, v, p, causal, scale=1.0):
+    """Factorised moment forward (Sec. 2.4) with weights f_p(scale * s);
+    returns (O, G)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, N, D = _shape4(q)
     out = np.empty_like(q)
     g = np.empty((B, H, N))
     _load().fmo_fwd_fact(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
-                         int(causal), _ptr(out), _ptr(g))
+                         int(causal), float(scale), _ptr(out), _ptr(g))
     return out, g
 
 
-def fwd_rows(q, k, v, p, causal, rows, with_abs=False):
+def fwd_rows(q, k, v, p, causal, rows, with_abs=False, scale=1.0):
     """Brute force for selected rows (flat index b*H*N + h*N + i).
 
     Returns (O_rows [n, D], G_rows [n]) and, with ``with_abs``, also
@@ -143,13 +146,13 @@ def fwd_rows(q, k, v, p, causal, rows, with_abs=False):
     g = np.empty(rows.size)
     gabs = np.empty(rows.size) if with_abs else None
     _load().fmo_fwd_rows(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, int(p),
-                         int(causal), rows.size,
+                         int(causal), float(scale), rows.size,
                          rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                          _ptr(out), _ptr(g), _ptr(gabs))
     return (out, g, gabs) if with_abs else (out, g)
 
 
-def bwd_brute(q, k, v, dout, p, causal, o_used=None):
+def bwd_brute(q, k, v, dout, p, causal, o_used=None, scale=1.0):
     """Brute force O(N^2 D) backward; returns (dq, dk, dv).
 
     ``o_used``: the forward output the gradient is taken at (default: the
@@ -164,6 +167,6 @@ def bwd_brute(q, k, v, dout, p, causal, o_used=None):
     dk = np.empty_like(q)
     dv = np.empty_like(q)
     _load().fmo_bwd_brute(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(o_used),
-                          B, H, N, D, int(p), int(causal), _ptr(dq), _ptr(dk),
-                          _ptr(dv))
+                          B, H, N, D, int(p), int(causal), float(scale), _ptr(dq),
+                          _ptr(dk), _ptr(dv))
     return dq, dk, dv

@@ -16,8 +16,11 @@
  *    without its 1/2, the definition in Sec. 2.2 has it, and the definition wins.
  *  - Standardisation (Sec. 2.2, Eqs. 6-7) is over the D channels of one token,
  *    with the population standard deviation and no epsilon.
- *  - No temperature: the score is q^.k^ itself (Sec. 2.2), unlike softmax's
- *    1/sqrt(D) (Sec. 2.1).
+ *  - No temperature by default: the score is q^.k^ itself (Sec. 2.2), unlike
+ *    softmax's 1/sqrt(D) (Sec. 2.1).  Every routine takes a score scale tau
+ *    (weights f_p(tau q^.k^)); tau = 1 is the paper's definition, tau = 1/D
+ *    the unit-norm variant (q^ and k^ divided by sqrt(D), so |tau s| <= 1 as
+ *    the bound of Sec. 2.3 assumes and f_1 >= 0, Eq. "valid").
  *  - Causal mask is inclusive: row i sums over n <= i (Sec. 2.1 tril, Sec. 2.4
  *    causal F and G).
  *  - The "I" in the matrix forms of F and G (Sec. 2.4) is the all-ones matrix:
@@ -95,7 +98,7 @@ void fmo_standardize(const double *x, long rows, long D, double *xh, double *mu,
 /* masked with tril when causal, Sec. 2.1).  A is N x N, row-major.           */
 /* ------------------------------------------------------------------------ */
 void fmo_attention_matrix(const double *q, const double *k, long N, long D,
-                          int p, int causal, double *A)
+                          int p, int causal, double tau, double *A)
 {
     double *qh = malloc(sizeof(double) * N * D);
     double *kh = malloc(sizeof(double) * N * D);
@@ -110,7 +113,7 @@ void fmo_attention_matrix(const double *q, const double *k, long N, long D,
             if (!causal || n <= i) {
                 double s = 0.0;
                 for (long d = 0; d < D; ++d) s += qh[i * D + d] * kh[n * D + d];
-                w = f_taylor(s, p);
+                w = f_taylor(tau * s, p);
             }
             row[n] = w;
             g += w;
@@ -127,8 +130,8 @@ void fmo_attention_matrix(const double *q, const double *k, long N, long D,
 /* qh_i: standardised query row; kh, v: the head's N x D blocks.              */
 /* ------------------------------------------------------------------------ */
 static void brute_row(const double *qh_i, const double *kh, const double *v,
-                      long i, long N, long D, int p, int causal, double *o,
-                      double *g_out, double *gabs_out)
+                      long i, long N, long D, int p, int causal, double tau,
+                      double *o, double *g_out, double *gabs_out)
 {
     long nend = causal ? i + 1 : N;
     double g = 0.0, gabs = 0.0;
@@ -136,7 +139,7 @@ static void brute_row(const double *qh_i, const double *kh, const double *v,
     for (long n = 0; n < nend; ++n) {
         double s = 0.0;
         for (long d = 0; d < D; ++d) s += qh_i[d] * kh[n * D + d];
-        double w = f_taylor(s, p);
+        double w = f_taylor(tau * s, p);
         g += w;
         gabs += fabs(w);
         for (long d = 0; d < D; ++d) o[d] += w * v[n * D + d];
@@ -149,8 +152,8 @@ static void brute_row(const double *qh_i, const double *kh, const double *v,
 /* Full brute-force forward, O(N^2 D) per head.  g (row sums G_i) and gabs
  * (sum_n |w_in|, the scale of the cancellation in G for p = 1) may be NULL. */
 void fmo_fwd_brute(const double *q, const double *k, const double *v, long B,
-                   long H, long N, long D, int p, int causal, double *out,
-                   double *g, double *gabs)
+                   long H, long N, long D, int p, int causal, double tau,
+                   double *out, double *g, double *gabs)
 {
     long rows = B * H * N;
     double *qh = malloc(sizeof(double) * rows * D);
@@ -161,7 +164,8 @@ void fmo_fwd_brute(const double *q, const double *k, const double *v, long B,
     for (long r = 0; r < rows; ++r) {
         long head = r / N, i = r % N;
         brute_row(qh + r * D, kh + head * N * D, v + head * N * D, i, N, D, p,
-                  causal, out + r * D, g ? g + r : NULL, gabs ? gabs + r : NULL);
+                  causal, tau, out + r * D, g ? g + r : NULL,
+                  gabs ? gabs + r : NULL);
     }
     free(qh);
     free(kh);
@@ -170,7 +174,7 @@ void fmo_fwd_brute(const double *q, const double *k, const double *v, long B,
 /* Brute force on a sample of rows.  rows[] holds flat indices b*H*N + h*N + i;
  * out_rows is [nrows, D]; g_rows and gabs_rows are [nrows] (may be NULL). */
 void fmo_fwd_rows(const double *q, const double *k, const double *v, long B,
-                  long H, long N, long D, int p, int causal, long nrows,
+                  long H, long N, long D, int p, int causal, double tau, long nrows,
                   const int64_t *rows, double *out_rows, double *g_rows,
                   double *gabs_rows)
 {
@@ -186,7 +190,7 @@ void fmo_fwd_rows(const double *q, const double *k, const double *v, long B,
         standardize_row(q + r * D, D, qh, NULL, NULL);
         for (long n = 0; n < nend; ++n)
             standardize_row(k + (head * N + n) * D, D, kh + n * D, NULL, NULL);
-        brute_row(qh, kh, v + head * N * D, i, N, D, p, causal,
+        brute_row(qh, kh, v + head * N * D, i, N, D, p, causal, tau,
                   out_rows + t * D, g_rows ? g_rows + t : NULL,
                   gabs_rows ? gabs_rows + t : NULL);
         free(qh);
@@ -256,22 +260,26 @@ static void moments_add(moments_t *M, const double *k, const double *v, int p)
     }
 }
 
-/* Contract the moments with a standardised query row; writes o (D) and g. */
-static void moments_query(const moments_t *M, const double *q, int p, double *o,
-                          double *g_out)
+/* Contract the moments with a standardised query row; writes o (D) and g.
+ * With the score scale tau, f(tau s) = 1 + tau s + tau^2 s^2 / 2, so the
+ * linear moments enter with tau and the quadratic ones with tau^2 / 2. */
+static void moments_query(const moments_t *M, const double *q, int p,
+                          double tau, double *o, double *g_out)
 {
     long D = M->D;
-    double g = M->y1;
-    for (long m = 0; m < D; ++m) g += q[m] * M->y2[m];
+    double lin = 0.0;
+    for (long m = 0; m < D; ++m) lin += q[m] * M->y2[m];
+    double g = M->y1 + tau * lin;
     if (p >= 2) {
         double quad = 0.0;
         for (long m = 0; m < D; ++m)
             for (long l = 0; l < D; ++l) quad += q[m] * q[l] * M->y3[m * D + l];
-        g += 0.5 * quad;
+        g += 0.5 * tau * tau * quad;
     }
     for (long j = 0; j < D; ++j) {
-        double f = M->x1[j];
-        for (long m = 0; m < D; ++m) f += q[m] * M->x2[j * D + m];
+        double fl = 0.0;
+        for (long m = 0; m < D; ++m) fl += q[m] * M->x2[j * D + m];
+        double f = M->x1[j] + tau * fl;
         if (p >= 2) {
             double quad = 0.0;
             for (long m = 0; m < D; ++m) {
@@ -280,7 +288,7 @@ static void moments_query(const moments_t *M, const double *q, int p, double *o,
                 for (long l = 0; l < D; ++l) inner += q[l] * x3jm[l];
                 quad += q[m] * inner;
             }
-            f += 0.5 * quad;
+            f += 0.5 * tau * tau * quad;
         }
         o[j] = f / g;
     }
@@ -288,8 +296,8 @@ static void moments_query(const moments_t *M, const double *q, int p, double *o,
 }
 
 void fmo_fwd_fact(const double *q, const double *k, const double *v, long B,
-                  long H, long N, long D, int p, int causal, double *out,
-                  double *g)
+                  long H, long N, long D, int p, int causal, double tau,
+                  double *out, double *g)
 {
     long heads = B * H;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -309,14 +317,14 @@ void fmo_fwd_fact(const double *q, const double *k, const double *v, long B,
             }
             for (long i = 0; i < N; ++i) {
                 standardize_row(qb + i * D, D, qh, NULL, NULL);
-                moments_query(&M, qh, p, ob + i * D, gb ? gb + i : NULL);
+                moments_query(&M, qh, p, tau, ob + i * D, gb ? gb + i : NULL);
             }
         } else {
             for (long i = 0; i < N; ++i) {
                 standardize_row(kb + i * D, D, kh, NULL, NULL);
                 moments_add(&M, kh, vb + i * D, p);
                 standardize_row(qb + i * D, D, qh, NULL, NULL);
-                moments_query(&M, qh, p, ob + i * D, gb ? gb + i : NULL);
+                moments_query(&M, qh, p, tau, ob + i * D, gb ? gb + i : NULL);
             }
         }
         moments_free(&M);
@@ -330,8 +338,10 @@ void fmo_fwd_fact(const double *q, const double *k, const double *v, long B,
 /*                                                                           */
 /* Score derivative (Sec. 2.3, Eq. "bound", with the index typos read as     */
 /* a_in / a_il):  d o_ij / d s_il = f'(s_il) / G_i * (v_lj - o_ij), and       */
-/* d o_ij / d v_lj = a_il.  With upstream dO:                                 */
-/*   ds_il  = sum_j dO_ij f'(s_il)/G_i (v_lj - o_ij)                           */
+/* d o_ij / d v_lj = a_il.  With the score scale tau the weight is            */
+/* f(tau s_il), whose derivative in s_il is tau f'(tau s_il).  With upstream  */
+/* dO:                                                                        */
+/*   ds_il  = sum_j dO_ij tau f'(tau s_il)/G_i (v_lj - o_ij)                   */
 /*   dv_l   = sum_i a_il dO_i                                                 */
 /*   dq^_i  = sum_l ds_il k^_l,   dk^_l = sum_i ds_il q^_i                     */
 /* then back through Eqs. (6)-(7):                                            */
@@ -356,8 +366,8 @@ static void std_backward_row(const double *xh, const double *dxh, double sig,
  * to its storage precision (the stored output a bf16 backward consumes). */
 void fmo_bwd_brute(const double *q, const double *k, const double *v,
                    const double *dout, const double *o_used, long B, long H,
-                   long N, long D, int p, int causal, double *dq, double *dk,
-                   double *dv)
+                   long N, long D, int p, int causal, double tau, double *dq,
+                   double *dk, double *dv)
 {
     long heads = B * H;
     for (long hd = 0; hd < heads; ++hd) {
@@ -375,7 +385,7 @@ void fmo_bwd_brute(const double *q, const double *k, const double *v,
         /* forward, per row */
 #pragma omp parallel for schedule(dynamic, 8)
         for (long i = 0; i < N; ++i)
-            brute_row(qh + i * D, kh, vb, i, N, D, p, causal, o + i * D, G + i,
+            brute_row(qh + i * D, kh, vb, i, N, D, p, causal, tau, o + i * D, G + i,
                       NULL);
         if (o_used)
             memcpy(o, o_used + hd * N * D, sizeof(double) * N * D);
@@ -388,7 +398,7 @@ void fmo_bwd_brute(const double *q, const double *k, const double *v,
             for (long l = 0; l < lend; ++l) {
                 double s = 0.0;
                 for (long d = 0; d < D; ++d) s += qh[i * D + d] * kh[l * D + d];
-                double coef = df_taylor(s, p) / G[i];
+                double coef = tau * df_taylor(tau * s, p) / G[i];
                 double ds = 0.0;
                 for (long j = 0; j < D; ++j)
                     ds += dob[i * D + j] * coef * (vb[l * D + j] - o[i * D + j]);
@@ -405,8 +415,8 @@ void fmo_bwd_brute(const double *q, const double *k, const double *v,
             for (long i = istart; i < N; ++i) {
                 double s = 0.0;
                 for (long d = 0; d < D; ++d) s += qh[i * D + d] * kh[l * D + d];
-                double a = f_taylor(s, p) / G[i];
-                double coef = df_taylor(s, p) / G[i];
+                double a = f_taylor(tau * s, p) / G[i];
+                double coef = tau * df_taylor(tau * s, p) / G[i];
                 double ds = 0.0;
                 for (long j = 0; j < D; ++j)
                     ds += dob[i * D + j] * coef * (vb[l * D + j] - o[i * D + j]);

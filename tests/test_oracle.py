@@ -108,9 +108,9 @@ def check_brute_vs_fact(shapes=((1, 2, 37, 4), (2, 1, 64, 8), (1, 1, 33, 16))):
                 np.testing.assert_allclose(gb, gf, rtol=1e-10, atol=1e-9)
 
 
-def _fd_grads(q, k, v, do, p, causal, h=1e-6):
+def _fd_grads(q, k, v, do, p, causal, h=1e-6, scale=1.0):
     def loss(q_, k_, v_):
-        o, _ = oracle.fwd_brute(q_, k_, v_, p, causal)
+        o, _ = oracle.fwd_brute(q_, k_, v_, p, causal, scale=scale)
         return float((o * do).sum())
     grads = []
     for which in range(3):
@@ -140,9 +140,100 @@ def check_bwd_finite_differences():
                 assert err < 2e-6, (nm, p, causal, err)
 
 
+def _std_np(x):
+    c = x - x.mean(-1, keepdims=True)
+    return c / np.sqrt((c ** 2).mean(-1, keepdims=True))
+
+
+# Score scale tau (weights f_p(tau s); tau = 1/D is the unit-norm variant,
+# Sec. 2.3 assumes |s| <= 1).
+def check_scale_p1_closed_form():
+    """p = 1: w = 1 + tau s, so o_i = (sum v + tau (sum v k^T) q^_i) /
+    (n_i + tau q^_i . sum k^), on both oracle routes."""
+    q, k, v = _rand(1, 1, 25, 6, 31)
+    qh, kh, vv = _std_np(q)[0, 0], _std_np(k)[0, 0], v[0, 0]
+    tau = 1.0 / 6
+    for causal in (False, True):
+        exp = np.empty((25, 6))
+        for i in range(25):
+            n = i + 1 if causal else 25
+            exp[i] = (vv[:n].sum(0) + tau * (vv[:n].T @ kh[:n]) @ qh[i]) / \
+                (n + tau * qh[i] @ kh[:n].sum(0))
+        for route in (oracle.fwd_brute, oracle.fwd_fact):
+            o, _ = route(q, k, v, 1, causal, scale=tau)
+            np.testing.assert_allclose(o[0, 0], exp, rtol=1e-10, atol=1e-10)
+
+
+def check_scale_p2_explicit():
+    """p = 2 on a tiny problem: W = 1 + tau S + (tau S)^2 / 2 written out."""
+    q, k, v = _rand(1, 1, 9, 4, 33)
+    qh, kh, vv = _std_np(q)[0, 0], _std_np(k)[0, 0], v[0, 0]
+    tau = 0.37
+    S = tau * (qh @ kh.T)
+    W = 1 + S + S * S / 2
+    for causal in (False, True):
+        Wc = np.tril(W) if causal else W
+        exp, gexp = (Wc @ vv) / Wc.sum(1, keepdims=True), Wc.sum(1)
+        for route in (oracle.fwd_brute, oracle.fwd_fact):
+            o, g = route(q, k, v, 2, causal, scale=tau)
+            np.testing.assert_allclose(o[0, 0], exp, rtol=1e-11, atol=1e-11)
+            np.testing.assert_allclose(g[0, 0], gexp, rtol=1e-11)
+
+
+def check_scale_small_limit():
+    """tau -> 0: every weight tends to 1, O_i to the mean of the visible values."""
+    q, k, v = _rand(1, 2, 30, 8, 32)
+    pref = np.cumsum(v, 2) / np.arange(1, 31)[:, None]
+    for p in (1, 2):
+        for causal in (False, True):
+            exp = pref if causal else np.broadcast_to(v.mean(2, keepdims=True), v.shape)
+            for route in (oracle.fwd_brute, oracle.fwd_fact):
+                o, _ = route(q, k, v, p, causal, scale=1e-9)
+                np.testing.assert_allclose(o, exp, atol=1e-6)
+
+
+def check_scale_bwd_finite_differences():
+    for p in (1, 2):
+        for causal in (False, True):
+            q, k, v = _rand(1, 1, 5, 4, 40 + p)
+            do = np.random.default_rng([2402, 7901, 78]).standard_normal(q.shape)
+            dq, dk, dv = oracle.bwd_brute(q, k, v, do, p, causal, scale=0.3)
+            fq, fk, fv = _fd_grads(q, k, v, do, p, causal, scale=0.3)
+            for a, b, nm in ((dq, fq, "dq"), (dk, fk, "dk"), (dv, fv, "dv")):
+                err = np.abs(a - b).max() / max(1.0, np.abs(b).max())
+                assert err < 2e-6, (nm, p, causal, err)
+
+
 # --------------------------------------------------------------------------
 # pytest entry points
 # --------------------------------------------------------------------------
+def test_scale_p1_closed_form():
+    check_scale_p1_closed_form()
+
+
+def test_scale_p2_explicit():
+    check_scale_p2_explicit()
+
+
+def test_scale_small_limit():
+    check_scale_small_limit()
+
+
+def test_scale_bwd_finite_differences():
+    check_scale_bwd_finite_differences()
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_unit_norm_makes_p1_weights_valid(causal):
+    """With tau = 1/D, |tau s| <= 1, so f_1 = 1 + tau s >= 0 and the rows of A
+    are convex weights (Eq. "valid"); with tau = 1 some weights are negative
+    on the same inputs."""
+    q, k, _ = _rand(1, 1, 64, 8, 34)
+    A = oracle.attention_matrix(q[0, 0], k[0, 0], 1, causal, scale=1.0 / 8)
+    assert A.min() >= 0.0
+    np.testing.assert_allclose(A.sum(1), 1.0, rtol=1e-12)
+    A1 = oracle.attention_matrix(q[0, 0], k[0, 0], 1, causal)
+    assert A1.min() < 0.0
 def test_golden_standardize():
     check_golden_standardize()
 
@@ -329,7 +420,13 @@ MUTATIONS = {
                    "var /= (double)(D - 1);"),
     "exclusive_causal": ("long nend = causal ? i + 1 : N;\n    double g = 0.0, gabs",
                          "long nend = causal ? i : N;\n    double g = 0.0, gabs"),
-    "fact_drop_half_g": ("g += 0.5 * quad;", "g += quad;"),
+    "fact_drop_half_g": ("g += 0.5 * tau * tau * quad;", "g += tau * tau * quad;"),
+    "scale_brute_dropped": ("double w = f_taylor(tau * s, p);\n        g += w;",
+                            "double w = f_taylor(s, p);\n        g += w;"),
+    "scale_fact_quad_once": ("f += 0.5 * tau * tau * quad;", "f += 0.5 * tau * quad;"),
+    "scale_fact_lin_g": ("double g = M->y1 + tau * lin;", "double g = M->y1 + lin;"),
+    "scale_bwd_chain": ("double a = f_taylor(tau * s, p) / G[i];\n                double coef = tau * df_taylor",
+                        "double a = f_taylor(tau * s, p) / G[i];\n                double coef = df_taylor"),
     "fact_transposed_x2": ("M->x2[j * D + m] += k[m] * vj;", "M->x2[m * D + j] += k[m] * vj;"),
     "fact_wrong_query_index": ("for (long l = 0; l < D; ++l) inner += q[l] * x3jm[l];",
                                "for (long l = 0; l < D; ++l) inner += q[m] * x3jm[l];"),
@@ -341,7 +438,9 @@ MUTATIONS = {
 }
 
 ALL_CHECKS = (check_golden_standardize, check_golden_forward, check_golden_backward,
-              check_brute_vs_fact, check_bwd_finite_differences)
+              check_brute_vs_fact, check_bwd_finite_differences, check_scale_p1_closed_form,
+              check_scale_p2_explicit, check_scale_small_limit,
+              check_scale_bwd_finite_differences)
 
 
 @pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
