@@ -53,7 +53,7 @@ typedef enum {
 
 enum {
     FASTMAX_OK = 0,
-    FASTMAX_EINVAL = -1,       /* p, causal or dt out of range; B, H or N < 1 */
+    FASTMAX_EINVAL = -1,       /* p, causal, dt or qk_scale out of range; B, H or N < 1 */
     FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64}        */
     FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
     FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */
@@ -112,6 +112,28 @@ int fastmax_bwd(const void *q, const void *k, const void *v, const void *out,
                 int B, int H, int N, int D, int p, int causal,
                 fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
                 hipStream_t stream);
+
+/*
+ * Score-scaled variants: the weights become f_p(qk_scale * q^.k^).  The
+ * paper's definition (Sec. 2.2) has no temperature, which is qk_scale = 1
+ * (fastmax_fwd and fastmax_bwd are these calls with 1).  qk_scale = 1/D is
+ * the unit-norm variant (q^ and k^ divided by sqrt(D)), under which
+ * |qk_scale * s| <= 1 as the bound of Sec. 2.3 assumes, so f_1 >= 0 and the
+ * rows of the attention matrix are convex weights (Eq. "valid"); 1/sqrt(D)
+ * is softmax's temperature (Sec. 2.1).  qk_scale must lie in (0, 1], else
+ * FASTMAX_EINVAL.  Arguments, layouts, workspace and errors are otherwise
+ * those of fastmax_fwd and fastmax_bwd (the workspace size does not depend
+ * on qk_scale); the backward must be given the forward's qk_scale.
+ */
+int fastmax_fwd_scaled(const void *q, const void *k, const void *v, void *out,
+                       float *g, int B, int H, int N, int D, int p, int causal,
+                       float qk_scale, fastmax_dtype_t dt, void *workspace,
+                       size_t workspace_bytes, hipStream_t stream);
+int fastmax_bwd_scaled(const void *q, const void *k, const void *v, const void *out,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv,
+                       int B, int H, int N, int D, int p, int causal, float qk_scale,
+                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream);
 
 /* Static description of a return code (never NULL). */
 const char *fastmax_strerror(int code);

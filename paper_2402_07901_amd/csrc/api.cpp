@@ -25,6 +25,12 @@ int check_common(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t 
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+// The score scale multiplies q^.k^ inside f_p.  (0, 1] covers the definition
+// (1) and the unit-norm and temperature variants (1/D, 1/sqrt(D)); the fp16
+// moment scaling of the MFMA backward assumes |qs q^_m qs q^_l| <= 64.  NaN
+// fails both comparisons.
+bool valid_scale(float qs) { return qs > 0.0f && qs <= 1.0f; }
+
 // The segmented MFMA path rounds the moments to fp16; with very few keys G
 // can be far smaller than the moment terms it is summed from (G = f_2(s) >= 1/2
 // for one key against terms of size ~|q^||k^|^2/2), which amplifies that
@@ -64,12 +70,14 @@ size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
     return backward ? bwd_ws(B, H, N, D, p, causal, dt) : fwd_ws(B, H, N, D, p, causal, dt);
 }
 
-int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,
-                int N, int D, int p, int causal, fastmax_dtype_t dt, void *workspace,
-                size_t workspace_bytes, hipStream_t stream)
+int fastmax_fwd_scaled(const void *q, const void *k, const void *v, void *out, float *g, int B,
+                       int H, int N, int D, int p, int causal, float qk_scale,
+                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream)
 {
     int rc = check_common(B, H, N, D, p, causal, dt);
     if (rc != FASTMAX_OK) return rc;
+    if (!valid_scale(qk_scale)) return FASTMAX_EINVAL;
     if (!q || !k || !v || !out) return FASTMAX_ENULL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
         (g && !aligned16(g)))
@@ -79,22 +87,32 @@ int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
     hipError_t e;
     if (mfma_causal(D, p, causal, dt))
-        e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, workspace, stream);
+        e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
     else if (mfma_noncausal(N, D, p, causal, dt))
-        e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, workspace, stream);
+        e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
     else
-        e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, workspace,
-                            stream);
+        e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
+                            workspace, stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 
-int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, const void *dout,
-                const float *g, void *dq, void *dk, void *dv, int B, int H, int N, int D, int p,
-                int causal, fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
-                hipStream_t stream)
+int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,
+                int N, int D, int p, int causal, fastmax_dtype_t dt, void *workspace,
+                size_t workspace_bytes, hipStream_t stream)
+{
+    return fastmax_fwd_scaled(q, k, v, out, g, B, H, N, D, p, causal, 1.0f, dt, workspace,
+                              workspace_bytes, stream);
+}
+
+int fastmax_bwd_scaled(const void *q, const void *k, const void *v, const void *out,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int B,
+                       int H, int N, int D, int p, int causal, float qk_scale,
+                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream)
 {
     int rc = check_common(B, H, N, D, p, causal, dt);
     if (rc != FASTMAX_OK) return rc;
+    if (!valid_scale(qk_scale)) return FASTMAX_EINVAL;
     if (!q || !k || !v || !out || !dout || !g || !dq || !dk || !dv) return FASTMAX_ENULL;
     const void *ptrs[] = {q, k, v, out, dout, g, dq, dk, dv};
     for (const void *ptr : ptrs)
@@ -104,18 +122,28 @@ int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, co
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
     hipError_t e;
     if (mfma_causal(D, p, causal, dt))
-        e = fm::mfma_causal_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, workspace, stream);
+        e = fm::mfma_causal_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, qk_scale, workspace,
+                                stream);
     else
         e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
-                            dt == FASTMAX_BF16, workspace, stream);
+                            dt == FASTMAX_BF16, qk_scale, workspace, stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
+int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, const void *dout,
+                const float *g, void *dq, void *dk, void *dv, int B, int H, int N, int D, int p,
+                int causal, fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                hipStream_t stream)
+{
+    return fastmax_bwd_scaled(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, 1.0f, dt,
+                              workspace, workspace_bytes, stream);
 }
 
 const char *fastmax_strerror(int code)
 {
     switch (code) {
     case FASTMAX_OK: return "success";
-    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, or B/H/N < 1)";
+    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, or qk_scale not in (0, 1])";
     case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32 or 64)";
     case FASTMAX_ENULL: return "required pointer is NULL";
     case FASTMAX_EALIGN: return "pointer not 16-byte aligned";

@@ -57,7 +57,7 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
                                                 const float *__restrict__ g,
                                                 float *__restrict__ rg, float *__restrict__ cc,
                                                 float *__restrict__ pmax, _Float16 *__restrict__ qh,
-                                                _Float16 *__restrict__ kh, int N, int nch)
+                                                _Float16 *__restrict__ kh, int N, int nch, float qs)
 {
     __shared__ float red[3][4];
     const int head = blockIdx.x / nch, c = blockIdx.x % nch, tid = threadIdx.x;
@@ -103,7 +103,7 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
         if (valid) {
             float x[8];
             bf16x8_to_f32(*(const uint4 *)(q + (size_t)n * D + 8 * cg), x);
-            *(h8 *)(qh + (size_t)n * D + 8 * cg) = standardise8(x, true);
+            *(h8 *)(qh + (size_t)n * D + 8 * cg) = standardise8(x, true, qs);
             bf16x8_to_f32(*(const uint4 *)(k + (size_t)n * D + 8 * cg), x);
             *(h8 *)(kh + (size_t)n * D + 8 * cg) = standardise8(x, true);
         }
@@ -677,7 +677,7 @@ __global__ __launch_bounds__(256) void bwd_finish(const bf16_t *__restrict__ q,
                                                   const float *__restrict__ dqh,
                                                   const float *__restrict__ dkh,
                                                   bf16_t *__restrict__ dq, bf16_t *__restrict__ dk,
-                                                  size_t rows)
+                                                  size_t rows, float qs)
 {
     const size_t r = (size_t)blockIdx.x * 32 + (threadIdx.x >> 3);
     const int cg = threadIdx.x & 7;
@@ -691,10 +691,12 @@ __global__ __launch_bounds__(256) void bwd_finish(const bf16_t *__restrict__ q,
             bf16x8_to_f32(*(const uint4 *)(xs + r * D + 8 * cg), xv);
             const f4 a = *(const f4 *)(dh + r * D + 8 * cg);
             const f4 bq = *(const f4 *)(dh + r * D + 8 * cg + 4);
+            // the scans differentiate with respect to the scaled query qs q^
+            const float sc = which ? 1.0f : qs;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                d[i] = a[i];
-                d[4 + i] = bq[i];
+                d[i] = a[i] * sc;
+                d[4 + i] = bq[i] * sc;
             }
         }
         float s = 0.f;
@@ -742,7 +744,7 @@ size_t mfma_causal_bwd_workspace(int BH, int N)
 
 hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
                            const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                           int N, void *ws, hipStream_t st)
+                           int N, float qs, void *ws, hipStream_t st)
 {
     using namespace mfma_bwd;
     static_assert(sizeof(ISmem) <= 160 * 1024 && sizeof(GSmem) <= 160 * 1024 &&
@@ -772,7 +774,7 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
     const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
     hipLaunchKernelGGL(bwd_prep, dim3(BH * nch), dim3(256), 0, st, Q, K, O, DO, V, g, rg, cc, hmax,
-                       qh, kh, N, nch);
+                       qh, kh, N, nch, qs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t smem1 = sizeof(ISmem) > sizeof(mfma_causal::Smem) ? sizeof(ISmem)
@@ -792,7 +794,7 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q, K,
-                       dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows);
+                       dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows, qs);
     return hipGetLastError();
 }
 

@@ -27,11 +27,13 @@ __global__ __launch_bounds__(NTH, 2) void fwd_causal_kernel(const _Float16 *__re
 }
 
 // q^, k^ (Sec. 2.2, Eqs. 6-7) in fp16 for the scan: an octet of lanes per row,
-// 32 rows per workgroup.
+// 32 rows per workgroup.  q^ is multiplied by the score scale qs, so every
+// later step sees the scaled score qs q^.k^.
 __global__ __launch_bounds__(256) void standardise_qk(const bf16_t *__restrict__ q,
                                                       const bf16_t *__restrict__ k,
                                                       _Float16 *__restrict__ qh,
-                                                      _Float16 *__restrict__ kh, size_t rows)
+                                                      _Float16 *__restrict__ kh, size_t rows,
+                                                      float qs)
 {
     const size_t r = (size_t)blockIdx.x * 32 + (threadIdx.x >> 3);
     const int cg = threadIdx.x & 7;
@@ -41,7 +43,7 @@ __global__ __launch_bounds__(256) void standardise_qk(const bf16_t *__restrict__
         bf16x8_to_f32(*(const uint4 *)(q + r * D + 8 * cg), xq);
         bf16x8_to_f32(*(const uint4 *)(k + r * D + 8 * cg), xk);
     }
-    const h8 hq = standardise8(xq, valid), hk = standardise8(xk, valid);
+    const h8 hq = standardise8(xq, valid, qs), hk = standardise8(xk, valid);
     if (valid) {
         *(h8 *)(qh + r * D + 8 * cg) = hq;
         *(h8 *)(kh + r * D + 8 * cg) = hk;
@@ -59,7 +61,7 @@ size_t mfma_causal_fwd_workspace(int BH, int N)
 size_t mfma_causal_smem_bytes() { return sizeof(mfma_causal::Smem); }
 
 hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
-                           int BH, int N, void *ws, hipStream_t st)
+                           int BH, int N, float qs, void *ws, hipStream_t st)
 {
     using namespace mfma_causal;
     static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
@@ -69,7 +71,7 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
     _Float16 *qh = (_Float16 *)ws;
     _Float16 *kh = (_Float16 *)((unsigned char *)ws + mfma_causal_fwd_workspace(BH, N) / 2);
     hipLaunchKernelGGL(standardise_qk, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st,
-                       (const bf16_t *)q, (const bf16_t *)k, qh, kh, rows);
+                       (const bf16_t *)q, (const bf16_t *)k, qh, kh, rows, qs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t smem = sizeof(Smem);

@@ -63,9 +63,11 @@ __device__ __forceinline__ float psi(int f, const float *x, const uint8_t *pm, c
 
 // Loads `rows` token rows starting at token n0 of a head and standardises
 // them (Sec. 2.2, Eqs. 6-7: population std, no epsilon) into dst (stride
-// D + 1, float32).  Rows past N are zero.  Optionally writes 1/std.
+// D + 1, float32), times `scale` (the score scale on the query side, else 1).
+// Rows past N are zero.  Optionally writes 1/std.
 template <int D, typename T>
-__device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_out)
+__device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_out,
+                         float scale = 1.0f)
 {
     constexpr int DP = D + 1;
     for (int e = threadIdx.x; e < CH * D; e += NT) {
@@ -102,7 +104,7 @@ __device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_ou
         if (n0 + r < N) {
             const float rs = rsqrtf(var * (1.0f / D));
 #pragma unroll
-            for (int i = 0; i < E; ++i) x[l + 16 * i] = xv[i] * rs;
+            for (int i = 0; i < E; ++i) x[l + 16 * i] = xv[i] * (rs * scale);
             if (rstd_out && l == 0) rstd_out[r] = rs;
         } else if (rstd_out && l == 0) {
             rstd_out[r] = 0.0f;
@@ -255,7 +257,7 @@ template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                  const T *__restrict__ v, T *__restrict__ out,
                                                  float *__restrict__ g, int N, int cps,
-                                                 const float *__restrict__ sseg)
+                                                 const float *__restrict__ sseg, float qs)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -329,7 +331,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             }
         }
         for (int c = cb; c < ce; ++c) {
-            load_std<D>(q, c * CH, N, xq, nullptr);
+            load_std<D>(q, c * CH, N, xq, nullptr, qs);
             for (int e = threadIdx.x; e < CH * WS; e += NT) F[e] = 0.0f;
             __syncthreads();
             contract_psi<D, P2, WS>(S, xq, F, pm, pl);
@@ -340,7 +342,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
     } else {
         for (int c = cb; c < ce; ++c) {
             const int n0 = c * CH;
-            load_std<D>(q, n0, N, xq, nullptr);
+            load_std<D>(q, n0, N, xq, nullptr, qs);
             load_std<D>(k, n0, N, xk, nullptr);
             load_vals(n0);
             // in-chunk tril block of weights
@@ -431,7 +433,7 @@ template <int D, bool P2, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dqh, float *__restrict__ dkh, float *__restrict__ dva, int N)
+    float *__restrict__ dqh, float *__restrict__ dkh, float *__restrict__ dva, int N, float qs)
 {
     constexpr int DP = D + 1;
     constexpr int D1 = D + 1;
@@ -460,7 +462,7 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
         }
         return;
     }
-    load_std<D>(q, n0, N, xq, nullptr);
+    load_std<D>(q, n0, N, xq, nullptr, qs);
     load_std<D>(k, n0, N, xk, nullptr);
     load_vprime<D, D1>(v, n0, N, 0, vp);
     load_utilde<D, D1>(dout, g, cvec, n0, N, 0, ut);
@@ -502,7 +504,7 @@ template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dqh, int N)
+    float *__restrict__ dqh, int N, float qs)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -528,7 +530,7 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     const int nch = (N + CH - 1) / CH;
 
     auto contract_and_add = [&](int n0) {
-        load_std<D>(q, n0, N, xq, nullptr);
+        load_std<D>(q, n0, N, xq, nullptr, qs);
         load_utilde<D, WS>(dout, g, cvec, n0, N, gc0, ut);
         __syncthreads();
         contract_grad<D, P2, WS>(S, xq, ut, part);
@@ -565,7 +567,7 @@ template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dkh, float *__restrict__ dva, int N)
+    float *__restrict__ dkh, float *__restrict__ dva, int N, float qs)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -610,7 +612,7 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
         __syncthreads();
     };
     auto update = [&](int n0) {
-        load_std<D>(q, n0, N, xq, nullptr);
+        load_std<D>(q, n0, N, xq, nullptr, qs);
         load_utilde<D, WS>(dout, g, cvec, n0, N, gc0, ut);
         __syncthreads();
         state_update<D, P2, WS>(S, xq, ut, pm, pl);
@@ -632,7 +634,7 @@ template <int D, typename T>
 __global__ __launch_bounds__(NT) void bwd_finish_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const float *__restrict__ dqh,
     const float *__restrict__ dkh, const float *__restrict__ dva, T *__restrict__ dq,
-    T *__restrict__ dk, T *__restrict__ dv, size_t rows)
+    T *__restrict__ dk, T *__restrict__ dv, size_t rows, float qs)
 {
     size_t r = (size_t)blockIdx.x * NT + threadIdx.x;
     if (r >= rows) return;
@@ -641,6 +643,8 @@ __global__ __launch_bounds__(NT) void bwd_finish_kernel(
         const T *x = which ? k : q;
         const float *dxh = which ? dkh : dqh;
         T *dx = which ? dk : dq;
+        // the scans differentiate with respect to the scaled query qs q^
+        const float sc = which ? 1.0f : qs;
         float mu = 0.0f;
         for (int d = 0; d < D; ++d) mu += io<T>::ld(x, b + d);
         mu *= 1.0f / D;
@@ -653,14 +657,14 @@ __global__ __launch_bounds__(NT) void bwd_finish_kernel(
         float m1 = 0.0f, m2 = 0.0f;
         for (int d = 0; d < D; ++d) {
             float xh = (io<T>::ld(x, b + d) - mu) * rs;
-            m1 += dxh[b + d];
-            m2 = fmaf(dxh[b + d], xh, m2);
+            m1 += sc * dxh[b + d];
+            m2 = fmaf(sc * dxh[b + d], xh, m2);
         }
         m1 *= 1.0f / D;
         m2 *= 1.0f / D;
         for (int d = 0; d < D; ++d) {
             float xh = (io<T>::ld(x, b + d) - mu) * rs;
-            io<T>::st(dx, b + d, (dxh[b + d] - m1 - xh * m2) * rs);
+            io<T>::st(dx, b + d, (sc * dxh[b + d] - m1 - xh * m2) * rs);
         }
     }
     for (int d = 0; d < D; ++d) io<T>::st(dv, b + d, dva[b + d]);
@@ -702,7 +706,7 @@ SegPlan seg_plan(int BH, int N)
 
 template <int D, bool P2, typename T>
 static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void *out, float *g,
-                               int BH, int N, int causal, void *ws, hipStream_t st)
+                               int BH, int N, int causal, float qs, void *ws, hipStream_t st)
 {
     constexpr int WS = slice_width<D, P2>::v;
     const SegPlan sp = seg_plan<D, P2>(BH, N);
@@ -727,18 +731,18 @@ static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void
     if (causal)
         hipLaunchKernelGGL((fwd_kernel<D, P2, WS, true, T>), grid, dim3(NT), 0, st,
                            (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N, sp.cps,
-                           (const float *)sseg);
+                           (const float *)sseg, qs);
     else
         hipLaunchKernelGGL((fwd_kernel<D, P2, WS, false, T>), grid, dim3(NT), 0, st,
                            (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N, sp.cps,
-                           (const float *)sseg);
+                           (const float *)sseg, qs);
     return hipGetLastError();
 }
 
 template <int D, bool P2, bool CAUSAL, typename T>
 static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, const void *o,
                                 const void *dout, const float *g, void *dq, void *dk, void *dv,
-                                int BH, int N, float *ws, hipStream_t st)
+                                int BH, int N, float qs, float *ws, hipStream_t st)
 {
     constexpr int WS = slice_width<D, P2>::v;
     const size_t rows = (size_t)BH * N;
@@ -751,27 +755,27 @@ static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, con
                        (const T *)dout, g, cvec, rows);
     hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T>), dim3(BH, (N + CH - 1) / CH),
                        dim3(NT), 0, st, (const T *)q, (const T *)k, (const T *)v,
-                       (const T *)dout, g, cvec, dqh, dkh, dva, N);
+                       (const T *)dout, g, cvec, dqh, dkh, dva, N, qs);
     dim3 grid(BH, (D + 1 + WS - 1) / WS);
     hipLaunchKernelGGL((bwd_qscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
                        (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dqh,
-                       N);
+                       N, qs);
     hipLaunchKernelGGL((bwd_kscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
                        (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dkh,
-                       dva, N);
+                       dva, N, qs);
     hipLaunchKernelGGL((bwd_finish_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)q,
-                       (const T *)k, dqh, dkh, dva, (T *)dq, (T *)dk, (T *)dv, rows);
+                       (const T *)k, dqh, dkh, dva, (T *)dq, (T *)dk, (T *)dv, rows, qs);
     return hipGetLastError();
 }
 
 template <int D, bool P2, typename T>
 static hipError_t bwd_dispatch(const void *q, const void *k, const void *v, const void *o,
                                const void *dout, const float *g, void *dq, void *dk, void *dv,
-                               int BH, int N, int causal, float *ws, hipStream_t st)
+                               int BH, int N, int causal, float qs, float *ws, hipStream_t st)
 {
     if (causal)
-        return bwd_dispatch2<D, P2, true, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, ws, st);
-    return bwd_dispatch2<D, P2, false, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, ws, st);
+        return bwd_dispatch2<D, P2, true, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs, ws, st);
+    return bwd_dispatch2<D, P2, false, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs, ws, st);
 }
 
 }  // namespace generic
@@ -789,9 +793,11 @@ size_t generic_bwd_workspace(int B, int H, int N, int D)
 
 template <typename T>
 static hipError_t gen_fwd_t(const void *q, const void *k, const void *v, void *out, float *g,
-                            int BH, int N, int D, int p, int causal, void *ws, hipStream_t st)
+                            int BH, int N, int D, int p, int causal, float qs, void *ws,
+                            hipStream_t st)
 {
-    return FM_DISPATCH_D_P(generic::fwd_dispatch, D, p, q, k, v, out, g, BH, N, causal, ws, st);
+    return FM_DISPATCH_D_P(generic::fwd_dispatch, D, p, q, k, v, out, g, BH, N, causal, qs, ws,
+                           st);
 }
 
 size_t generic_fwd_workspace(int BH, int N, int D, int p)
@@ -805,28 +811,31 @@ size_t generic_fwd_workspace(int BH, int N, int D, int p)
 template <typename T>
 static hipError_t gen_bwd_t(const void *q, const void *k, const void *v, const void *o,
                             const void *dout, const float *g, void *dq, void *dk, void *dv,
-                            int BH, int N, int D, int p, int causal, float *ws, hipStream_t st)
+                            int BH, int N, int D, int p, int causal, float qs, float *ws,
+                            hipStream_t st)
 {
     return FM_DISPATCH_D_P(generic::bwd_dispatch, D, p, q, k, v, o, dout, g, dq, dk, dv, BH, N,
-                           causal, ws, st);
+                           causal, qs, ws, st);
 }
 
 hipError_t generic_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st)
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st)
 {
-    if (is_bf16) return gen_fwd_t<bf16_t>(q, k, v, out, g, BH, N, D, p, causal, ws, st);
-    return gen_fwd_t<float>(q, k, v, out, g, BH, N, D, p, causal, ws, st);
+    if (is_bf16) return gen_fwd_t<bf16_t>(q, k, v, out, g, BH, N, D, p, causal, qs, ws, st);
+    return gen_fwd_t<float>(q, k, v, out, g, BH, N, D, p, causal, qs, ws, st);
 }
 
 hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *o,
                        const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st)
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st)
 {
     if (is_bf16)
-        return gen_bwd_t<bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, p, causal,
+        return gen_bwd_t<bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, p, causal, qs,
                                  (float *)ws, st);
-    return gen_bwd_t<float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, p, causal, (float *)ws,
-                            st);
+    return gen_bwd_t<float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, p, causal, qs,
+                            (float *)ws, st);
 }
 
 }  // namespace fm

@@ -7,20 +7,24 @@
 namespace fm {
 
 // Generic float32-VALU path: every (D, p, causal, dtype).
+// qs: score scale (weights f_p(qs q^.k^)), applied to q^ where it is
+// standardised and to dq^ before the standardisation backward.
 hipError_t generic_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st);
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st);
 // Forward workspace of the generic path: per-segment moment states when a
 // head's sequence is split into segments (few heads), else 0.
 size_t generic_fwd_workspace(int BH, int N, int D, int p);
 hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *o,
                        const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                       int N, int D, int p, int causal, int is_bf16, void *ws, hipStream_t st);
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st);
 size_t generic_bwd_workspace(int B, int H, int N, int D);
 
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
 // ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16.
 hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
-                           int BH, int N, void *ws, hipStream_t st);
+                           int BH, int N, float qs, void *ws, hipStream_t st);
 size_t mfma_causal_fwd_workspace(int BH, int N);
 size_t mfma_causal_smem_bytes();
 
@@ -28,13 +32,13 @@ size_t mfma_causal_smem_bytes();
 // mfma_causal_bwd_workspace(BH, N) bytes.
 hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
                            const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                           int N, void *ws, hipStream_t st);
+                           int N, float qs, void *ws, hipStream_t st);
 size_t mfma_causal_bwd_workspace(int BH, int N);
 
 // MFMA non-causal path: D = 64, p = 2, bf16 I/O (moment build, segment
 // reduction, query contraction).  ws holds mfma_nc_workspace(BH, N) bytes.
 hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, void *ws, hipStream_t st);
+                       int N, float qs, void *ws, hipStream_t st);
 size_t mfma_nc_workspace(int BH, int N);
 
 }  // namespace fm

@@ -169,7 +169,9 @@ __device__ __forceinline__ float octet_sum(float x)
 // Standardises the 8 channels this lane holds of one token (the token's 64
 // channels are spread over the 8 lanes of an aligned octet) and returns them
 // as fp16.  Population variance, no epsilon; invalid rows become zero.
-__device__ __forceinline__ h8 standardise8(const float *xin, bool valid)
+// `scale` multiplies the standardised row (the score scale of the query side;
+// 1 leaves it unchanged).
+__device__ __forceinline__ h8 standardise8(const float *xin, bool valid, float scale = 1.0f)
 {
     float x[8];
     float s = 0.f;
@@ -182,7 +184,7 @@ __device__ __forceinline__ h8 standardise8(const float *xin, bool valid)
         x[i] = xin[i] - mu;
         v = fmaf(x[i], x[i], v);
     }
-    const float r = valid ? __builtin_amdgcn_rsqf(octet_sum(v) * (1.0f / D)) : 0.0f;
+    const float r = valid ? __builtin_amdgcn_rsqf(octet_sum(v) * (1.0f / D)) * scale : 0.0f;
     h8 o;
 #pragma unroll
     for (int i = 0; i < 8; i += 2) {

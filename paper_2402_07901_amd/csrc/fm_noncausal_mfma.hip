@@ -408,7 +408,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
                                                    const float *__restrict__ hdrg,
                                                    bf16_t *__restrict__ out,
                                                    float *__restrict__ g, int N, int BH, int tb,
-                                                   int ntb)
+                                                   int ntb, float qs)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     QSmem &sm = *reinterpret_cast<QSmem *>(smem_raw);
@@ -461,7 +461,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
         float x[8];
         bf16x8_to_f32(pq, x);
         const int row = tid >> 3, cg = tid & 7;
-        const h8 hq = standardise8(x, tok0 + s * QS + row < tok1);
+        const h8 hq = standardise8(x, tok0 + s * QS + row < tok1, qs);
         *(h8 *)(sm.qrow[buf] + sw64(row, 8 * cg)) = hq;
 #pragma unroll
         for (int i = 0; i < 8; ++i) sm.qperm[buf][sw64(row, 8 * i + cg)] = hq[i];
@@ -562,7 +562,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
 size_t mfma_nc_workspace(int BH, int N) { return mfma_nc::make_plan(BH, N).total; }
 
 hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, void *ws, hipStream_t st)
+                       int N, float qs, void *ws, hipStream_t st)
 {
     using namespace mfma_nc;
     static_assert(sizeof(QSmem) <= 160 * 1024, "LDS budget");
@@ -594,7 +594,7 @@ hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, f
                             (int)smem);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(nc_query, dim3((unsigned)gq), dim3(NTH), smem, st, (const bf16_t *)q, aq,
-                       y3h, hdr, (bf16_t *)out, g, N, BH, P.tb, P.ntb);
+                       y3h, hdr, (bf16_t *)out, g, N, BH, P.tb, P.ntb, qs);
     return hipGetLastError();
 }
 

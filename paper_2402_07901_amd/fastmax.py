@@ -49,6 +49,12 @@ def lib():
         L.fastmax_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i,
                                   vp, sz, vp]
         L.fastmax_bwd.restype = i
+        f = ctypes.c_float
+        L.fastmax_fwd_scaled.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp, sz, vp]
+        L.fastmax_fwd_scaled.restype = i
+        L.fastmax_bwd_scaled.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, f,
+                                         i, vp, sz, vp]
+        L.fastmax_bwd_scaled.restype = i
         L.fastmax_strerror.argtypes = [i]
         L.fastmax_strerror.restype = ctypes.c_char_p
         L.fastmax_version.restype = ctypes.c_char_p
@@ -90,17 +96,28 @@ def _dtype_code(t):
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_bytes, stream):
-    """Direct call of fastmax_fwd with raw pointers/ints; returns the code."""
-    return lib().fastmax_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(g), B, H, N, D, p,
-                             int(causal), dt, _ptr(workspace), ws_bytes, _stream(stream))
+def fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_bytes, stream,
+                    scale=None):
+    """Direct call of fastmax_fwd (fastmax_fwd_scaled when ``scale`` is given)
+    with raw pointers/ints; returns the code."""
+    if scale is None:
+        return lib().fastmax_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(g), B, H, N, D, p,
+                                 int(causal), dt, _ptr(workspace), ws_bytes, _stream(stream))
+    return lib().fastmax_fwd_scaled(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(g), B, H, N, D,
+                                    p, int(causal), float(scale), dt, _ptr(workspace), ws_bytes,
+                                    _stream(stream))
 
 
 def fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt, workspace,
-                    ws_bytes, stream):
-    return lib().fastmax_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(g), _ptr(dq),
-                             _ptr(dk), _ptr(dv), B, H, N, D, p, int(causal), dt, _ptr(workspace),
-                             ws_bytes, _stream(stream))
+                    ws_bytes, stream, scale=None):
+    if scale is None:
+        return lib().fastmax_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(g),
+                                 _ptr(dq), _ptr(dk), _ptr(dv), B, H, N, D, p, int(causal), dt,
+                                 _ptr(workspace), ws_bytes, _stream(stream))
+    return lib().fastmax_bwd_scaled(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(g),
+                                    _ptr(dq), _ptr(dk), _ptr(dv), B, H, N, D, p, int(causal),
+                                    float(scale), dt, _ptr(workspace), ws_bytes,
+                                    _stream(stream))
 
 
 def _alloc_ws(nbytes, device):
@@ -111,8 +128,9 @@ def _alloc_ws(nbytes, device):
 
 
 def fastmax_fwd(q, k, v, p=2, causal=False, out=None, g=None, want_g=True, workspace=None,
-                stream=None):
-    """O = Fastmax(q, k, v) for [B, H, N, D] device tensors; returns (O, G)."""
+                stream=None, scale=None):
+    """O = Fastmax(q, k, v) for [B, H, N, D] device tensors; returns (O, G).
+    ``scale``: score scale (weights f_p(scale * q^.k^)); None = the definition."""
     import torch
     B, H, N, D = q.shape
     dt = _dtype_code(q)
@@ -124,15 +142,16 @@ def fastmax_fwd(q, k, v, p=2, causal=False, out=None, g=None, want_g=True, works
     if workspace is None:
         workspace = _alloc_ws(need, q.device)
     ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    rc = fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_n, stream)
+    rc = fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_n, stream,
+                         scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_fwd")
     return out, g
 
 
 def fastmax_bwd(q, k, v, out, dout, g, p=2, causal=False, dq=None, dk=None, dv=None,
-                workspace=None, stream=None):
-    """Gradients (dq, dk, dv) of sum(dout * O)."""
+                workspace=None, stream=None, scale=None):
+    """Gradients (dq, dk, dv) of sum(dout * O); ``scale`` as in the forward."""
     import torch
     B, H, N, D = q.shape
     dt = _dtype_code(q)
@@ -144,7 +163,7 @@ def fastmax_bwd(q, k, v, out, dout, g, p=2, causal=False, dq=None, dk=None, dv=N
         workspace = _alloc_ws(need, q.device)
     ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
     rc = fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt, workspace,
-                         ws_n, stream)
+                         ws_n, stream, scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_bwd")
     return dq, dk, dv

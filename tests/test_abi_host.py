@@ -154,3 +154,35 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(fm, "_lib", None)
     with pytest.raises(RuntimeError, match="not found"):
         fm.lib()
+
+
+def fwd_scaled(scale, q=A, B=1, H=1, N=8, D=64, p=2, causal=1, dt=fm.BF16):
+    return fm.lib().fastmax_fwd_scaled(ctypes.c_void_p(q) if q else None, ctypes.c_void_p(A),
+                                       ctypes.c_void_p(A), ctypes.c_void_p(A), None, B, H, N, D,
+                                       p, causal, ctypes.c_float(scale), dt, None, 0, None)
+
+
+def bwd_scaled(scale, first=A, B=1, H=1, N=8, D=64, p=2, causal=1, dt=fm.BF16):
+    cp = [ctypes.c_void_p(first) if first else None] + [ctypes.c_void_p(A)] * 8
+    return fm.lib().fastmax_bwd_scaled(*cp, B, H, N, D, p, causal, ctypes.c_float(scale), dt,
+                                       None, 0, None)
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.5, 1.5, float("nan"), float("inf"), -float("inf")])
+def test_scaled_entry_points_reject_bad_scale(scale):
+    # every other argument is valid: the scale check alone must stop the call
+    # (fake pointers, nothing may launch)
+    assert fwd_scaled(scale) == fm.EINVAL
+    assert bwd_scaled(scale) == fm.EINVAL
+
+
+def test_scaled_entry_points_validate_the_rest():
+    for s in (1.0, 1.0 / 64, 0.125):
+        assert fwd_scaled(s, q=0) == fm.ENULL
+        assert bwd_scaled(s, first=0) == fm.ENULL
+        assert fwd_scaled(s, D=48) == fm.EUNSUPPORTED
+        assert bwd_scaled(s, p=3) == fm.EINVAL
+        assert fwd_scaled(s, q=A + 4) == fm.EALIGN
+    # causal bf16 D = 64 p = 2 needs a workspace (none given)
+    assert fwd_scaled(0.5) == fm.EWORKSPACE
+    assert bwd_scaled(0.5) == fm.EWORKSPACE
