@@ -78,7 +78,7 @@ def load_traffic(kernel, workload):
     return ent.get("bytes_per_launch")
 
 
-def cpu_baseline(w, inp_bits):
+def cpu_baseline(w, inp_bits, scale=1.0):
     """The fp64 oracle (factorised form) on a bounded sample of the workload."""
     import numpy as np
 
@@ -101,7 +101,7 @@ def cpu_baseline(w, inp_bits):
         q, k, v = inp["q64"], inp["k64"], inp["v64"]
         sample = f"{heads} heads at N={N} drawn with the workload's recipe"
     t0 = time.perf_counter()
-    oracle.fwd_fact(q, k, v, w.p, w.causal)
+    oracle.fwd_fact(q, k, v, w.p, w.causal, scale=scale)
     dt = time.perf_counter() - t0
     rec = {"value": heads * N / dt, "unit": "tokens*heads/s", "cores": threads,
            "kind": "oracle", "sample": sample + f" (fwd_fact, {dt:.1f} s)",
@@ -109,7 +109,7 @@ def cpu_baseline(w, inp_bits):
     if N <= 4096:
         # the explicit N x N definition as well, on the same sample
         t0 = time.perf_counter()
-        oracle.fwd_brute(q, k, v, w.p, w.causal)
+        oracle.fwd_brute(q, k, v, w.p, w.causal, scale=scale)
         rec["brute_force_value"] = heads * N / (time.perf_counter() - t0)
     return rec
 
@@ -135,6 +135,9 @@ def main():
                     help="fwd: one forward per step (the headline); fwdbwd: forward + "
                          "backward per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--qk-scale", type=float, default=None, metavar="TAU",
+                    help="time the score-scaled entry points with weights f_p(TAU q^.k^) "
+                         "(e.g. 1/D, the unit-norm variant); default: the plain entry points")
     ap.add_argument("--cold", type=int, default=None, metavar="ITERS",
                     help="after the timed region, time ITERS calls each preceded by a "
                          "512 MiB write that flushes the caches (default 10 for the bf16 "
@@ -196,14 +199,14 @@ def main():
 
     def step(i=None):
         rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
-                                need, stream)
+                                need, stream, args.qk_scale)
         if rc != fm.OK:
             raise fm.FastmaxError(rc, "fastmax_fwd")
         if args.mode == "fwdbwd":
             if i is not None:
                 bwd_start[i].record(stream)
             rc = fm.fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, w.B, w.H, w.N, w.D, w.p,
-                                    w.causal, dt, ws_b, need_b, stream)
+                                    w.causal, dt, ws_b, need_b, stream, args.qk_scale)
             if rc != fm.OK:
                 raise fm.FastmaxError(rc, "fastmax_bwd")
 
@@ -262,7 +265,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "mode": args.mode, "B": w.B, "H": w.H, "N": w.N,
                    "D": w.D, "p": w.p, "causal": w.causal, "io_dtype": w.dtype,
-                   "global_batch": w.B, "seq_len": w.N, "parallelism": "none (1 GPU)"},
+                   "global_batch": w.B, "seq_len": w.N, "parallelism": "none (1 GPU)",
+                   "qk_scale": 1.0 if args.qk_scale is None else args.qk_scale},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": load_traffic(kernel, w.name),
                      "kernel": kernel, "avg_launch_ms": avg_launch_s * 1e3,
@@ -301,13 +305,13 @@ def main():
 
         def fwd_call():
             rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
-                                    need, stream)
+                                    need, stream, args.qk_scale)
             if rc != fm.OK:
                 raise fm.FastmaxError(rc, "fastmax_fwd")
 
         def bwd_call():
             rc = fm.fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, w.B, w.H, w.N, w.D, w.p,
-                                    w.causal, dt, ws_b, need_b, stream)
+                                    w.causal, dt, ws_b, need_b, stream, args.qk_scale)
             if rc != fm.OK:
                 raise fm.FastmaxError(rc, "fastmax_bwd")
 
@@ -331,7 +335,7 @@ def main():
             if j >= 0:
                 ev[2 * j].record(stream)
             rc = fm.fastmax_fwd_raw(qs, ks, vs, outs, None, w.B, w.H, n_s, w.D, w.p, w.causal,
-                                    dt, ws_s, need_s, stream)
+                                    dt, ws_s, need_s, stream, args.qk_scale)
             if rc != fm.OK:
                 raise fm.FastmaxError(rc, "fastmax_fwd")
             if j >= 0:
@@ -344,7 +348,7 @@ def main():
                               "full_median_ms": t_f, "ratio": t_f / t_s,
                               "ideal": w.N / n_s}
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, inp)
+        rec["cpu_baseline"] = cpu_baseline(w, inp, 1.0 if args.qk_scale is None else args.qk_scale)
     print(json.dumps(rec), flush=True)
 
 
