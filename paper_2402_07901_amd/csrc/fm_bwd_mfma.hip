@@ -135,6 +135,8 @@ __device__ __forceinline__ HeadMax head_max(const float *pmax, int head, int nch
 {
     HeadMax r{0.f, 0.f, 0.f};
     const float *p = pmax + (size_t)head * nch * 4;
+    // unrolled so that several scalar loads are in flight per wait
+#pragma unroll 8
     for (int c = 0; c < nch; ++c) {
         r.u = fmaxf(r.u, p[4 * c]);
         r.v = fmaxf(r.v, p[4 * c + 1]);

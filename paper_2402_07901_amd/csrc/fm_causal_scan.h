@@ -167,17 +167,32 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
     if (g) g += (size_t)head * N;
     if (rg) rg += (size_t)head * N;
 
-    // max |v| over this slice -> power-of-two scale
+    // max |v| over this slice -> power-of-two scale (eight loads in flight
+    // per thread, not one round trip per row pair)
     {
         const int tid = threadIdx.x;
         float vmax = 0.f;
-        for (int p = tid; p < 2 * N; p += NTH) {
-            const int n = p >> 1, hh = p & 1;
-            float x[8];
-            bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh), x);
-            const float r = DV ? fabsf(rg[n]) : 1.0f;
+        constexpr int U = 8;
+        for (int p0 = tid; p0 < 2 * N; p0 += U * NTH) {
+            uint4 raw[U];
+            float rr[U];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * r);
+            for (int u = 0; u < U; ++u) {
+                const int p = p0 + u * NTH, n = p >> 1, hh = p & 1;
+                raw[u] = uint4{0u, 0u, 0u, 0u};
+                rr[u] = 0.0f;
+                if (p < 2 * N) {
+                    raw[u] = *(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh);
+                    rr[u] = DV ? fabsf(rg[n]) : 1.0f;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                float x[8];
+                bf16x8_to_f32(raw[u], x);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * rr[u]);
+            }
         }
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));

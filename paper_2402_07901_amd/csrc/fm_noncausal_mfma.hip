@@ -136,12 +136,23 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ 
     // 8 * max|v| * 2^-e <= 2^15 (|k^_m| <= 8)
     int tid = threadIdx.x;
     float vmax = 0.f;
-    for (int p = 4 * t0 + tid; p < 4 * t1; p += NTH) {
-        const int n = p >> 2, qq = p & 3;
-        float x[8];
-        bf16x8_to_f32(*(const uint4 *)(v + (size_t)n * D + MSW * sl + 8 * qq), x);
+    // eight loads in flight per thread, not one round trip per row quarter
+    constexpr int U = 8;
+    for (int p0 = 4 * t0 + tid; p0 < 4 * t1; p0 += U * NTH) {
+        uint4 raw[U];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]));
+        for (int u = 0; u < U; ++u) {
+            const int p = p0 + u * NTH, n = p >> 2, qq = p & 3;
+            raw[u] = uint4{0u, 0u, 0u, 0u};
+            if (p < 4 * t1) raw[u] = *(const uint4 *)(v + (size_t)n * D + MSW * sl + 8 * qq);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            float x[8];
+            bf16x8_to_f32(raw[u], x);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]));
+        }
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
