@@ -135,6 +135,9 @@ def main():
                     help="fwd: one forward per step (the headline); fwdbwd: forward + "
                          "backward per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--timed-only", action="store_true",
+                    help="no cold calls and no N = 8192 comparison run (for profiling: "
+                         "every dispatch of the kernels is then a timed-region call)")
     ap.add_argument("--qk-scale", type=float, default=None, metavar="TAU",
                     help="time the score-scaled entry points with weights f_p(TAU q^.k^) "
                          "(e.g. 1/D, the unit-norm variant); default: the plain entry points")
@@ -290,6 +293,8 @@ def main():
 
     # cold calls: caches flushed by a 512 MiB write before each one
     cold = args.cold if args.cold is not None else (10 if w.dtype == "bf16" and w.p == 2 else 0)
+    if args.timed_only:
+        cold = 0
     if cold > 0:
         flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * cold)]
@@ -322,7 +327,8 @@ def main():
         del flush
 
     # linear in N (long non-causal workload): the same recipe at N = 8192
-    if not w.causal and w.N > 8192 and w.dtype == "bf16" and w.p == 2 and args.mode == "fwd":
+    if (not w.causal and w.N > 8192 and w.dtype == "bf16" and w.p == 2 and args.mode == "fwd"
+            and not args.timed_only):
         n_s = 8192
         inp_s = workload_inputs(w, want64=False, N=n_s)
         qs, ks, vs = (to_dev(inp_s[n]) for n in ("q", "k", "v"))
