@@ -245,10 +245,18 @@ __global__ __launch_bounds__(NT) void seg_prefix_kernel(float *__restrict__ sseg
     if (e >= PWS) return;
     float *base = sseg + (size_t)blockIdx.y * nseg * PWS + e;
     float run = 0.0f;
-    for (int s2 = 0; s2 < nseg; ++s2) {
-        const float x = base[(size_t)s2 * PWS];
-        if (CAUSAL) base[(size_t)s2 * PWS] = run;
-        run += x;
+    // eight segments loaded before any is overwritten: the loads are in
+    // flight together instead of one round trip each
+    constexpr int U = 8;
+    for (int s0 = 0; s0 < nseg; s0 += U) {
+        float x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = s0 + u < nseg ? base[(size_t)(s0 + u) * PWS] : 0.0f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (CAUSAL && s0 + u < nseg) base[(size_t)(s0 + u) * PWS] = run;
+            run += x[u];
+        }
     }
     if (!CAUSAL) base[0] = run;
 }

@@ -353,6 +353,9 @@ __global__ __launch_bounds__(512) void nc_reduce(const float *__restrict__ part,
     auto tile_exp = [&](int ct) {
         const int sl = ct / MCT;
         float bound = 0.f;
+        // unrolled: several loads in flight per wait (a loop of dependent
+        // waits would cost one memory round trip per segment)
+#pragma unroll 8
         for (int s = 0; s < nseg; ++s)
             bound += (float)seg_tokens(s, N, cps) * vmx[((size_t)head * NMS + sl) * nseg + s];
         return pow2_exponent(63.0f * bound);
@@ -379,17 +382,20 @@ __global__ __launch_bounds__(512) void nc_reduce(const float *__restrict__ part,
         const float gs = ldexpf(1.0f, -gexp);
         for (int e = tid; e < D * D; e += 512) {
             float s = 0.f;
+#pragma unroll 8
             for (int sg = 0; sg < nseg; ++sg) s += y3p[((size_t)head * nseg + sg) * D * D + e];
             y3h[(size_t)head * D * D + e] = (_Float16)(s * gs);
         }
         float *hd = hdr + (size_t)head * HDR;
         if (tid < D) {
             float s = 0.f;
+#pragma unroll 8
             for (int sg = 0; sg < nseg; ++sg) s += y2p[((size_t)head * nseg + sg) * D + tid];
             hd[tid] = s * ldexpf(2.0f, -gexp);
         } else if (tid < 2 * D) {
             const int j = tid - D;
             float s = 0.f;
+#pragma unroll 8
             for (int sg = 0; sg < nseg; ++sg) s += x1p[((size_t)head * nseg + sg) * D + j];
             hd[D + j] = s * ldexpf(1.0f, -tile_exp(j / 16));
         } else if (tid < 2 * D + NCT) {
