@@ -240,11 +240,12 @@ def main():
     value = tokens_heads / (ms_per_step / 1e3)
     flops = fwd_flops(w.B, w.H, w.N, w.D, w.p)
     kernel = "fastmax_fwd"
-    if w.p == 2 and w.dtype == "bf16":
+    if w.p == 2 and w.dtype == "bf16" and w.D == 64:
         bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "bf16")]
         achieved = flops / avg_launch_s / 1e12
     elif w.p == 2:
-        # the float32 path computes on the vector ALU in fp32
+        # the float32 path (every case but D = 64, p = 2, bf16) computes on
+        # the vector ALU in fp32
         bound, unit, peak = "alu", "TFLOP/s", PEAK[("alu", "f32")]
         achieved = flops / avg_launch_s / 1e12
     else:
@@ -280,7 +281,7 @@ def main():
         bf = bwd_flops(w.B, w.H, w.N, w.D, w.p)
         rec["backward"] = {"avg_ms": bms,
                            "note": "fastmax_bwd call (all its kernels), HIP events on the stream"}
-        if bf is not None and w.dtype == "bf16":
+        if bf is not None and w.dtype == "bf16" and w.D == 64:
             ach = bf / (bms / 1e3) / 1e12
             rec["backward"].update({"algorithmic_flops_per_call": bf, "achieved": ach,
                                     "unit": "TFLOP/s", "bound": "mfma",

@@ -30,7 +30,9 @@
  *    that point.  Inputs must stay valid until then.
  *  - Validation happens on the host before the first HIP call: on any error
  *    nothing is enqueued and nothing is written.
- *  - Supported: D in {16, 32, 64}; p in {1, 2}; causal in {0, 1};
+ *  - Supported: D in {16, 32, 64, 128} (the MFMA kernels serve D = 64, p = 2,
+ *    bf16; every other case, D = 128 included, runs on float32 VALU kernels);
+ *    p in {1, 2}; causal in {0, 1};
  *    dt in {FASTMAX_F32, FASTMAX_BF16}; B, H, N >= 1 and B*H*N*D < 2^62.
  *  - A token whose q or k row is constant has std 0; its standardised row is
  *    undefined (as in the paper) and its outputs are not finite.
@@ -54,7 +56,7 @@ typedef enum {
 enum {
     FASTMAX_OK = 0,
     FASTMAX_EINVAL = -1,       /* p, causal, dt or qk_scale out of range; B, H or N < 1 */
-    FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64}        */
+    FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64, 128}   */
     FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
     FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */
     FASTMAX_EWORKSPACE = -5,   /* workspace NULL or smaller than required     */

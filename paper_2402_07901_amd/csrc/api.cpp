@@ -7,7 +7,9 @@
 
 namespace {
 
-bool supported_d(int D) { return D == 16 || D == 32 || D == 64; }
+// D = 128 (the head size of Sec. 3.1's Llama-2 remark) runs on the generic
+// float32 kernels; the MFMA kernels cover D = 64.
+bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
 
 int check_common(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
 {
@@ -144,7 +146,7 @@ const char *fastmax_strerror(int code)
     switch (code) {
     case FASTMAX_OK: return "success";
     case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, or qk_scale not in (0, 1])";
-    case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32 or 64)";
+    case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32, 64 or 128)";
     case FASTMAX_ENULL: return "required pointer is NULL";
     case FASTMAX_EALIGN: return "pointer not 16-byte aligned";
     case FASTMAX_EWORKSPACE: return "workspace missing or too small";

@@ -679,7 +679,8 @@ __global__ __launch_bounds__(NT) void bwd_finish_kernel(
 }
 
 // Column-slice width (including the ones column) that keeps the LDS state
-// of a workgroup under 64 KiB.
+// of a workgroup under 64 KiB (D = 128, p = 2, whose state is 33 KB per
+// column, uses most of the 160 KB of LDS instead).
 template <int D, bool P2> struct slice_width;
 template <> struct slice_width<16, true> { static constexpr int v = 17; };
 template <> struct slice_width<32, true> { static constexpr int v = 17; };
@@ -687,6 +688,10 @@ template <> struct slice_width<64, true> { static constexpr int v = 5; };
 template <> struct slice_width<16, false> { static constexpr int v = 17; };
 template <> struct slice_width<32, false> { static constexpr int v = 33; };
 template <> struct slice_width<64, false> { static constexpr int v = 65; };
+// D = 128, p = 2: two value columns and the ones column per forward slice
+// (8385 features x 3 columns = 101 KB of LDS state; 142 KB per workgroup in all)
+template <> struct slice_width<128, true> { static constexpr int v = 3; };
+template <> struct slice_width<128, false> { static constexpr int v = 65; };
 
 // Segments per head: enough workgroups for ~256 CUs, at most one per chunk.
 struct SegPlan {
@@ -698,6 +703,7 @@ SegPlan seg_plan(int BH, int N)
 {
     constexpr int WS = slice_width<D, P2>::v;
     constexpr int W = WS - 1;
+    static_assert(W >= 1, "a forward slice holds at least one value column besides the ones column");
     SegPlan sp;
     sp.slices = (D + W - 1) / W;
     const int nch = (N + CH - 1) / CH;
@@ -797,7 +803,8 @@ size_t generic_bwd_workspace(int B, int H, int N, int D)
 #define FM_DISPATCH_D_P(FN, D, p, ...)                                   \
     ((D) == 16 ? ((p) == 2 ? FN<16, true, T>(__VA_ARGS__) : FN<16, false, T>(__VA_ARGS__)) : \
      (D) == 32 ? ((p) == 2 ? FN<32, true, T>(__VA_ARGS__) : FN<32, false, T>(__VA_ARGS__)) : \
-                 ((p) == 2 ? FN<64, true, T>(__VA_ARGS__) : FN<64, false, T>(__VA_ARGS__)))
+     (D) == 64 ? ((p) == 2 ? FN<64, true, T>(__VA_ARGS__) : FN<64, false, T>(__VA_ARGS__)) : \
+                 ((p) == 2 ? FN<128, true, T>(__VA_ARGS__) : FN<128, false, T>(__VA_ARGS__)))
 
 template <typename T>
 static hipError_t gen_fwd_t(const void *q, const void *k, const void *v, void *out, float *g,
@@ -813,7 +820,8 @@ size_t generic_fwd_workspace(int BH, int N, int D, int p)
     using namespace generic;
     if (D == 16) return p == 2 ? seg_plan<16, true>(BH, N).bytes : seg_plan<16, false>(BH, N).bytes;
     if (D == 32) return p == 2 ? seg_plan<32, true>(BH, N).bytes : seg_plan<32, false>(BH, N).bytes;
-    return p == 2 ? seg_plan<64, true>(BH, N).bytes : seg_plan<64, false>(BH, N).bytes;
+    if (D == 64) return p == 2 ? seg_plan<64, true>(BH, N).bytes : seg_plan<64, false>(BH, N).bytes;
+    return p == 2 ? seg_plan<128, true>(BH, N).bytes : seg_plan<128, false>(BH, N).bytes;
 }
 
 template <typename T>
