@@ -26,10 +26,11 @@
 //
 // State numerics.  The state lives in fp16 (v is pre-scaled by a power of two
 // 2^-e per workgroup so that no entry, bounded by N * 63 * max|v|, can exceed
-// 2^15).  Each update rebuilds a tile's fp32 accumulator exactly with one MFMA
-// against a 0/1 permutation matrix, adds the chunk's contribution in fp32 and
-// rounds back to fp16 once per chunk.  Diagonal tiles are stored halved (the
-// 1/2 of f_2), and rebuilt with a 0/2 matrix.
+// 2^15).  A tile's accumulator layout holds exactly the elements of its half of
+// the paired operand, so each update accumulates the chunk's contribution in
+// fp32 from zero, rounds it to fp16 and adds it to the state with packed fp16
+// arithmetic (two roundings per chunk).  Diagonal tiles are stored halved (the
+// 1/2 of f_2) and take half the contribution.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -110,18 +111,6 @@ struct Smem {
     alignas(16) float x1[2][SL];    // sum of scaled v before the chunk
     float red[NW];
 };
-
-// rows a (slots 0..3) or b (slots 4..7) of a paired fp16 operand -> the
-// accumulator layout of that tile, times `one` (exact)
-__device__ __forceinline__ h8 perm_operand(int r16, int h, bool hi, _Float16 one)
-{
-    h8 p = {0, 0, 0, 0, 0, 0, 0, 0};
-    const bool on = h == (r16 >> 2);
-    const int slot = (r16 & 3) + (hi ? 4 : 0);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) p[j] = (on && slot == j) ? one : (_Float16)0.0f;
-    return p;
-}
 
 template <int HALF>
 __device__ __forceinline__ h8 set_half(h8 x, h4 r)
@@ -300,17 +289,14 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             h8 Vf[NKS2];
 #pragma unroll
             for (int s = 0; s < NKS2; ++s) Vf[s] = ld8(vTc + sw128(r16, 32 * s + 8 * h));
-            const h8 pa = perm_operand(r16, h, false, (_Float16)1.0f);
-            const h8 pb = perm_operand(r16, h, true, (_Float16)1.0f);
-            const h8 pa2 = perm_operand(r16, h, false, (_Float16)2.0f);
-            const h8 pb2 = perm_operand(r16, h, true, (_Float16)2.0f);
             {
                 // linear tile: x2[l][j] += sum_t k_tl v_tj, l in tile w
-                f4 acc = mfma(pa, Ast[0], f4{0.f, 0.f, 0.f, 0.f});
+                f4 acc = mfma(ld8(kTc + sw128(16 * w + r16, 8 * h)), Vf[0], f4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                for (int s = 0; s < NKS2; ++s)
+                for (int s = 1; s < NKS2; ++s)
                     acc = mfma(ld8(kTc + sw128(16 * w + r16, 32 * s + 8 * h)), Vf[s], acc);
-                Ast[0] = set_half<0>(Ast[0], cvt4(acc));
+                const h8 cur = Ast[0];
+                Ast[0] = set_half<0>(Ast[0], cvt4(acc) + h4{cur[0], cur[1], cur[2], cur[3]});
             }
             static_for<0, NQ>([&](auto ii) {
                 constexpr int i = decltype(ii)::value;
@@ -321,16 +307,16 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 h8 Wm[NKS2];
 #pragma unroll
                 for (int s = 0; s < NKS2; ++s) Wm[s] = ld8(kTc + sw128(m, 32 * s + 8 * h)) * Vf[s];
-                // rebuild the fp32 tiles (diagonal tile: stored halved, 0/2 matrix)
+                // the chunk's contribution from zero, rounded to fp16 and added
+                // to the fp16 state with packed fp16 arithmetic (the diagonal
+                // tile, stored halved, takes half the contribution)
                 f4 acc[nu];
                 static_for<0, nu>([&](auto ui) {
                     constexpr int uu = decltype(ui)::value;
-                    constexpr int t = t0 + uu;
-                    const h8 P = (t & 1) ? (uu == 0 ? pb2 : pb) : (uu == 0 ? pa2 : pa);
-                    acc[uu] = mfma(P, Ast[t / 2], f4{0.f, 0.f, 0.f, 0.f});
+                    acc[uu] = mfma(Ak[u0 + uu][0], Wm[0], f4{0.f, 0.f, 0.f, 0.f});
                 });
 #pragma unroll
-                for (int s = 0; s < NKS2; ++s)
+                for (int s = 1; s < NKS2; ++s)
                     static_for<0, nu>([&](auto ui) {
                         constexpr int uu = decltype(ui)::value;
                         acc[uu] = mfma(Ak[u0 + uu][s], Wm[s], acc[uu]);
@@ -338,8 +324,13 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 static_for<0, nu>([&](auto ui) {
                     constexpr int uu = decltype(ui)::value;
                     constexpr int t = t0 + uu;
-                    h4 r = cvt4(acc[uu]);
-                    if constexpr (uu == 0) r = scale4(r, (_Float16)0.5f);
+                    const h4 a16 = cvt4(acc[uu]);
+                    const h8 cur = Ast[t / 2];
+                    const h4 old = (t & 1) ? h4{cur[4], cur[5], cur[6], cur[7]}
+                                           : h4{cur[0], cur[1], cur[2], cur[3]};
+                    h4 r;
+                    if constexpr (uu == 0) r = a16 * (_Float16)0.5f + old;
+                    else r = a16 + old;
                     Ast[t / 2] = set_half<t & 1>(Ast[t / 2], r);
                 });
             });
