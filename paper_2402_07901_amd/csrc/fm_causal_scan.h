@@ -324,14 +324,11 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 static_for<0, nu>([&](auto ui) {
                     constexpr int uu = decltype(ui)::value;
                     constexpr int t = t0 + uu;
-                    const h4 a16 = cvt4(acc[uu]);
-                    const h8 cur = Ast[t / 2];
-                    const h4 old = (t & 1) ? h4{cur[4], cur[5], cur[6], cur[7]}
-                                           : h4{cur[0], cur[1], cur[2], cur[3]};
-                    h4 r;
-                    if constexpr (uu == 0) r = a16 * (_Float16)0.5f + old;
-                    else r = a16 + old;
-                    Ast[t / 2] = set_half<t & 1>(Ast[t / 2], r);
+                    h4 a16 = cvt4(acc[uu]);
+                    if constexpr (uu == 0) a16 = a16 * (_Float16)0.5f;
+                    // in place on the whole pair (the other half adds zero)
+                    const h4 z4 = {0, 0, 0, 0};
+                    Ast[t / 2] = Ast[t / 2] + ((t & 1) ? cat(z4, a16) : cat(a16, z4));
                 });
             });
             __syncthreads();
