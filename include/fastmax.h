@@ -77,7 +77,9 @@ enum {
  * the standardised q and k in fp16 (256 bytes per row).  The backward always
  * needs one: per token 1/G, c = dO.O/G, the fp32
  * gradient accumulators of q^ and k^ and (causal bf16, D = 64, p = 2) the
- * standardised q^, k^ in fp16, plus per-chunk maxima.
+ * standardised q^, k^ in fp16, plus per-chunk maxima; on the float32 path
+ * with few heads (B*H times the column slices under about 256) also the
+ * per-segment moment states of its two scans.
  */
 size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
                                fastmax_dtype_t dt, int backward);

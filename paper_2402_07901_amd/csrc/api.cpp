@@ -58,7 +58,7 @@ size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
 size_t bwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_bwd_workspace(B * H, N);
-    return fm::generic_bwd_workspace(B, H, N, D);
+    return fm::generic_bwd_workspace(B, H, N, D, p);
 }
 
 }  // namespace

@@ -236,9 +236,10 @@ __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
 }
 
 // In place over the segments of each (head, slice): causal -> the exclusive
-// prefix sum (segment s gets the sum of segments < s), non-causal -> the total
-// in segment 0.  One thread per state element.
-template <int PWS, bool CAUSAL>
+// prefix sum (segment s gets the sum of segments < s; with REVERSE the
+// exclusive suffix, the sum of segments > s), non-causal -> the total in
+// segment 0.  One thread per state element.
+template <int PWS, bool CAUSAL, bool REVERSE = false>
 __global__ __launch_bounds__(NT) void seg_prefix_kernel(float *__restrict__ sseg, int nseg)
 {
     const int e = blockIdx.x * NT + threadIdx.x;
@@ -251,10 +252,14 @@ __global__ __launch_bounds__(NT) void seg_prefix_kernel(float *__restrict__ sseg
     for (int s0 = 0; s0 < nseg; s0 += U) {
         float x[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) x[u] = s0 + u < nseg ? base[(size_t)(s0 + u) * PWS] : 0.0f;
+        for (int u = 0; u < U; ++u) {
+            const int sg = REVERSE ? nseg - 1 - (s0 + u) : s0 + u;
+            x[u] = s0 + u < nseg ? base[(size_t)sg * PWS] : 0.0f;
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (CAUSAL && s0 + u < nseg) base[(size_t)(s0 + u) * PWS] = run;
+            const int sg = REVERSE ? nseg - 1 - (s0 + u) : s0 + u;
+            if (CAUSAL && s0 + u < nseg) base[(size_t)sg * PWS] = run;
             run += x[u];
         }
     }
@@ -512,7 +517,7 @@ template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dqh, int N, float qs)
+    float *__restrict__ dqh, int N, float qs, const float *__restrict__ sseg, int cps)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -532,10 +537,19 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     g += (size_t)head * N;
     cvec += (size_t)head * N;
 
-    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    // initial state: the moments of the earlier segments (causal) or of all
+    // of them, as seg_prefix_kernel left them (zero with one segment)
+    const int nseg = gridDim.z, seg = blockIdx.z;
+    {
+        const float *src = sseg ? sseg + (((size_t)head * gridDim.y + blockIdx.y) * nseg +
+                                          (CAUSAL ? seg : 0)) * P * WS
+                                : nullptr;
+        for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = src ? src[e] : 0.0f;
+    }
     build_pairs<D, P2>(pm, pl);
     __syncthreads();
     const int nch = (N + CH - 1) / CH;
+    const int cb = seg * cps, ce = min(nch, cb + cps);
 
     auto contract_and_add = [&](int n0) {
         load_std<D>(q, n0, N, xq, nullptr, qs);
@@ -557,10 +571,11 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
         __syncthreads();
     };
     if (!CAUSAL) {
-        for (int c = 0; c < nch; ++c) update(c * CH);
-        for (int c = 0; c < nch; ++c) contract_and_add(c * CH);
+        if (!sseg)
+            for (int c = 0; c < nch; ++c) update(c * CH);
+        for (int c = cb; c < ce; ++c) contract_and_add(c * CH);
     } else {
-        for (int c = 0; c < nch; ++c) {
+        for (int c = cb; c < ce; ++c) {
             contract_and_add(c * CH);
             update(c * CH);
         }
@@ -575,7 +590,8 @@ template <int D, bool P2, int WS, bool CAUSAL, typename T>
 __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dkh, float *__restrict__ dva, int N, float qs)
+    float *__restrict__ dkh, float *__restrict__ dva, int N, float qs,
+    const float *__restrict__ sseg, int cps)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -596,10 +612,19 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     g += (size_t)head * N;
     cvec += (size_t)head * N;
 
-    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    // initial state: the moments of the later segments (causal: exclusive
+    // suffix) or of all of them (zero with one segment)
+    const int nseg = gridDim.z, seg = blockIdx.z;
+    {
+        const float *src = sseg ? sseg + (((size_t)head * gridDim.y + blockIdx.y) * nseg +
+                                          (CAUSAL ? seg : 0)) * P * WS
+                                : nullptr;
+        for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = src ? src[e] : 0.0f;
+    }
     build_pairs<D, P2>(pm, pl);
     __syncthreads();
     const int nch = (N + CH - 1) / CH;
+    const int cb = seg * cps, ce = min(nch, cb + cps);
 
     auto contract_and_add = [&](int n0) {
         load_std<D>(k, n0, N, xk, nullptr);
@@ -627,14 +652,60 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
         __syncthreads();
     };
     if (!CAUSAL) {
-        for (int c = 0; c < nch; ++c) update(c * CH);
-        for (int c = 0; c < nch; ++c) contract_and_add(c * CH);
+        if (!sseg)
+            for (int c = 0; c < nch; ++c) update(c * CH);
+        for (int c = cb; c < ce; ++c) contract_and_add(c * CH);
     } else {
-        for (int c = nch - 1; c >= 0; --c) {
+        for (int c = ce - 1; c >= cb; --c) {
             contract_and_add(c * CH);
             update(c * CH);
         }
     }
+}
+
+// Moment sums of one segment of chunks for the backward scans (all segments
+// in parallel): SIDE 0 -> sum phi(k^_n) v'_n (the q-scan's state), SIDE 1 ->
+// sum phi(qs q^_i) u~_i (the k-scan's state), columns gc0.. of the D + 1.
+template <int D, bool P2, int WS, int SIDE, typename T>
+__global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+    const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
+    float *__restrict__ sseg, int N, float qs, int cps)
+{
+    constexpr int P = feat<D, P2>::P;
+    constexpr int NPAIR = feat<D, P2>::NPAIR;
+    constexpr int DP = D + 1;
+    __shared__ float S[P * WS];
+    __shared__ float xs[CH * DP];
+    __shared__ float vals[CH * WS];
+    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+
+    const int head = blockIdx.x, gc0 = blockIdx.y * WS;
+    const int nseg = gridDim.z, seg = blockIdx.z;
+    const size_t hb = (size_t)head * N * D;
+    q += hb; k += hb; v += hb; dout += hb;
+    g += (size_t)head * N;
+    cvec += (size_t)head * N;
+    for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
+    build_pairs<D, P2>(pm, pl);
+    __syncthreads();
+    const int nch = (N + CH - 1) / CH;
+    const int cb = seg * cps, ce = min(nch, cb + cps);
+    for (int c = cb; c < ce; ++c) {
+        if (SIDE == 0) {
+            load_std<D>(k, c * CH, N, xs, nullptr);
+            load_vprime<D, WS>(v, c * CH, N, gc0, vals);
+        } else {
+            load_std<D>(q, c * CH, N, xs, nullptr, qs);
+            load_utilde<D, WS>(dout, g, cvec, c * CH, N, gc0, vals);
+        }
+        __syncthreads();
+        state_update<D, P2, WS>(S, xs, vals, pm, pl);
+        __syncthreads();
+    }
+    float *dst = sseg + (((size_t)head * gridDim.y + blockIdx.y) * nseg + seg) * P * WS;
+    for (int e = threadIdx.x; e < P * WS; e += NT) dst[e] = S[e];
 }
 
 // Back through Eqs. (6)-(7) and cast: dx = (dx^ - mean dx^ - x^ mean(dx^ x^)) / std.
@@ -753,30 +824,75 @@ static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void
     return hipGetLastError();
 }
 
+// Backward scans: column slices of the D + 1 columns, and segments of chunks
+// (states summed in parallel, then prefix- or suffix-summed) when there are too
+// few (head, slice) pairs to fill the CUs.
+struct BwdPlan {
+    int slices, nseg, cps;
+    size_t seg_bytes;
+};
+template <int D, bool P2>
+BwdPlan bwd_plan(int BH, int N)
+{
+    constexpr int WS = slice_width<D, P2>::v;
+    BwdPlan bp;
+    bp.slices = (D + 1 + WS - 1) / WS;
+    const int nch = (N + CH - 1) / CH;
+    long long want = 256 / ((long long)BH * bp.slices);
+    if (want < 1) want = 1;
+    if (want > nch) want = nch;
+    if (want > 65535) want = 65535;
+    bp.cps = (int)((nch + want - 1) / want);
+    bp.nseg = (nch + bp.cps - 1) / bp.cps;
+    bp.seg_bytes = bp.nseg > 1 ? (size_t)BH * bp.slices * bp.nseg * feat<D, P2>::P * WS *
+                                     sizeof(float)
+                               : 0;
+    return bp;
+}
+
 template <int D, bool P2, bool CAUSAL, typename T>
 static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, const void *o,
                                 const void *dout, const float *g, void *dq, void *dk, void *dv,
                                 int BH, int N, float qs, float *ws, hipStream_t st)
 {
     constexpr int WS = slice_width<D, P2>::v;
+    constexpr int PWS = feat<D, P2>::P * WS;
     const size_t rows = (size_t)BH * N;
     float *cvec = ws;
     float *dqh = cvec + rows;
     float *dkh = dqh + rows * D;
     float *dva = dkh + rows * D;
+    const BwdPlan bp = bwd_plan<D, P2>(BH, N);
+    float *sseg = bp.nseg > 1 ? dva + rows * D : nullptr;
     const int rb = (int)((rows + NT - 1) / NT);
     hipLaunchKernelGGL((bwd_rowdot_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)o,
                        (const T *)dout, g, cvec, rows);
     hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T>), dim3(BH, (N + CH - 1) / CH),
                        dim3(NT), 0, st, (const T *)q, (const T *)k, (const T *)v,
                        (const T *)dout, g, cvec, dqh, dkh, dva, N, qs);
-    dim3 grid(BH, (D + 1 + WS - 1) / WS);
+    const dim3 grid(BH, bp.slices, bp.nseg);
+    const dim3 pgrid((PWS + NT - 1) / NT, BH * bp.slices);
+    if (sseg) {
+        hipLaunchKernelGGL((bwd_seg_state_kernel<D, P2, WS, 0, T>), grid, dim3(NT), 0, st,
+                           (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec,
+                           sseg, N, qs, bp.cps);
+        hipLaunchKernelGGL((seg_prefix_kernel<PWS, CAUSAL, false>), pgrid, dim3(NT), 0, st, sseg,
+                           bp.nseg);
+    }
     hipLaunchKernelGGL((bwd_qscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
                        (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dqh,
-                       N, qs);
+                       N, qs, (const float *)sseg, bp.cps);
+    if (sseg) {
+        // the same buffer, reused in stream order for the k-scan's states
+        hipLaunchKernelGGL((bwd_seg_state_kernel<D, P2, WS, 1, T>), grid, dim3(NT), 0, st,
+                           (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec,
+                           sseg, N, qs, bp.cps);
+        hipLaunchKernelGGL((seg_prefix_kernel<PWS, CAUSAL, true>), pgrid, dim3(NT), 0, st, sseg,
+                           bp.nseg);
+    }
     hipLaunchKernelGGL((bwd_kscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
                        (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dkh,
-                       dva, N, qs);
+                       dva, N, qs, (const float *)sseg, bp.cps);
     hipLaunchKernelGGL((bwd_finish_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)q,
                        (const T *)k, dqh, dkh, dva, (T *)dq, (T *)dk, (T *)dv, rows, qs);
     return hipGetLastError();
@@ -794,10 +910,17 @@ static hipError_t bwd_dispatch(const void *q, const void *k, const void *v, cons
 
 }  // namespace generic
 
-size_t generic_bwd_workspace(int B, int H, int N, int D)
+size_t generic_bwd_workspace(int B, int H, int N, int D, int p)
 {
-    size_t rows = (size_t)B * H * N;
-    return sizeof(float) * (rows + 3 * rows * (size_t)D);
+    using namespace generic;
+    const size_t rows = (size_t)B * H * N;
+    const int BH = B * H;
+    size_t seg = 0;
+    if (D == 16) seg = p == 2 ? bwd_plan<16, true>(BH, N).seg_bytes : bwd_plan<16, false>(BH, N).seg_bytes;
+    else if (D == 32) seg = p == 2 ? bwd_plan<32, true>(BH, N).seg_bytes : bwd_plan<32, false>(BH, N).seg_bytes;
+    else if (D == 64) seg = p == 2 ? bwd_plan<64, true>(BH, N).seg_bytes : bwd_plan<64, false>(BH, N).seg_bytes;
+    else seg = p == 2 ? bwd_plan<128, true>(BH, N).seg_bytes : bwd_plan<128, false>(BH, N).seg_bytes;
+    return sizeof(float) * (rows + 3 * rows * (size_t)D) + seg;
 }
 
 #define FM_DISPATCH_D_P(FN, D, p, ...)                                   \

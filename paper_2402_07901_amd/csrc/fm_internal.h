@@ -19,7 +19,7 @@ hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *
                        const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
                        int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
                        hipStream_t st);
-size_t generic_bwd_workspace(int B, int H, int N, int D);
+size_t generic_bwd_workspace(int B, int H, int N, int D, int p);
 
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
 // ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16.

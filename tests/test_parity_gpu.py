@@ -203,3 +203,16 @@ def test_causal_prefix_is_subproblem(dtype):
         a = to_f64(o_full)[:, :, :n]
         b = to_f64(o_sub)
         assert max_rel(a, b) <= TOL[dtype] / 10
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("p", [1, 2])
+@pytest.mark.parametrize("D", [16, 32, 64])
+def test_bwd_generic_segments(D, p, causal):
+    """One head over 700 tokens on the float32 kernels: the backward's two
+    scans are split into segments of chunks whose moment states are summed in
+    parallel, then prefix- (dq) or suffix-summed (dk)."""
+    label = f"bwd segments D={D} p={p} causal={causal} f32"
+    say(label)
+    inp = make_inputs(1, 1, 700, D, 900 + D + p, "f32", with_dout=True)
+    bwd_case(inp, p, causal, "f32", label=label)
