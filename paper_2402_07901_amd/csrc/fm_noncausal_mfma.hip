@@ -411,7 +411,7 @@ __global__ __launch_bounds__(512) void nc_reduce(const float *__restrict__ part,
 
 struct QSmem {
     float fpart[2][NW * NCT * 4 * QS * 4];   // [buf][wave][tile][row quad][token][4]
-    float gpart[2][16 * QS];                 // [buf][channel tile][row quad][token]
+    float gpart[2][4 * QS];                  // [buf][channel tile][token]
     _Float16 qrow[2][QS * RS64];             // q^ [token][m], double-buffered by step parity
     _Float16 qperm[2][QS * RS64];            // q^ [token][8 (m % 8) + m / 8]: a wave's channels
                                              // m = w + 8 idx are one 16-byte load
@@ -495,7 +495,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
             F += *(const f4 *)(sm.fpart[buf] + (((ww * NCT + ct) * 4 + hq) * QS + tk) * 4);
         float gq = 0.f;
 #pragma unroll
-        for (int k = 0; k < 16; ++k) gq += sm.gpart[buf][k * QS + tk];
+        for (int k = 0; k < 4; ++k) gq += sm.gpart[buf][k * QS + tk];
         const float G = fmaf(sm.hdr[2 * D + NCT], gq, Nf);
         if (n < tok1) {
             const float sc = sm.hdr[2 * D + ct] * __builtin_amdgcn_rcpf(G);
@@ -564,7 +564,11 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
                 float gq = 0.f;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) gq = fmaf((float)ql[i], T[i], gq);
-                sm.gpart[buf][(4 * cc + h) * QS + tk] = gq;
+                // summed over the four lane groups here, so the combine reads
+                // one value per channel tile instead of four
+                gq += __shfl_xor(gq, 16);
+                gq += __shfl_xor(gq, 32);
+                if (h == 0) sm.gpart[buf][cc * QS + tk] = gq;
             }
         }
         if (s > 0) combine(s - 1);
