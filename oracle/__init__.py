@@ -49,6 +49,15 @@ def _bind(path):
                                  ctypes.POINTER(ctypes.c_int64), dp, dp, dp]
     lib.fmo_bwd_brute.argtypes = [dp, dp, dp, dp, dp, L, L, L, L, I, I, F,
                                   dp, dp, dp]
+    up = ctypes.POINTER(ctypes.c_uint32)
+    lib.fmo_mask_words.argtypes = [L]
+    lib.fmo_mask_words.restype = L
+    lib.fmo_philox4x32_10.argtypes = [up, up, up]
+    lib.fmo_dropout_mask.argtypes = [L, L, L, L, F, ctypes.c_uint64, up]
+    lib.fmo_fwd_drop_brute.argtypes = [dp, dp, dp, up, L, L, L, L, I, F, F, dp, dp]
+    lib.fmo_fwd_drop_fact.argtypes = [dp, dp, dp, up, L, L, L, L, I, F, F, dp, dp]
+    lib.fmo_bwd_drop_brute.argtypes = [dp, dp, dp, dp, dp, up, L, L, L, L, I, F, F,
+                                       dp, dp, dp]
     return lib
 
 
@@ -169,4 +178,82 @@ def bwd_brute(q, k, v, dout, p, causal, o_used=None, scale=1.0):
     _load().fmo_bwd_brute(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(o_used),
                           B, H, N, D, int(p), int(causal), float(scale), _ptr(dq),
                           _ptr(dk), _ptr(dv))
+    return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# "Quadratic" dropout (Sec. 2.4, dropout paragraph; Fig. 2): keep bits on each
+# key token's D(D+1)/2 quadratic features, kept ones scaled by 1/(1 - rate).
+# ``bits`` is uint32 [B, H, N, mask_words(D)]; feature t(m, l) = m D -
+# m(m-1)/2 + l - m (m <= l) is bit t % 32 of word t // 32.
+# ---------------------------------------------------------------------------
+def _uptr(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+
+
+def mask_words(D):
+    """uint32 words per token of a keep-bit row: ceil(D(D+1)/2 / 32)."""
+    return int(_load().fmo_mask_words(int(D)))
+
+
+def philox4x32_10(ctr, key):
+    """Philox4x32-10 (Salmon et al., SC 2011): 4 counter words, 2 key words
+    -> 4 output words."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    o = np.empty(4, dtype=np.uint32)
+    _load().fmo_philox4x32_10(_uptr(c), _uptr(k), _uptr(o))
+    return o
+
+
+def dropout_mask(B, H, N, D, rate, seed):
+    """Keep bits drawn with Philox4x32-10: key = (seed & 0xffffffff, seed >> 32),
+    counter = (n, t // 4, b H + h, 0), word t % 4; dropped iff the word is below
+    floor(rate 2^32)."""
+    bits = np.empty((B, H, N, mask_words(D)), dtype=np.uint32)
+    _load().fmo_dropout_mask(B, H, N, D, float(rate), ctypes.c_uint64(int(seed)), _uptr(bits))
+    return bits
+
+
+def _bits(bits, B, H, N, D):
+    b = np.ascontiguousarray(bits, dtype=np.uint32)
+    if b.shape != (B, H, N, mask_words(D)):
+        raise ValueError(f"keep bits shaped {b.shape}, expected {(B, H, N, mask_words(D))}")
+    return b
+
+
+def fwd_drop_brute(q, k, v, bits, rate, causal, scale=1.0):
+    """Brute force forward (p = 2) with the masked weights; returns (O, G)."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, D = _shape4(q)
+    b = _bits(bits, B, H, N, D)
+    out = np.empty_like(q)
+    g = np.empty((B, H, N))
+    _load().fmo_fwd_drop_brute(_ptr(q), _ptr(k), _ptr(v), _uptr(b), B, H, N, D, int(causal),
+                               float(scale), float(rate), _ptr(out), _ptr(g))
+    return out, g
+
+
+def fwd_drop_fact(q, k, v, bits, rate, causal, scale=1.0):
+    """Factorised forward (p = 2) with the masked quadratic embedding; (O, G)."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, D = _shape4(q)
+    b = _bits(bits, B, H, N, D)
+    out = np.empty_like(q)
+    g = np.empty((B, H, N))
+    _load().fmo_fwd_drop_fact(_ptr(q), _ptr(k), _ptr(v), _uptr(b), B, H, N, D, int(causal),
+                              float(scale), float(rate), _ptr(out), _ptr(g))
+    return out, g
+
+
+def bwd_drop_brute(q, k, v, dout, bits, rate, causal, scale=1.0, o_used=None):
+    """Gradients (dq, dk, dv) of the masked forward, the mask held fixed."""
+    q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
+    B, H, N, D = _shape4(q)
+    b = _bits(bits, B, H, N, D)
+    ou = None if o_used is None else _f64(o_used)
+    dq, dk, dv = np.empty_like(q), np.empty_like(q), np.empty_like(q)
+    _load().fmo_bwd_drop_brute(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(ou), _uptr(b),
+                               B, H, N, D, int(causal), float(scale), float(rate),
+                               _ptr(dq), _ptr(dk), _ptr(dv))
     return dq, dk, dv

@@ -443,3 +443,301 @@ void fmo_bwd_brute(const double *q, const double *k, const double *v,
         free(dkh);
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* "Quadratic" dropout on the factorised terms (Sec. 2.4, the dropout        */
+/* paragraph, and Fig. 2).  For p = 2 every key token n carries a keep bit   */
+/* b_nt for each of its quadratic features, the D(D+1)/2 distinct products  */
+/* k^_nm k^_nl (m <= l), numbered m-major: t(m, l) = m D - m(m-1)/2 + l - m. */
+/* A kept feature is scaled by 1/(1 - rate), a dropped one is zero; the      */
+/* masked feature enters both x^(3) and y^(3) (it is one embedding), so the  */
+/* weight of the pair (i, n) is                                              */
+/*   w_in = 1 + tau s_in + sum_{m<=l} c_ml tau^2 q^_im q^_il k^_nm k^_nl b~, */
+/* c_mm = 1/2, c_ml = 1 (m < l), b~ = b_nt / (1 - rate).  With every bit set */
+/* and rate 0 this is f_2(tau s_in).                                         */
+/* Bits: for head hd and token n a row of NW = ceil(D(D+1)/2 / 32) uint32    */
+/* words at bits + (hd N + n) NW; feature t is bit t % 32 of word t / 32.    */
+/* ------------------------------------------------------------------------ */
+static long pair_index(long D, long m, long l)
+{
+    return m * D - m * (m - 1) / 2 + (l - m);
+}
+
+long fmo_mask_words(long D) { return (D * (D + 1) / 2 + 31) / 32; }
+
+/* Philox4x32-10, the counter-based generator of Salmon, Moraes, Dror and
+ * Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3" (SC 2011): ten rounds
+ * of two 32x32->64 multiplications on a 4-word counter, the 2-word key
+ * advanced by the Weyl constants between rounds. */
+void fmo_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out)
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        uint32_t n1 = (uint32_t)p1;
+        uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        uint32_t n3 = (uint32_t)p0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Keep bits drawn with Philox4x32-10: key = (seed low word, seed high word),
+ * counter = (n, t / 4, hd, 0), feature t uses output word t % 4 and is dropped
+ * iff that word is below floor(rate 2^32). */
+void fmo_dropout_mask(long B, long H, long N, long D, double rate, uint64_t seed,
+                      uint32_t *bits)
+{
+    long heads = B * H, npair = D * (D + 1) / 2, nw = fmo_mask_words(D);
+    double t32 = floor(rate * 4294967296.0);
+    uint32_t thr = t32 >= 4294967295.0 ? 0xFFFFFFFFu : (uint32_t)t32;
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+#pragma omp parallel for schedule(static)
+    for (long r = 0; r < heads * N; ++r) {
+        long hd = r / N, n = r % N;
+        uint32_t *row = bits + r * nw;
+        for (long w = 0; w < nw; ++w) row[w] = 0u;
+        for (long t = 0; t < npair; ++t) {
+            uint32_t ctr[4] = {(uint32_t)n, (uint32_t)(t / 4), (uint32_t)hd, 0u}, o[4];
+            fmo_philox4x32_10(ctr, key, o);
+            if (o[t % 4] >= thr) row[t / 32] |= 1u << (t % 32);
+        }
+    }
+}
+
+static double keep_mult(const uint32_t *row, long t, double inv_keep)
+{
+    return (row[t / 32] >> (t % 32)) & 1u ? inv_keep : 0.0;
+}
+
+/* w_in of the definition above for standardised rows qh_i (already times
+ * tau) and kh_n with the keep row of token n. */
+static double drop_weight(const double *qt, const double *kn, const uint32_t *row,
+                          long D, double inv_keep)
+{
+    double s = 0.0, quad = 0.0;
+    for (long m = 0; m < D; ++m) {
+        s += qt[m] * kn[m];
+        for (long l = m; l < D; ++l) {
+            double c = (l == m) ? 0.5 : 1.0;
+            quad += c * qt[m] * qt[l] * kn[m] * kn[l] *
+                    keep_mult(row, pair_index(D, m, l), inv_keep);
+        }
+    }
+    return 1.0 + s + quad;
+}
+
+/* Brute force with the masked weights: O_i = sum_n w_in v_n / sum_n w_in. */
+void fmo_fwd_drop_brute(const double *q, const double *k, const double *v,
+                        const uint32_t *bits, long B, long H, long N, long D,
+                        int causal, double tau, double rate, double *out,
+                        double *g)
+{
+    long heads = B * H, nw = fmo_mask_words(D);
+    double inv_keep = 1.0 / (1.0 - rate);
+    for (long hd = 0; hd < heads; ++hd) {
+        double *qh = malloc(sizeof(double) * N * D);
+        double *kh = malloc(sizeof(double) * N * D);
+        standardize_all(q + hd * N * D, N, D, qh, NULL, NULL);
+        standardize_all(k + hd * N * D, N, D, kh, NULL, NULL);
+        for (long r = 0; r < N * D; ++r) qh[r] *= tau;
+        const double *vb = v + hd * N * D;
+#pragma omp parallel for schedule(dynamic, 4)
+        for (long i = 0; i < N; ++i) {
+            double *o = out + (hd * N + i) * D;
+            for (long j = 0; j < D; ++j) o[j] = 0.0;
+            double G = 0.0;
+            long nend = causal ? i + 1 : N;
+            for (long n = 0; n < nend; ++n) {
+                double w = drop_weight(qh + i * D, kh + n * D,
+                                       bits + (hd * N + n) * nw, D, inv_keep);
+                G += w;
+                for (long j = 0; j < D; ++j) o[j] += w * vb[n * D + j];
+            }
+            for (long j = 0; j < D; ++j) o[j] /= G;
+            if (g) g[hd * N + i] = G;
+        }
+        free(qh);
+        free(kh);
+    }
+}
+
+/* The same by the factorised moments of Sec. 2.4 with the masked quadratic
+ * embedding: X1 = sum v'_n, X2[m] = sum k^_nm v'_n, X3[t(m,l)] = sum b~_nt
+ * k^_nm k^_nl v'_n over n (all n, or n <= i as a running prefix), v' = [v|1];
+ * F_i, G_i = X1 + sum_m tau q^_im X2[m] + sum_{m<=l} c_ml tau^2 q^_im q^_il X3[t]. */
+void fmo_fwd_drop_fact(const double *q, const double *k, const double *v,
+                       const uint32_t *bits, long B, long H, long N, long D,
+                       int causal, double tau, double rate, double *out,
+                       double *g)
+{
+    long heads = B * H, nw = fmo_mask_words(D), npair = D * (D + 1) / 2;
+    long D1 = D + 1;
+    double inv_keep = 1.0 / (1.0 - rate);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (long hd = 0; hd < heads; ++hd) {
+        double *qh = malloc(sizeof(double) * N * D);
+        double *kh = malloc(sizeof(double) * N * D);
+        double *X1 = calloc(D1, sizeof(double));
+        double *X2 = calloc(D * D1, sizeof(double));
+        double *X3 = calloc(npair * D1, sizeof(double));
+        double *vp = malloc(sizeof(double) * D1);
+        for (long r = 0; r < N; ++r) {
+            standardize_row(q + (hd * N + r) * D, D, qh + r * D, NULL, NULL);
+            standardize_row(k + (hd * N + r) * D, D, kh + r * D, NULL, NULL);
+        }
+        const double *vb = v + hd * N * D;
+        /* adds token n to the moments */
+        #define DROP_ADD(n)                                                       \
+            do {                                                                  \
+                const double *kn = kh + (n) * D;                                  \
+                const uint32_t *row = bits + (hd * N + (n)) * nw;                 \
+                for (long j = 0; j < D; ++j) vp[j] = vb[(n) * D + j];             \
+                vp[D] = 1.0;                                                      \
+                for (long j = 0; j < D1; ++j) X1[j] += vp[j];                     \
+                for (long m = 0; m < D; ++m)                                      \
+                    for (long j = 0; j < D1; ++j) X2[m * D1 + j] += kn[m] * vp[j]; \
+                for (long m = 0; m < D; ++m)                                      \
+                    for (long l = m; l < D; ++l) {                                \
+                        long t = pair_index(D, m, l);                             \
+                        double e = kn[m] * kn[l] * keep_mult(row, t, inv_keep);   \
+                        for (long j = 0; j < D1; ++j) X3[t * D1 + j] += e * vp[j]; \
+                    }                                                             \
+            } while (0)
+        if (!causal)
+            for (long n = 0; n < N; ++n) DROP_ADD(n);
+        for (long i = 0; i < N; ++i) {
+            if (causal) DROP_ADD(i);
+            const double *qi = qh + i * D;
+            double *o = out + (hd * N + i) * D;
+            double F[D1];
+            for (long j = 0; j < D1; ++j) {
+                double acc = X1[j];
+                for (long m = 0; m < D; ++m) acc += tau * qi[m] * X2[m * D1 + j];
+                for (long m = 0; m < D; ++m)
+                    for (long l = m; l < D; ++l) {
+                        double c = (l == m) ? 0.5 : 1.0;
+                        acc += c * tau * tau * qi[m] * qi[l] *
+                               X3[pair_index(D, m, l) * D1 + j];
+                    }
+                F[j] = acc;
+            }
+            for (long j = 0; j < D; ++j) o[j] = F[j] / F[D];
+            if (g) g[hd * N + i] = F[D];
+        }
+        #undef DROP_ADD
+        free(qh); free(kh); free(X1); free(X2); free(X3); free(vp);
+    }
+}
+
+/* Gradients of the masked forward (the mask is a constant).  With
+ * q~ = tau q^, z_l = q~_l k^_nl and h_a = 1 + sum_l z_l b~_{n,t(a,l)}:
+ *   dw_in/dq~_ia = k^_na h_a,  dw_in/dk^_na = q~_ia h_a,
+ * and, as in the unmasked case, dO_i/dw_in = (v_n - O_i) / G_i, so
+ *   dq~_i = sum_n (dO_i.(v_n - O_i)/G_i) k^_n (.) h,  dq^ = tau dq~,
+ *   dk^_n = sum_i (dO_i.(v_n - O_i)/G_i) q~_i (.) h,  dv_n = sum_i w_in dO_i/G_i,
+ * then back through Eqs. (6)-(7).  o_used as in fmo_bwd_brute. */
+void fmo_bwd_drop_brute(const double *q, const double *k, const double *v,
+                        const double *dout, const double *o_used,
+                        const uint32_t *bits, long B, long H, long N, long D,
+                        int causal, double tau, double rate, double *dq,
+                        double *dk, double *dv)
+{
+    long heads = B * H, nw = fmo_mask_words(D);
+    double inv_keep = 1.0 / (1.0 - rate);
+    for (long hd = 0; hd < heads; ++hd) {
+        const double *vb = v + hd * N * D, *dob = dout + hd * N * D;
+        double *qh = malloc(sizeof(double) * N * D);
+        double *kh = malloc(sizeof(double) * N * D);
+        double *qs = malloc(sizeof(double) * N), *ks = malloc(sizeof(double) * N);
+        double *o = malloc(sizeof(double) * N * D);
+        double *G = malloc(sizeof(double) * N);
+        double *dqt = calloc(N * D, sizeof(double));
+        double *dkh = calloc(N * D, sizeof(double));
+        double *dvh = calloc(N * D, sizeof(double));
+        standardize_all(q + hd * N * D, N, D, qh, NULL, qs);
+        standardize_all(k + hd * N * D, N, D, kh, NULL, ks);
+        double *qt = malloc(sizeof(double) * N * D);
+        for (long r = 0; r < N * D; ++r) qt[r] = tau * qh[r];
+        const uint32_t *hb = bits + hd * N * nw;
+        /* forward at the same mask */
+        for (long i = 0; i < N; ++i) {
+            double Gi = 0.0;
+            for (long j = 0; j < D; ++j) o[i * D + j] = 0.0;
+            long nend = causal ? i + 1 : N;
+            for (long n = 0; n < nend; ++n) {
+                double w = drop_weight(qt + i * D, kh + n * D, hb + n * nw, D, inv_keep);
+                Gi += w;
+                for (long j = 0; j < D; ++j) o[i * D + j] += w * vb[n * D + j];
+            }
+            for (long j = 0; j < D; ++j) o[i * D + j] /= Gi;
+            G[i] = Gi;
+        }
+        if (o_used) memcpy(o, o_used + hd * N * D, sizeof(double) * N * D);
+        /* dq~: row i over the keys it sees; dk^, dv: key n over the rows
+         * that see it (each loop parallel over the index it owns) */
+#pragma omp parallel for schedule(dynamic, 4)
+        for (long i = 0; i < N; ++i) {
+            double h[D];
+            long nend = causal ? i + 1 : N;
+            for (long n = 0; n < nend; ++n) {
+                const uint32_t *row = hb + n * nw;
+                const double *qi = qt + i * D, *kn = kh + n * D;
+                double dw = 0.0;
+                for (long j = 0; j < D; ++j) dw += dob[i * D + j] * (vb[n * D + j] - o[i * D + j]);
+                dw /= G[i];
+                for (long a = 0; a < D; ++a) {
+                    double acc = 1.0;
+                    for (long l = 0; l < D; ++l) {
+                        long t = a <= l ? pair_index(D, a, l) : pair_index(D, l, a);
+                        acc += qi[l] * kn[l] * keep_mult(row, t, inv_keep);
+                    }
+                    h[a] = acc;
+                }
+                for (long a = 0; a < D; ++a) dqt[i * D + a] += dw * kn[a] * h[a];
+            }
+        }
+#pragma omp parallel for schedule(dynamic, 4)
+        for (long n = 0; n < N; ++n) {
+            double h[D];
+            long istart = causal ? n : 0;
+            const uint32_t *row = hb + n * nw;
+            for (long i = istart; i < N; ++i) {
+                const double *qi = qt + i * D, *kn = kh + n * D;
+                double dw = 0.0;
+                for (long j = 0; j < D; ++j) dw += dob[i * D + j] * (vb[n * D + j] - o[i * D + j]);
+                dw /= G[i];
+                double w = drop_weight(qi, kn, row, D, inv_keep);
+                for (long a = 0; a < D; ++a) {
+                    double acc = 1.0;
+                    for (long l = 0; l < D; ++l) {
+                        long t = a <= l ? pair_index(D, a, l) : pair_index(D, l, a);
+                        acc += qi[l] * kn[l] * keep_mult(row, t, inv_keep);
+                    }
+                    h[a] = acc;
+                }
+                for (long a = 0; a < D; ++a) {
+                    dkh[n * D + a] += dw * qi[a] * h[a];
+                    dvh[n * D + a] += w * dob[i * D + a] / G[i];
+                }
+            }
+        }
+#pragma omp parallel for schedule(static)
+        for (long r = 0; r < N; ++r) {
+            double dqh[D];
+            for (long a = 0; a < D; ++a) dqh[a] = tau * dqt[r * D + a];
+            std_backward_row(qh + r * D, dqh, qs[r], D, dq + (hd * N + r) * D);
+            std_backward_row(kh + r * D, dkh + r * D, ks[r], D, dk + (hd * N + r) * D);
+            for (long a = 0; a < D; ++a) dv[(hd * N + r) * D + a] = dvh[r * D + a];
+        }
+        free(qh); free(kh); free(qs); free(ks); free(o); free(G);
+        free(dqt); free(dkh); free(dvh); free(qt);
+    }
+}
