@@ -42,6 +42,7 @@
 #define FASTMAX_H
 
 #include <stddef.h>
+#include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
 #ifdef __cplusplus
@@ -55,7 +56,7 @@ typedef enum {
 
 enum {
     FASTMAX_OK = 0,
-    FASTMAX_EINVAL = -1,       /* p, causal, dt or qk_scale out of range; B, H or N < 1 */
+    FASTMAX_EINVAL = -1,       /* p, causal, dt, qk_scale or dropout rate out of range; B, H or N < 1 */
     FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64, 128}   */
     FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
     FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */
@@ -140,6 +141,65 @@ int fastmax_bwd_scaled(const void *q, const void *k, const void *v, const void *
                        hipStream_t stream);
 
 /* Static description of a return code (never NULL). */
+/*
+ * Quadratic-term dropout, for training (Sec. 2.4, the dropout paragraph, and
+ * Fig. 2, whose "quadratic" variant is the one built here).  Only p = 2.
+ * Every key token n carries a keep bit for each of its D(D+1)/2 quadratic
+ * features k^_nm k^_nl (m <= l, numbered m-major: t = m D - m(m-1)/2 + l - m).
+ * A kept feature is multiplied by 1/(1 - rate), a dropped one by 0, in both
+ * the numerator and the denominator moments (it is one embedding), so the
+ * weight of the pair (i, n) becomes
+ *     w_in = 1 + tau s_in + sum_{m<=l} c_ml tau^2 q^_im q^_il k^_nm k^_nl b~_nt
+ * (c_mm = 1/2, c_ml = 1 for m < l, b~ = bit / (1 - rate)); O = F / G as before.
+ * With every bit set and rate 0 this is the plain p = 2 forward.
+ *
+ * keep_bits: uint32 [B, H, N, fastmax_dropout_mask_words(D)], 4-byte aligned,
+ *   feature t of token n at bit t % 32 of word t / 32 of the token's row
+ *   (bits past D(D+1)/2 are ignored).  The caller owns it and passes the same
+ *   bits to the forward and the backward of one step.
+ * The dropout calls run on the float32 VALU kernels for every D and dtype.
+ */
+
+/* Words per token of a keep-bit row: ceil(D(D+1)/2 / 32); 0 for an
+ * unsupported D. */
+size_t fastmax_dropout_mask_words(int D);
+
+/*
+ * Draws keep bits with the counter-based generator Philox4x32-10 (Salmon,
+ * Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3", SC 2011):
+ * for head h = b H + head index and token n, feature t uses output word t % 4
+ * of the counter (n, t / 4, h, 0) under the key (seed & 0xffffffff,
+ * seed >> 32) and is kept iff that word is >= floor(rate 2^32).  Writes every
+ * word of keep_bits (padding bits 0).  Same seed, same bits, on any device.
+ * rate in [0, 1); EINVAL otherwise.
+ */
+int fastmax_dropout_mask(uint32_t *keep_bits, int B, int H, int N, int D, float rate,
+                         uint64_t seed, hipStream_t stream);
+
+/* Workspace of fastmax_fwd_dropout (backward = 0) / fastmax_bwd_dropout
+ * (backward = 1): that of the float32 kernels at p = 2 (see
+ * fastmax_workspace_bytes). */
+size_t fastmax_dropout_workspace_bytes(int B, int H, int N, int D, int causal,
+                                       fastmax_dtype_t dt, int backward);
+
+/* Forward with the masked weights.  Arguments as fastmax_fwd_scaled with
+ * p = 2, plus keep_bits and rate (the drop probability the bits were drawn
+ * with; kept features are scaled by 1/(1 - rate)).  g receives G of the
+ * masked weights. */
+int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
+                        const uint32_t *keep_bits, float rate, int B, int H, int N, int D,
+                        int causal, float qk_scale, fastmax_dtype_t dt, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream);
+
+/* Backward of fastmax_fwd_dropout with the same keep_bits and rate (the
+ * mask is a constant of the step): out and g are that forward's outputs.
+ * Arguments as fastmax_bwd_scaled with p = 2. */
+int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void *out,
+                        const void *dout, const float *g, const uint32_t *keep_bits, float rate,
+                        void *dq, void *dk, void *dv, int B, int H, int N, int D, int causal,
+                        float qk_scale, fastmax_dtype_t dt, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream);
+
 const char *fastmax_strerror(int code);
 
 /* Library version as "major.minor.patch". */

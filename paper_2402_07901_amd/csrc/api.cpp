@@ -3,6 +3,7 @@
 #include <stdint.h>
 
 #include "../../include/fastmax.h"
+#include "fm_common.h"
 #include "fm_internal.h"
 
 namespace {
@@ -42,6 +43,11 @@ bool mfma_noncausal(int N, int D, int p, int causal, fastmax_dtype_t dt)
 {
     return D == 64 && p == 2 && !causal && dt == FASTMAX_BF16 && N >= 128;
 }
+
+// Drop probability of the quadratic-term dropout: [0, 1) (NaN fails).
+bool valid_rate(float rate) { return rate >= 0.0f && rate < 1.0f; }
+
+bool aligned4(const void *p) { return ((uintptr_t)p & 3u) == 0; }
 
 bool mfma_causal(int D, int p, int causal, fastmax_dtype_t dt)
 {
@@ -141,11 +147,83 @@ int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, co
                               workspace, workspace_bytes, stream);
 }
 
+size_t fastmax_dropout_mask_words(int D)
+{
+    return supported_d(D) ? (size_t)fm::mask_words(D) : 0;
+}
+
+int fastmax_dropout_mask(uint32_t *keep_bits, int B, int H, int N, int D, float rate,
+                         uint64_t seed, hipStream_t stream)
+{
+    int rc = check_common(B, H, N, D, 2, 0, FASTMAX_F32);
+    if (rc != FASTMAX_OK) return rc;
+    if (!valid_rate(rate)) return FASTMAX_EINVAL;
+    if (!keep_bits) return FASTMAX_ENULL;
+    if (!aligned4(keep_bits)) return FASTMAX_EALIGN;
+    // floor(rate 2^32) in double: exact for every float rate in [0, 1)
+    const uint32_t thr = (uint32_t)((double)rate * 4294967296.0);
+    hipError_t e = fm::dropout_mask(keep_bits, B * H, N, D, thr, seed, stream);
+    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
+size_t fastmax_dropout_workspace_bytes(int B, int H, int N, int D, int causal,
+                                       fastmax_dtype_t dt, int backward)
+{
+    if (check_common(B, H, N, D, 2, causal, dt) != FASTMAX_OK) return 0;
+    return backward ? fm::generic_bwd_workspace(B, H, N, D, 2)
+                    : fm::generic_fwd_workspace(B * H, N, D, 2);
+}
+
+int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
+                        const uint32_t *keep_bits, float rate, int B, int H, int N, int D,
+                        int causal, float qk_scale, fastmax_dtype_t dt, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_common(B, H, N, D, 2, causal, dt);
+    if (rc != FASTMAX_OK) return rc;
+    if (!valid_scale(qk_scale) || !valid_rate(rate)) return FASTMAX_EINVAL;
+    if (!q || !k || !v || !out || !keep_bits) return FASTMAX_ENULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+        (g && !aligned16(g)) || !aligned4(keep_bits))
+        return FASTMAX_EALIGN;
+    size_t need = fm::generic_fwd_workspace(B * H, N, D, 2);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
+    if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
+    hipError_t e = fm::generic_fwd_dropout(q, k, v, out, g, B * H, N, D, causal,
+                                           dt == FASTMAX_BF16, qk_scale, keep_bits,
+                                           1.0f / (1.0f - rate), workspace, stream);
+    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
+int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void *out,
+                        const void *dout, const float *g, const uint32_t *keep_bits, float rate,
+                        void *dq, void *dk, void *dv, int B, int H, int N, int D, int causal,
+                        float qk_scale, fastmax_dtype_t dt, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_common(B, H, N, D, 2, causal, dt);
+    if (rc != FASTMAX_OK) return rc;
+    if (!valid_scale(qk_scale) || !valid_rate(rate)) return FASTMAX_EINVAL;
+    if (!q || !k || !v || !out || !dout || !g || !keep_bits || !dq || !dk || !dv)
+        return FASTMAX_ENULL;
+    const void *ptrs[] = {q, k, v, out, dout, g, dq, dk, dv};
+    for (const void *ptr : ptrs)
+        if (!aligned16(ptr)) return FASTMAX_EALIGN;
+    if (!aligned4(keep_bits)) return FASTMAX_EALIGN;
+    size_t need = fm::generic_bwd_workspace(B, H, N, D, 2);
+    if (!workspace || workspace_bytes < need) return FASTMAX_EWORKSPACE;
+    if (!aligned16(workspace)) return FASTMAX_EALIGN;
+    hipError_t e = fm::generic_bwd_dropout(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D,
+                                           causal, dt == FASTMAX_BF16, qk_scale, keep_bits,
+                                           1.0f / (1.0f - rate), workspace, stream);
+    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
 const char *fastmax_strerror(int code)
 {
     switch (code) {
     case FASTMAX_OK: return "success";
-    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, or qk_scale not in (0, 1])";
+    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, qk_scale not in (0, 1], or dropout rate not in [0, 1))";
     case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32, 64 or 128)";
     case FASTMAX_ENULL: return "required pointer is NULL";
     case FASTMAX_EALIGN: return "pointer not 16-byte aligned";

@@ -53,4 +53,13 @@ __host__ __device__ constexpr int pair_feature(int D, int m, int l)
     return 1 + D + m * D - (m * (m - 1)) / 2 + (l - m);
 }
 
+// Quadratic-term dropout (Sec. 2.4, dropout paragraph; Fig. 2): keep bits
+// on the D(D+1)/2 quadratic features of every key token.  A token's bits
+// fill mask_words(D) uint32 words; pair feature t (m-major, m <= l, the
+// order of pair_feature) is bit t % 32 of word t / 32.
+__host__ __device__ constexpr int mask_words(int D)
+{
+    return (D * (D + 1) / 2 + 31) / 32;
+}
+
 }  // namespace fm

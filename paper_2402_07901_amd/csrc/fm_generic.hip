@@ -10,6 +10,13 @@
 // moment state of a slice of value columns J is S[f][j] = sum_n phi_f(k^_n)
 // v'_nj, v' = [v | 1] (the ones column yields G).  Causal rows use the
 // chunk-exclusive prefix of S plus the in-chunk tril block.
+//
+// Quadratic-term dropout (Sec. 2.4, dropout paragraph; Fig. 2), p = 2 only:
+// the kernels' DROP variants multiply each key token's quadratic features
+// phi_t(k^_n) by its keep bit times 1/(1 - rate) wherever they enter (the
+// moment states built from keys, the in-chunk weights, and the backward's
+// key-side contractions).  The weight of a pair is then
+// w_in = 1 + s + sum_{m<=l} c_ml q_m q_l k_m k_l b~_n(m,l) instead of f_2(s).
 #include <hip/hip_runtime.h>
 
 #include "fm_common.h"
@@ -20,6 +27,26 @@ namespace generic {
 
 constexpr int CH = 16;    // tokens per chunk
 constexpr int NT = 256;   // threads per workgroup
+
+// Dropout arguments: keep bits ([B*H][N][mask_words(D)] words) and the scale
+// 1/(1 - rate) of a kept feature.  bits == nullptr in the plain kernels.
+struct Drop {
+    const uint32_t *bits;
+    float inv;
+};
+
+// Multiplier of quadratic feature t of the token whose bit row is `row`.
+__device__ __forceinline__ float keep_mult(const uint32_t *row, int t, float inv)
+{
+    return (row[t >> 5] >> (t & 31)) & 1u ? inv : 0.0f;
+}
+
+// Bit row of token n0 of a head (the chunk's first row).
+template <int D>
+__device__ __forceinline__ const uint32_t *mask_rows(const Drop &dr, int head, int N, int n0)
+{
+    return dr.bits + ((size_t)head * N + n0) * mask_words(D);
+}
 
 template <int D, bool P2> struct feat {
     static constexpr int P = n_features(D, P2 ? 2 : 1);
@@ -113,19 +140,26 @@ __device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_ou
     __syncthreads();
 }
 
-// S[f][j] += sum_{r < CH} phi_f(x_r) val[r][j], j < WS.
-template <int D, bool P2, int WS>
+// S[f][j] += sum_{r < CH} phi_f(x_r) val[r][j], j < WS.  DROP: the
+// quadratic features of row r < nvalid are multiplied by the keep bits of
+// its row in mrow (rows past nvalid are past N and carry zero values).
+template <int D, bool P2, int WS, bool DROP = false>
 __device__ void state_update(float *S, const float *x, const float *val, const uint8_t *pm,
-                             const uint8_t *pl)
+                             const uint8_t *pl, const uint32_t *mrow = nullptr, int nvalid = 0,
+                             float inv = 1.0f)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int DP = D + 1;
+    constexpr int NW = mask_words(D);
     for (int f = threadIdx.x; f < P; f += NT) {
         float acc[WS];
 #pragma unroll
         for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
         for (int r = 0; r < CH; ++r) {
             float ph = phi<D>(f, x + r * DP, pm, pl);
+            if constexpr (DROP) {
+                if (f > D) ph *= r < nvalid ? keep_mult(mrow + r * NW, f - 1 - D, inv) : 0.0f;
+            }
 #pragma unroll
             for (int j = 0; j < WS; ++j) acc[j] = fmaf(ph, val[r * WS + j], acc[j]);
         }
@@ -135,19 +169,25 @@ __device__ void state_update(float *S, const float *x, const float *val, const u
 }
 
 // out[r][j] += sum_f psi_f(x_r) S[f][j]   (LDS atomics; out is CH x WS).
-template <int D, bool P2, int WS>
+// DROP: x holds keys, whose quadratic features take their keep bits.
+template <int D, bool P2, int WS, bool DROP = false>
 __device__ void contract_psi(const float *S, const float *x, float *out, const uint8_t *pm,
-                             const uint8_t *pl)
+                             const uint8_t *pl, const uint32_t *mrow = nullptr, int nvalid = 0,
+                             float inv = 1.0f)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int DP = D + 1;
     constexpr int NG = NT / CH;
+    constexpr int NW = mask_words(D);
     const int r = threadIdx.x % CH, fg = threadIdx.x / CH;
     float acc[WS];
 #pragma unroll
     for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
     for (int f = fg; f < P; f += NG) {
         float ps = psi<D>(f, x + r * DP, pm, pl);
+        if constexpr (DROP) {
+            if (f > D) ps *= r < nvalid ? keep_mult(mrow + r * NW, f - 1 - D, inv) : 0.0f;
+        }
 #pragma unroll
         for (int j = 0; j < WS; ++j) acc[j] = fmaf(ps, S[f * WS + j], acc[j]);
     }
@@ -158,12 +198,15 @@ __device__ void contract_psi(const float *S, const float *x, float *out, const u
 // Gradient-side contraction (backward):
 //   out[r][a] = sum_{j<WS} coef[r][j] (S[1+a][j] + [p=2] sum_m x_rm S[(a,m)][j])
 // which is the moment form of sum_n f'(s_rn) (coef_r . val_n) y_n[a] when S
-// holds the moments of (y, val).
-template <int D, bool P2, int WS>
-__device__ void contract_grad(const float *S, const float *x, const float *coef, float *out)
+// holds the moments of (y, val).  DROP: x holds keys, and x_rm carries the
+// keep multiplier of row r's feature (a, m).
+template <int D, bool P2, int WS, bool DROP = false>
+__device__ void contract_grad(const float *S, const float *x, const float *coef, float *out,
+                              const uint32_t *mrow = nullptr, int nvalid = 0, float inv = 1.0f)
 {
     constexpr int DP = D + 1;
     constexpr int AG = NT / CH;          // a-groups
+    constexpr int NW = mask_words(D);
     const int r = threadIdx.x % CH, ag = threadIdx.x / CH;
     const float *xr = x + r * DP;
     for (int a = ag; a < D; a += AG) {
@@ -173,13 +216,53 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
             if (P2) {
                 for (int m = 0; m < D; ++m) {
                     int lo = m < a ? m : a, hi = m < a ? a : m;
-                    inner = fmaf(xr[m], S[pair_feature(D, lo, hi) * WS + j], inner);
+                    const int pf = pair_feature(D, lo, hi);
+                    float xm = xr[m];
+                    if constexpr (DROP)
+                        xm *= r < nvalid ? keep_mult(mrow + r * NW, pf - 1 - D, inv) : 0.0f;
+                    inner = fmaf(xm, S[pf * WS + j], inner);
                 }
             }
             acc = fmaf(coef[r * WS + j], inner, acc);
         }
         out[r * D + a] = acc;
     }
+}
+
+// Dropout weight of one (query, key) pair, xq already scaled by the score
+// scale: 1 + s + sum_{m<=l} c_ml z_m z_l b~_t(m,l), z = xq (.) xk, c_mm = 1/2.
+template <int D>
+__device__ float drop_weight(const float *xq, const float *xk, const uint32_t *row, float inv)
+{
+    float s = 0.0f, quad = 0.0f;
+    int t = 0;
+    uint32_t word = 0;
+    for (int m = 0; m < D; ++m) {
+        const float zm = xq[m] * xk[m];
+        s += zm;
+        float inner = 0.0f;
+        for (int l = m; l < D; ++l, ++t) {
+            if ((t & 31) == 0) word = row[t >> 5];
+            const float zl = l == m ? 0.5f * zm : xq[l] * xk[l];
+            if ((word >> (t & 31)) & 1u) inner += zl;
+        }
+        quad = fmaf(zm, inner, quad);
+    }
+    return 1.0f + s + quad * inv;
+}
+
+// d w / d xq_a = xk_a h_a and d w / d xk_a = xq_a h_a for the dropout weight,
+// h_a = 1 + sum_l xq_l xk_l b~_t(a,l).
+template <int D>
+__device__ float drop_h(const float *xq, const float *xk, const uint32_t *row, int a, float inv)
+{
+    float acc = 0.0f;
+    for (int l = 0; l < D; ++l) {
+        const int lo = l < a ? l : a, hi = l < a ? a : l;
+        const int t = pair_feature(D, lo, hi) - 1 - D;
+        if ((row[t >> 5] >> (t & 31)) & 1u) acc = fmaf(xq[l], xk[l], acc);
+    }
+    return fmaf(acc, inv, 1.0f);
 }
 
 // ---------------------------------------------------------------------------
@@ -191,10 +274,11 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
 // Sec. 2.4's causal moments at the segment start), a non-causal one contracts
 // its queries against the sum of all segments.
 // ---------------------------------------------------------------------------
-template <int D, bool P2, int WS, typename T>
+template <int D, bool P2, int WS, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
                                                        const T *__restrict__ v,
-                                                       float *__restrict__ sseg, int N, int cps)
+                                                       float *__restrict__ sseg, int N, int cps,
+                                                       Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -228,7 +312,11 @@ __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
             vv[e] = x;
         }
         __syncthreads();
-        state_update<D, P2, WS>(S, xk, vv, pm, pl);
+        if constexpr (DROP)
+            state_update<D, P2, WS, true>(S, xk, vv, pm, pl, mask_rows<D>(dr, head, N, c * CH),
+                                          min(CH, N - c * CH), dr.inv);
+        else
+            state_update<D, P2, WS>(S, xk, vv, pm, pl);
         __syncthreads();
     }
     float *dst = sseg + (((size_t)head * gridDim.y + blockIdx.y) * gridDim.z + seg) * P * WS;
@@ -266,11 +354,12 @@ __global__ __launch_bounds__(NT) void seg_prefix_kernel(float *__restrict__ sseg
     if (!CAUSAL) base[0] = run;
 }
 
-template <int D, bool P2, int WS, bool CAUSAL, typename T>
+template <int D, bool P2, int WS, bool CAUSAL, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                  const T *__restrict__ v, T *__restrict__ out,
                                                  float *__restrict__ g, int N, int cps,
-                                                 const float *__restrict__ sseg, float qs)
+                                                 const float *__restrict__ sseg, float qs,
+                                                 Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -339,7 +428,12 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
                 load_std<D>(k, c * CH, N, xk, nullptr);
                 load_vals(c * CH);
                 __syncthreads();
-                state_update<D, P2, WS>(S, xk, vv, pm, pl);
+                if constexpr (DROP)
+                    state_update<D, P2, WS, true>(S, xk, vv, pm, pl,
+                                                  mask_rows<D>(dr, head, N, c * CH),
+                                                  min(CH, N - c * CH), dr.inv);
+                else
+                    state_update<D, P2, WS>(S, xk, vv, pm, pl);
                 __syncthreads();
             }
         }
@@ -362,7 +456,12 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             {
                 int i = threadIdx.x / CH, t = threadIdx.x % CH;
                 float w = 0.0f;
-                if (t <= i) {
+                if constexpr (DROP) {
+                    // keys past N are never seen by a valid row (t <= i < N)
+                    if (t <= i && n0 + i < N)
+                        w = drop_weight<D>(xq + i * DP, xk + t * DP,
+                                           mask_rows<D>(dr, head, N, n0 + t), dr.inv);
+                } else if (t <= i) {
                     float s = 0.0f;
                     for (int d = 0; d < D; ++d) s = fmaf(xq[i * DP + d], xk[t * DP + d], s);
                     w = taylor<POW>(s);
@@ -380,7 +479,11 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             contract_psi<D, P2, WS>(S, xq, F, pm, pl);   // exclusive prefix S_<c
             __syncthreads();
             write_out(n0);
-            state_update<D, P2, WS>(S, xk, vv, pm, pl);
+            if constexpr (DROP)
+                state_update<D, P2, WS, true>(S, xk, vv, pm, pl, mask_rows<D>(dr, head, N, n0),
+                                              min(CH, N - n0), dr.inv);
+            else
+                state_update<D, P2, WS>(S, xk, vv, pm, pl);
             __syncthreads();
         }
     }
@@ -442,21 +545,26 @@ __device__ void load_vprime(const T *v, int n0, int N, int gc0, float *dst)
 // In-chunk (tril) part of all three gradients; plain stores initialise the
 // float32 accumulators (zeros for the non-causal problem, whose every pair is
 // handled by the moment kernels).
-template <int D, bool P2, bool CAUSAL, typename T>
+// DROP: E holds dw alone and Wm the dropout weight; the derivative factor
+// is the per-channel h of drop_h, with the key rows' keep bits staged in LDS.
+template <int D, bool P2, bool CAUSAL, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dqh, float *__restrict__ dkh, float *__restrict__ dva, int N, float qs)
+    float *__restrict__ dqh, float *__restrict__ dkh, float *__restrict__ dva, int N, float qs,
+    Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int DP = D + 1;
     constexpr int D1 = D + 1;
     constexpr int POW = P2 ? 2 : 1;
+    constexpr int NW = mask_words(D);
     __shared__ float xq[CH * DP];
     __shared__ float xk[CH * DP];
     __shared__ float vp[CH * D1];
     __shared__ float ut[CH * D1];
     __shared__ float E[CH * CH];   // f'(s) dw
     __shared__ float Wm[CH * CH];  // f(s)
+    __shared__ uint32_t mk[DROP ? CH * NW : 1];
 
     const int head = blockIdx.x, n0 = blockIdx.y * CH;
     const size_t hb = (size_t)head * N * D;
@@ -479,17 +587,27 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     load_std<D>(k, n0, N, xk, nullptr);
     load_vprime<D, D1>(v, n0, N, 0, vp);
     load_utilde<D, D1>(dout, g, cvec, n0, N, 0, ut);
+    if constexpr (DROP) {
+        const uint32_t *src = mask_rows<D>(dr, head, N, n0);
+        const int nv = min(CH, N - n0) * NW;
+        for (int e = threadIdx.x; e < CH * NW; e += NT) mk[e] = e < nv ? src[e] : 0u;
+    }
     __syncthreads();
     {
         int i = threadIdx.x / CH, t = threadIdx.x % CH;
         float e = 0.0f, w = 0.0f;
         if (t <= i && n0 + i < N) {
-            float s = 0.0f;
-            for (int d = 0; d < D; ++d) s = fmaf(xq[i * DP + d], xk[t * DP + d], s);
             float dw = 0.0f;
             for (int j = 0; j < D1; ++j) dw = fmaf(ut[i * D1 + j], vp[t * D1 + j], dw);
-            e = dtaylor<POW>(s) * dw;
-            w = taylor<POW>(s);
+            if constexpr (DROP) {
+                e = dw;
+                w = drop_weight<D>(xq + i * DP, xk + t * DP, mk + t * NW, dr.inv);
+            } else {
+                float s = 0.0f;
+                for (int d = 0; d < D; ++d) s = fmaf(xq[i * DP + d], xk[t * DP + d], s);
+                e = dtaylor<POW>(s) * dw;
+                w = taylor<POW>(s);
+            }
         }
         E[i * CH + t] = e;
         Wm[i * CH + t] = w;
@@ -499,10 +617,20 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
         int r = e / D, a = e % D, n = n0 + r;
         if (n >= N) continue;
         float aq = 0.0f, ak = 0.0f, av = 0.0f;
-        for (int t = 0; t < CH; ++t) {
-            aq = fmaf(E[r * CH + t], xk[t * DP + a], aq);   // row r as query
-            ak = fmaf(E[t * CH + r], xq[t * DP + a], ak);   // row r as key
-            av = fmaf(Wm[t * CH + r], ut[t * D1 + a], av);
+        if constexpr (DROP) {
+            for (int t = 0; t <= r; ++t)   // row r as query, keys t <= r
+                aq = fmaf(E[r * CH + t] * xk[t * DP + a],
+                          drop_h<D>(xq + r * DP, xk + t * DP, mk + t * NW, a, dr.inv), aq);
+            for (int t = r; t < CH; ++t)   // row r as key, queries t >= r
+                ak = fmaf(E[t * CH + r] * xq[t * DP + a],
+                          drop_h<D>(xq + t * DP, xk + r * DP, mk + r * NW, a, dr.inv), ak);
+            for (int t = 0; t < CH; ++t) av = fmaf(Wm[t * CH + r], ut[t * D1 + a], av);
+        } else {
+            for (int t = 0; t < CH; ++t) {
+                aq = fmaf(E[r * CH + t], xk[t * DP + a], aq);   // row r as query
+                ak = fmaf(E[t * CH + r], xq[t * DP + a], ak);   // row r as key
+                av = fmaf(Wm[t * CH + r], ut[t * D1 + a], av);
+            }
         }
         size_t o = (size_t)n * D + a;
         dqh[o] = aq;
@@ -513,11 +641,12 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
 
 // dq^ from the forward-direction moments of (k^, v'): grid = (B*H, slices over
 // the D+1 columns of v').  Causal rows see the chunk-exclusive prefix.
-template <int D, bool P2, int WS, bool CAUSAL, typename T>
+template <int D, bool P2, int WS, bool CAUSAL, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ dqh, int N, float qs, const float *__restrict__ sseg, int cps)
+    float *__restrict__ dqh, int N, float qs, const float *__restrict__ sseg, int cps,
+    Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -567,7 +696,11 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
         load_std<D>(k, n0, N, xk, nullptr);
         load_vprime<D, WS>(v, n0, N, gc0, vp);
         __syncthreads();
-        state_update<D, P2, WS>(S, xk, vp, pm, pl);
+        if constexpr (DROP)
+            state_update<D, P2, WS, true>(S, xk, vp, pm, pl, mask_rows<D>(dr, head, N, n0),
+                                          min(CH, N - n0), dr.inv);
+        else
+            state_update<D, P2, WS>(S, xk, vp, pm, pl);
         __syncthreads();
     };
     if (!CAUSAL) {
@@ -586,12 +719,12 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
 //   T[f][j] = sum_i phi_f(q^_i) u~_ij over rows i after the chunk (causal) or
 //   all rows; dk^_n[a] += sum_j v'_nj (T[1+a][j] + sum_m k^_nm T[(a,m)][j]),
 //   dv_n[j] += sum_f psi_f(k^_n) T[f][j].
-template <int D, bool P2, int WS, bool CAUSAL, typename T>
+template <int D, bool P2, int WS, bool CAUSAL, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
     float *__restrict__ dkh, float *__restrict__ dva, int N, float qs,
-    const float *__restrict__ sseg, int cps)
+    const float *__restrict__ sseg, int cps, Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -631,8 +764,15 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
         load_vprime<D, WS>(v, n0, N, gc0, vp);
         for (int e = threadIdx.x; e < CH * WS; e += NT) pv[e] = 0.0f;
         __syncthreads();
-        contract_grad<D, P2, WS>(S, xk, vp, part);
-        contract_psi<D, P2, WS>(S, xk, pv, pm, pl);
+        if constexpr (DROP) {
+            const uint32_t *mr = mask_rows<D>(dr, head, N, n0);
+            const int nv = min(CH, N - n0);
+            contract_grad<D, P2, WS, true>(S, xk, vp, part, mr, nv, dr.inv);
+            contract_psi<D, P2, WS, true>(S, xk, pv, pm, pl, mr, nv, dr.inv);
+        } else {
+            contract_grad<D, P2, WS>(S, xk, vp, part);
+            contract_psi<D, P2, WS>(S, xk, pv, pm, pl);
+        }
         __syncthreads();
         for (int e = threadIdx.x; e < CH * D; e += NT) {
             int n = n0 + e / D;
@@ -666,11 +806,11 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
 // Moment sums of one segment of chunks for the backward scans (all segments
 // in parallel): SIDE 0 -> sum phi(k^_n) v'_n (the q-scan's state), SIDE 1 ->
 // sum phi(qs q^_i) u~_i (the k-scan's state), columns gc0.. of the D + 1.
-template <int D, bool P2, int WS, int SIDE, typename T>
+template <int D, bool P2, int WS, int SIDE, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ sseg, int N, float qs, int cps)
+    float *__restrict__ sseg, int N, float qs, int cps, Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -701,7 +841,11 @@ __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
             load_utilde<D, WS>(dout, g, cvec, c * CH, N, gc0, vals);
         }
         __syncthreads();
-        state_update<D, P2, WS>(S, xs, vals, pm, pl);
+        if constexpr (DROP && SIDE == 0)   // keys: their quadratic features are masked
+            state_update<D, P2, WS, true>(S, xs, vals, pm, pl, mask_rows<D>(dr, head, N, c * CH),
+                                          min(CH, N - c * CH), dr.inv);
+        else
+            state_update<D, P2, WS>(S, xs, vals, pm, pl);
         __syncthreads();
     }
     float *dst = sseg + (((size_t)head * gridDim.y + blockIdx.y) * nseg + seg) * P * WS;
@@ -789,17 +933,18 @@ SegPlan seg_plan(int BH, int N)
     return sp;
 }
 
-template <int D, bool P2, typename T>
+template <int D, bool P2, typename T, bool DROP = false>
 static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void *out, float *g,
-                               int BH, int N, int causal, float qs, void *ws, hipStream_t st)
+                               int BH, int N, int causal, float qs, void *ws, hipStream_t st,
+                               Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int WS = slice_width<D, P2>::v;
     const SegPlan sp = seg_plan<D, P2>(BH, N);
     dim3 grid(BH, sp.slices, sp.nseg);
     float *sseg = sp.nseg > 1 ? (float *)ws : nullptr;
     if (sseg) {
-        hipLaunchKernelGGL((seg_state_kernel<D, P2, WS, T>), grid, dim3(NT), 0, st, (const T *)k,
-                           (const T *)v, sseg, N, sp.cps);
+        hipLaunchKernelGGL((seg_state_kernel<D, P2, WS, T, DROP>), grid, dim3(NT), 0, st,
+                           (const T *)k, (const T *)v, sseg, N, sp.cps, dr);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         constexpr int PWS = feat<D, P2>::P * WS;
@@ -814,13 +959,13 @@ static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void
         if (e != hipSuccess) return e;
     }
     if (causal)
-        hipLaunchKernelGGL((fwd_kernel<D, P2, WS, true, T>), grid, dim3(NT), 0, st,
+        hipLaunchKernelGGL((fwd_kernel<D, P2, WS, true, T, DROP>), grid, dim3(NT), 0, st,
                            (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N, sp.cps,
-                           (const float *)sseg, qs);
+                           (const float *)sseg, qs, dr);
     else
-        hipLaunchKernelGGL((fwd_kernel<D, P2, WS, false, T>), grid, dim3(NT), 0, st,
+        hipLaunchKernelGGL((fwd_kernel<D, P2, WS, false, T, DROP>), grid, dim3(NT), 0, st,
                            (const T *)q, (const T *)k, (const T *)v, (T *)out, g, N, sp.cps,
-                           (const float *)sseg, qs);
+                           (const float *)sseg, qs, dr);
     return hipGetLastError();
 }
 
@@ -850,10 +995,11 @@ BwdPlan bwd_plan(int BH, int N)
     return bp;
 }
 
-template <int D, bool P2, bool CAUSAL, typename T>
+template <int D, bool P2, bool CAUSAL, typename T, bool DROP = false>
 static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, const void *o,
                                 const void *dout, const float *g, void *dq, void *dk, void *dv,
-                                int BH, int N, float qs, float *ws, hipStream_t st)
+                                int BH, int N, float qs, float *ws, hipStream_t st,
+                                Drop dr = Drop{nullptr, 1.0f})
 {
     constexpr int WS = slice_width<D, P2>::v;
     constexpr int PWS = feat<D, P2>::P * WS;
@@ -867,21 +1013,21 @@ static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, con
     const int rb = (int)((rows + NT - 1) / NT);
     hipLaunchKernelGGL((bwd_rowdot_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)o,
                        (const T *)dout, g, cvec, rows);
-    hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T>), dim3(BH, (N + CH - 1) / CH),
+    hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T, DROP>), dim3(BH, (N + CH - 1) / CH),
                        dim3(NT), 0, st, (const T *)q, (const T *)k, (const T *)v,
-                       (const T *)dout, g, cvec, dqh, dkh, dva, N, qs);
+                       (const T *)dout, g, cvec, dqh, dkh, dva, N, qs, dr);
     const dim3 grid(BH, bp.slices, bp.nseg);
     const dim3 pgrid((PWS + NT - 1) / NT, BH * bp.slices);
     if (sseg) {
-        hipLaunchKernelGGL((bwd_seg_state_kernel<D, P2, WS, 0, T>), grid, dim3(NT), 0, st,
+        hipLaunchKernelGGL((bwd_seg_state_kernel<D, P2, WS, 0, T, DROP>), grid, dim3(NT), 0, st,
                            (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec,
-                           sseg, N, qs, bp.cps);
+                           sseg, N, qs, bp.cps, dr);
         hipLaunchKernelGGL((seg_prefix_kernel<PWS, CAUSAL, false>), pgrid, dim3(NT), 0, st, sseg,
                            bp.nseg);
     }
-    hipLaunchKernelGGL((bwd_qscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
+    hipLaunchKernelGGL((bwd_qscan_kernel<D, P2, WS, CAUSAL, T, DROP>), grid, dim3(NT), 0, st,
                        (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dqh,
-                       N, qs, (const float *)sseg, bp.cps);
+                       N, qs, (const float *)sseg, bp.cps, dr);
     if (sseg) {
         // the same buffer, reused in stream order for the k-scan's states
         hipLaunchKernelGGL((bwd_seg_state_kernel<D, P2, WS, 1, T>), grid, dim3(NT), 0, st,
@@ -890,9 +1036,9 @@ static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, con
         hipLaunchKernelGGL((seg_prefix_kernel<PWS, CAUSAL, true>), pgrid, dim3(NT), 0, st, sseg,
                            bp.nseg);
     }
-    hipLaunchKernelGGL((bwd_kscan_kernel<D, P2, WS, CAUSAL, T>), grid, dim3(NT), 0, st,
+    hipLaunchKernelGGL((bwd_kscan_kernel<D, P2, WS, CAUSAL, T, DROP>), grid, dim3(NT), 0, st,
                        (const T *)q, (const T *)k, (const T *)v, (const T *)dout, g, cvec, dkh,
-                       dva, N, qs, (const float *)sseg, bp.cps);
+                       dva, N, qs, (const float *)sseg, bp.cps, dr);
     hipLaunchKernelGGL((bwd_finish_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)q,
                        (const T *)k, dqh, dkh, dva, (T *)dq, (T *)dk, (T *)dv, rows, qs);
     return hipGetLastError();
@@ -908,7 +1054,137 @@ static hipError_t bwd_dispatch(const void *q, const void *k, const void *v, cons
     return bwd_dispatch2<D, P2, false, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs, ws, st);
 }
 
+// Keep bits with Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): one
+// thread per mask word (32 features = 8 generator calls).  Feature t of
+// token n of head h draws from counter (n, t / 4, h, 0) under the key
+// (seed low word, seed high word), output word t % 4, and is kept iff that
+// word is >= thr = floor(rate 2^32).
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]), lo0 = 0xD2511F53u * c[0];
+        const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]), lo1 = 0xCD9E8D57u * c[2];
+        const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(NT) void dropout_mask_kernel(uint32_t *__restrict__ bits,
+                                                          size_t words, int N, uint32_t thr,
+                                                          uint32_t key0, uint32_t key1)
+{
+    constexpr int NW = mask_words(D);
+    constexpr int NPAIR = D * (D + 1) / 2;
+    const size_t stride = (size_t)gridDim.x * NT;
+    for (size_t idx = (size_t)blockIdx.x * NT + threadIdx.x; idx < words; idx += stride) {
+        const size_t row = idx / NW;
+        const int w = (int)(idx % NW);
+        const uint32_t n = (uint32_t)(row % (size_t)N), head = (uint32_t)(row / (size_t)N);
+        uint32_t word = 0;
+#pragma unroll
+        for (int g4 = 0; g4 < 8; ++g4) {
+            const int t0 = 32 * w + 4 * g4;
+            if (t0 >= NPAIR) break;
+            uint32_t c[4] = {n, (uint32_t)(t0 >> 2), head, 0u};
+            philox4x32_10(c, key0, key1);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (t0 + u < NPAIR && c[u] >= thr) word |= 1u << (4 * g4 + u);
+        }
+        bits[idx] = word;
+    }
+}
+
 }  // namespace generic
+
+hipError_t dropout_mask(uint32_t *bits, int BH, int N, int D, uint32_t thr, uint64_t seed,
+                        hipStream_t st)
+{
+    using namespace generic;
+    const size_t words = (size_t)BH * N * (size_t)mask_words(D);
+    // grid-stride: at most 2^20 workgroups (enough to fill the chip many times)
+    const size_t want = (words + NT - 1) / NT;
+    const dim3 grid((unsigned)(want < ((size_t)1 << 20) ? want : ((size_t)1 << 20)));
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    switch (D) {
+    case 16: hipLaunchKernelGGL((dropout_mask_kernel<16>), grid, dim3(NT), 0, st, bits, words, N, thr, k0, k1); break;
+    case 32: hipLaunchKernelGGL((dropout_mask_kernel<32>), grid, dim3(NT), 0, st, bits, words, N, thr, k0, k1); break;
+    case 64: hipLaunchKernelGGL((dropout_mask_kernel<64>), grid, dim3(NT), 0, st, bits, words, N, thr, k0, k1); break;
+    default: hipLaunchKernelGGL((dropout_mask_kernel<128>), grid, dim3(NT), 0, st, bits, words, N, thr, k0, k1); break;
+    }
+    return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t drop_fwd_t(const void *q, const void *k, const void *v, void *out, float *g,
+                             int BH, int N, int D, int causal, float qs, const uint32_t *bits,
+                             float inv, void *ws, hipStream_t st)
+{
+    using namespace generic;
+    const Drop dr{bits, inv};
+    switch (D) {
+    case 16: return fwd_dispatch<16, true, T, true>(q, k, v, out, g, BH, N, causal, qs, ws, st, dr);
+    case 32: return fwd_dispatch<32, true, T, true>(q, k, v, out, g, BH, N, causal, qs, ws, st, dr);
+    case 64: return fwd_dispatch<64, true, T, true>(q, k, v, out, g, BH, N, causal, qs, ws, st, dr);
+    default: return fwd_dispatch<128, true, T, true>(q, k, v, out, g, BH, N, causal, qs, ws, st, dr);
+    }
+}
+
+template <int D, typename T>
+static hipError_t drop_bwd_d(const void *q, const void *k, const void *v, const void *o,
+                             const void *dout, const float *g, void *dq, void *dk, void *dv,
+                             int BH, int N, int causal, float qs, float *ws, hipStream_t st,
+                             generic::Drop dr)
+{
+    using namespace generic;
+    if (causal)
+        return bwd_dispatch2<D, true, true, T, true>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs,
+                                                     ws, st, dr);
+    return bwd_dispatch2<D, true, false, T, true>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs, ws,
+                                                  st, dr);
+}
+
+template <typename T>
+static hipError_t drop_bwd_t(const void *q, const void *k, const void *v, const void *o,
+                             const void *dout, const float *g, void *dq, void *dk, void *dv,
+                             int BH, int N, int D, int causal, float qs, const uint32_t *bits,
+                             float inv, float *ws, hipStream_t st)
+{
+    const generic::Drop dr{bits, inv};
+    switch (D) {
+    case 16: return drop_bwd_d<16, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
+    case 32: return drop_bwd_d<32, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
+    case 64: return drop_bwd_d<64, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
+    default: return drop_bwd_d<128, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
+    }
+}
+
+hipError_t generic_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
+                               int BH, int N, int D, int causal, int is_bf16, float qs,
+                               const uint32_t *bits, float inv, void *ws, hipStream_t st)
+{
+    if (is_bf16) return drop_fwd_t<bf16_t>(q, k, v, out, g, BH, N, D, causal, qs, bits, inv, ws, st);
+    return drop_fwd_t<float>(q, k, v, out, g, BH, N, D, causal, qs, bits, inv, ws, st);
+}
+
+hipError_t generic_bwd_dropout(const void *q, const void *k, const void *v, const void *o,
+                               const void *dout, const float *g, void *dq, void *dk, void *dv,
+                               int BH, int N, int D, int causal, int is_bf16, float qs,
+                               const uint32_t *bits, float inv, void *ws, hipStream_t st)
+{
+    if (is_bf16)
+        return drop_bwd_t<bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, causal, qs, bits,
+                                  inv, (float *)ws, st);
+    return drop_bwd_t<float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, causal, qs, bits, inv,
+                             (float *)ws, st);
+}
 
 size_t generic_bwd_workspace(int B, int H, int N, int D, int p)
 {

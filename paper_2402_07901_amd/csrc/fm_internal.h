@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stddef.h>
+#include <stdint.h>
 
 namespace fm {
 
@@ -20,6 +21,21 @@ hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *
                        int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
                        hipStream_t st);
 size_t generic_bwd_workspace(int B, int H, int N, int D, int p);
+
+// Quadratic-term dropout (p = 2) on the generic kernels: bits are the keep
+// bits ([BH][N][mask_words(D)] words), inv = 1 / (1 - rate).  Workspaces as
+// generic_fwd_workspace / generic_bwd_workspace with p = 2.
+hipError_t generic_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
+                               int BH, int N, int D, int causal, int is_bf16, float qs,
+                               const uint32_t *bits, float inv, void *ws, hipStream_t st);
+hipError_t generic_bwd_dropout(const void *q, const void *k, const void *v, const void *o,
+                               const void *dout, const float *g, void *dq, void *dk, void *dv,
+                               int BH, int N, int D, int causal, int is_bf16, float qs,
+                               const uint32_t *bits, float inv, void *ws, hipStream_t st);
+// Philox4x32-10 keep bits for BH heads of N tokens; a feature is kept iff its
+// generator word is >= thr.
+hipError_t dropout_mask(uint32_t *bits, int BH, int N, int D, uint32_t thr, uint64_t seed,
+                        hipStream_t st);
 
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
 // ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16.

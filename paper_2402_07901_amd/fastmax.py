@@ -55,6 +55,19 @@ def lib():
         L.fastmax_bwd_scaled.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, f,
                                          i, vp, sz, vp]
         L.fastmax_bwd_scaled.restype = i
+        u64 = ctypes.c_uint64
+        L.fastmax_dropout_mask_words.argtypes = [i]
+        L.fastmax_dropout_mask_words.restype = sz
+        L.fastmax_dropout_mask.argtypes = [vp, i, i, i, i, f, u64, vp]
+        L.fastmax_dropout_mask.restype = i
+        L.fastmax_dropout_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
+        L.fastmax_dropout_workspace_bytes.restype = sz
+        L.fastmax_fwd_dropout.argtypes = [vp, vp, vp, vp, vp, vp, f, i, i, i, i, i, f, i, vp, sz,
+                                          vp]
+        L.fastmax_fwd_dropout.restype = i
+        L.fastmax_bwd_dropout.argtypes = [vp, vp, vp, vp, vp, vp, vp, f, vp, vp, vp, i, i, i, i,
+                                          i, f, i, vp, sz, vp]
+        L.fastmax_bwd_dropout.restype = i
         L.fastmax_strerror.argtypes = [i]
         L.fastmax_strerror.restype = ctypes.c_char_p
         L.fastmax_version.restype = ctypes.c_char_p
@@ -166,4 +179,88 @@ def fastmax_bwd(q, k, v, out, dout, g, p=2, causal=False, dq=None, dk=None, dv=N
                          ws_n, stream, scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_bwd")
+    return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# Quadratic-term dropout (Sec. 2.4, dropout paragraph; Fig. 2), p = 2.  Keep
+# bits are an int32 tensor [B, H, N, mask_words(D)] holding the uint32 words.
+# ---------------------------------------------------------------------------
+def mask_words(D) -> int:
+    """uint32 words per token of a keep-bit row (0 for an unsupported D)."""
+    return int(lib().fastmax_dropout_mask_words(int(D)))
+
+
+def fastmax_dropout_mask_raw(bits, B, H, N, D, rate, seed, stream):
+    return lib().fastmax_dropout_mask(_ptr(bits), B, H, N, D, float(rate),
+                                      ctypes.c_uint64(int(seed)), _stream(stream))
+
+
+def dropout_mask(B, H, N, D, rate, seed, device="cuda", stream=None):
+    """Philox4x32-10 keep bits for the quadratic features of every key token."""
+    import torch
+    bits = torch.empty((B, H, N, mask_words(D)), dtype=torch.int32, device=device)
+    rc = fastmax_dropout_mask_raw(bits, B, H, N, D, rate, seed, stream)
+    if rc != OK:
+        raise FastmaxError(rc, "fastmax_dropout_mask")
+    return bits
+
+
+def dropout_workspace_bytes(B, H, N, D, causal, dt, backward=False) -> int:
+    return int(lib().fastmax_dropout_workspace_bytes(B, H, N, D, int(causal), dt,
+                                                     int(bool(backward))))
+
+
+def fastmax_fwd_dropout_raw(q, k, v, out, g, bits, rate, B, H, N, D, causal, scale, dt,
+                            workspace, ws_bytes, stream):
+    return lib().fastmax_fwd_dropout(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(g), _ptr(bits),
+                                     float(rate), B, H, N, D, int(causal), float(scale), dt,
+                                     _ptr(workspace), ws_bytes, _stream(stream))
+
+
+def fastmax_bwd_dropout_raw(q, k, v, out, dout, g, bits, rate, dq, dk, dv, B, H, N, D, causal,
+                            scale, dt, workspace, ws_bytes, stream):
+    return lib().fastmax_bwd_dropout(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(g),
+                                     _ptr(bits), float(rate), _ptr(dq), _ptr(dk), _ptr(dv), B, H,
+                                     N, D, int(causal), float(scale), dt, _ptr(workspace),
+                                     ws_bytes, _stream(stream))
+
+
+def fastmax_fwd_dropout(q, k, v, bits, rate, causal=False, scale=None, out=None, g=None,
+                        workspace=None, stream=None):
+    """Forward with the quadratic features of the keys masked by ``bits``
+    (kept ones scaled by 1/(1 - rate)); returns (O, G)."""
+    import torch
+    B, H, N, D = q.shape
+    dt = _dtype_code(q)
+    out = torch.empty_like(q) if out is None else out
+    if g is None:
+        g = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = _alloc_ws(dropout_workspace_bytes(B, H, N, D, causal, dt, False), q.device)
+    ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = fastmax_fwd_dropout_raw(q, k, v, out, g, bits, rate, B, H, N, D, causal,
+                                 1.0 if scale is None else scale, dt, workspace, ws_n, stream)
+    if rc != OK:
+        raise FastmaxError(rc, "fastmax_fwd_dropout")
+    return out, g
+
+
+def fastmax_bwd_dropout(q, k, v, out, dout, g, bits, rate, causal=False, scale=None, dq=None,
+                        dk=None, dv=None, workspace=None, stream=None):
+    """Gradients (dq, dk, dv) of sum(dout * O) for the forward with the same bits."""
+    import torch
+    B, H, N, D = q.shape
+    dt = _dtype_code(q)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    if workspace is None:
+        workspace = _alloc_ws(dropout_workspace_bytes(B, H, N, D, causal, dt, True), q.device)
+    ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = fastmax_bwd_dropout_raw(q, k, v, out, dout, g, bits, rate, dq, dk, dv, B, H, N, D,
+                                 causal, 1.0 if scale is None else scale, dt, workspace, ws_n,
+                                 stream)
+    if rc != OK:
+        raise FastmaxError(rc, "fastmax_bwd_dropout")
     return dq, dk, dv

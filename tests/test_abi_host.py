@@ -186,3 +186,80 @@ def test_scaled_entry_points_validate_the_rest():
     # causal bf16 D = 64 p = 2 needs a workspace (none given)
     assert fwd_scaled(0.5) == fm.EWORKSPACE
     assert bwd_scaled(0.5) == fm.EWORKSPACE
+
+
+# --------------------------------------------------------------------------
+# Quadratic-term dropout entry points
+# --------------------------------------------------------------------------
+def test_dropout_mask_words():
+    for D, nw in ((16, 5), (32, 17), (64, 65), (128, 258), (8, 0), (256, 0)):
+        assert fm.lib().fastmax_dropout_mask_words(D) == nw, D
+
+
+def test_dropout_workspace_is_the_float32_p2_one():
+    for B, H, N, D in ((1, 1, 700, 16), (4, 16, 8192, 64), (1, 8, 4096, 128)):
+        for causal in (0, 1):
+            for bwd in (0, 1):
+                a = fm.lib().fastmax_dropout_workspace_bytes(B, H, N, D, causal, fm.BF16, bwd)
+                b = fm.lib().fastmax_workspace_bytes(B, H, N, D, 2, causal, fm.F32, bwd)
+                assert a == b, (B, H, N, D, causal, bwd)
+
+
+def mask_call(bits=A, B=1, H=1, N=8, D=64, rate=0.1, seed=1):
+    return fm.lib().fastmax_dropout_mask(ctypes.c_void_p(bits) if bits else None, B, H, N, D,
+                                         ctypes.c_float(rate), ctypes.c_uint64(seed), None)
+
+
+def test_dropout_mask_rejects():
+    assert mask_call(rate=-0.1) == fm.EINVAL
+    assert mask_call(rate=1.0) == fm.EINVAL
+    assert mask_call(rate=float("nan")) == fm.EINVAL
+    assert mask_call(bits=None) == fm.ENULL
+    assert mask_call(bits=A + 2) == fm.EALIGN
+    assert mask_call(D=48) == fm.EUNSUPPORTED
+    assert mask_call(N=0) == fm.EINVAL
+
+
+def fwd_drop(ptrs=None, rate=0.1, B=1, H=1, N=8, D=64, causal=1, scale=1.0, dt=fm.BF16,
+             ws=None, wsb=0):
+    ptrs = ptrs or [A] * 6     # q, k, v, out, g, bits
+    cp = [ctypes.c_void_p(x) if x else None for x in ptrs]
+    return fm.lib().fastmax_fwd_dropout(*cp, ctypes.c_float(rate), B, H, N, D, causal,
+                                        ctypes.c_float(scale), dt,
+                                        ctypes.c_void_p(ws) if ws else None, wsb, None)
+
+
+def bwd_drop(ptrs=None, rate=0.1, B=1, H=1, N=8, D=64, causal=1, scale=1.0, dt=fm.BF16,
+             ws=None, wsb=0):
+    ptrs = ptrs or [A] * 10    # q, k, v, out, dout, g, bits, dq, dk, dv
+    cp = [ctypes.c_void_p(x) if x else None for x in ptrs]
+    return fm.lib().fastmax_bwd_dropout(*cp[:7], ctypes.c_float(rate), *cp[7:], B, H, N, D,
+                                        causal, ctypes.c_float(scale), dt,
+                                        ctypes.c_void_p(ws) if ws else None, wsb, None)
+
+
+def test_fwd_dropout_rejects():
+    for rate in (-1e-3, 1.0, float("nan")):
+        assert fwd_drop(rate=rate) == fm.EINVAL
+    assert fwd_drop(scale=0.0) == fm.EINVAL
+    assert fwd_drop(D=24) == fm.EUNSUPPORTED
+    assert fwd_drop(causal=2) == fm.EINVAL
+    assert fwd_drop(ptrs=[A, A, A, A, A, None]) == fm.ENULL
+    assert fwd_drop(ptrs=[A, A, A, A, A, A + 2]) == fm.EALIGN
+    assert fwd_drop(ptrs=[A, A, A + 8, A, A, A]) == fm.EALIGN
+    # few heads and many tokens: segment states, so a workspace is required
+    assert fwd_drop(N=100000, causal=1) == fm.EWORKSPACE
+
+
+def test_bwd_dropout_rejects():
+    assert bwd_drop(rate=1.5) == fm.EINVAL
+    for i in range(10):
+        ptrs = [A] * 10
+        ptrs[i] = None
+        assert bwd_drop(ptrs=ptrs) == fm.ENULL, i
+    ptrs = [A] * 10
+    ptrs[6] = A + 1
+    assert bwd_drop(ptrs=ptrs) == fm.EALIGN
+    assert bwd_drop() == fm.EWORKSPACE   # the backward always needs one
+    need = fm.lib().fastmax_dropout_workspace_bytes(1, 1, 8, 64, 1, fm.BF16, 1)
+    assert bwd_drop(ws=A, wsb=need - 1) == fm.EWORKSPACE
