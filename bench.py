@@ -78,11 +78,12 @@ def load_traffic(kernel, workload):
     return ent.get("bytes_per_launch")
 
 
-def cpu_baseline(w, inp_bits, scale=1.0, budget_s=12.0):
+def cpu_baseline(w, inp_bits, scale=1.0, budget_s=12.0, dropout=None):
     """The fp64 oracle (factorised form) on a bounded sample of the workload:
     the workload's own heads, in groups of one head per host thread (the
     oracle runs one head per thread), until the whole workload is done or
-    about budget_s seconds have passed."""
+    about budget_s seconds have passed.  With ``dropout`` the oracle's masked
+    factorised forward, its keep bits drawn (untimed) by the oracle."""
     import numpy as np
 
     import oracle
@@ -100,16 +101,23 @@ def cpu_baseline(w, inp_bits, scale=1.0, budget_s=12.0):
         q, k, v = (cut(inp_bits[n], sel) for n in ("q", "k", "v"))
         if first is None:
             first = (q, k, v)
-        t0 = time.perf_counter()
-        oracle.fwd_fact(q, k, v, w.p, w.causal, scale=scale)
+        if dropout is None:
+            t0 = time.perf_counter()
+            oracle.fwd_fact(q, k, v, w.p, w.causal, scale=scale)
+        else:
+            bits = oracle.dropout_mask(1, len(sel), w.N, w.D, float(np.float32(dropout)), done)
+            t0 = time.perf_counter()
+            oracle.fwd_drop_fact(q, k, v, bits, float(np.float32(dropout)), w.causal, scale=scale)
         dt += time.perf_counter() - t0
         done += len(sel)
     sample = (f"all {total} heads of the workload" if done == total
               else f"first {done} of the workload's {total} heads") + f" at full N={w.N}"
     rec = {"value": done * w.N / dt, "unit": "tokens*heads/s", "cores": group,
-           "kind": "oracle", "sample": sample + f" (fwd_fact, {dt:.1f} s)",
+           "kind": "oracle",
+           "sample": sample + (f" (fwd_fact, {dt:.1f} s)" if dropout is None
+                               else f" (fwd_drop_fact, {dt:.1f} s)"),
            "cpu_model": cpu_model()}
-    if w.N <= 4096:
+    if w.N <= 4096 and dropout is None:
         # the explicit N x N definition as well, on the first group
         t0 = time.perf_counter()
         oracle.fwd_brute(*first, w.p, w.causal, scale=scale)
@@ -144,6 +152,10 @@ def main():
     ap.add_argument("--qk-scale", type=float, default=None, metavar="TAU",
                     help="time the score-scaled entry points with weights f_p(TAU q^.k^) "
                          "(e.g. 1/D, the unit-norm variant); default: the plain entry points")
+    ap.add_argument("--dropout", type=float, default=None, metavar="RATE",
+                    help="time the quadratic-term dropout entry points: each step draws "
+                         "fresh keep bits (fastmax_dropout_mask) and runs the masked "
+                         "forward (and backward in --mode fwdbwd)")
     ap.add_argument("--cold", type=int, default=None, metavar="ITERS",
                     help="after the timed region, time ITERS calls each preceded by a "
                          "512 MiB write that flushes the caches (default 10 for the bf16 "
@@ -193,26 +205,56 @@ def main():
     out = torch.empty_like(q)
     g = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
     dt = fm.BF16 if w.dtype == "bf16" else fm.F32
-    need = fm.workspace_bytes(w.B, w.H, w.N, w.D, w.p, w.causal, dt, False)
+    drop = args.dropout
+    if drop is not None and w.p != 2:
+        print("--dropout needs a p = 2 workload (it masks the quadratic features)",
+              file=sys.stderr)
+        sys.exit(2)
+    if drop is None:
+        need = fm.workspace_bytes(w.B, w.H, w.N, w.D, w.p, w.causal, dt, False)
+    else:
+        need = fm.dropout_workspace_bytes(w.B, w.H, w.N, w.D, w.causal, dt, False)
+        bits = torch.empty((w.B, w.H, w.N, fm.mask_words(w.D)), dtype=torch.int32, device=dev)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
+    scale = 1.0 if args.qk_scale is None else args.qk_scale
 
     if args.mode == "fwdbwd":
-        need_b = fm.workspace_bytes(w.B, w.H, w.N, w.D, w.p, w.causal, dt, True)
+        if drop is None:
+            need_b = fm.workspace_bytes(w.B, w.H, w.N, w.D, w.p, w.causal, dt, True)
+        else:
+            need_b = fm.dropout_workspace_bytes(w.B, w.H, w.N, w.D, w.causal, dt, True)
         ws_b = torch.empty(max(need_b, 1), dtype=torch.uint8, device=dev)
         dq, dk, dv = (torch.empty_like(q) for _ in range(3))
     bwd_start = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    fwd_start = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
 
     def step(i=None):
-        rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
-                                need, stream, args.qk_scale)
+        if drop is not None:
+            # a training step draws fresh keep bits, then runs the masked calls
+            rc = fm.fastmax_dropout_mask_raw(bits, w.B, w.H, w.N, w.D, drop,
+                                             0x5EED0000 + (i or 0), stream)
+            if rc != fm.OK:
+                raise fm.FastmaxError(rc, "fastmax_dropout_mask")
+            if i is not None:
+                fwd_start[i].record(stream)
+            rc = fm.fastmax_fwd_dropout_raw(q, k, v, out, g, bits, drop, w.B, w.H, w.N, w.D,
+                                            w.causal, scale, dt, ws, need, stream)
+        else:
+            rc = fm.fastmax_fwd_raw(q, k, v, out, g, w.B, w.H, w.N, w.D, w.p, w.causal, dt, ws,
+                                    need, stream, args.qk_scale)
         if rc != fm.OK:
             raise fm.FastmaxError(rc, "fastmax_fwd")
         if args.mode == "fwdbwd":
             if i is not None:
                 bwd_start[i].record(stream)
-            rc = fm.fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, w.B, w.H, w.N, w.D, w.p,
-                                    w.causal, dt, ws_b, need_b, stream, args.qk_scale)
+            if drop is not None:
+                rc = fm.fastmax_bwd_dropout_raw(q, k, v, out, dout, g, bits, drop, dq, dk, dv,
+                                                w.B, w.H, w.N, w.D, w.causal, scale, dt, ws_b,
+                                                need_b, stream)
+            else:
+                rc = fm.fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, w.B, w.H, w.N, w.D,
+                                        w.p, w.causal, dt, ws_b, need_b, stream, args.qk_scale)
             if rc != fm.OK:
                 raise fm.FastmaxError(rc, "fastmax_bwd")
 
@@ -230,12 +272,15 @@ def main():
         stops[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    fstarts = fwd_start if drop is not None else starts
+    if drop is not None:
+        mask_ms = [s.elapsed_time(e) for s, e in zip(starts, fwd_start)]
     if args.mode == "fwdbwd":
-        fwd_ms = [s.elapsed_time(e) for s, e in zip(starts, bwd_start)]
+        fwd_ms = [s.elapsed_time(e) for s, e in zip(fstarts, bwd_start)]
         bwd_ms = [s.elapsed_time(e) for s, e in zip(bwd_start, stops)]
         launch_ms = fwd_ms
     else:
-        launch_ms = [s.elapsed_time(e) for s, e in zip(starts, stops)]
+        launch_ms = [s.elapsed_time(e) for s, e in zip(fstarts, stops)]
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
     ms_per_step = wall / args.steps * 1e3
 
@@ -243,7 +288,7 @@ def main():
     value = tokens_heads / (ms_per_step / 1e3)
     flops = fwd_flops(w.B, w.H, w.N, w.D, w.p)
     kernel = "fastmax_fwd"
-    if w.p == 2 and w.dtype == "bf16" and w.D == 64:
+    if w.p == 2 and w.dtype == "bf16" and w.D == 64 and drop is None:
         bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "bf16")]
         achieved = flops / avg_launch_s / 1e12
     elif w.p == 2:
@@ -257,8 +302,9 @@ def main():
         achieved = tokens_heads * (4 * w.D * elt + 4) / avg_launch_s / 1e9
 
     rec = {
-        "metric": METRIC if (w.name == "gpt_causal_bf16" and args.mode == "fwd") else
-                  f"Fastmax {args.mode} tokens·heads/s on 1 GPU ({w.name})",
+        "metric": METRIC if (w.name == "gpt_causal_bf16" and args.mode == "fwd" and drop is None)
+                  else f"Fastmax {args.mode} tokens·heads/s on 1 GPU ({w.name}"
+                       + ("" if drop is None else f", quadratic dropout {drop}") + ")",
         "value": value,
         "unit": "tokens*heads/s",
         "n_gpus": 1,
@@ -273,7 +319,8 @@ def main():
         "config": {"workload": w.name, "mode": args.mode, "B": w.B, "H": w.H, "N": w.N,
                    "D": w.D, "p": w.p, "causal": w.causal, "io_dtype": w.dtype,
                    "global_batch": w.B, "seq_len": w.N, "parallelism": "none (1 GPU)",
-                   "qk_scale": 1.0 if args.qk_scale is None else args.qk_scale},
+                   "qk_scale": 1.0 if args.qk_scale is None else args.qk_scale,
+                   "dropout": drop},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": load_traffic(kernel, w.name),
                      "kernel": kernel, "avg_launch_ms": avg_launch_s * 1e3,
@@ -284,7 +331,13 @@ def main():
         bf = bwd_flops(w.B, w.H, w.N, w.D, w.p)
         rec["backward"] = {"avg_ms": bms,
                            "note": "fastmax_bwd call (all its kernels), HIP events on the stream"}
-        if bf is not None and w.dtype == "bf16" and w.D == 64:
+        if bf is not None and drop is not None:
+            ach = bf / (bms / 1e3) / 1e12
+            rec["backward"].update({"algorithmic_flops_per_call": bf, "achieved": ach,
+                                    "unit": "TFLOP/s", "bound": "alu",
+                                    "peak": PEAK[("alu", "f32")],
+                                    "frac": ach / PEAK[("alu", "f32")], "traffic": None})
+        elif bf is not None and w.dtype == "bf16" and w.D == 64:
             ach = bf / (bms / 1e3) / 1e12
             rec["backward"].update({"algorithmic_flops_per_call": bf, "achieved": ach,
                                     "unit": "TFLOP/s", "bound": "mfma",
@@ -292,11 +345,19 @@ def main():
                                     "frac": ach / PEAK[("mfma", "bf16")],
                                     "traffic": load_traffic("fastmax_bwd", w.name)})
     rec["roofline"]["median_launch_ms"] = float(np.median(launch_ms))
+    if drop is not None:
+        # the generator's cost per step (its own kernel), beside the forward
+        mw = fm.mask_words(w.D)
+        mms = sum(mask_ms) / len(mask_ms)
+        rec["dropout_mask"] = {"avg_ms": mms, "words": w.B * w.H * w.N * mw,
+                               "written_GBps": w.B * w.H * w.N * mw * 4 / (mms / 1e3) / 1e9}
+        rec["roofline"]["traffic"] = None
     if args.mode == "fwdbwd":
         rec["backward"]["median_ms"] = float(np.median(bwd_ms))
 
     # cold calls: caches flushed by a 512 MiB write before each one
-    cold = args.cold if args.cold is not None else (10 if w.dtype == "bf16" and w.p == 2 else 0)
+    cold = args.cold if args.cold is not None else (
+        10 if w.dtype == "bf16" and w.p == 2 and drop is None else 0)
     if args.timed_only:
         cold = 0
     if cold > 0:
@@ -332,7 +393,7 @@ def main():
 
     # linear in N (long non-causal workload): the same recipe at N = 8192
     if (not w.causal and w.N > 8192 and w.dtype == "bf16" and w.p == 2 and args.mode == "fwd"
-            and not args.timed_only):
+            and not args.timed_only and drop is None):
         n_s = 8192
         inp_s = workload_inputs(w, want64=False, N=n_s)
         qs, ks, vs = (to_dev(inp_s[n]) for n in ("q", "k", "v"))
@@ -358,7 +419,8 @@ def main():
                               "full_median_ms": t_f, "ratio": t_f / t_s,
                               "ideal": w.N / n_s}
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, inp, 1.0 if args.qk_scale is None else args.qk_scale)
+        rec["cpu_baseline"] = cpu_baseline(w, inp, 1.0 if args.qk_scale is None else args.qk_scale,
+                                           dropout=drop)
     print(json.dumps(rec), flush=True)
 
 

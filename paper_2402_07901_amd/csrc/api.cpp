@@ -171,7 +171,7 @@ size_t fastmax_dropout_workspace_bytes(int B, int H, int N, int D, int causal,
 {
     if (check_common(B, H, N, D, 2, causal, dt) != FASTMAX_OK) return 0;
     return backward ? fm::generic_bwd_workspace(B, H, N, D, 2)
-                    : fm::generic_fwd_workspace(B * H, N, D, 2);
+                    : fm::generic_fwd_dropout_workspace(B * H, N, D, causal);
 }
 
 int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
@@ -186,7 +186,7 @@ int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, 
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
         (g && !aligned16(g)) || !aligned4(keep_bits))
         return FASTMAX_EALIGN;
-    size_t need = fm::generic_fwd_workspace(B * H, N, D, 2);
+    size_t need = fm::generic_fwd_dropout_workspace(B * H, N, D, causal);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
     hipError_t e = fm::generic_fwd_dropout(q, k, v, out, g, B * H, N, D, causal,

@@ -30,9 +30,13 @@ constexpr int NT = 256;   // threads per workgroup
 
 // Dropout arguments: keep bits ([B*H][N][mask_words(D)] words) and the scale
 // 1/(1 - rate) of a kept feature.  bits == nullptr in the plain kernels.
+// wblk (causal forward only): the masked in-chunk weights of every chunk,
+// [B*H][chunks][CH][CH], written once per head by drop_wblk_kernel and read
+// by every column slice.
 struct Drop {
     const uint32_t *bits;
     float inv;
+    const float *wblk;
 };
 
 // Multiplier of quadratic feature t of the token whose bit row is `row`.
@@ -209,6 +213,27 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
     constexpr int NW = mask_words(D);
     const int r = threadIdx.x % CH, ag = threadIdx.x / CH;
     const float *xr = x + r * DP;
+    if constexpr (DROP) {
+        // the keep multiplier of feature (a, m) is read once for all WS columns
+        const uint32_t *row = mrow + (r < nvalid ? r : 0) * NW;
+        for (int a = ag; a < D; a += AG) {
+            float inner[WS];
+#pragma unroll
+            for (int j = 0; j < WS; ++j) inner[j] = S[(1 + a) * WS + j];
+            for (int m = 0; m < D; ++m) {
+                const int lo = m < a ? m : a, hi = m < a ? a : m;
+                const int pf = pair_feature(D, lo, hi);
+                const float xm = r < nvalid ? xr[m] * keep_mult(row, pf - 1 - D, inv) : 0.0f;
+#pragma unroll
+                for (int j = 0; j < WS; ++j) inner[j] = fmaf(xm, S[pf * WS + j], inner[j]);
+            }
+            float acc = 0.0f;
+#pragma unroll
+            for (int j = 0; j < WS; ++j) acc = fmaf(coef[r * WS + j], inner[j], acc);
+            out[r * D + a] = acc;
+        }
+        return;
+    }
     for (int a = ag; a < D; a += AG) {
         float acc = 0.0f;
         for (int j = 0; j < WS; ++j) {
@@ -216,11 +241,7 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
             if (P2) {
                 for (int m = 0; m < D; ++m) {
                     int lo = m < a ? m : a, hi = m < a ? a : m;
-                    const int pf = pair_feature(D, lo, hi);
-                    float xm = xr[m];
-                    if constexpr (DROP)
-                        xm *= r < nvalid ? keep_mult(mrow + r * NW, pf - 1 - D, inv) : 0.0f;
-                    inner = fmaf(xm, S[pf * WS + j], inner);
+                    inner = fmaf(xr[m], S[pair_feature(D, lo, hi) * WS + j], inner);
                 }
             }
             acc = fmaf(coef[r * WS + j], inner, acc);
@@ -265,6 +286,29 @@ __device__ float drop_h(const float *xq, const float *xk, const uint32_t *row, i
     return fmaf(acc, inv, 1.0f);
 }
 
+// Masked in-chunk weights of the causal forward, once per (head, chunk):
+// out[i][t] = w_it for t <= i < rows left, else 0.  grid = (B*H, chunks).
+template <int D, typename T>
+__global__ __launch_bounds__(NT) void drop_wblk_kernel(const T *__restrict__ q,
+                                                       const T *__restrict__ k,
+                                                       float *__restrict__ wblk, int N,
+                                                       float qs, Drop dr)
+{
+    constexpr int DP = D + 1;
+    __shared__ float xq[CH * DP];
+    __shared__ float xk[CH * DP];
+    const int head = blockIdx.x, c = blockIdx.y, n0 = c * CH;
+    const size_t hb = (size_t)head * N * D;
+    load_std<D>(q + hb, n0, N, xq, nullptr, qs);
+    load_std<D>(k + hb, n0, N, xk, nullptr);
+    const int i = threadIdx.x / CH, t = threadIdx.x % CH;
+    float w = 0.0f;
+    // keys past N are never seen by a valid row (t <= i < N)
+    if (t <= i && n0 + i < N)
+        w = drop_weight<D>(xq + i * DP, xk + t * DP, mask_rows<D>(dr, head, N, n0 + t), dr.inv);
+    wblk[((size_t)head * gridDim.y + c) * (CH * CH) + threadIdx.x] = w;
+}
+
 // ---------------------------------------------------------------------------
 // Forward.  grid = (B*H, slices, segments); slice s owns value columns
 // [s*W, s*W+W) plus the ones column (local index W), so every slice has G for
@@ -278,7 +322,7 @@ template <int D, bool P2, int WS, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
                                                        const T *__restrict__ v,
                                                        float *__restrict__ sseg, int N, int cps,
-                                                       Drop dr = Drop{nullptr, 1.0f})
+                                                       Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -359,7 +403,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
                                                  const T *__restrict__ v, T *__restrict__ out,
                                                  float *__restrict__ g, int N, int cps,
                                                  const float *__restrict__ sseg, float qs,
-                                                 Drop dr = Drop{nullptr, 1.0f})
+                                                 Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -457,10 +501,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
                 int i = threadIdx.x / CH, t = threadIdx.x % CH;
                 float w = 0.0f;
                 if constexpr (DROP) {
-                    // keys past N are never seen by a valid row (t <= i < N)
-                    if (t <= i && n0 + i < N)
-                        w = drop_weight<D>(xq + i * DP, xk + t * DP,
-                                           mask_rows<D>(dr, head, N, n0 + t), dr.inv);
+                    w = dr.wblk[((size_t)head * nch + c) * (CH * CH) + i * CH + t];
                 } else if (t <= i) {
                     float s = 0.0f;
                     for (int d = 0; d < D; ++d) s = fmaf(xq[i * DP + d], xk[t * DP + d], s);
@@ -552,7 +593,7 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
     float *__restrict__ dqh, float *__restrict__ dkh, float *__restrict__ dva, int N, float qs,
-    Drop dr = Drop{nullptr, 1.0f})
+    Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int DP = D + 1;
     constexpr int D1 = D + 1;
@@ -646,7 +687,7 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
     float *__restrict__ dqh, int N, float qs, const float *__restrict__ sseg, int cps,
-    Drop dr = Drop{nullptr, 1.0f})
+    Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -724,7 +765,7 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
     float *__restrict__ dkh, float *__restrict__ dva, int N, float qs,
-    const float *__restrict__ sseg, int cps, Drop dr = Drop{nullptr, 1.0f})
+    const float *__restrict__ sseg, int cps, Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -810,7 +851,7 @@ template <int D, bool P2, int WS, int SIDE, typename T, bool DROP = false>
 __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ g, const float *__restrict__ cvec,
-    float *__restrict__ sseg, int N, float qs, int cps, Drop dr = Drop{nullptr, 1.0f})
+    float *__restrict__ sseg, int N, float qs, int cps, Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int NPAIR = feat<D, P2>::NPAIR;
@@ -936,7 +977,7 @@ SegPlan seg_plan(int BH, int N)
 template <int D, bool P2, typename T, bool DROP = false>
 static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void *out, float *g,
                                int BH, int N, int causal, float qs, void *ws, hipStream_t st,
-                               Drop dr = Drop{nullptr, 1.0f})
+                               Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int WS = slice_width<D, P2>::v;
     const SegPlan sp = seg_plan<D, P2>(BH, N);
@@ -957,6 +998,18 @@ static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void
                                sp.nseg);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
+    }
+    if constexpr (DROP) {
+        if (causal) {
+            // after the segment states in the workspace, 256-byte aligned
+            const size_t off = (sp.bytes + 255) & ~(size_t)255;
+            float *wb = (float *)((char *)ws + off);
+            hipLaunchKernelGGL((drop_wblk_kernel<D, T>), dim3(BH, (N + CH - 1) / CH), dim3(NT), 0,
+                               st, (const T *)q, (const T *)k, wb, N, qs, dr);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            dr.wblk = wb;
+        }
     }
     if (causal)
         hipLaunchKernelGGL((fwd_kernel<D, P2, WS, true, T, DROP>), grid, dim3(NT), 0, st,
@@ -999,7 +1052,7 @@ template <int D, bool P2, bool CAUSAL, typename T, bool DROP = false>
 static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, const void *o,
                                 const void *dout, const float *g, void *dq, void *dk, void *dv,
                                 int BH, int N, float qs, float *ws, hipStream_t st,
-                                Drop dr = Drop{nullptr, 1.0f})
+                                Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int WS = slice_width<D, P2>::v;
     constexpr int PWS = feat<D, P2>::P * WS;
@@ -1128,7 +1181,7 @@ static hipError_t drop_fwd_t(const void *q, const void *k, const void *v, void *
                              float inv, void *ws, hipStream_t st)
 {
     using namespace generic;
-    const Drop dr{bits, inv};
+    const Drop dr{bits, inv, nullptr};
     switch (D) {
     case 16: return fwd_dispatch<16, true, T, true>(q, k, v, out, g, BH, N, causal, qs, ws, st, dr);
     case 32: return fwd_dispatch<32, true, T, true>(q, k, v, out, g, BH, N, causal, qs, ws, st, dr);
@@ -1157,13 +1210,22 @@ static hipError_t drop_bwd_t(const void *q, const void *k, const void *v, const 
                              int BH, int N, int D, int causal, float qs, const uint32_t *bits,
                              float inv, float *ws, hipStream_t st)
 {
-    const generic::Drop dr{bits, inv};
+    const generic::Drop dr{bits, inv, nullptr};
     switch (D) {
     case 16: return drop_bwd_d<16, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
     case 32: return drop_bwd_d<32, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
     case 64: return drop_bwd_d<64, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
     default: return drop_bwd_d<128, T>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st, dr);
     }
+}
+
+size_t generic_fwd_dropout_workspace(int BH, int N, int D, int causal)
+{
+    const size_t seg = generic_fwd_workspace(BH, N, D, 2);
+    if (!causal) return seg;
+    const size_t nch = ((size_t)N + generic::CH - 1) / generic::CH;
+    return ((seg + 255) & ~(size_t)255) +
+           (size_t)BH * nch * generic::CH * generic::CH * sizeof(float);
 }
 
 hipError_t generic_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,

@@ -23,8 +23,8 @@ hipError_t generic_bwd(const void *q, const void *k, const void *v, const void *
 size_t generic_bwd_workspace(int B, int H, int N, int D, int p);
 
 // Quadratic-term dropout (p = 2) on the generic kernels: bits are the keep
-// bits ([BH][N][mask_words(D)] words), inv = 1 / (1 - rate).  Workspaces as
-// generic_fwd_workspace / generic_bwd_workspace with p = 2.
+// bits ([BH][N][mask_words(D)] words), inv = 1 / (1 - rate).  Workspaces:
+// generic_fwd_dropout_workspace and generic_bwd_workspace with p = 2.
 hipError_t generic_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
                                int BH, int N, int D, int causal, int is_bf16, float qs,
                                const uint32_t *bits, float inv, void *ws, hipStream_t st);
@@ -32,6 +32,9 @@ hipError_t generic_bwd_dropout(const void *q, const void *k, const void *v, cons
                                const void *dout, const float *g, void *dq, void *dk, void *dv,
                                int BH, int N, int D, int causal, int is_bf16, float qs,
                                const uint32_t *bits, float inv, void *ws, hipStream_t st);
+// Dropout forward workspace: the p = 2 segment states and, causal, the masked
+// in-chunk weights (64 bytes per token).
+size_t generic_fwd_dropout_workspace(int BH, int N, int D, int causal);
 // Philox4x32-10 keep bits for BH heads of N tokens; a feature is kept iff its
 // generator word is >= thr.
 hipError_t dropout_mask(uint32_t *bits, int BH, int N, int D, uint32_t thr, uint64_t seed,

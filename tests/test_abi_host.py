@@ -196,12 +196,17 @@ def test_dropout_mask_words():
         assert fm.lib().fastmax_dropout_mask_words(D) == nw, D
 
 
-def test_dropout_workspace_is_the_float32_p2_one():
-    for B, H, N, D in ((1, 1, 700, 16), (4, 16, 8192, 64), (1, 8, 4096, 128)):
+def test_dropout_workspace():
+    """Backward and non-causal forward: the float32 kernels' p = 2 workspace;
+    causal forward: that (256-byte aligned) plus the masked in-chunk weights,
+    16 x 16 floats per chunk of 16 tokens."""
+    for B, H, N, D in ((1, 1, 700, 16), (4, 16, 8192, 64), (1, 8, 4096, 128), (2, 3, 33, 32)):
         for causal in (0, 1):
             for bwd in (0, 1):
                 a = fm.lib().fastmax_dropout_workspace_bytes(B, H, N, D, causal, fm.BF16, bwd)
                 b = fm.lib().fastmax_workspace_bytes(B, H, N, D, 2, causal, fm.F32, bwd)
+                if causal and not bwd:
+                    b = (b + 255) // 256 * 256 + B * H * ((N + 15) // 16) * 16 * 16 * 4
                 assert a == b, (B, H, N, D, causal, bwd)
 
 
@@ -248,7 +253,9 @@ def test_fwd_dropout_rejects():
     assert fwd_drop(ptrs=[A, A, A, A, A, A + 2]) == fm.EALIGN
     assert fwd_drop(ptrs=[A, A, A + 8, A, A, A]) == fm.EALIGN
     # few heads and many tokens: segment states, so a workspace is required
-    assert fwd_drop(N=100000, causal=1) == fm.EWORKSPACE
+    assert fwd_drop(N=100000, causal=0) == fm.EWORKSPACE
+    # causal: the masked in-chunk weights always need one
+    assert fwd_drop(N=8, causal=1) == fm.EWORKSPACE
 
 
 def test_bwd_dropout_rejects():
