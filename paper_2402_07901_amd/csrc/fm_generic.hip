@@ -52,44 +52,51 @@ __device__ __forceinline__ const uint32_t *mask_rows(const Drop &dr, int head, i
     return dr.bits + ((size_t)head * N + n0) * mask_words(D);
 }
 
+// Copies the bit rows of the chunk starting at token n0 into LDS (rows past
+// N are zero), so the kernels read every bit from LDS.  Callers synchronise.
+template <int D>
+__device__ __forceinline__ void stage_mask(uint32_t *mk, const Drop &dr, int head, int N, int n0)
+{
+    constexpr int NW = mask_words(D);
+    const uint32_t *src = mask_rows<D>(dr, head, N, n0);
+    const int nv = min(CH, N - n0) * NW;
+    for (int e = threadIdx.x; e < CH * NW; e += NT) mk[e] = e < nv ? src[e] : 0u;
+}
+
 template <int D, bool P2> struct feat {
     static constexpr int P = n_features(D, P2 ? 2 : 1);
     static constexpr int NPAIR = P2 ? D * (D + 1) / 2 : 0;
 };
 
-// Builds the (m, l) table of the quadratic features in LDS.
+// Feature table in LDS: phi_f(x) = x[fa[f]] * x[fb[f]], where every staged
+// row carries x[D] = 1 (load_std writes it into the padding column): f = 0 is
+// (D, D), the linear feature f = 1 + m is (m, D), the quadratic feature of
+// the pair (m, l), m <= l, is (m, l) (m-major order).  Branch-free in the
+// feature index.
 template <int D, bool P2>
-__device__ void build_pairs(uint8_t *pm, uint8_t *pl)
+__device__ void build_features(uint8_t *fa, uint8_t *fb)
 {
-    constexpr int NPAIR = feat<D, P2>::NPAIR;
-    for (int t = threadIdx.x; t < NPAIR; t += NT) {
-        int m = 0, r = t;
-        while (r >= D - m) { r -= D - m; ++m; }
-        pm[t] = (uint8_t)m;
-        pl[t] = (uint8_t)(m + r);
+    constexpr int P = feat<D, P2>::P;
+    for (int f = threadIdx.x; f < P; f += NT) {
+        int a = D, b = D;
+        if (f >= 1 && f <= D) {
+            a = f - 1;
+        } else if (f > D) {
+            int m = 0, r = f - 1 - D;
+            while (r >= D - m) { r -= D - m; ++m; }
+            a = m;
+            b = m + r;
+        }
+        fa[f] = (uint8_t)a;
+        fb[f] = (uint8_t)b;
     }
 }
 
-// Key-side feature phi_f of a standardised row x (LDS).
+// Query-side factor of feature (a, b): 1/2 on the diagonal pairs, else 1.
 template <int D>
-__device__ __forceinline__ float phi(int f, const float *x, const uint8_t *pm, const uint8_t *pl)
+__device__ __forceinline__ float psi_coef(int a, int b)
 {
-    if (f == 0) return 1.0f;
-    if (f <= D) return x[f - 1];
-    int t = f - 1 - D;
-    return x[pm[t]] * x[pl[t]];
-}
-
-// Query-side feature psi_f (carries the 1/2 of the diagonal pairs).
-template <int D>
-__device__ __forceinline__ float psi(int f, const float *x, const uint8_t *pm, const uint8_t *pl)
-{
-    if (f == 0) return 1.0f;
-    if (f <= D) return x[f - 1];
-    int t = f - 1 - D;
-    int m = pm[t], l = pl[t];
-    float v = x[m] * x[l];
-    return m == l ? 0.5f * v : v;
+    return (a == b && a < D) ? 0.5f : 1.0f;
 }
 
 // Loads `rows` token rows starting at token n0 of a head and standardises
@@ -140,29 +147,34 @@ __device__ void load_std(const T *src, int n0, int N, float *dst, float *rstd_ou
         } else if (rstd_out && l == 0) {
             rstd_out[r] = 0.0f;
         }
+        if (l == 0) x[D] = 1.0f;   // the constant of the feature table
     }
     __syncthreads();
 }
 
 // S[f][j] += sum_{r < CH} phi_f(x_r) val[r][j], j < WS.  DROP: the
 // quadratic features of row r < nvalid are multiplied by the keep bits of
-// its row in mrow (rows past nvalid are past N and carry zero values).
+// its row in mrow (the chunk's rows staged in LDS by stage_mask).
 template <int D, bool P2, int WS, bool DROP = false>
-__device__ void state_update(float *S, const float *x, const float *val, const uint8_t *pm,
-                             const uint8_t *pl, const uint32_t *mrow = nullptr, int nvalid = 0,
+__device__ void state_update(float *S, const float *x, const float *val, const uint8_t *fa,
+                             const uint8_t *fb, const uint32_t *mrow = nullptr, int nvalid = 0,
                              float inv = 1.0f)
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int DP = D + 1;
     constexpr int NW = mask_words(D);
     for (int f = threadIdx.x; f < P; f += NT) {
+        const int a = fa[f], b = fb[f];
+        const bool quad = f > D;
+        const int t = quad ? f - 1 - D : 0;
         float acc[WS];
 #pragma unroll
         for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
         for (int r = 0; r < CH; ++r) {
-            float ph = phi<D>(f, x + r * DP, pm, pl);
+            float ph = x[r * DP + a] * x[r * DP + b];
             if constexpr (DROP) {
-                if (f > D) ph *= r < nvalid ? keep_mult(mrow + r * NW, f - 1 - D, inv) : 0.0f;
+                const float km = r < nvalid ? keep_mult(mrow + r * NW, t, inv) : 0.0f;
+                ph *= quad ? km : 1.0f;
             }
 #pragma unroll
             for (int j = 0; j < WS; ++j) acc[j] = fmaf(ph, val[r * WS + j], acc[j]);
@@ -175,8 +187,8 @@ __device__ void state_update(float *S, const float *x, const float *val, const u
 // out[r][j] += sum_f psi_f(x_r) S[f][j]   (LDS atomics; out is CH x WS).
 // DROP: x holds keys, whose quadratic features take their keep bits.
 template <int D, bool P2, int WS, bool DROP = false>
-__device__ void contract_psi(const float *S, const float *x, float *out, const uint8_t *pm,
-                             const uint8_t *pl, const uint32_t *mrow = nullptr, int nvalid = 0,
+__device__ void contract_psi(const float *S, const float *x, float *out, const uint8_t *fa,
+                             const uint8_t *fb, const uint32_t *mrow = nullptr, int nvalid = 0,
                              float inv = 1.0f)
 {
     constexpr int P = feat<D, P2>::P;
@@ -187,10 +199,14 @@ __device__ void contract_psi(const float *S, const float *x, float *out, const u
     float acc[WS];
 #pragma unroll
     for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
+    const float *xr = x + r * DP;
     for (int f = fg; f < P; f += NG) {
-        float ps = psi<D>(f, x + r * DP, pm, pl);
+        const int a = fa[f], b = fb[f];
+        float ps = psi_coef<D>(a, b) * (xr[a] * xr[b]);
         if constexpr (DROP) {
-            if (f > D) ps *= r < nvalid ? keep_mult(mrow + r * NW, f - 1 - D, inv) : 0.0f;
+            const bool quad = f > D;
+            const float km = r < nvalid ? keep_mult(mrow + r * NW, quad ? f - 1 - D : 0, inv) : 0.0f;
+            ps *= quad ? km : 1.0f;
         }
 #pragma unroll
         for (int j = 0; j < WS; ++j) acc[j] = fmaf(ps, S[f * WS + j], acc[j]);
@@ -297,15 +313,17 @@ __global__ __launch_bounds__(NT) void drop_wblk_kernel(const T *__restrict__ q,
     constexpr int DP = D + 1;
     __shared__ float xq[CH * DP];
     __shared__ float xk[CH * DP];
+    __shared__ uint32_t mk[CH * mask_words(D)];
     const int head = blockIdx.x, c = blockIdx.y, n0 = c * CH;
     const size_t hb = (size_t)head * N * D;
-    load_std<D>(q + hb, n0, N, xq, nullptr, qs);
+    stage_mask<D>(mk, dr, head, N, n0);
+    load_std<D>(q + hb, n0, N, xq, nullptr, qs);   // synchronises the staging too
     load_std<D>(k + hb, n0, N, xk, nullptr);
     const int i = threadIdx.x / CH, t = threadIdx.x % CH;
     float w = 0.0f;
     // keys past N are never seen by a valid row (t <= i < N)
     if (t <= i && n0 + i < N)
-        w = drop_weight<D>(xq + i * DP, xk + t * DP, mask_rows<D>(dr, head, N, n0 + t), dr.inv);
+        w = drop_weight<D>(xq + i * DP, xk + t * DP, mk + t * mask_words(D), dr.inv);
     wblk[((size_t)head * gridDim.y + c) * (CH * CH) + threadIdx.x] = w;
 }
 
@@ -325,22 +343,22 @@ __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
                                                        Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
-    constexpr int NPAIR = feat<D, P2>::NPAIR;
     constexpr int W = WS - 1;
     constexpr int DP = D + 1;
 
     __shared__ float S[P * WS];
     __shared__ float xk[CH * DP];
     __shared__ float vv[CH * WS];
-    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
-    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t fa[P];
+    __shared__ uint8_t fb[P];
+    __shared__ uint32_t mk[DROP ? CH * mask_words(D) : 1];
 
     const int head = blockIdx.x, c0 = blockIdx.y * W, seg = blockIdx.z;
     const size_t hb = (size_t)head * N * D;
     k += hb;
     v += hb;
     for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
-    build_pairs<D, P2>(pm, pl);
+    build_features<D, P2>(fa, fb);
     __syncthreads();
     const int nch = (N + CH - 1) / CH;
     const int cb = seg * cps, ce = min(nch, cb + cps);
@@ -355,12 +373,12 @@ __global__ __launch_bounds__(NT) void seg_state_kernel(const T *__restrict__ k,
             }
             vv[e] = x;
         }
+        if constexpr (DROP) stage_mask<D>(mk, dr, head, N, c * CH);
         __syncthreads();
         if constexpr (DROP)
-            state_update<D, P2, WS, true>(S, xk, vv, pm, pl, mask_rows<D>(dr, head, N, c * CH),
-                                          min(CH, N - c * CH), dr.inv);
+            state_update<D, P2, WS, true>(S, xk, vv, fa, fb, mk, CH, dr.inv);
         else
-            state_update<D, P2, WS>(S, xk, vv, pm, pl);
+            state_update<D, P2, WS>(S, xk, vv, fa, fb);
         __syncthreads();
     }
     float *dst = sseg + (((size_t)head * gridDim.y + blockIdx.y) * gridDim.z + seg) * P * WS;
@@ -406,7 +424,6 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
                                                  Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
-    constexpr int NPAIR = feat<D, P2>::NPAIR;
     constexpr int W = WS - 1;
     constexpr int DP = D + 1;
     constexpr int POW = P2 ? 2 : 1;
@@ -417,8 +434,9 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
     __shared__ float vv[CH * WS];
     __shared__ float wblk[CH * CH];
     __shared__ float F[CH * WS];
-    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
-    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t fa[P];
+    __shared__ uint8_t fb[P];
+    __shared__ uint32_t mk[DROP ? CH * mask_words(D) : 1];
 
     const int head = blockIdx.x;
     const int c0 = blockIdx.y * W;
@@ -439,7 +457,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
                                 : nullptr;
         for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = src ? src[e] : 0.0f;
     }
-    build_pairs<D, P2>(pm, pl);
+    build_features<D, P2>(fa, fb);
     __syncthreads();
 
     auto load_vals = [&](int n0) {
@@ -471,13 +489,12 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             for (int c = 0; c < nch; ++c) {
                 load_std<D>(k, c * CH, N, xk, nullptr);
                 load_vals(c * CH);
+                if constexpr (DROP) stage_mask<D>(mk, dr, head, N, c * CH);
                 __syncthreads();
                 if constexpr (DROP)
-                    state_update<D, P2, WS, true>(S, xk, vv, pm, pl,
-                                                  mask_rows<D>(dr, head, N, c * CH),
-                                                  min(CH, N - c * CH), dr.inv);
+                    state_update<D, P2, WS, true>(S, xk, vv, fa, fb, mk, CH, dr.inv);
                 else
-                    state_update<D, P2, WS>(S, xk, vv, pm, pl);
+                    state_update<D, P2, WS>(S, xk, vv, fa, fb);
                 __syncthreads();
             }
         }
@@ -485,7 +502,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             load_std<D>(q, c * CH, N, xq, nullptr, qs);
             for (int e = threadIdx.x; e < CH * WS; e += NT) F[e] = 0.0f;
             __syncthreads();
-            contract_psi<D, P2, WS>(S, xq, F, pm, pl);
+            contract_psi<D, P2, WS>(S, xq, F, fa, fb);
             __syncthreads();
             write_out(c * CH);
             __syncthreads();
@@ -496,6 +513,7 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
             load_std<D>(q, n0, N, xq, nullptr, qs);
             load_std<D>(k, n0, N, xk, nullptr);
             load_vals(n0);
+            if constexpr (DROP) stage_mask<D>(mk, dr, head, N, n0);
             // in-chunk tril block of weights
             {
                 int i = threadIdx.x / CH, t = threadIdx.x % CH;
@@ -517,14 +535,13 @@ __global__ __launch_bounds__(NT) void fwd_kernel(const T *__restrict__ q, const 
                 F[e] = acc;
             }
             __syncthreads();
-            contract_psi<D, P2, WS>(S, xq, F, pm, pl);   // exclusive prefix S_<c
+            contract_psi<D, P2, WS>(S, xq, F, fa, fb);   // exclusive prefix S_<c
             __syncthreads();
             write_out(n0);
             if constexpr (DROP)
-                state_update<D, P2, WS, true>(S, xk, vv, pm, pl, mask_rows<D>(dr, head, N, n0),
-                                              min(CH, N - n0), dr.inv);
+                state_update<D, P2, WS, true>(S, xk, vv, fa, fb, mk, CH, dr.inv);
             else
-                state_update<D, P2, WS>(S, xk, vv, pm, pl);
+                state_update<D, P2, WS>(S, xk, vv, fa, fb);
             __syncthreads();
         }
     }
@@ -628,11 +645,7 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     load_std<D>(k, n0, N, xk, nullptr);
     load_vprime<D, D1>(v, n0, N, 0, vp);
     load_utilde<D, D1>(dout, g, cvec, n0, N, 0, ut);
-    if constexpr (DROP) {
-        const uint32_t *src = mask_rows<D>(dr, head, N, n0);
-        const int nv = min(CH, N - n0) * NW;
-        for (int e = threadIdx.x; e < CH * NW; e += NT) mk[e] = e < nv ? src[e] : 0u;
-    }
+    if constexpr (DROP) stage_mask<D>(mk, dr, head, N, n0);
     __syncthreads();
     {
         int i = threadIdx.x / CH, t = threadIdx.x % CH;
@@ -690,7 +703,6 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
-    constexpr int NPAIR = feat<D, P2>::NPAIR;
     constexpr int DP = D + 1;
     __shared__ float S[P * WS];
     __shared__ float xq[CH * DP];
@@ -698,8 +710,9 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     __shared__ float vp[CH * WS];
     __shared__ float ut[CH * WS];
     __shared__ float part[CH * D];
-    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
-    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t fa[P];
+    __shared__ uint8_t fb[P];
+    __shared__ uint32_t mk[DROP ? CH * mask_words(D) : 1];
 
     const int head = blockIdx.x, gc0 = blockIdx.y * WS;
     const size_t hb = (size_t)head * N * D;
@@ -716,7 +729,7 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
                                 : nullptr;
         for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = src ? src[e] : 0.0f;
     }
-    build_pairs<D, P2>(pm, pl);
+    build_features<D, P2>(fa, fb);
     __syncthreads();
     const int nch = (N + CH - 1) / CH;
     const int cb = seg * cps, ce = min(nch, cb + cps);
@@ -736,12 +749,12 @@ __global__ __launch_bounds__(NT) void bwd_qscan_kernel(
     auto update = [&](int n0) {
         load_std<D>(k, n0, N, xk, nullptr);
         load_vprime<D, WS>(v, n0, N, gc0, vp);
+        if constexpr (DROP) stage_mask<D>(mk, dr, head, N, n0);
         __syncthreads();
         if constexpr (DROP)
-            state_update<D, P2, WS, true>(S, xk, vp, pm, pl, mask_rows<D>(dr, head, N, n0),
-                                          min(CH, N - n0), dr.inv);
+            state_update<D, P2, WS, true>(S, xk, vp, fa, fb, mk, CH, dr.inv);
         else
-            state_update<D, P2, WS>(S, xk, vp, pm, pl);
+            state_update<D, P2, WS>(S, xk, vp, fa, fb);
         __syncthreads();
     };
     if (!CAUSAL) {
@@ -768,7 +781,6 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     const float *__restrict__ sseg, int cps, Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
-    constexpr int NPAIR = feat<D, P2>::NPAIR;
     constexpr int DP = D + 1;
     __shared__ float S[P * WS];
     __shared__ float xq[CH * DP];
@@ -777,8 +789,9 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
     __shared__ float ut[CH * WS];
     __shared__ float part[CH * D];
     __shared__ float pv[CH * WS];
-    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
-    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t fa[P];
+    __shared__ uint8_t fb[P];
+    __shared__ uint32_t mk[DROP ? CH * mask_words(D) : 1];
 
     const int head = blockIdx.x, gc0 = blockIdx.y * WS;
     const size_t hb = (size_t)head * N * D;
@@ -795,7 +808,7 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
                                 : nullptr;
         for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = src ? src[e] : 0.0f;
     }
-    build_pairs<D, P2>(pm, pl);
+    build_features<D, P2>(fa, fb);
     __syncthreads();
     const int nch = (N + CH - 1) / CH;
     const int cb = seg * cps, ce = min(nch, cb + cps);
@@ -804,15 +817,14 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
         load_std<D>(k, n0, N, xk, nullptr);
         load_vprime<D, WS>(v, n0, N, gc0, vp);
         for (int e = threadIdx.x; e < CH * WS; e += NT) pv[e] = 0.0f;
+        if constexpr (DROP) stage_mask<D>(mk, dr, head, N, n0);
         __syncthreads();
         if constexpr (DROP) {
-            const uint32_t *mr = mask_rows<D>(dr, head, N, n0);
-            const int nv = min(CH, N - n0);
-            contract_grad<D, P2, WS, true>(S, xk, vp, part, mr, nv, dr.inv);
-            contract_psi<D, P2, WS, true>(S, xk, pv, pm, pl, mr, nv, dr.inv);
+            contract_grad<D, P2, WS, true>(S, xk, vp, part, mk, CH, dr.inv);
+            contract_psi<D, P2, WS, true>(S, xk, pv, fa, fb, mk, CH, dr.inv);
         } else {
             contract_grad<D, P2, WS>(S, xk, vp, part);
-            contract_psi<D, P2, WS>(S, xk, pv, pm, pl);
+            contract_psi<D, P2, WS>(S, xk, pv, fa, fb);
         }
         __syncthreads();
         for (int e = threadIdx.x; e < CH * D; e += NT) {
@@ -829,7 +841,7 @@ __global__ __launch_bounds__(NT) void bwd_kscan_kernel(
         load_std<D>(q, n0, N, xq, nullptr, qs);
         load_utilde<D, WS>(dout, g, cvec, n0, N, gc0, ut);
         __syncthreads();
-        state_update<D, P2, WS>(S, xq, ut, pm, pl);
+        state_update<D, P2, WS>(S, xq, ut, fa, fb);
         __syncthreads();
     };
     if (!CAUSAL) {
@@ -854,13 +866,13 @@ __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
     float *__restrict__ sseg, int N, float qs, int cps, Drop dr = Drop{nullptr, 1.0f, nullptr})
 {
     constexpr int P = feat<D, P2>::P;
-    constexpr int NPAIR = feat<D, P2>::NPAIR;
     constexpr int DP = D + 1;
     __shared__ float S[P * WS];
     __shared__ float xs[CH * DP];
     __shared__ float vals[CH * WS];
-    __shared__ uint8_t pm[NPAIR > 0 ? NPAIR : 1];
-    __shared__ uint8_t pl[NPAIR > 0 ? NPAIR : 1];
+    __shared__ uint8_t fa[P];
+    __shared__ uint8_t fb[P];
+    __shared__ uint32_t mk[DROP && SIDE == 0 ? CH * mask_words(D) : 1];
 
     const int head = blockIdx.x, gc0 = blockIdx.y * WS;
     const int nseg = gridDim.z, seg = blockIdx.z;
@@ -869,7 +881,7 @@ __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
     g += (size_t)head * N;
     cvec += (size_t)head * N;
     for (int e = threadIdx.x; e < P * WS; e += NT) S[e] = 0.0f;
-    build_pairs<D, P2>(pm, pl);
+    build_features<D, P2>(fa, fb);
     __syncthreads();
     const int nch = (N + CH - 1) / CH;
     const int cb = seg * cps, ce = min(nch, cb + cps);
@@ -877,16 +889,16 @@ __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
         if (SIDE == 0) {
             load_std<D>(k, c * CH, N, xs, nullptr);
             load_vprime<D, WS>(v, c * CH, N, gc0, vals);
+            if constexpr (DROP) stage_mask<D>(mk, dr, head, N, c * CH);
         } else {
             load_std<D>(q, c * CH, N, xs, nullptr, qs);
             load_utilde<D, WS>(dout, g, cvec, c * CH, N, gc0, vals);
         }
         __syncthreads();
         if constexpr (DROP && SIDE == 0)   // keys: their quadratic features are masked
-            state_update<D, P2, WS, true>(S, xs, vals, pm, pl, mask_rows<D>(dr, head, N, c * CH),
-                                          min(CH, N - c * CH), dr.inv);
+            state_update<D, P2, WS, true>(S, xs, vals, fa, fb, mk, CH, dr.inv);
         else
-            state_update<D, P2, WS>(S, xs, vals, pm, pl);
+            state_update<D, P2, WS>(S, xs, vals, fa, fb);
         __syncthreads();
     }
     float *dst = sseg + (((size_t)head * gridDim.y + blockIdx.y) * nseg + seg) * P * WS;
