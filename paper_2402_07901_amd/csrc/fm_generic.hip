@@ -92,6 +92,13 @@ __device__ void build_features(uint8_t *fa, uint8_t *fb)
     }
 }
 
+// p = 1 features [1, x]: feature f of row x.
+__device__ __forceinline__ float phi1(int f, const float *x)
+{
+    if (f == 0) return 1.0f;
+    return x[f - 1];
+}
+
 // Query-side factor of feature (a, b): 1/2 on the diagonal pairs, else 1.
 template <int D>
 __device__ __forceinline__ float psi_coef(int a, int b)
@@ -164,14 +171,14 @@ __device__ void state_update(float *S, const float *x, const float *val, const u
     constexpr int DP = D + 1;
     constexpr int NW = mask_words(D);
     for (int f = threadIdx.x; f < P; f += NT) {
-        const int a = fa[f], b = fb[f];
+        const int a = P2 ? fa[f] : 0, b = P2 ? fb[f] : 0;
         const bool quad = f > D;
         const int t = quad ? f - 1 - D : 0;
         float acc[WS];
 #pragma unroll
         for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
         for (int r = 0; r < CH; ++r) {
-            float ph = x[r * DP + a] * x[r * DP + b];
+            float ph = P2 ? x[r * DP + a] * x[r * DP + b] : phi1(f, x + r * DP);
             if constexpr (DROP) {
                 const float km = r < nvalid ? keep_mult(mrow + r * NW, t, inv) : 0.0f;
                 ph *= quad ? km : 1.0f;
@@ -200,9 +207,11 @@ __device__ void contract_psi(const float *S, const float *x, float *out, const u
 #pragma unroll
     for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
     const float *xr = x + r * DP;
+    // p = 2: unrolled so the table reads of several features are in flight
+#pragma unroll(P2 ? 4 : 1)
     for (int f = fg; f < P; f += NG) {
-        const int a = fa[f], b = fb[f];
-        float ps = psi_coef<D>(a, b) * (xr[a] * xr[b]);
+        const int a = P2 ? fa[f] : 0, b = P2 ? fb[f] : 0;
+        float ps = P2 ? psi_coef<D>(a, b) * (xr[a] * xr[b]) : phi1(f, xr);
         if constexpr (DROP) {
             const bool quad = f > D;
             const float km = r < nvalid ? keep_mult(mrow + r * NW, quad ? f - 1 - D : 0, inv) : 0.0f;
