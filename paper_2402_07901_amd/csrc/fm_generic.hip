@@ -238,39 +238,27 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
     constexpr int NW = mask_words(D);
     const int r = threadIdx.x % CH, ag = threadIdx.x / CH;
     const float *xr = x + r * DP;
-    if constexpr (DROP) {
-        // the keep multiplier of feature (a, m) is read once for all WS columns
-        const uint32_t *row = mrow + (r < nvalid ? r : 0) * NW;
-        for (int a = ag; a < D; a += AG) {
-            float inner[WS];
+    // (a, m) outer, the WS columns inner: each state row and (DROP) each keep
+    // bit is read once for all columns
+    const uint32_t *row = DROP ? mrow + (r < nvalid ? r : 0) * NW : nullptr;
+    for (int a = ag; a < D; a += AG) {
+        float inner[WS];
 #pragma unroll
-            for (int j = 0; j < WS; ++j) inner[j] = S[(1 + a) * WS + j];
+        for (int j = 0; j < WS; ++j) inner[j] = S[(1 + a) * WS + j];
+        if constexpr (P2) {
             for (int m = 0; m < D; ++m) {
                 const int lo = m < a ? m : a, hi = m < a ? a : m;
                 const int pf = pair_feature(D, lo, hi);
-                const float xm = r < nvalid ? xr[m] * keep_mult(row, pf - 1 - D, inv) : 0.0f;
+                float xm = xr[m];
+                if constexpr (DROP)
+                    xm = r < nvalid ? xm * keep_mult(row, pf - 1 - D, inv) : 0.0f;
 #pragma unroll
                 for (int j = 0; j < WS; ++j) inner[j] = fmaf(xm, S[pf * WS + j], inner[j]);
             }
-            float acc = 0.0f;
-#pragma unroll
-            for (int j = 0; j < WS; ++j) acc = fmaf(coef[r * WS + j], inner[j], acc);
-            out[r * D + a] = acc;
         }
-        return;
-    }
-    for (int a = ag; a < D; a += AG) {
         float acc = 0.0f;
-        for (int j = 0; j < WS; ++j) {
-            float inner = S[(1 + a) * WS + j];
-            if (P2) {
-                for (int m = 0; m < D; ++m) {
-                    int lo = m < a ? m : a, hi = m < a ? a : m;
-                    inner = fmaf(xr[m], S[pair_feature(D, lo, hi) * WS + j], inner);
-                }
-            }
-            acc = fmaf(coef[r * WS + j], inner, acc);
-        }
+#pragma unroll
+        for (int j = 0; j < WS; ++j) acc = fmaf(coef[r * WS + j], inner[j], acc);
         out[r * D + a] = acc;
     }
 }
