@@ -620,6 +620,8 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     __shared__ float E[CH * CH];   // f'(s) dw
     __shared__ float Wm[CH * CH];  // f(s)
     __shared__ uint32_t mk[DROP ? CH * NW : 1];
+    __shared__ float accq[DROP ? CH * D : 1];   // DROP: in-chunk dq^, dk^ sums
+    __shared__ float acck[DROP ? CH * D : 1];
 
     const int head = blockIdx.x, n0 = blockIdx.y * CH;
     const size_t hb = (size_t)head * N * D;
@@ -642,7 +644,10 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     load_std<D>(k, n0, N, xk, nullptr);
     load_vprime<D, D1>(v, n0, N, 0, vp);
     load_utilde<D, D1>(dout, g, cvec, n0, N, 0, ut);
-    if constexpr (DROP) stage_mask<D>(mk, dr, head, N, n0);
+    if constexpr (DROP) {
+        stage_mask<D>(mk, dr, head, N, n0);
+        for (int e = threadIdx.x; e < CH * D; e += NT) accq[e] = acck[e] = 0.0f;
+    }
     __syncthreads();
     {
         int i = threadIdx.x / CH, t = threadIdx.x % CH;
@@ -664,17 +669,30 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
         Wm[i * CH + t] = w;
     }
     __syncthreads();
+    if constexpr (DROP) {
+        // one (pair, channel) per item: h of the pair (i, t), t <= i, is
+        // shared by dq^_i (k_t h) and dk^_t (q_i h)
+        constexpr int NPR = CH * (CH + 1) / 2;
+        for (int e = threadIdx.x; e < NPR * D; e += NT) {
+            const int pr = e / D, a = e % D;
+            int i = 0;
+            while ((i + 1) * (i + 2) / 2 <= pr) ++i;
+            const int t = pr - i * (i + 1) / 2;
+            const float eit = E[i * CH + t];   // 0 for rows past N
+            if (eit == 0.0f) continue;
+            const float h = drop_h<D>(xq + i * DP, xk + t * DP, mk + t * NW, a, dr.inv);
+            atomicAdd(&accq[i * D + a], eit * xk[t * DP + a] * h);
+            atomicAdd(&acck[t * D + a], eit * xq[i * DP + a] * h);
+        }
+        __syncthreads();
+    }
     for (int e = threadIdx.x; e < CH * D; e += NT) {
         int r = e / D, a = e % D, n = n0 + r;
         if (n >= N) continue;
         float aq = 0.0f, ak = 0.0f, av = 0.0f;
         if constexpr (DROP) {
-            for (int t = 0; t <= r; ++t)   // row r as query, keys t <= r
-                aq = fmaf(E[r * CH + t] * xk[t * DP + a],
-                          drop_h<D>(xq + r * DP, xk + t * DP, mk + t * NW, a, dr.inv), aq);
-            for (int t = r; t < CH; ++t)   // row r as key, queries t >= r
-                ak = fmaf(E[t * CH + r] * xq[t * DP + a],
-                          drop_h<D>(xq + t * DP, xk + r * DP, mk + r * NW, a, dr.inv), ak);
+            aq = accq[r * D + a];
+            ak = acck[r * D + a];
             for (int t = 0; t < CH; ++t) av = fmaf(Wm[t * CH + r], ut[t * D1 + a], av);
         } else {
             for (int t = 0; t < CH; ++t) {
