@@ -209,3 +209,47 @@ def test_workload_dropout_fwdbwd_bf16():
         say(f"{w.name} dropout head ({b},{h}): E_O={e:.3e} E_G={eg:.3e}")
         assert e <= TOL[w.dtype] and eg <= TOL[w.dtype], (b, h, e, eg)
     bwd_case(2, 2, 256, 64, True, "bf16", rate, 1800, label="dropout bwd N=256 D=64 bf16")
+
+
+def test_padding_bits_are_ignored():
+    """Bits past D(D+1)/2 in a token's last word carry nothing: setting them
+    all leaves O, G and the gradients unchanged (D = 16: 136 features, 5 words,
+    the last 24 bits padding)."""
+    import torch
+    B, H, N, D, rate = 1, 2, 40, 16, 0.3
+    inp = make_inputs(B, H, N, D, 1900, "f32", with_dout=True)
+    bits = oracle.dropout_mask(B, H, N, D, f32(rate), 77)
+    padded = bits.copy()
+    padded[..., -1] |= np.uint32(0xFFFFFFFF) << np.uint32(136 % 32)
+    assert not np.array_equal(bits, padded)
+    q, k, v = (to_dev(inp[n], "f32") for n in ("q", "k", "v"))
+    do = to_dev(inp["dout"], "f32")
+    outs = []
+    for b in (bits, padded):
+        bd = bits_dev(b)
+        o, g = fm.fastmax_fwd_dropout(q, k, v, bd, rate, causal=True)
+        grads = fm.fastmax_bwd_dropout(q, k, v, o, do, g, bd, rate, causal=True)
+        torch.cuda.synchronize()
+        outs.append([to_f64(t) for t in (o, g) + tuple(grads)])
+    for a, b in zip(*outs):
+        assert max_rel(b, a) <= 2e-6
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_generator_feeds_the_masked_calls(causal):
+    """End to end: bits drawn on the GPU by fastmax_dropout_mask drive the
+    masked forward; the oracle draws its own bits from the same seed."""
+    import torch
+    B, H, N, D, rate, seed = 2, 2, 90, 32, 0.25, 0xDEADBEEFCAFE
+    inp = make_inputs(B, H, N, D, 2000, "bf16")
+    q, k, v = (to_dev(inp[n], "bf16") for n in ("q", "k", "v"))
+    bd = fm.dropout_mask(B, H, N, D, rate, seed)
+    o, g = fm.fastmax_fwd_dropout(q, k, v, bd, rate, causal=causal)
+    torch.cuda.synchronize()
+    bits = oracle.dropout_mask(B, H, N, D, f32(rate), seed)
+    ref_o, ref_g = oracle.fwd_drop_fact(inp["q64"], inp["k64"], inp["v64"], bits, f32(rate),
+                                        causal)
+    e = max_rel(to_f64(o), ref_o)
+    eg = float((np.abs(g.cpu().numpy() - ref_g) / np.abs(ref_g)).max())
+    say(f"generator -> fwd causal={causal}: E_O={e:.3e} E_G={eg:.3e}")
+    assert e <= TOL["bf16"] and eg <= TOL["bf16"], (e, eg)
