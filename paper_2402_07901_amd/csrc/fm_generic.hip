@@ -300,7 +300,8 @@ __device__ float drop_h(const float *xq, const float *xk, const uint32_t *row, i
 }
 
 // Masked in-chunk weights of the causal forward, once per (head, chunk):
-// out[i][t] = w_it for t <= i < rows left, else 0.  grid = (B*H, chunks).
+// out[i][t] = w_it for t <= i < rows left, else 0.  grid = (B*H, y, z), chunk
+// y + 65535 z (grid y is at most 65535).
 template <int D, typename T>
 __global__ __launch_bounds__(NT) void drop_wblk_kernel(const T *__restrict__ q,
                                                        const T *__restrict__ k,
@@ -311,7 +312,9 @@ __global__ __launch_bounds__(NT) void drop_wblk_kernel(const T *__restrict__ q,
     __shared__ float xq[CH * DP];
     __shared__ float xk[CH * DP];
     __shared__ uint32_t mk[CH * mask_words(D)];
-    const int head = blockIdx.x, c = blockIdx.y, n0 = c * CH;
+    const int head = blockIdx.x, nch = (N + CH - 1) / CH;
+    const int c = blockIdx.y + 65535 * blockIdx.z, n0 = c * CH;
+    if (c >= nch) return;   // the whole block, before any barrier
     const size_t hb = (size_t)head * N * D;
     stage_mask<D>(mk, dr, head, N, n0);
     load_std<D>(q + hb, n0, N, xq, nullptr, qs);   // synchronises the staging too
@@ -321,7 +324,7 @@ __global__ __launch_bounds__(NT) void drop_wblk_kernel(const T *__restrict__ q,
     // keys past N are never seen by a valid row (t <= i < N)
     if (t <= i && n0 + i < N)
         w = drop_weight<D>(xq + i * DP, xk + t * DP, mk + t * mask_words(D), dr.inv);
-    wblk[((size_t)head * gridDim.y + c) * (CH * CH) + threadIdx.x] = w;
+    wblk[((size_t)head * nch + c) * (CH * CH) + threadIdx.x] = w;
 }
 
 // ---------------------------------------------------------------------------
@@ -623,7 +626,10 @@ __global__ __launch_bounds__(NT) void bwd_intra_kernel(
     __shared__ float accq[DROP ? CH * D : 1];   // DROP: in-chunk dq^, dk^ sums
     __shared__ float acck[DROP ? CH * D : 1];
 
-    const int head = blockIdx.x, n0 = blockIdx.y * CH;
+    // chunk y + 65535 z (grid y is at most 65535); blocks past the last chunk
+    // leave before any barrier
+    const int head = blockIdx.x, c = blockIdx.y + 65535 * blockIdx.z, n0 = c * CH;
+    if (n0 >= N) return;
     const size_t hb = (size_t)head * N * D;
     q += hb; k += hb; v += hb; dout += hb;
     g += (size_t)head * N;
@@ -1031,8 +1037,10 @@ static hipError_t fwd_dispatch(const void *q, const void *k, const void *v, void
             // after the segment states in the workspace, 256-byte aligned
             const size_t off = (sp.bytes + 255) & ~(size_t)255;
             float *wb = (float *)((char *)ws + off);
-            hipLaunchKernelGGL((drop_wblk_kernel<D, T>), dim3(BH, (N + CH - 1) / CH), dim3(NT), 0,
-                               st, (const T *)q, (const T *)k, wb, N, qs, dr);
+            const int nch = (N + CH - 1) / CH;
+            hipLaunchKernelGGL((drop_wblk_kernel<D, T>),
+                               dim3(BH, nch < 65535 ? nch : 65535, (nch + 65534) / 65535),
+                               dim3(NT), 0, st, (const T *)q, (const T *)k, wb, N, qs, dr);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
             dr.wblk = wb;
@@ -1093,8 +1101,9 @@ static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, con
     const int rb = (int)((rows + NT - 1) / NT);
     hipLaunchKernelGGL((bwd_rowdot_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)o,
                        (const T *)dout, g, cvec, rows);
-    hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T, DROP>), dim3(BH, (N + CH - 1) / CH),
-                       dim3(NT), 0, st, (const T *)q, (const T *)k, (const T *)v,
+    const int nch = (N + CH - 1) / CH;
+    hipLaunchKernelGGL((bwd_intra_kernel<D, P2, CAUSAL, T, DROP>),
+                       dim3(BH, nch < 65535 ? nch : 65535, (nch + 65534) / 65535), dim3(NT), 0, st, (const T *)q, (const T *)k, (const T *)v,
                        (const T *)dout, g, cvec, dqh, dkh, dva, N, qs, dr);
     const dim3 grid(BH, bp.slices, bp.nseg);
     const dim3 pgrid((PWS + NT - 1) / NT, BH * bp.slices);

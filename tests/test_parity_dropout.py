@@ -253,3 +253,23 @@ def test_generator_feeds_the_masked_calls(causal):
     eg = float((np.abs(g.cpu().numpy() - ref_g) / np.abs(ref_g)).max())
     say(f"generator -> fwd causal={causal}: E_O={e:.3e} E_G={eg:.3e}")
     assert e <= TOL["bf16"] and eg <= TOL["bf16"], (e, eg)
+
+
+def test_fwd_dropout_past_65535_chunks():
+    """One head of 1,048,616 tokens (65539 chunks of 16, more than the 65535
+    blocks of a grid's y dimension): the masked in-chunk weights are computed
+    by blocks that stride over the chunks; every row of the tail against the
+    oracle's factorised masked forward."""
+    import torch
+    B, H, N, D, rate = 1, 1, 65536 * 16 + 40, 16, 0.2
+    inp = make_inputs(B, H, N, D, 2100, "f32")
+    bits = oracle.dropout_mask(B, H, N, D, f32(rate), 5)
+    q, k, v = (to_dev(inp[n], "f32") for n in ("q", "k", "v"))
+    o, g = fm.fastmax_fwd_dropout(q, k, v, bits_dev(bits), rate, causal=True)
+    torch.cuda.synchronize()
+    ref_o, ref_g = oracle.fwd_drop_fact(inp["q64"], inp["k64"], inp["v64"], bits, f32(rate), True)
+    tail = slice(65535 * 16 - 20, N)
+    e = max_rel(to_f64(o)[0, 0, tail], ref_o[0, 0, tail])
+    eg = float((np.abs(g.cpu().numpy()[0, 0, tail] - ref_g[0, 0, tail]) / np.abs(ref_g[0, 0, tail])).max())
+    say(f"N={N}: tail E_O={e:.3e} E_G={eg:.3e}")
+    assert e <= TOL["f32"] and eg <= TOL["f32"], (e, eg)
