@@ -273,3 +273,27 @@ def test_fwd_dropout_past_65535_chunks():
     eg = float((np.abs(g.cpu().numpy()[0, 0, tail] - ref_g[0, 0, tail]) / np.abs(ref_g[0, 0, tail])).max())
     say(f"N={N}: tail E_O={e:.3e} E_G={eg:.3e}")
     assert e <= TOL["f32"] and eg <= TOL["f32"], (e, eg)
+
+
+def test_workload_rate0_matches_the_mfma_path():
+    """At the bench's full shape (B8 H12 N4096 D64, causal, bf16): every bit
+    kept at rate 0 makes the masked calls compute f_2, so the float32 dropout
+    kernels must agree with the plain calls, which take the (independently
+    oracle-checked) MFMA forward and backward here -- forward and backward
+    compared on every element."""
+    import torch
+    from paper_2402_07901_amd.inputs import WORKLOADS, workload_inputs
+    w = WORKLOADS["fwdbwd_causal_bf16"]
+    inp = workload_inputs(w, want64=False)
+    q, k, v = (to_dev(inp[n], w.dtype) for n in ("q", "k", "v"))
+    do = to_dev(inp["dout"], w.dtype)
+    bits = fm.dropout_mask(w.B, w.H, w.N, w.D, 0.0, 1)
+    o0, g0 = fm.fastmax_fwd(q, k, v, p=2, causal=True)
+    o1, g1 = fm.fastmax_fwd_dropout(q, k, v, bits, 0.0, causal=True)
+    d0 = fm.fastmax_bwd(q, k, v, o0, do, g0, p=2, causal=True)
+    d1 = fm.fastmax_bwd_dropout(q, k, v, o0, do, g0, bits, 0.0, causal=True)
+    torch.cuda.synchronize()
+    for nm, a, b in (("O", o0, o1), ("G", g0, g1)) + tuple(zip(("dq", "dk", "dv"), d0, d1)):
+        e = max_rel(to_f64(b), to_f64(a))
+        say(f"{w.name} rate 0 vs MFMA {nm}: E={e:.3e}")
+        assert e <= TOL["bf16"], (nm, e)
