@@ -192,7 +192,10 @@ __device__ void state_update(float *S, const float *x, const float *val, const u
 }
 
 // out[r][j] += sum_f psi_f(x_r) S[f][j]   (LDS atomics; out is CH x WS).
-// DROP: x holds keys, whose quadratic features take their keep bits.
+// DROP: x holds keys, whose quadratic features take their keep bits.  At p = 2
+// with slices of at most 3 columns (D = 128) a thread takes RPT = 4 rows, so
+// each state row and table entry it reads serves four rows (measured slower
+// for the wider slices of D <= 64).
 template <int D, bool P2, int WS, bool DROP = false>
 __device__ void contract_psi(const float *S, const float *x, float *out, const uint8_t *fa,
                              const uint8_t *fb, const uint32_t *mrow = nullptr, int nvalid = 0,
@@ -200,28 +203,43 @@ __device__ void contract_psi(const float *S, const float *x, float *out, const u
 {
     constexpr int P = feat<D, P2>::P;
     constexpr int DP = D + 1;
-    constexpr int NG = NT / CH;
     constexpr int NW = mask_words(D);
-    const int r = threadIdx.x % CH, fg = threadIdx.x / CH;
-    float acc[WS];
+    constexpr int RPT = (P2 && WS <= 3) ? 4 : 1;    // rows per thread
+    constexpr int RG = CH / RPT;                     // row groups: rows rg + RG u
+    constexpr int NG = NT / RG;                      // feature groups
+    const int rg = threadIdx.x % RG, fg = threadIdx.x / RG;
+    float acc[RPT][WS];
 #pragma unroll
-    for (int j = 0; j < WS; ++j) acc[j] = 0.0f;
-    const float *xr = x + r * DP;
-    // p = 2: unrolled so the table reads of several features are in flight
-#pragma unroll(P2 ? 4 : 1)
+    for (int u = 0; u < RPT; ++u)
+#pragma unroll
+        for (int j = 0; j < WS; ++j) acc[u][j] = 0.0f;
+    // p = 2 with one row per thread: unrolled so several table reads are in flight
+#pragma unroll(P2 && RPT == 1 ? 4 : 1)
     for (int f = fg; f < P; f += NG) {
         const int a = P2 ? fa[f] : 0, b = P2 ? fb[f] : 0;
-        float ps = P2 ? psi_coef<D>(a, b) * (xr[a] * xr[b]) : phi1(f, xr);
-        if constexpr (DROP) {
-            const bool quad = f > D;
-            const float km = r < nvalid ? keep_mult(mrow + r * NW, quad ? f - 1 - D : 0, inv) : 0.0f;
-            ps *= quad ? km : 1.0f;
-        }
+        const bool quad = f > D;
+        const float c = P2 ? psi_coef<D>(a, b) : 1.0f;
+        float sv[WS];
 #pragma unroll
-        for (int j = 0; j < WS; ++j) acc[j] = fmaf(ps, S[f * WS + j], acc[j]);
+        for (int j = 0; j < WS; ++j) sv[j] = S[f * WS + j];
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) {
+            const int r = rg + RG * u;
+            const float *xr = x + r * DP;
+            float ps = P2 ? c * (xr[a] * xr[b]) : phi1(f, xr);
+            if constexpr (DROP) {
+                const float km =
+                    r < nvalid ? keep_mult(mrow + r * NW, quad ? f - 1 - D : 0, inv) : 0.0f;
+                ps *= quad ? km : 1.0f;
+            }
+#pragma unroll
+            for (int j = 0; j < WS; ++j) acc[u][j] = fmaf(ps, sv[j], acc[u][j]);
+        }
     }
 #pragma unroll
-    for (int j = 0; j < WS; ++j) atomicAdd(&out[r * WS + j], acc[j]);
+    for (int u = 0; u < RPT; ++u)
+#pragma unroll
+        for (int j = 0; j < WS; ++j) atomicAdd(&out[(rg + RG * u) * WS + j], acc[u][j]);
 }
 
 // Gradient-side contraction (backward):
