@@ -178,7 +178,10 @@ int fastmax_dropout_mask(uint32_t *keep_bits, int B, int H, int N, int D, float 
 
 /* Workspace of fastmax_fwd_dropout (backward = 0) / fastmax_bwd_dropout
  * (backward = 1): that of the float32 kernels at p = 2 (see
- * fastmax_workspace_bytes). */
+ * fastmax_workspace_bytes) and, for the causal forward, after it (rounded up
+ * to 256 bytes) the masked in-chunk weights: 16 x 16 floats per chunk of 16
+ * tokens of every head (64 bytes per token).  Returns 0 for arguments the
+ * entry points would reject. */
 size_t fastmax_dropout_workspace_bytes(int B, int H, int N, int D, int causal,
                                        fastmax_dtype_t dt, int backward);
 
