@@ -118,7 +118,9 @@ def test_fwd_dropout_segments(causal):
     fwd_case(1, 1, 700, 16, causal, "f32", 0.4, 1300, label=label)
 
 
-def bwd_case(B, H, N, D, causal, dtype, rate, seed, scale=1.0, label=""):
+def bwd_case(B, H, N, D, causal, dtype, rate, seed, scale=1.0, label="", floor=None):
+    """floor: a lower bound for the error's denominator (the tensor's max |ref|),
+    for gradients that are exactly zero."""
     import torch
     inp = make_inputs(B, H, N, D, seed, dtype, with_dout=True)
     bits = oracle.dropout_mask(B, H, N, D, f32(rate), seed * 31 + 5)
@@ -132,10 +134,14 @@ def bwd_case(B, H, N, D, causal, dtype, rate, seed, scale=1.0, label=""):
                                        f32(rate), causal, scale=scale)
     for nm, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
         x = to_f64(got)
-        e = max_rel(x, ref)
+        if floor is None:
+            e = max_rel(x, ref)
+        else:
+            e = float(np.abs(x - ref).max() / max(np.abs(ref).max(), floor))
         say(f"{label} {nm}: E={e:.3e}")
         assert np.isfinite(x).all()
         assert e <= TOL[dtype], (label, nm, e)
+    return inp
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -297,3 +303,17 @@ def test_workload_rate0_matches_the_mfma_path():
         e = max_rel(to_f64(b), to_f64(a))
         say(f"{w.name} rate 0 vs MFMA {nm}: E={e:.3e}")
         assert e <= TOL["bf16"], (nm, e)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("N", [1, 16, 17])
+def test_bwd_dropout_edges(N, causal):
+    """One token, exactly one chunk, and one chunk plus one token.  With one
+    token O = v whatever q and k are, so the exact dq and dk are zero: errors
+    are measured against the gradient scale max|dO| max|v| where the exact
+    gradient is smaller."""
+    label = f"bwd dropout edge N={N} causal={causal}"
+    say(label)
+    inp = make_inputs(1, 2, N, 64, 2200 + N, "f32", with_dout=True)
+    floor = float(np.abs(inp["dout64"]).max() * np.abs(inp["v64"]).max())
+    bwd_case(1, 2, N, 64, causal, "f32", 0.5, 2200 + N, label=label, floor=floor)
