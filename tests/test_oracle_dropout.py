@@ -204,7 +204,33 @@ def check_mask_layout():
     assert abs(kept - total * (1 - r)) <= 5 * sd, (kept, total)
 
 
+def check_all_quadratic_dropped_is_p1():
+    """With every quadratic feature dropped the masked weight is the p = 1
+    weight 1 + tau s at any rate (the constant and linear terms are never
+    dropped): the whole forward equals the unmasked p = 1 oracle, and a row
+    with one key and tau s < -1 gets a negative G."""
+    q, k, v = _rand(1, 2, 19, 8, 6)
+    zero = np.zeros((1, 2, 19, oracle.mask_words(8)), dtype=np.uint32)
+    for causal in (False, True):
+        ref_o, ref_g = oracle.fwd_brute(q, k, v, 1, causal, scale=0.6)
+        for fn in (oracle.fwd_drop_brute, oracle.fwd_drop_fact):
+            o, g = fn(q, k, v, zero, 0.7, causal, scale=0.6)
+            np.testing.assert_allclose(g, ref_g, rtol=1e-9, atol=1e-12)
+            np.testing.assert_allclose(o * g[..., None], ref_o * ref_g[..., None],
+                                       rtol=1e-9, atol=1e-9)
+    qh, kh = _std(q[0, 0, 0]), _std(k[0, 0, 0])
+    s = float(qh @ kh)
+    kk = k[:, :, :1].copy()
+    if s > -2:   # make tau s < -1 with tau = 1: k = -q gives s = -D
+        kk = -q[:, :, :1].copy()
+        s = -8.0
+    _, g = oracle.fwd_drop_brute(q[:, :, :1], kk, v[:, :, :1], zero[:, :, :1], 0.5, False)
+    np.testing.assert_allclose(g[0, 0, 0], 1 + s, rtol=1e-12)
+    assert g[0, 0, 0] < 0
+
+
 CHECKS = (check_philox_kat, check_rate0_all_kept_is_f2, check_single_dropped_feature,
+          check_all_quadratic_dropped_is_p1,
           check_drop_brute_vs_fact, check_expectation_over_masks,
           check_drop_bwd_finite_differences, check_mask_layout)
 
