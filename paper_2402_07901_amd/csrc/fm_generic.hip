@@ -305,14 +305,19 @@ __device__ float drop_weight(const float *xq, const float *xk, const uint32_t *r
 
 // d w / d xq_a = xk_a h_a and d w / d xk_a = xq_a h_a for the dropout weight,
 // h_a = 1 + sum_l xq_l xk_l b~_t(a,l).
+// One loop over l (the lanes of a wave hold different a, so split loops would
+// run both to their longest): feature (l, a), l < a, is t(l, l) + a - l with
+// t(l + 1, l + 1) = t(l, l) + D - l; feature (a, l), l >= a, is t(a, a) + l - a.
 template <int D>
 __device__ float drop_h(const float *xq, const float *xk, const uint32_t *row, int a, float inv)
 {
     float acc = 0.0f;
+    const int taa = a * D - a * (a - 1) / 2;   // t(a, a)
+    int tll = 0;                               // t(l, l)
     for (int l = 0; l < D; ++l) {
-        const int lo = l < a ? l : a, hi = l < a ? a : l;
-        const int t = pair_feature(D, lo, hi) - 1 - D;
+        const int t = l < a ? tll + a - l : taa + l - a;
         if ((row[t >> 5] >> (t & 31)) & 1u) acc = fmaf(xq[l], xk[l], acc);
+        tll += D - l;
     }
     return fmaf(acc, inv, 1.0f);
 }
