@@ -264,9 +264,13 @@ __device__ void contract_grad(const float *S, const float *x, const float *coef,
 #pragma unroll
         for (int j = 0; j < WS; ++j) inner[j] = S[(1 + a) * WS + j];
         if constexpr (P2) {
+            // packed index of the pair (min(a, m), max(a, m)), walked with adds:
+            // t(m, a) = t(m, m) + a - m for m < a, t(a, m) = t(a, a) + m - a
+            const int taa = a * D - a * (a - 1) / 2;
+            int tmm = 0;
             for (int m = 0; m < D; ++m) {
-                const int lo = m < a ? m : a, hi = m < a ? a : m;
-                const int pf = pair_feature(D, lo, hi);
+                const int pf = 1 + D + (m < a ? tmm + a - m : taa + m - a);
+                tmm += D - m;
                 float xm = xr[m];
                 if constexpr (DROP)
                     xm = r < nvalid ? xm * keep_mult(row, pf - 1 - D, inv) : 0.0f;
