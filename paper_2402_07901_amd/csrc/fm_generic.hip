@@ -934,7 +934,7 @@ __global__ __launch_bounds__(NT) void bwd_seg_state_kernel(
     const int nch = (N + CH - 1) / CH;
     const int cb = seg * cps, ce = min(nch, cb + cps);
     for (int c = cb; c < ce; ++c) {
-        if (SIDE == 0) {
+        if constexpr (SIDE == 0) {
             load_std<D>(k, c * CH, N, xs, nullptr);
             load_vprime<D, WS>(v, c * CH, N, gc0, vals);
             if constexpr (DROP) stage_mask<D>(mk, dr, head, N, c * CH);
