@@ -48,3 +48,47 @@ def row_scaled(x, ref, g_ref, gabs_ref, vmax):
     kappa = gabs_ref / np.abs(g_ref)
     e = np.abs(x - ref).max(-1) / (kappa * (1.0 + kappa) * vmax)
     return float(e.max()), int((kappa > 10).sum())
+
+
+def grad_bounds(q64, k64, v64, dout64, o_ref, g_ref, gabs_ref, p, causal, tau=1.0):
+    """First-order rounding bounds of the gradient entries of ONE head
+    ([N, D] arrays), for conditioning-aware comparisons (p = 1, where
+    weights change sign and G_i may nearly cancel).
+
+    The gradient is a sum over (query i, key n) of terms that each carry
+    1/G_i, O_i and f'(tau s_in); a relative rounding error eps in the
+    forward's sums gives G_i a relative error ~ eps kappa_i
+    (kappa_i = sum_n |w_in| / |G_i|) and O_i an absolute error
+    ~ eps kappa_i (1 + kappa_i) max|v|, so each term (i, n) has an error of
+    about eps kappa_i times its magnitude
+        A_in = |f'(tau s_in)| |dO_i|_1 max|v| (1 + kappa_i) / |G_i|.
+    Summed without cancellation, and carried through the standardisation
+    backward (|d x| <= (2 + max|x^|) |d x^| / sigma), this gives per row i
+    of dq, and per key n of dk and dv, a bound B such that
+    |error| <= eps B.  Returns (Bq [N], Bk [N], Bv [N])."""
+    import oracle
+    qh, _, sq = oracle.standardize(q64)
+    kh, _, sk = oracle.standardize(k64)
+    N = q64.shape[0]
+    s = tau * (qh @ kh.T)
+    w = 1.0 + s + (0.5 * s * s if p == 2 else 0.0)
+    dw = np.ones_like(s) if p == 1 else 1.0 + s
+    if causal:
+        mask = np.tril(np.ones((N, N), dtype=bool))
+        w = np.where(mask, w, 0.0)
+        dw = np.where(mask, dw, 0.0)
+    kappa = gabs_ref / np.abs(g_ref)
+    vmax = np.abs(v64).max()
+    a_row = np.abs(dout64).sum(-1) * vmax * (1.0 + kappa) / np.abs(g_ref)   # [N] over i
+    A = np.abs(dw) * (kappa * a_row)[:, None]                               # [i, n]
+    bq_hat = tau * (A @ np.abs(kh)).max(-1)                                 # [i]
+    bk_hat = tau * (A.T @ np.abs(qh)).max(-1)                               # [n]
+    Bq = (2.0 + np.abs(qh).max(-1)) * bq_hat / sq
+    Bk = (2.0 + np.abs(kh).max(-1)) * bk_hat / sk
+    Bv = (np.abs(w) * (kappa * np.abs(dout64).max(-1) / np.abs(g_ref))[:, None]).sum(0)
+    return Bq, Bk, Bv
+
+
+def bounded_err(x, ref, bound):
+    """max over rows r of max_j |x_rj - ref_rj| / bound_r."""
+    return float((np.abs(x - ref).max(-1) / bound).max())

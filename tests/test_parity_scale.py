@@ -107,15 +107,20 @@ def bwd_check(inp, p, causal, dtype, tau, label):
         assert e <= TOL[dtype], (label, tau, nm, e)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("p", [1, 2])
 @pytest.mark.parametrize("D", [16, 64])
-def test_bwd_scaled_generic(D, p, causal):
-    label = f"bwd scaled generic D={D} p={p} causal={causal} f32"
+def test_bwd_scaled_generic(D, p, causal, dtype):
+    """At tau = 1/D every p = 1 weight 1 + tau s is >= 0 (|tau s| <= 1), so
+    kappa = 1 and the plain tensor-wide bar pins the p = 1 backward in both
+    I/O dtypes (with bf16 I/O, D = 64, p = 2 this is the MFMA backward when
+    causal)."""
+    label = f"bwd scaled generic D={D} p={p} causal={causal} {dtype}"
     say(label)
-    inp = make_inputs(1, 2, 37, D, 730 + D, "f32", with_dout=True)
+    inp = make_inputs(1, 2, 37, D, 730 + D, dtype, with_dout=True)
     for tau in taus(D):
-        bwd_check(inp, p, causal, "f32", tau, label)
+        bwd_check(inp, p, causal, dtype, tau, label)
 
 
 @pytest.mark.parametrize("N", [37, 300])
