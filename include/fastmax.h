@@ -20,11 +20,17 @@
  * Conventions shared by every entry point
  *  - Layout: q, k, v, out, dout, dq, dk, dv are [B, H, N, D] contiguous
  *    (D fastest) in the I/O dtype `dt`; g is [B, H, N] float32.
- *    Statistics and accumulation are float32 whatever `dt` is.
+ *    Statistics (standardisation, G) are float32 whatever `dt` is; moment
+ *    contractions accumulate in float32.  The causal bf16, D = 64, p = 2
+ *    MFMA path carries its moment state between 128-token chunks in fp16
+ *    (each chunk's float32 contribution is rounded and added); its error
+ *    stays within the bf16 tolerance on every row of 65536-token causal
+ *    sequences (tested).
  *  - Pointers are device pointers (HBM) and must be 16-byte aligned.
  *  - Ownership: the caller owns every buffer, including `workspace`.  The
  *    library keeps no pointer after return, allocates no device memory,
- *    creates no stream and holds no global mutable state (thread-safe).
+ *    creates no stream and holds no global mutable state (thread-safe);
+ *    the one exception is fastmax_fwd_noalloc's per-GPU scratch array.
  *  - Asynchrony: work is enqueued on `stream` (0 = the null stream);
  *    FASTMAX_OK means "enqueued".  Outputs are valid once the stream reaches
  *    that point.  Inputs must stay valid until then.
@@ -207,6 +213,29 @@ const char *fastmax_strerror(int code);
 
 /* Library version as "major.minor.patch". */
 const char *fastmax_version(void);
+
+/*
+ * Allocation-free forward, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * it).  Arguments, layouts, results and errors are those of
+ * fastmax_fwd_scaled, without the workspace: the library uses a static
+ * device array of FASTMAX_NOALLOC_MAX_WORKSPACE_BYTES (64 MiB) per GPU
+ * instead, which each GPU the library runs on holds until the process ends.
+ * Problems whose fastmax_workspace_bytes(..., backward = 0) exceeds that
+ * size are rejected with FASTMAX_EWORKSPACE before anything is enqueued
+ * (e.g. the causal bf16, D = 64, p = 2 forward takes up to B*H*N = 262144
+ * rows).  The call allocates nothing (no hipMalloc, no library allocation);
+ * the first call on a GPU looks the array's device address up once
+ * (FASTMAX_EHIP if HIP refuses).  Every call on one GPU shares that GPU's
+ * array: calls whose work overlaps on one GPU (different streams without
+ * ordering, or several host threads) race on it and must be serialised by
+ * the caller.  The array keeps the last call's contents; no forward path
+ * needs it zeroed.
+ */
+#define FASTMAX_NOALLOC_MAX_WORKSPACE_BYTES ((size_t)64 << 20)
+int fastmax_fwd_noalloc(const void *q, const void *k, const void *v, void *out,
+                        float *g, int B, int H, int N, int D, int p, int causal,
+                        float qk_scale, fastmax_dtype_t dt, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -69,6 +69,43 @@ size_t bwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
 
 }  // namespace
 
+namespace fm {
+
+int fwd_validate(const void *q, const void *k, const void *v, const void *out, const float *g,
+                 int B, int H, int N, int D, int p, int causal, float qk_scale, int dt)
+{
+    int rc = check_common(B, H, N, D, p, causal, (fastmax_dtype_t)dt);
+    if (rc != FASTMAX_OK) return rc;
+    if (!valid_scale(qk_scale)) return FASTMAX_EINVAL;
+    if (!q || !k || !v || !out) return FASTMAX_ENULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+        (g && !aligned16(g)))
+        return FASTMAX_EALIGN;
+    return FASTMAX_OK;
+}
+
+size_t fwd_workspace(int B, int H, int N, int D, int p, int causal, int dt)
+{
+    return fwd_ws(B, H, N, D, p, causal, (fastmax_dtype_t)dt);
+}
+
+int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, int B, int H, int N,
+            int D, int p, int causal, float qk_scale, int dt, void *workspace, hipStream_t stream)
+{
+    const fastmax_dtype_t t = (fastmax_dtype_t)dt;
+    hipError_t e;
+    if (mfma_causal(D, p, causal, t))
+        e = mfma_causal_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
+    else if (mfma_noncausal(N, D, p, causal, t))
+        e = mfma_nc_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
+    else
+        e = generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, t == FASTMAX_BF16, qk_scale,
+                        workspace, stream);
+    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+}
+
+}  // namespace fm
+
 extern "C" {
 
 size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
@@ -83,25 +120,12 @@ int fastmax_fwd_scaled(const void *q, const void *k, const void *v, void *out, f
                        fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
                        hipStream_t stream)
 {
-    int rc = check_common(B, H, N, D, p, causal, dt);
+    int rc = fm::fwd_validate(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt);
     if (rc != FASTMAX_OK) return rc;
-    if (!valid_scale(qk_scale)) return FASTMAX_EINVAL;
-    if (!q || !k || !v || !out) return FASTMAX_ENULL;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
-        (g && !aligned16(g)))
-        return FASTMAX_EALIGN;
     size_t need = fwd_ws(B, H, N, D, p, causal, dt);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
-    hipError_t e;
-    if (mfma_causal(D, p, causal, dt))
-        e = fm::mfma_causal_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
-    else if (mfma_noncausal(N, D, p, causal, dt))
-        e = fm::mfma_nc_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
-    else
-        e = fm::generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
-                            workspace, stream);
-    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+    return fm::fwd_run(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt, workspace, stream);
 }
 
 int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,

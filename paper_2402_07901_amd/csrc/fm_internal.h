@@ -7,6 +7,16 @@
 
 namespace fm {
 
+// The forward behind the C ABI in three steps (api.cpp): host-side argument
+// checks (a FASTMAX_* code), the workspace it needs, and the launch on the
+// path that serves the configuration (a FASTMAX_* code).  dt is a
+// fastmax_dtype_t.
+int fwd_validate(const void *q, const void *k, const void *v, const void *out, const float *g,
+                 int B, int H, int N, int D, int p, int causal, float qk_scale, int dt);
+size_t fwd_workspace(int B, int H, int N, int D, int p, int causal, int dt);
+int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, int B, int H, int N,
+            int D, int p, int causal, float qk_scale, int dt, void *workspace, hipStream_t stream);
+
 // Generic float32-VALU path: every (D, p, causal, dtype).
 // qs: score scale (weights f_p(qs q^.k^)), applied to q^ where it is
 // standardised and to dq^ before the standardisation backward.

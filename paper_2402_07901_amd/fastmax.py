@@ -68,6 +68,8 @@ def lib():
         L.fastmax_bwd_dropout.argtypes = [vp, vp, vp, vp, vp, vp, vp, f, vp, vp, vp, i, i, i, i,
                                           i, f, i, vp, sz, vp]
         L.fastmax_bwd_dropout.restype = i
+        L.fastmax_fwd_noalloc.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp]
+        L.fastmax_fwd_noalloc.restype = i
         L.fastmax_strerror.argtypes = [i]
         L.fastmax_strerror.restype = ctypes.c_char_p
         L.fastmax_version.restype = ctypes.c_char_p
@@ -131,6 +133,27 @@ def fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt
                                     _ptr(dq), _ptr(dk), _ptr(dv), B, H, N, D, p, int(causal),
                                     float(scale), dt, _ptr(workspace), ws_bytes,
                                     _stream(stream))
+
+
+# the library's per-GPU scratch size for fastmax_fwd_noalloc (include/fastmax.h)
+NOALLOC_MAX_WORKSPACE_BYTES = 64 << 20
+
+
+def fastmax_fwd_noalloc_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, stream, scale=1.0):
+    """Direct call of fastmax_fwd_noalloc with raw pointers/ints; returns the code."""
+    return lib().fastmax_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(g), B, H, N, D,
+                                     p, int(causal), float(scale), dt, _stream(stream))
+
+
+def fastmax_fwd_noalloc(q, k, v, out, g=None, p=2, causal=False, stream=None, scale=None):
+    """fastmax_fwd into caller-provided ``out`` (and ``g``) with the library's
+    per-GPU scratch as workspace: nothing is allocated."""
+    B, H, N, D = q.shape
+    rc = fastmax_fwd_noalloc_raw(q, k, v, out, g, B, H, N, D, p, causal, _dtype_code(q), stream,
+                                 1.0 if scale is None else scale)
+    if rc != OK:
+        raise FastmaxError(rc, "fastmax_fwd_noalloc")
+    return out, g
 
 
 def _alloc_ws(nbytes, device):

@@ -270,3 +270,39 @@ def test_bwd_dropout_rejects():
     assert bwd_drop() == fm.EWORKSPACE   # the backward always needs one
     need = fm.lib().fastmax_dropout_workspace_bytes(1, 1, 8, 64, 1, fm.BF16, 1)
     assert bwd_drop(ws=A, wsb=need - 1) == fm.EWORKSPACE
+
+
+def fwd_noalloc(q=A, k=A, v=A, out=A, g=None, B=1, H=1, N=8, D=64, p=2, causal=1, dt=fm.BF16,
+                scale=1.0):
+    return fm.lib().fastmax_fwd_noalloc(ctypes.c_void_p(q), ctypes.c_void_p(k),
+                                        ctypes.c_void_p(v), ctypes.c_void_p(out),
+                                        ctypes.c_void_p(g) if g else None, B, H, N, D, p, causal,
+                                        float(scale), dt, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), fm.EINVAL), (dict(p=3), fm.EINVAL), (dict(dt=7), fm.EINVAL),
+    (dict(scale=0.0), fm.EINVAL), (dict(scale=1.5), fm.EINVAL), (dict(D=48), fm.EUNSUPPORTED),
+    (dict(q=0), fm.ENULL), (dict(out=0), fm.ENULL), (dict(k=A + 8), fm.EALIGN),
+    (dict(g=A + 4), fm.EALIGN),
+])
+def test_fwd_noalloc_validates_like_the_forward(kw, code):
+    assert fwd_noalloc(**kw) == code
+
+
+def test_fwd_noalloc_rejects_problems_beyond_its_scratch():
+    """A problem whose forward workspace exceeds the 64 MiB scratch is
+    rejected on the host (EWORKSPACE), one that fits is not rejected for
+    its size (with a NULL q it then fails on the pointer check)."""
+    lim = fm.NOALLOC_MAX_WORKSPACE_BYTES
+    big = dict(B=1, H=1, N=1 << 20, D=64, p=2, causal=1, dt=fm.BF16)
+    need = fm.workspace_bytes(big["B"], big["H"], big["N"], big["D"], big["p"], big["causal"],
+                              big["dt"])
+    assert need > lim
+    assert fwd_noalloc(**big) == fm.EWORKSPACE
+    small = dict(B=1, H=1, N=4096, D=64, p=2, causal=1, dt=fm.BF16)
+    assert 0 < fm.workspace_bytes(1, 1, 4096, 64, 2, 1, fm.BF16) <= lim
+    assert fwd_noalloc(q=0, **small) == fm.ENULL
+    # the largest causal bf16 D = 64 problem the header quotes fits exactly
+    assert fm.workspace_bytes(1, 1, 262144, 64, 2, 1, fm.BF16) <= lim
+    assert fm.workspace_bytes(1, 1, 262144 + 4096, 64, 2, 1, fm.BF16) > lim
