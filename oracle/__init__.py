@@ -18,19 +18,36 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "fastmax_ref.c")
-_LIB = os.path.join(_HERE, "libfastmax_oracle.so")
+_LIB_DEFAULT = os.path.join(_HERE, "libfastmax_oracle.so")
+# the sanitizer tier (tests/test_sanitize.py) points this at the
+# AddressSanitizer/UBSan build of the same source
+_LIB = os.environ.get("FASTMAX_ORACLE_LIB", _LIB_DEFAULT)
+LIB_ASAN = os.path.join(_HERE, "libfastmax_oracle_asan.so")
 _lib = None
 
 
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc (-O2, OpenMP). Returns the library path."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
+    if force or not os.path.exists(_LIB_DEFAULT):
+        tmp = _LIB_DEFAULT + ".tmp"
         cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
                "-Wall", "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, _LIB_DEFAULT)
+    return _LIB_DEFAULT
+
+
+def build_sanitized() -> str:
+    """Compile the oracle with AddressSanitizer and UndefinedBehaviorSanitizer
+    (gcc; any report aborts).  Returns the library path; a process loading it
+    needs gcc's libasan preloaded."""
+    tmp = LIB_ASAN + ".tmp"
+    cmd = ["gcc", "-O1", "-g", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-fno-omit-frame-pointer", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_ASAN)
+    return LIB_ASAN
 
 
 def _bind(path):

@@ -39,31 +39,53 @@ def sources():
 EXTRA = {}
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *COMMON, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
+# Sanitizer build (tests/test_sanitize.py): AddressSanitizer and UBSan on the
+# host code only (argument validation, workspace plans, dispatch); the GPU
+# code is built as usual.  Linked by clang++ against the HIP runtime.
+LIB_ASAN = os.path.join(HERE, "libfastmax_asan.so")
+OBJDIR_ASAN = os.path.join(HERE, "_build_asan")
+HOST_SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host",
+                 "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
+CLANGXX = os.environ.get("CLANGXX", "/opt/rocm/llvm/bin/clang++")
+
+
+def _compile(src: str, sanitize: bool = False) -> str:
+    objdir = OBJDIR_ASAN if sanitize else OBJDIR
+    obj = os.path.join(objdir, os.path.basename(src) + ".o")
+    extra = HOST_SANITIZE if sanitize else []
+    cmd = [HIPCC, *COMMON, *EXTRA.get(os.path.basename(src), []), *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compiles every source in csrc/ and links libfastmax.so. Returns its path."""
-    os.makedirs(OBJDIR, exist_ok=True)
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compiles every source in csrc/ and links libfastmax.so (with
+    ``sanitize``: libfastmax_asan.so, host code under ASan/UBSan).  Returns
+    its path."""
+    objdir = OBJDIR_ASAN if sanitize else OBJDIR
+    lib = LIB_ASAN if sanitize else LIB
+    os.makedirs(objdir, exist_ok=True)
     srcs = sources()
     jobs = min(len(srcs), int(os.environ.get("MAX_JOBS", "8")))
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+        objs = list(ex.map(lambda s: _compile(s, sanitize), srcs))
+    tmp = lib + ".tmp"
+    if sanitize:
+        rocm = os.path.dirname(os.path.dirname(HIPCC))
+        cmd = [CLANGXX, "-shared", "-fPIC", "-fsanitize=address,undefined", "-o", tmp, *objs,
+               f"-L{os.path.join(rocm, 'lib')}", "-lamdhip64"]
+    else:
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {lib}")
+    return lib
 
 
 if __name__ == "__main__":

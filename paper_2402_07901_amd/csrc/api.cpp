@@ -1,6 +1,7 @@
 // C ABI of the Fastmax library: host-side validation, workspace sizing and
 // dispatch to the HIP kernels.  Every check runs before the first HIP call.
 #include <stdint.h>
+#include <string.h>
 
 #include "../../include/fastmax.h"
 #include "fm_common.h"
@@ -12,7 +13,7 @@ namespace {
 // float32 kernels; the MFMA kernels cover D = 64.
 bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
 
-int check_common(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+int check_common(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (B < 1 || H < 1 || N < 1) return FASTMAX_EINVAL;
     if (p != 1 && p != 2) return FASTMAX_EINVAL;
@@ -28,6 +29,17 @@ int check_common(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t 
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+// The dtype argument as an int, read without loading it as an enum: a C
+// caller may pass any int, and a C++ enum value outside the enumerators'
+// range is undefined behaviour (UBSan reports it), so validation reads the
+// bits.
+int dt_bits(const fastmax_dtype_t *dt)
+{
+    int v;
+    memcpy(&v, dt, sizeof v);
+    return v;
+}
+
 // The score scale multiplies q^.k^ inside f_p.  (0, 1] covers the definition
 // (1) and the unit-norm and temperature variants (1/D, 1/sqrt(D)); the fp16
 // moment scaling of the MFMA backward assumes |qs q^_m qs q^_l| <= 64.  NaN
@@ -39,7 +51,7 @@ bool valid_scale(float qs) { return qs > 0.0f && qs <= 1.0f; }
 // for one key against terms of size ~|q^||k^|^2/2), which amplifies that
 // rounding past the bf16 tolerance.  Below one 128-token chunk of keys the
 // fp32 generic kernel is exact to fp32 and costs next to nothing.
-bool mfma_noncausal(int N, int D, int p, int causal, fastmax_dtype_t dt)
+bool mfma_noncausal(int N, int D, int p, int causal, int dt)
 {
     return D == 64 && p == 2 && !causal && dt == FASTMAX_BF16 && N >= 128;
 }
@@ -49,19 +61,19 @@ bool valid_rate(float rate) { return rate >= 0.0f && rate < 1.0f; }
 
 bool aligned4(const void *p) { return ((uintptr_t)p & 3u) == 0; }
 
-bool mfma_causal(int D, int p, int causal, fastmax_dtype_t dt)
+bool mfma_causal(int D, int p, int causal, int dt)
 {
     return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
 }
 
-size_t fwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+size_t fwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_fwd_workspace(B * H, N);
     if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_workspace(B * H, N);
     return fm::generic_fwd_workspace(B * H, N, D, p);
 }
 
-size_t bwd_ws(int B, int H, int N, int D, int p, int causal, fastmax_dtype_t dt)
+size_t bwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_bwd_workspace(B * H, N);
     return fm::generic_bwd_workspace(B, H, N, D, p);
@@ -74,7 +86,7 @@ namespace fm {
 int fwd_validate(const void *q, const void *k, const void *v, const void *out, const float *g,
                  int B, int H, int N, int D, int p, int causal, float qk_scale, int dt)
 {
-    int rc = check_common(B, H, N, D, p, causal, (fastmax_dtype_t)dt);
+    int rc = check_common(B, H, N, D, p, causal, dt);
     if (rc != FASTMAX_OK) return rc;
     if (!valid_scale(qk_scale)) return FASTMAX_EINVAL;
     if (!q || !k || !v || !out) return FASTMAX_ENULL;
@@ -86,39 +98,30 @@ int fwd_validate(const void *q, const void *k, const void *v, const void *out, c
 
 size_t fwd_workspace(int B, int H, int N, int D, int p, int causal, int dt)
 {
-    return fwd_ws(B, H, N, D, p, causal, (fastmax_dtype_t)dt);
+    return fwd_ws(B, H, N, D, p, causal, dt);
 }
 
 int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, int B, int H, int N,
             int D, int p, int causal, float qk_scale, int dt, void *workspace, hipStream_t stream)
 {
-    const fastmax_dtype_t t = (fastmax_dtype_t)dt;
     hipError_t e;
-    if (mfma_causal(D, p, causal, t))
+    if (mfma_causal(D, p, causal, dt))
         e = mfma_causal_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
-    else if (mfma_noncausal(N, D, p, causal, t))
+    else if (mfma_noncausal(N, D, p, causal, dt))
         e = mfma_nc_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
     else
-        e = generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, t == FASTMAX_BF16, qk_scale,
+        e = generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
                         workspace, stream);
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 
 }  // namespace fm
 
-extern "C" {
+namespace {
 
-size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
-                               fastmax_dtype_t dt, int backward)
-{
-    if (check_common(B, H, N, D, p, causal, dt) != FASTMAX_OK) return 0;
-    return backward ? bwd_ws(B, H, N, D, p, causal, dt) : fwd_ws(B, H, N, D, p, causal, dt);
-}
-
-int fastmax_fwd_scaled(const void *q, const void *k, const void *v, void *out, float *g, int B,
-                       int H, int N, int D, int p, int causal, float qk_scale,
-                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
-                       hipStream_t stream)
+int fwd_impl(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,
+             int N, int D, int p, int causal, float qk_scale, int dt, void *workspace,
+             size_t workspace_bytes, hipStream_t stream)
 {
     int rc = fm::fwd_validate(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt);
     if (rc != FASTMAX_OK) return rc;
@@ -128,19 +131,10 @@ int fastmax_fwd_scaled(const void *q, const void *k, const void *v, void *out, f
     return fm::fwd_run(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt, workspace, stream);
 }
 
-int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,
-                int N, int D, int p, int causal, fastmax_dtype_t dt, void *workspace,
-                size_t workspace_bytes, hipStream_t stream)
-{
-    return fastmax_fwd_scaled(q, k, v, out, g, B, H, N, D, p, causal, 1.0f, dt, workspace,
-                              workspace_bytes, stream);
-}
-
-int fastmax_bwd_scaled(const void *q, const void *k, const void *v, const void *out,
-                       const void *dout, const float *g, void *dq, void *dk, void *dv, int B,
-                       int H, int N, int D, int p, int causal, float qk_scale,
-                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
-                       hipStream_t stream)
+int bwd_impl(const void *q, const void *k, const void *v, const void *out, const void *dout,
+             const float *g, void *dq, void *dk, void *dv, int B, int H, int N, int D, int p,
+             int causal, float qk_scale, int dt, void *workspace, size_t workspace_bytes,
+             hipStream_t stream)
 {
     int rc = check_common(B, H, N, D, p, causal, dt);
     if (rc != FASTMAX_OK) return rc;
@@ -162,13 +156,52 @@ int fastmax_bwd_scaled(const void *q, const void *k, const void *v, const void *
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 
+}  // namespace
+
+extern "C" {
+
+size_t fastmax_workspace_bytes(int B, int H, int N, int D, int p, int causal,
+                               fastmax_dtype_t dt, int backward)
+{
+    const int d = dt_bits(&dt);
+    if (check_common(B, H, N, D, p, causal, d) != FASTMAX_OK) return 0;
+    return backward ? bwd_ws(B, H, N, D, p, causal, d) : fwd_ws(B, H, N, D, p, causal, d);
+}
+
+int fastmax_fwd_scaled(const void *q, const void *k, const void *v, void *out, float *g, int B,
+                       int H, int N, int D, int p, int causal, float qk_scale,
+                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream)
+{
+    return fwd_impl(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt_bits(&dt), workspace,
+                    workspace_bytes, stream);
+}
+
+int fastmax_fwd(const void *q, const void *k, const void *v, void *out, float *g, int B, int H,
+                int N, int D, int p, int causal, fastmax_dtype_t dt, void *workspace,
+                size_t workspace_bytes, hipStream_t stream)
+{
+    return fwd_impl(q, k, v, out, g, B, H, N, D, p, causal, 1.0f, dt_bits(&dt), workspace,
+                    workspace_bytes, stream);
+}
+
+int fastmax_bwd_scaled(const void *q, const void *k, const void *v, const void *out,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int B,
+                       int H, int N, int D, int p, int causal, float qk_scale,
+                       fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream)
+{
+    return bwd_impl(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, qk_scale,
+                    dt_bits(&dt), workspace, workspace_bytes, stream);
+}
+
 int fastmax_bwd(const void *q, const void *k, const void *v, const void *out, const void *dout,
                 const float *g, void *dq, void *dk, void *dv, int B, int H, int N, int D, int p,
                 int causal, fastmax_dtype_t dt, void *workspace, size_t workspace_bytes,
                 hipStream_t stream)
 {
-    return fastmax_bwd_scaled(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, 1.0f, dt,
-                              workspace, workspace_bytes, stream);
+    return bwd_impl(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, 1.0f,
+                    dt_bits(&dt), workspace, workspace_bytes, stream);
 }
 
 size_t fastmax_dropout_mask_words(int D)
@@ -193,16 +226,17 @@ int fastmax_dropout_mask(uint32_t *keep_bits, int B, int H, int N, int D, float 
 size_t fastmax_dropout_workspace_bytes(int B, int H, int N, int D, int causal,
                                        fastmax_dtype_t dt, int backward)
 {
-    if (check_common(B, H, N, D, 2, causal, dt) != FASTMAX_OK) return 0;
+    if (check_common(B, H, N, D, 2, causal, dt_bits(&dt)) != FASTMAX_OK) return 0;
     return backward ? fm::generic_bwd_workspace(B, H, N, D, 2)
                     : fm::generic_fwd_dropout_workspace(B * H, N, D, causal);
 }
 
 int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, float *g,
                         const uint32_t *keep_bits, float rate, int B, int H, int N, int D,
-                        int causal, float qk_scale, fastmax_dtype_t dt, void *workspace,
+                        int causal, float qk_scale, fastmax_dtype_t dt_arg, void *workspace,
                         size_t workspace_bytes, hipStream_t stream)
 {
+    const int dt = dt_bits(&dt_arg);
     int rc = check_common(B, H, N, D, 2, causal, dt);
     if (rc != FASTMAX_OK) return rc;
     if (!valid_scale(qk_scale) || !valid_rate(rate)) return FASTMAX_EINVAL;
@@ -222,9 +256,10 @@ int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, 
 int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void *out,
                         const void *dout, const float *g, const uint32_t *keep_bits, float rate,
                         void *dq, void *dk, void *dv, int B, int H, int N, int D, int causal,
-                        float qk_scale, fastmax_dtype_t dt, void *workspace,
+                        float qk_scale, fastmax_dtype_t dt_arg, void *workspace,
                         size_t workspace_bytes, hipStream_t stream)
 {
+    const int dt = dt_bits(&dt_arg);
     int rc = check_common(B, H, N, D, 2, causal, dt);
     if (rc != FASTMAX_OK) return rc;
     if (!valid_scale(qk_scale) || !valid_rate(rate)) return FASTMAX_EINVAL;

@@ -5,6 +5,8 @@
 // by every call on that GPU.
 #include <hip/hip_runtime.h>
 
+#include <string.h>
+
 #include <mutex>
 
 #include "../../include/fastmax.h"
@@ -44,13 +46,16 @@ extern "C" int fastmax_fwd_noalloc(const void *q, const void *k, const void *v, 
                                    float *g, int B, int H, int N, int D, int p, int causal,
                                    float qk_scale, fastmax_dtype_t dt, hipStream_t stream)
 {
-    const int rc = fm::fwd_validate(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt);
+    // the dtype's bits, not a load of the enum (a C caller may pass any int)
+    int d;
+    memcpy(&d, &dt, sizeof d);
+    const int rc = fm::fwd_validate(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, d);
     if (rc != FASTMAX_OK) return rc;
-    if (fm::fwd_workspace(B, H, N, D, p, causal, dt) > FASTMAX_NOALLOC_MAX_WORKSPACE_BYTES)
+    if (fm::fwd_workspace(B, H, N, D, p, causal, d) > FASTMAX_NOALLOC_MAX_WORKSPACE_BYTES)
         return FASTMAX_EWORKSPACE;
     // No forward kernel relies on zeroed workspace (every buffer in it is
     // written before it is read), so nothing is cleared.
     void *ws = scratch_ptr();
     if (!ws) return FASTMAX_EHIP;
-    return fm::fwd_run(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt, ws, stream);
+    return fm::fwd_run(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, d, ws, stream);
 }

@@ -11,7 +11,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfastmax.so")
+# the sanitizer tier (tests/test_sanitize.py) points FASTMAX_LIB at the build
+# whose host code carries AddressSanitizer/UBSan
+LIB_PATH = os.environ.get("FASTMAX_LIB", os.path.join(_HERE, "libfastmax.so"))
 
 F32 = 0
 BF16 = 1
