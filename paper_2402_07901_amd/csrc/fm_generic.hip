@@ -1,8 +1,9 @@
 // Generic Fastmax kernels: float32 VALU arithmetic, the moment state of one
 // column slice held in LDS, tokens processed in chunks of CH.  They serve
-// every supported (D, p, causal, dtype) and are the reference GPU path the
-// MFMA kernels are checked against; the MFMA kernels take over where they
-// apply.
+// every supported (D, p, causal, dtype) that the MFMA kernels do not (those
+// take over for bf16, D = 64, p = 2 where they apply).  Like the MFMA
+// kernels, they are checked against the fp64 CPU oracle; they are not a
+// reference for the MFMA kernels.
 //
 // Notation (Sec. 2.4): phi(k) = [1, k, (k_m k_l)_{m<=l}] are the key-side
 // features, psi(q) = [1, q, (c_ml q_m q_l)_{m<=l}] with c_mm = 1/2 and
