@@ -76,6 +76,7 @@ size_t fwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 size_t bwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_bwd_workspace(B * H, N);
+    if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_bwd_workspace(B * H, N);
     return fm::generic_bwd_workspace(B, H, N, D, p);
 }
 
@@ -150,6 +151,9 @@ int bwd_impl(const void *q, const void *k, const void *v, const void *out, const
     if (mfma_causal(D, p, causal, dt))
         e = fm::mfma_causal_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, qk_scale, workspace,
                                 stream);
+    else if (mfma_noncausal(N, D, p, causal, dt))
+        e = fm::mfma_nc_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, qk_scale, workspace,
+                            stream);
     else
         e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
                             dt == FASTMAX_BF16, qk_scale, workspace, stream);

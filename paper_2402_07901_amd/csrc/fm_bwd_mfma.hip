@@ -340,7 +340,7 @@ struct GSmem {
     f4 ex[4][3][64];              // the extra accumulator tiles of waves 0-3, between uses
 };
 
-template <int DIR>
+template <int DIR, bool CAUSAL>
 __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
                                         const _Float16 *__restrict__ x,
                                         const _Float16 *__restrict__ y,
@@ -473,147 +473,190 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
         }
     };
 
-    prefetch(chunk_of(0));
-    stage_xz(chunk_of(0));
-    stage_yw(chunk_of(0));
-    __syncthreads();
-
-    for (int kk = 0; kk < nch; ++kk) {
-        const int c = chunk_of(kk);
-        const bool more = kk + 1 < nch;
-        __builtin_amdgcn_sched_barrier(0);
-        refresh_ids();
-        // ---- (A) contraction of chunk c with the moments of earlier chunks --
-        if (kk > 0) {
-            if (w == 0 && h == 0) sm.m1g[r16] = sm.ex[0][2][lane][0];
-            h8 Aex = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (w < 4) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
+    // (A) contraction of the staged output side (chunk c) with the moments
+    // accumulated so far; partial outputs to LDS
+    auto contract = [&]() {
+        if (w == 0 && h == 0) sm.m1g[r16] = sm.ex[0][2][lane][0];
+        h8 Aex = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (w < 4) Aex = cat(cvt4(sm.ex[w][0][lane]), cvt4(sm.ex[w][1][lane]));
 #pragma unroll 1
-            for (int rt = 0; rt < C / 16; ++rt) {
-                const int t = 16 * rt + r16;
-                const h8 xv = ld8(sm.xrow + sw64(t, MG_MPW * w));
-                h8 Zb[2];
+        for (int rt = 0; rt < C / 16; ++rt) {
+            const int t = 16 * rt + r16;
+            const h8 xv = ld8(sm.xrow + sw64(t, MG_MPW * w));
+            h8 Zb[2];
 #pragma unroll
-                for (int p = 0; p < 2; ++p)
-                    Zb[p] = cat(ld4(sm.zrow + sw64(t, 32 * p + 4 * h)),
-                                ld4(sm.zrow + sw64(t, 32 * p + 16 + 4 * h)));
-                f4 Dout = {0.f, 0.f, 0.f, 0.f};
+            for (int p = 0; p < 2; ++p)
+                Zb[p] = cat(ld4(sm.zrow + sw64(t, 32 * p + 4 * h)),
+                            ld4(sm.zrow + sw64(t, 32 * p + 16 + 4 * h)));
+            f4 Dout = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int mm = 0; mm < MG_MPW; ++mm) {
-                    f4 E = {0.f, 0.f, 0.f, 0.f};
-                    E = mfma(Ast[mm][0], Zb[0], E);
-                    E = mfma(Ast[mm][1], Zb[1], E);
-                    const float xm = (float)xv[mm];
+            for (int mm = 0; mm < MG_MPW; ++mm) {
+                f4 E = {0.f, 0.f, 0.f, 0.f};
+                E = mfma(Ast[mm][0], Zb[0], E);
+                E = mfma(Ast[mm][1], Zb[1], E);
+                const float xm = (float)xv[mm];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) Dout[i] = fmaf(xm, E[i], Dout[i]);
-                }
-                if (w < 4) {
-                    const float zd = sm.zD[t];
-                    if (w < 2) {
-                        // z at this wave's M1 column pair
-                        const h8 Zw = cat(ld4(sm.zrow + sw64(t, 32 * w + 4 * h)),
-                                          ld4(sm.zrow + sw64(t, 32 * w + 16 + 4 * h)));
-                        Dout = mfma(Aex, Zw, Dout);
-                        if (w == 0) {
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, sm.m1g[4 * h + i], Dout[i]);
-                        }
-                    } else {
-                        const h8 Xb = cat(ld4(sm.xrow + sw64(t, 32 * (w - 2) + 4 * h)),
-                                          ld4(sm.xrow + sw64(t, 32 * (w - 2) + 16 + 4 * h)));
-                        f4 Eg = {0.f, 0.f, 0.f, 0.f};
-                        Eg = mfma(Aex, Xb, Eg);
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, Eg[i], Dout[i]);
-                    }
-                }
-                *(f4 *)(sm.fpart + ((w * 4 + h) * C + t) * 4) = Dout;
+                for (int i = 0; i < 4; ++i) Dout[i] = fmaf(xm, E[i], Dout[i]);
             }
-        }
-        __syncthreads();
-
-        // ---- (B) add chunk c's contribution, update the moments with chunk c,
-        //          stage the output side of the next chunk ----------------------
-        __builtin_amdgcn_sched_barrier(0);
-        refresh_ids();
-        if (kk > 0) {
-            const int t = tid & (C - 1), qd = tid >> 7;
-            const int n = c * C + t;
-            if (n < N) {
-                f4 F = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ww = 0; ww < MG_NW; ++ww)
-                    F += *(const f4 *)(sm.fpart + ((ww * 4 + qd) * C + t) * 4);
-                f4 *dst = (f4 *)(dxh + (size_t)n * D + 16 * L + 4 * qd);
-                *dst = *dst + F * sout;
-            }
-        }
-        if (more) prefetch(chunk_of(kk + 1));
-        {
-            // moments += chunk c, 32 tokens per K step, on fp32 tiles rebuilt
-            // from the fp16 pairs
-            h8 pa = {0, 0, 0, 0, 0, 0, 0, 0}, pb = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const bool on = h == (r16 >> 2) && jj == (r16 & 3);
-                pa[jj] = on ? (_Float16)1.0f : (_Float16)0.0f;
-                pb[4 + jj] = on ? (_Float16)1.0f : (_Float16)0.0f;
-            }
-            f4 acc[MG_MPW][4];
-#pragma unroll
-            for (int m = 0; m < MG_MPW; ++m)
-#pragma unroll
-                for (int jt = 0; jt < 4; ++jt)
-                    acc[m][jt] = mfma((jt & 1) ? pb : pa, Ast[m][jt >> 1], f4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll 1
-            for (int ks = 0; ks < C / 32; ++ks) {
-                const int col = 32 * ks + 8 * h;
-                h8 Aw[4];
-#pragma unroll
-                for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(sm.wT + swx(16 * jt + r16, col));
-                const h8 Yl = ld8(sm.yT + swx(16 * L + r16, col));
-#pragma unroll
-                for (int m = 0; m < MG_MPW; ++m) {
-                    const h8 Ym = ld8(sm.yT + swx(MG_MPW * w + m, col));
-                    const h8 Bm = Ym * Yl;
-#pragma unroll
-                    for (int jt = 0; jt < 4; ++jt) acc[m][jt] = mfma(Aw[jt], Bm, acc[m][jt]);
-                }
-                if (w < 4) {
-                    const h8 WD = ld8(sm.wDh + col);
-                    f4 ex[3];
-#pragma unroll
-                    for (int e = 0; e < 3; ++e) ex[e] = sm.ex[w][e][lane];
+            if (w < 4) {
+                const float zd = sm.zD[t];
+                if (w < 2) {
+                    // z at this wave's M1 column pair
+                    const h8 Zw = cat(ld4(sm.zrow + sw64(t, 32 * w + 4 * h)),
+                                      ld4(sm.zrow + sw64(t, 32 * w + 16 + 4 * h)));
+                    Dout = mfma(Aex, Zw, Dout);
                     if (w == 0) {
-                        ex[0] = mfma(Aw[0], Yl, ex[0]);
-                        ex[1] = mfma(Aw[1], Yl, ex[1]);
-                        const h8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
-                        ex[2] = mfma(r16 == 0 ? WD : zero8, Yl, ex[2]);
-                    } else if (w == 1) {
-                        ex[0] = mfma(Aw[2], Yl, ex[0]);
-                        ex[1] = mfma(Aw[3], Yl, ex[1]);
-                    } else {
-                        const h8 YW = Yl * WD;
 #pragma unroll
-                        for (int e = 0; e < 2; ++e) {
-                            const int mt = 2 * (w - 2) + e;
-                            ex[e] = mfma(ld8(sm.yT + swx(16 * mt + r16, col)), YW, ex[e]);
-                        }
+                        for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, sm.m1g[4 * h + i], Dout[i]);
                     }
+                } else {
+                    const h8 Xb = cat(ld4(sm.xrow + sw64(t, 32 * (w - 2) + 4 * h)),
+                                      ld4(sm.xrow + sw64(t, 32 * (w - 2) + 16 + 4 * h)));
+                    f4 Eg = {0.f, 0.f, 0.f, 0.f};
+                    Eg = mfma(Aex, Xb, Eg);
 #pragma unroll
-                    for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = ex[e];
+                    for (int i = 0; i < 4; ++i) Dout[i] = fmaf(zd, Eg[i], Dout[i]);
                 }
             }
-#pragma unroll
-            for (int m = 0; m < MG_MPW; ++m)
-#pragma unroll
-                for (int p = 0; p < 2; ++p) Ast[m][p] = cat(cvt4(acc[m][2 * p]), cvt4(acc[m][2 * p + 1]));
+            *(f4 *)(sm.fpart + ((w * 4 + h) * C + t) * 4) = Dout;
         }
-        if (more) stage_xz(chunk_of(kk + 1));
+    };
+    // the waves' partial outputs of chunk c summed into dx^ (added to the
+    // in-chunk part when causal, stored when the moments are totals)
+    auto combine = [&](int c) {
+        const int t = tid & (C - 1), qd = tid >> 7;
+        const int n = c * C + t;
+        if (n < N) {
+            f4 F = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ww = 0; ww < MG_NW; ++ww)
+                F += *(const f4 *)(sm.fpart + ((ww * 4 + qd) * C + t) * 4);
+            f4 *dst = (f4 *)(dxh + (size_t)n * D + 16 * L + 4 * qd);
+            if constexpr (CAUSAL) *dst = *dst + F * sout;
+            else *dst = F * sout;
+        }
+    };
+    // (B) moments += the staged summed side (chunk c), 32 tokens per K step,
+    // on fp32 tiles rebuilt from the fp16 pairs
+    auto update = [&]() {
+        h8 pa = {0, 0, 0, 0, 0, 0, 0, 0}, pb = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const bool on = h == (r16 >> 2) && jj == (r16 & 3);
+            pa[jj] = on ? (_Float16)1.0f : (_Float16)0.0f;
+            pb[4 + jj] = on ? (_Float16)1.0f : (_Float16)0.0f;
+        }
+        f4 acc[MG_MPW][4];
+#pragma unroll
+        for (int m = 0; m < MG_MPW; ++m)
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt)
+                acc[m][jt] = mfma((jt & 1) ? pb : pa, Ast[m][jt >> 1], f4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll 1
+        for (int ks = 0; ks < C / 32; ++ks) {
+            const int col = 32 * ks + 8 * h;
+            h8 Aw[4];
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) Aw[jt] = ld8(sm.wT + swx(16 * jt + r16, col));
+            const h8 Yl = ld8(sm.yT + swx(16 * L + r16, col));
+#pragma unroll
+            for (int m = 0; m < MG_MPW; ++m) {
+                const h8 Ym = ld8(sm.yT + swx(MG_MPW * w + m, col));
+                const h8 Bm = Ym * Yl;
+#pragma unroll
+                for (int jt = 0; jt < 4; ++jt) acc[m][jt] = mfma(Aw[jt], Bm, acc[m][jt]);
+            }
+            if (w < 4) {
+                const h8 WD = ld8(sm.wDh + col);
+                f4 ex[3];
+#pragma unroll
+                for (int e = 0; e < 3; ++e) ex[e] = sm.ex[w][e][lane];
+                if (w == 0) {
+                    ex[0] = mfma(Aw[0], Yl, ex[0]);
+                    ex[1] = mfma(Aw[1], Yl, ex[1]);
+                    const h8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+                    ex[2] = mfma(r16 == 0 ? WD : zero8, Yl, ex[2]);
+                } else if (w == 1) {
+                    ex[0] = mfma(Aw[2], Yl, ex[0]);
+                    ex[1] = mfma(Aw[3], Yl, ex[1]);
+                } else {
+                    const h8 YW = Yl * WD;
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int mt = 2 * (w - 2) + e;
+                        ex[e] = mfma(ld8(sm.yT + swx(16 * mt + r16, col)), YW, ex[e]);
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 3; ++e) sm.ex[w][e][lane] = ex[e];
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < MG_MPW; ++m)
+#pragma unroll
+            for (int p = 0; p < 2; ++p) Ast[m][p] = cat(cvt4(acc[m][2 * p]), cvt4(acc[m][2 * p + 1]));
+    };
+
+    if constexpr (CAUSAL) {
+        prefetch(chunk_of(0));
+        stage_xz(chunk_of(0));
+        stage_yw(chunk_of(0));
         __syncthreads();
-        // ---- (C) stage the summed side of the next chunk (after the update) ---
-        if (more) {
-            stage_yw(chunk_of(kk + 1));
+        for (int kk = 0; kk < nch; ++kk) {
+            const int c = chunk_of(kk);
+            const bool more = kk + 1 < nch;
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            // (A) chunk c against the moments of earlier chunks
+            if (kk > 0) contract();
+            __syncthreads();
+            // (B) chunk c's contribution out, the moments updated with chunk
+            //     c, the output side of the next chunk staged
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            if (kk > 0) combine(c);
+            if (more) prefetch(chunk_of(kk + 1));
+            update();
+            if (more) stage_xz(chunk_of(kk + 1));
+            __syncthreads();
+            // (C) the summed side of the next chunk (after the update)
+            if (more) {
+                stage_yw(chunk_of(kk + 1));
+                __syncthreads();
+            }
+        }
+    } else {
+        // totals (Sec. 2.5 with every pair (s, t) present): the moments of
+        // all chunks first, then every chunk contracted against them
+        prefetch(0);
+        stage_yw(0);
+        __syncthreads();
+        for (int c = 0; c < nch; ++c) {
+            const bool more = c + 1 < nch;
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            if (more) prefetch(c + 1);
+            update();
+            __syncthreads();
+            if (more) {
+                stage_yw(c + 1);
+                __syncthreads();
+            }
+        }
+        prefetch(0);
+        stage_xz(0);
+        __syncthreads();
+        for (int c = 0; c < nch; ++c) {
+            const bool more = c + 1 < nch;
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            contract();
+            if (more) prefetch(c + 1);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+            refresh_ids();
+            combine(c);
+            if (more) stage_xz(c + 1);
             __syncthreads();
         }
     }
@@ -621,6 +664,7 @@ __device__ __forceinline__ void mg_scan(GSmem &sm, int b, int nblk,
 
 // Both moment-gradient scans in one launch: blocks [0, 4BH) build dq^ (chunks
 // in order), blocks [4BH, 8BH) build dk^ (chunks in reverse order).
+template <bool CAUSAL>
 __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__restrict__ qh,
                                                           const _Float16 *__restrict__ kh,
                                                           const bf16_t *__restrict__ v,
@@ -636,9 +680,9 @@ __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__rest
     const int half = 4 * BH;
     const int b = blockIdx.x;
     if (b < half)
-        mg_scan<0>(sm, b, half, qh, kh, dout, v, rg, cc, hmax, dqh, N, BH);
+        mg_scan<0, CAUSAL>(sm, b, half, qh, kh, dout, v, rg, cc, hmax, dqh, N, BH);
     else
-        mg_scan<1>(sm, b - half, half, kh, qh, v, dout, rg, cc, hmax, dkh, N, BH);
+        mg_scan<1, CAUSAL>(sm, b - half, half, kh, qh, v, dout, rg, cc, hmax, dkh, N, BH);
 }
 
 // dv and the in-chunk pairs in one launch: blocks [0, 4BH) run the causal scan
@@ -735,20 +779,27 @@ __global__ __launch_bounds__(256) void bwd_finish(const bf16_t *__restrict__ q,
 
 }  // namespace mfma_bwd
 
-size_t mfma_causal_bwd_workspace(int BH, int N)
+namespace mfma_bwd {
+
+size_t base_workspace(int BH, int N)
 {
     const size_t rows = (size_t)BH * N;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t nch = ((size_t)N + mfma_bwd::C - 1) / mfma_bwd::C;
+    const size_t nch = ((size_t)N + C - 1) / C;
     return a256(rows * 4) * 2 + a256((size_t)BH * nch * 16) + 2 * a256(rows * mx::D * 4) +
            2 * a256(rows * mx::D * 2);
 }
 
-hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
-                           const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                           int N, float qs, void *ws, hipStream_t st)
+// Causal: dv by the reverse scan with the in-chunk blocks, then the
+// moment-gradient scans over earlier chunks.  Non-causal: dv by the
+// non-causal forward kernels (queries and keys exchanged, no divide; their
+// workspace after the backward's own), then the moment-gradient scans
+// against the totals.
+template <bool CAUSAL>
+hipError_t run(const void *q, const void *k, const void *v, const void *o, const void *dout,
+               const float *g, void *dq, void *dk, void *dv, int BH, int N, float qs, void *ws,
+               hipStream_t st)
 {
-    using namespace mfma_bwd;
     static_assert(sizeof(ISmem) <= 160 * 1024 && sizeof(GSmem) <= 160 * 1024 &&
                       sizeof(mfma_causal::Smem) <= 160 * 1024,
                   "LDS budget");
@@ -772,6 +823,7 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
     _Float16 *qh = (_Float16 *)p;
     p += a256(rows * D * 2);
     _Float16 *kh = (_Float16 *)p;
+    p += a256(rows * D * 2);
 
     const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
     const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
@@ -779,25 +831,52 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                        qh, kh, N, nch, qs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t smem1 = sizeof(ISmem) > sizeof(mfma_causal::Smem) ? sizeof(ISmem)
-                                                                    : sizeof(mfma_causal::Smem);
-    e = hipFuncSetAttribute((const void *)bwd_dv_intra,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem1);
+    if constexpr (CAUSAL) {
+        const size_t smem1 = sizeof(ISmem) > sizeof(mfma_causal::Smem) ? sizeof(ISmem)
+                                                                        : sizeof(mfma_causal::Smem);
+        e = hipFuncSetAttribute((const void *)bwd_dv_intra,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem1);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(bwd_dv_intra, dim3(BH * 4 + BH * nch), dim3(512), smem1, st, qh, kh, V,
+                           DO, rg, cc, hmax, dqh, dkh, (bf16_t *)dv, N, nch, BH);
+    } else {
+        e = mfma_nc_dv(qh, kh, DO, rg, dv, BH, N, p, st);
+    }
+    e = e == hipSuccess ? hipGetLastError() : e;
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_dv_intra, dim3(BH * 4 + BH * nch), dim3(512), smem1, st, qh, kh, V, DO,
-                       rg, cc, hmax, dqh, dkh, (bf16_t *)dv, N, nch, BH);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void *)bwd_mg_scans,
+    e = hipFuncSetAttribute((const void *)bwd_mg_scans<CAUSAL>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GSmem));
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_mg_scans, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, qh, kh, V,
-                       DO, rg, cc, hmax, dqh, dkh, N, BH);
+    hipLaunchKernelGGL(bwd_mg_scans<CAUSAL>, dim3(BH * 8), dim3(MG_NTH), sizeof(GSmem), st, qh, kh,
+                       V, DO, rg, cc, hmax, dqh, dkh, N, BH);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bwd_finish, dim3((unsigned)((rows + 31) / 32)), dim3(256), 0, st, Q, K,
                        dqh, dkh, (bf16_t *)dq, (bf16_t *)dk, rows, qs);
     return hipGetLastError();
+}
+
+}  // namespace mfma_bwd
+
+size_t mfma_causal_bwd_workspace(int BH, int N) { return mfma_bwd::base_workspace(BH, N); }
+
+hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const void *o,
+                           const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                           int N, float qs, void *ws, hipStream_t st)
+{
+    return mfma_bwd::run<true>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs, ws, st);
+}
+
+size_t mfma_nc_bwd_workspace(int BH, int N)
+{
+    return mfma_bwd::base_workspace(BH, N) + mfma_nc_workspace(BH, N);
+}
+
+hipError_t mfma_nc_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                       int N, float qs, void *ws, hipStream_t st)
+{
+    return mfma_bwd::run<false>(q, k, v, o, dout, g, dq, dk, dv, BH, N, qs, ws, st);
 }
 
 }  // namespace fm

@@ -64,10 +64,23 @@ hipError_t mfma_causal_bwd(const void *q, const void *k, const void *v, const vo
                            int N, float qs, void *ws, hipStream_t st);
 size_t mfma_causal_bwd_workspace(int BH, int N);
 
+// MFMA non-causal backward: D = 64, p = 2, bf16 I/O, N >= 128 (dv on the
+// non-causal forward kernels, dq^ and dk^ by the moment-gradient scans
+// against the totals).  ws holds mfma_nc_bwd_workspace(BH, N) bytes.
+hipError_t mfma_nc_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                       int N, float qs, void *ws, hipStream_t st);
+size_t mfma_nc_bwd_workspace(int BH, int N);
+
 // MFMA non-causal path: D = 64, p = 2, bf16 I/O (moment build, segment
 // reduction, query contraction).  ws holds mfma_nc_workspace(BH, N) bytes.
 hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
                        int N, float qs, void *ws, hipStream_t st);
 size_t mfma_nc_workspace(int BH, int N);
+// The non-causal backward's dv on the same kernels (keys q^, queries k^, both
+// standardised in fp16; values dO scaled per row by rg = 1/G; no divide).
+// ws holds mfma_nc_workspace(BH, N) bytes.
+hipError_t mfma_nc_dv(const void *qh, const void *kh, const void *dout, const float *rg, void *dv,
+                      int BH, int N, void *ws, hipStream_t st);
 
 }  // namespace fm

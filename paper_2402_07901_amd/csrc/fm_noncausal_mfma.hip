@@ -96,8 +96,15 @@ struct MSmem {
     float red[NW];
 };
 
-__global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ k,
+// KF16: the keys arrive standardised in fp16 (else bf16 rows, standardised
+// here).  The backward's dv (Sec. 2.5: dv_n = sum_i f(s_in) u_i, the forward
+// with queries and keys exchanged) uses KF16 with the standardised queries
+// as keys and the values u_i = dO_i / G_i: each value row v_n is multiplied
+// by vrow[n] when vrow is given.
+template <bool KF16>
+__global__ __launch_bounds__(NTH, 2) void nc_moments(const void *__restrict__ kin,
                                                      const bf16_t *__restrict__ v,
+                                                     const float *__restrict__ vrow,
                                                      float *__restrict__ part,
                                                      float *__restrict__ vmx,
                                                      float *__restrict__ y3p,
@@ -125,8 +132,9 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ 
     const int nch = (N + C - 1) / C;
     const int c0 = seg * cps, c1 = min(nch, c0 + cps);
     const int t0 = c0 * C, t1 = min(N, c1 * C);
-    k += (size_t)head * N * D;
+    const uint16_t *k = (const uint16_t *)kin + (size_t)head * N * D;
     v += (size_t)head * N * D;
+    if (vrow) vrow += (size_t)head * N;
 
     const int w = threadIdx.x >> 6;
     const bool has_lin = w < 4;
@@ -140,18 +148,23 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ 
     constexpr int U = 8;
     for (int p0 = 4 * t0 + tid; p0 < 4 * t1; p0 += U * NTH) {
         uint4 raw[U];
+        float rr[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int p = p0 + u * NTH, n = p >> 2, qq = p & 3;
             raw[u] = uint4{0u, 0u, 0u, 0u};
-            if (p < 4 * t1) raw[u] = *(const uint4 *)(v + (size_t)n * D + MSW * sl + 8 * qq);
+            rr[u] = 1.0f;
+            if (p < 4 * t1) {
+                raw[u] = *(const uint4 *)(v + (size_t)n * D + MSW * sl + 8 * qq);
+                if (vrow) rr[u] = fabsf(vrow[n]);
+            }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             float x[8];
             bf16x8_to_f32(raw[u], x);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]));
+            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * rr[u]);
         }
     }
 #pragma unroll
@@ -191,6 +204,7 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ 
     };
 
     uint4 pk[2], pv;
+    float pr = 1.0f;
     auto prefetch = [&](int c) {
         const uint4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -201,7 +215,10 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ 
         }
         const int nv = c * C + vt;
         pv = z;
-        if (nv < N) pv = *(const uint4 *)(v + (size_t)nv * D + MSW * sl + 8 * vq);
+        if (nv < N) {
+            pv = *(const uint4 *)(v + (size_t)nv * D + MSW * sl + 8 * vq);
+            if (vrow) pr = vrow[nv];
+        }
     };
     // standardise k rows (Sec. 2.2, Eqs. 6-7), store k^ transposed and the
     // scaled v transposed
@@ -209,17 +226,22 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const bf16_t *__restrict__ 
         h8 hk[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            float x[8];
-            bf16x8_to_f32(pk[j], x);
-            hk[j] = standardise8(x, c * C + 2 * tg + j < N);
+            if constexpr (KF16) {
+                hk[j] = __builtin_bit_cast(h8, pk[j]);   // rows past N load as zero
+            } else {
+                float x[8];
+                bf16x8_to_f32(pk[j], x);
+                hk[j] = standardise8(x, c * C + 2 * tg + j < N);
+            }
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i)
             *(h2 *)(sm.kT[buf] + sw128(8 * cg + i, 2 * tg)) = h2{hk[0][i], hk[1][i]};
         float xv[8];
         bf16x8_to_f32(pv, xv);
+        const float vs = vrow ? vscale * pr : vscale;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) sm.vT[buf][sw128(8 * vq + i, vt)] = (_Float16)(xv[i] * vscale);
+        for (int i = 0; i < 8; ++i) sm.vT[buf][sw128(8 * vq + i, vt)] = (_Float16)(xv[i] * vs);
     };
 
     prefetch(c0);
@@ -419,7 +441,11 @@ struct QSmem {
     float hdr[HDR];
 };
 
-__global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
+// QF16: the queries arrive standardised in fp16 (else bf16 rows,
+// standardised here with the score scale).  DIVIDE = false stores the
+// numerator F undivided and no G (the backward's dv).
+template <bool QF16, bool DIVIDE>
+__global__ __launch_bounds__(NTH, 1) void nc_query(const void *__restrict__ qin,
                                                    const h8 *__restrict__ aq,
                                                    const _Float16 *__restrict__ y3g,
                                                    const float *__restrict__ hdrg,
@@ -438,7 +464,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
     if (head >= BH) return;
     const int tok0 = tbi * tb, tok1 = min(N, tok0 + tb);
     const int nsteps = (tok1 - tok0 + QS - 1) / QS;
-    q += (size_t)head * N * D;
+    const uint16_t *q = (const uint16_t *)qin + (size_t)head * N * D;
     out += (size_t)head * N * D;
     if (g) g += (size_t)head * N;
 
@@ -475,10 +501,15 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
         if (n < tok1) pq = *(const uint4 *)(q + (size_t)n * D + 8 * (tid & 7));
     };
     auto stage = [&](int s, int buf) {
-        float x[8];
-        bf16x8_to_f32(pq, x);
         const int row = tid >> 3, cg = tid & 7;
-        const h8 hq = standardise8(x, tok0 + s * QS + row < tok1, qs);
+        h8 hq;
+        if constexpr (QF16) {
+            hq = __builtin_bit_cast(h8, pq);   // rows past the block load as zero
+        } else {
+            float x[8];
+            bf16x8_to_f32(pq, x);
+            hq = standardise8(x, tok0 + s * QS + row < tok1, qs);
+        }
         *(h8 *)(sm.qrow[buf] + sw64(row, 8 * cg)) = hq;
 #pragma unroll
         for (int i = 0; i < 8; ++i) sm.qperm[buf][sw64(row, 8 * i + cg)] = hq[i];
@@ -498,12 +529,12 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
         for (int k = 0; k < 4; ++k) gq += sm.gpart[buf][k * QS + tk];
         const float G = fmaf(sm.hdr[2 * D + NCT], gq, Nf);
         if (n < tok1) {
-            const float sc = sm.hdr[2 * D + ct] * __builtin_amdgcn_rcpf(G);
+            const float sc = DIVIDE ? sm.hdr[2 * D + ct] * __builtin_amdgcn_rcpf(G) : sm.hdr[2 * D + ct];
             uint2 o;
             o.x = pack_bf16x2(F[0] * sc, F[1] * sc);
             o.y = pack_bf16x2(F[2] * sc, F[3] * sc);
             *(uint2 *)(out + (size_t)n * D + 4 * cq) = o;
-            if (g && cq == 0) g[n] = G;
+            if (DIVIDE && g && cq == 0) g[n] = G;
         }
     };
 
@@ -582,10 +613,15 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const bf16_t *__restrict__ q,
 
 size_t mfma_nc_workspace(int BH, int N) { return mfma_nc::make_plan(BH, N).total; }
 
-hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, float qs, void *ws, hipStream_t st)
+namespace mfma_nc {
+
+// The three launches on a workspace laid out by make_plan.  KQF16: keys and
+// queries arrive standardised in fp16; vrow: per-row value scale (nullptr:
+// none); DIVIDE: O = F / G (else F).
+template <bool KQF16, bool DIVIDE>
+hipError_t launch(const void *q, const void *k, const void *v, const float *vrow, void *out,
+                  float *g, int BH, int N, float qs, void *ws, hipStream_t st)
 {
-    using namespace mfma_nc;
     static_assert(sizeof(QSmem) <= 160 * 1024, "LDS budget");
     const Plan P = make_plan(BH, N);
     const long long gm = (long long)BH * NMS * P.nseg;
@@ -602,8 +638,8 @@ hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, f
     _Float16 *y3h = (_Float16 *)(w + P.off_y3h);
     float *hdr = (float *)(w + P.off_hdr);
 
-    hipLaunchKernelGGL(nc_moments, dim3((unsigned)gm), dim3(NTH), 0, st, (const bf16_t *)k,
-                       (const bf16_t *)v, part, vmx, y3p, y2p, x1p, N, BH, P.nseg, P.cps);
+    hipLaunchKernelGGL(nc_moments<KQF16>, dim3((unsigned)gm), dim3(NTH), 0, st, k,
+                       (const bf16_t *)v, vrow, part, vmx, y3p, y2p, x1p, N, BH, P.nseg, P.cps);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(nc_reduce, dim3((unsigned)gr), dim3(512), 0, st, part, vmx, y3p, y2p, x1p,
@@ -611,12 +647,30 @@ hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, f
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t smem = sizeof(QSmem);
-    e = hipFuncSetAttribute((const void *)nc_query, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)smem);
+    e = hipFuncSetAttribute((const void *)nc_query<KQF16, DIVIDE>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(nc_query, dim3((unsigned)gq), dim3(NTH), smem, st, (const bf16_t *)q, aq,
+    hipLaunchKernelGGL((nc_query<KQF16, DIVIDE>), dim3((unsigned)gq), dim3(NTH), smem, st, q, aq,
                        y3h, hdr, (bf16_t *)out, g, N, BH, P.tb, P.ntb, qs);
     return hipGetLastError();
+}
+
+}  // namespace mfma_nc
+
+hipError_t mfma_nc_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
+                       int N, float qs, void *ws, hipStream_t st)
+{
+    return mfma_nc::launch<false, true>(q, k, v, nullptr, out, g, BH, N, qs, ws, st);
+}
+
+// dv_n = sum_i f(qs q^_i . k^_n) u_i, u_i = dO_i / G_i (Sec. 2.5), over all
+// i: the non-causal forward with queries and keys exchanged (keys qs q^,
+// queries k^, both standardised in fp16), values dO scaled per row by 1/G,
+// and no divide.
+hipError_t mfma_nc_dv(const void *qh, const void *kh, const void *dout, const float *rg, void *dv,
+                      int BH, int N, void *ws, hipStream_t st)
+{
+    return mfma_nc::launch<true, false>(kh, qh, dout, rg, dv, nullptr, BH, N, 1.0f, ws, st);
 }
 
 }  // namespace fm

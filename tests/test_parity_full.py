@@ -106,3 +106,17 @@ def test_long_causal_state_error_vs_n():
         e_tail = max_rel(out[:, :, lo:n], ref_o[:, :, lo:n])
         say(f"{label}: first {n} rows E_O={e:.3e}; rows {lo}..{n - 1} E_O={e_tail:.3e}")
         assert e <= TOL["bf16"] and e_tail <= TOL["bf16"], (n, e, e_tail)
+
+
+def test_fwdbwd_noncausal_16_heads_backward():
+    """The forward+backward workload's shape without the mask (B8 H12 N4096,
+    non-causal): every row of the forward, and the backward on 16 heads spread
+    over B and H against the fp64 explicit backward (MFMA kernels on both)."""
+    from test_parity_gpu import bwd_case
+    w = WORKLOADS["fwdbwd_causal_bf16"]
+    say(f"{w.name} non-causal")
+    inp = workload_inputs(w)
+    full_compare(inp, False, w.name + " non-causal")
+    heads = [(i % w.B, (7 * i + 3) % w.H) for i in range(16)]
+    assert len(set(heads)) == 16
+    bwd_case(inp, w.p, False, w.dtype, heads=heads, label=w.name + " non-causal bwd")

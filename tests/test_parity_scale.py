@@ -123,6 +123,15 @@ def test_bwd_scaled_generic(D, p, causal, dtype):
         bwd_check(inp, p, causal, dtype, tau, label)
 
 
+@pytest.mark.parametrize("N", [300])
+def test_bwd_scaled_mfma_noncausal(N):
+    label = f"bwd scaled MFMA non-causal N={N} bf16"
+    say(label)
+    inp = make_inputs(1, 2, N, 64, 760 + N, "bf16", with_dout=True)
+    for tau in taus(64):
+        bwd_check(inp, 2, False, "bf16", tau, label)
+
+
 @pytest.mark.parametrize("N", [37, 300])
 def test_bwd_scaled_mfma_causal(N):
     label = f"bwd scaled MFMA causal N={N} bf16"
