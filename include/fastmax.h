@@ -30,7 +30,8 @@
  *  - Ownership: the caller owns every buffer, including `workspace`.  The
  *    library keeps no pointer after return, allocates no device memory,
  *    creates no stream and holds no global mutable state (thread-safe);
- *    the one exception is fastmax_fwd_noalloc's per-GPU scratch array.
+ *    the exceptions are fastmax_fwd_noalloc's per-GPU scratch array and the
+ *    process-wide mode of fastmax_set_scan_segments.
  *  - Asynchrony: work is enqueued on `stream` (0 = the null stream);
  *    FASTMAX_OK means "enqueued".  Outputs are valid once the stream reaches
  *    that point.  Inputs must stay valid until then.
@@ -81,10 +82,13 @@ enum {
  * denominator terms, about 0.7 MB per (head, segment)), and every other
  * non-MFMA forward when B*H is small (fp32 segment states, enough segments
  * for about 256 workgroups).  The causal bf16, D = 64, p = 2 forward keeps
- * the standardised q and k in fp16 (256 bytes per row).  The backward always
+ * the standardised q and k in fp16 (256 bytes per row) and, for N > 128,
+ * room for the summaries of split scans (99072 bytes per head and 16-column
+ * slice, see fastmax_set_scan_segments).  The backward always
  * needs one: per token 1/G, c = dO.O/G, the fp32
  * gradient accumulators of q^ and k^ and (causal bf16, D = 64, p = 2) the
- * standardised q^, k^ in fp16, plus per-chunk maxima; on the float32 path
+ * standardised q^, k^ in fp16, the dv scan's segment summaries, plus
+ * per-chunk maxima; on the float32 path
  * with few heads (B*H times the column slices under about 256) also the
  * per-segment moment states of its two scans.
  */
@@ -211,6 +215,37 @@ int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void 
 
 const char *fastmax_strerror(int code);
 
+/*
+ * Segments of the causal MFMA scans (bf16, D = 64, p = 2: the forward and
+ * the backward's dv scan).  These scans carry the moment state of Sec. 2.4's
+ * causal recurrences (Eqs. "xcausal", "ycausal") across 128-token chunks,
+ * one workgroup per (head, 16-column slice).  A split cuts each such scan at
+ * a chunk boundary into two workgroups: the first scans its chunks and then
+ * emits its summary (the moment sums over its tokens, which are the exclusive
+ * prefix of the second), the second starts from that summary.
+ *   FASTMAX_SCAN_SEGMENTS_AUTO (default): split the forward's scans when
+ *     two half-length workgroups per scan fill the GPU's 256 CUs in fewer
+ *     rounds than one (e.g. B*H = 96; not B*H = 64); the backward's dv scan
+ *     is not split (it shares its launch with the in-chunk gradient blocks,
+ *     which already fill its last round);
+ *   FASTMAX_SCAN_SEGMENTS_OFF: never split;
+ *   FASTMAX_SCAN_SEGMENTS_ON: split both scans for every sequence of two
+ *     chunks or more;
+ *   FASTMAX_SCAN_SEGMENTS_REBUILD: as ON, but the second workgroup rebuilds
+ *     the first's summary itself (state updates over the earlier chunks)
+ *     instead of waiting for it -- the path a second workgroup also takes
+ *     if the summary has not arrived within about 0.3 s.
+ * Every mode gives bit-identical results; the workspace sizes do not depend
+ * on the mode.  The mode is process-wide and applies to calls made after
+ * this returns.  Returns the previous mode, or FASTMAX_EINVAL for any other
+ * value.
+ */
+#define FASTMAX_SCAN_SEGMENTS_AUTO 0
+#define FASTMAX_SCAN_SEGMENTS_OFF 1
+#define FASTMAX_SCAN_SEGMENTS_ON 2
+#define FASTMAX_SCAN_SEGMENTS_REBUILD 3
+int fastmax_set_scan_segments(int mode);
+
 /* Library version as "major.minor.patch". */
 const char *fastmax_version(void);
 
@@ -223,8 +258,9 @@ const char *fastmax_version(void);
  * instead, which each GPU the library runs on holds until the process ends.
  * Problems whose fastmax_workspace_bytes(..., backward = 0) exceeds that
  * size are rejected with FASTMAX_EWORKSPACE before anything is enqueued
- * (e.g. the causal bf16, D = 64, p = 2 forward takes up to B*H*N = 262144
- * rows).  The call allocates nothing (no hipMalloc, no library allocation);
+ * (e.g. the causal bf16, D = 64, p = 2 forward, whose workspace holds q^ and
+ * k^ in fp16 and about 0.4 MB of scan-segment summaries per head, takes one
+ * head of up to 260594 tokens, or up to 46 heads of 4096 tokens).  The call allocates nothing (no hipMalloc, no library allocation);
  * the first call on a GPU looks the array's device address up once
  * (FASTMAX_EHIP if HIP refuses).  Every call on one GPU shares that GPU's
  * array: calls whose work overlaps on one GPU (different streams without

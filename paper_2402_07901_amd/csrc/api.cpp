@@ -282,6 +282,13 @@ int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void 
     return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
 }
 
+int fastmax_set_scan_segments(int mode)
+{
+    if (mode < FASTMAX_SCAN_SEGMENTS_AUTO || mode > FASTMAX_SCAN_SEGMENTS_REBUILD)
+        return FASTMAX_EINVAL;
+    return fm::set_scan_segment_mode(mode);
+}
+
 const char *fastmax_strerror(int code)
 {
     switch (code) {

@@ -57,9 +57,13 @@ __global__ __launch_bounds__(256) void bwd_prep(const bf16_t *__restrict__ q,
                                                 const float *__restrict__ g,
                                                 float *__restrict__ rg, float *__restrict__ cc,
                                                 float *__restrict__ pmax, _Float16 *__restrict__ qh,
-                                                _Float16 *__restrict__ kh, int N, int nch, float qs)
+                                                _Float16 *__restrict__ kh, int N, int nch, float qs,
+                                                unsigned int *__restrict__ flags, int nflags)
 {
     __shared__ float red[3][4];
+    // the segment flags of the dv scan that follows start lowered
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < nflags; i += 256) flags[i] = 0u;
     const int head = blockIdx.x / nch, c = blockIdx.x % nch, tid = threadIdx.x;
     const size_t hb = (size_t)head * N;
     q += hb * D;
@@ -685,10 +689,11 @@ __global__ __launch_bounds__(MG_NTH, 1) void bwd_mg_scans(const _Float16 *__rest
         mg_scan<1, CAUSAL>(sm, b - half, half, kh, qh, v, dout, rg, cc, hmax, dkh, N, BH);
 }
 
-// dv and the in-chunk pairs in one launch: blocks [0, 4BH) run the causal scan
-// in reverse for dv (fm_causal_scan.h), the rest are the in-chunk blocks
-// (head, chunk).  The short in-chunk blocks come last and fill the CUs the
-// dv blocks leave idle in their last, partly filled round.
+// dv and the in-chunk pairs in one launch: blocks [0, ndv) run the causal scan
+// in reverse for dv (fm_causal_scan.h; ndv = 4BH, or 8BH when the scan is
+// split into two segments), the rest are the in-chunk blocks (head, chunk).
+// The short in-chunk blocks come last and fill the CUs the dv blocks leave
+// idle in their last, partly filled round.
 __global__ __launch_bounds__(512, 2) void bwd_dv_intra(const _Float16 *__restrict__ qh,
                                                        const _Float16 *__restrict__ kh,
                                                        const bf16_t *__restrict__ v,
@@ -699,16 +704,16 @@ __global__ __launch_bounds__(512, 2) void bwd_dv_intra(const _Float16 *__restric
                                                        float *__restrict__ dqh,
                                                        float *__restrict__ dkh,
                                                        bf16_t *__restrict__ dv, int N, int nch,
-                                                       int BH)
+                                                       int BH, mfma_causal::SegArgs sa)
 {
     static_assert(mfma_causal::NTH == 512, "one block size for both");
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    const int ndv = 4 * BH;
+    const int ndv = 4 * BH * (1 + sa.split);
     const int b = blockIdx.x;
     if (b < ndv) {
         // queries of the dv scan are the keys k^ (and vice versa), values dO / G
         mfma_causal::Smem &sm = *reinterpret_cast<mfma_causal::Smem *>(smem_raw);
-        mfma_causal::scan_block<true>(sm, kh, qh, dout, dv, nullptr, rg, N, BH, b, ndv);
+        mfma_causal::scan_block<true>(sm, kh, qh, dout, dv, nullptr, rg, N, BH, b, 4 * BH, sa);
     } else {
         ISmem &sm = *reinterpret_cast<ISmem *>(smem_raw);
         intra_block(sm, qh, kh, v, dout, rg, cc, hmax, dqh, dkh, N, nch, b - ndv);
@@ -787,7 +792,7 @@ size_t base_workspace(int BH, int N)
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t nch = ((size_t)N + C - 1) / C;
     return a256(rows * 4) * 2 + a256((size_t)BH * nch * 16) + 2 * a256(rows * mx::D * 4) +
-           2 * a256(rows * mx::D * 2);
+           2 * a256(rows * mx::D * 2) + causal_scan_seg_workspace(4 * BH, (int)nch);
 }
 
 // Causal: dv by the reverse scan with the in-chunk blocks, then the
@@ -805,7 +810,7 @@ hipError_t run(const void *q, const void *k, const void *v, const void *o, const
                   "LDS budget");
     const size_t rows = (size_t)BH * N;
     const int nch = (N + C - 1) / C;
-    if ((long long)BH * (nch + 4) > INT_MAX || (long long)BH * 8 > INT_MAX ||
+    if ((long long)BH * (nch + 8) > INT_MAX || (long long)BH * 8 > INT_MAX ||
         (rows + 31) / 32 > (size_t)INT_MAX)
         return hipErrorInvalidConfiguration;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -824,11 +829,19 @@ hipError_t run(const void *q, const void *k, const void *v, const void *o, const
     p += a256(rows * D * 2);
     _Float16 *kh = (_Float16 *)p;
     p += a256(rows * D * 2);
+    // the dv scan's segment summaries and flags (causal)
+    const ScanSplit plan = CAUSAL ? causal_scan_split(4 * BH, nch, false) : ScanSplit{0, 0, 1};
+    mfma_causal::SegArgs sa{nullptr, nullptr, plan.split, plan.csplit, plan.wait};
+    if (plan.split) {
+        sa.sum = p;
+        sa.flags = (unsigned int *)(p + a256((size_t)4 * BH * mfma_causal::SUM_BYTES));
+    }
+    p += causal_scan_seg_workspace(4 * BH, nch);
 
     const bf16_t *Q = (const bf16_t *)q, *K = (const bf16_t *)k, *V = (const bf16_t *)v;
     const bf16_t *O = (const bf16_t *)o, *DO = (const bf16_t *)dout;
     hipLaunchKernelGGL(bwd_prep, dim3(BH * nch), dim3(256), 0, st, Q, K, O, DO, V, g, rg, cc, hmax,
-                       qh, kh, N, nch, qs);
+                       qh, kh, N, nch, qs, sa.flags, plan.split ? 4 * BH : 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if constexpr (CAUSAL) {
@@ -837,8 +850,9 @@ hipError_t run(const void *q, const void *k, const void *v, const void *o, const
         e = hipFuncSetAttribute((const void *)bwd_dv_intra,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem1);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(bwd_dv_intra, dim3(BH * 4 + BH * nch), dim3(512), smem1, st, qh, kh, V,
-                           DO, rg, cc, hmax, dqh, dkh, (bf16_t *)dv, N, nch, BH);
+        hipLaunchKernelGGL(bwd_dv_intra, dim3(BH * 4 * (1 + plan.split) + BH * nch), dim3(512),
+                           smem1, st, qh, kh, V, DO, rg, cc, hmax, dqh, dkh, (bf16_t *)dv, N, nch,
+                           BH, sa);
     } else {
         e = mfma_nc_dv(qh, kh, DO, rg, dv, BH, N, p, st);
     }

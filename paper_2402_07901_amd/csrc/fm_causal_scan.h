@@ -24,6 +24,22 @@
 // prefix sums, Y3 update and staging of the next chunk.  The two kinds of
 // work overlap on each SIMD instead of running in lockstep.
 //
+// Segments (load balance, Sec. 2.4's causal recurrences cut at a chunk
+// boundary).  When a launch of one workgroup per (head, slice) would leave
+// the GPU's CUs idle for part of the time (e.g. 384 workgroups on 256 CUs),
+// each (head, slice) is scanned by two workgroups: segment 0 takes the
+// chunks before csplit and, at its end, writes its summary -- the moment
+// state, Y3, y2 and x1 accumulated over those chunks, i.e. the exclusive
+// prefix of segment 1 -- and raises a flag; segment 1 waits for the flag
+// (bounded), loads the summary and scans the remaining chunks from it.  The
+// second segments come after all first segments in the grid, so they are
+// dispatched after them.  If the flag does not come within the bound, the
+// segment builds the prefix itself (state updates and prefix sums over the
+// earlier chunks, no outputs), so the result never depends on the order in
+// which workgroups run.  Both segments scale v from the whole slice's max|v|
+// and perform the same operations in the same order as one workgroup over
+// all chunks: split and unsplit scans give bit-identical results.
+//
 // State numerics.  The state lives in fp16 (v is pre-scaled by a power of two
 // 2^-e per workgroup so that no entry, bounded by N * 63 * max|v|, can exceed
 // 2^15).  A tile's accumulator layout holds exactly the elements of its half of
@@ -110,7 +126,66 @@ struct Smem {
     alignas(16) float y2s[2][D];    // the same times 2^(1-gexp), gexp the Y3 scale
     alignas(16) float x1[2][SL];    // sum of scaled v before the chunk
     float red[NW];
+    int segok;                      // the summary of segment 0 arrived
 };
+
+// Two-segment split of a scan (see "Segments" above).
+struct SegArgs {
+    unsigned char *sum;     // summaries, SUM_BYTES per (head, slice); null if no split
+    unsigned int *flags;    // one per (head, slice), zeroed before the launch
+    int split;              // 0: one workgroup per (head, slice); 1: two
+    int csplit;             // first chunk of segment 1
+    int wait;               // 1: segment 1 waits for segment 0's summary; 0: rebuilds it
+};
+// summary layout: fp16 state [wave][pair][lane] (h8), Y3 accumulators
+// [helper][tile][lane] (f4), y2, y2 scaled, x1 (fp32)
+constexpr size_t SUM_AST = (size_t)NSW * NKS * 64 * 16;
+constexpr size_t SUM_Y3 = (size_t)4 * 3 * 64 * 16;
+constexpr size_t SUM_MISC = (size_t)(D + D + SL) * 4;
+constexpr size_t SUM_BYTES = (SUM_AST + SUM_Y3 + SUM_MISC + 255) & ~(size_t)255;
+// polls of a waiting segment (about 0.3 s at 2 GHz) before it rebuilds the
+// prefix itself
+constexpr int SEG_SPIN = 1 << 20;
+
+// Summary words are written and read as relaxed atomics at device scope:
+// such accesses go to the level where every XCD's CUs see the same data (the
+// per-XCD L2s are not coherent with each other), so the flag protocol needs
+// no cache-wide write-back or invalidation (which, done by every first
+// segment and every second one, cost more than the split gains).  Ordering:
+// each thread's summary stores have completed before the workgroup barrier
+// that precedes the flag store, and the summary loads are issued after the
+// flag load has returned.  A 16-byte per-lane value of a wave is stored
+// word-major (8-byte word i of lane l at grp[64 i + l]) so that each store
+// writes 512 contiguous bytes: these stores go through to memory, where
+// lane-interleaved partial lines cost several times more.
+typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+template <typename T>
+__device__ __forceinline__ void sum_put_lane(unsigned long long *grp, int lane, const T &x)
+{
+    static_assert(sizeof(T) == 16, "16-byte lane values");
+    const u64x2 w = __builtin_bit_cast(u64x2, x);
+    __hip_atomic_store(grp + lane, w[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(grp + 64 + lane, w[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T sum_get_lane(const unsigned long long *grp, int lane)
+{
+    static_assert(sizeof(T) == 16, "16-byte lane values");
+    u64x2 w;
+    w[0] = __hip_atomic_load(grp + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    w[1] = __hip_atomic_load(grp + 64 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return __builtin_bit_cast(T, w);
+}
+__device__ __forceinline__ void sum_put_f(float *p, float x)
+{
+    __hip_atomic_store((unsigned int *)p, __float_as_uint(x), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float sum_get_f(const float *p)
+{
+    return __uint_as_float(
+        __hip_atomic_load((const unsigned int *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
 
 template <int HALF>
 __device__ __forceinline__ h8 set_half(h8 x, h4 r)
@@ -125,21 +200,29 @@ __device__ __forceinline__ h8 set_half(h8 x, h4 r)
 // q and q^ as k, both already standardised, in fp16), v is dO scaled per row
 // by rg = 1/G, and F is stored without the divide; the denominator terms are
 // skipped.
-// One workgroup of the scan: block b of nblk (the scan's own numbering; when
-// the scan shares a launch with other work, b counts from its first block,
-// whose id must be a multiple of 8 for the XCD mapping below).
+// One workgroup of the scan: block b (the scan's own numbering; when the
+// scan shares a launch with other work, b counts from its first block, whose
+// id must be a multiple of 8 for the XCD mapping below).  Blocks
+// [0, nitems) are the (head, slice) items (their first segments when the
+// scan is split), blocks [nitems, 2 nitems) their second segments.
 template <bool DV>
 __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict__ q,
                                            const _Float16 *__restrict__ k,
                                            const bf16_t *__restrict__ v, bf16_t *__restrict__ out,
                                            float *__restrict__ g, const float *__restrict__ rg,
-                                           int N, int BH, int b, int nblk)
+                                           int N, int BH, int b, int nitems, const SegArgs &sa)
 {
+    int seg = 0;
+    if (sa.split && b >= nitems) {
+        seg = 1;
+        b -= nitems;
+    }
+    const int item = b;
     // XCD-aware mapping: consecutive block ids land on different XCDs
     // (round-robin over 8); keep the 4 slices of a head on one XCD so that
     // its q and k rows are shared through that XCD's L2.
     int head, sl;
-    if ((nblk & 31) == 0) {
+    if ((nitems & 31) == 0) {
         const int xcd = b & 7, idx = b >> 3;
         sl = idx & 3;
         head = (idx >> 2) * 8 + xcd;
@@ -199,6 +282,36 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
     const float oscale = ldexpf(1.0f, vexp);
     const int nch = (N + C - 1) / C;
 
+    // chunk range of this workgroup; [cstart, cbeg) are build-only chunks
+    // (a second segment rebuilding its prefix)
+    const int cbeg = seg ? sa.csplit : 0;
+    const int cend = (sa.split && seg == 0) ? sa.csplit : nch;
+    int cstart = cbeg;
+    bool loaded = false;
+    unsigned char *sum = sa.split ? sa.sum + (size_t)item * SUM_BYTES : nullptr;
+    if (seg == 1) {
+        if (sa.wait) {
+            // one thread polls; the summary loads (sum_get) come after the
+            // barrier that follows
+            if (threadIdx.x == 0) {
+                unsigned int f = 0;
+                for (int it = 0; it < SEG_SPIN; ++it) {
+                    f = __hip_atomic_load(sa.flags + item, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (f) break;
+                    __builtin_amdgcn_s_sleep(8);
+                }
+                sm.segok = f != 0;
+            }
+            __syncthreads();
+            loaded = sm.segok != 0;
+        }
+        if (!loaded) cstart = 0;
+    }
+    // summary groups of 64 lanes x 16 bytes: state (wave, pair), Y3 (helper, tile)
+    unsigned long long *sum_ast = (unsigned long long *)sum;
+    unsigned long long *sum_y3 = (unsigned long long *)(sum + SUM_AST);
+    float *sum_misc = (float *)(sum + SUM_AST + SUM_Y3);
+
     const int w = threadIdx.x >> 6;
     const bool is_state = w < NSW;
     const int hw = w - NSW;   // helper index
@@ -221,12 +334,15 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
         // fp16 state, paired per query K step
         h8 Ast[NKS];
 #pragma unroll
-        for (int p = 0; p < NKS; ++p) Ast[p] = h8{0, 0, 0, 0, 0, 0, 0, 0};
+        for (int p = 0; p < NKS; ++p)
+            Ast[p] = loaded ? sum_get_lane<h8>(sum_ast + (w * NKS + p) * 128, lane)
+                            : h8{0, 0, 0, 0, 0, 0, 0, 0};
         __syncthreads();
-        for (int c = 0; c < nch; ++c) {
+        for (int c = cstart; c < cend; ++c) {
             // ---- (1) query contraction over the wave's tiles, 128 tokens ----
             __builtin_amdgcn_sched_barrier(0);
             refresh_ids();
+            const bool build = c < cbeg;
             // the q^ values of a row tile: l blocks, the linear tile and the
             // wave's channels; loaded one row tile ahead of their use
             struct QRow {
@@ -265,14 +381,16 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 });
                 *(f4 *)(sm.fpart + ((w * 4 + h) * C + tok) * 4) = F0 + F1;
             };
-            QRow ra, rb;
-            loadq(0, ra);
+            if (!build) {
+                QRow ra, rb;
+                loadq(0, ra);
 #pragma unroll 1
-            for (int rt = 0; rt < NRT; rt += 2) {
-                loadq(rt + 1, rb);
-                contract(rt, ra);
-                if (rt + 2 < NRT) loadq(rt + 2, ra);
-                contract(rt + 1, rb);
+                for (int rt = 0; rt < NRT; rt += 2) {
+                    loadq(rt + 1, rb);
+                    contract(rt, ra);
+                    if (rt + 2 < NRT) loadq(rt + 2, ra);
+                    contract(rt + 1, rb);
+                }
             }
             __syncthreads();
 
@@ -333,14 +451,40 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             });
             __syncthreads();
         }
+        if (sum && seg == 0) {
+#pragma unroll
+            for (int p = 0; p < NKS; ++p)
+                sum_put_lane(sum_ast + (w * NKS + p) * 128, threadIdx.x & 63, Ast[p]);
+        }
     } else {
         // loader roles: tokens 4*tg .. 4*tg+3, channels 8*cg .. 8*cg+7; v:
         // token vt, columns 8*vh .. 8*vh+7
         uint4 pq[4], pk[4], pv;
         float prg = 1.0f;
         f4 y3acc[3] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
-        int gexp = 0;   // Y3 in LDS is Y3 * 2^-gexp
+        // Y3 in LDS is Y3 * 2^-gexp, gexp fixed by the tokens summed so far
+        int gexp = loaded ? max(0, pow2_exponent(64.0f * (float)(cbeg * C))) : 0;
+        if (loaded) {
+#pragma unroll
+            for (int kk = 0; kk < 3; ++kk) y3acc[kk] = sum_get_lane<f4>(sum_y3 + (hw * 3 + kk) * 128, lane);
+        }
         const h8 ones8 = {1, 1, 1, 1, 1, 1, 1, 1};
+        // the scaled fp16 copy of this helper's Y3 tile kk (Y3[m][l] and, off
+        // the diagonal, Y3[l][m])
+        auto put_y3h = [&](int kk, float gs) {
+            int u, u2;
+            y3_tile(hw, kk, u, u2);
+            // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
+            const int mcol = 16 * u2 + r16;
+            h4 hv;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) hv[i] = (_Float16)(y3acc[kk][i] * gs);
+            *(h4 *)(sm.y3h + sw64(mcol, 16 * u + 4 * h)) = hv;   // Y3[m][l]
+            if (u != u2) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sm.y3h[sw64(16 * u + 4 * h + i, mcol)] = hv[i];
+            }
+        };
 
         auto prefetch = [&](int c) {
             const int ht = tid - NSW * 64;
@@ -408,14 +552,31 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             for (int i = 0; i < 8; ++i) sm.vT[buf][sw128(8 * vh + i, vt)] = (_Float16)(xv[i] * vs);
         };
 
-        prefetch(0);
-        stage(0);
+        prefetch(cstart);
+        stage(cstart);
+        if (loaded) {
+            // segment 0's prefix sums, as its last chunk left them in LDS
+            const int ht = tid - NSW * 64, cb = cbeg & 1;
+            if (!DV && ht < D) {
+                sm.y2[cb][ht] = sum_get_f(sum_misc + ht);
+                sm.y2s[cb][ht] = sum_get_f(sum_misc + D + ht);
+            }
+            if (ht < SL) sm.x1[cb][ht] = sum_get_f(sum_misc + 2 * D + ht);
+            if (!DV) {
+                const int ny3 = y3_count(hw);
+                const float gs = ldexpf(1.0f, -gexp);
+#pragma unroll
+                for (int kk = 0; kk < 3; ++kk)
+                    if (kk < ny3) put_y3h(kk, gs);
+            }
+        }
         __syncthreads();
-        for (int c = 0; c < nch; ++c) {
+        for (int c = cstart; c < cend; ++c) {
             const int n0 = c * C;
             const int nvalid = min(C, N - n0);
             const int cur = c & 1, nxt = cur ^ 1;
-            const bool more = c + 1 < nch;
+            const bool more = c + 1 < cend;
+            const bool build = c < cbeg;   // prefix only: no outputs
 
             // ---- (1) in-chunk block and denominators, row tiles hw, 7 - hw
             //      (1 + 4, 1 + 4, 2 + 3, 2 + 3 tile-pair items) ---------------
@@ -424,7 +585,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             if (more) prefetch(c + 1);
             f4 Fin[2];
             float Gs[2];
-            {
+            if (!build) {
                 const _Float16 *vTc = sm.vT[cur];
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
@@ -510,6 +671,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
             const _Float16 *vTc = sm.vT[cur];
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
+                if (build) break;
                 const int rt = r ? NRT - 1 - hw : hw;
                 const int tok = 16 * rt + r16;
                 f4 F = 0.5f * Fin[r] + *(const f4 *)(sm.x1[cur] + 4 * h);
@@ -561,22 +723,32 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                     for (int s = 0; s < NKS2; ++s)
                         y3acc[kk] = mfma(ld8(kTc + sw128(16 * u + r16, 32 * s + 8 * h)),
                                          ld8(kTc + sw128(16 * u2 + r16, 32 * s + 8 * h)), y3acc[kk]);
-                    // lane: column m = 16*u2 + r16, rows l = 16*u + 4h + i
-                    const int mcol = 16 * u2 + r16;
-                    h4 hv;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) hv[i] = (_Float16)(y3acc[kk][i] * gs);
-                    *(h4 *)(sm.y3h + sw64(mcol, 16 * u + 4 * h)) = hv;   // Y3[m][l]
-                    if (u != u2) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) sm.y3h[sw64(16 * u + 4 * h + i, mcol)] = hv[i];
-                    }
+                    put_y3h(kk, gs);
                 }
                 gexp = gnext;
             }
             if (more) stage(c + 1);
             __syncthreads();
         }
+        if (sum && seg == 0) {
+            // the summary: Y3 accumulators and the prefix sums after the last chunk
+            const int ln = threadIdx.x & 63, ht = threadIdx.x - NSW * 64, cb = cend & 1;
+#pragma unroll
+            for (int kk = 0; kk < 3; ++kk) sum_put_lane(sum_y3 + (hw * 3 + kk) * 128, ln, y3acc[kk]);
+            if (!DV && ht < D) {
+                sum_put_f(sum_misc + ht, sm.y2[cb][ht]);
+                sum_put_f(sum_misc + D + ht, sm.y2s[cb][ht]);
+            }
+            if (ht < SL) sum_put_f(sum_misc + 2 * D + ht, sm.x1[cb][ht]);
+        }
+    }
+    if (sum && seg == 0) {
+        // publish: every thread's summary stores have completed (waitcnt on
+        // all counters) before the barrier, the flag goes up after it
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0)
+            __hip_atomic_store(sa.flags + item, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 

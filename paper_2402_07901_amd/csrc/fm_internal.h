@@ -50,8 +50,26 @@ size_t generic_fwd_dropout_workspace(int BH, int N, int D, int causal);
 hipError_t dropout_mask(uint32_t *bits, int BH, int N, int D, uint32_t thr, uint64_t seed,
                         hipStream_t st);
 
+// Two-segment split of the MFMA causal scans (forward and the backward's dv
+// scan): whether the (head, slice) items of one launch are split, and where.
+// mode: FASTMAX_SCAN_SEGMENTS_* (fastmax.h).
+struct ScanSplit {
+    int split;    // 0 or 1
+    int csplit;   // first chunk of the second segment
+    int wait;     // the second segment waits for the first's summary
+};
+// auto_split: whether the automatic mode may split this launch (the
+// backward's dv scan shares its launch with the in-chunk gradient blocks,
+// which already fill its last round; there a split only adds work).
+ScanSplit causal_scan_split(int items, int nch, bool auto_split);
+int set_scan_segment_mode(int mode);
+// Summaries and flags of a split scan of `items` (head, slice) items of nch
+// chunks (reserved whenever nch >= 2, whatever the mode).
+size_t causal_scan_seg_workspace(int items, int nch);
+
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
-// ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16.
+// ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16, then
+// the segment summaries and flags.
 hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *out, float *g,
                            int BH, int N, float qs, void *ws, hipStream_t st);
 size_t mfma_causal_fwd_workspace(int BH, int N);

@@ -72,6 +72,8 @@ def lib():
         L.fastmax_bwd_dropout.restype = i
         L.fastmax_fwd_noalloc.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp]
         L.fastmax_fwd_noalloc.restype = i
+        L.fastmax_set_scan_segments.argtypes = [i]
+        L.fastmax_set_scan_segments.restype = i
         L.fastmax_strerror.argtypes = [i]
         L.fastmax_strerror.restype = ctypes.c_char_p
         L.fastmax_version.restype = ctypes.c_char_p
@@ -85,6 +87,15 @@ def strerror(code: int) -> str:
 
 def version() -> str:
     return lib().fastmax_version().decode()
+
+
+# fastmax_set_scan_segments modes
+SCAN_SEGMENTS_AUTO, SCAN_SEGMENTS_OFF, SCAN_SEGMENTS_ON, SCAN_SEGMENTS_REBUILD = 0, 1, 2, 3
+
+
+def set_scan_segments(mode: int) -> int:
+    """Process-wide segment mode of the causal MFMA scans; returns the previous one."""
+    return lib().fastmax_set_scan_segments(int(mode))
 
 
 def workspace_bytes(B, H, N, D, p, causal, dt, backward=False) -> int:

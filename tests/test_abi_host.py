@@ -303,6 +303,28 @@ def test_fwd_noalloc_rejects_problems_beyond_its_scratch():
     small = dict(B=1, H=1, N=4096, D=64, p=2, causal=1, dt=fm.BF16)
     assert 0 < fm.workspace_bytes(1, 1, 4096, 64, 2, 1, fm.BF16) <= lim
     assert fwd_noalloc(q=0, **small) == fm.ENULL
-    # the largest causal bf16 D = 64 problem the header quotes fits exactly
-    assert fm.workspace_bytes(1, 1, 262144, 64, 2, 1, fm.BF16) <= lim
-    assert fm.workspace_bytes(1, 1, 262144 + 4096, 64, 2, 1, fm.BF16) > lim
+    # the largest causal bf16 D = 64 problems the header quotes fit exactly
+    assert fm.workspace_bytes(1, 1, 260594, 64, 2, 1, fm.BF16) <= lim
+    assert fm.workspace_bytes(1, 1, 260595, 64, 2, 1, fm.BF16) > lim
+    assert fm.workspace_bytes(1, 46, 4096, 64, 2, 1, fm.BF16) <= lim
+    assert fm.workspace_bytes(1, 47, 4096, 64, 2, 1, fm.BF16) > lim
+
+
+def test_scan_segment_mode_setter():
+    """fastmax_set_scan_segments: unknown modes are rejected, valid ones
+    return the previous mode; the workspace sizes do not depend on it."""
+    L = fm.lib()
+    for bad in (-1, 4, 1 << 30):
+        assert L.fastmax_set_scan_segments(bad) == fm.EINVAL
+    prev = fm.set_scan_segments(fm.SCAN_SEGMENTS_AUTO)
+    try:
+        sizes = []
+        for mode in (fm.SCAN_SEGMENTS_OFF, fm.SCAN_SEGMENTS_ON, fm.SCAN_SEGMENTS_REBUILD,
+                     fm.SCAN_SEGMENTS_AUTO):
+            before = fm.set_scan_segments(mode)
+            assert fm.set_scan_segments(mode) == mode
+            sizes.append([fm.workspace_bytes(8, 12, 4096, 64, 2, 1, fm.BF16, bw) for bw in (0, 1)])
+            assert before in (0, 1, 2, 3)
+        assert all(x == sizes[0] for x in sizes)
+    finally:
+        fm.set_scan_segments(prev)
