@@ -66,10 +66,19 @@ bool mfma_causal(int D, int p, int causal, int dt)
     return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
 }
 
+// The float32 MFMA forward serves p = 2 wherever the fp16 MFMA kernels do
+// not: float32 I/O for D <= 64 and bf16 I/O for D <= 32.
+bool f32mfma(int D, int p, int causal, int dt, int N)
+{
+    if (mfma_causal(D, p, causal, dt) || mfma_noncausal(N, D, p, causal, dt)) return false;
+    return fm::f32mfma_applies(D, p, dt == FASTMAX_BF16);
+}
+
 size_t fwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_fwd_workspace(B * H, N);
     if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_workspace(B * H, N);
+    if (f32mfma(D, p, causal, dt, N)) return fm::f32mfma_fwd_workspace(B * H, N, D);
     return fm::generic_fwd_workspace(B * H, N, D, p);
 }
 
@@ -110,6 +119,9 @@ int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, in
         e = mfma_causal_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
     else if (mfma_noncausal(N, D, p, causal, dt))
         e = mfma_nc_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
+    else if (f32mfma(D, p, causal, dt, N))
+        e = f32mfma_fwd(q, k, v, out, g, B * H, N, D, causal, dt == FASTMAX_BF16, qk_scale,
+                        workspace, stream);
     else
         e = generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
                         workspace, stream);

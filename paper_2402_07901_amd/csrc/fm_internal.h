@@ -67,6 +67,14 @@ int set_scan_segment_mode(int mode);
 // chunks (reserved whenever nch >= 2, whatever the mode).
 size_t causal_scan_seg_workspace(int items, int nch);
 
+// Float32 MFMA forward (v_mfma_f32_16x16x4_f32): p = 2, D in {16, 32} for
+// float32 and bf16 I/O, D = 64 for float32 I/O; causal and non-causal.  ws
+// holds f32mfma_fwd_workspace(BH, N, D) bytes (segment sums).
+bool f32mfma_applies(int D, int p, int is_bf16);
+size_t f32mfma_fwd_workspace(int BH, int N, int D);
+hipError_t f32mfma_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
+                       int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st);
+
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
 // ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16, then
 // the segment summaries and flags.

@@ -117,7 +117,7 @@ def test_fwd_workspace_checks():
     assert need_c >= 2 * 1000 * 256
     assert fwd(causal=1, N=1000, H=2, ws=None, wsb=0) == fm.EWORKSPACE
     assert fwd(causal=1, N=1000, H=2, ws=A, wsb=need_c - 1) == fm.EWORKSPACE
-    # the generic kernels need segment states only when few heads must be
+    # the float32 kernels (generic and MFMA) need segment sums only when few heads must be
     # spread over the CUs; with many heads (>= 256 workgroups) none
     for D, p, causal, dt in ((64, 2, False, fm.F32), (32, 2, False, fm.BF16),
                              (32, 1, True, fm.F32), (16, 2, True, fm.F32)):
@@ -197,17 +197,18 @@ def test_dropout_mask_words():
 
 
 def test_dropout_workspace():
-    """Backward and non-causal forward: the float32 kernels' p = 2 workspace;
-    causal forward: that (256-byte aligned) plus the masked in-chunk weights,
-    16 x 16 floats per chunk of 16 tokens."""
+    """Backward: the float32 kernels' p = 2 backward workspace; causal
+    forward: the non-causal one (256-byte aligned, the generic kernels' p = 2
+    segment states) plus the masked in-chunk weights, 16 x 16 floats per
+    chunk of 16 tokens."""
+    L = fm.lib()
     for B, H, N, D in ((1, 1, 700, 16), (4, 16, 8192, 64), (1, 8, 4096, 128), (2, 3, 33, 32)):
         for causal in (0, 1):
-            for bwd in (0, 1):
-                a = fm.lib().fastmax_dropout_workspace_bytes(B, H, N, D, causal, fm.BF16, bwd)
-                b = fm.lib().fastmax_workspace_bytes(B, H, N, D, 2, causal, fm.F32, bwd)
-                if causal and not bwd:
-                    b = (b + 255) // 256 * 256 + B * H * ((N + 15) // 16) * 16 * 16 * 4
-                assert a == b, (B, H, N, D, causal, bwd)
+            a = L.fastmax_dropout_workspace_bytes(B, H, N, D, causal, fm.BF16, 1)
+            assert a == L.fastmax_workspace_bytes(B, H, N, D, 2, causal, fm.F32, 1), (B, H, N, D)
+        a_nc = L.fastmax_dropout_workspace_bytes(B, H, N, D, 0, fm.BF16, 0)
+        a_c = L.fastmax_dropout_workspace_bytes(B, H, N, D, 1, fm.BF16, 0)
+        assert a_c == (a_nc + 255) // 256 * 256 + B * H * ((N + 15) // 16) * 16 * 16 * 4, (B, H, N, D)
 
 
 def mask_call(bits=A, B=1, H=1, N=8, D=64, rate=0.1, seed=1):
