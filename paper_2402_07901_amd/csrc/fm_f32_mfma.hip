@@ -61,20 +61,32 @@ __device__ __forceinline__ f4 mma(float a, float b, f4 c)
 
 template <int D>
 struct Pat {
+    // workgroups sharing one (head, slice): D = 128 has too many feature
+    // tiles for one workgroup's accumulators, so four workgroups each take a
+    // quarter of them (and a quarter of the Y3 rows) and write partial F, G
+    static constexpr int NPART = D == 128 ? 4 : 1;
     static constexpr int NU = D / 16;                  // 16-channel blocks
-    static constexpr int NCH = D / 4;                  // channels per wave
-    static constexpr int NQ = 4 * NU * (NU + 1) / 2;   // quadratic tiles per wave
-    static constexpr int NT = 1 + NQ;                  // + the linear slot
-    static constexpr int NY3 = NU * (NU + 1) / 2;      // Y3 tiles (u <= u2)
-    // first tile of channel c (its diagonal tile; u runs from c/4 to NU-1)
+    static constexpr int NGW = NW * NPART;             // waves over the parts
+    static constexpr int NCH = D / NGW;                // channels per wave
+    // block of channel m = gw + NGW c (gw < NGW, 16 a multiple of NGW)
+    static constexpr int u0(int c) { return NGW * c / 16; }
+    // first tile of channel c (its diagonal tile; u runs from u0(c) to NU-1)
     static constexpr int first(int c)
     {
         int t = 1;
-        for (int cc = 0; cc < c; ++cc) t += NU - cc / 4;
+        for (int cc = 0; cc < c; ++cc) t += NU - u0(cc);
         return t;
     }
+    static constexpr int NQ = first(NCH) - 1;          // quadratic tiles per wave
+    static constexpr int NT = 1 + NQ;                  // + the linear slot
+    static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
+    static constexpr int Y3R = 16 * NLB;               // Y3 rows per part
+    // Y3 tiles per part: one part keeps the blocks u <= u2 and mirrors them,
+    // several parts keep full rows
+    static constexpr int NY3 = NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
     static constexpr int RS = D + 2;   // row stride of row-major tiles (floats)
     static constexpr int TS = C + 2;   // row stride of transposed tiles
+    static_assert(16 % NGW == 0, "a wave's channels share their 16-blocks");
 };
 
 template <int D>
@@ -83,19 +95,21 @@ struct Smem {
     float krow[C * Pat<D>::RS];     // k^ [token][channel]
     float kT[D * Pat<D>::TS];       // k^ [channel][token]
     float vrow[C * SL];             // v slice [token][column]
-    float y3[D * Pat<D>::RS];       // Y3 prefix (before the chunk)
+    float y3[Pat<D>::Y3R * Pat<D>::RS];   // Y3 prefix rows of the part (before the chunk)
     float y2s[D];                   // 2 y2 prefix
     float x1[SL];                   // x1 prefix
     f4 fpart[NW][C / 16][64];       // partial F^T of the waves
     float gin[C];                   // in-chunk row sums
-    float gint[NW][C];              // partial q^T(Y3 q^ + 2 y2) per l block
+    float gint[Pat<D>::NLB][C];     // partial q^T(Y3 q^ + 2 y2) per l block
 };
 
-// summary of a segment: [wave][tile][lane] f4 state, Y3 [D][D], y2 [D], x1 [SL]
+// summary of a segment: [wave][tile][lane] f4 state, the part's Y3 rows
+// [Y3R][D], y2 [D], x1 [SL]
 template <int D>
 struct Sum {
     static constexpr size_t STATE = (size_t)NW * Pat<D>::NT * 64 * 4;
-    static constexpr size_t FLOATS = STATE + (size_t)D * D + D + SL;
+    static constexpr size_t Y3 = (size_t)Pat<D>::Y3R * D;
+    static constexpr size_t FLOATS = STATE + Y3 + D + SL;
     static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
 };
 
@@ -127,20 +141,35 @@ __device__ __forceinline__ void standardise_part(float (&x)[D / 8], bool valid, 
     for (int i = 0; i < D / 8; ++i) x[i] *= r;
 }
 
-// One workgroup: (item = head * NSL + slice, segment).
+// In-chunk block (row tile rt, key tile st <= rt) of a 32-token chunk: the
+// part that adds it to its partial F and G.
+template <int NPART>
+__host__ __device__ constexpr int inchunk_owner(int rt, int st)
+{
+    return (rt * (rt + 1) / 2 + st) % NPART;
+}
+
+// One workgroup: (item = (head * NSL + slice) * NPART + part, segment).
+// With one part the outputs O = F / G and G go to out and g; with several,
+// each part's F and G (no division) go to fpw [head][part][N][D] and
+// gpw [head][part][N] for the finalize kernel.
 template <int D, typename T, bool CAUSAL, int MODE>
 __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                    const T *__restrict__ v, T *__restrict__ out,
                                                    float *__restrict__ g, float *__restrict__ sums,
+                                                   float *__restrict__ fpw, float *__restrict__ gpw,
                                                    int N, int nseg, float qs)
 {
     using PT = Pat<D>;
     constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
+    constexpr int NPART = PT::NPART, NGW = PT::NGW, NLB = PT::NLB, Y3R = PT::Y3R;
     constexpr int NSL = D / SL;
     __shared__ Smem<D> sm;
 
     const int item = blockIdx.x / nseg, seg = blockIdx.x % nseg;
-    const int head = item / NSL, sl = item % NSL;
+    const int pp = NPART == 1 ? 0 : item % NPART;
+    const int head = item / (NSL * NPART), sl = (item / NPART) % NSL;
+    const int LB0 = pp * NLB;   // first Y3 row block of the part
     const int nch = (N + C - 1) / C;
     const int cbeg = (int)((long long)seg * nch / nseg), cend = (int)((long long)(seg + 1) * nch / nseg);
     const size_t hb = (size_t)head * N * D;
@@ -149,9 +178,16 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     v += hb;
     out += hb;
     if (g) g += (size_t)head * N;
+    if (NPART > 1) {
+        fpw += (size_t)(head * NPART + pp) * N * D;
+        gpw += (size_t)(head * NPART + pp) * N;
+    }
     float *sum = sums ? sums + (size_t)(item * nseg + seg) * (Sum<D>::BYTES / 4) : nullptr;
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    const int gw = pp * NW + w;   // wave index over the parts
+    // waves holding a Y3 row block for the denominator: the last NLB
+    const int lbl = w - (NW - NLB), lb = LB0 + lbl;
 
     // ---- state, prefix sums and Y3 -------------------------------------
     f4 S[NT];
@@ -162,30 +198,37 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     float y2reg = 0.f, x1reg = 0.f;   // thread d < D: y2[d]; D <= tid < D + SL: x1[tid - D]
     {
         const float *sy3 = loaded ? sum + Sum<D>::STATE : nullptr;
-        for (int e = tid; e < D * D; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy3[e] : 0.f;
+        constexpr int Y3N = Y3R * D;
+        for (int e = tid; e < Y3N; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy3[e] : 0.f;
         if (tid < D) {
-            y2reg = loaded ? sy3[D * D + tid] : 0.f;
+            y2reg = loaded ? sy3[Y3N + tid] : 0.f;
             sm.y2s[tid] = 2.0f * y2reg;
         } else if (tid < D + SL) {
-            x1reg = loaded ? sy3[D * D + D + (tid - D)] : 0.f;
+            x1reg = loaded ? sy3[Y3N + D + (tid - D)] : 0.f;
             sm.x1[tid - D] = x1reg;
         }
     }
-    // Y3 accumulator tiles of this wave: tile index yi = w + 4 kk over the
-    // pairs (u, u2), u <= u2, in row order
+    // Y3 accumulator tiles of this wave, tile index yi = w + 4 kk: one part
+    // takes the pairs (u, u2), u <= u2, in row order; with several parts,
+    // part pp takes rows u = LB0 .. LB0 + NLB - 1, every u2
     constexpr int NYW = (PT::NY3 + NW - 1) / NW;
     f4 Y[NYW];
     int yu[NYW], yu2[NYW];
 #pragma unroll
     for (int kk = 0; kk < NYW; ++kk) {
         const int yi = w + NW * kk;
-        int u = 0, rem = yi;
-        while (u < NU && rem >= NU - u) {
-            rem -= NU - u;
-            ++u;
+        if (NPART == 1) {
+            int u = 0, rem = yi;
+            while (u < NU && rem >= NU - u) {
+                rem -= NU - u;
+                ++u;
+            }
+            yu[kk] = u;
+            yu2[kk] = u + rem;
+        } else {
+            yu[kk] = LB0 + yi / NU;
+            yu2[kk] = yi % NU;
         }
-        yu[kk] = u;
-        yu2[kk] = u + rem;
         Y[kk] = f4{0.f, 0.f, 0.f, 0.f};
     }
     __syncthreads();
@@ -194,7 +237,8 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
         for (int kk = 0; kk < NYW; ++kk) {
             if (w + NW * kk >= PT::NY3) break;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) Y[kk][i] = sm.y3[(16 * yu[kk] + 4 * h + i) * RS + 16 * yu2[kk] + r16];
+            for (int i = 0; i < 4; ++i)
+                Y[kk][i] = sm.y3[(16 * (yu[kk] - LB0) + 4 * h + i) * RS + 16 * yu2[kk] + r16];
         }
     }
 
@@ -251,15 +295,15 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     #pragma unroll
                         for (int i = 0; i < 4; ++i) ql[u][i] = qr[16 * u + 4 * h + i];
                     f4 F = {0.f, 0.f, 0.f, 0.f};
-                    if (w < NU) {
-                        const float *qw = qr + 16 * w + 4 * h;
+                    if (gw < NU) {
+                        const float *qw = qr + 16 * gw + 4 * h;
     #pragma unroll
                         for (int i = 0; i < 4; ++i) F = mma(S[0][i], qw[i], F);
                     }
                     static_for<0, NCH>([&](auto ci) {
                         constexpr int cc = decltype(ci)::value;
-                        constexpr int u0 = cc / 4;
-                        const float qm = qr[w + 4 * cc];
+                        constexpr int u0 = PT::u0(cc);
+                        const float qm = qr[gw + NGW * cc];
                         static_for<u0, NU>([&](auto ui) {
                             constexpr int u = decltype(ui)::value;
                             constexpr int t = PT::first(cc) + u - u0;
@@ -269,11 +313,13 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                         });
                     });
                     if constexpr (M == SCAN && CAUSAL) {
-                        // in-chunk block of row tile rt (wave rt): key tiles st <= rt
+                        // in-chunk blocks of row tile rt (wave rt): the key tiles
+                        // st <= rt that this part owns
                         if (w == rt) {
                             float gsum = 0.f;
     #pragma unroll
                             for (int st = 0; st <= rt; ++st) {
+                                if (inchunk_owner<NPART>(rt, st) != pp) continue;
                                 f4 Sc = {0.f, 0.f, 0.f, 0.f};
                                 const float *kr = sm.krow + (16 * st + r16) * RS;
     #pragma unroll
@@ -296,43 +342,51 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                         }
                     }
                     sm.fpart[w][rt][lane] = F;
-                    // denominator: q^T (Y3 q + 2 y2) over l block w
-                    if (w < NU) {
+                    // denominator: q^T (Y3 q + 2 y2) over l block lb (the last
+                    // NLB waves; the first ones hold the linear and in-chunk work)
+                    if (lbl >= 0) {
                         f4 Tq;
     #pragma unroll
-                        for (int i = 0; i < 4; ++i) Tq[i] = sm.y2s[16 * w + 4 * h + i];
-                        const float *yr = sm.y3 + (16 * w + r16) * RS;
+                        for (int i = 0; i < 4; ++i) Tq[i] = sm.y2s[16 * lb + 4 * h + i];
+                        const float *yr = sm.y3 + (16 * lbl + r16) * RS;
     #pragma unroll
                         for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], qr[4 * kk + h], Tq);
                         float gq = 0.f;
     #pragma unroll
-                        for (int i = 0; i < 4; ++i) gq = fmaf(qr[16 * w + 4 * h + i], Tq[i], gq);
+                        for (int i = 0; i < 4; ++i) gq = fmaf(qr[16 * lb + 4 * h + i], Tq[i], gq);
                         gq += __shfl_xor(gq, 16);
                         gq += __shfl_xor(gq, 32);
-                        if (h == 0) sm.gint[w][tok] = gq;
+                        if (h == 0) sm.gint[lbl][tok] = gq;
                     }
                 }
                 __syncthreads();
                 // ---- outputs O = F / G: token tg, columns 2 part, 2 part + 1 --
+                // (part 0 of several adds the count and x1; each part its
+                // share of the rest)
                 {
                     const int n = n0 + tg;
                     if (n < N) {
                         const int rt = tg >> 4, t16 = tg & 15;
                         float gsum = 0.f;
     #pragma unroll
-                        for (int ww = 0; ww < NU; ++ww) gsum += sm.gint[ww][tg];
-                        float G = (M == QUERY ? (float)N : (float)n0) + 0.5f * gsum;
+                        for (int ww = 0; ww < NLB; ++ww) gsum += sm.gint[ww][tg];
+                        float G = (pp == 0 ? (M == QUERY ? (float)N : (float)n0) : 0.f) + 0.5f * gsum;
                         if (M == SCAN && CAUSAL) G += sm.gin[tg];
                         const float rG = 1.0f / G;
     #pragma unroll
                         for (int i = 0; i < 2; ++i) {
                             const int j = 2 * part + i;
-                            float F = sm.x1[j];
+                            float F = pp == 0 ? sm.x1[j] : 0.f;
     #pragma unroll
                             for (int ww = 0; ww < NW; ++ww) F += sm.fpart[ww][rt][16 * (j >> 2) + t16][j & 3];
-                            io<T>::st(out, (size_t)n * D + SL * sl + j, F * rG);
+                            if (NPART == 1) io<T>::st(out, (size_t)n * D + SL * sl + j, F * rG);
+                            else fpw[(size_t)n * D + SL * sl + j] = F;
                         }
-                        if (g && sl == 0 && part == 0) g[n] = G;
+                        if (NPART == 1) {
+                            if (g && sl == 0 && part == 0) g[n] = G;
+                        } else if (sl == 0 && part == 0) {
+                            gpw[n] = G;
+                        }
                     }
                 }
             }
@@ -346,15 +400,15 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                     for (int ks = 0; ks < C / 4; ++ks) Ak[u][ks] = sm.kT[(16 * u + r16) * TS + 4 * ks + h];
     #pragma unroll
                 for (int ks = 0; ks < C / 4; ++ks) Vb[ks] = sm.vrow[(4 * ks + h) * SL + r16];
-                if (w < NU) {
-                    const float *kl = sm.kT + (16 * w + r16) * TS + h;
+                if (gw < NU) {
+                    const float *kl = sm.kT + (16 * gw + r16) * TS + h;
     #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) S[0] = mma(kl[4 * ks], Vb[ks], S[0]);
                 }
                 static_for<0, NCH>([&](auto ci) {
                     constexpr int cc = decltype(ci)::value;
-                    constexpr int u0 = cc / 4;
-                    const float *km = sm.kT + (w + 4 * cc) * TS + h;
+                    constexpr int u0 = PT::u0(cc);
+                    const float *km = sm.kT + (gw + NGW * cc) * TS + h;
                     float Bm[C / 4];
     #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) Bm[ks] = km[4 * ks] * Vb[ks];
@@ -392,8 +446,8 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int l = 16 * yu[kk] + 4 * h + i, m = 16 * yu2[kk] + r16;
-                        sm.y3[l * RS + m] = Y[kk][i];
-                        sm.y3[m * RS + l] = Y[kk][i];
+                        sm.y3[(l - 16 * LB0) * RS + m] = Y[kk][i];
+                        if (NPART == 1) sm.y3[m * RS + l] = Y[kk][i];
                     }
                 }
                 if (tid < D) sm.y2s[tid] = 2.0f * y2reg;
@@ -418,9 +472,10 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
 #pragma unroll
         for (int t = 0; t < NT; ++t) *(f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) = S[t];
         float *sy3 = sum + Sum<D>::STATE;
-        for (int e = tid; e < D * D; e += NTH) sy3[e] = sm.y3[(e / D) * RS + e % D];
-        if (tid < D) sy3[D * D + tid] = y2reg;
-        else if (tid < D + SL) sy3[D * D + D + (tid - D)] = x1reg;
+        constexpr int Y3N = Y3R * D;
+        for (int e = tid; e < Y3N; e += NTH) sy3[e] = sm.y3[(e / D) * RS + e % D];
+        if (tid < D) sy3[Y3N + tid] = y2reg;
+        else if (tid < D + SL) sy3[Y3N + D + (tid - D)] = x1reg;
     }
 }
 
@@ -464,38 +519,98 @@ int nseg_of(int items, int nch)
     return s;
 }
 
+// Several parts: out = (sum of the parts' F) / (sum of their G), g = that
+// sum; 16 tokens per workgroup, 16 threads per token, D/16 columns each.
+template <int D, typename T>
+__global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ fpw,
+                                                       const float *__restrict__ gpw,
+                                                       T *__restrict__ out, float *__restrict__ g,
+                                                       int N, int nblk)
+{
+    constexpr int NP = Pat<D>::NPART, CPT = D / 16;
+    static_assert(CPT % 4 == 0, "float4 columns");
+    const int head = blockIdx.x / nblk, n = (blockIdx.x % nblk) * 16 + (threadIdx.x >> 4);
+    const int cg = threadIdx.x & 15;
+    if (n >= N) return;
+    float G = 0.f;
+    f4 F[CPT / 4];
+#pragma unroll
+    for (int i = 0; i < CPT / 4; ++i) F[i] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp) {
+        const size_t row = (size_t)(head * NP + pp) * N + n;
+        G += gpw[row];
+        const f4 *src = (const f4 *)(fpw + row * D + CPT * cg);
+#pragma unroll
+        for (int i = 0; i < CPT / 4; ++i) F[i] += src[i];
+    }
+    const float rG = 1.0f / G;
+    const size_t o = ((size_t)head * N + n) * D + CPT * cg;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) io<T>::st(out, o + i, F[i / 4][i % 4] * rG);
+    if (g && cg == 0) g[(size_t)head * N + n] = G;
+}
+
+inline size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Workspace: segment sums (several segments), then the parts' F and G
+// (several parts).
+template <int D>
+struct Plan {
+    int items, nch, nseg;
+    size_t sum_bytes, fp_bytes, gp_bytes;
+    Plan(int BH, int N)
+    {
+        constexpr int NP = Pat<D>::NPART;
+        items = BH * (D / SL) * NP;
+        nch = (N + C - 1) / C;
+        nseg = nseg_of(items, nch);
+        sum_bytes = nseg > 1 ? a256((size_t)items * nseg * Sum<D>::BYTES) : 0;
+        fp_bytes = NP > 1 ? a256((size_t)BH * NP * N * D * 4) : 0;
+        gp_bytes = NP > 1 ? a256((size_t)BH * NP * N * 4) : 0;
+    }
+    size_t bytes() const { return sum_bytes + fp_bytes + gp_bytes; }
+};
+
 template <int D, typename T>
 hipError_t run(const void *q, const void *k, const void *v, void *out, float *g, int BH, int N,
                int causal, float qs, void *ws, hipStream_t st)
 {
-    constexpr int NSL = D / SL;
-    const int items = BH * NSL;
-    const int nch = (N + C - 1) / C;
-    const int nseg = nseg_of(items, nch);
+    const Plan<D> pl(BH, N);
+    const int items = pl.items, nseg = pl.nseg;
     if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)(items * nseg));
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v;
     float *sums = nseg > 1 ? (float *)ws : nullptr;
+    float *fpw = pl.fp_bytes ? (float *)((char *)ws + pl.sum_bytes) : nullptr;
+    float *gpw = pl.gp_bytes ? (float *)((char *)ws + pl.sum_bytes + pl.fp_bytes) : nullptr;
     const size_t stride = Sum<D>::BYTES / 4;
+    const dim3 pgrid((unsigned)((Sum<D>::FLOATS + 255) / 256), items);
     if (causal) {
         if (nseg > 1) {
             hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA>), grid, dim3(NTH), 0, st, Q, K, V,
-                               (T *)out, g, sums, N, nseg, qs);
-            hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)((Sum<D>::FLOATS + 255) / 256), items),
-                               dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS, stride, 1);
+                               (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+            hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
+                               stride, 1);
         }
         hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, sums, N, nseg, qs);
+                           (T *)out, g, sums, fpw, gpw, N, nseg, qs);
     } else if (nseg == 1) {
         hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, nullptr, N, nseg, qs);
+                           (T *)out, g, nullptr, fpw, gpw, N, nseg, qs);
     } else {
         hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, sums, N, nseg, qs);
-        hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)((Sum<D>::FLOATS + 255) / 256), items),
-                           dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS, stride, 0);
+                           (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+        hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
+                           stride, 0);
         hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, sums, N, nseg, qs);
+                           (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+    }
+    if constexpr (Pat<D>::NPART > 1) {
+        const int nblk = (N + 15) / 16;
+        if ((long long)BH * nblk > INT_MAX) return hipErrorInvalidConfiguration;
+        hipLaunchKernelGGL((finalize_kernel<D, T>), dim3((unsigned)(BH * nblk)), dim3(256), 0, st,
+                           fpw, gpw, (T *)out, g, N, nblk);
     }
     return hipGetLastError();
 }
@@ -504,18 +619,19 @@ hipError_t run(const void *q, const void *k, const void *v, void *out, float *g,
 
 bool f32mfma_applies(int D, int p, int is_bf16)
 {
-    return p == 2 && (D == 16 || D == 32 || (D == 64 && !is_bf16));
+    return p == 2 && (D == 16 || D == 32 || D == 128 || (D == 64 && !is_bf16));
 }
 
 size_t f32mfma_fwd_workspace(int BH, int N, int D)
 {
     using namespace m32;
-    const int nch = (N + C - 1) / C;
-    const int items = BH * (D / SL);
-    const int nseg = nseg_of(items, nch);
-    if (nseg == 1) return 0;   // one workgroup per (head, slice): no segment sums
-    const size_t per = D == 16 ? Sum<16>::BYTES : D == 32 ? Sum<32>::BYTES : Sum<64>::BYTES;
-    return (size_t)items * nseg * per;
+    switch (D) {
+    case 16: return Plan<16>(BH, N).bytes();
+    case 32: return Plan<32>(BH, N).bytes();
+    case 64: return Plan<64>(BH, N).bytes();
+    case 128: return Plan<128>(BH, N).bytes();
+    }
+    return 0;
 }
 
 hipError_t f32mfma_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
@@ -525,11 +641,13 @@ hipError_t f32mfma_fwd(const void *q, const void *k, const void *v, void *out, f
     if (is_bf16) {
         if (D == 16) return run<16, bf16_t>(q, k, v, out, g, BH, N, causal, qs, ws, st);
         if (D == 32) return run<32, bf16_t>(q, k, v, out, g, BH, N, causal, qs, ws, st);
+        if (D == 128) return run<128, bf16_t>(q, k, v, out, g, BH, N, causal, qs, ws, st);
         return hipErrorInvalidValue;
     }
     if (D == 16) return run<16, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
     if (D == 32) return run<32, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
     if (D == 64) return run<64, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
+    if (D == 128) return run<128, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
     return hipErrorInvalidValue;
 }
 

@@ -1,9 +1,10 @@
 """GPU parity at head dimension D = 128 (the Llama-2 head size of the paper's
-Sec. 3.1 remark; P = 8385 features at p = 2).  D = 128 runs on the float32
-VALU kernels (one value column per workgroup slice at p = 2, since the state
-of one column is already 33 KB of LDS), so these are correctness tests at
-small N; the multi-chunk, ragged and segmented cases are covered, and the
-backward against the brute-force oracle gradient.
+Sec. 3.1 remark; P = 8385 features at p = 2).  The p = 2 forward runs on the
+float32 MFMA kernels (four workgroups per head and 16-column slice, each with
+a quarter of the feature tiles), p = 1 and the backward on the float32 VALU
+kernels; these are correctness tests at small N (multi-chunk, ragged and
+segmented cases, the backward against the brute-force oracle gradient) and
+the full-size workload on sampled rows.
 """
 import numpy as np
 import pytest

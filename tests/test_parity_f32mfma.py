@@ -1,12 +1,14 @@
 """GPU parity of the float32 MFMA forward (v_mfma_f32_16x16x4_f32; p = 2,
-D in {16, 32} with float32 or bf16 I/O, D = 64 with float32 I/O; causal and
-non-causal) against the fp64 oracle: the explicit N x N definition (Sec. 2.2,
-Eq. "tobeexpanded") on small shapes, the factorised oracle (Sec. 2.4) on the
-full LRA-shaped and small configurations.
+D in {16, 32, 128} with float32 or bf16 I/O, D = 64 with float32 I/O; causal
+and non-causal) against the fp64 oracle: the explicit N x N definition
+(Sec. 2.2, Eq. "tobeexpanded") on small shapes, the factorised oracle
+(Sec. 2.4) on the full LRA-shaped and small configurations.
 
 Shapes cover one token, ragged 32-token chunks, one and many segments per
 head (few heads split a sequence into segments whose sums are prefix-summed),
-and the score scale.  Bars: float32 max|dO|/max|O_ref| <= 1e-4 and
+and the score scale.  At D = 128 four workgroups share each (head, slice),
+each holding a quarter of the feature tiles, and a finalize pass sums their
+partial F and G; those cases run with one and with several segments.  Bars: float32 max|dO|/max|O_ref| <= 1e-4 and
 max_i |dG_i|/G_i <= 1e-4; bf16 I/O 2e-2.
 """
 import numpy as np
@@ -50,7 +52,7 @@ def check(inp, causal, dtype, label, ref="brute", scale=None):
     assert e <= TOL[dtype] and eg <= TOL[dtype], (label, e, eg)
 
 
-CASES = [(D, causal, dtype) for D in (16, 32, 64) for causal in (False, True)
+CASES = [(D, causal, dtype) for D in (16, 32, 64, 128) for causal in (False, True)
          for dtype in ("f32", "bf16") if not (D == 64 and dtype == "bf16")]
 SHAPES = [(1, 1, 1), (1, 2, 5), (2, 1, 31), (1, 1, 32), (1, 2, 33), (2, 3, 100), (1, 1, 257),
           (1, 1, 1000)]
@@ -65,11 +67,12 @@ def test_f32mfma_vs_brute(case, shape):
     check(inp, causal, dtype, f"f32mfma D={D} causal={causal} {dtype} B={B} H={H} N={N}")
 
 
-@pytest.mark.parametrize("D", [16, 32, 64])
+@pytest.mark.parametrize("D", [16, 32, 64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 def test_f32mfma_many_segments(D, causal):
-    """One head, 4000 tokens: up to 125 segments of one 32-token chunk each,
-    their sums prefix-summed (causal) or totalled (non-causal)."""
+    """One head, 4000 tokens: up to 125 segments of one 32-token chunk each
+    (8 at D = 128, whose head spans 32 workgroups), their sums prefix-summed
+    (causal) or totalled (non-causal)."""
     inp = make_inputs(1, 1, 4000, D, 9300 + D, "f32")
     check(inp, causal, "f32", f"f32mfma segments D={D} causal={causal}", ref="fact")
 
@@ -97,3 +100,18 @@ def test_f32mfma_one_segment_per_head(D, dtype, causal):
     assert fm.workspace_bytes(B, H, 100, D, 2, causal, fm.F32 if dtype == "f32" else fm.BF16) == 0
     inp = make_inputs(B, H, 100, D, 9500 + D, dtype)
     check(inp, causal, dtype, f"f32mfma one segment D={D} {dtype} causal={causal}")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("BH", [(2, 4), (3, 4)])
+def test_f32mfma_d128_one_segment(BH, dtype, causal):
+    """D = 128 with one workgroup per (head, slice, quarter of the features):
+    no segment sums, the workspace holds only the partial F and G."""
+    B, H = BH
+    N = 100
+    ws = fm.workspace_bytes(B, H, N, 128, 2, causal, fm.F32 if dtype == "f32" else fm.BF16)
+    r256 = lambda b: (b + 255) // 256 * 256
+    assert ws == r256(B * H * 4 * N * 128 * 4) + r256(B * H * 4 * N * 4), ws
+    inp = make_inputs(B, H, N, 128, 9600 + B, dtype)
+    check(inp, causal, dtype, f"f32mfma D=128 one segment B={B} H={H} {dtype} causal={causal}")
