@@ -260,7 +260,11 @@ const char *fastmax_version(void);
  * size are rejected with FASTMAX_EWORKSPACE before anything is enqueued
  * (e.g. the causal bf16, D = 64, p = 2 forward, whose workspace holds q^ and
  * k^ in fp16 and about 0.4 MB of scan-segment summaries per head, takes one
- * head of up to 260594 tokens, or up to 46 heads of 4096 tokens).  The call allocates nothing (no hipMalloc, no library allocation);
+ * head of up to 260594 tokens, or up to 46 heads of 4096 tokens; the D = 128,
+ * p = 2 forward keeps four partial float32 numerators per token, about 2 KB
+ * per token and head, and takes 8 heads of up to 4064 tokens, or one head of
+ * up to 11589).  The call allocates nothing (no hipMalloc, no library
+ * allocation);
  * the first call on a GPU looks the array's device address up once
  * (FASTMAX_EHIP if HIP refuses).  Every call on one GPU shares that GPU's
  * array: calls whose work overlaps on one GPU (different streams without

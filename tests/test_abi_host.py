@@ -309,6 +309,11 @@ def test_fwd_noalloc_rejects_problems_beyond_its_scratch():
     assert fm.workspace_bytes(1, 1, 260595, 64, 2, 1, fm.BF16) > lim
     assert fm.workspace_bytes(1, 46, 4096, 64, 2, 1, fm.BF16) <= lim
     assert fm.workspace_bytes(1, 47, 4096, 64, 2, 1, fm.BF16) > lim
+    # and the D = 128 p = 2 ones (four partial numerators per token)
+    assert fm.workspace_bytes(1, 8, 4064, 128, 2, 1, fm.BF16) <= lim
+    assert fm.workspace_bytes(1, 8, 4065, 128, 2, 1, fm.BF16) > lim
+    assert fm.workspace_bytes(1, 1, 11589, 128, 2, 1, fm.BF16) <= lim
+    assert fm.workspace_bytes(1, 1, 11590, 128, 2, 1, fm.BF16) > lim
 
 
 def test_scan_segment_mode_setter():
