@@ -66,8 +66,8 @@ bool mfma_causal(int D, int p, int causal, int dt)
     return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
 }
 
-// The float32 MFMA forward serves p = 2 wherever the fp16 MFMA kernels do
-// not: float32 I/O for D <= 64 and bf16 I/O for D <= 32.
+// The float32 MFMA kernels (forward and backward) serve p = 2 wherever the
+// fp16 MFMA kernels do not: float32 I/O for every D, bf16 I/O for D != 64.
 bool f32mfma(int D, int p, int causal, int dt, int N)
 {
     if (mfma_causal(D, p, causal, dt) || mfma_noncausal(N, D, p, causal, dt)) return false;
@@ -86,6 +86,7 @@ size_t bwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_bwd_workspace(B * H, N);
     if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_bwd_workspace(B * H, N);
+    if (f32mfma(D, p, causal, dt, N)) return fm::f32mfma_bwd_workspace(B * H, N, D);
     return fm::generic_bwd_workspace(B, H, N, D, p);
 }
 
@@ -166,6 +167,9 @@ int bwd_impl(const void *q, const void *k, const void *v, const void *out, const
     else if (mfma_noncausal(N, D, p, causal, dt))
         e = fm::mfma_nc_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, qk_scale, workspace,
                             stream);
+    else if (f32mfma(D, p, causal, dt, N))
+        e = fm::f32mfma_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, causal,
+                            dt == FASTMAX_BF16, qk_scale, workspace, stream);
     else
         e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
                             dt == FASTMAX_BF16, qk_scale, workspace, stream);

@@ -1,0 +1,607 @@
+// Fastmax backward on float32 MFMA (v_mfma_f32_16x16x4_f32), p = 2, the cases
+// of the float32 MFMA forward.  Sec. 2.5's custom gradient: only O and G are
+// kept from the forward, q^ and k^ are recomputed, and the moments are
+// rebuilt by scans instead of stored.  With u_i = dO_i / G_i,
+// c_i = (dO_i . O_i) / G_i and s_in = q~_i . k^_n (q~ = tau q^):
+//
+//   dv_n  = sum_{i >= n} f(s_in) u_i
+//   dq~_i = sum_{n <= i} f'(s_in) (u_i . v_n - c_i) k^_n
+//   dk^_n = sum_{i >= n} f'(s_in) (u_i . v_n - c_i) q~_i       (f' = 1 + s)
+//
+// (all n, i for the non-causal problem), then back through the
+// standardisation (Eqs. 6-7).  dv is the forward's scan over the reversed
+// sequence with queries and keys exchanged (fm_f32_mfma.hip).  dq~ and dk^
+// are one "gradient scan" run twice with the roles exchanged: with state
+// keys X, state values VS, state weights w, contraction features Z,
+// contraction columns UC and contraction scalars z,
+//
+//   out_t = sum_{r before t} f'(Z_t . X_r) (UC_t . VS_r + z_t w_r) X_r
+//
+// dq~: X = k^, VS = v, w = 1, Z = q~, UC = u, z = -c (forward order);
+// dk^: X = q~, VS = u, w = c, Z = k^, UC = v, z = -1 (reverse order).
+// Expanded, out_t[l] = sum_c UC_tc L[l][c] + z_t y2w[l]
+//                      + sum_m Z_tm (sum_c UC_tc Q[m,l][c] + z_t Y3w[m][l])
+// with the moment state L = sum_r X_r VS_r^T, Q[m,l] = sum_r X_rm X_rl VS_r^T
+// (the forward's state, per 16-column slice of VS), y2w = sum_r w_r X_r and
+// Y3w = sum_r w_r X_r X_r^T; chunks of 32 tokens add their in-chunk pairs
+// directly.
+//
+// The state tiles are kept transposed with respect to the forward's: lane
+// (r16, h) element i holds feature 16u + r16, column 4h + i, so element i
+// is the A operand of K step i of a contraction over the columns, whose B
+// operand UC_t[4h + i] is shared by every tile; each tile gives
+// T[l][t] = sum_c Q[m,l][c] UC_tc in the layout (token r16, feature 4h + i)
+// of the per-wave output rows.  A diagonal tile (both orders of its pairs)
+// adds Z_tm T[l] to out_t[l]; an off-diagonal tile (m's block below l's)
+// also adds sum_l Z_tl T[l] to out_t[m].  The waves' rows meet in LDS
+// (LDS float atomics), and each chunk's rows are added to the float32
+// gradient with global float atomics (the column slices and feature parts of
+// a head add into the same rows).
+#include <hip/hip_runtime.h>
+
+#include <limits.h>
+
+#include "fm_common.h"
+#include "fm_f32_mfma.h"
+#include "fm_internal.h"
+
+namespace fm {
+namespace m32 {
+
+template <int D>
+struct alignas(16) GSmem {
+    float xrow[C * Pat<D>::RS];    // state keys X [token][channel]
+    float xT[D * Pat<D>::TS];      // X [channel][token]
+    alignas(16) float zrow[C * (D + 4)];   // contraction features Z [token][channel] (16-byte rows)
+    float vs[C * SL];              // state values, this slice [token][column]
+    float uc[C * SL];              // contraction columns, this slice
+    float wt[C];                   // state weights w
+    float zt[C];                   // contraction scalars z
+    float y3[16 * Pat<D>::RS];     // the item's row block of Y3w (before the chunk)
+    float y2[16];                  // its entries of y2w
+    float ob[C * Pat<D>::RS];      // the chunk's output rows, summed over the waves
+};
+
+// Segment summary: [wave][tile][lane] f4 state, the Y3w row block [16][D],
+// y2w [16].
+template <int D>
+struct GSum {
+    static constexpr size_t STATE = (size_t)NW * Pat<D>::NT * 64 * 4;
+    static constexpr size_t FLOATS = STATE + 16 * D + 16;
+    static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
+};
+
+// One workgroup: (item = (head * NSL + slice) * NPART + part, segment).  The
+// item (slice, part) with index sl * NPART + part = b < D/16 also keeps row
+// block b of Y3w and y2w; slice 0 adds the z_t w_r term of the in-chunk pairs.
+template <int D, typename T, bool CAUSAL, int MODE, bool REV>
+__global__ __launch_bounds__(NTH) void grad_kernel(
+    const T *__restrict__ X, const T *__restrict__ Z, const T *__restrict__ VS,
+    const T *__restrict__ UC, const float *__restrict__ vsm, const float *__restrict__ ucm,
+    const float *__restrict__ wv, const float *__restrict__ zv, float *__restrict__ outh,
+    float *__restrict__ sums, int N, int nseg, float xs, float zsc)
+{
+    using PT = Pat<D>;
+    constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
+    constexpr int NPART = PT::NPART, NGW = PT::NGW;
+    constexpr int NSL = D / SL;
+    constexpr int ZS = D + 4;   // row stride of Z
+    __shared__ GSmem<D> sm;
+
+    const int item = blockIdx.x / nseg, seg = blockIdx.x % nseg;
+    const int pp = NPART == 1 ? 0 : item % NPART;
+    const int head = item / (NSL * NPART), sl = (item / NPART) % NSL;
+    const int yb = item % (NSL * NPART);
+    const int ylb = yb < NU ? yb : -1;   // the item's Y3w row block, if any
+    const bool scal = sl == 0;
+    const int nch = (N + C - 1) / C;
+    const int cbeg = (int)((long long)seg * nch / nseg), cend = (int)((long long)(seg + 1) * nch / nseg);
+    const size_t hb = (size_t)head * N * D;
+    X += hb;
+    Z += hb;
+    VS += hb;
+    UC += hb;
+    outh += hb;
+    if (vsm) vsm += (size_t)head * N;
+    if (ucm) ucm += (size_t)head * N;
+    if (wv) wv += (size_t)head * N;
+    if (zv) zv += (size_t)head * N;
+    float *sum = sums ? sums + (size_t)(item * nseg + seg) * (GSum<D>::BYTES / 4) : nullptr;
+
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, h = lane >> 4;
+    const int gw = pp * NW + w;
+
+    // ---- state, Y3w block, y2w -----------------------------------------
+    f4 S[NT];
+    const bool loaded = MODE == QUERY || (MODE == SCAN && seg > 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+        S[t] = loaded ? *(const f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) : f4{0.f, 0.f, 0.f, 0.f};
+    float y2reg = 0.f;   // thread tid < 16 of an item with a Y3w block: y2w[16 ylb + tid]
+    {
+        const float *sy = loaded ? sum + GSum<D>::STATE : nullptr;
+        for (int e = tid; e < 16 * D; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy[e] : 0.f;
+        if (tid < 16) {
+            y2reg = loaded ? sy[16 * D + tid] : 0.f;
+            sm.y2[tid] = y2reg;
+        }
+        for (int e = tid; e < C * RS; e += NTH) sm.ob[e] = 0.f;
+    }
+    // Y3w tiles (ylb, u2), u2 = w + 4 kk
+    constexpr int NYW = (NU + NW - 1) / NW;
+    f4 Y[NYW];
+#pragma unroll
+    for (int kk = 0; kk < NYW; ++kk) Y[kk] = f4{0.f, 0.f, 0.f, 0.f};
+    __syncthreads();
+    if (loaded && ylb >= 0) {
+#pragma unroll
+        for (int kk = 0; kk < NYW; ++kk) {
+            const int u2 = w + NW * kk;
+            if (u2 >= NU) break;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) Y[kk][i] = sm.y3[(4 * h + i) * RS + 16 * u2 + r16];
+        }
+    }
+
+    // ---- staging: token tg = tid / 8, channels 8-way split, 2 columns ---
+    const int tg = tid >> 3, part = tid & 7;
+    constexpr int DP = D / 8;
+    float px[DP], pz[DP], pvs[2], puc[2], pw = 0.f, pzs = 0.f;
+    bool pvalid = false;
+    auto prefetch = [&](int c) {
+        const int n0 = c * C + tg;
+        pvalid = n0 < N;
+        const int n = REV ? N - 1 - n0 : n0;   // the token's place in memory
+#pragma unroll
+        for (int i = 0; i < DP; ++i) {
+            px[i] = pvalid ? io<T>::ld(X, (size_t)n * D + part * DP + i) : 0.f;
+            pz[i] = pvalid ? io<T>::ld(Z, (size_t)n * D + part * DP + i) : 0.f;
+        }
+        const float vm = vsm && pvalid ? vsm[n] : 1.0f, um = ucm && pvalid ? ucm[n] : 1.0f;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const size_t e = (size_t)n * D + SL * sl + 2 * part + i;
+            pvs[i] = pvalid ? io<T>::ld(VS, e) * vm : 0.f;
+            puc[i] = pvalid ? io<T>::ld(UC, e) * um : 0.f;
+        }
+        pw = pvalid ? (wv ? wv[n] : 1.0f) : 0.f;
+        pzs = pvalid ? -(zv ? zv[n] : 1.0f) : 0.f;
+    };
+    auto stage = [&]() {
+        standardise_part<D>(px, pvalid, xs);
+        standardise_part<D>(pz, pvalid, zsc);
+#pragma unroll
+        for (int i = 0; i < DP; ++i) {
+            const int ch = part * DP + i;
+            sm.xrow[tg * RS + ch] = px[i];
+            sm.xT[ch * TS + tg] = px[i];
+            sm.zrow[tg * ZS + ch] = pz[i];
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            sm.vs[tg * SL + 2 * part + i] = pvs[i];
+            sm.uc[tg * SL + 2 * part + i] = puc[i];
+        }
+        if (part == 0) {
+            sm.wt[tg] = pw;
+            sm.zt[tg] = pzs;
+        }
+    };
+
+    // one chunk in mode M (DELTA: state update only; QUERY: outputs only;
+    // SCAN: outputs, then the update unless the segment ends here)
+    auto chunk = [&](auto mc, int c) {
+        constexpr int M = decltype(mc)::value;
+        const int n0 = c * C;
+        stage();
+        if (c + 1 < cend) prefetch(c + 1);
+        __syncthreads();
+
+        if constexpr (M != DELTA) {
+#pragma unroll
+            for (int rt = 0; rt < C / 16; ++rt) {
+                const int tok = 16 * rt + r16;
+                const float *zr = sm.zrow + tok * ZS;
+                float *orow = sm.ob + tok * RS;
+                float ub[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) ub[i] = sm.uc[tok * SL + 4 * h + i];
+                // linear tile: out[l] += sum_c UC_c L[l][c], l in block gw
+                if (gw < NU) {
+                    f4 Tl = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) Tl = mma(S[0][i], ub[i], Tl);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * gw + 4 * h + i, Tl[i]);
+                }
+                // quadratic tiles, by output block u: tile (m, u) of channel
+                // m = gw + NGW cc adds Z_m T[l] to out[l], l in block u, and (off
+                // the diagonal) sum_l Z_l T[l] to out[m]
+                float dmv[NCH];
+#pragma unroll
+                for (int cc = 0; cc < NCH; ++cc) dmv[cc] = 0.f;
+                static_for<0, NU>([&](auto ui) {
+                    constexpr int u = decltype(ui)::value;
+                    const f4 zlu = *(const f4 *)(zr + 16 * u + 4 * h);
+                    f4 a4 = {0.f, 0.f, 0.f, 0.f};
+                    static_for<0, NCH>([&](auto ci) {
+                        constexpr int cc = decltype(ci)::value;
+                        constexpr int u0 = PT::u0(cc);
+                        if constexpr (u >= u0) {
+                            constexpr int t = PT::first(cc) + u - u0;
+                            const float zm = zr[gw + NGW * cc];
+                            f4 Tt = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) Tt = mma(S[t][i], ub[i], Tt);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) a4[i] = fmaf(zm, Tt[i], a4[i]);
+                            if constexpr (u > u0) {
+#pragma unroll
+                                for (int i = 0; i < 4; ++i) dmv[cc] = fmaf(zlu[i], Tt[i], dmv[cc]);
+                            }
+                        }
+                    });
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * u + 4 * h + i, a4[i]);
+                });
+                static_for<0, NCH>([&](auto ci) {
+                    constexpr int cc = decltype(ci)::value;
+                    if constexpr (PT::u0(cc) + 1 < NU) {
+                        float dm = dmv[cc];
+                        dm += __shfl_xor(dm, 16);
+                        dm += __shfl_xor(dm, 32);
+                        if (h == 0) atomicAdd(orow + gw + NGW * cc, dm);
+                    }
+                });
+                if constexpr (M == SCAN && CAUSAL) {
+                    // in-chunk pairs: key tile st <= rt, on wave b of the owning part
+#pragma unroll
+                    for (int st = 0; st <= rt; ++st) {
+                        const int b = rt * (rt + 1) / 2 + st;
+                        if (inchunk_owner<NPART>(rt, st) != pp || w != b) continue;
+                        // S^T and P^T: lane (token tok, keys 16 st + 4h + i)
+                        f4 Sc = {0.f, 0.f, 0.f, 0.f}, Pc = {0.f, 0.f, 0.f, 0.f};
+                        const float *xr = sm.xrow + (16 * st + r16) * RS;
+#pragma unroll
+                        for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[4 * kk + h], zr[4 * kk + h], Sc);
+                        const float *vr = sm.vs + (16 * st + r16) * SL;
+#pragma unroll
+                        for (int kk = 0; kk < 4; ++kk)
+                            Pc = mma(vr[4 * kk + h], sm.uc[tok * SL + 4 * kk + h], Pc);
+                        const float zs = scal ? sm.zt[tok] : 0.f;
+                        float Wt[4];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            float wgt = (1.0f + Sc[i]) * fmaf(zs, sm.wt[16 * st + 4 * h + i], Pc[i]);
+                            if (st == rt && 4 * h + i > r16) wgt = 0.0f;
+                            Wt[i] = wgt;
+                        }
+                        // out[l] += sum_r W[t][r] X_r[l]
+#pragma unroll
+                        for (int u = 0; u < NU; ++u) {
+                            f4 ic = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                ic = mma(sm.xrow[(16 * st + 4 * h + i) * RS + 16 * u + r16], Wt[i], ic);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * u + 4 * h + i, ic[i]);
+                        }
+                    }
+                }
+                // the item's Y3w block: out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
+                if (ylb >= 0 && w == NW - 1) {
+                    f4 Tq;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
+                    const float *yr = sm.y3 + r16 * RS;
+#pragma unroll
+                    for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], zr[4 * kk + h], Tq);
+                    const float zs = sm.zt[tok];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * ylb + 4 * h + i, zs * Tq[i]);
+                }
+            }
+            __syncthreads();
+            // the chunk's rows into the float32 gradient; clear them for the next chunk
+            for (int e = tid; e < C * D; e += NTH) {
+                const int t = e / D, d = e % D, n = n0 + t;
+                const float val = sm.ob[t * RS + d];
+                sm.ob[t * RS + d] = 0.f;
+                if (n < N) atomicAdd(outh + (size_t)(REV ? N - 1 - n : n) * D + d, val);
+            }
+        }
+        if constexpr (M != QUERY) {
+            if (M == SCAN && c + 1 == cend) return;   // the next segment starts from its prefix
+            // ---- state update (transposed tiles), Y3w block, y2w --------------
+            float Ak[NU][C / 4], Vb[C / 4];
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+#pragma unroll
+                for (int ks = 0; ks < C / 4; ++ks) Ak[u][ks] = sm.xT[(16 * u + r16) * TS + 4 * ks + h];
+#pragma unroll
+            for (int ks = 0; ks < C / 4; ++ks) Vb[ks] = sm.vs[(4 * ks + h) * SL + r16];
+            if (gw < NU) {
+                const float *xl = sm.xT + (16 * gw + r16) * TS + h;
+#pragma unroll
+                for (int ks = 0; ks < C / 4; ++ks) S[0] = mma(Vb[ks], xl[4 * ks], S[0]);
+            }
+            static_for<0, NCH>([&](auto ci) {
+                constexpr int cc = decltype(ci)::value;
+                constexpr int u0 = PT::u0(cc);
+                const float *xm = sm.xT + (gw + NGW * cc) * TS + h;
+                float Bm[C / 4];
+#pragma unroll
+                for (int ks = 0; ks < C / 4; ++ks) Bm[ks] = xm[4 * ks] * Vb[ks];
+                static_for<u0, NU>([&](auto ui) {
+                    constexpr int u = decltype(ui)::value;
+                    constexpr int t = PT::first(cc) + u - u0;
+#pragma unroll
+                    for (int ks = 0; ks < C / 4; ++ks) S[t] = mma(Bm[ks], Ak[u][ks], S[t]);
+                });
+            });
+            if (ylb >= 0) {
+                const float *xa = sm.xT + (16 * ylb + r16) * TS + h;
+                float aw[C / 4];
+#pragma unroll
+                for (int ks = 0; ks < C / 4; ++ks) aw[ks] = xa[4 * ks] * sm.wt[4 * ks + h];
+#pragma unroll
+                for (int kk = 0; kk < NYW; ++kk) {
+                    const int u2 = w + NW * kk;
+                    if (u2 >= NU) break;
+                    const float *xb = sm.xT + (16 * u2 + r16) * TS + h;
+#pragma unroll
+                    for (int ks = 0; ks < C / 4; ++ks) Y[kk] = mma(aw[ks], xb[4 * ks], Y[kk]);
+                }
+                if (tid < 16) {
+                    float s = 0.f;
+#pragma unroll 8
+                    for (int t = 0; t < C; ++t) s = fmaf(sm.wt[t], sm.xrow[t * RS + 16 * ylb + tid], s);
+                    y2reg += s;
+                }
+            }
+            __syncthreads();
+            if (ylb >= 0) {
+#pragma unroll
+                for (int kk = 0; kk < NYW; ++kk) {
+                    const int u2 = w + NW * kk;
+                    if (u2 >= NU) break;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) sm.y3[(4 * h + i) * RS + 16 * u2 + r16] = Y[kk][i];
+                }
+                if (tid < 16) sm.y2[tid] = y2reg;
+            }
+        }
+        __syncthreads();
+    };
+    if constexpr (MODE == BOTH) {
+        // non-causal, one segment: the totals first, then every output row
+        prefetch(cbeg);
+        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, DELTA>{}, c);
+        prefetch(cbeg);
+        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, QUERY>{}, c);
+    } else {
+        prefetch(cbeg);
+        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, MODE>{}, c);
+    }
+
+    if constexpr (MODE == DELTA) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) *(f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) = S[t];
+        float *sy = sum + GSum<D>::STATE;
+        for (int e = tid; e < 16 * D; e += NTH) sy[e] = sm.y3[(e / D) * RS + e % D];
+        if (tid < 16) sy[16 * D + tid] = y2reg;
+    }
+}
+
+// rg_i = 1 / G_i, c_i = (dO_i . O_i) / G_i; clears the float32 gradients.
+// 16 threads per token.
+template <int D, typename T>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const T *__restrict__ o,
+                                                       const T *__restrict__ dout,
+                                                       const float *__restrict__ g,
+                                                       float *__restrict__ rg,
+                                                       float *__restrict__ cvec,
+                                                       float *__restrict__ dqh,
+                                                       float *__restrict__ dkh, size_t rows)
+{
+    const size_t r = (size_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+    const int j = threadIdx.x & 15;
+    if (r >= rows) return;   // whole groups of 16 lanes
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) {
+        const size_t e = r * D + j + 16 * i;
+        acc = fmaf(io<T>::ld(dout, e), io<T>::ld(o, e), acc);
+        dqh[e] = 0.f;
+        dkh[e] = 0.f;
+    }
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    acc += __shfl_xor(acc, 8);
+    if (j == 0) {
+        const float G = g[r];
+        rg[r] = 1.0f / G;
+        cvec[r] = acc / G;
+    }
+}
+
+// Back through Eqs. (6)-(7) and cast: dx = (dx^ - mean dx^ - x^ mean(dx^ x^)) / std,
+// dx^ = sc dxh (the scans differentiate with respect to the scaled query
+// tau q^).  blockIdx.y: 0 = dq, 1 = dk; 16 threads per token.
+template <int D, typename T>
+__global__ __launch_bounds__(256) void bwd_finish_kernel(const T *__restrict__ q,
+                                                         const T *__restrict__ k,
+                                                         const float *__restrict__ dqh,
+                                                         const float *__restrict__ dkh,
+                                                         T *__restrict__ dq, T *__restrict__ dk,
+                                                         size_t rows, float qs)
+{
+    const int which = blockIdx.y;
+    const T *x = which ? k : q;
+    const float *dxh = which ? dkh : dqh;
+    T *dx = which ? dk : dq;
+    const float sc = which ? 1.0f : qs;
+    const size_t r = (size_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+    const int j = threadIdx.x & 15;
+    if (r >= rows) return;
+    constexpr int CPT = D / 16;
+    float xv[CPT], gv[CPT];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+        const size_t e = r * D + j + 16 * i;
+        xv[i] = io<T>::ld(x, e);
+        gv[i] = sc * dxh[e];
+        s += xv[i];
+    }
+    auto sum16 = [](float a) {
+        a += __shfl_xor(a, 1);
+        a += __shfl_xor(a, 2);
+        a += __shfl_xor(a, 4);
+        a += __shfl_xor(a, 8);
+        return a;
+    };
+    const float mu = sum16(s) * (1.0f / D);
+    float var = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+        xv[i] -= mu;
+        var = fmaf(xv[i], xv[i], var);
+    }
+    const float rs = rsqrtf(sum16(var) * (1.0f / D));
+    float m1 = 0.f, m2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+        xv[i] *= rs;
+        m1 += gv[i];
+        m2 = fmaf(gv[i], xv[i], m2);
+    }
+    m1 = sum16(m1) * (1.0f / D);
+    m2 = sum16(m2) * (1.0f / D);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+        io<T>::st(dx, r * D + j + 16 * i, (gv[i] - m1 - xv[i] * m2) * rs);
+}
+
+template <int D>
+struct BwdPlan {
+    int items, nch, nseg;
+    size_t vec_bytes, grad_bytes, scan_bytes;
+    BwdPlan(int BH, int N)
+    {
+        items = BH * (D / SL) * Pat<D>::NPART;
+        nch = (N + C - 1) / C;
+        nseg = nseg_of(items, nch);
+        const size_t rows = (size_t)BH * N;
+        vec_bytes = a256(rows * 4);
+        grad_bytes = a256(rows * D * 4);
+        const size_t gsum = nseg > 1 ? a256((size_t)items * nseg * GSum<D>::BYTES) : 0;
+        const size_t fwd = f32mfma_fwd_workspace(BH, N, D);   // the dv scan's
+        scan_bytes = gsum > fwd ? gsum : fwd;
+    }
+    // rg, c, dq~, dk^, then the scans' region (used by one scan at a time)
+    size_t bytes() const { return 2 * vec_bytes + 2 * grad_bytes + scan_bytes; }
+};
+
+template <int D, typename T, bool REV>
+hipError_t grad_launch(const BwdPlan<D> &pl, const T *X, const T *Z, const T *VS, const T *UC,
+                       const float *vsm, const float *ucm, const float *wv, const float *zv,
+                       float *outh, float *sums, int N, int causal, float xs, float zsc,
+                       hipStream_t st)
+{
+    const int items = pl.items, nseg = pl.nseg;
+    if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)(items * nseg));
+    const size_t stride = GSum<D>::BYTES / 4;
+    const dim3 pgrid((unsigned)((GSum<D>::FLOATS + 255) / 256), items);
+    if (causal) {
+        if (nseg > 1) {
+            hipLaunchKernelGGL((grad_kernel<D, T, true, DELTA, REV>), grid, dim3(NTH), 0, st, X, Z,
+                               VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+            hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg,
+                               GSum<D>::FLOATS, stride, 1);
+        }
+        hipLaunchKernelGGL((grad_kernel<D, T, true, SCAN, REV>), grid, dim3(NTH), 0, st, X, Z, VS,
+                           UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+    } else if (nseg == 1) {
+        hipLaunchKernelGGL((grad_kernel<D, T, false, BOTH, REV>), grid, dim3(NTH), 0, st, X, Z,
+                           VS, UC, vsm, ucm, wv, zv, outh, nullptr, N, nseg, xs, zsc);
+    } else {
+        hipLaunchKernelGGL((grad_kernel<D, T, false, DELTA, REV>), grid, dim3(NTH), 0, st, X, Z,
+                           VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+        hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, GSum<D>::FLOATS,
+                           stride, 0);
+        hipLaunchKernelGGL((grad_kernel<D, T, false, QUERY, REV>), grid, dim3(NTH), 0, st, X, Z,
+                           VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+    }
+    return hipGetLastError();
+}
+
+template <int D, typename T>
+hipError_t bwd_run(const void *q, const void *k, const void *v, const void *o, const void *dout,
+                   const float *g, void *dq, void *dk, void *dv, int BH, int N, int causal,
+                   float qs, void *ws, hipStream_t st)
+{
+    const BwdPlan<D> pl(BH, N);
+    const size_t rows = (size_t)BH * N;
+    char *p = (char *)ws;
+    float *rg = (float *)p;
+    float *cvec = (float *)(p + pl.vec_bytes);
+    float *dqh = (float *)(p + 2 * pl.vec_bytes);
+    float *dkh = (float *)(p + 2 * pl.vec_bytes + pl.grad_bytes);
+    void *scan = p + 2 * pl.vec_bytes + 2 * pl.grad_bytes;
+    const size_t rb = (rows + 15) / 16;
+    if (rb > (size_t)INT_MAX) return hipErrorInvalidConfiguration;
+    const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v, *DO = (const T *)dout;
+    hipLaunchKernelGGL((bwd_prep_kernel<D, T>), dim3((unsigned)rb), dim3(256), 0, st, (const T *)o,
+                       DO, g, rg, cvec, dqh, dkh, rows);
+    hipError_t e = f32mfma_dv(q, k, dout, rg, dv, BH, N, D, causal, std::is_same<T, bf16_t>::value,
+                              qs, scan, st);
+    if (e != hipSuccess) return e;
+    // dq~: X = k^, VS = v, w = 1; Z = tau q^, UC = dO / G, z = -c
+    e = grad_launch<D, T, false>(pl, K, Q, V, DO, nullptr, rg, nullptr, cvec, dqh, (float *)scan,
+                                 N, causal, 1.0f, qs, st);
+    if (e != hipSuccess) return e;
+    // dk^: X = tau q^, VS = dO / G, w = c; Z = k^, UC = v, z = -1 (reverse order)
+    e = grad_launch<D, T, true>(pl, Q, K, DO, V, rg, nullptr, cvec, nullptr, dkh, (float *)scan,
+                                N, causal, qs, 1.0f, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((bwd_finish_kernel<D, T>), dim3((unsigned)rb, 2), dim3(256), 0, st, Q, K,
+                       dqh, dkh, (T *)dq, (T *)dk, rows, qs);
+    return hipGetLastError();
+}
+
+}  // namespace m32
+
+size_t f32mfma_bwd_workspace(int BH, int N, int D)
+{
+    using namespace m32;
+    switch (D) {
+    case 16: return BwdPlan<16>(BH, N).bytes();
+    case 32: return BwdPlan<32>(BH, N).bytes();
+    case 64: return BwdPlan<64>(BH, N).bytes();
+    case 128: return BwdPlan<128>(BH, N).bytes();
+    }
+    return 0;
+}
+
+hipError_t f32mfma_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
+                       int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st)
+{
+    using namespace m32;
+    if (is_bf16) {
+        if (D == 16) return bwd_run<16, bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+        if (D == 32) return bwd_run<32, bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+        if (D == 128) return bwd_run<128, bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+        return hipErrorInvalidValue;
+    }
+    if (D == 16) return bwd_run<16, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    if (D == 32) return bwd_run<32, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    if (D == 64) return bwd_run<64, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    if (D == 128) return bwd_run<128, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace fm

@@ -1,0 +1,151 @@
+// Shared pieces of the float32 MFMA kernels (v_mfma_f32_16x16x4_f32, p = 2):
+// the forward and backward scans of fm_f32_mfma.hip and fm_f32_bwd.hip.
+//
+// MFMA lane layout (16x16x4 f32, lane = 16h + r16): A holds row r16, K index
+// h; B holds column r16, K index h; the accumulator holds column r16, rows
+// 4h..4h+3.  Contractions over 16 rows of an accumulator run as four K steps
+// i = 0..3 with K index h <-> row 4h + i, so element i of an accumulator is
+// directly the A operand of step i (no data movement).
+//
+// Feature tiles (16 features of phi(k) = [k_l, (k_m k_l)] x 16 value
+// columns): the linear tiles u (features k_l, l = 16u..16u+15) and the
+// quadratic tiles (m, u) for u >= m/16 (features k_m k_l); a diagonal tile
+// u = m/16 holds both (m, l) and (l, m) of its block.  Wave gw (over the
+// parts of a head and slice) owns the linear tile u = gw (gw < D/16) and the
+// quadratic tiles of the channels m = gw (mod 4 * parts).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <stddef.h>
+
+#include "fm_common.h"
+#include "fm_mfma.h"
+
+namespace fm {
+namespace m32 {
+
+using mx::static_for;
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int C = 32;      // tokens per chunk
+constexpr int NW = 4;      // waves
+constexpr int NTH = NW * 64;
+constexpr int SL = 16;     // value columns per workgroup
+constexpr int TARGET_BLOCKS = 256;
+
+__device__ __forceinline__ f4 mma(float a, float b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <int D>
+struct Pat {
+    // workgroups sharing one (head, slice): D = 128 has too many feature
+    // tiles for one workgroup's accumulators, so four workgroups each take a
+    // quarter of them (and a quarter of the Y3 rows) and write partial F, G
+    static constexpr int NPART = D == 128 ? 4 : 1;
+    static constexpr int NU = D / 16;                  // 16-channel blocks
+    static constexpr int NGW = NW * NPART;             // waves over the parts
+    static constexpr int NCH = D / NGW;                // channels per wave
+    // block of channel m = gw + NGW c (gw < NGW, 16 a multiple of NGW)
+    static constexpr int u0(int c) { return NGW * c / 16; }
+    // first tile of channel c (its diagonal tile; u runs from u0(c) to NU-1)
+    static constexpr int first(int c)
+    {
+        int t = 1;
+        for (int cc = 0; cc < c; ++cc) t += NU - u0(cc);
+        return t;
+    }
+    static constexpr int NQ = first(NCH) - 1;          // quadratic tiles per wave
+    static constexpr int NT = 1 + NQ;                  // + the linear slot
+    static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
+    static constexpr int Y3R = 16 * NLB;               // Y3 rows per part
+    // Y3 tiles per part: one part keeps the blocks u <= u2 and mirrors them,
+    // several parts keep full rows
+    static constexpr int NY3 = NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
+    static constexpr int RS = D + 2;   // row stride of row-major tiles (floats)
+    static constexpr int TS = C + 2;   // row stride of transposed tiles
+    static_assert(16 % NGW == 0, "a wave's channels share their 16-blocks");
+};
+
+enum Mode { DELTA = 0, SCAN = 1, QUERY = 2, BOTH = 3 };
+
+// Standardises the D/8 channels [8 lanes per token] this thread holds
+// (Sec. 2.2, Eqs. 6-7: population std, no epsilon) and scales them.
+template <int D>
+__device__ __forceinline__ void standardise_part(float (&x)[D / 8], bool valid, float scale)
+{
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) s += x[i];
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    const float mu = s * (1.0f / D);
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) {
+        x[i] -= mu;
+        v = fmaf(x[i], x[i], v);
+    }
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    const float r = valid ? __builtin_amdgcn_rsqf(v * (1.0f / D)) * scale : 0.0f;
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) x[i] *= r;
+}
+
+// In-chunk block (row tile rt, key tile st <= rt) of a 32-token chunk: the
+// part that adds it to its partial F and G.
+template <int NPART>
+__host__ __device__ constexpr int inchunk_owner(int rt, int st)
+{
+    return (rt * (rt + 1) / 2 + st) % NPART;
+}
+
+// Segment sums -> exclusive prefix over segments (causal) or the total in
+// every segment (non-causal), in place; one thread per float of one item.
+static __global__ __launch_bounds__(256) void prefix_kernel(float *__restrict__ sums, int nseg,
+                                                     size_t floats, size_t stride, int causal)
+{
+    const size_t f = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (f >= floats) return;
+    float *p = sums + (size_t)blockIdx.y * nseg * stride + f;
+    // 16 segments' values loaded at a time (one memory latency per batch)
+    constexpr int BT = 16;
+    float run = 0.f;
+    if (!causal) {
+        for (int s0 = 0; s0 < nseg; s0 += BT) {
+            float d[BT];
+#pragma unroll
+            for (int b = 0; b < BT; ++b) d[b] = s0 + b < nseg ? p[(size_t)(s0 + b) * stride] : 0.f;
+#pragma unroll
+            for (int b = 0; b < BT; ++b) run += d[b];
+        }
+    }
+    for (int s0 = 0; s0 < nseg; s0 += BT) {
+        float d[BT];
+#pragma unroll
+        for (int b = 0; b < BT; ++b) d[b] = causal && s0 + b < nseg ? p[(size_t)(s0 + b) * stride] : 0.f;
+#pragma unroll
+        for (int b = 0; b < BT; ++b) {
+            if (s0 + b < nseg) p[(size_t)(s0 + b) * stride] = run;
+            if (causal) run += d[b];
+        }
+    }
+}
+
+inline int nseg_of(int items, int nch)
+{
+    int s = TARGET_BLOCKS / (items > 0 ? items : 1);
+    if (s < 1) s = 1;
+    if (s > nch) s = nch;
+    return s;
+}
+
+inline size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+}  // namespace m32
+}  // namespace fm

@@ -40,54 +40,10 @@
 
 #include "fm_common.h"
 #include "fm_internal.h"
-#include "fm_mfma.h"
+#include "fm_f32_mfma.h"
 
 namespace fm {
 namespace m32 {
-
-using mx::static_for;
-typedef float f4 __attribute__((ext_vector_type(4)));
-
-constexpr int C = 32;      // tokens per chunk
-constexpr int NW = 4;      // waves
-constexpr int NTH = NW * 64;
-constexpr int SL = 16;     // value columns per workgroup
-constexpr int TARGET_BLOCKS = 256;
-
-__device__ __forceinline__ f4 mma(float a, float b, f4 c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-template <int D>
-struct Pat {
-    // workgroups sharing one (head, slice): D = 128 has too many feature
-    // tiles for one workgroup's accumulators, so four workgroups each take a
-    // quarter of them (and a quarter of the Y3 rows) and write partial F, G
-    static constexpr int NPART = D == 128 ? 4 : 1;
-    static constexpr int NU = D / 16;                  // 16-channel blocks
-    static constexpr int NGW = NW * NPART;             // waves over the parts
-    static constexpr int NCH = D / NGW;                // channels per wave
-    // block of channel m = gw + NGW c (gw < NGW, 16 a multiple of NGW)
-    static constexpr int u0(int c) { return NGW * c / 16; }
-    // first tile of channel c (its diagonal tile; u runs from u0(c) to NU-1)
-    static constexpr int first(int c)
-    {
-        int t = 1;
-        for (int cc = 0; cc < c; ++cc) t += NU - u0(cc);
-        return t;
-    }
-    static constexpr int NQ = first(NCH) - 1;          // quadratic tiles per wave
-    static constexpr int NT = 1 + NQ;                  // + the linear slot
-    static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
-    static constexpr int Y3R = 16 * NLB;               // Y3 rows per part
-    // Y3 tiles per part: one part keeps the blocks u <= u2 and mirrors them,
-    // several parts keep full rows
-    static constexpr int NY3 = NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
-    static constexpr int RS = D + 2;   // row stride of row-major tiles (floats)
-    static constexpr int TS = C + 2;   // row stride of transposed tiles
-    static_assert(16 % NGW == 0, "a wave's channels share their 16-blocks");
-};
 
 template <int D>
 struct Smem {
@@ -113,53 +69,25 @@ struct Sum {
     static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
 };
 
-enum Mode { DELTA = 0, SCAN = 1, QUERY = 2, BOTH = 3 };
-
-// Standardises the D/8 channels [8 lanes per token] this thread holds
-// (Sec. 2.2, Eqs. 6-7: population std, no epsilon) and scales them.
-template <int D>
-__device__ __forceinline__ void standardise_part(float (&x)[D / 8], bool valid, float scale)
-{
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < D / 8; ++i) s += x[i];
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
-    s += __shfl_xor(s, 4);
-    const float mu = s * (1.0f / D);
-    float v = 0.f;
-#pragma unroll
-    for (int i = 0; i < D / 8; ++i) {
-        x[i] -= mu;
-        v = fmaf(x[i], x[i], v);
-    }
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 4);
-    const float r = valid ? __builtin_amdgcn_rsqf(v * (1.0f / D)) * scale : 0.0f;
-#pragma unroll
-    for (int i = 0; i < D / 8; ++i) x[i] *= r;
-}
-
-// In-chunk block (row tile rt, key tile st <= rt) of a 32-token chunk: the
-// part that adds it to its partial F and G.
-template <int NPART>
-__host__ __device__ constexpr int inchunk_owner(int rt, int st)
-{
-    return (rt * (rt + 1) / 2 + st) % NPART;
-}
-
 // One workgroup: (item = (head * NSL + slice) * NPART + part, segment).
 // With one part the outputs O = F / G and G go to out and g; with several,
 // each part's F and G (no division) go to fpw [head][part][N][D] and
 // gpw [head][part][N] for the finalize kernel.
-template <int D, typename T, bool CAUSAL, int MODE>
+//
+// DV (the backward's dv_n = sum_{i >= n} f(s_in) dO_i / G_i, Sec. 2.5): the
+// same scan over the reversed sequence (token n at N-1-n) with the roles of
+// queries and keys exchanged (q <- k, k <- q and the score scale on the
+// keys), values dO scaled by 1/G per token (vsc), and no denominator: the
+// numerator F is the output.
+template <int D, typename T, bool CAUSAL, int MODE, bool DV = false>
 __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                    const T *__restrict__ v, T *__restrict__ out,
                                                    float *__restrict__ g, float *__restrict__ sums,
                                                    float *__restrict__ fpw, float *__restrict__ gpw,
-                                                   int N, int nseg, float qs)
+                                                   const float *__restrict__ vsc, int N, int nseg,
+                                                   float qs, float ks)
 {
+    constexpr bool DEN = !DV;   // the denominator G (forward only)
     using PT = Pat<D>;
     constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
     constexpr int NPART = PT::NPART, NGW = PT::NGW, NLB = PT::NLB, Y3R = PT::Y3R;
@@ -178,6 +106,7 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     v += hb;
     out += hb;
     if (g) g += (size_t)head * N;
+    if (DV) vsc += (size_t)head * N;
     if (NPART > 1) {
         fpw += (size_t)(head * NPART + pp) * N * D;
         gpw += (size_t)(head * NPART + pp) * N;
@@ -250,19 +179,22 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     float pq[DP], pk[DP], pv[2];
     bool pvalid = false;
     auto prefetch = [&](int c) {
-        const int n = c * C + tg;
-        pvalid = n < N;
+        const int n0 = c * C + tg;
+        pvalid = n0 < N;
+        const int n = DV ? N - 1 - n0 : n0;   // the token's place in memory
 #pragma unroll
         for (int i = 0; i < DP; ++i) {
             pq[i] = pvalid ? io<T>::ld(q, (size_t)n * D + part * DP + i) : 0.f;
             pk[i] = pvalid ? io<T>::ld(k, (size_t)n * D + part * DP + i) : 0.f;
         }
+        const float vm = DV && pvalid ? vsc[n] : 1.0f;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) pv[i] = pvalid ? io<T>::ld(v, (size_t)n * D + SL * sl + 2 * part + i) : 0.f;
+        for (int i = 0; i < 2; ++i)
+            pv[i] = pvalid ? io<T>::ld(v, (size_t)n * D + SL * sl + 2 * part + i) * vm : 0.f;
     };
     auto stage = [&]() {
         standardise_part<D>(pq, pvalid, qs);
-        standardise_part<D>(pk, pvalid, 1.0f);
+        standardise_part<D>(pk, pvalid, ks);
 #pragma unroll
         for (int i = 0; i < DP; ++i) {
             const int ch = part * DP + i;
@@ -336,15 +268,17 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                                 for (int i = 0; i < 4; ++i)
                                     F = mma(sm.vrow[(16 * st + 4 * h + i) * SL + r16], Sc[i], F);
                             }
-                            gsum += __shfl_xor(gsum, 16);
-                            gsum += __shfl_xor(gsum, 32);
-                            if (h == 0) sm.gin[tok] = gsum;
+                            if (DEN) {
+                                gsum += __shfl_xor(gsum, 16);
+                                gsum += __shfl_xor(gsum, 32);
+                                if (h == 0) sm.gin[tok] = gsum;
+                            }
                         }
                     }
                     sm.fpart[w][rt][lane] = F;
                     // denominator: q^T (Y3 q + 2 y2) over l block lb (the last
                     // NLB waves; the first ones hold the linear and in-chunk work)
-                    if (lbl >= 0) {
+                    if (DEN && lbl >= 0) {
                         f4 Tq;
     #pragma unroll
                         for (int i = 0; i < 4; ++i) Tq[i] = sm.y2s[16 * lb + 4 * h + i];
@@ -366,12 +300,16 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                 {
                     const int n = n0 + tg;
                     if (n < N) {
+                        const int nm = DV ? N - 1 - n : n;   // the token's place in memory
                         const int rt = tg >> 4, t16 = tg & 15;
-                        float gsum = 0.f;
+                        float G = 1.f;
+                        if (DEN) {
+                            float gsum = 0.f;
     #pragma unroll
-                        for (int ww = 0; ww < NLB; ++ww) gsum += sm.gint[ww][tg];
-                        float G = (pp == 0 ? (M == QUERY ? (float)N : (float)n0) : 0.f) + 0.5f * gsum;
-                        if (M == SCAN && CAUSAL) G += sm.gin[tg];
+                            for (int ww = 0; ww < NLB; ++ww) gsum += sm.gint[ww][tg];
+                            G = (pp == 0 ? (M == QUERY ? (float)N : (float)n0) : 0.f) + 0.5f * gsum;
+                            if (M == SCAN && CAUSAL) G += sm.gin[tg];
+                        }
                         const float rG = 1.0f / G;
     #pragma unroll
                         for (int i = 0; i < 2; ++i) {
@@ -379,13 +317,15 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                             float F = pp == 0 ? sm.x1[j] : 0.f;
     #pragma unroll
                             for (int ww = 0; ww < NW; ++ww) F += sm.fpart[ww][rt][16 * (j >> 2) + t16][j & 3];
-                            if (NPART == 1) io<T>::st(out, (size_t)n * D + SL * sl + j, F * rG);
-                            else fpw[(size_t)n * D + SL * sl + j] = F;
+                            if (NPART == 1) io<T>::st(out, (size_t)nm * D + SL * sl + j, DEN ? F * rG : F);
+                            else fpw[(size_t)nm * D + SL * sl + j] = F;
                         }
-                        if (NPART == 1) {
-                            if (g && sl == 0 && part == 0) g[n] = G;
-                        } else if (sl == 0 && part == 0) {
-                            gpw[n] = G;
+                        if (DEN) {
+                            if (NPART == 1) {
+                                if (g && sl == 0 && part == 0) g[n] = G;
+                            } else if (sl == 0 && part == 0) {
+                                gpw[n] = G;
+                            }
                         }
                     }
                 }
@@ -421,17 +361,19 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                 });
     #pragma unroll
                 for (int kk = 0; kk < NYW; ++kk) {
-                    if (w + NW * kk >= PT::NY3) break;
+                    if (!DEN || w + NW * kk >= PT::NY3) break;
                     const float *a = sm.kT + (16 * yu[kk] + r16) * TS + h;
                     const float *b = sm.kT + (16 * yu2[kk] + r16) * TS + h;
     #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) Y[kk] = mma(a[4 * ks], b[4 * ks], Y[kk]);
                 }
                 if (tid < D) {
-                    float s = 0.f;
+                    if (DEN) {
+                        float s = 0.f;
     #pragma unroll 8
-                    for (int t = 0; t < C; ++t) s += sm.krow[t * RS + tid];
-                    y2reg += s;
+                        for (int t = 0; t < C; ++t) s += sm.krow[t * RS + tid];
+                        y2reg += s;
+                    }
                 } else if (tid < D + SL) {
                     float s = 0.f;
     #pragma unroll 8
@@ -442,7 +384,7 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                 // the prefix after this chunk, for the next chunk's outputs
     #pragma unroll
                 for (int kk = 0; kk < NYW; ++kk) {
-                    if (w + NW * kk >= PT::NY3) break;
+                    if (!DEN || w + NW * kk >= PT::NY3) break;
     #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int l = 16 * yu[kk] + 4 * h + i, m = 16 * yu2[kk] + r16;
@@ -479,49 +421,9 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     }
 }
 
-// Segment sums -> exclusive prefix over segments (causal) or the total in
-// every segment (non-causal), in place; one thread per float of one item.
-__global__ __launch_bounds__(256) void prefix_kernel(float *__restrict__ sums, int nseg,
-                                                     size_t floats, size_t stride, int causal)
-{
-    const size_t f = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (f >= floats) return;
-    float *p = sums + (size_t)blockIdx.y * nseg * stride + f;
-    // 16 segments' values loaded at a time (one memory latency per batch)
-    constexpr int BT = 16;
-    float run = 0.f;
-    if (!causal) {
-        for (int s0 = 0; s0 < nseg; s0 += BT) {
-            float d[BT];
-#pragma unroll
-            for (int b = 0; b < BT; ++b) d[b] = s0 + b < nseg ? p[(size_t)(s0 + b) * stride] : 0.f;
-#pragma unroll
-            for (int b = 0; b < BT; ++b) run += d[b];
-        }
-    }
-    for (int s0 = 0; s0 < nseg; s0 += BT) {
-        float d[BT];
-#pragma unroll
-        for (int b = 0; b < BT; ++b) d[b] = causal && s0 + b < nseg ? p[(size_t)(s0 + b) * stride] : 0.f;
-#pragma unroll
-        for (int b = 0; b < BT; ++b) {
-            if (s0 + b < nseg) p[(size_t)(s0 + b) * stride] = run;
-            if (causal) run += d[b];
-        }
-    }
-}
-
-int nseg_of(int items, int nch)
-{
-    int s = TARGET_BLOCKS / (items > 0 ? items : 1);
-    if (s < 1) s = 1;
-    if (s > nch) s = nch;
-    return s;
-}
-
 // Several parts: out = (sum of the parts' F) / (sum of their G), g = that
 // sum; 16 tokens per workgroup, 16 threads per token, D/16 columns each.
-template <int D, typename T>
+template <int D, typename T, bool DIV>
 __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ fpw,
                                                        const float *__restrict__ gpw,
                                                        T *__restrict__ out, float *__restrict__ g,
@@ -532,26 +434,24 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__
     const int head = blockIdx.x / nblk, n = (blockIdx.x % nblk) * 16 + (threadIdx.x >> 4);
     const int cg = threadIdx.x & 15;
     if (n >= N) return;
-    float G = 0.f;
+    float G = 0.f;   // (no division: the sum of F alone)
     f4 F[CPT / 4];
 #pragma unroll
     for (int i = 0; i < CPT / 4; ++i) F[i] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp) {
         const size_t row = (size_t)(head * NP + pp) * N + n;
-        G += gpw[row];
+        if (DIV) G += gpw[row];
         const f4 *src = (const f4 *)(fpw + row * D + CPT * cg);
 #pragma unroll
         for (int i = 0; i < CPT / 4; ++i) F[i] += src[i];
     }
-    const float rG = 1.0f / G;
+    const float rG = DIV ? 1.0f / G : 1.0f;
     const size_t o = ((size_t)head * N + n) * D + CPT * cg;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) io<T>::st(out, o + i, F[i / 4][i % 4] * rG);
-    if (g && cg == 0) g[(size_t)head * N + n] = G;
+    if (DIV && g && cg == 0) g[(size_t)head * N + n] = G;
 }
-
-inline size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // Workspace: segment sums (several segments), then the parts' F and G
 // (several parts).
@@ -572,15 +472,18 @@ struct Plan {
     size_t bytes() const { return sum_bytes + fp_bytes + gp_bytes; }
 };
 
-template <int D, typename T>
-hipError_t run(const void *q, const void *k, const void *v, void *out, float *g, int BH, int N,
-               int causal, float qs, void *ws, hipStream_t st)
+// The forward (DV = false: O = F / G and G) or the backward's dv (DV = true:
+// q <- k, k <- q, v <- dout scaled by vsc = 1/G, the score scale on the keys).
+template <int D, typename T, bool DV>
+hipError_t launch(const void *q, const void *k, const void *v, const float *vsc, void *out,
+                  float *g, int BH, int N, int causal, float qs, float ks, void *ws, hipStream_t st)
 {
     const Plan<D> pl(BH, N);
     const int items = pl.items, nseg = pl.nseg;
     if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)(items * nseg));
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v;
+    T *O = (T *)out;
     float *sums = nseg > 1 ? (float *)ws : nullptr;
     float *fpw = pl.fp_bytes ? (float *)((char *)ws + pl.sum_bytes) : nullptr;
     float *gpw = pl.gp_bytes ? (float *)((char *)ws + pl.sum_bytes + pl.fp_bytes) : nullptr;
@@ -588,31 +491,49 @@ hipError_t run(const void *q, const void *k, const void *v, void *out, float *g,
     const dim3 pgrid((unsigned)((Sum<D>::FLOATS + 255) / 256), items);
     if (causal) {
         if (nseg > 1) {
-            hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA>), grid, dim3(NTH), 0, st, Q, K, V,
-                               (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+            hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA, DV>), grid, dim3(NTH), 0, st, Q, K,
+                               V, O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
             hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
                                stride, 1);
         }
-        hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+        hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN, DV>), grid, dim3(NTH), 0, st, Q, K, V, O,
+                           g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
     } else if (nseg == 1) {
-        hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, nullptr, fpw, gpw, N, nseg, qs);
+        hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH, DV>), grid, dim3(NTH), 0, st, Q, K, V,
+                           O, g, nullptr, fpw, gpw, vsc, N, nseg, qs, ks);
     } else {
-        hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+        hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA, DV>), grid, dim3(NTH), 0, st, Q, K, V,
+                           O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
         hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
                            stride, 0);
-        hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY>), grid, dim3(NTH), 0, st, Q, K, V,
-                           (T *)out, g, sums, fpw, gpw, N, nseg, qs);
+        hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY, DV>), grid, dim3(NTH), 0, st, Q, K, V,
+                           O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
     }
     if constexpr (Pat<D>::NPART > 1) {
         const int nblk = (N + 15) / 16;
         if ((long long)BH * nblk > INT_MAX) return hipErrorInvalidConfiguration;
-        hipLaunchKernelGGL((finalize_kernel<D, T>), dim3((unsigned)(BH * nblk)), dim3(256), 0, st,
-                           fpw, gpw, (T *)out, g, N, nblk);
+        hipLaunchKernelGGL((finalize_kernel<D, T, !DV>), dim3((unsigned)(BH * nblk)), dim3(256), 0,
+                           st, fpw, gpw, O, g, N, nblk);
     }
     return hipGetLastError();
+}
+
+template <bool DV>
+hipError_t launch_d(const void *q, const void *k, const void *v, const float *vsc, void *out,
+                    float *g, int BH, int N, int D, int causal, int is_bf16, float qs, float ks,
+                    void *ws, hipStream_t st)
+{
+    if (is_bf16) {
+        if (D == 16) return launch<16, bf16_t, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+        if (D == 32) return launch<32, bf16_t, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+        if (D == 128) return launch<128, bf16_t, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+        return hipErrorInvalidValue;
+    }
+    if (D == 16) return launch<16, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    if (D == 32) return launch<32, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    if (D == 64) return launch<64, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    if (D == 128) return launch<128, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace m32
@@ -637,18 +558,16 @@ size_t f32mfma_fwd_workspace(int BH, int N, int D)
 hipError_t f32mfma_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
                        int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st)
 {
-    using namespace m32;
-    if (is_bf16) {
-        if (D == 16) return run<16, bf16_t>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-        if (D == 32) return run<32, bf16_t>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-        if (D == 128) return run<128, bf16_t>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-        return hipErrorInvalidValue;
-    }
-    if (D == 16) return run<16, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-    if (D == 32) return run<32, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-    if (D == 64) return run<64, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-    if (D == 128) return run<128, float>(q, k, v, out, g, BH, N, causal, qs, ws, st);
-    return hipErrorInvalidValue;
+    return m32::launch_d<false>(q, k, v, nullptr, out, g, BH, N, D, causal, is_bf16, qs, 1.0f, ws,
+                                st);
+}
+
+hipError_t f32mfma_dv(const void *q, const void *k, const void *dout, const float *rg, void *dv,
+                      int BH, int N, int D, int causal, int is_bf16, float qs, void *ws,
+                      hipStream_t st)
+{
+    return m32::launch_d<true>(k, q, dout, rg, dv, nullptr, BH, N, D, causal, is_bf16, 1.0f, qs,
+                               ws, st);
 }
 
 }  // namespace fm

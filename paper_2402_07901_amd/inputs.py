@@ -73,7 +73,7 @@ WORKLOADS = {
     "fwdbwd_noncausal_bf16": Workload("fwdbwd_noncausal_bf16", 8, 12, 4096, 64, 2, False, "bf16",
                                       5, with_dout=True),
     # head dimension 128 (the Llama-2 head size of Sec. 3.1's remark), causal,
-    # p = 2: P = 8385 features, served by the float32 VALU kernels
+    # p = 2: P = 8385 features, served by the float32 MFMA kernels
     "d128_causal_bf16": Workload("d128_causal_bf16", 1, 8, 4096, 128, 2, True, "bf16", 6,
                                  with_dout=True),
 }

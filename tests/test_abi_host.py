@@ -197,7 +197,8 @@ def test_dropout_mask_words():
 
 
 def test_dropout_workspace():
-    """Backward: the float32 kernels' p = 2 backward workspace; causal
+    """Backward: the generic float32 backward's (c, dq^, dk^ and dv in fp32,
+    plus segment states when few heads are split into segments); causal
     forward: the non-causal one (256-byte aligned, the generic kernels' p = 2
     segment states) plus the masked in-chunk weights, 16 x 16 floats per
     chunk of 16 tokens."""
@@ -205,7 +206,10 @@ def test_dropout_workspace():
     for B, H, N, D in ((1, 1, 700, 16), (4, 16, 8192, 64), (1, 8, 4096, 128), (2, 3, 33, 32)):
         for causal in (0, 1):
             a = L.fastmax_dropout_workspace_bytes(B, H, N, D, causal, fm.BF16, 1)
-            assert a == L.fastmax_workspace_bytes(B, H, N, D, 2, causal, fm.F32, 1), (B, H, N, D)
+            base = 4 * B * H * N * (1 + 3 * D)
+            assert a >= base, (B, H, N, D)
+            if (B, H) == (4, 16):   # 832 (head, slice) items: no segments
+                assert a == base
         a_nc = L.fastmax_dropout_workspace_bytes(B, H, N, D, 0, fm.BF16, 0)
         a_c = L.fastmax_dropout_workspace_bytes(B, H, N, D, 1, fm.BF16, 0)
         assert a_c == (a_nc + 255) // 256 * 256 + B * H * ((N + 15) // 16) * 16 * 16 * 4, (B, H, N, D)
