@@ -33,8 +33,10 @@
 // T[l][t] = sum_c Q[m,l][c] UC_tc in the layout (token r16, feature 4h + i)
 // of the per-wave output rows.  A diagonal tile (both orders of its pairs)
 // adds Z_tm T[l] to out_t[l]; an off-diagonal tile (m's block below l's)
-// also adds sum_l Z_tl T[l] to out_t[m].  The waves' rows meet in LDS
-// (LDS float atomics), and each chunk's rows are added to the float32
+// also adds sum_l Z_tl T[l] to out_t[m].  Each wave folds all its terms for
+// one 16-feature block into registers and stores the block once into its own
+// LDS region (LDS float atomics, measured, cost more than the MFMAs); the
+// chunk's rows, summed over the four regions, are added to the float32
 // gradient with global float atomics (the column slices and feature parts of
 // a head add into the same rows).
 #include <hip/hip_runtime.h>
@@ -59,7 +61,7 @@ struct alignas(16) GSmem {
     float zt[C];                   // contraction scalars z
     float y3[16 * Pat<D>::RS];     // the item's row block of Y3w (before the chunk)
     float y2[16];                  // its entries of y2w
-    float ob[C * Pat<D>::RS];      // the chunk's output rows, summed over the waves
+    float ob[NW][D * (C + 4)];     // each wave's outputs of the chunk [feature][token]
 };
 
 // Segment summary: [wave][tile][lane] f4 state, the Y3w row block [16][D],
@@ -86,6 +88,9 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
     constexpr int NPART = PT::NPART, NGW = PT::NGW;
     constexpr int NSL = D / SL;
     constexpr int ZS = D + 4;   // row stride of Z
+    // feature stride of the output blocks: the lanes (token r16, features
+    // 4h + i) of one LDS store fall in 64 distinct banks
+    constexpr int OS = C + 4;
     __shared__ GSmem<D> sm;
 
     const int item = blockIdx.x / nseg, seg = blockIdx.x % nseg;
@@ -125,7 +130,6 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
             y2reg = loaded ? sy[16 * D + tid] : 0.f;
             sm.y2[tid] = y2reg;
         }
-        for (int e = tid; e < C * RS; e += NTH) sm.ob[e] = 0.f;
     }
     // Y3w tiles (ylb, u2), u2 = w + 4 kk
     constexpr int NYW = (NU + NW - 1) / NW;
@@ -202,26 +206,68 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
             for (int rt = 0; rt < C / 16; ++rt) {
                 const int tok = 16 * rt + r16;
                 const float *zr = sm.zrow + tok * ZS;
-                float *orow = sm.ob + tok * RS;
+                // this wave's outputs of the row tile, every (feature, token)
+                // written once: feature f of token tok at ocol[f * OS]
+                float *ocol = sm.ob[w] + tok;
                 float ub[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) ub[i] = sm.uc[tok * SL + 4 * h + i];
                 // linear tile: out[l] += sum_c UC_c L[l][c], l in block gw
+                f4 Tl = {0.f, 0.f, 0.f, 0.f};
                 if (gw < NU) {
-                    f4 Tl = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int i = 0; i < 4; ++i) Tl = mma(S[0][i], ub[i], Tl);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * gw + 4 * h + i, Tl[i]);
                 }
-                // quadratic tiles, by output block u: tile (m, u) of channel
-                // m = gw + NGW cc adds Z_m T[l] to out[l], l in block u, and (off
-                // the diagonal) sum_l Z_l T[l] to out[m]
+                // in-chunk pairs: key tile st <= rt on wave b of the owning part;
+                // the weights here, their products with X by output block below
+                float Wt[2][4] = {};
+                bool ich[2] = {false, false};
+                if constexpr (M == SCAN && CAUSAL) {
+#pragma unroll
+                    for (int st = 0; st < 2; ++st) {
+                        ich[st] = st <= rt && inchunk_owner<NPART>(rt, st) == pp &&
+                                  w == rt * (rt + 1) / 2 + st;
+                        if (!ich[st]) continue;
+                        // S^T and P^T: lane (token tok, keys 16 st + 4h + i)
+                        f4 Sc = {0.f, 0.f, 0.f, 0.f}, Pc = {0.f, 0.f, 0.f, 0.f};
+                        const float *xr = sm.xrow + (16 * st + r16) * RS;
+#pragma unroll
+                        for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[4 * kk + h], zr[4 * kk + h], Sc);
+                        const float *vr = sm.vs + (16 * st + r16) * SL;
+#pragma unroll
+                        for (int kk = 0; kk < 4; ++kk)
+                            Pc = mma(vr[4 * kk + h], sm.uc[tok * SL + 4 * kk + h], Pc);
+                        const float zs = scal ? sm.zt[tok] : 0.f;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            float wgt = (1.0f + Sc[i]) * fmaf(zs, sm.wt[16 * st + 4 * h + i], Pc[i]);
+                            if (st == rt && 4 * h + i > r16) wgt = 0.0f;
+                            Wt[st][i] = wgt;
+                        }
+                    }
+                }
+                // the item's Y3w block: out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
+                f4 Tq = {0.f, 0.f, 0.f, 0.f};
+                const bool yw = ylb >= 0 && w == NW - 1;
+                if (yw) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
+                    const float *yr = sm.y3 + r16 * RS;
+#pragma unroll
+                    for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], zr[4 * kk + h], Tq);
+                    const float zs = sm.zt[tok];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) Tq[i] *= zs;
+                }
+                // quadratic tiles by output block u, from the last block down: tile
+                // (m, u) of channel m = gw + NGW cc adds Z_m T[l] to out[l], l in
+                // block u, and (off the diagonal) sum_l Z_l T[l] to out[m], which is
+                // complete when the loop reaches m's own block u0
                 float dmv[NCH];
 #pragma unroll
                 for (int cc = 0; cc < NCH; ++cc) dmv[cc] = 0.f;
-                static_for<0, NU>([&](auto ui) {
-                    constexpr int u = decltype(ui)::value;
+                static_for<0, NU>([&](auto ri) {
+                    constexpr int u = NU - 1 - decltype(ri)::value;
                     const f4 zlu = *(const f4 *)(zr + 16 * u + 4 * h);
                     f4 a4 = {0.f, 0.f, 0.f, 0.f};
                     static_for<0, NCH>([&](auto ci) {
@@ -240,73 +286,39 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
                                 for (int i = 0; i < 4; ++i) dmv[cc] = fmaf(zlu[i], Tt[i], dmv[cc]);
                             }
                         }
-                    });
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * u + 4 * h + i, a4[i]);
-                });
-                static_for<0, NCH>([&](auto ci) {
-                    constexpr int cc = decltype(ci)::value;
-                    if constexpr (PT::u0(cc) + 1 < NU) {
-                        float dm = dmv[cc];
-                        dm += __shfl_xor(dm, 16);
-                        dm += __shfl_xor(dm, 32);
-                        if (h == 0) atomicAdd(orow + gw + NGW * cc, dm);
-                    }
-                });
-                if constexpr (M == SCAN && CAUSAL) {
-                    // in-chunk pairs: key tile st <= rt, on wave b of the owning part
-#pragma unroll
-                    for (int st = 0; st <= rt; ++st) {
-                        const int b = rt * (rt + 1) / 2 + st;
-                        if (inchunk_owner<NPART>(rt, st) != pp || w != b) continue;
-                        // S^T and P^T: lane (token tok, keys 16 st + 4h + i)
-                        f4 Sc = {0.f, 0.f, 0.f, 0.f}, Pc = {0.f, 0.f, 0.f, 0.f};
-                        const float *xr = sm.xrow + (16 * st + r16) * RS;
-#pragma unroll
-                        for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[4 * kk + h], zr[4 * kk + h], Sc);
-                        const float *vr = sm.vs + (16 * st + r16) * SL;
-#pragma unroll
-                        for (int kk = 0; kk < 4; ++kk)
-                            Pc = mma(vr[4 * kk + h], sm.uc[tok * SL + 4 * kk + h], Pc);
-                        const float zs = scal ? sm.zt[tok] : 0.f;
-                        float Wt[4];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            float wgt = (1.0f + Sc[i]) * fmaf(zs, sm.wt[16 * st + 4 * h + i], Pc[i]);
-                            if (st == rt && 4 * h + i > r16) wgt = 0.0f;
-                            Wt[i] = wgt;
-                        }
-                        // out[l] += sum_r W[t][r] X_r[l]
-#pragma unroll
-                        for (int u = 0; u < NU; ++u) {
-                            f4 ic = {0.f, 0.f, 0.f, 0.f};
+                        if constexpr (u == u0 && u0 + 1 < NU) {
+                            float dm = dmv[cc];
+                            dm += __shfl_xor(dm, 16);
+                            dm += __shfl_xor(dm, 32);
+                            const int ml = (gw + NGW * cc) & 15;
 #pragma unroll
                             for (int i = 0; i < 4; ++i)
-                                ic = mma(sm.xrow[(16 * st + 4 * h + i) * RS + 16 * u + r16], Wt[i], ic);
+                                if (h == (ml >> 2) && i == (ml & 3)) a4[i] += dm;
+                        }
+                    });
+                    if (gw == u) a4 += Tl;
+                    if (yw && ylb == u) a4 += Tq;
+                    if constexpr (M == SCAN && CAUSAL) {
 #pragma unroll
-                            for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * u + 4 * h + i, ic[i]);
+                        for (int st = 0; st < 2; ++st) {
+                            if (!ich[st]) continue;
+                            // out[l] += sum_r W[t][r] X_r[l]
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                a4 = mma(sm.xrow[(16 * st + 4 * h + i) * RS + 16 * u + r16], Wt[st][i], a4);
                         }
                     }
-                }
-                // the item's Y3w block: out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
-                if (ylb >= 0 && w == NW - 1) {
-                    f4 Tq;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
-                    const float *yr = sm.y3 + r16 * RS;
-#pragma unroll
-                    for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], zr[4 * kk + h], Tq);
-                    const float zs = sm.zt[tok];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) atomicAdd(orow + 16 * ylb + 4 * h + i, zs * Tq[i]);
-                }
+                    for (int i = 0; i < 4; ++i) ocol[(16 * u + 4 * h + i) * OS] = a4[i];
+                });
             }
             __syncthreads();
-            // the chunk's rows into the float32 gradient; clear them for the next chunk
+            // the chunk's rows (summed over the waves) into the float32 gradient
             for (int e = tid; e < C * D; e += NTH) {
                 const int t = e / D, d = e % D, n = n0 + t;
-                const float val = sm.ob[t * RS + d];
-                sm.ob[t * RS + d] = 0.f;
+                float val = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) val += sm.ob[ww][d * OS + t];
                 if (n < N) atomicAdd(outh + (size_t)(REV ? N - 1 - n : n) * D + d, val);
             }
         }
