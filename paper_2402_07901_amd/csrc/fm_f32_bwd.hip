@@ -50,6 +50,11 @@
 namespace fm {
 namespace m32 {
 
+// Tokens of the per-wave output blocks: the whole chunk where the waves'
+// blocks fit 64 KB of LDS, else one 16-token row tile at a time.
+template <int D>
+constexpr int out_tokens() { return Pat<D>::NW * D * (C + 4) * 4 <= 65536 ? C : 16; }
+
 template <int D>
 struct alignas(16) GSmem {
     float xrow[C * Pat<D>::RS];    // state keys X [token][channel]
@@ -61,14 +66,14 @@ struct alignas(16) GSmem {
     float zt[C];                   // contraction scalars z
     float y3[16 * Pat<D>::RS];     // the item's row block of Y3w (before the chunk)
     float y2[16];                  // its entries of y2w
-    float ob[NW][D * (C + 4)];     // each wave's outputs of the chunk [feature][token]
+    float ob[Pat<D>::NW][D * (out_tokens<D>() + 4)];   // each wave's outputs [feature][token]
 };
 
 // Segment summary: [wave][tile][lane] f4 state, the Y3w row block [16][D],
 // y2w [16].
 template <int D>
 struct GSum {
-    static constexpr size_t STATE = (size_t)NW * Pat<D>::NT * 64 * 4;
+    static constexpr size_t STATE = (size_t)Pat<D>::NW * Pat<D>::NT * 64 * 4;
     static constexpr size_t FLOATS = STATE + 16 * D + 16;
     static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
 };
@@ -77,7 +82,7 @@ struct GSum {
 // item (slice, part) with index sl * NPART + part = b < D/16 also keeps row
 // block b of Y3w and y2w; slice 0 adds the z_t w_r term of the in-chunk pairs.
 template <int D, typename T, bool CAUSAL, int MODE, bool REV>
-__global__ __launch_bounds__(NTH) void grad_kernel(
+__global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
     const T *__restrict__ X, const T *__restrict__ Z, const T *__restrict__ VS,
     const T *__restrict__ UC, const float *__restrict__ vsm, const float *__restrict__ ucm,
     const float *__restrict__ wv, const float *__restrict__ zv, float *__restrict__ outh,
@@ -86,11 +91,12 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
     using PT = Pat<D>;
     constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
     constexpr int NPART = PT::NPART, NGW = PT::NGW;
+    constexpr int NW = PT::NW, NTH = PT::NTH, LPT = PT::LPT, VPL = PT::VPL;
     constexpr int NSL = D / SL;
     constexpr int ZS = D + 4;   // row stride of Z
-    // feature stride of the output blocks: the lanes (token r16, features
-    // 4h + i) of one LDS store fall in 64 distinct banks
-    constexpr int OS = C + 4;
+    // output block: FT tokens; its feature stride puts the lanes (token r16,
+    // features 4h + i) of one LDS store in 64 distinct banks
+    constexpr int FT = out_tokens<D>(), OS = FT + 4;
     __shared__ GSmem<D> sm;
 
     const int item = blockIdx.x / nseg, seg = blockIdx.x % nseg;
@@ -148,9 +154,9 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
     }
 
     // ---- staging: token tg = tid / 8, channels 8-way split, 2 columns ---
-    const int tg = tid >> 3, part = tid & 7;
-    constexpr int DP = D / 8;
-    float px[DP], pz[DP], pvs[2], puc[2], pw = 0.f, pzs = 0.f;
+    const int tg = tid / LPT, part = tid % LPT;
+    constexpr int DP = PT::DP;
+    float px[DP], pz[DP], pvs[VPL], puc[VPL], pw = 0.f, pzs = 0.f;
     bool pvalid = false;
     auto prefetch = [&](int c) {
         const int n0 = c * C + tg;
@@ -163,8 +169,8 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
         }
         const float vm = vsm && pvalid ? vsm[n] : 1.0f, um = ucm && pvalid ? ucm[n] : 1.0f;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const size_t e = (size_t)n * D + SL * sl + 2 * part + i;
+        for (int i = 0; i < VPL; ++i) {
+            const size_t e = (size_t)n * D + SL * sl + VPL * part + i;
             pvs[i] = pvalid ? io<T>::ld(VS, e) * vm : 0.f;
             puc[i] = pvalid ? io<T>::ld(UC, e) * um : 0.f;
         }
@@ -182,9 +188,9 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
             sm.zrow[tg * ZS + ch] = pz[i];
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            sm.vs[tg * SL + 2 * part + i] = pvs[i];
-            sm.uc[tg * SL + 2 * part + i] = puc[i];
+        for (int i = 0; i < VPL; ++i) {
+            sm.vs[tg * SL + VPL * part + i] = pvs[i];
+            sm.uc[tg * SL + VPL * part + i] = puc[i];
         }
         if (part == 0) {
             sm.wt[tg] = pw;
@@ -194,9 +200,21 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
 
     // one chunk in mode M (DELTA: state update only; QUERY: outputs only;
     // SCAN: outputs, then the update unless the segment ends here)
-    auto chunk = [&](auto mc, int c) {
+    auto chunk = [&](auto mc, auto ghc, int c) {
         constexpr int M = decltype(mc)::value;
+        constexpr int GH = decltype(ghc)::value;   // wave class (channel blocks)
         const int n0 = c * C;
+        // the waves' output blocks of tokens t0 .. t0 + FT - 1 (summed) into
+        // the float32 gradient
+        auto flush = [&](int t0) {
+            for (int e = tid; e < FT * D; e += NTH) {
+                const int t = e / D, d = e % D, n = n0 + t0 + t;
+                float val = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) val += sm.ob[ww][d * OS + t];
+                if (n < N) atomicAdd(outh + (size_t)(REV ? N - 1 - n : n) * D + d, val);
+            }
+        };
         stage();
         if (c + 1 < cend) prefetch(c + 1);
         __syncthreads();
@@ -208,7 +226,7 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
                 const float *zr = sm.zrow + tok * ZS;
                 // this wave's outputs of the row tile, every (feature, token)
                 // written once: feature f of token tok at ocol[f * OS]
-                float *ocol = sm.ob[w] + tok;
+                float *ocol = sm.ob[w] + (FT == C ? tok : r16);
                 float ub[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) ub[i] = sm.uc[tok * SL + 4 * h + i];
@@ -272,9 +290,9 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
                     f4 a4 = {0.f, 0.f, 0.f, 0.f};
                     static_for<0, NCH>([&](auto ci) {
                         constexpr int cc = decltype(ci)::value;
-                        constexpr int u0 = PT::u0(cc);
+                        constexpr int u0 = PT::u0(cc, GH);
                         if constexpr (u >= u0) {
-                            constexpr int t = PT::first(cc) + u - u0;
+                            constexpr int t = PT::first(cc, GH) + u - u0;
                             const float zm = zr[gw + NGW * cc];
                             f4 Tt = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -311,15 +329,15 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
 #pragma unroll
                     for (int i = 0; i < 4; ++i) ocol[(16 * u + 4 * h + i) * OS] = a4[i];
                 });
+                if constexpr (FT == 16) {
+                    __syncthreads();
+                    flush(16 * rt);
+                    __syncthreads();   // the blocks are written again by the next row tile
+                }
             }
-            __syncthreads();
-            // the chunk's rows (summed over the waves) into the float32 gradient
-            for (int e = tid; e < C * D; e += NTH) {
-                const int t = e / D, d = e % D, n = n0 + t;
-                float val = 0.f;
-#pragma unroll
-                for (int ww = 0; ww < NW; ++ww) val += sm.ob[ww][d * OS + t];
-                if (n < N) atomicAdd(outh + (size_t)(REV ? N - 1 - n : n) * D + d, val);
+            if constexpr (FT == C) {
+                __syncthreads();
+                flush(0);
             }
         }
         if constexpr (M != QUERY) {
@@ -339,14 +357,14 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
             }
             static_for<0, NCH>([&](auto ci) {
                 constexpr int cc = decltype(ci)::value;
-                constexpr int u0 = PT::u0(cc);
+                constexpr int u0 = PT::u0(cc, GH);
                 const float *xm = sm.xT + (gw + NGW * cc) * TS + h;
                 float Bm[C / 4];
 #pragma unroll
                 for (int ks = 0; ks < C / 4; ++ks) Bm[ks] = xm[4 * ks] * Vb[ks];
                 static_for<u0, NU>([&](auto ui) {
                     constexpr int u = decltype(ui)::value;
-                    constexpr int t = PT::first(cc) + u - u0;
+                    constexpr int t = PT::first(cc, GH) + u - u0;
 #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) S[t] = mma(Bm[ks], Ak[u][ks], S[t]);
                 });
@@ -385,16 +403,18 @@ __global__ __launch_bounds__(NTH) void grad_kernel(
         }
         __syncthreads();
     };
-    if constexpr (MODE == BOTH) {
-        // non-causal, one segment: the totals first, then every output row
-        prefetch(cbeg);
-        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, DELTA>{}, c);
-        prefetch(cbeg);
-        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, QUERY>{}, c);
-    } else {
-        prefetch(cbeg);
-        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, MODE>{}, c);
-    }
+    with_wave_class<D>(gw, [&](auto ghc) {
+        if constexpr (MODE == BOTH) {
+            // non-causal, one segment: the totals first, then every output row
+            prefetch(cbeg);
+            for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, DELTA>{}, ghc, c);
+            prefetch(cbeg);
+            for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, QUERY>{}, ghc, c);
+        } else {
+            prefetch(cbeg);
+            for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, MODE>{}, ghc, c);
+        }
+    });
 
     if constexpr (MODE == DELTA) {
 #pragma unroll
@@ -529,22 +549,22 @@ hipError_t grad_launch(const BwdPlan<D> &pl, const T *X, const T *Z, const T *VS
     const dim3 pgrid((unsigned)((GSum<D>::FLOATS + 255) / 256), items);
     if (causal) {
         if (nseg > 1) {
-            hipLaunchKernelGGL((grad_kernel<D, T, true, DELTA, REV>), grid, dim3(NTH), 0, st, X, Z,
+            hipLaunchKernelGGL((grad_kernel<D, T, true, DELTA, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
                                VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
             hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg,
                                GSum<D>::FLOATS, stride, 1);
         }
-        hipLaunchKernelGGL((grad_kernel<D, T, true, SCAN, REV>), grid, dim3(NTH), 0, st, X, Z, VS,
+        hipLaunchKernelGGL((grad_kernel<D, T, true, SCAN, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z, VS,
                            UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
     } else if (nseg == 1) {
-        hipLaunchKernelGGL((grad_kernel<D, T, false, BOTH, REV>), grid, dim3(NTH), 0, st, X, Z,
+        hipLaunchKernelGGL((grad_kernel<D, T, false, BOTH, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
                            VS, UC, vsm, ucm, wv, zv, outh, nullptr, N, nseg, xs, zsc);
     } else {
-        hipLaunchKernelGGL((grad_kernel<D, T, false, DELTA, REV>), grid, dim3(NTH), 0, st, X, Z,
+        hipLaunchKernelGGL((grad_kernel<D, T, false, DELTA, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
                            VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
         hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, GSum<D>::FLOATS,
                            stride, 0);
-        hipLaunchKernelGGL((grad_kernel<D, T, false, QUERY, REV>), grid, dim3(NTH), 0, st, X, Z,
+        hipLaunchKernelGGL((grad_kernel<D, T, false, QUERY, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
                            VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
     }
     return hipGetLastError();

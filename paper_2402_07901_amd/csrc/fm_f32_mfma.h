@@ -12,12 +12,14 @@
 // quadratic tiles (m, u) for u >= m/16 (features k_m k_l); a diagonal tile
 // u = m/16 holds both (m, l) and (l, m) of its block.  Wave gw (over the
 // parts of a head and slice) owns the linear tile u = gw (gw < D/16) and the
-// quadratic tiles of the channels m = gw (mod 4 * parts).
+// quadratic tiles of the channels m = gw (mod waves * parts).
 #pragma once
 
 #include <hip/hip_runtime.h>
 
 #include <stddef.h>
+
+#include <type_traits>
 
 #include "fm_common.h"
 #include "fm_mfma.h"
@@ -29,8 +31,6 @@ using mx::static_for;
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int C = 32;      // tokens per chunk
-constexpr int NW = 4;      // waves
-constexpr int NTH = NW * 64;
 constexpr int SL = 16;     // value columns per workgroup
 constexpr int TARGET_BLOCKS = 256;
 
@@ -41,23 +41,33 @@ __device__ __forceinline__ f4 mma(float a, float b, f4 c)
 
 template <int D>
 struct Pat {
-    // workgroups sharing one (head, slice): D = 128 has too many feature
-    // tiles for one workgroup's accumulators, so four workgroups each take a
-    // quarter of them (and a quarter of the Y3 rows) and write partial F, G
+    // Workgroups sharing one (head, slice) and waves per workgroup.  D = 128
+    // has too many feature tiles for one workgroup's accumulators: four
+    // workgroups each take a quarter of them (and a quarter of the Y3 rows)
+    // and write partial F, G; their eight waves (two per SIMD) keep about 84
+    // state registers each, so a second wave hides each wave's stalls.
     static constexpr int NPART = D == 128 ? 4 : 1;
+    static constexpr int NW = D == 128 ? 8 : 4;
+    static constexpr int NTH = NW * 64;
+    static constexpr int LPT = NTH / C;                // staging lanes per token
+    static constexpr int DP = D / LPT;                 // staged channels per lane
+    static constexpr int VPL = SL / LPT;               // staged value columns per lane
     static constexpr int NU = D / 16;                  // 16-channel blocks
     static constexpr int NGW = NW * NPART;             // waves over the parts
     static constexpr int NCH = D / NGW;                // channels per wave
-    // block of channel m = gw + NGW c (gw < NGW, 16 a multiple of NGW)
-    static constexpr int u0(int c) { return NGW * c / 16; }
-    // first tile of channel c (its diagonal tile; u runs from u0(c) to NU-1)
-    static constexpr int first(int c)
+    // Block of channel m = gw + NGW c (gw < NGW): NGW c / 16 while 16 is a
+    // multiple of NGW; beyond 16 waves, NGW/16 c + gw/16, where the wave
+    // class gw/16 is the same for every wave of a workgroup.
+    static constexpr int NH = NGW > 16 ? NGW / 16 : 1;  // wave classes
+    static constexpr int u0(int c, int gh) { return NGW >= 16 ? (NGW / 16) * c + gh : NGW * c / 16; }
+    // first tile of channel c (its diagonal tile; u runs from u0 to NU-1)
+    static constexpr int first(int c, int gh)
     {
         int t = 1;
-        for (int cc = 0; cc < c; ++cc) t += NU - u0(cc);
+        for (int cc = 0; cc < c; ++cc) t += NU - u0(cc, gh);
         return t;
     }
-    static constexpr int NQ = first(NCH) - 1;          // quadratic tiles per wave
+    static constexpr int NQ = first(NCH, 0) - 1;       // quadratic tiles per wave (class 0: most)
     static constexpr int NT = 1 + NQ;                  // + the linear slot
     static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
     static constexpr int Y3R = 16 * NLB;               // Y3 rows per part
@@ -66,35 +76,47 @@ struct Pat {
     static constexpr int NY3 = NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
     static constexpr int RS = D + 2;   // row stride of row-major tiles (floats)
     static constexpr int TS = C + 2;   // row stride of transposed tiles
-    static_assert(16 % NGW == 0, "a wave's channels share their 16-blocks");
+    static_assert(NGW <= 16 ? 16 % NGW == 0 : NGW % 16 == 0 && NH <= 2, "channel blocks");
+    static_assert(LPT * C == NTH && DP * LPT == D && VPL * LPT == SL, "staging");
 };
+
+// Runs f(integral_constant<int, gh>) for the workgroup's wave class gh.
+template <int D, typename F>
+__device__ __forceinline__ void with_wave_class(int gw, F &&f)
+{
+    if constexpr (Pat<D>::NH == 1) {
+        f(std::integral_constant<int, 0>{});
+    } else {
+        if (gw < 16) f(std::integral_constant<int, 0>{});
+        else f(std::integral_constant<int, 1>{});
+    }
+}
 
 enum Mode { DELTA = 0, SCAN = 1, QUERY = 2, BOTH = 3 };
 
-// Standardises the D/8 channels [8 lanes per token] this thread holds
-// (Sec. 2.2, Eqs. 6-7: population std, no epsilon) and scales them.
+// Standardises the channels this thread holds of its token (Sec. 2.2, Eqs.
+// 6-7: population std, no epsilon; LPT lanes per token) and scales them.
 template <int D>
-__device__ __forceinline__ void standardise_part(float (&x)[D / 8], bool valid, float scale)
+__device__ __forceinline__ void standardise_part(float (&x)[Pat<D>::DP], bool valid, float scale)
 {
+    constexpr int DP = Pat<D>::DP, LPT = Pat<D>::LPT;
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < D / 8; ++i) s += x[i];
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
-    s += __shfl_xor(s, 4);
+    for (int i = 0; i < DP; ++i) s += x[i];
+#pragma unroll
+    for (int o = 1; o < LPT; o <<= 1) s += __shfl_xor(s, o);
     const float mu = s * (1.0f / D);
     float v = 0.f;
 #pragma unroll
-    for (int i = 0; i < D / 8; ++i) {
+    for (int i = 0; i < DP; ++i) {
         x[i] -= mu;
         v = fmaf(x[i], x[i], v);
     }
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 4);
+#pragma unroll
+    for (int o = 1; o < LPT; o <<= 1) v += __shfl_xor(v, o);
     const float r = valid ? __builtin_amdgcn_rsqf(v * (1.0f / D)) * scale : 0.0f;
 #pragma unroll
-    for (int i = 0; i < D / 8; ++i) x[i] *= r;
+    for (int i = 0; i < DP; ++i) x[i] *= r;
 }
 
 // In-chunk block (row tile rt, key tile st <= rt) of a 32-token chunk: the

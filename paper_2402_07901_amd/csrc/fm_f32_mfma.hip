@@ -54,7 +54,7 @@ struct Smem {
     float y3[Pat<D>::Y3R * Pat<D>::RS];   // Y3 prefix rows of the part (before the chunk)
     float y2s[D];                   // 2 y2 prefix
     float x1[SL];                   // x1 prefix
-    f4 fpart[NW][C / 16][64];       // partial F^T of the waves
+    f4 fpart[Pat<D>::NW][C / 16][64];   // partial F^T of the waves
     float gin[C];                   // in-chunk row sums
     float gint[Pat<D>::NLB][C];     // partial q^T(Y3 q^ + 2 y2) per l block
 };
@@ -63,7 +63,7 @@ struct Smem {
 // [Y3R][D], y2 [D], x1 [SL]
 template <int D>
 struct Sum {
-    static constexpr size_t STATE = (size_t)NW * Pat<D>::NT * 64 * 4;
+    static constexpr size_t STATE = (size_t)Pat<D>::NW * Pat<D>::NT * 64 * 4;
     static constexpr size_t Y3 = (size_t)Pat<D>::Y3R * D;
     static constexpr size_t FLOATS = STATE + Y3 + D + SL;
     static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
@@ -80,7 +80,7 @@ struct Sum {
 // keys), values dO scaled by 1/G per token (vsc), and no denominator: the
 // numerator F is the output.
 template <int D, typename T, bool CAUSAL, int MODE, bool DV = false>
-__global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, const T *__restrict__ k,
+__global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                    const T *__restrict__ v, T *__restrict__ out,
                                                    float *__restrict__ g, float *__restrict__ sums,
                                                    float *__restrict__ fpw, float *__restrict__ gpw,
@@ -91,6 +91,7 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
     using PT = Pat<D>;
     constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
     constexpr int NPART = PT::NPART, NGW = PT::NGW, NLB = PT::NLB, Y3R = PT::Y3R;
+    constexpr int NW = PT::NW, NTH = PT::NTH, LPT = PT::LPT, VPL = PT::VPL;
     constexpr int NSL = D / SL;
     __shared__ Smem<D> sm;
 
@@ -171,12 +172,12 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
         }
     }
 
-    // ---- staging: token tg = tid / 8, channels 8-way split, 2 v columns -
-    const int tg = tid >> 3, part = tid & 7;
-    constexpr int DP = D / 8;
+    // ---- staging: token tg = tid / LPT, channels LPT-way split, VPL v columns
+    const int tg = tid / LPT, part = tid % LPT;
+    constexpr int DP = PT::DP;
     // the next chunk's rows are loaded into registers while the current one
     // is processed
-    float pq[DP], pk[DP], pv[2];
+    float pq[DP], pk[DP], pv[VPL];
     bool pvalid = false;
     auto prefetch = [&](int c) {
         const int n0 = c * C + tg;
@@ -189,8 +190,8 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
         }
         const float vm = DV && pvalid ? vsc[n] : 1.0f;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-            pv[i] = pvalid ? io<T>::ld(v, (size_t)n * D + SL * sl + 2 * part + i) * vm : 0.f;
+        for (int i = 0; i < VPL; ++i)
+            pv[i] = pvalid ? io<T>::ld(v, (size_t)n * D + SL * sl + VPL * part + i) * vm : 0.f;
     };
     auto stage = [&]() {
         standardise_part<D>(pq, pvalid, qs);
@@ -203,13 +204,14 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
             sm.kT[ch * TS + tg] = pk[i];
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) sm.vrow[tg * SL + 2 * part + i] = pv[i];
+        for (int i = 0; i < VPL; ++i) sm.vrow[tg * SL + VPL * part + i] = pv[i];
     };
 
     // one chunk in mode M (DELTA: state update only; QUERY: outputs only;
     // SCAN: outputs, then the update unless the segment ends here)
-    auto chunk = [&](auto mc, int c) {
+    auto chunk = [&](auto mc, auto ghc, int c) {
         constexpr int M = decltype(mc)::value;
+        constexpr int GH = decltype(ghc)::value;   // wave class (channel blocks)
             const int n0 = c * C;
             stage();
             if (c + 1 < cend) prefetch(c + 1);
@@ -234,11 +236,11 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                     }
                     static_for<0, NCH>([&](auto ci) {
                         constexpr int cc = decltype(ci)::value;
-                        constexpr int u0 = PT::u0(cc);
+                        constexpr int u0 = PT::u0(cc, GH);
                         const float qm = qr[gw + NGW * cc];
                         static_for<u0, NU>([&](auto ui) {
                             constexpr int u = decltype(ui)::value;
-                            constexpr int t = PT::first(cc) + u - u0;
+                            constexpr int t = PT::first(cc, GH) + u - u0;
                             const float qmw = (u == u0) ? 0.5f * qm : qm;
     #pragma unroll
                             for (int i = 0; i < 4; ++i) F = mma(S[t][i], qmw * ql[u][i], F);
@@ -294,7 +296,7 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                     }
                 }
                 __syncthreads();
-                // ---- outputs O = F / G: token tg, columns 2 part, 2 part + 1 --
+                // ---- outputs O = F / G: token tg, columns VPL part .. + VPL - 1
                 // (part 0 of several adds the count and x1; each part its
                 // share of the rest)
                 {
@@ -312,8 +314,8 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                         }
                         const float rG = 1.0f / G;
     #pragma unroll
-                        for (int i = 0; i < 2; ++i) {
-                            const int j = 2 * part + i;
+                        for (int i = 0; i < VPL; ++i) {
+                            const int j = VPL * part + i;
                             float F = pp == 0 ? sm.x1[j] : 0.f;
     #pragma unroll
                             for (int ww = 0; ww < NW; ++ww) F += sm.fpart[ww][rt][16 * (j >> 2) + t16][j & 3];
@@ -347,14 +349,14 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
                 }
                 static_for<0, NCH>([&](auto ci) {
                     constexpr int cc = decltype(ci)::value;
-                    constexpr int u0 = PT::u0(cc);
+                    constexpr int u0 = PT::u0(cc, GH);
                     const float *km = sm.kT + (gw + NGW * cc) * TS + h;
                     float Bm[C / 4];
     #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) Bm[ks] = km[4 * ks] * Vb[ks];
                     static_for<u0, NU>([&](auto ui) {
                         constexpr int u = decltype(ui)::value;
-                        constexpr int t = PT::first(cc) + u - u0;
+                        constexpr int t = PT::first(cc, GH) + u - u0;
     #pragma unroll
                         for (int ks = 0; ks < C / 4; ++ks) S[t] = mma(Ak[u][ks], Bm[ks], S[t]);
                     });
@@ -397,16 +399,18 @@ __global__ __launch_bounds__(NTH) void scan_kernel(const T *__restrict__ q, cons
             }
             __syncthreads();
     };
-    if constexpr (MODE == BOTH) {
-        // non-causal, one segment: the totals first, then every query
-        prefetch(cbeg);
-        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, DELTA>{}, c);
-        prefetch(cbeg);
-        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, QUERY>{}, c);
-    } else {
-        prefetch(cbeg);
-        for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, MODE>{}, c);
-    }
+    with_wave_class<D>(gw, [&](auto ghc) {
+        if constexpr (MODE == BOTH) {
+            // non-causal, one segment: the totals first, then every query
+            prefetch(cbeg);
+            for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, DELTA>{}, ghc, c);
+            prefetch(cbeg);
+            for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, QUERY>{}, ghc, c);
+        } else {
+            prefetch(cbeg);
+            for (int c = cbeg; c < cend; ++c) chunk(std::integral_constant<int, MODE>{}, ghc, c);
+        }
+    });
 
     if constexpr (MODE == DELTA) {
         // this segment's sums: state, Y3 (from LDS, written by the last
@@ -491,22 +495,22 @@ hipError_t launch(const void *q, const void *k, const void *v, const float *vsc,
     const dim3 pgrid((unsigned)((Sum<D>::FLOATS + 255) / 256), items);
     if (causal) {
         if (nseg > 1) {
-            hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA, DV>), grid, dim3(NTH), 0, st, Q, K,
+            hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K,
                                V, O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
             hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
                                stride, 1);
         }
-        hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN, DV>), grid, dim3(NTH), 0, st, Q, K, V, O,
+        hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V, O,
                            g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
     } else if (nseg == 1) {
-        hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH, DV>), grid, dim3(NTH), 0, st, Q, K, V,
+        hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V,
                            O, g, nullptr, fpw, gpw, vsc, N, nseg, qs, ks);
     } else {
-        hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA, DV>), grid, dim3(NTH), 0, st, Q, K, V,
+        hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V,
                            O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
         hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
                            stride, 0);
-        hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY, DV>), grid, dim3(NTH), 0, st, Q, K, V,
+        hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V,
                            O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
     }
     if constexpr (Pat<D>::NPART > 1) {
