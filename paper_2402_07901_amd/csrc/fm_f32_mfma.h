@@ -47,7 +47,7 @@ struct Pat {
     // and write partial F, G; their eight waves (two per SIMD) keep about 84
     // state registers each, so a second wave hides each wave's stalls.
     static constexpr int NPART = D == 128 ? 4 : 1;
-    static constexpr int NW = D == 128 ? 8 : 4;
+    static constexpr int NW = 8;
     static constexpr int NTH = NW * 64;
     static constexpr int LPT = NTH / C;                // staging lanes per token
     static constexpr int DP = D / LPT;                 // staged channels per lane
