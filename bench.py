@@ -294,9 +294,12 @@ def main():
     if w.p == 2 and w.dtype == "bf16" and w.D == 64 and drop is None:
         bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "bf16")]
         achieved = flops / avg_launch_s / 1e12
+    elif w.p == 2 and drop is None:
+        # every other p = 2 case runs on the float32 MFMA kernels
+        bound, unit, peak = "mfma", "TFLOP/s", PEAK[("mfma", "f32")]
+        achieved = flops / avg_launch_s / 1e12
     elif w.p == 2:
-        # the float32 path (every case but D = 64, p = 2, bf16) computes on
-        # the vector ALU in fp32
+        # quadratic dropout: the float32 kernels on the vector ALU
         bound, unit, peak = "alu", "TFLOP/s", PEAK[("alu", "f32")]
         achieved = flops / avg_launch_s / 1e12
     else:
@@ -340,12 +343,14 @@ def main():
                                     "unit": "TFLOP/s", "bound": "alu",
                                     "peak": PEAK[("alu", "f32")],
                                     "frac": ach / PEAK[("alu", "f32")], "traffic": None})
-        elif bf is not None and w.dtype == "bf16" and w.D == 64:
+        elif bf is not None:
+            # bf16 D = 64: the fp16 MFMA kernels; every other p = 2 case the
+            # float32 MFMA kernels
             ach = bf / (bms / 1e3) / 1e12
+            pk = PEAK[("mfma", "bf16" if w.dtype == "bf16" and w.D == 64 else "f32")]
             rec["backward"].update({"algorithmic_flops_per_call": bf, "achieved": ach,
-                                    "unit": "TFLOP/s", "bound": "mfma",
-                                    "peak": PEAK[("mfma", "bf16")],
-                                    "frac": ach / PEAK[("mfma", "bf16")],
+                                    "unit": "TFLOP/s", "bound": "mfma", "peak": pk,
+                                    "frac": ach / pk,
                                     "traffic": load_traffic("fastmax_bwd", w.name)})
     rec["roofline"]["median_launch_ms"] = float(np.median(launch_ms))
     if drop is not None:
