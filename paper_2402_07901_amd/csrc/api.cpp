@@ -66,8 +66,9 @@ bool mfma_causal(int D, int p, int causal, int dt)
     return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
 }
 
-// The float32 MFMA kernels (forward and backward) serve p = 2 wherever the
-// fp16 MFMA kernels do not: float32 I/O for every D, bf16 I/O for D != 64.
+// The float32 MFMA kernels (forward and backward) serve p = 1, and p = 2
+// wherever the fp16 MFMA kernels do not: float32 I/O for every D, bf16 I/O
+// for D != 64.
 bool f32mfma(int D, int p, int causal, int dt, int N)
 {
     if (mfma_causal(D, p, causal, dt) || mfma_noncausal(N, D, p, causal, dt)) return false;
@@ -78,7 +79,7 @@ size_t fwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_fwd_workspace(B * H, N);
     if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_workspace(B * H, N);
-    if (f32mfma(D, p, causal, dt, N)) return fm::f32mfma_fwd_workspace(B * H, N, D);
+    if (f32mfma(D, p, causal, dt, N)) return fm::f32mfma_fwd_workspace(B * H, N, D, p);
     return fm::generic_fwd_workspace(B * H, N, D, p);
 }
 
@@ -86,7 +87,7 @@ size_t bwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 {
     if (mfma_causal(D, p, causal, dt)) return fm::mfma_causal_bwd_workspace(B * H, N);
     if (mfma_noncausal(N, D, p, causal, dt)) return fm::mfma_nc_bwd_workspace(B * H, N);
-    if (f32mfma(D, p, causal, dt, N)) return fm::f32mfma_bwd_workspace(B * H, N, D);
+    if (f32mfma(D, p, causal, dt, N)) return fm::f32mfma_bwd_workspace(B * H, N, D, p);
     return fm::generic_bwd_workspace(B, H, N, D, p);
 }
 
@@ -121,7 +122,7 @@ int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, in
     else if (mfma_noncausal(N, D, p, causal, dt))
         e = mfma_nc_fwd(q, k, v, out, g, B * H, N, qk_scale, workspace, stream);
     else if (f32mfma(D, p, causal, dt, N))
-        e = f32mfma_fwd(q, k, v, out, g, B * H, N, D, causal, dt == FASTMAX_BF16, qk_scale,
+        e = f32mfma_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
                         workspace, stream);
     else
         e = generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
@@ -168,7 +169,7 @@ int bwd_impl(const void *q, const void *k, const void *v, const void *out, const
         e = fm::mfma_nc_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, qk_scale, workspace,
                             stream);
     else if (f32mfma(D, p, causal, dt, N))
-        e = fm::f32mfma_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, causal,
+        e = fm::f32mfma_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
                             dt == FASTMAX_BF16, qk_scale, workspace, stream);
     else
         e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,

@@ -1,5 +1,5 @@
-// Fastmax backward on float32 MFMA (v_mfma_f32_16x16x4_f32), p = 2, the cases
-// of the float32 MFMA forward.  Sec. 2.5's custom gradient: only O and G are
+// Fastmax backward on float32 MFMA (v_mfma_f32_16x16x4_f32), p = 1 and 2, the
+// cases of the float32 MFMA forward (p = 1: f' = 1, the linear tiles only).  Sec. 2.5's custom gradient: only O and G are
 // kept from the forward, q^ and k^ are recomputed, and the moments are
 // rebuilt by scans instead of stored.  With u_i = dO_i / G_i,
 // c_i = (dO_i . O_i) / G_i and s_in = q~_i . k^_n (q~ = tau q^):
@@ -52,43 +52,47 @@ namespace m32 {
 
 // Tokens of the per-wave output blocks: the whole chunk where the waves'
 // blocks fit 64 KB of LDS, else one 16-token row tile at a time.
-template <int D>
-constexpr int out_tokens() { return Pat<D>::NW * D * (C + 4) * 4 <= 65536 ? C : 16; }
+template <int D, int P>
+constexpr int out_tokens() { return Pat<D, P>::NW * D * (C + 4) * 4 <= 65536 ? C : 16; }
 
-template <int D>
+template <int D, int P>
 struct alignas(16) GSmem {
-    float xrow[C * Pat<D>::RS];    // state keys X [token][channel]
-    float xT[D * Pat<D>::TS];      // X [channel][token]
+    float xrow[C * Pat<D, P>::RS];  // state keys X [token][channel]
+    float xT[D * Pat<D, P>::TS];    // X [channel][token]
     alignas(16) float zrow[C * (D + 4)];   // contraction features Z [token][channel] (16-byte rows)
     float vs[C * SL];              // state values, this slice [token][column]
     float uc[C * SL];              // contraction columns, this slice
     float wt[C];                   // state weights w
     float zt[C];                   // contraction scalars z
-    float y3[16 * Pat<D>::RS];     // the item's row block of Y3w (before the chunk)
-    float y2[16];                  // its entries of y2w
-    float ob[Pat<D>::NW][D * (out_tokens<D>() + 4)];   // each wave's outputs [feature][token]
+    float y3[(P == 2 ? 16 : 1) * Pat<D, P>::RS];   // the item's row block of Y3w (p = 2)
+    float y2[P == 2 ? 16 : D];     // its entries of y2w (p = 1: all of y2w)
+    float ob[Pat<D, P>::NW][D * (out_tokens<D, P>() + 4)];   // each wave's outputs [feature][token]
 };
 
-// Segment summary: [wave][tile][lane] f4 state, the Y3w row block [16][D],
-// y2w [16].
-template <int D>
+// Segment summary: [wave][tile][lane] f4 state, the Y3w row block [16][D]
+// and y2w [16] (p = 1: y2w [D]).
+template <int D, int P>
 struct GSum {
-    static constexpr size_t STATE = (size_t)Pat<D>::NW * Pat<D>::NT * 64 * 4;
-    static constexpr size_t FLOATS = STATE + 16 * D + 16;
+    static constexpr size_t STATE = (size_t)Pat<D, P>::NW * Pat<D, P>::NT * 64 * 4;
+    static constexpr int Y3N = P == 2 ? 16 * D : 0, Y2N = P == 2 ? 16 : D;
+    static constexpr size_t FLOATS = STATE + Y3N + Y2N;
     static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
 };
 
 // One workgroup: (item = (head * NSL + slice) * NPART + part, segment).  The
 // item (slice, part) with index sl * NPART + part = b < D/16 also keeps row
-// block b of Y3w and y2w; slice 0 adds the z_t w_r term of the in-chunk pairs.
-template <int D, typename T, bool CAUSAL, int MODE, bool REV>
-__global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
+// block b of Y3w and y2w (p = 1: item 0 keeps y2w); slice 0 adds the z_t w_r
+// term of the in-chunk pairs.  p = 1 (f' = 1): only the linear tiles, no
+// Y3w, in-chunk weights UC_t.VS_r + z_t w_r.
+template <int D, typename T, bool CAUSAL, int MODE, bool REV, int P>
+__global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
     const T *__restrict__ X, const T *__restrict__ Z, const T *__restrict__ VS,
     const T *__restrict__ UC, const float *__restrict__ vsm, const float *__restrict__ ucm,
     const float *__restrict__ wv, const float *__restrict__ zv, float *__restrict__ outh,
     float *__restrict__ sums, int N, int nseg, float xs, float zsc)
 {
-    using PT = Pat<D>;
+    using PT = Pat<D, P>;
+    using GS = GSum<D, P>;
     constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
     constexpr int NPART = PT::NPART, NGW = PT::NGW;
     constexpr int NW = PT::NW, NTH = PT::NTH, LPT = PT::LPT, VPL = PT::VPL;
@@ -96,14 +100,16 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
     constexpr int ZS = D + 4;   // row stride of Z
     // output block: FT tokens; its feature stride puts the lanes (token r16,
     // features 4h + i) of one LDS store in 64 distinct banks
-    constexpr int FT = out_tokens<D>(), OS = FT + 4;
-    __shared__ GSmem<D> sm;
+    constexpr int FT = out_tokens<D, P>(), OS = FT + 4;
+    constexpr int NCQ = P == 2 ? NCH : 0;   // channels with quadratic tiles
+    __shared__ GSmem<D, P> sm;
 
     const int item = blockIdx.x / nseg, seg = blockIdx.x % nseg;
     const int pp = NPART == 1 ? 0 : item % NPART;
     const int head = item / (NSL * NPART), sl = (item / NPART) % NSL;
     const int yb = item % (NSL * NPART);
-    const int ylb = yb < NU ? yb : -1;   // the item's Y3w row block, if any
+    // the item's Y3w row block, if any (p = 1: 0 for the item that keeps y2w)
+    const int ylb = (P == 2 ? yb < NU : yb == 0) ? yb : -1;
     const bool scal = sl == 0;
     const int nch = (N + C - 1) / C;
     const int cbeg = (int)((long long)seg * nch / nseg), cend = (int)((long long)(seg + 1) * nch / nseg);
@@ -117,7 +123,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
     if (ucm) ucm += (size_t)head * N;
     if (wv) wv += (size_t)head * N;
     if (zv) zv += (size_t)head * N;
-    float *sum = sums ? sums + (size_t)(item * nseg + seg) * (GSum<D>::BYTES / 4) : nullptr;
+    float *sum = sums ? sums + (size_t)(item * nseg + seg) * (GS::BYTES / 4) : nullptr;
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, h = lane >> 4;
     const int gw = pp * NW + w;
@@ -128,12 +134,13 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
 #pragma unroll
     for (int t = 0; t < NT; ++t)
         S[t] = loaded ? *(const f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) : f4{0.f, 0.f, 0.f, 0.f};
-    float y2reg = 0.f;   // thread tid < 16 of an item with a Y3w block: y2w[16 ylb + tid]
+    // thread tid < Y2N of an item with a Y3w block: y2w[16 ylb + tid] (p = 1: y2w[tid])
+    float y2reg = 0.f;
     {
-        const float *sy = loaded ? sum + GSum<D>::STATE : nullptr;
-        for (int e = tid; e < 16 * D; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy[e] : 0.f;
-        if (tid < 16) {
-            y2reg = loaded ? sy[16 * D + tid] : 0.f;
+        const float *sy = loaded ? sum + GS::STATE : nullptr;
+        for (int e = tid; e < GS::Y3N; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy[e] : 0.f;
+        if (tid < GS::Y2N) {
+            y2reg = loaded ? sy[GS::Y3N + tid] : 0.f;
             sm.y2[tid] = y2reg;
         }
     }
@@ -143,7 +150,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
 #pragma unroll
     for (int kk = 0; kk < NYW; ++kk) Y[kk] = f4{0.f, 0.f, 0.f, 0.f};
     __syncthreads();
-    if (loaded && ylb >= 0) {
+    if (P == 2 && loaded && ylb >= 0) {
 #pragma unroll
         for (int kk = 0; kk < NYW; ++kk) {
             const int u2 = w + NW * kk;
@@ -248,9 +255,11 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
                         if (!ich[st]) continue;
                         // S^T and P^T: lane (token tok, keys 16 st + 4h + i)
                         f4 Sc = {0.f, 0.f, 0.f, 0.f}, Pc = {0.f, 0.f, 0.f, 0.f};
-                        const float *xr = sm.xrow + (16 * st + r16) * RS;
+                        if constexpr (P == 2) {
+                            const float *xr = sm.xrow + (16 * st + r16) * RS;
 #pragma unroll
-                        for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[4 * kk + h], zr[4 * kk + h], Sc);
+                            for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[4 * kk + h], zr[4 * kk + h], Sc);
+                        }
                         const float *vr = sm.vs + (16 * st + r16) * SL;
 #pragma unroll
                         for (int kk = 0; kk < 4; ++kk)
@@ -258,16 +267,19 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
                         const float zs = scal ? sm.zt[tok] : 0.f;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            float wgt = (1.0f + Sc[i]) * fmaf(zs, sm.wt[16 * st + 4 * h + i], Pc[i]);
+                            float wgt = fmaf(zs, sm.wt[16 * st + 4 * h + i], Pc[i]);
+                            if (P == 2) wgt *= 1.0f + Sc[i];
                             if (st == rt && 4 * h + i > r16) wgt = 0.0f;
                             Wt[st][i] = wgt;
                         }
                     }
                 }
                 // the item's Y3w block: out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
+                // (p = 1: out[l] += z_t y2w[l], every block)
                 f4 Tq = {0.f, 0.f, 0.f, 0.f};
                 const bool yw = ylb >= 0 && w == NW - 1;
-                if (yw) {
+                const float zst = sm.zt[tok];
+                if (P == 2 && yw) {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
                     const float *yr = sm.y3 + r16 * RS;
@@ -288,7 +300,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
                     constexpr int u = NU - 1 - decltype(ri)::value;
                     const f4 zlu = *(const f4 *)(zr + 16 * u + 4 * h);
                     f4 a4 = {0.f, 0.f, 0.f, 0.f};
-                    static_for<0, NCH>([&](auto ci) {
+                    static_for<0, NCQ>([&](auto ci) {
                         constexpr int cc = decltype(ci)::value;
                         constexpr int u0 = PT::u0(cc, GH);
                         if constexpr (u >= u0) {
@@ -315,7 +327,11 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
                         }
                     });
                     if (gw == u) a4 += Tl;
-                    if (yw && ylb == u) a4 += Tq;
+                    if (P == 2 && yw && ylb == u) a4 += Tq;
+                    if (P == 1 && yw) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) a4[i] = fmaf(zst, sm.y2[16 * u + 4 * h + i], a4[i]);
+                    }
                     if constexpr (M == SCAN && CAUSAL) {
 #pragma unroll
                         for (int st = 0; st < 2; ++st) {
@@ -355,7 +371,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
 #pragma unroll
                 for (int ks = 0; ks < C / 4; ++ks) S[0] = mma(Vb[ks], xl[4 * ks], S[0]);
             }
-            static_for<0, NCH>([&](auto ci) {
+            static_for<0, NCQ>([&](auto ci) {
                 constexpr int cc = decltype(ci)::value;
                 constexpr int u0 = PT::u0(cc, GH);
                 const float *xm = sm.xT + (gw + NGW * cc) * TS + h;
@@ -369,7 +385,13 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
                     for (int ks = 0; ks < C / 4; ++ks) S[t] = mma(Bm[ks], Ak[u][ks], S[t]);
                 });
             });
-            if (ylb >= 0) {
+            if (P == 1 && ylb >= 0 && tid < D) {
+                float s = 0.f;
+#pragma unroll 8
+                for (int t = 0; t < C; ++t) s = fmaf(sm.wt[t], sm.xrow[t * RS + tid], s);
+                y2reg += s;
+            }
+            if (P == 2 && ylb >= 0) {
                 const float *xa = sm.xT + (16 * ylb + r16) * TS + h;
                 float aw[C / 4];
 #pragma unroll
@@ -390,7 +412,8 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
                 }
             }
             __syncthreads();
-            if (ylb >= 0) {
+            if (P == 1 && ylb >= 0 && tid < D) sm.y2[tid] = y2reg;
+            if (P == 2 && ylb >= 0) {
 #pragma unroll
                 for (int kk = 0; kk < NYW; ++kk) {
                     const int u2 = w + NW * kk;
@@ -403,7 +426,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
         }
         __syncthreads();
     };
-    with_wave_class<D>(gw, [&](auto ghc) {
+    with_wave_class<D, P>(gw, [&](auto ghc) {
         if constexpr (MODE == BOTH) {
             // non-causal, one segment: the totals first, then every output row
             prefetch(cbeg);
@@ -419,9 +442,9 @@ __global__ __launch_bounds__(Pat<D>::NTH) void grad_kernel(
     if constexpr (MODE == DELTA) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) *(f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) = S[t];
-        float *sy = sum + GSum<D>::STATE;
-        for (int e = tid; e < 16 * D; e += NTH) sy[e] = sm.y3[(e / D) * RS + e % D];
-        if (tid < 16) sy[16 * D + tid] = y2reg;
+        float *sy = sum + GS::STATE;
+        for (int e = tid; e < GS::Y3N; e += NTH) sy[e] = sm.y3[(e / D) * RS + e % D];
+        if (tid < GS::Y2N) sy[GS::Y3N + tid] = y2reg;
     }
 }
 
@@ -516,66 +539,67 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(const T *__restrict__ q
         io<T>::st(dx, r * D + j + 16 * i, (gv[i] - m1 - xv[i] * m2) * rs);
 }
 
-template <int D>
+template <int D, int P>
 struct BwdPlan {
     int items, nch, nseg;
     size_t vec_bytes, grad_bytes, scan_bytes;
     BwdPlan(int BH, int N)
     {
-        items = BH * (D / SL) * Pat<D>::NPART;
+        items = BH * (D / SL) * Pat<D, P>::NPART;
         nch = (N + C - 1) / C;
         nseg = nseg_of(items, nch);
         const size_t rows = (size_t)BH * N;
         vec_bytes = a256(rows * 4);
         grad_bytes = a256(rows * D * 4);
-        const size_t gsum = nseg > 1 ? a256((size_t)items * nseg * GSum<D>::BYTES) : 0;
-        const size_t fwd = f32mfma_fwd_workspace(BH, N, D);   // the dv scan's
+        const size_t gsum = nseg > 1 ? a256((size_t)items * nseg * GSum<D, P>::BYTES) : 0;
+        const size_t fwd = f32mfma_fwd_workspace(BH, N, D, P);   // the dv scan's
         scan_bytes = gsum > fwd ? gsum : fwd;
     }
     // rg, c, dq~, dk^, then the scans' region (used by one scan at a time)
     size_t bytes() const { return 2 * vec_bytes + 2 * grad_bytes + scan_bytes; }
 };
 
-template <int D, typename T, bool REV>
-hipError_t grad_launch(const BwdPlan<D> &pl, const T *X, const T *Z, const T *VS, const T *UC,
+template <int D, typename T, bool REV, int P>
+hipError_t grad_launch(const BwdPlan<D, P> &pl, const T *X, const T *Z, const T *VS, const T *UC,
                        const float *vsm, const float *ucm, const float *wv, const float *zv,
                        float *outh, float *sums, int N, int causal, float xs, float zsc,
                        hipStream_t st)
 {
+    using GS = GSum<D, P>;
     const int items = pl.items, nseg = pl.nseg;
     if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
-    const dim3 grid((unsigned)(items * nseg));
-    const size_t stride = GSum<D>::BYTES / 4;
-    const dim3 pgrid((unsigned)((GSum<D>::FLOATS + 255) / 256), items);
+    const dim3 grid((unsigned)(items * nseg)), blk(Pat<D, P>::NTH);
+    const size_t stride = GS::BYTES / 4;
+    const dim3 pgrid((unsigned)((GS::FLOATS + 255) / 256), items);
     if (causal) {
         if (nseg > 1) {
-            hipLaunchKernelGGL((grad_kernel<D, T, true, DELTA, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
-                               VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
-            hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg,
-                               GSum<D>::FLOATS, stride, 1);
+            hipLaunchKernelGGL((grad_kernel<D, T, true, DELTA, REV, P>), grid, blk, 0, st, X, Z, VS,
+                               UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+            hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, GS::FLOATS,
+                               stride, 1);
         }
-        hipLaunchKernelGGL((grad_kernel<D, T, true, SCAN, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z, VS,
-                           UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+        hipLaunchKernelGGL((grad_kernel<D, T, true, SCAN, REV, P>), grid, blk, 0, st, X, Z, VS, UC,
+                           vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
     } else if (nseg == 1) {
-        hipLaunchKernelGGL((grad_kernel<D, T, false, BOTH, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
-                           VS, UC, vsm, ucm, wv, zv, outh, nullptr, N, nseg, xs, zsc);
+        hipLaunchKernelGGL((grad_kernel<D, T, false, BOTH, REV, P>), grid, blk, 0, st, X, Z, VS, UC,
+                           vsm, ucm, wv, zv, outh, nullptr, N, nseg, xs, zsc);
     } else {
-        hipLaunchKernelGGL((grad_kernel<D, T, false, DELTA, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
-                           VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
-        hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, GSum<D>::FLOATS,
-                           stride, 0);
-        hipLaunchKernelGGL((grad_kernel<D, T, false, QUERY, REV>), grid, dim3(Pat<D>::NTH), 0, st, X, Z,
-                           VS, UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+        hipLaunchKernelGGL((grad_kernel<D, T, false, DELTA, REV, P>), grid, blk, 0, st, X, Z, VS,
+                           UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
+        hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, GS::FLOATS, stride,
+                           0);
+        hipLaunchKernelGGL((grad_kernel<D, T, false, QUERY, REV, P>), grid, blk, 0, st, X, Z, VS,
+                           UC, vsm, ucm, wv, zv, outh, sums, N, nseg, xs, zsc);
     }
     return hipGetLastError();
 }
 
-template <int D, typename T>
+template <int D, typename T, int P>
 hipError_t bwd_run(const void *q, const void *k, const void *v, const void *o, const void *dout,
                    const float *g, void *dq, void *dk, void *dv, int BH, int N, int causal,
                    float qs, void *ws, hipStream_t st)
 {
-    const BwdPlan<D> pl(BH, N);
+    const BwdPlan<D, P> pl(BH, N);
     const size_t rows = (size_t)BH * N;
     char *p = (char *)ws;
     float *rg = (float *)p;
@@ -588,52 +612,74 @@ hipError_t bwd_run(const void *q, const void *k, const void *v, const void *o, c
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v, *DO = (const T *)dout;
     hipLaunchKernelGGL((bwd_prep_kernel<D, T>), dim3((unsigned)rb), dim3(256), 0, st, (const T *)o,
                        DO, g, rg, cvec, dqh, dkh, rows);
-    hipError_t e = f32mfma_dv(q, k, dout, rg, dv, BH, N, D, causal, std::is_same<T, bf16_t>::value,
-                              qs, scan, st);
+    hipError_t e = f32mfma_dv(q, k, dout, rg, dv, BH, N, D, P, causal,
+                              std::is_same<T, bf16_t>::value, qs, scan, st);
     if (e != hipSuccess) return e;
     // dq~: X = k^, VS = v, w = 1; Z = tau q^, UC = dO / G, z = -c
-    e = grad_launch<D, T, false>(pl, K, Q, V, DO, nullptr, rg, nullptr, cvec, dqh, (float *)scan,
-                                 N, causal, 1.0f, qs, st);
+    e = grad_launch<D, T, false, P>(pl, K, Q, V, DO, nullptr, rg, nullptr, cvec, dqh,
+                                    (float *)scan, N, causal, 1.0f, qs, st);
     if (e != hipSuccess) return e;
     // dk^: X = tau q^, VS = dO / G, w = c; Z = k^, UC = v, z = -1 (reverse order)
-    e = grad_launch<D, T, true>(pl, Q, K, DO, V, rg, nullptr, cvec, nullptr, dkh, (float *)scan,
-                                N, causal, qs, 1.0f, st);
+    e = grad_launch<D, T, true, P>(pl, Q, K, DO, V, rg, nullptr, cvec, nullptr, dkh,
+                                   (float *)scan, N, causal, qs, 1.0f, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((bwd_finish_kernel<D, T>), dim3((unsigned)rb, 2), dim3(256), 0, st, Q, K,
                        dqh, dkh, (T *)dq, (T *)dk, rows, qs);
     return hipGetLastError();
 }
 
+template <typename T, int P>
+hipError_t bwd_dt(const void *q, const void *k, const void *v, const void *o, const void *dout,
+                  const float *g, void *dq, void *dk, void *dv, int BH, int N, int D, int causal,
+                  float qs, void *ws, hipStream_t st)
+{
+    switch (D) {
+    case 16: return bwd_run<16, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    case 32: return bwd_run<32, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    case 64:
+        // bf16 D = 64, p = 2 has the fp16 MFMA kernels of its own
+        if constexpr (std::is_same<T, bf16_t>::value && P == 2) return hipErrorInvalidValue;
+        else return bwd_run<64, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    case 128: return bwd_run<128, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 }  // namespace m32
 
-size_t f32mfma_bwd_workspace(int BH, int N, int D)
+size_t f32mfma_bwd_workspace(int BH, int N, int D, int p)
 {
     using namespace m32;
+    if (p == 1) {
+        switch (D) {
+        case 16: return BwdPlan<16, 1>(BH, N).bytes();
+        case 32: return BwdPlan<32, 1>(BH, N).bytes();
+        case 64: return BwdPlan<64, 1>(BH, N).bytes();
+        case 128: return BwdPlan<128, 1>(BH, N).bytes();
+        }
+        return 0;
+    }
     switch (D) {
-    case 16: return BwdPlan<16>(BH, N).bytes();
-    case 32: return BwdPlan<32>(BH, N).bytes();
-    case 64: return BwdPlan<64>(BH, N).bytes();
-    case 128: return BwdPlan<128>(BH, N).bytes();
+    case 16: return BwdPlan<16, 2>(BH, N).bytes();
+    case 32: return BwdPlan<32, 2>(BH, N).bytes();
+    case 64: return BwdPlan<64, 2>(BH, N).bytes();
+    case 128: return BwdPlan<128, 2>(BH, N).bytes();
     }
     return 0;
 }
 
 hipError_t f32mfma_bwd(const void *q, const void *k, const void *v, const void *o,
                        const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                       int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st)
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st)
 {
     using namespace m32;
-    if (is_bf16) {
-        if (D == 16) return bwd_run<16, bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-        if (D == 32) return bwd_run<32, bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-        if (D == 128) return bwd_run<128, bf16_t>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-        return hipErrorInvalidValue;
-    }
-    if (D == 16) return bwd_run<16, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-    if (D == 32) return bwd_run<32, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-    if (D == 64) return bwd_run<64, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-    if (D == 128) return bwd_run<128, float>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-    return hipErrorInvalidValue;
+    if (!f32mfma_applies(D, p, is_bf16)) return hipErrorInvalidValue;
+    if (is_bf16)
+        return p == 2 ? bwd_dt<bf16_t, 2>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, causal, qs, ws, st)
+                      : bwd_dt<bf16_t, 1>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, causal, qs, ws, st);
+    return p == 2 ? bwd_dt<float, 2>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, causal, qs, ws, st)
+                  : bwd_dt<float, 1>(q, k, v, o, dout, g, dq, dk, dv, BH, N, D, causal, qs, ws, st);
 }
 
 }  // namespace fm

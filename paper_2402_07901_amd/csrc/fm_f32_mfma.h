@@ -39,14 +39,16 @@ __device__ __forceinline__ f4 mma(float a, float b, f4 c)
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-template <int D>
+// P: the order of the Taylor weight (1: f = 1 + s, state = the linear tiles
+// only; 2: f = 1 + s + s^2/2, plus the quadratic tiles and Y3).
+template <int D, int P = 2>
 struct Pat {
-    // Workgroups sharing one (head, slice) and waves per workgroup.  D = 128
-    // has too many feature tiles for one workgroup's accumulators: four
+    // Workgroups sharing one (head, slice) and waves per workgroup.  D = 128,
+    // p = 2 has too many feature tiles for one workgroup's accumulators: four
     // workgroups each take a quarter of them (and a quarter of the Y3 rows)
-    // and write partial F, G; their eight waves (two per SIMD) keep about 84
-    // state registers each, so a second wave hides each wave's stalls.
-    static constexpr int NPART = D == 128 ? 4 : 1;
+    // and write partial F, G.  Eight waves (two per SIMD) keep at most about
+    // 84 state registers each, so a second wave hides each wave's stalls.
+    static constexpr int NPART = (P == 2 && D == 128) ? 4 : 1;
     static constexpr int NW = 8;
     static constexpr int NTH = NW * 64;
     static constexpr int LPT = NTH / C;                // staging lanes per token
@@ -67,13 +69,14 @@ struct Pat {
         for (int cc = 0; cc < c; ++cc) t += NU - u0(cc, gh);
         return t;
     }
-    static constexpr int NQ = first(NCH, 0) - 1;       // quadratic tiles per wave (class 0: most)
+    // quadratic tiles per wave (class 0 has the most)
+    static constexpr int NQ = P == 2 ? first(NCH, 0) - 1 : 0;
     static constexpr int NT = 1 + NQ;                  // + the linear slot
     static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
-    static constexpr int Y3R = 16 * NLB;               // Y3 rows per part
+    static constexpr int Y3R = P == 2 ? 16 * NLB : 0;  // Y3 rows per part
     // Y3 tiles per part: one part keeps the blocks u <= u2 and mirrors them,
     // several parts keep full rows
-    static constexpr int NY3 = NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
+    static constexpr int NY3 = P != 2 ? 0 : NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
     static constexpr int RS = D + 2;   // row stride of row-major tiles (floats)
     static constexpr int TS = C + 2;   // row stride of transposed tiles
     static_assert(NGW <= 16 ? 16 % NGW == 0 : NGW % 16 == 0 && NH <= 2, "channel blocks");
@@ -81,10 +84,10 @@ struct Pat {
 };
 
 // Runs f(integral_constant<int, gh>) for the workgroup's wave class gh.
-template <int D, typename F>
+template <int D, int P, typename F>
 __device__ __forceinline__ void with_wave_class(int gw, F &&f)
 {
-    if constexpr (Pat<D>::NH == 1) {
+    if constexpr (Pat<D, P>::NH == 1) {
         f(std::integral_constant<int, 0>{});
     } else {
         if (gw < 16) f(std::integral_constant<int, 0>{});

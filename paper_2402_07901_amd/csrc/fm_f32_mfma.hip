@@ -1,7 +1,8 @@
-// Fastmax forward on float32 MFMA (v_mfma_f32_16x16x4_f32), p = 2,
-// D in {16, 32, 64}, causal and non-causal, float32 or bf16 I/O (the bf16,
-// D = 64 cases have their own fp16 kernels).  Every product and sum is fp32,
-// so the results meet the float32 bar.
+// Fastmax forward on float32 MFMA (v_mfma_f32_16x16x4_f32): p = 1 and 2,
+// D in {16, 32, 64, 128}, causal and non-causal, float32 or bf16 I/O (bf16,
+// D = 64, p = 2 has its own fp16 kernels).  Every product and sum is fp32, so
+// the results meet the float32 bar.  p = 1 keeps only the linear tiles and
+// the denominator n + q^.y2.
 //
 // The factorisation of Sec. 2.4: per (head, 16-column slice of V) the moment
 // state S[f][j] = sum_n phi_f(k^_n) v_nj over the features
@@ -45,26 +46,26 @@
 namespace fm {
 namespace m32 {
 
-template <int D>
+template <int D, int P>
 struct Smem {
-    float qrow[C * Pat<D>::RS];     // q^ (times the score scale) [token][channel]
-    float krow[C * Pat<D>::RS];     // k^ [token][channel]
-    float kT[D * Pat<D>::TS];       // k^ [channel][token]
+    float qrow[C * Pat<D, P>::RS];  // q^ (times the score scale) [token][channel]
+    float krow[C * Pat<D, P>::RS];  // k^ [token][channel]
+    float kT[D * Pat<D, P>::TS];    // k^ [channel][token]
     float vrow[C * SL];             // v slice [token][column]
-    float y3[Pat<D>::Y3R * Pat<D>::RS];   // Y3 prefix rows of the part (before the chunk)
+    float y3[(Pat<D, P>::Y3R > 0 ? Pat<D, P>::Y3R : 1) * Pat<D, P>::RS];   // Y3 prefix rows of the part
     float y2s[D];                   // 2 y2 prefix
     float x1[SL];                   // x1 prefix
-    f4 fpart[Pat<D>::NW][C / 16][64];   // partial F^T of the waves
+    f4 fpart[Pat<D, P>::NW][C / 16][64];   // partial F^T of the waves
     float gin[C];                   // in-chunk row sums
-    float gint[Pat<D>::NLB][C];     // partial q^T(Y3 q^ + 2 y2) per l block
+    float gint[Pat<D, P>::NLB][C];  // partial q^T(Y3 q^ + 2 y2) per l block (p = 1: 2 q^.y2)
 };
 
 // summary of a segment: [wave][tile][lane] f4 state, the part's Y3 rows
 // [Y3R][D], y2 [D], x1 [SL]
-template <int D>
+template <int D, int P>
 struct Sum {
-    static constexpr size_t STATE = (size_t)Pat<D>::NW * Pat<D>::NT * 64 * 4;
-    static constexpr size_t Y3 = (size_t)Pat<D>::Y3R * D;
+    static constexpr size_t STATE = (size_t)Pat<D, P>::NW * Pat<D, P>::NT * 64 * 4;
+    static constexpr size_t Y3 = (size_t)Pat<D, P>::Y3R * D;
     static constexpr size_t FLOATS = STATE + Y3 + D + SL;
     static constexpr size_t BYTES = (FLOATS * 4 + 255) & ~(size_t)255;
 };
@@ -79,8 +80,8 @@ struct Sum {
 // queries and keys exchanged (q <- k, k <- q and the score scale on the
 // keys), values dO scaled by 1/G per token (vsc), and no denominator: the
 // numerator F is the output.
-template <int D, typename T, bool CAUSAL, int MODE, bool DV = false>
-__global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__ q, const T *__restrict__ k,
+template <int D, typename T, bool CAUSAL, int MODE, bool DV, int P>
+__global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restrict__ q, const T *__restrict__ k,
                                                    const T *__restrict__ v, T *__restrict__ out,
                                                    float *__restrict__ g, float *__restrict__ sums,
                                                    float *__restrict__ fpw, float *__restrict__ gpw,
@@ -88,12 +89,14 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
                                                    float qs, float ks)
 {
     constexpr bool DEN = !DV;   // the denominator G (forward only)
-    using PT = Pat<D>;
+    using PT = Pat<D, P>;
+    using SM = Sum<D, P>;
     constexpr int NU = PT::NU, NCH = PT::NCH, NT = PT::NT, RS = PT::RS, TS = PT::TS;
     constexpr int NPART = PT::NPART, NGW = PT::NGW, NLB = PT::NLB, Y3R = PT::Y3R;
     constexpr int NW = PT::NW, NTH = PT::NTH, LPT = PT::LPT, VPL = PT::VPL;
     constexpr int NSL = D / SL;
-    __shared__ Smem<D> sm;
+    constexpr int NCQ = P == 2 ? NCH : 0;   // channels with quadratic tiles
+    __shared__ Smem<D, P> sm;
 
     const int item = blockIdx.x / nseg, seg = blockIdx.x % nseg;
     const int pp = NPART == 1 ? 0 : item % NPART;
@@ -112,7 +115,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
         fpw += (size_t)(head * NPART + pp) * N * D;
         gpw += (size_t)(head * NPART + pp) * N;
     }
-    float *sum = sums ? sums + (size_t)(item * nseg + seg) * (Sum<D>::BYTES / 4) : nullptr;
+    float *sum = sums ? sums + (size_t)(item * nseg + seg) * (SM::BYTES / 4) : nullptr;
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, h = lane >> 4;
     const int gw = pp * NW + w;   // wave index over the parts
@@ -127,7 +130,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
         S[t] = loaded ? *(const f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) : f4{0.f, 0.f, 0.f, 0.f};
     float y2reg = 0.f, x1reg = 0.f;   // thread d < D: y2[d]; D <= tid < D + SL: x1[tid - D]
     {
-        const float *sy3 = loaded ? sum + Sum<D>::STATE : nullptr;
+        const float *sy3 = loaded ? sum + SM::STATE : nullptr;
         constexpr int Y3N = Y3R * D;
         for (int e = tid; e < Y3N; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy3[e] : 0.f;
         if (tid < D) {
@@ -141,7 +144,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
     // Y3 accumulator tiles of this wave, tile index yi = w + 4 kk: one part
     // takes the pairs (u, u2), u <= u2, in row order; with several parts,
     // part pp takes rows u = LB0 .. LB0 + NLB - 1, every u2
-    constexpr int NYW = (PT::NY3 + NW - 1) / NW;
+    constexpr int NYW = PT::NY3 > 0 ? (PT::NY3 + NW - 1) / NW : 1;
     f4 Y[NYW];
     int yu[NYW], yu2[NYW];
 #pragma unroll
@@ -234,7 +237,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
     #pragma unroll
                         for (int i = 0; i < 4; ++i) F = mma(S[0][i], qw[i], F);
                     }
-                    static_for<0, NCH>([&](auto ci) {
+                    static_for<0, NCQ>([&](auto ci) {
                         constexpr int cc = decltype(ci)::value;
                         constexpr int u0 = PT::u0(cc, GH);
                         const float qm = qr[gw + NGW * cc];
@@ -261,7 +264,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
                                 // lane: query tok, keys 16 st + 4h + i
     #pragma unroll
                                 for (int i = 0; i < 4; ++i) {
-                                    float wv = fmaf(0.5f * Sc[i], Sc[i], 1.0f + Sc[i]);
+                                    float wv = P == 2 ? fmaf(0.5f * Sc[i], Sc[i], 1.0f + Sc[i]) : 1.0f + Sc[i];
                                     if (st == rt && 4 * h + i > r16) wv = 0.0f;
                                     Sc[i] = wv;
                                     gsum += wv;
@@ -278,15 +281,18 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
                         }
                     }
                     sm.fpart[w][rt][lane] = F;
-                    // denominator: q^T (Y3 q + 2 y2) over l block lb (the last
-                    // NLB waves; the first ones hold the linear and in-chunk work)
+                    // denominator: q^T (Y3 q + 2 y2) over l block lb (p = 1: 2 q.y2;
+                    // the last NLB waves; the first ones hold the linear and
+                    // in-chunk work)
                     if (DEN && lbl >= 0) {
                         f4 Tq;
     #pragma unroll
                         for (int i = 0; i < 4; ++i) Tq[i] = sm.y2s[16 * lb + 4 * h + i];
-                        const float *yr = sm.y3 + (16 * lbl + r16) * RS;
+                        if constexpr (P == 2) {
+                            const float *yr = sm.y3 + (16 * lbl + r16) * RS;
     #pragma unroll
-                        for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], qr[4 * kk + h], Tq);
+                            for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], qr[4 * kk + h], Tq);
+                        }
                         float gq = 0.f;
     #pragma unroll
                         for (int i = 0; i < 4; ++i) gq = fmaf(qr[16 * lb + 4 * h + i], Tq[i], gq);
@@ -347,7 +353,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
     #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) S[0] = mma(kl[4 * ks], Vb[ks], S[0]);
                 }
-                static_for<0, NCH>([&](auto ci) {
+                static_for<0, NCQ>([&](auto ci) {
                     constexpr int cc = decltype(ci)::value;
                     constexpr int u0 = PT::u0(cc, GH);
                     const float *km = sm.kT + (gw + NGW * cc) * TS + h;
@@ -399,7 +405,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
             }
             __syncthreads();
     };
-    with_wave_class<D>(gw, [&](auto ghc) {
+    with_wave_class<D, P>(gw, [&](auto ghc) {
         if constexpr (MODE == BOTH) {
             // non-causal, one segment: the totals first, then every query
             prefetch(cbeg);
@@ -417,7 +423,7 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
         // update), y2, x1
 #pragma unroll
         for (int t = 0; t < NT; ++t) *(f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) = S[t];
-        float *sy3 = sum + Sum<D>::STATE;
+        float *sy3 = sum + SM::STATE;
         constexpr int Y3N = Y3R * D;
         for (int e = tid; e < Y3N; e += NTH) sy3[e] = sm.y3[(e / D) * RS + e % D];
         if (tid < D) sy3[Y3N + tid] = y2reg;
@@ -427,13 +433,13 @@ __global__ __launch_bounds__(Pat<D>::NTH) void scan_kernel(const T *__restrict__
 
 // Several parts: out = (sum of the parts' F) / (sum of their G), g = that
 // sum; 16 tokens per workgroup, 16 threads per token, D/16 columns each.
-template <int D, typename T, bool DIV>
+template <int D, int P, typename T, bool DIV>
 __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ fpw,
                                                        const float *__restrict__ gpw,
                                                        T *__restrict__ out, float *__restrict__ g,
                                                        int N, int nblk)
 {
-    constexpr int NP = Pat<D>::NPART, CPT = D / 16;
+    constexpr int NP = Pat<D, P>::NPART, CPT = D / 16;
     static_assert(CPT % 4 == 0, "float4 columns");
     const int head = blockIdx.x / nblk, n = (blockIdx.x % nblk) * 16 + (threadIdx.x >> 4);
     const int cg = threadIdx.x & 15;
@@ -459,17 +465,17 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__
 
 // Workspace: segment sums (several segments), then the parts' F and G
 // (several parts).
-template <int D>
+template <int D, int P>
 struct Plan {
     int items, nch, nseg;
     size_t sum_bytes, fp_bytes, gp_bytes;
     Plan(int BH, int N)
     {
-        constexpr int NP = Pat<D>::NPART;
+        constexpr int NP = Pat<D, P>::NPART;
         items = BH * (D / SL) * NP;
         nch = (N + C - 1) / C;
         nseg = nseg_of(items, nch);
-        sum_bytes = nseg > 1 ? a256((size_t)items * nseg * Sum<D>::BYTES) : 0;
+        sum_bytes = nseg > 1 ? a256((size_t)items * nseg * Sum<D, P>::BYTES) : 0;
         fp_bytes = NP > 1 ? a256((size_t)BH * NP * N * D * 4) : 0;
         gp_bytes = NP > 1 ? a256((size_t)BH * NP * N * 4) : 0;
     }
@@ -478,100 +484,126 @@ struct Plan {
 
 // The forward (DV = false: O = F / G and G) or the backward's dv (DV = true:
 // q <- k, k <- q, v <- dout scaled by vsc = 1/G, the score scale on the keys).
-template <int D, typename T, bool DV>
+template <int D, typename T, bool DV, int P>
 hipError_t launch(const void *q, const void *k, const void *v, const float *vsc, void *out,
                   float *g, int BH, int N, int causal, float qs, float ks, void *ws, hipStream_t st)
 {
-    const Plan<D> pl(BH, N);
+    using PT = Pat<D, P>;
+    using SM = Sum<D, P>;
+    const Plan<D, P> pl(BH, N);
     const int items = pl.items, nseg = pl.nseg;
     if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
-    const dim3 grid((unsigned)(items * nseg));
+    const dim3 grid((unsigned)(items * nseg)), blk(PT::NTH);
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v;
     T *O = (T *)out;
     float *sums = nseg > 1 ? (float *)ws : nullptr;
     float *fpw = pl.fp_bytes ? (float *)((char *)ws + pl.sum_bytes) : nullptr;
     float *gpw = pl.gp_bytes ? (float *)((char *)ws + pl.sum_bytes + pl.fp_bytes) : nullptr;
-    const size_t stride = Sum<D>::BYTES / 4;
-    const dim3 pgrid((unsigned)((Sum<D>::FLOATS + 255) / 256), items);
+    const size_t stride = SM::BYTES / 4;
+    const dim3 pgrid((unsigned)((SM::FLOATS + 255) / 256), items);
     if (causal) {
         if (nseg > 1) {
-            hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K,
-                               V, O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
-            hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
+            hipLaunchKernelGGL((scan_kernel<D, T, true, DELTA, DV, P>), grid, blk, 0, st, Q, K, V,
+                               O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
+            hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, SM::FLOATS,
                                stride, 1);
         }
-        hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V, O,
-                           g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
+        hipLaunchKernelGGL((scan_kernel<D, T, true, SCAN, DV, P>), grid, blk, 0, st, Q, K, V, O, g,
+                           sums, fpw, gpw, vsc, N, nseg, qs, ks);
     } else if (nseg == 1) {
-        hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V,
-                           O, g, nullptr, fpw, gpw, vsc, N, nseg, qs, ks);
+        hipLaunchKernelGGL((scan_kernel<D, T, false, BOTH, DV, P>), grid, blk, 0, st, Q, K, V, O,
+                           g, nullptr, fpw, gpw, vsc, N, nseg, qs, ks);
     } else {
-        hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V,
-                           O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
-        hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, Sum<D>::FLOATS,
-                           stride, 0);
-        hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY, DV>), grid, dim3(Pat<D>::NTH), 0, st, Q, K, V,
-                           O, g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
+        hipLaunchKernelGGL((scan_kernel<D, T, false, DELTA, DV, P>), grid, blk, 0, st, Q, K, V, O,
+                           g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
+        hipLaunchKernelGGL(prefix_kernel, pgrid, dim3(256), 0, st, sums, nseg, SM::FLOATS, stride,
+                           0);
+        hipLaunchKernelGGL((scan_kernel<D, T, false, QUERY, DV, P>), grid, blk, 0, st, Q, K, V, O,
+                           g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
     }
-    if constexpr (Pat<D>::NPART > 1) {
+    if constexpr (PT::NPART > 1) {
         const int nblk = (N + 15) / 16;
         if ((long long)BH * nblk > INT_MAX) return hipErrorInvalidConfiguration;
-        hipLaunchKernelGGL((finalize_kernel<D, T, !DV>), dim3((unsigned)(BH * nblk)), dim3(256), 0,
-                           st, fpw, gpw, O, g, N, nblk);
+        hipLaunchKernelGGL((finalize_kernel<D, P, T, !DV>), dim3((unsigned)(BH * nblk)), dim3(256),
+                           0, st, fpw, gpw, O, g, N, nblk);
     }
     return hipGetLastError();
 }
 
+template <bool DV, typename T, int P>
+hipError_t launch_dt(const void *q, const void *k, const void *v, const float *vsc, void *out,
+                     float *g, int BH, int N, int D, int causal, float qs, float ks, void *ws,
+                     hipStream_t st)
+{
+    switch (D) {
+    case 16: return launch<16, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    case 32: return launch<32, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    case 64:
+        // bf16 D = 64, p = 2 has the fp16 MFMA kernels of its own
+        if constexpr (std::is_same<T, bf16_t>::value && P == 2) return hipErrorInvalidValue;
+        else return launch<64, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    case 128: return launch<128, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <bool DV>
 hipError_t launch_d(const void *q, const void *k, const void *v, const float *vsc, void *out,
-                    float *g, int BH, int N, int D, int causal, int is_bf16, float qs, float ks,
-                    void *ws, hipStream_t st)
+                    float *g, int BH, int N, int D, int p, int causal, int is_bf16, float qs,
+                    float ks, void *ws, hipStream_t st)
 {
-    if (is_bf16) {
-        if (D == 16) return launch<16, bf16_t, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-        if (D == 32) return launch<32, bf16_t, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-        if (D == 128) return launch<128, bf16_t, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-        return hipErrorInvalidValue;
-    }
-    if (D == 16) return launch<16, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-    if (D == 32) return launch<32, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-    if (D == 64) return launch<64, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-    if (D == 128) return launch<128, float, DV>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-    return hipErrorInvalidValue;
+    if (!f32mfma_applies(D, p, is_bf16)) return hipErrorInvalidValue;
+    if (is_bf16)
+        return p == 2 ? launch_dt<DV, bf16_t, 2>(q, k, v, vsc, out, g, BH, N, D, causal, qs, ks, ws, st)
+                      : launch_dt<DV, bf16_t, 1>(q, k, v, vsc, out, g, BH, N, D, causal, qs, ks, ws, st);
+    return p == 2 ? launch_dt<DV, float, 2>(q, k, v, vsc, out, g, BH, N, D, causal, qs, ks, ws, st)
+                  : launch_dt<DV, float, 1>(q, k, v, vsc, out, g, BH, N, D, causal, qs, ks, ws, st);
 }
 
 }  // namespace m32
 
 bool f32mfma_applies(int D, int p, int is_bf16)
 {
-    return p == 2 && (D == 16 || D == 32 || D == 128 || (D == 64 && !is_bf16));
+    const bool d_ok = D == 16 || D == 32 || D == 64 || D == 128;
+    if (p == 1) return d_ok;
+    return p == 2 && d_ok && !(D == 64 && is_bf16);
 }
 
-size_t f32mfma_fwd_workspace(int BH, int N, int D)
+size_t f32mfma_fwd_workspace(int BH, int N, int D, int p)
 {
     using namespace m32;
+    if (p == 1) {
+        switch (D) {
+        case 16: return Plan<16, 1>(BH, N).bytes();
+        case 32: return Plan<32, 1>(BH, N).bytes();
+        case 64: return Plan<64, 1>(BH, N).bytes();
+        case 128: return Plan<128, 1>(BH, N).bytes();
+        }
+        return 0;
+    }
     switch (D) {
-    case 16: return Plan<16>(BH, N).bytes();
-    case 32: return Plan<32>(BH, N).bytes();
-    case 64: return Plan<64>(BH, N).bytes();
-    case 128: return Plan<128>(BH, N).bytes();
+    case 16: return Plan<16, 2>(BH, N).bytes();
+    case 32: return Plan<32, 2>(BH, N).bytes();
+    case 64: return Plan<64, 2>(BH, N).bytes();
+    case 128: return Plan<128, 2>(BH, N).bytes();
     }
     return 0;
 }
 
 hipError_t f32mfma_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st)
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st)
 {
-    return m32::launch_d<false>(q, k, v, nullptr, out, g, BH, N, D, causal, is_bf16, qs, 1.0f, ws,
-                                st);
+    return m32::launch_d<false>(q, k, v, nullptr, out, g, BH, N, D, p, causal, is_bf16, qs, 1.0f,
+                                ws, st);
 }
 
 hipError_t f32mfma_dv(const void *q, const void *k, const void *dout, const float *rg, void *dv,
-                      int BH, int N, int D, int causal, int is_bf16, float qs, void *ws,
+                      int BH, int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
                       hipStream_t st)
 {
-    return m32::launch_d<true>(k, q, dout, rg, dv, nullptr, BH, N, D, causal, is_bf16, 1.0f, qs,
-                               ws, st);
+    return m32::launch_d<true>(k, q, dout, rg, dv, nullptr, BH, N, D, p, causal, is_bf16, 1.0f,
+                               qs, ws, st);
 }
 
 }  // namespace fm

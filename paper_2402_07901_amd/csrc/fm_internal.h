@@ -67,24 +67,27 @@ int set_scan_segment_mode(int mode);
 // chunks (reserved whenever nch >= 2, whatever the mode).
 size_t causal_scan_seg_workspace(int items, int nch);
 
-// Float32 MFMA forward (v_mfma_f32_16x16x4_f32): p = 2, D in {16, 32, 128}
-// for float32 and bf16 I/O, D = 64 for float32 I/O; causal and non-causal.
-// ws holds f32mfma_fwd_workspace(BH, N, D) bytes (segment sums; at D = 128
+// Float32 MFMA kernels (v_mfma_f32_16x16x4_f32): p = 1 for D in {16, 32, 64,
+// 128}; p = 2 for D in {16, 32, 128} with float32 or bf16 I/O and D = 64 with
+// float32 I/O; causal and non-causal.  The forward's ws holds
+// f32mfma_fwd_workspace(BH, N, D, p) bytes (segment sums; at D = 128, p = 2
 // the partial numerators and denominators).
 bool f32mfma_applies(int D, int p, int is_bf16);
-size_t f32mfma_fwd_workspace(int BH, int N, int D);
+size_t f32mfma_fwd_workspace(int BH, int N, int D, int p);
 hipError_t f32mfma_fwd(const void *q, const void *k, const void *v, void *out, float *g, int BH,
-                       int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st);
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st);
 // The backward's dv_n = sum_{i >= n (causal)} f(s_in) dO_i rg_i (rg = 1/G) on
 // the forward's kernels; ws as for the forward.
 hipError_t f32mfma_dv(const void *q, const void *k, const void *dout, const float *rg, void *dv,
-                      int BH, int N, int D, int causal, int is_bf16, float qs, void *ws,
+                      int BH, int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
                       hipStream_t st);
-// Float32 MFMA backward (same cases as the forward): dq, dk, dv.
-size_t f32mfma_bwd_workspace(int BH, int N, int D);
+// The backward (same cases as the forward): dq, dk, dv.
+size_t f32mfma_bwd_workspace(int BH, int N, int D, int p);
 hipError_t f32mfma_bwd(const void *q, const void *k, const void *v, const void *o,
                        const void *dout, const float *g, void *dq, void *dk, void *dv, int BH,
-                       int N, int D, int causal, int is_bf16, float qs, void *ws, hipStream_t st);
+                       int N, int D, int p, int causal, int is_bf16, float qs, void *ws,
+                       hipStream_t st);
 
 // MFMA causal scan: D = 64, p = 2, bf16 I/O.
 // ws holds mfma_causal_fwd_workspace(BH, N) bytes: q^ and k^ in fp16, then

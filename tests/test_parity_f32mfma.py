@@ -115,3 +115,60 @@ def test_f32mfma_d128_one_segment(BH, dtype, causal):
     assert ws == r256(B * H * 4 * N * 128 * 4) + r256(B * H * 4 * N * 4), ws
     inp = make_inputs(B, H, N, 128, 9600 + B, dtype)
     check(inp, causal, dtype, f"f32mfma D=128 one segment B={B} H={H} {dtype} causal={causal}")
+
+
+# ---------------------------------------------------------------------------
+# p = 1 (f = 1 + s: the linear tiles alone, G = n + q^.y2), every D and dtype.
+# Weights change sign and G_i may nearly cancel, so O is held to its
+# conditioning-scaled bar (gpu_util.row_scaled: |dO_ij| <= TOL kappa_i
+# (1 + kappa_i) max|v|, kappa_i = sum_n |w_in| / |G_i|) and G to TOL times
+# sum_n |w_in|.
+# ---------------------------------------------------------------------------
+def check_p1(inp, causal, dtype, label, scale=None):
+    import torch
+    from gpu_util import row_scaled
+    q, k, v = (to_dev(inp[n], dtype) for n in ("q", "k", "v"))
+    o, g = fm.fastmax_fwd(q, k, v, p=1, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    tau = 1.0 if scale is None else scale
+    ro, rg, rabs = oracle.fwd_brute(inp["q64"], inp["k64"], inp["v64"], 1, causal,
+                                    with_abs=True, scale=tau)
+    out = to_f64(o)
+    gg = g.cpu().numpy().astype(np.float64)
+    assert np.isfinite(out).all() and np.isfinite(gg).all(), label
+    e, nill = row_scaled(out, ro, rg, rabs, np.abs(inp["v64"]).max())
+    eg = float((np.abs(gg - rg) / rabs).max())
+    say(f"{label}: E_O/bound={e:.3e} E_G={eg:.3e} (rows with kappa > 10: {nill})")
+    assert e <= TOL[dtype] and eg <= TOL[dtype], (label, e, eg)
+
+
+P1_CASES = [(D, causal, dtype) for D in (16, 32, 64, 128) for causal in (False, True)
+            for dtype in ("f32", "bf16")]
+P1_SHAPES = [(1, 1, 1), (1, 2, 33), (2, 3, 100), (1, 1, 1000)]
+
+
+@pytest.mark.parametrize("shape", P1_SHAPES, ids=[f"B{b}H{h}N{n}" for b, h, n in P1_SHAPES])
+@pytest.mark.parametrize("case", P1_CASES, ids=[f"D{d}-{'causal' if c else 'noncausal'}-{t}" for d, c, t in P1_CASES])
+def test_f32mfma_p1_vs_brute(case, shape):
+    D, causal, dtype = case
+    B, H, N = shape
+    inp = make_inputs(B, H, N, D, 9150 + D + N + 7 * H, dtype)
+    check_p1(inp, causal, dtype, f"f32mfma p=1 D={D} causal={causal} {dtype} B={B} H={H} N={N}")
+
+
+@pytest.mark.parametrize("D", [16, 64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_f32mfma_p1_many_segments(D, causal):
+    """One head of 4000 tokens split into segments (p = 1)."""
+    inp = make_inputs(1, 1, 4000, D, 9350 + D, "f32")
+    check_p1(inp, causal, "f32", f"f32mfma p=1 segments D={D} causal={causal}")
+
+
+def test_f32mfma_p1_scale_and_lra_workload():
+    """The LRA-shaped p = 1 workload (B2 H4 N2048 D32, causal, f32) on every
+    row, and a scaled call (tau = 1/32)."""
+    w = WORKLOADS["lra_causal_f32_p1"]
+    inp = workload_inputs(w)
+    check_p1(inp, w.causal, w.dtype, f"{w.name} (every row)")
+    inp = make_inputs(1, 2, 300, 32, 9450, "f32")
+    check_p1(inp, True, "f32", "f32mfma p=1 tau=1/32", scale=1.0 / 32)

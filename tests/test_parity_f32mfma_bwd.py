@@ -123,3 +123,29 @@ def test_f32mfma_bwd_lra_workload():
         inp["dout"] = d64.astype(np.float32)
         inp["dout64"] = inp["dout"].astype(np.float64)
     check(inp, w.causal, w.dtype, w.name, heads=[(0, 0), (w.B - 1, w.H - 1)])
+
+
+# ---------------------------------------------------------------------------
+# p = 1 (f' = 1): every D and dtype, against the brute-force gradient with the
+# per-entry first-order rounding bounds of gpu_util.grad_bounds (weights
+# change sign and G_i may nearly cancel), through test_parity_gpu.bwd_case.
+# ---------------------------------------------------------------------------
+P1_BWD = [(D, causal, dtype) for D in (16, 32, 64, 128) for causal in (False, True)
+          for dtype in ("f32", "bf16")]
+
+
+@pytest.mark.parametrize("N", [1, 33, 100])
+@pytest.mark.parametrize("case", P1_BWD, ids=[f"D{d}-{'causal' if c else 'noncausal'}-{t}" for d, c, t in P1_BWD])
+def test_f32mfma_bwd_p1(case, N):
+    from test_parity_gpu import bwd_case
+    D, causal, dtype = case
+    inp = make_inputs(1, 2, N, D, 9750 + D + N, dtype, with_dout=True)
+    bwd_case(inp, 1, causal, dtype, label=f"f32mfma bwd p=1 D={D} causal={causal} {dtype} N={N}")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_f32mfma_bwd_p1_segments(causal):
+    """One head of 2000 tokens (63 chunks, up to 63 segments), p = 1."""
+    from test_parity_gpu import bwd_case
+    inp = make_inputs(1, 1, 2000, 32, 9850, "f32", with_dout=True)
+    bwd_case(inp, 1, causal, "f32", label=f"f32mfma bwd p=1 segments causal={causal}")
