@@ -38,9 +38,8 @@
  *  - Validation happens on the host before the first HIP call: on any error
  *    nothing is enqueued and nothing is written.
  *  - Supported: D in {16, 32, 64, 128} (fp16 MFMA kernels serve D = 64,
- *    p = 2, bf16; every other case runs on float32 MFMA kernels, except
- *    dropout and the bf16 D = 64 non-causal backward below 128 tokens, which
- *    run on float32 VALU kernels);
+ *    p = 2, bf16, except non-causal below 128 tokens; every other case runs
+ *    on float32 MFMA kernels, and the dropout calls on float32 VALU kernels);
  *    p in {1, 2}; causal in {0, 1};
  *    dt in {FASTMAX_F32, FASTMAX_BF16}; B, H, N >= 1 and B*H*N*D < 2^62.
  *  - A token whose q or k row is constant has std 0; its standardised row is

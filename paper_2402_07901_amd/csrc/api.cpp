@@ -66,9 +66,9 @@ bool mfma_causal(int D, int p, int causal, int dt)
     return D == 64 && p == 2 && causal && dt == FASTMAX_BF16;
 }
 
-// The float32 MFMA kernels (forward and backward) serve p = 1, and p = 2
-// wherever the fp16 MFMA kernels do not: float32 I/O for every D, bf16 I/O
-// for D != 64.
+// The float32 MFMA kernels (forward and backward) serve every case the fp16
+// MFMA kernels do not (p = 1; p = 2 with float32 I/O, with D != 64, or
+// non-causal below 128 tokens).
 bool f32mfma(int D, int p, int causal, int dt, int N)
 {
     if (mfma_causal(D, p, causal, dt) || mfma_noncausal(N, D, p, causal, dt)) return false;

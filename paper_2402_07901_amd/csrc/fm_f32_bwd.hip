@@ -636,10 +636,7 @@ hipError_t bwd_dt(const void *q, const void *k, const void *v, const void *o, co
     switch (D) {
     case 16: return bwd_run<16, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
     case 32: return bwd_run<32, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
-    case 64:
-        // bf16 D = 64, p = 2 has the fp16 MFMA kernels of its own
-        if constexpr (std::is_same<T, bf16_t>::value && P == 2) return hipErrorInvalidValue;
-        else return bwd_run<64, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
+    case 64: return bwd_run<64, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
     case 128: return bwd_run<128, T, P>(q, k, v, o, dout, g, dq, dk, dv, BH, N, causal, qs, ws, st);
     }
     return hipErrorInvalidValue;

@@ -538,10 +538,7 @@ hipError_t launch_dt(const void *q, const void *k, const void *v, const float *v
     switch (D) {
     case 16: return launch<16, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
     case 32: return launch<32, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
-    case 64:
-        // bf16 D = 64, p = 2 has the fp16 MFMA kernels of its own
-        if constexpr (std::is_same<T, bf16_t>::value && P == 2) return hipErrorInvalidValue;
-        else return launch<64, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
+    case 64: return launch<64, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
     case 128: return launch<128, T, DV, P>(q, k, v, vsc, out, g, BH, N, causal, qs, ks, ws, st);
     }
     return hipErrorInvalidValue;
@@ -564,9 +561,8 @@ hipError_t launch_d(const void *q, const void *k, const void *v, const float *vs
 
 bool f32mfma_applies(int D, int p, int is_bf16)
 {
-    const bool d_ok = D == 16 || D == 32 || D == 64 || D == 128;
-    if (p == 1) return d_ok;
-    return p == 2 && d_ok && !(D == 64 && is_bf16);
+    (void)is_bf16;   // every dtype (bf16 D = 64, p = 2 only where the fp16 kernels do not serve)
+    return (p == 1 || p == 2) && (D == 16 || D == 32 || D == 64 || D == 128);
 }
 
 size_t f32mfma_fwd_workspace(int BH, int N, int D, int p)

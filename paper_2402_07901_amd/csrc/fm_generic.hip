@@ -215,7 +215,8 @@ __device__ void contract_psi(const float *S, const float *x, float *out, const u
 #pragma unroll
         for (int j = 0; j < WS; ++j) acc[u][j] = 0.0f;
     // p = 2 with one row per thread: unrolled so several table reads are in flight
-#pragma unroll(P2 && RPT == 1 ? 4 : 1)
+    constexpr int UNROLL = P2 && RPT == 1 ? 4 : 1;
+#pragma unroll UNROLL
     for (int f = fg; f < P; f += NG) {
         const int a = P2 ? fa[f] : 0, b = P2 ? fb[f] : 0;
         const bool quad = f > D;

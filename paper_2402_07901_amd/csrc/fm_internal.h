@@ -67,9 +67,9 @@ int set_scan_segment_mode(int mode);
 // chunks (reserved whenever nch >= 2, whatever the mode).
 size_t causal_scan_seg_workspace(int items, int nch);
 
-// Float32 MFMA kernels (v_mfma_f32_16x16x4_f32): p = 1 for D in {16, 32, 64,
-// 128}; p = 2 for D in {16, 32, 128} with float32 or bf16 I/O and D = 64 with
-// float32 I/O; causal and non-causal.  The forward's ws holds
+// Float32 MFMA kernels (v_mfma_f32_16x16x4_f32): p in {1, 2}, D in {16, 32,
+// 64, 128}, float32 or bf16 I/O, causal and non-causal (dispatch sends bf16
+// D = 64 p = 2 here only where the fp16 MFMA kernels do not serve it).  The forward's ws holds
 // f32mfma_fwd_workspace(BH, N, D, p) bytes (segment sums; at D = 128, p = 2
 // the partial numerators and denominators).
 bool f32mfma_applies(int D, int p, int is_bf16);
