@@ -162,9 +162,9 @@ static __global__ __launch_bounds__(256) void prefix_kernel(float *__restrict__ 
     }
 }
 
-inline int nseg_of(int items, int nch)
+inline int nseg_of(int items, int nch, int target = TARGET_BLOCKS)
 {
-    int s = TARGET_BLOCKS / (items > 0 ? items : 1);
+    int s = target / (items > 0 ? items : 1);
     if (s < 1) s = 1;
     if (s > nch) s = nch;
     return s;

@@ -474,7 +474,8 @@ struct Plan {
         constexpr int NP = Pat<D, P>::NPART;
         items = BH * (D / SL) * NP;
         nch = (N + C - 1) / C;
-        nseg = nseg_of(items, nch);
+        // D <= 32: under 128 VGPRs, so two workgroups share a CU
+        nseg = nseg_of(items, nch, D <= 32 ? 2 * TARGET_BLOCKS : TARGET_BLOCKS);
         sum_bytes = nseg > 1 ? a256((size_t)items * nseg * Sum<D, P>::BYTES) : 0;
         fp_bytes = NP > 1 ? a256((size_t)BH * NP * N * D * 4) : 0;
         gp_bytes = NP > 1 ? a256((size_t)BH * NP * N * 4) : 0;

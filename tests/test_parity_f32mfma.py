@@ -94,9 +94,10 @@ def test_f32mfma_workloads_full(name):
 @pytest.mark.parametrize("D,dtype", [(16, "f32"), (32, "bf16")])
 def test_f32mfma_one_segment_per_head(D, dtype, causal):
     """Enough heads for one workgroup per (head, slice) (no segments, no
-    workspace): the non-causal totals and queries in one launch, the causal
-    scan from an empty state."""
-    B, H = (16, 16) if D == 16 else (8, 16)
+    workspace; at D <= 32 the plan aims at 512 workgroups, two per CU): the
+    non-causal totals and queries in one launch, the causal scan from an
+    empty state."""
+    B, H = (16, 32) if D == 16 else (16, 16)
     assert fm.workspace_bytes(B, H, 100, D, 2, causal, fm.F32 if dtype == "f32" else fm.BF16) == 0
     inp = make_inputs(B, H, 100, D, 9500 + D, dtype)
     check(inp, causal, dtype, f"f32mfma one segment D={D} {dtype} causal={causal}")
