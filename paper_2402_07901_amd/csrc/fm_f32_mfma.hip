@@ -17,9 +17,11 @@
 // lane and row quad): the linear tiles u (features k_l, l = 16u..16u+15) and
 // the quadratic tiles (m, u) for u >= m/16 (features k_m k_l): the diagonal
 // tiles u = m/16 hold both (m, l) and (l, m) and enter the query contraction
-// with weight 1/2, so psi(q).phi(k) = s + s^2/2.  Wave w owns the linear
-// tile u = w (w < D/16) and every quadratic tile of the channels
-// m = w + 4c: D/4 channels, 4 (D/16)(D/16 + 1)/2 tiles.
+// with weight 1/2, so psi(q).phi(k) = s + s^2/2.  Eight waves (two per
+// SIMD): wave w owns the linear tile u = w (w < D/16) and every quadratic
+// tile of the channels m = w + 8c (at D = 128, p = 2 the four workgroups of
+// a slice share the channels: m = gw + 32c over their 32 waves); at most 21
+// tiles per wave.
 //
 // MFMA lane layout (16x16x4 f32, lane = 16h + r16): A holds row r16, K index
 // h; B holds column r16, K index h; the accumulator holds column r16, rows
@@ -35,6 +37,9 @@
 // With one segment per (head, slice) a single launch does it all (non-causal:
 // the totals over every chunk, then every query; mode BOTH) and no workspace
 // is needed.
+//
+// DV mode: the backward's dv (the same scan over the reversed sequence with
+// queries and keys exchanged, values dO/G, no denominator).
 #include <hip/hip_runtime.h>
 
 #include <limits.h>
