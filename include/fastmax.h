@@ -264,7 +264,7 @@ const char *fastmax_version(void);
  * head of up to 260594 tokens, or up to 46 heads of 4096 tokens; the D = 128,
  * p = 2 forward keeps four partial float32 numerators per token, about 2 KB
  * per token and head, and takes 8 heads of up to 4064 tokens, or one head of
- * up to 9049).  The call allocates nothing (no hipMalloc, no library
+ * up to 11081).  The call allocates nothing (no hipMalloc, no library
  * allocation);
  * the first call on a GPU looks the array's device address up once
  * (FASTMAX_EHIP if HIP refuses).  Every call on one GPU shares that GPU's

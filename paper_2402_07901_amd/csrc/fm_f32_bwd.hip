@@ -290,7 +290,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                     for (int i = 0; i < 4; ++i) Tq[i] *= zs;
                 }
                 // quadratic tiles by output block u, from the last block down: tile
-                // (m, u) of channel m = gw + NGW cc adds Z_m T[l] to out[l], l in
+                // (m, u) of the wave's channel m = chan(cc) adds Z_m T[l] to out[l], l in
                 // block u, and (off the diagonal) sum_l Z_l T[l] to out[m], which is
                 // complete when the loop reaches m's own block u0
                 float dmv[NCH];
@@ -305,7 +305,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                         constexpr int u0 = PT::u0(cc, GH);
                         if constexpr (u >= u0) {
                             constexpr int t = PT::first(cc, GH) + u - u0;
-                            const float zm = zr[gw + NGW * cc];
+                            const float zm = zr[PT::chan(cc, GH, gw)];
                             f4 Tt = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                             for (int i = 0; i < 4; ++i) Tt = mma(S[t][i], ub[i], Tt);
@@ -320,7 +320,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                             float dm = dmv[cc];
                             dm += __shfl_xor(dm, 16);
                             dm += __shfl_xor(dm, 32);
-                            const int ml = (gw + NGW * cc) & 15;
+                            const int ml = PT::chan(cc, GH, gw) & 15;
 #pragma unroll
                             for (int i = 0; i < 4; ++i)
                                 if (h == (ml >> 2) && i == (ml & 3)) a4[i] += dm;
@@ -374,7 +374,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
             static_for<0, NCQ>([&](auto ci) {
                 constexpr int cc = decltype(ci)::value;
                 constexpr int u0 = PT::u0(cc, GH);
-                const float *xm = sm.xT + (gw + NGW * cc) * TS + h;
+                const float *xm = sm.xT + PT::chan(cc, GH, gw) * TS + h;
                 float Bm[C / 4];
 #pragma unroll
                 for (int ks = 0; ks < C / 4; ++ks) Bm[ks] = xm[4 * ks] * Vb[ks];

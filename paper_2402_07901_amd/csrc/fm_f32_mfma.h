@@ -57,11 +57,17 @@ struct Pat {
     static constexpr int NU = D / 16;                  // 16-channel blocks
     static constexpr int NGW = NW * NPART;             // waves over the parts
     static constexpr int NCH = D / NGW;                // channels per wave
-    // Block of channel m = gw + NGW c (gw < NGW): NGW c / 16 while 16 is a
-    // multiple of NGW; beyond 16 waves, NGW/16 c + gw/16, where the wave
-    // class gw/16 is the same for every wave of a workgroup.
+    // Block u0 of the wave's c-th channel.  Up to 16 waves: channel
+    // m = gw + NGW c, in block NGW c / 16.  With 32 waves (two wave classes
+    // gh = gw / 16, one per pair of workgroups) wave gw takes channel
+    // 16 u0 + gw % 16 of block u0 = 2c + ((c & 1) ^ gh): blocks 0, 3, 4, 7
+    // for class 0 and 1, 2, 5, 6 for class 1, so that both classes hold the
+    // same number of tiles (sum over c of NU - u0); the plain order 2c + gh
+    // would give class 0 NCH more tiles than class 1, and the workgroups of
+    // that class would set the pace.
     static constexpr int NH = NGW > 16 ? NGW / 16 : 1;  // wave classes
-    static constexpr int u0(int c, int gh) { return NGW >= 16 ? (NGW / 16) * c + gh : NGW * c / 16; }
+    static constexpr int u0(int c, int gh) { return NGW > 16 ? 2 * c + ((c & 1) ^ gh) : NGW * c / 16; }
+    __device__ static int chan(int c, int gh, int gw) { return NGW > 16 ? 16 * u0(c, gh) + (gw & 15) : gw + NGW * c; }
     // first tile of channel c (its diagonal tile; u runs from u0 to NU-1)
     static constexpr int first(int c, int gh)
     {
@@ -69,8 +75,8 @@ struct Pat {
         for (int cc = 0; cc < c; ++cc) t += NU - u0(cc, gh);
         return t;
     }
-    // quadratic tiles per wave (class 0 has the most)
-    static constexpr int NQ = P == 2 ? first(NCH, 0) - 1 : 0;
+    // quadratic tiles per wave (the larger class)
+    static constexpr int NQ = P != 2 ? 0 : first(NCH, 0) > first(NCH, NH - 1) ? first(NCH, 0) - 1 : first(NCH, NH - 1) - 1;
     static constexpr int NT = 1 + NQ;                  // + the linear slot
     static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
     static constexpr int Y3R = P == 2 ? 16 * NLB : 0;  // Y3 rows per part
@@ -79,7 +85,7 @@ struct Pat {
     static constexpr int NY3 = P != 2 ? 0 : NPART == 1 ? NU * (NU + 1) / 2 : NLB * NU;
     static constexpr int RS = D + 2;   // row stride of row-major tiles (floats)
     static constexpr int TS = C + 2;   // row stride of transposed tiles
-    static_assert(NGW <= 16 ? 16 % NGW == 0 : NGW % 16 == 0 && NH <= 2, "channel blocks");
+    static_assert(NGW <= 16 ? 16 % NGW == 0 : NGW == 32 && NCH % 2 == 0, "channel blocks");
     static_assert(LPT * C == NTH && DP * LPT == D && VPL * LPT == SL, "staging");
 };
 

@@ -20,8 +20,10 @@
 // with weight 1/2, so psi(q).phi(k) = s + s^2/2.  Eight waves (two per
 // SIMD): wave w owns the linear tile u = w (w < D/16) and every quadratic
 // tile of the channels m = w + 8c (at D = 128, p = 2 the four workgroups of
-// a slice share the channels: m = gw + 32c over their 32 waves); at most 21
-// tiles per wave.
+// a slice share the channels over their 32 waves gw, four channels each,
+// from blocks chosen so that every wave holds 18 quadratic tiles); at most
+// 21 tiles per wave.  The query contraction sums S[(m, l)] q^_l over the
+// tiles of channel m before it multiplies by q^_m.
 //
 // MFMA lane layout (16x16x4 f32, lane = 16h + r16): A holds row r16, K index
 // h; B holds column r16, K index h; the accumulator holds column r16, rows
@@ -133,18 +135,16 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
 #pragma unroll
     for (int t = 0; t < NT; ++t)
         S[t] = loaded ? *(const f4 *)(sum + ((size_t)(w * NT + t) * 64 + lane) * 4) : f4{0.f, 0.f, 0.f, 0.f};
-    float y2reg = 0.f, x1reg = 0.f;   // thread d < D: y2[d]; D <= tid < D + SL: x1[tid - D]
+    // thread tid < D keeps y2[tid], D <= tid < D + SL keeps x1[tid - D]
+    // (one register for both roles: the sums lie side by side after Y3)
+    float colsum = 0.f;
     {
         const float *sy3 = loaded ? sum + SM::STATE : nullptr;
         constexpr int Y3N = Y3R * D;
         for (int e = tid; e < Y3N; e += NTH) sm.y3[(e / D) * RS + e % D] = loaded ? sy3[e] : 0.f;
-        if (tid < D) {
-            y2reg = loaded ? sy3[Y3N + tid] : 0.f;
-            sm.y2s[tid] = 2.0f * y2reg;
-        } else if (tid < D + SL) {
-            x1reg = loaded ? sy3[Y3N + D + (tid - D)] : 0.f;
-            sm.x1[tid - D] = x1reg;
-        }
+        if (tid < D + SL) colsum = loaded ? sy3[Y3N + tid] : 0.f;
+        if (tid < D) sm.y2s[tid] = 2.0f * colsum;
+        else if (tid < D + SL) sm.x1[tid - D] = colsum;
     }
     // Y3 accumulator tiles of this wave, tile index yi = w + 4 kk: one part
     // takes the pairs (u, u2), u <= u2, in row order; with several parts,
@@ -245,14 +245,22 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                     static_for<0, NCQ>([&](auto ci) {
                         constexpr int cc = decltype(ci)::value;
                         constexpr int u0 = PT::u0(cc, GH);
-                        const float qm = qr[gw + NGW * cc];
+                        // sum over l of S[(m, l)] q_l first (the diagonal tile, holding
+                        // both (m, l) and (l, m), apart at half weight), then times
+                        // q_m: one multiply per channel instead of one per MFMA
+                        const float qm = qr[PT::chan(cc, GH, gw)];
+                        f4 Fd = {0.f, 0.f, 0.f, 0.f}, Fo = {0.f, 0.f, 0.f, 0.f};
                         static_for<u0, NU>([&](auto ui) {
                             constexpr int u = decltype(ui)::value;
                             constexpr int t = PT::first(cc, GH) + u - u0;
-                            const float qmw = (u == u0) ? 0.5f * qm : qm;
     #pragma unroll
-                            for (int i = 0; i < 4; ++i) F = mma(S[t][i], qmw * ql[u][i], F);
+                            for (int i = 0; i < 4; ++i) {
+                                if constexpr (u == u0) Fd = mma(S[t][i], ql[u][i], Fd);
+                                else Fo = mma(S[t][i], ql[u][i], Fo);
+                            }
                         });
+    #pragma unroll
+                        for (int i = 0; i < 4; ++i) F[i] = fmaf(qm, fmaf(0.5f, Fd[i], Fo[i]), F[i]);
                     });
                     if constexpr (M == SCAN && CAUSAL) {
                         // in-chunk blocks of row tile rt (wave rt): the key tiles
@@ -361,7 +369,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                 static_for<0, NCQ>([&](auto ci) {
                     constexpr int cc = decltype(ci)::value;
                     constexpr int u0 = PT::u0(cc, GH);
-                    const float *km = sm.kT + (gw + NGW * cc) * TS + h;
+                    const float *km = sm.kT + PT::chan(cc, GH, gw) * TS + h;
                     float Bm[C / 4];
     #pragma unroll
                     for (int ks = 0; ks < C / 4; ++ks) Bm[ks] = km[4 * ks] * Vb[ks];
@@ -385,13 +393,13 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                         float s = 0.f;
     #pragma unroll 8
                         for (int t = 0; t < C; ++t) s += sm.krow[t * RS + tid];
-                        y2reg += s;
+                        colsum += s;
                     }
                 } else if (tid < D + SL) {
                     float s = 0.f;
     #pragma unroll 8
                     for (int t = 0; t < C; ++t) s += sm.vrow[t * SL + tid - D];
-                    x1reg += s;
+                    colsum += s;
                 }
                 __syncthreads();
                 // the prefix after this chunk, for the next chunk's outputs
@@ -405,8 +413,8 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                         if (NPART == 1) sm.y3[m * RS + l] = Y[kk][i];
                     }
                 }
-                if (tid < D) sm.y2s[tid] = 2.0f * y2reg;
-                else if (tid < D + SL) sm.x1[tid - D] = x1reg;
+                if (tid < D) sm.y2s[tid] = 2.0f * colsum;
+                else if (tid < D + SL) sm.x1[tid - D] = colsum;
             }
             __syncthreads();
     };
@@ -431,8 +439,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
         float *sy3 = sum + SM::STATE;
         constexpr int Y3N = Y3R * D;
         for (int e = tid; e < Y3N; e += NTH) sy3[e] = sm.y3[(e / D) * RS + e % D];
-        if (tid < D) sy3[Y3N + tid] = y2reg;
-        else if (tid < D + SL) sy3[Y3N + D + (tid - D)] = x1reg;
+        if (tid < D + SL) sy3[Y3N + tid] = colsum;
     }
 }
 

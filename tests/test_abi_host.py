@@ -316,8 +316,8 @@ def test_fwd_noalloc_rejects_problems_beyond_its_scratch():
     # and the D = 128 p = 2 ones (four partial numerators per token)
     assert fm.workspace_bytes(1, 8, 4064, 128, 2, 1, fm.BF16) <= lim
     assert fm.workspace_bytes(1, 8, 4065, 128, 2, 1, fm.BF16) > lim
-    assert fm.workspace_bytes(1, 1, 9049, 128, 2, 1, fm.BF16) <= lim
-    assert fm.workspace_bytes(1, 1, 9050, 128, 2, 1, fm.BF16) > lim
+    assert fm.workspace_bytes(1, 1, 11081, 128, 2, 1, fm.BF16) <= lim
+    assert fm.workspace_bytes(1, 1, 11082, 128, 2, 1, fm.BF16) > lim
 
 
 def test_scan_segment_mode_setter():
