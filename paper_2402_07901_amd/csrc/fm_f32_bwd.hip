@@ -36,7 +36,7 @@
 // also adds sum_l Z_tl T[l] to out_t[m].  Each wave folds all its terms for
 // one 16-feature block into registers and stores the block once into its own
 // LDS region (LDS float atomics, measured, cost more than the MFMAs); the
-// chunk's rows, summed over the four regions, are added to the float32
+// chunk's rows, summed over the eight regions, are added to the float32
 // gradient with global float atomics (the column slices and feature parts of
 // a head add into the same rows).
 #include <hip/hip_runtime.h>
@@ -66,7 +66,7 @@ struct alignas(16) GSmem {
     float zt[C];                   // contraction scalars z
     float y3[(P == 2 ? 16 : 1) * Pat<D, P>::RS];   // the item's row block of Y3w (p = 2)
     float y2[P == 2 ? 16 : D];     // its entries of y2w (p = 1: all of y2w)
-    float ob[Pat<D, P>::NW][D * (out_tokens<D, P>() + 4)];   // each wave's outputs [feature][token]
+    alignas(16) float ob[Pat<D, P>::NW][D * (out_tokens<D, P>() + 4)];   // each wave's outputs [feature][token]
 };
 
 // Segment summary: [wave][tile][lane] f4 state, the Y3w row block [16][D]
@@ -213,13 +213,20 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
         const int n0 = c * C;
         // the waves' output blocks of tokens t0 .. t0 + FT - 1 (summed) into
         // the float32 gradient
+        // (a thread takes feature d of four consecutive tokens: one 16-byte
+        // LDS read per wave region, lanes 80 or 144 bytes apart, which is
+        // conflict-free; consecutive lanes add to consecutive features of a row)
         auto flush = [&](int t0) {
-            for (int e = tid; e < FT * D; e += NTH) {
-                const int t = e / D, d = e % D, n = n0 + t0 + t;
-                float val = 0.f;
+            for (int e = tid; e < (FT / 4) * D; e += NTH) {
+                const int j4 = e / D, d = e % D, o = d * OS + 4 * j4;
+                f4 val = *(const f4 *)&sm.ob[0][o];
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) val += sm.ob[ww][d * OS + t];
-                if (n < N) atomicAdd(outh + (size_t)(REV ? N - 1 - n : n) * D + d, val);
+                for (int ww = 1; ww < NW; ++ww) val += *(const f4 *)&sm.ob[ww][o];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int n = n0 + t0 + 4 * j4 + j;
+                    if (n < N) atomicAdd(outh + (size_t)(REV ? N - 1 - n : n) * D + d, val[j]);
+                }
             }
         };
         stage();
