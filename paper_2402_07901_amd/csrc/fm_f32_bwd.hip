@@ -244,12 +244,6 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                 float ub[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) ub[i] = sm.uc[tok * SL + 4 * h + i];
-                // linear tile: out[l] += sum_c UC_c L[l][c], l in block gw
-                f4 Tl = {0.f, 0.f, 0.f, 0.f};
-                if (gw < NU) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) Tl = mma(S[0][i], ub[i], Tl);
-                }
                 // in-chunk pairs: key tile st <= rt on wave b of the owning part;
                 // the weights here, their products with X by output block below
                 float Wt[2][4] = {};
@@ -281,21 +275,9 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                         }
                     }
                 }
-                // the item's Y3w block: out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
-                // (p = 1: out[l] += z_t y2w[l], every block)
-                f4 Tq = {0.f, 0.f, 0.f, 0.f};
+                // the item's Y3w block (wave NW - 1; p = 1: z_t y2w[l] to every block)
                 const bool yw = ylb >= 0 && w == NW - 1;
                 const float zst = sm.zt[tok];
-                if (P == 2 && yw) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
-                    const float *yr = sm.y3 + r16 * RS;
-#pragma unroll
-                    for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], zr[4 * kk + h], Tq);
-                    const float zs = sm.zt[tok];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) Tq[i] *= zs;
-                }
                 // quadratic tiles by output block u, from the last block down: tile
                 // (m, u) of the wave's channel m = chan(cc) adds Z_m T[l] to out[l], l in
                 // block u, and (off the diagonal) sum_l Z_l T[l] to out[m], which is
@@ -333,8 +315,6 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                                 if (h == (ml >> 2) && i == (ml & 3)) a4[i] += dm;
                         }
                     });
-                    if (gw == u) a4 += Tl;
-                    if (P == 2 && yw && ylb == u) a4 += Tq;
                     if (P == 1 && yw) {
 #pragma unroll
                         for (int i = 0; i < 4; ++i) a4[i] = fmaf(zst, sm.y2[16 * u + 4 * h + i], a4[i]);
@@ -352,6 +332,28 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
 #pragma unroll
                     for (int i = 0; i < 4; ++i) ocol[(16 * u + 4 * h + i) * OS] = a4[i];
                 });
+                // terms of a single block, added to the wave's stored block (rather
+                // than selected into every block's registers):
+                // the linear tile, out[l] += sum_c UC_c L[l][c] for l in block gw
+                if (gw < NU) {
+                    f4 Tl = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) Tl = mma(S[0][i], ub[i], Tl);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) ocol[(16 * gw + 4 * h + i) * OS] += Tl[i];
+                }
+                // and the Y3w block, out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
+                // for l in block ylb
+                if (P == 2 && yw) {
+                    f4 Tq;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
+                    const float *yr = sm.y3 + r16 * RS;
+#pragma unroll
+                    for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], zr[4 * kk + h], Tq);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) ocol[(16 * ylb + 4 * h + i) * OS] += zst * Tq[i];
+                }
                 if constexpr (FT == 16) {
                     __syncthreads();
                     flush(16 * rt);
