@@ -163,28 +163,39 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
     // ---- staging: token tg = tid / 8, channels 8-way split, 2 columns ---
     const int tg = tid / LPT, part = tid % LPT;
     constexpr int DP = PT::DP;
-    float px[DP], pz[DP], pvs[VPL], puc[VPL], pw = 0.f, pzs = 0.f;
+    // the next chunk's rows, raw (converted when staged, so that the loads
+    // overlap the current chunk)
+    RawRow<T, DP> rx, rz;
+    RawRow<T, VPL> rvs, ruc;
+    float rvm = 1.f, rum = 1.f, pw = 0.f, pzv = 0.f;
     bool pvalid = false;
     auto prefetch = [&](int c) {
         const int n0 = c * C + tg;
         pvalid = n0 < N;
         const int n = REV ? N - 1 - n0 : n0;   // the token's place in memory
-#pragma unroll
-        for (int i = 0; i < DP; ++i) {
-            px[i] = pvalid ? io<T>::ld(X, (size_t)n * D + part * DP + i) : 0.f;
-            pz[i] = pvalid ? io<T>::ld(Z, (size_t)n * D + part * DP + i) : 0.f;
+        rx.load(X + (size_t)n * D + part * DP, pvalid);
+        rz.load(Z + (size_t)n * D + part * DP, pvalid);
+        const size_t e = (size_t)n * D + SL * sl + VPL * part;
+        rvs.load(VS + e, pvalid);
+        ruc.load(UC + e, pvalid);
+        rvm = 1.f;
+        rum = 1.f;
+        pw = pvalid ? 1.f : 0.f;
+        pzv = pvalid ? 1.f : 0.f;
+        if (pvalid) {
+            if (vsm) rvm = vsm[n];
+            if (ucm) rum = ucm[n];
+            if (wv) pw = wv[n];
+            if (zv) pzv = zv[n];
         }
-        const float vm = vsm && pvalid ? vsm[n] : 1.0f, um = ucm && pvalid ? ucm[n] : 1.0f;
-#pragma unroll
-        for (int i = 0; i < VPL; ++i) {
-            const size_t e = (size_t)n * D + SL * sl + VPL * part + i;
-            pvs[i] = pvalid ? io<T>::ld(VS, e) * vm : 0.f;
-            puc[i] = pvalid ? io<T>::ld(UC, e) * um : 0.f;
-        }
-        pw = pvalid ? (wv ? wv[n] : 1.0f) : 0.f;
-        pzs = pvalid ? -(zv ? zv[n] : 1.0f) : 0.f;
     };
     auto stage = [&]() {
+        float px[DP], pz[DP];
+#pragma unroll
+        for (int i = 0; i < DP; ++i) {
+            px[i] = rx.get(i);
+            pz[i] = rz.get(i);
+        }
         standardise_part<D>(px, pvalid, xs);
         standardise_part<D>(pz, pvalid, zsc);
 #pragma unroll
@@ -196,12 +207,12 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
         }
 #pragma unroll
         for (int i = 0; i < VPL; ++i) {
-            sm.vs[tg * SL + VPL * part + i] = pvs[i];
-            sm.uc[tg * SL + VPL * part + i] = puc[i];
+            sm.vs[tg * SL + VPL * part + i] = rvs.get(i) * rvm;
+            sm.uc[tg * SL + VPL * part + i] = ruc.get(i) * rum;
         }
         if (part == 0) {
             sm.wt[tg] = pw;
-            sm.zt[tg] = pzs;
+            sm.zt[tg] = pvalid ? -pzv : 0.f;
         }
     };
 

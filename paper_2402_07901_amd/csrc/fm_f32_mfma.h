@@ -103,17 +103,73 @@ __device__ __forceinline__ void with_wave_class(int gw, F &&f)
 
 enum Mode { DELTA = 0, SCAN = 1, QUERY = 2, BOTH = 3 };
 
+// NE consecutive elements of T (bf16 or float) as raw 32-bit words, loaded as
+// one access of their size (the rows are 16-byte aligned and NE * sizeof(T)
+// divides the row) and converted to float only where they are used: a
+// prefetch into these registers does not wait for its loads.
+template <typename T, int NE>
+struct RawRow {
+    static constexpr int BYTES = NE * (int)sizeof(T);
+    static constexpr int NWD = BYTES < 4 ? 1 : BYTES / 4;
+    static_assert(BYTES == 2 || BYTES == 4 || BYTES == 8 || BYTES % 16 == 0, "row piece");
+    uint32_t w[NWD];
+    __device__ __forceinline__ void load(const T *p, bool valid)
+    {
+        if constexpr (BYTES == 2) {
+            w[0] = 0u;
+            if (valid) w[0] = *(const uint16_t *)p;
+        } else if constexpr (BYTES == 4) {
+            w[0] = 0u;
+            if (valid) w[0] = *(const uint32_t *)p;
+        } else if constexpr (BYTES == 8) {
+            uint2 x = make_uint2(0u, 0u);
+            if (valid) x = *(const uint2 *)p;
+            w[0] = x.x;
+            w[1] = x.y;
+        } else {
+#pragma unroll
+            for (int j = 0; j < BYTES / 16; ++j) {
+                uint4 x = make_uint4(0u, 0u, 0u, 0u);
+                if (valid) x = ((const uint4 *)p)[j];
+                w[4 * j] = x.x;
+                w[4 * j + 1] = x.y;
+                w[4 * j + 2] = x.z;
+                w[4 * j + 3] = x.w;
+            }
+        }
+    }
+    // element i (a compile-time index after unrolling)
+    __device__ __forceinline__ float get(int i) const
+    {
+        if constexpr (sizeof(T) == 4) return __uint_as_float(w[i]);
+        else return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
+    }
+};
+
+// Sum over an aligned row of 16 lanes, in every lane, with DPP moves (no LDS
+// round trip): swap neighbours, swap pairs, mirror the quads of each half
+// row, mirror the half rows.
+__device__ __forceinline__ float row16_sum(float x)
+{
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, true));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, true));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, true));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, true));
+    return x;
+}
+
 // Standardises the channels this thread holds of its token (Sec. 2.2, Eqs.
-// 6-7: population std, no epsilon; LPT lanes per token) and scales them.
+// 6-7: population std, no epsilon; the token's LPT = 16 lanes form one DPP
+// row) and scales them.  Every lane of the wave must take part.
 template <int D>
 __device__ __forceinline__ void standardise_part(float (&x)[Pat<D>::DP], bool valid, float scale)
 {
-    constexpr int DP = Pat<D>::DP, LPT = Pat<D>::LPT;
+    constexpr int DP = Pat<D>::DP;
+    static_assert(Pat<D>::LPT == 16, "one DPP row per token");
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < DP; ++i) s += x[i];
-#pragma unroll
-    for (int o = 1; o < LPT; o <<= 1) s += __shfl_xor(s, o);
+    s = row16_sum(s);
     const float mu = s * (1.0f / D);
     float v = 0.f;
 #pragma unroll
@@ -121,8 +177,7 @@ __device__ __forceinline__ void standardise_part(float (&x)[Pat<D>::DP], bool va
         x[i] -= mu;
         v = fmaf(x[i], x[i], v);
     }
-#pragma unroll
-    for (int o = 1; o < LPT; o <<= 1) v += __shfl_xor(v, o);
+    v = row16_sum(v);
     const float r = valid ? __builtin_amdgcn_rsqf(v * (1.0f / D)) * scale : 0.0f;
 #pragma unroll
     for (int i = 0; i < DP; ++i) x[i] *= r;

@@ -184,24 +184,30 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
     const int tg = tid / LPT, part = tid % LPT;
     constexpr int DP = PT::DP;
     // the next chunk's rows are loaded into registers while the current one
-    // is processed
-    float pq[DP], pk[DP], pv[VPL];
+    // is processed (raw, converted when staged)
+    RawRow<T, DP> rq, rk;
+    RawRow<T, VPL> rv;
+    float rvm = 1.0f;
     bool pvalid = false;
     auto prefetch = [&](int c) {
         const int n0 = c * C + tg;
         pvalid = n0 < N;
         const int n = DV ? N - 1 - n0 : n0;   // the token's place in memory
-#pragma unroll
-        for (int i = 0; i < DP; ++i) {
-            pq[i] = pvalid ? io<T>::ld(q, (size_t)n * D + part * DP + i) : 0.f;
-            pk[i] = pvalid ? io<T>::ld(k, (size_t)n * D + part * DP + i) : 0.f;
+        rq.load(q + (size_t)n * D + part * DP, pvalid);
+        rk.load(k + (size_t)n * D + part * DP, pvalid);
+        rv.load(v + (size_t)n * D + SL * sl + VPL * part, pvalid);
+        if (DV) {
+            rvm = 1.0f;
+            if (pvalid) rvm = vsc[n];
         }
-        const float vm = DV && pvalid ? vsc[n] : 1.0f;
-#pragma unroll
-        for (int i = 0; i < VPL; ++i)
-            pv[i] = pvalid ? io<T>::ld(v, (size_t)n * D + SL * sl + VPL * part + i) * vm : 0.f;
     };
     auto stage = [&]() {
+        float pq[DP], pk[DP];
+#pragma unroll
+        for (int i = 0; i < DP; ++i) {
+            pq[i] = rq.get(i);
+            pk[i] = rk.get(i);
+        }
         standardise_part<D>(pq, pvalid, qs);
         standardise_part<D>(pk, pvalid, ks);
 #pragma unroll
@@ -212,7 +218,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
             sm.kT[ch * TS + tg] = pk[i];
         }
 #pragma unroll
-        for (int i = 0; i < VPL; ++i) sm.vrow[tg * SL + VPL * part + i] = pv[i];
+        for (int i = 0; i < VPL; ++i) sm.vrow[tg * SL + VPL * part + i] = DV ? rv.get(i) * rvm : rv.get(i);
     };
 
     // one chunk in mode M (DELTA: state update only; QUERY: outputs only;
