@@ -255,15 +255,17 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                 rr[u] = 0.0f;
                 if (p < 2 * N) {
                     raw[u] = *(const uint4 *)(v + (size_t)n * D + SL * sl + 8 * hh);
-                    rr[u] = DV ? fabsf(rg[n]) : 1.0f;
+                    // raw: no arithmetic on a loaded value before all U are issued
+                    rr[u] = DV ? rg[n] : 1.0f;
                 }
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 float x[8];
                 bf16x8_to_f32(raw[u], x);
+                const float ar = fabsf(rr[u]);
 #pragma unroll
-                for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * rr[u]);
+                for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * ar);
             }
         }
 #pragma unroll

@@ -156,15 +156,17 @@ __global__ __launch_bounds__(NTH, 2) void nc_moments(const void *__restrict__ ki
             rr[u] = 1.0f;
             if (p < 4 * t1) {
                 raw[u] = *(const uint4 *)(v + (size_t)n * D + MSW * sl + 8 * qq);
-                if (vrow) rr[u] = fabsf(vrow[n]);
+                // raw: no arithmetic on a loaded value before all U are issued
+                if (vrow) rr[u] = vrow[n];
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             float x[8];
             bf16x8_to_f32(raw[u], x);
+            const float ar = fabsf(rr[u]);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * rr[u]);
+            for (int i = 0; i < 8; ++i) vmax = fmaxf(vmax, fabsf(x[i]) * ar);
         }
     }
 #pragma unroll
