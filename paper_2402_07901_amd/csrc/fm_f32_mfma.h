@@ -79,6 +79,11 @@ struct Pat {
     static constexpr int NQ = P != 2 ? 0 : first(NCH, 0) > first(NCH, NH - 1) ? first(NCH, 0) - 1 : first(NCH, NH - 1) - 1;
     static constexpr int NT = 1 + NQ;                  // + the linear slot
     static constexpr int NLB = NU / NPART;             // Y3 row blocks per part
+    // the denominator's contraction over each Y3 row block: split over KQ
+    // waves by K range where one workgroup holds two blocks of 128 channels
+    // (every wave takes a share), else on the last NLB waves whole
+    static constexpr int KQ = (P == 2 && NPART > 1) ? NW / NLB : 1;
+    static constexpr int NGI = NLB * KQ;               // partial sums per token
     static constexpr int Y3R = P == 2 ? 16 * NLB : 0;  // Y3 rows per part
     // Y3 tiles per part: one part keeps the blocks u <= u2 and mirrors them,
     // several parts keep full rows

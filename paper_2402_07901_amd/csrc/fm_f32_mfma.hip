@@ -64,7 +64,7 @@ struct Smem {
     float x1[SL];                   // x1 prefix
     f4 fpart[Pat<D, P>::NW][C / 16][64];   // partial F^T of the waves
     float gin[C];                   // in-chunk row sums
-    float gint[Pat<D, P>::NLB][C];  // partial q^T(Y3 q^ + 2 y2) per l block (p = 1: 2 q^.y2)
+    float gint[Pat<D, P>::NGI][C];  // partial q^T(Y3 q^ + 2 y2) per l block and K range (p = 1: 2 q^.y2)
 };
 
 // summary of a segment: [wave][tile][lane] f4 state, the part's Y3 rows
@@ -126,8 +126,11 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, h = lane >> 4;
     const int gw = pp * NW + w;   // wave index over the parts
-    // waves holding a Y3 row block for the denominator: the last NLB
-    const int lbl = w - (NW - NLB), lb = LB0 + lbl;
+    // waves holding a Y3 row block (and K range kq) for the denominator:
+    // the last NLB, or all of them with KQ per block
+    constexpr int KQ = PT::KQ;
+    const int lbl = KQ > 1 ? w / KQ : w - (NW - NLB), lb = LB0 + lbl;
+    const int kq = KQ > 1 ? w % KQ : 0, gslot = KQ > 1 ? w : lbl;
 
     // ---- state, prefix sums and Y3 -------------------------------------
     f4 S[NT];
@@ -300,24 +303,25 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                         }
                     }
                     sm.fpart[w][rt][lane] = F;
-                    // denominator: q^T (Y3 q + 2 y2) over l block lb (p = 1: 2 q.y2;
-                    // the last NLB waves; the first ones hold the linear and
-                    // in-chunk work)
+                    // denominator: q^T (Y3 q + 2 y2) over l block lb (p = 1: 2 q.y2),
+                    // K steps kq KK .. kq KK + KK - 1 of the contraction
                     if (DEN && lbl >= 0) {
+                        constexpr int KK = D / 4 / KQ;
                         f4 Tq;
     #pragma unroll
-                        for (int i = 0; i < 4; ++i) Tq[i] = sm.y2s[16 * lb + 4 * h + i];
+                        for (int i = 0; i < 4; ++i) Tq[i] = kq == 0 ? sm.y2s[16 * lb + 4 * h + i] : 0.f;
                         if constexpr (P == 2) {
-                            const float *yr = sm.y3 + (16 * lbl + r16) * RS;
+                            const float *yr = sm.y3 + (16 * lbl + r16) * RS + 4 * KK * kq + h;
+                            const float *qk = qr + 4 * KK * kq + h;
     #pragma unroll
-                            for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], qr[4 * kk + h], Tq);
+                            for (int kk = 0; kk < KK; ++kk) Tq = mma(yr[4 * kk], qk[4 * kk], Tq);
                         }
                         float gq = 0.f;
     #pragma unroll
                         for (int i = 0; i < 4; ++i) gq = fmaf(qr[16 * lb + 4 * h + i], Tq[i], gq);
                         gq += __shfl_xor(gq, 16);
                         gq += __shfl_xor(gq, 32);
-                        if (h == 0) sm.gint[lbl][tok] = gq;
+                        if (h == 0) sm.gint[gslot][tok] = gq;
                     }
                 }
                 __syncthreads();
@@ -333,7 +337,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                         if (DEN) {
                             float gsum = 0.f;
     #pragma unroll
-                            for (int ww = 0; ww < NLB; ++ww) gsum += sm.gint[ww][tg];
+                            for (int ww = 0; ww < PT::NGI; ++ww) gsum += sm.gint[ww][tg];
                             G = (pp == 0 ? (M == QUERY ? (float)N : (float)n0) : 0.f) + 0.5f * gsum;
                             if (M == SCAN && CAUSAL) G += sm.gin[tg];
                         }
