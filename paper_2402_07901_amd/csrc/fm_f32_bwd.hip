@@ -286,8 +286,10 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                         }
                     }
                 }
-                // the item's Y3w block (wave NW - 1; p = 1: z_t y2w[l] to every block)
-                const bool yw = ylb >= 0 && w == NW - 1;
+                // the item's Y3w block (p = 2: its contraction split by K range over
+                // the first YQ waves; p = 1: z_t y2w[l] to every block, wave NW - 1)
+                constexpr int YQ = D / 4 < NW ? D / 4 : NW;
+                const bool yw = ylb >= 0 && (P == 2 ? w < YQ : w == NW - 1);
                 const float zst = sm.zt[tok];
                 // quadratic tiles by output block u, from the last block down: tile
                 // (m, u) of the wave's channel m = chan(cc) adds Z_m T[l] to out[l], l in
@@ -354,14 +356,18 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                     for (int i = 0; i < 4; ++i) ocol[(16 * gw + 4 * h + i) * OS] += Tl[i];
                 }
                 // and the Y3w block, out[l] += z_t (y2w[l] + sum_m Y3w[l][m] Z_tm)
-                // for l in block ylb
+                // for l in block ylb: wave w adds K steps w KK .. w KK + KK - 1 of
+                // the sum over m (wave 0 the y2w term) to its own stored block,
+                // and the flush adds the waves' blocks
                 if (P == 2 && yw) {
+                    constexpr int KK = D / 4 / YQ;
                     f4 Tq;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) Tq[i] = sm.y2[4 * h + i];
-                    const float *yr = sm.y3 + r16 * RS;
+                    for (int i = 0; i < 4; ++i) Tq[i] = w == 0 ? sm.y2[4 * h + i] : 0.f;
+                    const float *yr = sm.y3 + r16 * RS + 4 * KK * w + h;
+                    const float *zk = zr + 4 * KK * w + h;
 #pragma unroll
-                    for (int kk = 0; kk < D / 4; ++kk) Tq = mma(yr[4 * kk + h], zr[4 * kk + h], Tq);
+                    for (int kk = 0; kk < KK; ++kk) Tq = mma(yr[4 * kk], zk[4 * kk], Tq);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) ocol[(16 * ylb + 4 * h + i) * OS] += zst * Tq[i];
                 }
