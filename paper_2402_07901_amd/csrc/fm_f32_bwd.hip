@@ -269,8 +269,10 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                         f4 Sc = {0.f, 0.f, 0.f, 0.f}, Pc = {0.f, 0.f, 0.f, 0.f};
                         if constexpr (P == 2) {
                             const float *xr = sm.xrow + (16 * st + r16) * RS;
+                            // K step kk takes channel (D/4) h + kk on lane h (both operands
+                            // alike): a lane's channels are contiguous, read a few per access
 #pragma unroll
-                            for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[4 * kk + h], zr[4 * kk + h], Sc);
+                            for (int kk = 0; kk < D / 4; ++kk) Sc = mma(xr[(D / 4) * h + kk], zr[(D / 4) * h + kk], Sc);
                         }
                         const float *vr = sm.vs + (16 * st + r16) * SL;
 #pragma unroll

@@ -12,7 +12,7 @@
 // quadratic tiles (m, u) for u >= m/16 (features k_m k_l); a diagonal tile
 // u = m/16 holds both (m, l) and (l, m) of its block.  Wave gw (over the
 // parts of a head and slice) owns the linear tile u = gw (gw < D/16) and the
-// quadratic tiles of the channels m = gw (mod waves * parts).
+// quadratic tiles of its channels chan(c, class, gw), c < D / (waves * parts).
 #pragma once
 
 #include <hip/hip_runtime.h>

@@ -281,8 +281,10 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                                 if (inchunk_owner<NPART>(rt, st) != pp) continue;
                                 f4 Sc = {0.f, 0.f, 0.f, 0.f};
                                 const float *kr = sm.krow + (16 * st + r16) * RS;
+                                // K step kk takes channel (D/4) h + kk on lane h (both operands
+                                // alike): a lane's channels are contiguous, read a few per access
     #pragma unroll
-                                for (int kk = 0; kk < D / 4; ++kk) Sc = mma(kr[4 * kk + h], qr[4 * kk + h], Sc);
+                                for (int kk = 0; kk < D / 4; ++kk) Sc = mma(kr[(D / 4) * h + kk], qr[(D / 4) * h + kk], Sc);
                                 // lane: query tok, keys 16 st + 4h + i
     #pragma unroll
                                 for (int i = 0; i < 4; ++i) {
