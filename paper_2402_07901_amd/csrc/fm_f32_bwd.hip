@@ -321,9 +321,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void grad_kernel(
                             }
                         }
                         if constexpr (u == u0 && u0 + 1 < NU) {
-                            float dm = dmv[cc];
-                            dm += __shfl_xor(dm, 16);
-                            dm += __shfl_xor(dm, 32);
+                            const float dm = rows4_sum(dmv[cc]);
                             const int ml = PT::chan(cc, GH, gw) & 15;
 #pragma unroll
                             for (int i = 0; i < 4; ++i)

@@ -298,8 +298,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                                     F = mma(sm.vrow[(16 * st + 4 * h + i) * SL + r16], Sc[i], F);
                             }
                             if (DEN) {
-                                gsum += __shfl_xor(gsum, 16);
-                                gsum += __shfl_xor(gsum, 32);
+                                gsum = rows4_sum(gsum);
                                 if (h == 0) sm.gin[tok] = gsum;
                             }
                         }
@@ -321,8 +320,7 @@ __global__ __launch_bounds__((Pat<D, P>::NTH)) void scan_kernel(const T *__restr
                         float gq = 0.f;
     #pragma unroll
                         for (int i = 0; i < 4; ++i) gq = fmaf(qr[16 * lb + 4 * h + i], Tq[i], gq);
-                        gq += __shfl_xor(gq, 16);
-                        gq += __shfl_xor(gq, 32);
+                        gq = rows4_sum(gq);
                         if (h == 0) sm.gint[gslot][tok] = gq;
                     }
                 }
