@@ -657,8 +657,7 @@ __device__ __forceinline__ void scan_block(Smem &sm, const _Float16 *__restrict_
                         gpart = fmaf(0.5f * ldexpf(1.0f, gexp), gq, gpart);
                         if (h == 0) gpart += (float)n0;
                     }
-                    gpart += __shfl_xor(gpart, 16);
-                    gpart += __shfl_xor(gpart, 32);
+                    gpart = rows4_sum(gpart);
                     gpart = fmaf(0.5f, Gin[0], gpart);
                     Fin[r] = F;
                     Gs[r] = gpart;

@@ -163,19 +163,6 @@ __device__ __forceinline__ float row16_sum(float x)
     return x;
 }
 
-// Sum over the four rows of 16 lanes (lanes r16, r16 + 16, r16 + 32, r16 + 48),
-// in every lane, with the permlane swaps (no LDS round trip): swapping the odd
-// rows of one copy with the even rows of another puts rows 2j and 2j + 1 side
-// by side, then the two halves of the wave likewise.  Every lane of the wave
-// must take part.
-__device__ __forceinline__ float rows4_sum(float x)
-{
-    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
 // Standardises the channels this thread holds of its token (Sec. 2.2, Eqs.
 // 6-7: population std, no epsilon; the token's LPT = 16 lanes form one DPP
 // row) and scales them.  Every lane of the wave must take part.

@@ -599,8 +599,7 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const void *__restrict__ qin,
                 for (int i = 0; i < 4; ++i) gq = fmaf((float)ql[i], T[i], gq);
                 // summed over the four lane groups here, so the combine reads
                 // one value per channel tile instead of four
-                gq += __shfl_xor(gq, 16);
-                gq += __shfl_xor(gq, 32);
+                gq = rows4_sum(gq);
                 if (h == 0) sm.gpart[buf][cc * QS + tk] = gq;
             }
         }
