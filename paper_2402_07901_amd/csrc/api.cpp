@@ -9,8 +9,10 @@
 
 namespace {
 
-// D = 128 (the head size of Sec. 3.1's Llama-2 remark) runs on the generic
-// float32 kernels; the MFMA kernels cover D = 64.
+// Head sizes served: 16, 32, 64 and 128 (the last the head size of Sec. 3.1's
+// Llama-2 remark).  bf16 D = 64, p = 2 runs on the fp16 MFMA kernels where they
+// apply, every other plain call on the float32 MFMA kernels, the dropout
+// calls on the generic float32 kernels.
 bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
 
 int check_common(int B, int H, int N, int D, int p, int causal, int dt)
@@ -50,7 +52,7 @@ bool valid_scale(float qs) { return qs > 0.0f && qs <= 1.0f; }
 // can be far smaller than the moment terms it is summed from (G = f_2(s) >= 1/2
 // for one key against terms of size ~|q^||k^|^2/2), which amplifies that
 // rounding past the bf16 tolerance.  Below one 128-token chunk of keys the
-// fp32 generic kernel is exact to fp32 and costs next to nothing.
+// float32 MFMA kernels take the call: exact to fp32, next to no cost.
 bool mfma_noncausal(int N, int D, int p, int causal, int dt)
 {
     return D == 64 && p == 2 && !causal && dt == FASTMAX_BF16 && N >= 128;

@@ -1,7 +1,7 @@
 // Generic Fastmax kernels: float32 VALU arithmetic, the moment state of one
-// column slice held in LDS, tokens processed in chunks of CH.  They serve
-// every supported (D, p, causal, dtype) that the MFMA kernels do not (those
-// take over for bf16, D = 64, p = 2 where they apply).  Like the MFMA
+// column slice held in LDS, tokens processed in chunks of CH.  General in
+// (D, p, causal, dtype); the entry points route the quadratic-term dropout
+// calls here and every other call to the MFMA kernels.  Like the MFMA
 // kernels, they are checked against the fp64 CPU oracle; they are not a
 // reference for the MFMA kernels.
 //
