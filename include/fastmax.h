@@ -41,7 +41,8 @@
  *    p = 2, bf16, except non-causal below 128 tokens; every other case runs
  *    on float32 MFMA kernels, and the dropout calls on float32 VALU kernels);
  *    p in {1, 2}; causal in {0, 1};
- *    dt in {FASTMAX_F32, FASTMAX_BF16}; B, H, N >= 1 and B*H*N*D < 2^62.
+ *    dt in {FASTMAX_F32, FASTMAX_BF16}; B, H, N >= 1, B*H <= 2^20 heads,
+ *    N <= 2^30 tokens per head and B*H*N*D < 2^62.
  *  - A token whose q or k row is constant has std 0; its standardised row is
  *    undefined (as in the paper) and its outputs are not finite.
  *  - Errors are reported only through the return code (nothing printed).
@@ -64,7 +65,8 @@ typedef enum {
 
 enum {
     FASTMAX_OK = 0,
-    FASTMAX_EINVAL = -1,       /* p, causal, dt, qk_scale or dropout rate out of range; B, H or N < 1 */
+    FASTMAX_EINVAL = -1,       /* p, causal, dt, qk_scale or dropout rate out of range; B, H or N
+                                  < 1, or beyond the size limits above */
     FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64, 128}   */
     FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
     FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */

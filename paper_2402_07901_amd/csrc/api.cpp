@@ -22,10 +22,12 @@ int check_common(int B, int H, int N, int D, int p, int causal, int dt)
     if (causal != 0 && causal != 1) return FASTMAX_EINVAL;
     if (dt != FASTMAX_F32 && dt != FASTMAX_BF16) return FASTMAX_EINVAL;
     if (!supported_d(D)) return FASTMAX_EUNSUPPORTED;
-    // B*H*N*D < 2^62 and B*H fits a grid dimension
+    // Size limits: B*H*N*D < 2^62; at most 2^20 heads (B*H) and 2^30 tokens
+    // per head, so that every chunk, workgroup and row count the launchers
+    // derive from them stays within int.
     unsigned __int128 tot = (unsigned __int128)B * H * N * D;
     if (tot >= ((unsigned __int128)1 << 62)) return FASTMAX_EINVAL;
-    if ((long long)B * H > 0x7fffffffLL) return FASTMAX_EINVAL;
+    if ((long long)B * H > (1LL << 20) || N > (1 << 30)) return FASTMAX_EINVAL;
     return FASTMAX_OK;
 }
 
@@ -312,7 +314,7 @@ const char *fastmax_strerror(int code)
 {
     switch (code) {
     case FASTMAX_OK: return "success";
-    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, qk_scale not in (0, 1], or dropout rate not in [0, 1))";
+    case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, B*H > 2^20, N > 2^30, qk_scale not in (0, 1], or dropout rate not in [0, 1))";
     case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32, 64 or 128)";
     case FASTMAX_ENULL: return "required pointer is NULL";
     case FASTMAX_EALIGN: return "pointer not 16-byte aligned";

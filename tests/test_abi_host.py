@@ -65,11 +65,23 @@ def bwd(ptrs=None, B=1, H=1, N=8, D=64, p=2, causal=1, dt=fm.BF16, ws=None, wsb=
     (dict(causal=2), fm.EINVAL), (dict(dt=7), fm.EINVAL),
     (dict(D=48), fm.EUNSUPPORTED), (dict(D=256), fm.EUNSUPPORTED), (dict(D=8), fm.EUNSUPPORTED),
     (dict(B=1 << 20, H=1 << 20, N=1 << 20), fm.EINVAL),
+    (dict(B=(1 << 10) + 1, H=1 << 10), fm.EINVAL), (dict(N=(1 << 30) + 1), fm.EINVAL),
 ])
 def test_fwd_rejects_bad_shape_args(kw, code):
     # also give a NULL q so that nothing could ever launch
     assert fwd(q=0, **kw) in (code, fm.ENULL)
     assert fwd(q=0, **kw) == code
+
+
+def test_size_limits_are_inclusive():
+    """2^20 heads and 2^30 tokens per head pass the size checks (a NULL q
+    then stops the call before anything is enqueued); one more does not."""
+    for B, H, N, D in ((1 << 10, 1 << 10, 1, 64), (1, 1, 1 << 30, 16)):
+        assert fwd(q=0, B=B, H=H, N=N, D=D) == fm.ENULL
+        assert bwd([0] + [A] * 8, B=B, H=H, N=N, D=D) == fm.ENULL
+        assert fm.workspace_bytes(B, H, N, D, 2, 1, fm.BF16, False) > 0
+    assert fm.workspace_bytes(1 << 10, (1 << 10) + 1, 1, 64, 2, 1, fm.BF16, False) == 0
+    assert fm.workspace_bytes(1, 1, (1 << 30) + 1, 16, 2, 1, fm.BF16, False) == 0
 
 
 @pytest.mark.parametrize("which", ["q", "k", "v", "out"])
