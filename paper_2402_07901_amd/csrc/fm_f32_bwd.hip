@@ -634,7 +634,10 @@ hipError_t bwd_run(const void *q, const void *k, const void *v, const void *o, c
     float *dkh = (float *)(p + 2 * pl.vec_bytes + pl.grad_bytes);
     void *scan = p + 2 * pl.vec_bytes + 2 * pl.grad_bytes;
     const size_t rb = (rows + 15) / 16;
-    if (rb > (size_t)INT_MAX) return hipErrorInvalidConfiguration;
+    // every grid of the sequence checked before the first launch
+    if (rb > (size_t)INT_MAX || (long long)pl.items * pl.nseg > INT_MAX ||
+        (long long)BH * ((N + 15) / 16) > INT_MAX)
+        return hipErrorInvalidConfiguration;
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v, *DO = (const T *)dout;
     hipLaunchKernelGGL((bwd_prep_kernel<D, T>), dim3((unsigned)rb), dim3(256), 0, st, (const T *)o,
                        DO, g, rg, cvec, dqh, dkh, rows);

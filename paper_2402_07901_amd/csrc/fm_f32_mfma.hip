@@ -515,7 +515,9 @@ hipError_t launch(const void *q, const void *k, const void *v, const float *vsc,
     using SM = Sum<D, P>;
     const Plan<D, P> pl(BH, N);
     const int items = pl.items, nseg = pl.nseg;
-    if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
+    const int nblk = (N + 15) / 16;   // finalize: 16 rows per workgroup
+    if ((long long)items * nseg > INT_MAX || (long long)BH * nblk > INT_MAX)
+        return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)(items * nseg)), blk(PT::NTH);
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v;
     T *O = (T *)out;
@@ -545,8 +547,6 @@ hipError_t launch(const void *q, const void *k, const void *v, const float *vsc,
                            g, sums, fpw, gpw, vsc, N, nseg, qs, ks);
     }
     if constexpr (PT::NPART > 1) {
-        const int nblk = (N + 15) / 16;
-        if ((long long)BH * nblk > INT_MAX) return hipErrorInvalidConfiguration;
         hipLaunchKernelGGL((finalize_kernel<D, P, T, !DV>), dim3((unsigned)(BH * nblk)), dim3(256),
                            0, st, fpw, gpw, O, g, N, nblk);
     }
