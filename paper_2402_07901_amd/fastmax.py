@@ -161,12 +161,48 @@ def fastmax_fwd_noalloc_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, stream, 
 def fastmax_fwd_noalloc(q, k, v, out, g=None, p=2, causal=False, stream=None, scale=None):
     """fastmax_fwd into caller-provided ``out`` (and ``g``) with the library's
     per-GPU scratch as workspace: nothing is allocated."""
-    B, H, N, D = q.shape
+    B, H, N, D = _check_args(q, k=(k, "like_q"), v=(v, "like_q"), out=(out, "like_q"),
+                             g=(g, "g"))
     rc = fastmax_fwd_noalloc_raw(q, k, v, out, g, B, H, N, D, p, causal, _dtype_code(q), stream,
                                  1.0 if scale is None else scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_fwd_noalloc")
     return out, g
+
+
+def _check_args(q, **tensors):
+    """Shape, dtype, layout and device checks the C ABI cannot make (it sees
+    pointers only): q is a contiguous [B, H, N, D] tensor on a GPU; every
+    other tensor is contiguous, on q's device, with the shape and dtype
+    its entry names ("like_q": q's; "g": float32 [B, H, N]; "bits": int32
+    [B, H, N, words]; "workspace": any dtype).  Returns (B, H, N, D)."""
+    import torch
+    if q.dim() != 4:
+        raise ValueError(f"q must be [B, H, N, D], got shape {tuple(q.shape)}")
+    B, H, N, D = q.shape
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    want = {"like_q": (tuple(q.shape), q.dtype), "g": ((B, H, N), torch.float32)}
+    for name, (t, kind) in tensors.items():
+        if t is None:
+            continue
+        if kind == "bits":
+            shape, dtype = (B, H, N, mask_words(D)), torch.int32
+        elif kind == "workspace":
+            shape, dtype = tuple(t.shape), t.dtype
+        else:
+            shape, dtype = want[kind]
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} must have shape {shape}, got {tuple(t.shape)}")
+        if t.dtype != dtype:
+            raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.device != q.device:
+            raise ValueError(f"{name} is on {t.device}, q on {q.device}")
+    if q.device.type != "cuda":
+        raise ValueError(f"the tensors must be on a GPU, q is on {q.device}")
+    return B, H, N, D
 
 
 def _alloc_ws(nbytes, device):
@@ -181,7 +217,8 @@ def fastmax_fwd(q, k, v, p=2, causal=False, out=None, g=None, want_g=True, works
     """O = Fastmax(q, k, v) for [B, H, N, D] device tensors; returns (O, G).
     ``scale``: score scale (weights f_p(scale * q^.k^)); None = the definition."""
     import torch
-    B, H, N, D = q.shape
+    B, H, N, D = _check_args(q, k=(k, "like_q"), v=(v, "like_q"), out=(out, "like_q"),
+                             g=(g, "g"), workspace=(workspace, "workspace"))
     dt = _dtype_code(q)
     if out is None:
         out = torch.empty_like(q)
@@ -202,7 +239,10 @@ def fastmax_bwd(q, k, v, out, dout, g, p=2, causal=False, dq=None, dk=None, dv=N
                 workspace=None, stream=None, scale=None):
     """Gradients (dq, dk, dv) of sum(dout * O); ``scale`` as in the forward."""
     import torch
-    B, H, N, D = q.shape
+    B, H, N, D = _check_args(q, k=(k, "like_q"), v=(v, "like_q"), out=(out, "like_q"),
+                             dout=(dout, "like_q"), g=(g, "g"), dq=(dq, "like_q"),
+                             dk=(dk, "like_q"), dv=(dv, "like_q"),
+                             workspace=(workspace, "workspace"))
     dt = _dtype_code(q)
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(q) if dk is None else dk
@@ -267,7 +307,9 @@ def fastmax_fwd_dropout(q, k, v, bits, rate, causal=False, scale=None, out=None,
     """Forward with the quadratic features of the keys masked by ``bits``
     (kept ones scaled by 1/(1 - rate)); returns (O, G)."""
     import torch
-    B, H, N, D = q.shape
+    B, H, N, D = _check_args(q, k=(k, "like_q"), v=(v, "like_q"), bits=(bits, "bits"),
+                             out=(out, "like_q"), g=(g, "g"),
+                             workspace=(workspace, "workspace"))
     dt = _dtype_code(q)
     out = torch.empty_like(q) if out is None else out
     if g is None:
@@ -286,7 +328,10 @@ def fastmax_bwd_dropout(q, k, v, out, dout, g, bits, rate, causal=False, scale=N
                         dk=None, dv=None, workspace=None, stream=None):
     """Gradients (dq, dk, dv) of sum(dout * O) for the forward with the same bits."""
     import torch
-    B, H, N, D = q.shape
+    B, H, N, D = _check_args(q, k=(k, "like_q"), v=(v, "like_q"), out=(out, "like_q"),
+                             dout=(dout, "like_q"), g=(g, "g"), bits=(bits, "bits"),
+                             dq=(dq, "like_q"), dk=(dk, "like_q"), dv=(dv, "like_q"),
+                             workspace=(workspace, "workspace"))
     dt = _dtype_code(q)
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(q) if dk is None else dk

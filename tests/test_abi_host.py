@@ -350,3 +350,60 @@ def test_scan_segment_mode_setter():
         assert all(x == sizes[0] for x in sizes)
     finally:
         fm.set_scan_segments(prev)
+
+
+# ---------------------------------------------------------------------------
+# The binding's tensor checks (the C ABI sees pointers only, so a tensor of
+# the wrong shape, dtype, layout or device must be refused before any call).
+# CPU tensors: every case below fails a check before the library is reached.
+# ---------------------------------------------------------------------------
+def _qkv(shape=(1, 2, 8, 16), dtype=None):
+    import torch
+    dtype = dtype or torch.float32
+    return [torch.zeros(shape, dtype=dtype) for _ in range(3)]
+
+
+def test_binding_rejects_mismatched_tensors():
+    import torch
+    q, k, v = _qkv()
+    with pytest.raises(ValueError, match=r"q must be \[B, H, N, D\]"):
+        fm.fastmax_fwd(q[0], k[0], v[0])
+    with pytest.raises(ValueError, match="k must have shape"):
+        fm.fastmax_fwd(q, k[:, :, :4], v)
+    with pytest.raises(ValueError, match="v must be torch.float32"):
+        fm.fastmax_fwd(q, k, v.to(torch.bfloat16))
+    with pytest.raises(ValueError, match="v must be contiguous"):
+        fm.fastmax_fwd(q, k, v.transpose(2, 3).contiguous().transpose(2, 3))
+    with pytest.raises(ValueError, match="q must be contiguous"):
+        fm.fastmax_fwd(q.transpose(2, 3).contiguous().transpose(2, 3), k, v)
+    with pytest.raises(ValueError, match="g must have shape"):
+        fm.fastmax_fwd(q, k, v, g=torch.zeros(1, 2, 7))
+    with pytest.raises(ValueError, match="g must be torch.float32"):
+        fm.fastmax_fwd(q, k, v, g=torch.zeros(1, 2, 8, dtype=torch.float64))
+    with pytest.raises(ValueError, match="dout must have shape"):
+        fm.fastmax_bwd(q, k, v, q, k[:, :1], torch.zeros(1, 2, 8))
+    with pytest.raises(ValueError, match="dq must be torch.float32"):
+        fm.fastmax_bwd(q, k, v, q, k, torch.zeros(1, 2, 8), dq=q.to(torch.bfloat16))
+    with pytest.raises(ValueError, match="bits must have shape"):
+        fm.fastmax_fwd_dropout(q, k, v, torch.zeros(1, 2, 8, 1, dtype=torch.int32), 0.1)
+    with pytest.raises(ValueError, match="bits must be torch.int32"):
+        fm.fastmax_fwd_dropout(q, k, v, torch.zeros(1, 2, 8, fm.mask_words(16)), 0.1)
+    with pytest.raises(ValueError, match="workspace must be contiguous"):
+        fm.fastmax_fwd(q, k, v, workspace=torch.zeros(8, 8, dtype=torch.uint8).t())
+
+
+def test_binding_refuses_host_tensors():
+    """Consistent tensors on the CPU: refused as not on a GPU (a kernel given
+    host pointers would fault), by every wrapper."""
+    import torch
+    q, k, v = _qkv()
+    g = torch.zeros(1, 2, 8)
+    bits = torch.zeros(1, 2, 8, fm.mask_words(16), dtype=torch.int32)
+    calls = [lambda: fm.fastmax_fwd(q, k, v),
+             lambda: fm.fastmax_bwd(q, k, v, q, q, g),
+             lambda: fm.fastmax_fwd_noalloc(q, k, v, q.clone(), g),
+             lambda: fm.fastmax_fwd_dropout(q, k, v, bits, 0.1),
+             lambda: fm.fastmax_bwd_dropout(q, k, v, q, q, g, bits, 0.1)]
+    for call in calls:
+        with pytest.raises(ValueError, match="must be on a GPU"):
+            call()
