@@ -32,11 +32,15 @@
  *    creates no stream and holds no global mutable state (thread-safe);
  *    the exceptions are fastmax_fwd_noalloc's per-GPU scratch array and the
  *    process-wide mode of fastmax_set_scan_segments.
+ *  - Device: the kernels run on the device that is current at the call;
+ *    `stream`, if not 0, must belong to it (FASTMAX_EINVAL otherwise).
  *  - Asynchrony: work is enqueued on `stream` (0 = the null stream);
  *    FASTMAX_OK means "enqueued".  Outputs are valid once the stream reaches
  *    that point.  Inputs must stay valid until then.
- *  - Validation happens on the host before the first HIP call: on any error
- *    nothing is enqueued and nothing is written.
+ *  - Validation happens on the host before anything is enqueued (the only
+ *    HIP calls before it ask which device is current and which device the
+ *    stream belongs to): on any error nothing is enqueued and nothing is
+ *    written.
  *  - Supported: D in {16, 32, 64, 128} (fp16 MFMA kernels serve D = 64,
  *    p = 2, bf16, except non-causal below 128 tokens; every other case runs
  *    on float32 MFMA kernels, and the dropout calls on float32 VALU kernels);
@@ -66,7 +70,8 @@ typedef enum {
 enum {
     FASTMAX_OK = 0,
     FASTMAX_EINVAL = -1,       /* p, causal, dt, qk_scale or dropout rate out of range; B, H or N
-                                  < 1, or beyond the size limits above */
+                                  < 1, or beyond the size limits above; a stream of another
+                                  device */
     FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64, 128}   */
     FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
     FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */
@@ -269,7 +274,8 @@ const char *fastmax_version(void);
  * up to 11081).  The call allocates nothing (no hipMalloc, no library
  * allocation);
  * the first call on a GPU looks the array's device address up once
- * (FASTMAX_EHIP if HIP refuses).  Every call on one GPU shares that GPU's
+ * (FASTMAX_EHIP if HIP refuses).  The array used is the current device's,
+ * which is why the stream must belong to that device (as for every call).  Every call on one GPU shares that GPU's
  * array: calls whose work overlaps on one GPU (different streams without
  * ordering, or several host threads) race on it and must be serialised by
  * the caller.  The array keeps the last call's contents; no forward path

@@ -1,5 +1,6 @@
 // C ABI of the Fastmax library: host-side validation, workspace sizing and
-// dispatch to the HIP kernels.  Every check runs before the first HIP call.
+// dispatch to the HIP kernels.  Every check runs before anything is enqueued
+// (the stream's device is the only one that asks HIP).
 #include <stdint.h>
 #include <string.h>
 
@@ -99,6 +100,20 @@ size_t bwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 
 namespace fm {
 
+// Kernels run on the current device.  A stream of another device would run
+// them there with this device's launch settings (and, for the allocation-free
+// forward, this device's scratch array), so such a stream is refused.  The
+// null stream is the current device's.
+int check_stream(hipStream_t stream)
+{
+    if (!stream) return FASTMAX_OK;
+    int cur = -1;
+    hipDevice_t sd = -1;
+    if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(stream, &sd) != hipSuccess)
+        return FASTMAX_EHIP;
+    return sd == cur ? FASTMAX_OK : FASTMAX_EINVAL;
+}
+
 int fwd_validate(const void *q, const void *k, const void *v, const void *out, const float *g,
                  int B, int H, int N, int D, int p, int causal, float qk_scale, int dt)
 {
@@ -147,6 +162,7 @@ int fwd_impl(const void *q, const void *k, const void *v, void *out, float *g, i
     size_t need = fwd_ws(B, H, N, D, p, causal, dt);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
+    if ((rc = fm::check_stream(stream)) != FASTMAX_OK) return rc;
     return fm::fwd_run(q, k, v, out, g, B, H, N, D, p, causal, qk_scale, dt, workspace, stream);
 }
 
@@ -165,6 +181,7 @@ int bwd_impl(const void *q, const void *k, const void *v, const void *out, const
     size_t need = bwd_ws(B, H, N, D, p, causal, dt);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
+    if ((rc = fm::check_stream(stream)) != FASTMAX_OK) return rc;
     hipError_t e;
     if (mfma_causal(D, p, causal, dt))
         e = fm::mfma_causal_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, qk_scale, workspace,
@@ -242,6 +259,7 @@ int fastmax_dropout_mask(uint32_t *keep_bits, int B, int H, int N, int D, float 
     if (!valid_rate(rate)) return FASTMAX_EINVAL;
     if (!keep_bits) return FASTMAX_ENULL;
     if (!aligned4(keep_bits)) return FASTMAX_EALIGN;
+    if ((rc = fm::check_stream(stream)) != FASTMAX_OK) return rc;
     // floor(rate 2^32) in double: exact for every float rate in [0, 1)
     const uint32_t thr = (uint32_t)((double)rate * 4294967296.0);
     hipError_t e = fm::dropout_mask(keep_bits, B * H, N, D, thr, seed, stream);
@@ -272,6 +290,7 @@ int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, 
     size_t need = fm::generic_fwd_dropout_workspace(B * H, N, D, causal);
     if (need > 0 && (!workspace || workspace_bytes < need)) return FASTMAX_EWORKSPACE;
     if (workspace && !aligned16(workspace)) return FASTMAX_EALIGN;
+    if ((rc = fm::check_stream(stream)) != FASTMAX_OK) return rc;
     hipError_t e = fm::generic_fwd_dropout(q, k, v, out, g, B * H, N, D, causal,
                                            dt == FASTMAX_BF16, qk_scale, keep_bits,
                                            1.0f / (1.0f - rate), workspace, stream);
@@ -297,6 +316,7 @@ int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void 
     size_t need = fm::generic_bwd_workspace(B, H, N, D, 2);
     if (!workspace || workspace_bytes < need) return FASTMAX_EWORKSPACE;
     if (!aligned16(workspace)) return FASTMAX_EALIGN;
+    if ((rc = fm::check_stream(stream)) != FASTMAX_OK) return rc;
     hipError_t e = fm::generic_bwd_dropout(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D,
                                            causal, dt == FASTMAX_BF16, qk_scale, keep_bits,
                                            1.0f / (1.0f - rate), workspace, stream);

@@ -13,6 +13,9 @@ namespace fm {
 // fastmax_dtype_t.
 int fwd_validate(const void *q, const void *k, const void *v, const void *out, const float *g,
                  int B, int H, int N, int D, int p, int causal, float qk_scale, int dt);
+// FASTMAX_OK if stream is 0 or belongs to the current device, FASTMAX_EINVAL
+// if it belongs to another one, FASTMAX_EHIP if HIP cannot tell.
+int check_stream(hipStream_t stream);
 size_t fwd_workspace(int B, int H, int N, int D, int p, int causal, int dt);
 int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, int B, int H, int N,
             int D, int p, int causal, float qk_scale, int dt, void *workspace, hipStream_t stream);

@@ -53,6 +53,9 @@ extern "C" int fastmax_fwd_noalloc(const void *q, const void *k, const void *v, 
     if (rc != FASTMAX_OK) return rc;
     if (fm::fwd_workspace(B, H, N, D, p, causal, d) > FASTMAX_NOALLOC_MAX_WORKSPACE_BYTES)
         return FASTMAX_EWORKSPACE;
+    // the scratch array is the current device's: the work must run there
+    const int rs = fm::check_stream(stream);
+    if (rs != FASTMAX_OK) return rs;
     // No forward kernel relies on zeroed workspace (every buffer in it is
     // written before it is read), so nothing is cleared.
     void *ws = scratch_ptr();

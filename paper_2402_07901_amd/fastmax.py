@@ -109,10 +109,27 @@ def _ptr(t):
 
 
 def _stream(stream):
+    """The stream argument as a handle: ``stream`` as given (a torch stream or
+    a raw handle), else the current device's current stream."""
     if stream is None:
         import torch
         stream = torch.cuda.current_stream()
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else stream)
+
+
+def _stream_of(stream, device):
+    """``stream``, or the current stream of ``device`` when None."""
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream(device)
+    return stream
+
+
+def _on(device):
+    """Context that makes ``device`` current for a library call (the library
+    runs its kernels, and requires its stream to be, on the current device)."""
+    import torch
+    return torch.cuda.device(device)
 
 
 def _dtype_code(t):
@@ -163,8 +180,9 @@ def fastmax_fwd_noalloc(q, k, v, out, g=None, p=2, causal=False, stream=None, sc
     per-GPU scratch as workspace: nothing is allocated."""
     B, H, N, D = _check_args(q, k=(k, "like_q"), v=(v, "like_q"), out=(out, "like_q"),
                              g=(g, "g"))
-    rc = fastmax_fwd_noalloc_raw(q, k, v, out, g, B, H, N, D, p, causal, _dtype_code(q), stream,
-                                 1.0 if scale is None else scale)
+    with _on(q.device):
+        rc = fastmax_fwd_noalloc_raw(q, k, v, out, g, B, H, N, D, p, causal, _dtype_code(q),
+                                     _stream_of(stream, q.device), 1.0 if scale is None else scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_fwd_noalloc")
     return out, g
@@ -228,8 +246,9 @@ def fastmax_fwd(q, k, v, p=2, causal=False, out=None, g=None, want_g=True, works
     if workspace is None:
         workspace = _alloc_ws(need, q.device)
     ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    rc = fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_n, stream,
-                         scale)
+    with _on(q.device):
+        rc = fastmax_fwd_raw(q, k, v, out, g, B, H, N, D, p, causal, dt, workspace, ws_n,
+                             _stream_of(stream, q.device), scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_fwd")
     return out, g
@@ -251,8 +270,9 @@ def fastmax_bwd(q, k, v, out, dout, g, p=2, causal=False, dq=None, dk=None, dv=N
     if workspace is None:
         workspace = _alloc_ws(need, q.device)
     ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    rc = fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt, workspace,
-                         ws_n, stream, scale)
+    with _on(q.device):
+        rc = fastmax_bwd_raw(q, k, v, out, dout, g, dq, dk, dv, B, H, N, D, p, causal, dt,
+                             workspace, ws_n, _stream_of(stream, q.device), scale)
     if rc != OK:
         raise FastmaxError(rc, "fastmax_bwd")
     return dq, dk, dv
@@ -276,7 +296,9 @@ def dropout_mask(B, H, N, D, rate, seed, device="cuda", stream=None):
     """Philox4x32-10 keep bits for the quadratic features of every key token."""
     import torch
     bits = torch.empty((B, H, N, mask_words(D)), dtype=torch.int32, device=device)
-    rc = fastmax_dropout_mask_raw(bits, B, H, N, D, rate, seed, stream)
+    with _on(bits.device):
+        rc = fastmax_dropout_mask_raw(bits, B, H, N, D, rate, seed,
+                                      _stream_of(stream, bits.device))
     if rc != OK:
         raise FastmaxError(rc, "fastmax_dropout_mask")
     return bits
@@ -317,8 +339,10 @@ def fastmax_fwd_dropout(q, k, v, bits, rate, causal=False, scale=None, out=None,
     if workspace is None:
         workspace = _alloc_ws(dropout_workspace_bytes(B, H, N, D, causal, dt, False), q.device)
     ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    rc = fastmax_fwd_dropout_raw(q, k, v, out, g, bits, rate, B, H, N, D, causal,
-                                 1.0 if scale is None else scale, dt, workspace, ws_n, stream)
+    with _on(q.device):
+        rc = fastmax_fwd_dropout_raw(q, k, v, out, g, bits, rate, B, H, N, D, causal,
+                                     1.0 if scale is None else scale, dt, workspace, ws_n,
+                                     _stream_of(stream, q.device))
     if rc != OK:
         raise FastmaxError(rc, "fastmax_fwd_dropout")
     return out, g
@@ -339,9 +363,10 @@ def fastmax_bwd_dropout(q, k, v, out, dout, g, bits, rate, causal=False, scale=N
     if workspace is None:
         workspace = _alloc_ws(dropout_workspace_bytes(B, H, N, D, causal, dt, True), q.device)
     ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    rc = fastmax_bwd_dropout_raw(q, k, v, out, dout, g, bits, rate, dq, dk, dv, B, H, N, D,
-                                 causal, 1.0 if scale is None else scale, dt, workspace, ws_n,
-                                 stream)
+    with _on(q.device):
+        rc = fastmax_bwd_dropout_raw(q, k, v, out, dout, g, bits, rate, dq, dk, dv, B, H, N, D,
+                                     causal, 1.0 if scale is None else scale, dt, workspace,
+                                     ws_n, _stream_of(stream, q.device))
     if rc != OK:
         raise FastmaxError(rc, "fastmax_bwd_dropout")
     return dq, dk, dv
