@@ -72,7 +72,11 @@ enum {
     FASTMAX_EINVAL = -1,       /* p, causal, dt, qk_scale or dropout rate out of range; B, H or N
                                   < 1, or beyond the size limits above; a stream of another
                                   device */
-    FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64, 128}   */
+    FASTMAX_EUNSUPPORTED = -2, /* head dimension D not in {16, 32, 64, 128}, or a call
+                                  whose launch grids would exceed the dispatch limits
+                                  (2^32 - 1 work-items per grid dimension; only at extreme
+                                  head counts, e.g. 2^18 heads at D = 128, p = 2, or 2^20
+                                  in the bf16 D = 64 backward); nothing is enqueued */
     FASTMAX_ENULL = -3,        /* a required pointer is NULL                  */
     FASTMAX_EALIGN = -4,       /* a tensor pointer is not 16-byte aligned     */
     FASTMAX_EWORKSPACE = -5,   /* workspace NULL or smaller than required     */

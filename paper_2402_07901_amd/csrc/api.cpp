@@ -100,6 +100,16 @@ size_t bwd_ws(int B, int H, int N, int D, int p, int causal, int dt)
 
 namespace fm {
 
+// A launcher's result as a FASTMAX code: hipErrorInvalidConfiguration is
+// what the launchers return, before their first launch, for a call whose
+// grids exceed the dispatch limits (an unsupported size); anything else from
+// HIP is FASTMAX_EHIP.
+int code_of(hipError_t e)
+{
+    if (e == hipSuccess) return FASTMAX_OK;
+    return e == hipErrorInvalidConfiguration ? FASTMAX_EUNSUPPORTED : FASTMAX_EHIP;
+}
+
 // Kernels run on the current device.  A stream of another device would run
 // them there with this device's launch settings (and, for the allocation-free
 // forward, this device's scratch array), so such a stream is refused.  The
@@ -146,7 +156,7 @@ int fwd_run(const void *q, const void *k, const void *v, void *out, float *g, in
     else
         e = generic_fwd(q, k, v, out, g, B * H, N, D, p, causal, dt == FASTMAX_BF16, qk_scale,
                         workspace, stream);
-    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+    return fm::code_of(e);
 }
 
 }  // namespace fm
@@ -195,7 +205,7 @@ int bwd_impl(const void *q, const void *k, const void *v, const void *out, const
     else
         e = fm::generic_bwd(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D, p, causal,
                             dt == FASTMAX_BF16, qk_scale, workspace, stream);
-    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+    return fm::code_of(e);
 }
 
 }  // namespace
@@ -263,7 +273,7 @@ int fastmax_dropout_mask(uint32_t *keep_bits, int B, int H, int N, int D, float 
     // floor(rate 2^32) in double: exact for every float rate in [0, 1)
     const uint32_t thr = (uint32_t)((double)rate * 4294967296.0);
     hipError_t e = fm::dropout_mask(keep_bits, B * H, N, D, thr, seed, stream);
-    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+    return fm::code_of(e);
 }
 
 size_t fastmax_dropout_workspace_bytes(int B, int H, int N, int D, int causal,
@@ -294,7 +304,7 @@ int fastmax_fwd_dropout(const void *q, const void *k, const void *v, void *out, 
     hipError_t e = fm::generic_fwd_dropout(q, k, v, out, g, B * H, N, D, causal,
                                            dt == FASTMAX_BF16, qk_scale, keep_bits,
                                            1.0f / (1.0f - rate), workspace, stream);
-    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+    return fm::code_of(e);
 }
 
 int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void *out,
@@ -320,7 +330,7 @@ int fastmax_bwd_dropout(const void *q, const void *k, const void *v, const void 
     hipError_t e = fm::generic_bwd_dropout(q, k, v, out, dout, g, dq, dk, dv, B * H, N, D,
                                            causal, dt == FASTMAX_BF16, qk_scale, keep_bits,
                                            1.0f / (1.0f - rate), workspace, stream);
-    return e == hipSuccess ? FASTMAX_OK : FASTMAX_EHIP;
+    return fm::code_of(e);
 }
 
 int fastmax_set_scan_segments(int mode)
@@ -335,7 +345,7 @@ const char *fastmax_strerror(int code)
     switch (code) {
     case FASTMAX_OK: return "success";
     case FASTMAX_EINVAL: return "invalid argument (p, causal, dtype, B/H/N < 1, B*H > 2^20, N > 2^30, qk_scale not in (0, 1], or dropout rate not in [0, 1))";
-    case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32, 64 or 128)";
+    case FASTMAX_EUNSUPPORTED: return "unsupported head dimension (D must be 16, 32, 64 or 128) or a problem whose launch grids exceed the dispatch limits";
     case FASTMAX_ENULL: return "required pointer is NULL";
     case FASTMAX_EALIGN: return "pointer not 16-byte aligned";
     case FASTMAX_EWORKSPACE: return "workspace missing or too small";

@@ -810,8 +810,14 @@ hipError_t run(const void *q, const void *k, const void *v, const void *o, const
                   "LDS budget");
     const size_t rows = (size_t)BH * N;
     const int nch = (N + C - 1) / C;
-    if ((long long)BH * (nch + 8) > INT_MAX || (long long)BH * 8 > INT_MAX ||
-        (rows + 31) / 32 > (size_t)INT_MAX)
+    // the dv scan's split (causal)
+    const ScanSplit plan = CAUSAL ? causal_scan_split(4 * BH, nch, false) : ScanSplit{0, 0, 1};
+    // prep, dv with the in-chunk blocks, the moment-gradient scans, finish;
+    // non-causal: the dv launches
+    if (!grid_fits((long long)BH * nch, 256) ||
+        (CAUSAL && !grid_fits((long long)BH * (4 * (1 + plan.split) + nch), 512)) ||
+        !grid_fits((long long)BH * 8, MG_NTH) || !grid_fits((long long)((rows + 31) / 32), 256) ||
+        (!CAUSAL && !mfma_nc_grids_fit(BH, N)))
         return hipErrorInvalidConfiguration;
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
     unsigned char *p = (unsigned char *)ws;
@@ -830,7 +836,6 @@ hipError_t run(const void *q, const void *k, const void *v, const void *o, const
     _Float16 *kh = (_Float16 *)p;
     p += a256(rows * D * 2);
     // the dv scan's segment summaries and flags (causal)
-    const ScanSplit plan = CAUSAL ? causal_scan_split(4 * BH, nch, false) : ScanSplit{0, 0, 1};
     mfma_causal::SegArgs sa{nullptr, nullptr, plan.split, plan.csplit, plan.wait};
     if (plan.split) {
         sa.sum = p;

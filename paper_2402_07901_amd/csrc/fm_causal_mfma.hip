@@ -114,15 +114,16 @@ hipError_t mfma_causal_fwd(const void *q, const void *k, const void *v, void *ou
     static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
     static_assert(NHT == 2 * C, "one helper thread per (token pair, v half)");
     const size_t rows = (size_t)BH * N;
-    if ((rows + 31) / 32 > (size_t)INT_MAX) return hipErrorInvalidConfiguration;
     const int items = BH * NSL, nch = (N + C - 1) / C;
-    if ((long long)items * 2 > INT_MAX) return hipErrorInvalidConfiguration;
+    const ScanSplit plan = causal_scan_split(items, nch, true);
+    if (!grid_fits((long long)((rows + 31) / 32), 256) ||
+        !grid_fits((long long)items * (1 + plan.split), NTH))
+        return hipErrorInvalidConfiguration;
     unsigned char *p = (unsigned char *)ws;
     _Float16 *qh = (_Float16 *)p;
     p += a256(rows * D * 2);
     _Float16 *kh = (_Float16 *)p;
     p += a256(rows * D * 2);
-    const ScanSplit plan = causal_scan_split(items, nch, true);
     SegArgs sa{nullptr, nullptr, plan.split, plan.csplit, plan.wait};
     if (plan.split) {
         sa.sum = p;

@@ -593,7 +593,7 @@ hipError_t grad_launch(const BwdPlan<D, P> &pl, const T *X, const T *Z, const T 
 {
     using GS = GSum<D, P>;
     const int items = pl.items, nseg = pl.nseg;
-    if ((long long)items * nseg > INT_MAX) return hipErrorInvalidConfiguration;
+    if (!grid_fits((long long)items * nseg, Pat<D, P>::NTH)) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)(items * nseg)), blk(Pat<D, P>::NTH);
     const size_t stride = GS::BYTES / 4;
     const dim3 pgrid((unsigned)((GS::FLOATS + 255) / 256), items);
@@ -635,8 +635,9 @@ hipError_t bwd_run(const void *q, const void *k, const void *v, const void *o, c
     void *scan = p + 2 * pl.vec_bytes + 2 * pl.grad_bytes;
     const size_t rb = (rows + 15) / 16;
     // every grid of the sequence checked before the first launch
-    if (rb > (size_t)INT_MAX || (long long)pl.items * pl.nseg > INT_MAX ||
-        (long long)BH * ((N + 15) / 16) > INT_MAX)
+    if (!grid_fits((long long)rb, 256) ||
+        !grid_fits((long long)pl.items * pl.nseg, Pat<D, P>::NTH) ||
+        !f32mfma_fwd_grids_fit(BH, N, D, P))
         return hipErrorInvalidConfiguration;
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v, *DO = (const T *)dout;
     hipLaunchKernelGGL((bwd_prep_kernel<D, T>), dim3((unsigned)rb), dim3(256), 0, st, (const T *)o,

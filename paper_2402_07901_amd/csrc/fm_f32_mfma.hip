@@ -516,8 +516,7 @@ hipError_t launch(const void *q, const void *k, const void *v, const float *vsc,
     const Plan<D, P> pl(BH, N);
     const int items = pl.items, nseg = pl.nseg;
     const int nblk = (N + 15) / 16;   // finalize: 16 rows per workgroup
-    if ((long long)items * nseg > INT_MAX || (long long)BH * nblk > INT_MAX)
-        return hipErrorInvalidConfiguration;
+    if (!f32mfma_fwd_grids_fit(BH, N, D, P)) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)(items * nseg)), blk(PT::NTH);
     const T *Q = (const T *)q, *K = (const T *)k, *V = (const T *)v;
     T *O = (T *)out;
@@ -586,6 +585,28 @@ bool f32mfma_applies(int D, int p, int is_bf16)
 {
     (void)is_bf16;   // every dtype (bf16 D = 64, p = 2 only where the fp16 kernels do not serve)
     return (p == 1 || p == 2) && (D == 16 || D == 32 || D == 64 || D == 128);
+}
+
+namespace m32 {
+template <int D, int P>
+bool grids_fit(int BH, int N)
+{
+    const Plan<D, P> pl(BH, N);
+    return grid_fits((long long)pl.items * pl.nseg, Pat<D, P>::NTH) &&
+           (Pat<D, P>::NPART == 1 || grid_fits((long long)BH * ((N + 15) / 16), 256));
+}
+}  // namespace m32
+
+bool f32mfma_fwd_grids_fit(int BH, int N, int D, int p)
+{
+    using namespace m32;
+    switch (D) {
+    case 16: return p == 1 ? grids_fit<16, 1>(BH, N) : grids_fit<16, 2>(BH, N);
+    case 32: return p == 1 ? grids_fit<32, 1>(BH, N) : grids_fit<32, 2>(BH, N);
+    case 64: return p == 1 ? grids_fit<64, 1>(BH, N) : grids_fit<64, 2>(BH, N);
+    case 128: return p == 1 ? grids_fit<128, 1>(BH, N) : grids_fit<128, 2>(BH, N);
+    }
+    return false;
 }
 
 size_t f32mfma_fwd_workspace(int BH, int N, int D, int p)

@@ -1127,7 +1127,7 @@ static hipError_t bwd_dispatch2(const void *q, const void *k, const void *v, con
     float *dva = dkh + rows * D;
     const BwdPlan bp = bwd_plan<D, P2>(BH, N);
     float *sseg = bp.nseg > 1 ? dva + rows * D : nullptr;
-    if ((rows + NT - 1) / NT > (size_t)INT_MAX) return hipErrorInvalidConfiguration;
+    if (!grid_fits((long long)((rows + NT - 1) / NT), NT)) return hipErrorInvalidConfiguration;
     const int rb = (int)((rows + NT - 1) / NT);
     hipLaunchKernelGGL((bwd_rowdot_kernel<D, T>), dim3(rb), dim3(NT), 0, st, (const T *)o,
                        (const T *)dout, g, cvec, rows);

@@ -13,6 +13,19 @@ namespace fm {
 // fastmax_dtype_t.
 int fwd_validate(const void *q, const void *k, const void *v, const void *out, const float *g,
                  int B, int H, int N, int D, int p, int causal, float qk_scale, int dt);
+// A launch of `blocks` workgroups of `threads` work-items along one grid
+// dimension fits the dispatch limits: at most 2^31 - 1 workgroups and
+// 2^32 - 1 work-items.  Every launcher checks all the grids of a call with it
+// before its first launch (hipErrorInvalidConfiguration otherwise).
+inline bool grid_fits(long long blocks, long long threads)
+{
+    return blocks >= 1 && blocks <= 0x7fffffffLL && blocks * threads <= 0xffffffffLL;
+}
+// The float32 MFMA forward's grids (also those of the backward's dv scan) and
+// the segmented non-causal MFMA path's grids fit.
+bool f32mfma_fwd_grids_fit(int BH, int N, int D, int p);
+bool mfma_nc_grids_fit(int BH, int N);
+
 // FASTMAX_OK if stream is 0 or belongs to the current device, FASTMAX_EINVAL
 // if it belongs to another one, FASTMAX_EHIP if HIP cannot tell.
 int check_stream(hipStream_t stream);

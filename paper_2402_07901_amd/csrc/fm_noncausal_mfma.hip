@@ -614,6 +614,14 @@ __global__ __launch_bounds__(NTH, 1) void nc_query(const void *__restrict__ qin,
 
 size_t mfma_nc_workspace(int BH, int N) { return mfma_nc::make_plan(BH, N).total; }
 
+bool mfma_nc_grids_fit(int BH, int N)
+{
+    using namespace mfma_nc;
+    const Plan P = make_plan(BH, N);
+    return grid_fits((long long)BH * NMS * P.nseg, NTH) &&
+           grid_fits((long long)BH * (RED_BLOCKS + 1), 512) && grid_fits((long long)BH * P.ntb, NTH);
+}
+
 namespace mfma_nc {
 
 // The three launches on a workspace laid out by make_plan.  KQF16: keys and
@@ -628,7 +636,7 @@ hipError_t launch(const void *q, const void *k, const void *v, const float *vrow
     const long long gm = (long long)BH * NMS * P.nseg;
     const long long gr = (long long)BH * (RED_BLOCKS + 1);
     const long long gq = (long long)BH * P.ntb;
-    if (gm > INT_MAX || gr > INT_MAX || gq > INT_MAX) return hipErrorInvalidConfiguration;
+    if (!mfma_nc_grids_fit(BH, N)) return hipErrorInvalidConfiguration;
     unsigned char *w = (unsigned char *)ws;
     float *part = (float *)(w + P.off_part);
     float *vmx = (float *)(w + P.off_vmx);

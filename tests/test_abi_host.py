@@ -407,3 +407,21 @@ def test_binding_refuses_host_tensors():
     for call in calls:
         with pytest.raises(ValueError, match="must be on a GPU"):
             call()
+
+
+@pytest.mark.parametrize("B,H,N,D,backward", [
+    (1, 1 << 18, 1, 128, False),   # float32 MFMA forward: 2^23 workgroups of 512 threads
+    (1, 1 << 18, 1, 128, True),
+    (1 << 10, 1 << 10, 1, 64, True),   # bf16 D = 64 backward: 2^23 moment-gradient workgroups
+])
+def test_grids_beyond_the_dispatch_limits_are_unsupported(B, H, N, D, backward):
+    """Within the size limits but with a launch grid of 2^32 work-items: the
+    launcher refuses it before its first launch (no HIP call is made, so this
+    runs without a GPU) and the call returns FASTMAX_EUNSUPPORTED."""
+    need = fm.workspace_bytes(B, H, N, D, 2, 1, fm.BF16, backward)
+    assert need > 0
+    if backward:
+        rc = bwd(B=B, H=H, N=N, D=D, ws=A, wsb=need)
+    else:
+        rc = fwd(B=B, H=H, N=N, D=D, ws=A, wsb=need)
+    assert rc == fm.EUNSUPPORTED
