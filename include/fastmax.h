@@ -87,7 +87,9 @@ enum {
  * Bytes of device workspace fastmax_fwd (backward = 0) or fastmax_bwd
  * (backward = 1) needs for this problem.  0 means no workspace is needed
  * (NULL may then be passed).  Returns 0 as well for arguments the entry
- * point would reject.  The workspace need not be zeroed.  The forward needs
+ * point would reject in its argument checks (EINVAL, EUNSUPPORTED for D); a
+ * call refused for its launch grids (EUNSUPPORTED at extreme head counts)
+ * still gets its size here.  The workspace need not be zeroed.  The forward needs
  * one when it splits each head's sequence into segments whose moment states
  * are built in parallel: the non-causal bf16, D = 64, p = 2 path with
  * N >= 128 (per-segment partial moments, their fp16 sum and the per-head
